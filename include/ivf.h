@@ -1,0 +1,178 @@
+/*
+ * ivf.h -- C ABI of the MI355X (gfx950) IVF routing and construction hot path
+ * of InSituANN (arXiv 2608.08751).
+ *
+ * What is computed (paper references are to sections and equations):
+ *   - coarse search, Eq. (1), Sec. "ANN Search and IVF": for each query the
+ *     nprobe centroids of smallest squared L2 distance;
+ *   - the distances are evaluated as in Eq. (6), Sec. "GPU coarse search"
+ *     (||q||^2 + ||c||^2 - 2 q.c, the -2 q.c term as a dense fp32 MFMA
+ *     contraction over LDS-staged tiles), with the row-wise top-P selected on
+ *     the device so that only O(B*P) ids and distances are produced
+ *     ("On-device list selection", same section);
+ *   - IVF construction, Sec. "System Architecture" (index layout) and
+ *     Sec. "Fast Index Construction": Lloyd k-means iterations (assignment +
+ *     mean update) and the assignment of every base vector to its nearest
+ *     centroid, stored cluster-major with per-list offset, length and ids.
+ *
+ * Exactness contract. Every id, label, count, offset and permutation entry is
+ * exactly what the definition gives with distances evaluated in fp64 as
+ *     s = 0; for d = 0..D-1: t = (double)x_d - (double)c_d; s = fma(t, t, s)
+ * and ties broken by the lower centroid id. Returned distances are that s
+ * rounded to fp32. The fp32 MFMA pass only screens candidates; a rigorous
+ * rounding-error bound decides which candidates are re-evaluated in fp64 and
+ * when a query or row falls back to an exact fp64 scan of all centroids.
+ *
+ * Conventions shared by every call:
+ *   - Array arguments are DEVICE pointers on the context's device, row-major,
+ *     contiguous, 16-byte aligned, allocated and owned by the caller. The
+ *     library never frees or retains them beyond the call.
+ *   - Calls are asynchronous: IVF_OK means every kernel was enqueued on the
+ *     context's stream. No call synchronises with the host. Device faults
+ *     surface at ivf_sync() as IVF_EDEVICE.
+ *   - Arguments are validated before anything is enqueued; on any status other
+ *     than IVF_OK nothing was enqueued and the outputs are untouched, and
+ *     ivf_last_error() describes the problem.
+ *   - Scratch memory is a caller-provided device workspace (ivf_set_workspace)
+ *     of at least ivf_workspace_bytes() for the call; too small gives
+ *     IVF_ENOMEM with the required size in ivf_last_error(). Two calls that
+ *     share a context must not overlap on different streams.
+ *   - Q, N == 0 is a no-op returning IVF_OK.
+ *   - Supported shapes: 4 <= D <= 256 with D % 4 == 0 (else IVF_EUNSUPPORTED).
+ */
+#ifndef IVF_H
+#define IVF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    IVF_OK = 0,
+    IVF_EINVAL = 1,       /* bad argument: sizes, null pointers, aliasing */
+    IVF_EUNSUPPORTED = 2, /* valid but outside the supported shapes */
+    IVF_ENOMEM = 3,       /* workspace missing or too small */
+    IVF_EDEVICE = 4       /* HIP runtime error (launch failure, device fault) */
+} ivf_status;
+
+typedef enum { IVF_F32 = 0, IVF_U8 = 1 } ivf_dtype;
+
+/* Operation codes for ivf_workspace_bytes. */
+typedef enum {
+    IVF_OP_ROUTE = 0,
+    IVF_OP_KMEANS_STEP = 1,
+    IVF_OP_ASSIGN_BUILD = 2,
+    IVF_OP_BUILD_LISTS = 3
+} ivf_op;
+
+typedef struct ivf_ctx ivf_ctx;
+
+/* Creates a context bound to HIP device `device` and to `hip_stream`
+ * (a hipStream_t; NULL = the device's null stream). *out receives the handle.
+ * Errors: IVF_EINVAL (out == NULL, bad device), IVF_EDEVICE. */
+ivf_status ivf_create(int device, void *hip_stream, ivf_ctx **out);
+
+/* Destroys a context; NULL is ignored. Does not free the workspace. */
+void ivf_destroy(ivf_ctx *ctx);
+
+/* Host string describing the last non-OK status of this context ("" if none).
+ * Valid until the next call on the context. */
+const char *ivf_last_error(const ivf_ctx *ctx);
+
+/* Rebinds the context to another stream (NULL = null stream). */
+ivf_status ivf_set_stream(ivf_ctx *ctx, void *hip_stream);
+
+/* Device workspace bytes that `op` needs for the given sizes:
+ *   IVF_OP_ROUTE        rows = Q, k = nprobe
+ *   IVF_OP_KMEANS_STEP  rows = N (k ignored)
+ *   IVF_OP_ASSIGN_BUILD rows = N (k ignored)
+ *   IVF_OP_BUILD_LISTS  rows = N (D, k ignored)
+ * Returns 0 for sizes that the op rejects. */
+size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k);
+
+/* Hands the context a caller-owned device buffer (256-byte aligned) used as
+ * scratch by later calls. The buffer must stay allocated while calls that use
+ * it are in flight. NULL/0 detaches it. */
+ivf_status ivf_set_workspace(ivf_ctx *ctx, void *dev_ptr, size_t bytes);
+
+/* Waits for the context's stream. IVF_EDEVICE if the device reported an error. */
+ivf_status ivf_sync(ivf_ctx *ctx);
+
+/* Coarse search, Eq. (1) with Eq. (6) (Sec. "GPU coarse search").
+ *   queries   [Q, D] fp32           centroids [C, D] fp32
+ *   nprobe    1 <= nprobe <= min(C, 1024)
+ *   out_ids   [Q, nprobe] int32     centroid ids, ascending (distance, id)
+ *   out_dist  [Q, nprobe] fp32      squared L2 distances (fp64 rounded to
+ *                                   fp32), may be NULL
+ * Outputs must not overlap the inputs or each other.
+ * Errors: IVF_EINVAL (Q < 0, C < 1, nprobe out of range, NULL required
+ * pointer, misaligned pointer, aliasing), IVF_EUNSUPPORTED (D), IVF_ENOMEM. */
+ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
+                     int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist);
+
+/* One Lloyd iteration of k-means (k-means training, Sec. "Fast Index
+ * Construction"): assignment against `centroids`, then the mean update.
+ *   train          [N, D] fp32 or uint8 (dt), N >= 1
+ *   centroids      [C, D] fp32 input centroids c^(t)
+ *   seed, iter     select the training row that replaces an empty cluster j:
+ *                  row = SplitMix64 output ((iter << 32) | j) + 1 of a
+ *                  generator seeded with `seed`, mod N
+ *   out_labels     [N] int32, nearest input centroid, ties to the lower id
+ *   out_centroids  [C, D] fp32 c^(t+1): for a non-empty cluster
+ *                  (float)(sum / (double)count) where the sum is exact for
+ *                  uint8 data and an fp64 sum in ascending row order for fp32
+ *                  data; an empty cluster takes the reseed row. Must not alias
+ *                  `centroids`.
+ *   out_counts     [C] int64 cluster sizes before reseeding, may be NULL
+ *   out_objective  device fp64 scalar: sum over rows of the squared distance
+ *                  to the assigned input centroid, may be NULL
+ * Errors: as ivf_route; N > 2^32 - 1 is IVF_EUNSUPPORTED. */
+ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
+                           const float *centroids, int64_t C, int32_t D, uint64_t seed,
+                           int32_t iter, int32_t *out_labels, float *out_centroids,
+                           int64_t *out_counts, double *out_objective);
+
+/* Full assignment and inverted-list build (Sec. "System Architecture", index
+ * layout: cluster-major lists with offset, length and vector ids).
+ *   base         [N, D] fp32 or uint8 (dt), N <= 2^32 - 1
+ *   centroids    [C, D] fp32
+ *   out_labels   [N] int32 nearest centroid, ties to the lower id
+ *   out_counts   [C] int64 list lengths
+ *   out_offsets  [C + 1] int64 exclusive prefix sum of counts, offsets[C] = N
+ *   out_perm     [N] uint32 row ids grouped by list, ascending inside a list
+ * Errors: as ivf_kmeans_step. */
+ivf_status ivf_assign_build(ivf_ctx *ctx, const void *base, int dt, int64_t N,
+                            const float *centroids, int64_t C, int32_t D, int32_t *out_labels,
+                            int64_t *out_counts, int64_t *out_offsets, uint32_t *out_perm);
+
+/* The inverted-list build alone, for given labels in [0, C) (the list-build
+ * step of ivf_assign_build). Outputs as in ivf_assign_build. Labels outside
+ * [0, C) give undefined lists (not detected on the host). */
+ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64_t C,
+                           int64_t *out_counts, int64_t *out_offsets, uint32_t *out_perm);
+
+/* Diagnostics of the last call on this context, copied synchronously from
+ * the workspace (waits on the stream):
+ *   out[0] queries / rows that went to the full fp64 fallback scan
+ *   out[1] rows whose top-1 was settled by fp64 re-evaluation of 2 candidates
+ *   out[2] route: sum over queries of screened candidates kept
+ *   out[3] route: queries whose candidate list overflowed
+ *   out[4] route: centroids in the threshold sample
+ *   out[5..7] reserved (0) */
+ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
+
+/* Test and tuning knobs (values persist on the context):
+ *   IVF_OPT_FORCE_FALLBACK  1 = every query / row takes the exact fp64
+ *                           fallback scan (results must not change)
+ *   IVF_OPT_SAMPLE_RANK     rank used for the routing threshold (0 = default) */
+typedef enum { IVF_OPT_FORCE_FALLBACK = 0, IVF_OPT_SAMPLE_RANK = 1 } ivf_option;
+ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IVF_H */

@@ -1,0 +1,198 @@
+"""CPU oracle for the IVF hot path of InSituANN (arXiv 2608.08751).
+
+TEST INFRASTRUCTURE ONLY. The tests, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this module; the product package
+``paper_2608_08751_amd`` never does, and shares no code with it.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64, explicit ``fma``,
+``-ffp-contract=off``); this module only builds it with gcc and marshals numpy
+arrays through ctypes. Definitions followed:
+
+* ``dist``           squared L2, the left-hand side of Eq. (6), evaluated directly;
+* ``route``          coarse search, Eq. (1): nprobe nearest centroids by (distance, id);
+* ``assign``         nearest centroid per vector, ties to the lower id;
+* ``kmeans_update``  Lloyd mean update with deterministic reseed of empty clusters;
+* ``objective``      sum of squared distances of every vector to its assigned centroid;
+* ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation.
+
+Parity pins for each function are in ``tests/test_oracle_*.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, U8 = 0, 1
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile ``liboracle.so`` with gcc (no GPU, no HIP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(
+        os.path.getmtime(_SRC), os.path.getmtime(os.path.join(_HERE, "oracle.h"))
+    ):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = [
+            "gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
+            "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
+            _SRC, "-o", tmp, "-lm",
+        ]
+        subprocess.check_call(cmd, cwd=_HERE)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+        ci = ctypes.c_int
+        lib.oracle_dist.argtypes = [p, p, ci]
+        lib.oracle_dist.restype = ctypes.c_double
+        lib.oracle_route.argtypes = [p, i64, p, i64, ci, ci, p, p, ci]
+        lib.oracle_assign.argtypes = [p, ci, i64, p, i64, ci, p, p, ci]
+        lib.oracle_splitmix64_nth.argtypes = [u64, u64]
+        lib.oracle_splitmix64_nth.restype = u64
+        lib.oracle_reseed_row.argtypes = [u64, i32, i64, i64]
+        lib.oracle_reseed_row.restype = i64
+        lib.oracle_kmeans_update.argtypes = [p, ci, i64, ci, p, i64, u64, i32, p, p]
+        lib.oracle_objective.argtypes = [p, ci, i64, ci, p, p, i64, p]
+        lib.oracle_kmeans_step.argtypes = [p, ci, i64, p, i64, ci, u64, i32, p, p, p, p, ci]
+        lib.oracle_build_lists.argtypes = [p, i64, i64, p, p, p]
+        lib.oracle_num_threads.argtypes = [ci]
+        for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
+                  lib.oracle_objective, lib.oracle_kmeans_step, lib.oracle_build_lists,
+                  lib.oracle_num_threads):
+            f.restype = ci
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _data(x):
+    x = np.ascontiguousarray(x)
+    if x.dtype == np.uint8:
+        return x, U8
+    return np.ascontiguousarray(x, dtype=np.float32), F32
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError("oracle_%s rejected its arguments (status %d)" % (what, rc))
+
+
+def num_threads(nthreads: int = 0) -> int:
+    return _load().oracle_num_threads(nthreads)
+
+
+def dist(x, c) -> float:
+    """Squared L2 distance in fp64: s = fma(x_d - c_d, x_d - c_d, s), d ascending."""
+    x, c = _f32(x), _f32(c)
+    assert x.shape == c.shape and x.ndim == 1
+    return _load().oracle_dist(_ptr(x), _ptr(c), x.shape[0])
+
+
+def route(queries, centroids, nprobe: int, nthreads: int = 0):
+    """Eq. (1): per query the nprobe nearest centroids, ascending (distance, id).
+
+    Returns (ids int32 [Q, nprobe], distances float32 [Q, nprobe]); the
+    distances are the fp64 values rounded to fp32."""
+    q, c = _f32(queries), _f32(centroids)
+    Q, D = q.shape
+    C = c.shape[0]
+    ids = np.empty((Q, nprobe), np.int32)
+    dd = np.empty((Q, nprobe), np.float32)
+    _check(_load().oracle_route(_ptr(q), Q, _ptr(c), C, D, nprobe, _ptr(ids), _ptr(dd), nthreads), "route")
+    return ids, dd
+
+
+def assign(x, centroids, nthreads: int = 0, return_dist: bool = False):
+    """Nearest centroid per row by (distance, id); optionally the fp64 distance."""
+    x, dt = _data(x)
+    c = _f32(centroids)
+    N, D = x.shape
+    labels = np.empty(N, np.int32)
+    md = np.empty(N, np.float64) if return_dist else None
+    _check(_load().oracle_assign(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(labels), _ptr(md), nthreads), "assign")
+    return (labels, md) if return_dist else labels
+
+
+def splitmix64_nth(seed: int, n: int) -> int:
+    return int(_load().oracle_splitmix64_nth(seed & (2**64 - 1), n & (2**64 - 1)))
+
+
+def reseed_row(seed: int, it: int, j: int, n: int) -> int:
+    return int(_load().oracle_reseed_row(seed & (2**64 - 1), it, j, n))
+
+
+def kmeans_update(x, labels, C: int, seed: int = 0, it: int = 0):
+    """Lloyd mean update for fixed labels; returns (centroids f32 [C, D], counts int64 [C])."""
+    x, dt = _data(x)
+    N, D = x.shape
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    out = np.empty((C, D), np.float32)
+    cnt = np.empty(C, np.int64)
+    _check(_load().oracle_kmeans_update(_ptr(x), dt, N, D, _ptr(lab), C, seed & (2**64 - 1), it, _ptr(out), _ptr(cnt)), "kmeans_update")
+    return out, cnt
+
+
+def objective(x, labels, centroids) -> float:
+    x, dt = _data(x)
+    c = _f32(centroids)
+    N, D = x.shape
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    out = np.zeros(1, np.float64)
+    _check(_load().oracle_objective(_ptr(x), dt, N, D, _ptr(lab), _ptr(c), c.shape[0], _ptr(out)), "objective")
+    return float(out[0])
+
+
+def kmeans_step(x, centroids, seed: int = 0, it: int = 0, nthreads: int = 0):
+    """One Lloyd iteration. Returns (labels, new centroids, counts, objective)."""
+    x, dt = _data(x)
+    c = _f32(centroids)
+    N, D = x.shape
+    C = c.shape[0]
+    labels = np.empty(N, np.int32)
+    out = np.empty((C, D), np.float32)
+    cnt = np.empty(C, np.int64)
+    obj = np.zeros(1, np.float64)
+    _check(_load().oracle_kmeans_step(_ptr(x), dt, N, _ptr(c), C, D, seed & (2**64 - 1), it,
+                                      _ptr(labels), _ptr(out), _ptr(cnt), _ptr(obj), nthreads), "kmeans_step")
+    return labels, out, cnt, float(obj[0])
+
+
+def build_lists(labels, C: int):
+    """Counting sort of ids by label: returns (counts int64 [C], offsets int64 [C+1], perm uint32 [N])."""
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    N = lab.shape[0]
+    counts = np.empty(C, np.int64)
+    offsets = np.empty(C + 1, np.int64)
+    perm = np.empty(N, np.uint32)
+    _check(_load().oracle_build_lists(_ptr(lab), N, C, _ptr(counts), _ptr(offsets), _ptr(perm)), "build_lists")
+    return counts, offsets, perm
+
+
+def assign_build(x, centroids, nthreads: int = 0):
+    """Full assignment followed by the inverted-list build."""
+    labels = assign(x, centroids, nthreads)
+    counts, offsets, perm = build_lists(labels, np.asarray(centroids).shape[0])
+    return labels, counts, offsets, perm

@@ -1,0 +1,340 @@
+/*
+ * CPU oracle for the IVF routing / construction hot path of InSituANN
+ * (arXiv 2608.08751).
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the plain, slow, obviously correct
+ * definition that the GPU path is checked against. Only the test suite, the
+ * smoke check and the CPU-baseline leg of the benchmark may load it; the
+ * product library never links, calls or falls back to it. It shares no code,
+ * header, table or helper with the HIP path.
+ *
+ * Everything is computed in fp64 in a fixed, documented operation order and
+ * compiled with -ffp-contract=off, so the only fused operation is the explicit
+ * fma() below.
+ *
+ * What each function follows:
+ *   oracle_dist          squared L2 distance, the left-hand side of Eq. (6)
+ *                        (Sec. "GPU coarse search"), evaluated directly.
+ *   oracle_route         coarse search, Eq. (1) (Sec. "ANN Search and IVF"):
+ *                        the nprobe nearest centroids, ordered by (distance, id).
+ *   oracle_assign        IVF construction: every vector goes to its nearest
+ *                        centroid (Sec. "ANN Search and IVF"; Sec. "System
+ *                        Architecture", index layout), ties to the lower id.
+ *   oracle_kmeans_update Lloyd's mean update (k-means training cited in the
+ *                        introduction and in "Fast Index Construction").
+ *   oracle_build_lists   cluster-major inverted lists with offset, length and
+ *                        vector ids (Sec. "System Architecture", index layout).
+ *   oracle_reseed_row    deterministic choice of a training row for an empty
+ *                        cluster; the paper is silent, the reading is SplitMix64
+ *                        (Steele, Lea & Flood, OOPSLA 2014).
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+#include "oracle.h"
+
+/* ---------------------------------------------------------------- helpers */
+
+static int resolve_threads(int nthreads)
+{
+    if (nthreads > 0) return nthreads;
+    long n = sysconf(_SC_NPROCESSORS_ONLN);
+    return n > 0 ? (int)n : 1;
+}
+
+/* Runs body(ctx, begin, end) over [0, n) split into contiguous ranges. */
+typedef void (*range_fn)(void *ctx, int64_t begin, int64_t end);
+typedef struct {
+    range_fn fn;
+    void *ctx;
+    int64_t begin, end;
+} range_job;
+
+static void *range_thread(void *arg)
+{
+    range_job *j = (range_job *)arg;
+    j->fn(j->ctx, j->begin, j->end);
+    return NULL;
+}
+
+static void parallel_for(int64_t n, int nthreads, range_fn fn, void *ctx)
+{
+    int t = resolve_threads(nthreads);
+    if (t > n) t = (int)(n > 0 ? n : 1);
+    if (t <= 1) {
+        fn(ctx, 0, n);
+        return;
+    }
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)t);
+    range_job *jobs = (range_job *)malloc(sizeof(range_job) * (size_t)t);
+    for (int i = 0; i < t; ++i) {
+        jobs[i].fn = fn;
+        jobs[i].ctx = ctx;
+        jobs[i].begin = n * i / t;
+        jobs[i].end = n * (i + 1) / t;
+        pthread_create(&th[i], NULL, range_thread, &jobs[i]);
+    }
+    for (int i = 0; i < t; ++i) pthread_join(th[i], NULL);
+    free(th);
+    free(jobs);
+}
+
+/* Element d of row i as a double, for either storage type. */
+static double elem(const void *x, int dtype, int64_t i, int D, int d)
+{
+    if (dtype == ORACLE_U8) return (double)((const uint8_t *)x)[i * (int64_t)D + d];
+    return (double)((const float *)x)[i * (int64_t)D + d];
+}
+
+/* ------------------------------------------------------------- distance */
+
+/* Squared L2 distance ||x - c||^2: s = 0; for d ascending: t = x_d - c_d;
+ * s = fma(t, t, s). All in fp64, round to nearest even. */
+double oracle_dist_row(const void *x, int dtype, int64_t i, const float *c, int D)
+{
+    double s = 0.0;
+    for (int d = 0; d < D; ++d) {
+        double t = elem(x, dtype, i, D, d) - (double)c[d];
+        s = fma(t, t, s);
+    }
+    return s;
+}
+
+double oracle_dist(const float *x, const float *c, int D)
+{
+    return oracle_dist_row(x, ORACLE_F32, 0, c, D);
+}
+
+/* (d1, id1) < (d2, id2) in the canonical total order used everywhere. */
+static int before(double d1, int64_t id1, double d2, int64_t id2)
+{
+    return d1 < d2 || (d1 == d2 && id1 < id2);
+}
+
+/* ---------------------------------------------------------------- route */
+
+typedef struct {
+    const float *q;
+    int64_t nq;
+    const float *c;
+    int64_t nc;
+    int D;
+    int k;
+    int32_t *ids;
+    float *dist;
+} route_ctx;
+
+static void route_range(void *vctx, int64_t begin, int64_t end)
+{
+    route_ctx *r = (route_ctx *)vctx;
+    double *bd = (double *)malloc(sizeof(double) * (size_t)r->k);
+    int64_t *bi = (int64_t *)malloc(sizeof(int64_t) * (size_t)r->k);
+    for (int64_t qi = begin; qi < end; ++qi) {
+        int have = 0;
+        for (int64_t j = 0; j < r->nc; ++j) {
+            double d = oracle_dist_row(r->q, ORACLE_F32, qi, r->c + j * r->D, r->D);
+            if (have == r->k && !before(d, j, bd[have - 1], bi[have - 1])) continue;
+            /* insert (d, j) into the sorted list, dropping the last if full */
+            int pos = have < r->k ? have : r->k - 1;
+            while (pos > 0 && before(d, j, bd[pos - 1], bi[pos - 1])) {
+                bd[pos] = bd[pos - 1];
+                bi[pos] = bi[pos - 1];
+                --pos;
+            }
+            bd[pos] = d;
+            bi[pos] = j;
+            if (have < r->k) ++have;
+        }
+        for (int t = 0; t < r->k; ++t) {
+            r->ids[qi * r->k + t] = (int32_t)bi[t];
+            if (r->dist) r->dist[qi * r->k + t] = (float)bd[t];
+        }
+    }
+    free(bd);
+    free(bi);
+}
+
+int oracle_route(const float *queries, int64_t nq, const float *centroids, int64_t nc, int D,
+                 int nprobe, int32_t *out_ids, float *out_dist, int nthreads)
+{
+    if (nq < 0 || nc < 1 || D < 1 || nprobe < 1 || nprobe > nc) return ORACLE_EINVAL;
+    if (nq == 0) return ORACLE_OK;
+    route_ctx ctx = {queries, nq, centroids, nc, D, nprobe, out_ids, out_dist};
+    parallel_for(nq, nthreads, route_range, &ctx);
+    return ORACLE_OK;
+}
+
+/* --------------------------------------------------------------- assign */
+
+typedef struct {
+    const void *x;
+    int dtype;
+    const float *c;
+    int64_t nc;
+    int D;
+    int32_t *labels;
+    double *mind;
+} assign_ctx;
+
+static void assign_range(void *vctx, int64_t begin, int64_t end)
+{
+    assign_ctx *a = (assign_ctx *)vctx;
+    for (int64_t i = begin; i < end; ++i) {
+        double best = 0.0;
+        int64_t arg = -1;
+        for (int64_t j = 0; j < a->nc; ++j) {
+            double d = oracle_dist_row(a->x, a->dtype, i, a->c + j * a->D, a->D);
+            if (arg < 0 || before(d, j, best, arg)) {
+                best = d;
+                arg = j;
+            }
+        }
+        a->labels[i] = (int32_t)arg;
+        if (a->mind) a->mind[i] = best;
+    }
+}
+
+int oracle_assign(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc, int D,
+                  int32_t *out_labels, double *out_mindist, int nthreads)
+{
+    if (n < 0 || nc < 1 || D < 1 || (dtype != ORACLE_F32 && dtype != ORACLE_U8)) return ORACLE_EINVAL;
+    if (n == 0) return ORACLE_OK;
+    assign_ctx ctx = {x, dtype, centroids, nc, D, out_labels, out_mindist};
+    parallel_for(n, nthreads, assign_range, &ctx);
+    return ORACLE_OK;
+}
+
+/* ---------------------------------------------------------- k-means update */
+
+/* SplitMix64 (Steele, Lea & Flood 2014): the generator state advances by the
+ * odd constant gamma, and each output is the state passed through the
+ * variant-13 finaliser. The n-th output (n >= 1) of a generator seeded with s
+ * is therefore mix(s + n * gamma). */
+#define SPLITMIX_GAMMA 0x9E3779B97F4A7C15ULL
+
+uint64_t oracle_splitmix64_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+uint64_t oracle_splitmix64_nth(uint64_t seed, uint64_t n)
+{
+    return oracle_splitmix64_mix(seed + n * SPLITMIX_GAMMA);
+}
+
+/* Row that replaces empty cluster j at Lloyd iteration `iter`: the output
+ * number ((iter << 32) | j) + 1 of SplitMix64 seeded with `seed`, mod N. */
+int64_t oracle_reseed_row(uint64_t seed, int32_t iter, int64_t j, int64_t n)
+{
+    uint64_t key = ((uint64_t)(uint32_t)iter << 32) | (uint64_t)(uint32_t)j;
+    return (int64_t)(oracle_splitmix64_nth(seed, key + 1) % (uint64_t)n);
+}
+
+/* Lloyd update for fixed labels.
+ *   counts_j = #{i : label_i = j}                      (before any reseed)
+ *   S_j      = sum of x_i with label j, in ascending i: an exact integer sum
+ *              for u8 data, a left-to-right fp64 sum for f32 data
+ *   c'_j     = (float)(S_j / (double)counts_j)          when counts_j > 0
+ *   c'_j     = (float)x_r, r = oracle_reseed_row(...)   when counts_j = 0 */
+int oracle_kmeans_update(const void *x, int dtype, int64_t n, int D, const int32_t *labels,
+                         int64_t nc, uint64_t seed, int32_t iter, float *out_centroids,
+                         int64_t *out_counts)
+{
+    if (n < 1 || nc < 1 || D < 1 || (dtype != ORACLE_F32 && dtype != ORACLE_U8)) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i)
+        if (labels[i] < 0 || labels[i] >= nc) return ORACLE_EINVAL;
+
+    int64_t *counts = (int64_t *)calloc((size_t)nc, sizeof(int64_t));
+    double *fsum = NULL;
+    uint64_t *isum = NULL;
+    if (dtype == ORACLE_U8)
+        isum = (uint64_t *)calloc((size_t)(nc * D), sizeof(uint64_t));
+    else
+        fsum = (double *)calloc((size_t)(nc * D), sizeof(double));
+
+    for (int64_t i = 0; i < n; ++i) {
+        int64_t j = labels[i];
+        counts[j] += 1;
+        for (int d = 0; d < D; ++d) {
+            if (isum)
+                isum[j * D + d] += ((const uint8_t *)x)[i * D + d];
+            else
+                fsum[j * D + d] = fsum[j * D + d] + (double)((const float *)x)[i * D + d];
+        }
+    }
+    for (int64_t j = 0; j < nc; ++j) {
+        if (counts[j] > 0) {
+            for (int d = 0; d < D; ++d) {
+                double s = isum ? (double)isum[j * D + d] : fsum[j * D + d];
+                out_centroids[j * D + d] = (float)(s / (double)counts[j]);
+            }
+        } else {
+            int64_t r = oracle_reseed_row(seed, iter, j, n);
+            for (int d = 0; d < D; ++d) out_centroids[j * D + d] = (float)elem(x, dtype, r, D, d);
+        }
+        if (out_counts) out_counts[j] = counts[j];
+    }
+    free(counts);
+    free(isum);
+    free(fsum);
+    return ORACLE_OK;
+}
+
+/* J = sum_i dist(x_i, c_{label_i}), accumulated in fp64 in ascending i. */
+int oracle_objective(const void *x, int dtype, int64_t n, int D, const int32_t *labels,
+                     const float *centroids, int64_t nc, double *out_j)
+{
+    if (n < 0 || nc < 1 || D < 1) return ORACLE_EINVAL;
+    double j = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (labels[i] < 0 || labels[i] >= nc) return ORACLE_EINVAL;
+        j = j + oracle_dist_row(x, dtype, i, centroids + (int64_t)labels[i] * D, D);
+    }
+    *out_j = j;
+    return ORACLE_OK;
+}
+
+/* One Lloyd iteration: assignment against the input centroids, then the
+ * update, then the objective of the assignment (against the input centroids). */
+int oracle_kmeans_step(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc,
+                       int D, uint64_t seed, int32_t iter, int32_t *out_labels,
+                       float *out_centroids, int64_t *out_counts, double *out_objective,
+                       int nthreads)
+{
+    int rc = oracle_assign(x, dtype, n, centroids, nc, D, out_labels, NULL, nthreads);
+    if (rc != ORACLE_OK) return rc;
+    rc = oracle_kmeans_update(x, dtype, n, D, out_labels, nc, seed, iter, out_centroids, out_counts);
+    if (rc != ORACLE_OK) return rc;
+    if (out_objective) rc = oracle_objective(x, dtype, n, D, out_labels, centroids, nc, out_objective);
+    return rc;
+}
+
+/* ----------------------------------------------------------- list build */
+
+/* counts = histogram of labels; offsets = exclusive prefix sum of counts
+ * (offsets[nc] = n); perm = ids 0..n-1 ordered by (label, id), i.e. a
+ * counting sort that keeps ids ascending inside each list. */
+int oracle_build_lists(const int32_t *labels, int64_t n, int64_t nc, int64_t *out_counts,
+                       int64_t *out_offsets, uint32_t *out_perm)
+{
+    if (n < 0 || nc < 1 || n > (int64_t)UINT32_MAX) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i)
+        if (labels[i] < 0 || labels[i] >= nc) return ORACLE_EINVAL;
+    memset(out_counts, 0, sizeof(int64_t) * (size_t)nc);
+    for (int64_t i = 0; i < n; ++i) out_counts[labels[i]] += 1;
+    out_offsets[0] = 0;
+    for (int64_t j = 0; j < nc; ++j) out_offsets[j + 1] = out_offsets[j] + out_counts[j];
+    int64_t *cursor = (int64_t *)malloc(sizeof(int64_t) * (size_t)nc);
+    memcpy(cursor, out_offsets, sizeof(int64_t) * (size_t)nc);
+    for (int64_t i = 0; i < n; ++i) out_perm[cursor[labels[i]]++] = (uint32_t)i;
+    free(cursor);
+    return ORACLE_OK;
+}
+
+int oracle_num_threads(int nthreads) { return resolve_threads(nthreads); }

@@ -1,0 +1,54 @@
+/*
+ * CPU oracle for the IVF hot path (InSituANN, arXiv 2608.08751).
+ * TEST INFRASTRUCTURE ONLY: used by the tests, the smoke check and the
+ * benchmark's CPU-baseline leg; never by the product library.
+ *
+ * All arrays are host memory, row-major and contiguous. Functions return
+ * ORACLE_OK or ORACLE_EINVAL (bad sizes, out-of-range labels); nothing else.
+ * nthreads <= 0 means one thread per online CPU.
+ */
+#ifndef IVF_ORACLE_H
+#define IVF_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORACLE_OK = 0, ORACLE_EINVAL = 1 };
+enum { ORACLE_F32 = 0, ORACLE_U8 = 1 };
+
+double oracle_dist(const float *x, const float *c, int D);
+double oracle_dist_row(const void *x, int dtype, int64_t i, const float *c, int D);
+
+int oracle_route(const float *queries, int64_t nq, const float *centroids, int64_t nc, int D,
+                 int nprobe, int32_t *out_ids, float *out_dist, int nthreads);
+
+int oracle_assign(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc, int D,
+                  int32_t *out_labels, double *out_mindist, int nthreads);
+
+uint64_t oracle_splitmix64_mix(uint64_t z);
+uint64_t oracle_splitmix64_nth(uint64_t seed, uint64_t n);
+int64_t oracle_reseed_row(uint64_t seed, int32_t iter, int64_t j, int64_t n);
+
+int oracle_kmeans_update(const void *x, int dtype, int64_t n, int D, const int32_t *labels,
+                         int64_t nc, uint64_t seed, int32_t iter, float *out_centroids,
+                         int64_t *out_counts);
+int oracle_objective(const void *x, int dtype, int64_t n, int D, const int32_t *labels,
+                     const float *centroids, int64_t nc, double *out_j);
+int oracle_kmeans_step(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc,
+                       int D, uint64_t seed, int32_t iter, int32_t *out_labels,
+                       float *out_centroids, int64_t *out_counts, double *out_objective,
+                       int nthreads);
+
+int oracle_build_lists(const int32_t *labels, int64_t n, int64_t nc, int64_t *out_counts,
+                       int64_t *out_offsets, uint32_t *out_perm);
+
+int oracle_num_threads(int nthreads);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
