@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of the IVF routing / construction hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input,
+on the 65,536-centroid, D = 128 index of the uint8-valued workloads:
+  1. ivf_kmeans_step  on 10M uint8 training rows (norms, fused fp32-MFMA
+                      screening with register top-1, certified fp64 refine,
+                      list build, Lloyd update with reseeding, objective);
+  2. ivf_assign_build on a batch of 10M uint8 base rows with the new
+                      centroids (full assignment + histogram / scan / stable
+                      scatter into cluster-major lists);
+  3. ivf_route        of 10,000 integer-valued fp32 queries, nprobe 64
+                      (threshold sample, fused filter, certified selection).
+Every routed query and every assigned row is one vector scored against all
+65,536 centroids with top-k selection, so `value` = (train rows + base rows +
+queries) / step time, in vectors/s. Inputs are resident in HBM before timing.
+
+The JSON line also carries, per call, the rates; the dominant kernel's
+roofline measured live with HIP events on the library's stream; and the CPU
+oracle timed on a bounded sample on this host (`cpu_baseline`). The
+normalised-float routing workload (262,144 centroids, D = 96, nprobe 128) is
+timed separately as an extra.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--train-rows", type=int, default=10_000_000)
+    ap.add_argument("--base-rows", type=int, default=10_000_000)
+    ap.add_argument("--queries", type=int, default=10_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the normalised routing extra")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
+                    help="also run one device copy of this size (HBM counter calibration for rocprofv3)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the sharding "
+              "design is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    C, D, K = 65536, 128, 64
+    Nt, Nb, Q = args.train_rows, args.base_rows, args.queries
+
+    t0 = time.time()
+    means = torch.from_numpy(synth.uniform_means(C, D, seed=0)).to(dev)
+    x_train = torch.empty((Nt, D), dtype=torch.uint8, device=dev)
+    x_base = torch.empty((Nb, D), dtype=torch.uint8, device=dev)
+    qrows = torch.empty((Q, D), dtype=torch.uint8, device=dev)
+    synth.device_mixture_rows_u8(means, 0, Nt, x_train, seed=0)
+    synth.device_mixture_rows_u8(means, Nt, Nb, x_base, seed=0)
+    synth.device_mixture_rows_u8(means, Nt + Nb, Q, qrows, seed=0)
+    queries = qrows.float().contiguous()
+    init = torch.from_numpy(synth.kmeans_init(Nt, C, seed=0)).to(dev)
+    c0 = x_train[init].float().contiguous()
+    torch.cuda.synchronize()
+    log("inputs generated on the device in %.1f s" % (time.time() - t0))
+
+    ctx = ivf.Context(0)
+    lab_t = torch.empty(Nt, dtype=torch.int32, device=dev)
+    c1 = torch.empty((C, D), dtype=torch.float32, device=dev)
+    cnt_t = torch.empty(C, dtype=torch.int64, device=dev)
+    obj = torch.empty(2, dtype=torch.float64, device=dev)
+    lab_b = torch.empty(Nb, dtype=torch.int32, device=dev)
+    cnt_b = torch.empty(C, dtype=torch.int64, device=dev)
+    off_b = torch.empty(C + 1, dtype=torch.int64, device=dev)
+    perm_b = torch.empty(Nb, dtype=torch.int32, device=dev)
+    ids = torch.empty((Q, K), dtype=torch.int32, device=dev)
+    dist = torch.empty((Q, K), dtype=torch.float32, device=dev)
+
+    stats = {}
+
+    def step(record=False):
+        ivf.ivf_kmeans_step(ctx, x_train, c0, seed=0, it=0, out_labels=lab_t, out_centroids=c1,
+                            out_counts=cnt_t, out_objective=obj)
+        if record:
+            stats["kmeans"] = ctx.last_stats()
+        ivf.ivf_assign_build(ctx, x_base, c1, out_labels=lab_b, out_counts=cnt_b, out_offsets=off_b,
+                             out_perm=perm_b)
+        if record:
+            stats["assign_build"] = ctx.last_stats()
+        ivf.ivf_route(ctx, queries, c1, K, out_ids=ids, out_dist=dist)
+        if record:
+            stats["route"] = ctx.last_stats()
+
+    for _ in range(args.warmup):
+        step(record=True)
+    torch.cuda.synchronize()
+    log("warmup done; fallback/refine stats:", stats)
+
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()  # clear
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step()
+        log("step %d enqueued" % i)
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    timeline = ctx.kernel_times()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+
+    ms_per_step = 1e3 * t_total / args.steps
+    vectors = Nt + Nb + Q
+    value = vectors / (t_total / args.steps)
+
+    # per-kernel aggregation over the timed steps
+    agg = {}
+    for name, ms in timeline:
+        a = agg.setdefault(name, [0, 0.0])
+        a[0] += 1
+        a[1] += ms
+    kernels = {n: {"launches": c, "avg_ms": t / c, "ms_per_step": t / args.steps} for n, (c, t) in agg.items()}
+    # the dominant kernel: fused screening with top-1 (one launch on Nt rows,
+    # one on Nb rows per step); algorithmic flops = 2 * rows * C * D
+    top1 = [ms for n, ms in timeline if n.endswith("/screen_top1")]
+    flops_top1 = 2.0 * C * D * (Nt + Nb) * args.steps
+    achieved = flops_top1 / (sum(top1) * 1e-3) / 1e12
+    roofline = {
+        "bound": "mfma",
+        "achieved": achieved,
+        "peak": PEAK_FP32_MFMA_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+        "traffic": None,
+        "kernel": "screen_kernel<128, uint8, top1>",
+        "flops_per_launch": 2.0 * C * D * Nt,
+        "avg_launch_ms": sum(top1) / len(top1),
+    }
+
+    def call_ms(call):
+        return sum(ms for n, ms in timeline if n.startswith(call + "/")) / args.steps
+
+    per_call = {
+        "kmeans_step_vectors_per_s": Nt / (call_ms("kmeans_step") * 1e-3),
+        "assign_build_vectors_per_s": Nb / (call_ms("assign_build") * 1e-3),
+        "route_queries_per_s": Q / (call_ms("route") * 1e-3),
+        "route_tflops": 2.0 * Q * C * D / (call_ms("route") * 1e-3) / 1e12,
+    }
+    build_ms = [ms for n, ms in timeline if n.endswith("/build_lists")]
+    # two builds per step: Nt rows (inside the k-means step) and Nb rows
+    per_call["build_lists_gbs"] = 12.0 * (Nt + Nb) * args.steps / (sum(build_ms) * 1e-3) / 1e9
+    per_call["build_lists_hbm_frac"] = per_call["build_lists_gbs"] / PEAK_HBM_GBS
+    per_call["step_mfma_frac"] = 2.0 * C * D * vectors / (ms_per_step * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS
+
+    result = {
+        "metric": "routed queries/s and assigned vectors/s at 1 GPU; % of fp32 MFMA peak",
+        "value": value,
+        "unit": "vectors/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded uint8 Gaussian mixture, 65,536 components, std 20, generated on the device)",
+        "config": {
+            "workload": "ivf_pipeline: kmeans_step(10M u8 rows) + assign_build(10M u8 rows) + route(10,000 queries, nprobe 64); C=65536, D=128",
+            "train_rows": Nt, "base_rows": Nb, "queries": Q, "centroids": C, "dim": D, "nprobe": K,
+        },
+        "roofline": roofline,
+        "per_call": per_call,
+        "kernels": kernels,
+        "stats": stats,
+    }
+
+    if args.copy_calibration_gib > 0:
+        n = int(args.copy_calibration_gib * 2**30)
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+
+    if not args.no_extra:
+        result["extra"] = {"route_normalised": bench_route_normalised(ctx)}
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(x_train, c0, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+def bench_route_normalised(ctx):
+    """Routing of 10,000 normalised queries against 262,144 unit-norm centroids
+    (D = 96), nprobe 128: median of 5 calls, whole-call event time."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    d = synth.normalised_route(262144, 10000, 96, seed=0)
+    q = torch.from_numpy(d["queries"]).cuda()
+    c = torch.from_numpy(d["centroids"]).cuda()
+    ids = torch.empty((10000, 128), dtype=torch.int32, device="cuda")
+    dist = torch.empty((10000, 128), dtype=torch.float32, device="cuda")
+    ivf.ivf_route(ctx, q, c, 128, out_ids=ids, out_dist=dist)
+    torch.cuda.synchronize()
+    st = ctx.last_stats()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    times = []
+    for _ in range(5):
+        ivf.ivf_route(ctx, q, c, 128, out_ids=ids, out_dist=dist)
+        tl = ctx.kernel_times()
+        times.append(sum(ms for _, ms in tl))
+        filt = sum(ms for n, ms in tl if n.endswith(("/screen_filter", "/screen_keys")))
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    t = float(np.median(times))
+    flops = 2.0 * 10000 * 262144 * 96
+    return {
+        "queries_per_s": 10000 / (t * 1e-3),
+        "ms_per_call": t,
+        "tflops": flops / (t * 1e-3) / 1e12,
+        "mfma_frac": flops / (t * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+        "screen_ms": filt,
+        "stats": st,
+    }
+
+
+def cpu_baseline(x_train, c0, target_s):
+    """The oracle (plain C, fp64, all host threads) on a bounded sample of the
+    same work: nearest-centroid search of sampled training rows against the
+    65,536 centroids. Each routed query / assigned row costs the same C*D
+    distance work, so its rate is the oracle's vectors/s for the step."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build()
+    cent = c0.cpu().numpy()
+    threads = oracle.num_threads(0)
+    rng = np.random.default_rng(99)
+    probe = max(8, threads)
+    rows = x_train[:probe].cpu().numpy()
+    t = time.perf_counter()
+    oracle.assign(rows, cent)
+    dt = time.perf_counter() - t
+    n = int(min(max(probe, probe * target_s / max(dt, 1e-6)), 200000))
+    idx = np.sort(rng.choice(x_train.shape[0], n, replace=False))
+    import torch
+
+    rows = x_train[torch.from_numpy(idx).cuda()].cpu().numpy()
+    t = time.perf_counter()
+    oracle.assign(rows, cent)
+    dt = time.perf_counter() - t
+    return {
+        "value": n / dt,
+        "unit": "vectors/s",
+        "cores": threads,
+        "kind": "oracle",
+        "cpu": cpu_model(),
+        "sample": "nearest-centroid search of %d sampled training rows against the 65,536 centroids (%.1f s)" % (n, dt),
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -164,12 +164,27 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
  *   out[5..7] reserved (0) */
 ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
 
-/* Test and tuning knobs (values persist on the context):
+/* Test, tuning and profiling knobs (values persist on the context):
  *   IVF_OPT_FORCE_FALLBACK  1 = every query / row takes the exact fp64
  *                           fallback scan (results must not change)
- *   IVF_OPT_SAMPLE_RANK     rank used for the routing threshold (0 = default) */
-typedef enum { IVF_OPT_FORCE_FALLBACK = 0, IVF_OPT_SAMPLE_RANK = 1 } ivf_option;
+ *   IVF_OPT_SAMPLE_RANK     rank used for the routing threshold (0 = default);
+ *                           changes speed only, never results or sizes
+ *   IVF_OPT_PROFILE         1 = record a HIP event pair on the context stream
+ *                           around every kernel launch of each call */
+typedef enum {
+    IVF_OPT_FORCE_FALLBACK = 0,
+    IVF_OPT_SAMPLE_RANK = 1,
+    IVF_OPT_PROFILE = 2
+} ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
+
+/* Kernel timeline recorded while IVF_OPT_PROFILE is on, across calls, since
+ * the last complete read: waits on the stream, then fills up to `max` entries
+ * of names[] (strings owned by the context, valid until the next read) and
+ * ms[] (event-to-event time of each launch, in launch order). Either array
+ * may be NULL. When max >= the number recorded, the timeline is cleared.
+ * Returns the number of launches recorded, or -1 on error. */
+int ivf_kernel_times(ivf_ctx *ctx, int max, const char **names, float *ms);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,263 @@
+"""ctypes binding of libivf.so (include/ivf.h): argument marshalling only.
+
+Every step of the computation runs in the HIP kernels behind the C ABI; this
+module only passes torch device pointers, sizes and the current HIP stream,
+and sizes the caller-owned workspace. There is no CPU path: if the library is
+not built, or no GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libivf.so")
+
+IVF_OK, IVF_EINVAL, IVF_EUNSUPPORTED, IVF_ENOMEM, IVF_EDEVICE = range(5)
+IVF_F32, IVF_U8 = 0, 1
+IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS = range(4)
+IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE = range(3)
+
+STATUS_NAMES = {0: "IVF_OK", 1: "IVF_EINVAL", 2: "IVF_EUNSUPPORTED", 3: "IVF_ENOMEM", 4: "IVF_EDEVICE"}
+
+# Exported symbols and their ctypes signatures: (name, restype, argtypes).
+_P = ctypes.c_void_p
+_I64, _I32, _U64, _INT, _SZ = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int, ctypes.c_size_t
+SIGNATURES = [
+    ("ivf_create", _INT, [_INT, _P, ctypes.POINTER(_P)]),
+    ("ivf_destroy", None, [_P]),
+    ("ivf_last_error", ctypes.c_char_p, [_P]),
+    ("ivf_set_stream", _INT, [_P, _P]),
+    ("ivf_workspace_bytes", _SZ, [_INT, _I64, _I64, _I32, _I32]),
+    ("ivf_set_workspace", _INT, [_P, _P, _SZ]),
+    ("ivf_sync", _INT, [_P]),
+    ("ivf_route", _INT, [_P, _P, _I64, _P, _I64, _I32, _I32, _P, _P]),
+    ("ivf_kmeans_step", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _U64, _I32, _P, _P, _P, _P]),
+    ("ivf_assign_build", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _P, _P]),
+    ("ivf_build_lists", _INT, [_P, _P, _I64, _I64, _P, _P, _P]),
+    ("ivf_last_stats", _INT, [_P, ctypes.POINTER(_I64)]),
+    ("ivf_set_option", _INT, [_P, _INT, _I64]),
+    ("ivf_kernel_times", _INT, [_P, _INT, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
+]
+
+_lib = None
+
+
+class IvfError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), message))
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libivf.so (after torch, so that both share one HIP runtime)."""
+    global _lib
+    if _lib is None:
+        try:
+            import torch  # noqa: F401
+        except ImportError:  # pragma: no cover - torch is part of the image
+            pass
+        if not os.path.exists(path):
+            raise RuntimeError("libivf.so is not built (%s); run __graft_entry__.build()" % path)
+        lib = ctypes.CDLL(path)
+        for name, res, args in SIGNATURES:
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream_handle():
+    import torch
+
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+class Context:
+    """An ivf_ctx bound to a device and to torch's current stream, plus a
+    grow-only workspace tensor allocated through torch."""
+
+    def __init__(self, device: int = 0):
+        import torch
+
+        self.lib = load_library()
+        self.device = device
+        self._ws = None
+        h = ctypes.c_void_p()
+        if device >= 0:
+            with torch.cuda.device(device):
+                st = self.lib.ivf_create(device, _stream_handle(), ctypes.byref(h))
+        else:
+            st = self.lib.ivf_create(device, None, ctypes.byref(h))
+        if st != IVF_OK:
+            raise IvfError(st, "ivf_create(%d) failed" % device)
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.ivf_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def error(self) -> str:
+        return (self.lib.ivf_last_error(self.handle) or b"").decode()
+
+    def check(self, st: int, what: str):
+        if st != IVF_OK:
+            raise IvfError(st, "%s: %s" % (what, self.error()))
+
+    def set_option(self, option: int, value: int):
+        self.check(self.lib.ivf_set_option(self.handle, option, value), "ivf_set_option")
+
+    def ensure_workspace(self, nbytes: int):
+        import torch
+
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = None
+            self._ws = torch.empty(max(nbytes, 1 << 20), dtype=torch.uint8, device="cuda:%d" % self.device)
+        self.check(self.lib.ivf_set_workspace(self.handle, _ptr(self._ws), self._ws.numel()),
+                   "ivf_set_workspace")
+
+    def bind_stream(self):
+        self.check(self.lib.ivf_set_stream(self.handle, _stream_handle()), "ivf_set_stream")
+
+    def sync(self):
+        self.check(self.lib.ivf_sync(self.handle), "ivf_sync")
+
+    def kernel_times(self):
+        """[(kernel name, ms)] of every launch recorded with IVF_OPT_PROFILE on
+        since the last read (the read clears the timeline)."""
+        n = self.lib.ivf_kernel_times(self.handle, 0, None, None)
+        if n < 0:
+            raise IvfError(IVF_EDEVICE, "ivf_kernel_times failed")
+        names = (ctypes.c_char_p * max(n, 1))()
+        ms = (ctypes.c_float * max(n, 1))()
+        self.lib.ivf_kernel_times(self.handle, n, names, ms)
+        return [(names[i].decode(), float(ms[i])) for i in range(n)]
+
+    def last_stats(self):
+        out = (ctypes.c_int64 * 8)()
+        self.check(self.lib.ivf_last_stats(self.handle, out), "ivf_last_stats")
+        keys = ("fallback", "refine2", "candidates", "overflow", "sample")
+        return {k: int(out[i]) for i, k in enumerate(keys)}
+
+
+def _dtype_code(t):
+    import torch
+
+    if t.dtype == torch.uint8:
+        return IVF_U8
+    if t.dtype == torch.float32:
+        return IVF_F32
+    raise TypeError("rows must be float32 or uint8, got %s" % t.dtype)
+
+
+def _device_tensor(t, name):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous device tensor" % name)
+
+
+def ivf_route(ctx: Context, queries, centroids, nprobe: int, out_ids=None, out_dist=None,
+              want_dist: bool = True):
+    """Coarse search (Eq. 1 with Eq. 6): ids [Q, nprobe] int32 and squared L2
+    distances [Q, nprobe] fp32, ascending (distance, id)."""
+    import torch
+
+    _device_tensor(queries, "queries")
+    _device_tensor(centroids, "centroids")
+    Q, D = queries.shape
+    C = centroids.shape[0]
+    dev = queries.device
+    if out_ids is None:
+        out_ids = torch.empty((Q, nprobe), dtype=torch.int32, device=dev)
+    if out_dist is None and want_dist:
+        out_dist = torch.empty((Q, nprobe), dtype=torch.float32, device=dev)
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_ROUTE, Q, C, D, nprobe))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_route(ctx.handle, _ptr(queries), Q, _ptr(centroids), C, D, nprobe,
+                                _ptr(out_ids), _ptr(out_dist)), "ivf_route")
+    return out_ids, out_dist
+
+
+def ivf_kmeans_step(ctx: Context, train, centroids, seed: int = 0, it: int = 0, out_labels=None,
+                    out_centroids=None, out_counts=None, out_objective=None):
+    """One Lloyd iteration: labels [N] int32, new centroids [C, D] fp32,
+    counts [C] int64 (before reseeding), objective (device fp64 scalar)."""
+    import torch
+
+    _device_tensor(train, "train")
+    _device_tensor(centroids, "centroids")
+    N, D = train.shape
+    C = centroids.shape[0]
+    dev = train.device
+    if out_labels is None:
+        out_labels = torch.empty(N, dtype=torch.int32, device=dev)
+    if out_centroids is None:
+        out_centroids = torch.empty((C, D), dtype=torch.float32, device=dev)
+    if out_counts is None:
+        out_counts = torch.empty(C, dtype=torch.int64, device=dev)
+    if out_objective is None:
+        out_objective = torch.empty(2, dtype=torch.float64, device=dev)
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_KMEANS_STEP, N, C, D, 0))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_kmeans_step(ctx.handle, _ptr(train), _dtype_code(train), N, _ptr(centroids),
+                                      C, D, seed & (2**64 - 1), it, _ptr(out_labels),
+                                      _ptr(out_centroids), _ptr(out_counts), _ptr(out_objective)),
+              "ivf_kmeans_step")
+    return out_labels, out_centroids, out_counts, out_objective
+
+
+def ivf_assign_build(ctx: Context, base, centroids, out_labels=None, out_counts=None,
+                     out_offsets=None, out_perm=None):
+    """Full assignment + inverted lists: labels [N], counts [C], offsets [C+1], perm [N]."""
+    import torch
+
+    _device_tensor(base, "base")
+    _device_tensor(centroids, "centroids")
+    N, D = base.shape
+    C = centroids.shape[0]
+    dev = base.device
+    if out_labels is None:
+        out_labels = torch.empty(N, dtype=torch.int32, device=dev)
+    if out_counts is None:
+        out_counts = torch.empty(C, dtype=torch.int64, device=dev)
+    if out_offsets is None:
+        out_offsets = torch.empty(C + 1, dtype=torch.int64, device=dev)
+    if out_perm is None:
+        out_perm = torch.empty(N, dtype=torch.int32, device=dev)  # uint32 bit pattern
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_ASSIGN_BUILD, N, C, D, 0))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_assign_build(ctx.handle, _ptr(base), _dtype_code(base), N, _ptr(centroids),
+                                       C, D, _ptr(out_labels), _ptr(out_counts), _ptr(out_offsets),
+                                       _ptr(out_perm)), "ivf_assign_build")
+    return out_labels, out_counts, out_offsets, out_perm
+
+
+def ivf_build_lists(ctx: Context, labels, C: int, out_counts=None, out_offsets=None, out_perm=None):
+    """Inverted lists for given labels: counts [C], offsets [C+1], perm [N] (uint32 bits in int32)."""
+    import torch
+
+    _device_tensor(labels, "labels")
+    N = labels.shape[0]
+    dev = labels.device
+    if out_counts is None:
+        out_counts = torch.empty(C, dtype=torch.int64, device=dev)
+    if out_offsets is None:
+        out_offsets = torch.empty(C + 1, dtype=torch.int64, device=dev)
+    if out_perm is None:
+        out_perm = torch.empty(N, dtype=torch.int32, device=dev)
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_BUILD_LISTS, N, C, 0, 0))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_build_lists(ctx.handle, _ptr(labels), N, C, _ptr(out_counts),
+                                      _ptr(out_offsets), _ptr(out_perm)), "ivf_build_lists")
+    return out_counts, out_offsets, out_perm

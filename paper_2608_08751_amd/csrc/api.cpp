@@ -1,0 +1,710 @@
+// C ABI of the gfx950 IVF routing / construction library (declared in
+// include/ivf.h). Validates arguments, sizes and carves the caller's
+// workspace, and enqueues the kernels on the context's stream. No call
+// synchronises with the host except ivf_sync and ivf_last_stats.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "ivf.h"
+#include "ivf_internal.h"
+
+using namespace ivf;
+
+struct ivf_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int num_cus = 1;
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+    std::string err;
+    int force_fallback = 0;
+    int sample_rank = 0;
+    unsigned long long *last_stats = nullptr;  // device, inside the workspace
+    int64_t last_sample = 0;
+    // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
+    int profile = 0;
+    std::vector<hipEvent_t> events;
+    std::vector<std::string> knames;
+    std::vector<std::string> retired;  // names handed out by the last read
+    size_t kused = 0;
+    const char *cur_call = "";
+    ~ivf_ctx()
+    {
+        for (hipEvent_t e : events) (void)hipEventDestroy(e);
+    }
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kRouteBatch = 16384;
+constexpr int kMaxNprobe = 1024;
+constexpr int kMaxD = 256;
+
+ivf_status fail(ivf_ctx *ctx, ivf_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (ctx) ctx->err = buf;
+    return st;
+}
+
+// Bump allocator over the workspace (base == nullptr: sizing only).
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base((char *)b) {}
+    template <typename T> T *take(size_t count)
+    {
+        off = (off + kAlign - 1) / kAlign * kAlign;
+        T *p = base ? (T *)(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+// Scalar area at the start of every workspace: [0] max centroid norm bits,
+// [1] worklist counter, then kNumStats uint64 counters.
+struct Scalars {
+    uint32_t *mc2_bits;
+    uint32_t *wl_cnt;
+    unsigned long long *stats;
+};
+
+Scalars take_scalars(Carver &c)
+{
+    uint32_t *p = c.take<uint32_t>(64);
+    Scalars s;
+    s.mc2_bits = p;
+    s.wl_cnt = p ? p + 1 : nullptr;
+    s.stats = p ? (unsigned long long *)(p + 16) : nullptr;
+    return s;
+}
+
+int padded_dim(int D)
+{
+    static const int dps[] = {32, 64, 96, 128, 192, 256};
+    for (int dp : dps)
+        if (D <= dp) return dp;
+    return 0;
+}
+
+double bound_coef(int DP)
+{
+    const double u = 0x1p-23;  // one fp32 ulp relative: covers any rounding mode
+    const double n = DP + 2;
+    return n * u / (1.0 - n * u);
+}
+
+int pow2_ceil(int64_t v)
+{
+    int p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+
+struct RoutePlan {
+    int64_t QB;   // queries per internal batch
+    int64_t Cs;   // threshold sample size (centroids [0, Cs)), 0 = none
+    int L;        // candidate capacity per query
+    int rank_j;
+};
+
+RoutePlan plan_route(int64_t Q, int64_t C, int k, int rank_override)
+{
+    RoutePlan p;
+    p.QB = std::max<int64_t>(1, std::min<int64_t>(Q, kRouteBatch));
+    if (C <= 2048) {
+        p.Cs = 0;
+        p.L = pow2_ceil(std::max<int64_t>(C, k));
+        p.rank_j = 0;
+        return p;
+    }
+    // sizes depend only on (Q, C, k); a rank override (a test knob) moves the
+    // threshold but never the buffers, so ivf_workspace_bytes stays valid
+    const int r = 32;
+    const int64_t mu = std::max<int64_t>(4 * (int64_t)k, 256);
+    int64_t f = mu / r;
+    f = std::min<int64_t>(std::max<int64_t>(f, 4), 64);
+    int64_t Cs = (C / f) / kChunk * kChunk;
+    Cs = std::max<int64_t>(Cs, (int64_t)2 * r * 16);
+    Cs = std::min<int64_t>(Cs, (C / 2) / kChunk * kChunk);
+    Cs = std::min<int64_t>(Cs, 65536);
+    Cs = std::max<int64_t>(Cs, kChunk);
+    p.Cs = Cs;
+    p.rank_j = (int)std::min<int64_t>(r, Cs / 16);
+    const double expected = (double)p.rank_j * (double)C / (double)Cs;
+    if (rank_override > 0) p.rank_j = (int)std::min<int64_t>(rank_override, Cs / 16);
+    int L = pow2_ceil((int64_t)(2.5 * expected) + 1);
+    L = std::max(L, std::max(512, pow2_ceil(k)));
+    p.L = std::min(L, 4096);
+    return p;
+}
+
+struct RouteLayout {
+    Scalars sc;
+    float *cnorm;
+    double *qn2;
+    float *tau;
+    uint32_t *cand_cnt;
+    uint2 *cand;
+    float *keys;
+    int32_t *wl;
+    size_t bytes;
+};
+
+RouteLayout layout_route(void *base, const RoutePlan &p, int64_t C)
+{
+    Carver c(base);
+    RouteLayout l;
+    l.sc = take_scalars(c);
+    l.cnorm = c.take<float>(C);
+    l.qn2 = c.take<double>(p.QB);
+    l.tau = c.take<float>(p.QB);
+    l.cand_cnt = c.take<uint32_t>(p.QB);
+    l.cand = c.take<uint2>((size_t)p.QB * p.L);
+    l.keys = c.take<float>((size_t)p.QB * p.Cs);
+    l.wl = c.take<int32_t>(p.QB);
+    l.bytes = c.off + kAlign;
+    return l;
+}
+
+int64_t worklist_cap(int64_t N) { return std::min<int64_t>(N, 4096 + N / 64); }
+
+struct AssignLayout {
+    Scalars sc;
+    float *cnorm;
+    int32_t *wl;
+    int64_t wl_cap;
+    // build
+    uint32_t *cntmat;
+    int64_t *counts;
+    int64_t *offsets;
+    uint32_t *perm;
+    double *jpart;
+    size_t bytes;
+};
+
+// need_lists: counts/offsets/perm live in the workspace (k-means step);
+// need_build: count matrix for the list build.
+AssignLayout layout_assign(void *base, int64_t N, int64_t C, bool need_build, bool need_lists,
+                           int num_cus)
+{
+    Carver c(base);
+    AssignLayout l{};
+    l.sc = take_scalars(c);
+    l.cnorm = c.take<float>(C);
+    l.wl_cap = worklist_cap(N);
+    l.wl = c.take<int32_t>(l.wl_cap);
+    if (need_build) l.cntmat = c.take<uint32_t>(build_scratch_bytes(plan_build(N, C, num_cus)) / 4);
+    if (need_lists) {
+        l.counts = c.take<int64_t>(C);
+        l.offsets = c.take<int64_t>(C + 1);
+        l.perm = c.take<uint32_t>(N);
+        l.jpart = c.take<double>(C);
+    }
+    l.bytes = c.off + kAlign;
+    return l;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb)
+{
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev)
+    {
+        if (dev < 0) {  // validation-only context
+            ok = false;
+            return;
+        }
+        if (hipGetDevice(&prev) != hipSuccess) {
+            ok = false;
+            return;
+        }
+        if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+    }
+    ~DeviceGuard()
+    {
+        int cur;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+ivf_status check_ws(ivf_ctx *ctx, size_t need)
+{
+    if (!ctx->ws || ctx->ws_bytes < need)
+        return fail(ctx, IVF_ENOMEM, "workspace too small: %zu bytes required, %zu provided", need,
+                    ctx->ws ? ctx->ws_bytes : (size_t)0);
+    return IVF_OK;
+}
+
+#define HIP_TRY(expr)                                                                      \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail(ctx, IVF_EDEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));  \
+    } while (0)
+
+// Drops the recorded kernel timeline.
+void prof_reset(ivf_ctx *ctx) { ctx->kused = 0; ctx->knames.clear(); }
+
+// Records the start event of a kernel launch; returns its slot or -1.
+int prof_start(ivf_ctx *ctx, const char *name)
+{
+    if (!ctx->profile) return -1;
+    const size_t i = ctx->kused++;
+    while (ctx->events.size() < 2 * ctx->kused) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) {
+            --ctx->kused;
+            return -1;
+        }
+        ctx->events.push_back(e);
+    }
+    ctx->knames.push_back(std::string(ctx->cur_call) + "/" + name);
+    (void)hipEventRecord(ctx->events[2 * i], ctx->stream);
+    return (int)i;
+}
+
+void prof_stop(ivf_ctx *ctx, int slot)
+{
+    if (slot >= 0) (void)hipEventRecord(ctx->events[2 * slot + 1], ctx->stream);
+}
+
+// Launch with optional event timing around it.
+#define TIMED(name, expr)                        \
+    do {                                         \
+        const int slot_ = prof_start(ctx, name); \
+        HIP_TRY(expr);                           \
+        prof_stop(ctx, slot_);                   \
+    } while (0)
+
+ivf_status check_common(ivf_ctx *ctx, int64_t C, int32_t D)
+{
+    if (C < 1) return fail(ctx, IVF_EINVAL, "C must be >= 1 (got %lld)", (long long)C);
+    if (C > INT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "C must fit int32 ids");
+    if (D < 4 || D > kMaxD || D % 4 != 0)
+        return fail(ctx, IVF_EUNSUPPORTED, "D must be a multiple of 4 in [4, %d] (got %d)", kMaxD, D);
+    return IVF_OK;
+}
+
+// Assignment of N rows (top-1 with certification and fallback) into labels.
+ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N,
+                          const float *cent, int64_t C, int D, int32_t *labels,
+                          const AssignLayout &l)
+{
+    hipStream_t s = ctx->stream;
+    const int DP = padded_dim(D);
+    TIMED("fill", launch_fill_u32(l.sc.mc2_bits, 64, 0u, s));
+    TIMED("centroid_norms", launch_centroid_norms(cent, C, D, l.cnorm, l.sc.mc2_bits, s));
+    ScreenArgs a{};
+    a.rows = rows;
+    a.nrows = N;
+    a.D = D;
+    a.cent = cent;
+    a.cnorm = l.cnorm;
+    a.c_begin = 0;
+    a.c_end = C;
+    a.nchunks = (C + kChunk - 1) / kChunk;
+    a.ntiles = (N + kTileRows - 1) / kTileRows;
+    a.units = a.ntiles * a.nchunks;
+    a.mc2_bits = l.sc.mc2_bits;
+    a.bound_coef = bound_coef(DP);
+    a.labels = labels;
+    a.wl = l.wl;
+    a.wl_cnt = l.sc.wl_cnt;
+    a.wl_cap = l.wl_cap;
+    a.stats = l.sc.stats;
+    a.force_fallback = ctx->force_fallback;
+    const int grid = (int)std::min<int64_t>(a.ntiles, (int64_t)ctx->num_cus);
+    TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, grid, s));
+    TIMED("assign_fallback", launch_assign_fallback(rows, rowtype, N, D, cent, C, labels, l.wl, l.sc.wl_cnt, l.wl_cap,
+                                   2 * ctx->num_cus, s));
+    ctx->last_stats = l.sc.stats;
+    ctx->last_sample = 0;
+    return IVF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ivf_status ivf_create(int device, void *hip_stream, ivf_ctx **out)
+{
+    if (!out) return IVF_EINVAL;
+    *out = nullptr;
+    if (device == -1) {  // validation-only context: checks arguments, enqueues nothing
+        ivf_ctx *c = new ivf_ctx();
+        c->device = -1;
+        c->num_cus = 256;
+        *out = c;
+        return IVF_OK;
+    }
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess) return IVF_EDEVICE;
+    if (device < 0 || device >= n) return IVF_EINVAL;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) != hipSuccess) return IVF_EDEVICE;
+    ivf_ctx *c = new ivf_ctx();
+    c->device = device;
+    c->stream = (hipStream_t)hip_stream;
+    c->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+    *out = c;
+    return IVF_OK;
+}
+
+void ivf_destroy(ivf_ctx *ctx) { delete ctx; }
+
+const char *ivf_last_error(const ivf_ctx *ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+ivf_status ivf_set_stream(ivf_ctx *ctx, void *hip_stream)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->stream = (hipStream_t)hip_stream;
+    return IVF_OK;
+}
+
+size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k)
+{
+    if (C < 1 || rows < 0) return 0;
+    (void)D;
+    int num_cus = 256;
+    int dev;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess &&
+        prop.multiProcessorCount > 0)
+        num_cus = prop.multiProcessorCount;
+    switch (op) {
+    case IVF_OP_ROUTE:
+        if (k < 1) return 0;
+        return layout_route(nullptr, plan_route(rows, C, k, 0), C).bytes;
+    case IVF_OP_KMEANS_STEP:
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, true, num_cus).bytes;
+    case IVF_OP_ASSIGN_BUILD:
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+    case IVF_OP_BUILD_LISTS:
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+    default:
+        return 0;
+    }
+}
+
+ivf_status ivf_set_workspace(ivf_ctx *ctx, void *dev_ptr, size_t bytes)
+{
+    if (!ctx) return IVF_EINVAL;
+    if (dev_ptr && ((uintptr_t)dev_ptr % kAlign) != 0)
+        return fail(ctx, IVF_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+    ctx->ws = dev_ptr;
+    ctx->ws_bytes = dev_ptr ? bytes : 0;
+    return IVF_OK;
+}
+
+ivf_status ivf_sync(ivf_ctx *ctx)
+{
+    if (!ctx) return IVF_EINVAL;
+    if (ctx->device < 0) return IVF_OK;
+    DeviceGuard g(ctx->device);
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return fail(ctx, IVF_EDEVICE, "device error: %s", hipGetErrorString(e));
+    return IVF_OK;
+}
+
+ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
+{
+    if (!ctx) return IVF_EINVAL;
+    switch (option) {
+    case IVF_OPT_FORCE_FALLBACK: ctx->force_fallback = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_SAMPLE_RANK:
+        if (value < 0 || value > 4096) return fail(ctx, IVF_EINVAL, "sample rank out of range");
+        ctx->sample_rank = (int)value;
+        return IVF_OK;
+    case IVF_OPT_PROFILE: ctx->profile = value ? 1 : 0; return IVF_OK;
+    default: return fail(ctx, IVF_EINVAL, "unknown option %d", option);
+    }
+}
+
+ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8])
+{
+    if (!ctx || !out) return IVF_EINVAL;
+    for (int i = 0; i < 8; ++i) out[i] = 0;
+    if (!ctx->last_stats) return IVF_OK;
+    DeviceGuard g(ctx->device);
+    unsigned long long h[kNumStats];
+    HIP_TRY(hipMemcpyAsync(h, ctx->last_stats, sizeof h, hipMemcpyDeviceToHost, ctx->stream));
+    HIP_TRY(hipStreamSynchronize(ctx->stream));
+    for (int i = 0; i < 8; ++i) out[i] = (int64_t)h[i];
+    out[kStatSample] = ctx->last_sample;
+    return IVF_OK;
+}
+
+int ivf_kernel_times(ivf_ctx *ctx, int max, const char **names, float *ms)
+{
+    if (!ctx || max < 0) return -1;
+    if (ctx->device < 0) return 0;
+    DeviceGuard g(ctx->device);
+    if (hipStreamSynchronize(ctx->stream) != hipSuccess) return -1;
+    const int n = (int)ctx->kused;
+    for (int i = 0; i < n && i < max; ++i) {
+        if (names) names[i] = ctx->knames[i].c_str();
+        if (ms) {
+            float t = 0.f;
+            if (hipEventElapsedTime(&t, ctx->events[2 * i], ctx->events[2 * i + 1]) != hipSuccess) t = -1.f;
+            ms[i] = t;
+        }
+    }
+    if (max > 0 && max >= n) {
+        // every entry delivered: start a new timeline (names stay valid until
+        // the next recorded launch)
+        ctx->kused = 0;
+        ctx->retired.swap(ctx->knames);
+        ctx->knames.clear();
+    }
+    return n;
+}
+
+ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
+                     int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "route";
+    if (Q < 0) return fail(ctx, IVF_EINVAL, "Q must be >= 0");
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    if (nprobe < 1 || nprobe > C)
+        return fail(ctx, IVF_EINVAL, "nprobe must be in [1, C] (got %d, C = %lld)", nprobe, (long long)C);
+    if (nprobe > kMaxNprobe) return fail(ctx, IVF_EUNSUPPORTED, "nprobe > %d", kMaxNprobe);
+    if (Q == 0) return IVF_OK;
+    if (!queries || !centroids || !out_ids) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(queries) || !aligned16(centroids) || !aligned16(out_ids) ||
+        (out_dist && !aligned16(out_dist)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t qb = (size_t)Q * D * 4, cb = (size_t)C * D * 4, ob = (size_t)Q * nprobe * 4;
+    if (overlap(out_ids, ob, queries, qb) || overlap(out_ids, ob, centroids, cb) ||
+        overlap(out_dist, ob, queries, qb) || overlap(out_dist, ob, centroids, cb) ||
+        overlap(out_ids, ob, out_dist, ob))
+        return fail(ctx, IVF_EINVAL, "outputs overlap inputs or each other");
+    const RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
+    const size_t need = layout_route(nullptr, p, C).bytes;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+
+    const RouteLayout l = layout_route(ctx->ws, p, C);
+    hipStream_t s = ctx->stream;
+    const int DP = padded_dim(D);
+    TIMED("fill", launch_fill_u32(l.sc.mc2_bits, 64, 0u, s));
+    TIMED("centroid_norms", launch_centroid_norms(centroids, C, D, l.cnorm, l.sc.mc2_bits, s));
+    for (int64_t q0 = 0; q0 < Q; q0 += p.QB) {
+        const int64_t nb = std::min(p.QB, Q - q0);
+        const float *qrows = queries + q0 * D;
+        TIMED("fill", launch_fill_u32(l.sc.wl_cnt, 1, 0u, s));
+        TIMED("row_norms", launch_row_norms(qrows, nb, D, l.qn2, s));
+        ScreenArgs a{};
+        a.rows = qrows;
+        a.nrows = nb;
+        a.D = D;
+        a.cent = centroids;
+        a.cnorm = l.cnorm;
+        a.ntiles = (nb + kTileRows - 1) / kTileRows;
+        if (p.Cs > 0) {
+            a.c_begin = 0;
+            a.c_end = p.Cs;
+            a.nchunks = p.Cs / kChunk;
+            a.units = a.ntiles * a.nchunks;
+            a.keys = l.keys;
+            TIMED("screen_keys", launch_screen(kModeKeys, kRowF32, DP, a,
+                                  (int)std::min<int64_t>(a.units, ctx->num_cus), s));
+        }
+        RouteArgs r{};
+        r.queries = qrows;
+        r.nq = nb;
+        r.cent = centroids;
+        r.C = C;
+        r.D = D;
+        r.k = nprobe;
+        r.L = p.L;
+        r.Cs = p.Cs;
+        r.rank_j = p.rank_j;
+        r.keys = l.keys;
+        r.tau = l.tau;
+        r.cand_cnt = l.cand_cnt;
+        r.cand = l.cand;
+        r.qn2 = l.qn2;
+        r.mc2_bits = l.sc.mc2_bits;
+        r.bound_coef = bound_coef(DP);
+        r.force_fallback = ctx->force_fallback;
+        r.out_ids = out_ids + q0 * nprobe;
+        r.out_dist = out_dist ? out_dist + q0 * nprobe : nullptr;
+        r.wl = l.wl;
+        r.wl_cnt = l.sc.wl_cnt;
+        r.stats = l.sc.stats;
+        TIMED("route_threshold", launch_route_threshold(r, s));
+        if (p.Cs < C) {
+            a.c_begin = p.Cs;
+            a.c_end = C;
+            a.nchunks = (C - p.Cs + kChunk - 1) / kChunk;
+            a.units = a.ntiles * a.nchunks;
+            a.keys = nullptr;
+            a.tau = l.tau;
+            a.cand_cnt = l.cand_cnt;
+            a.cand = l.cand;
+            a.L = p.L;
+            TIMED("screen_filter", launch_screen(kModeFilter, kRowF32, DP, a,
+                                  (int)std::min<int64_t>(a.units, ctx->num_cus), s));
+        }
+        TIMED("route_select", launch_route_select(r, s));
+        TIMED("route_fallback", launch_route_fallback(r, 2 * ctx->num_cus, s));
+    }
+    ctx->last_stats = l.sc.stats;
+    ctx->last_sample = p.Cs;
+    return IVF_OK;
+}
+
+static ivf_status check_rows(ivf_ctx *ctx, const void *rows, int dt, int64_t N, int32_t D,
+                             size_t *row_bytes)
+{
+    if (dt != IVF_F32 && dt != IVF_U8) return fail(ctx, IVF_EINVAL, "dtype must be IVF_F32 or IVF_U8");
+    if (N < 0) return fail(ctx, IVF_EINVAL, "N must be >= 0");
+    if (N > (int64_t)UINT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "N must be < 2^32");
+    if (N > 0 && !rows) return fail(ctx, IVF_EINVAL, "null data pointer");
+    if (rows && !aligned16(rows)) return fail(ctx, IVF_EINVAL, "data must be 16-byte aligned");
+    *row_bytes = (size_t)D * (dt == IVF_U8 ? 1 : 4);
+    return IVF_OK;
+}
+
+ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
+                           const float *centroids, int64_t C, int32_t D, uint64_t seed,
+                           int32_t iter, int32_t *out_labels, float *out_centroids,
+                           int64_t *out_counts, double *out_objective)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "kmeans_step";
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    size_t rb;
+    if ((st = check_rows(ctx, train, dt, N, D, &rb)) != IVF_OK) return st;
+    if (N == 0) return IVF_OK;
+    if (!centroids || !out_labels || !out_centroids) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(centroids) || !aligned16(out_labels) || !aligned16(out_centroids) ||
+        (out_counts && !aligned16(out_counts)) || (out_objective && !aligned16(out_objective)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t xb = (size_t)N * rb, cb = (size_t)C * D * 4, lb = (size_t)N * 4, nb = (size_t)C * 8;
+    const void *outs[4] = {out_labels, out_centroids, out_counts, out_objective};
+    const size_t osz[4] = {lb, cb, nb, 8};
+    for (int i = 0; i < 4; ++i) {
+        if (overlap(outs[i], osz[i], train, xb) || overlap(outs[i], osz[i], centroids, cb))
+            return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    }
+    const size_t need = layout_assign(nullptr, N, C, true, true, ctx->num_cus).bytes;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+
+    const AssignLayout l = layout_assign(ctx->ws, N, C, true, true, ctx->num_cus);
+    const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
+    if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
+    int64_t *counts = out_counts ? out_counts : l.counts;
+    TIMED("build_lists", launch_build_lists(bp, out_labels, l.cntmat, counts, l.offsets, l.perm, ctx->stream));
+    TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, centroids, C, counts, l.offsets, l.perm, seed,
+                                 iter, out_centroids, l.jpart, out_objective, ctx->stream));
+    return IVF_OK;
+}
+
+ivf_status ivf_assign_build(ivf_ctx *ctx, const void *base, int dt, int64_t N,
+                            const float *centroids, int64_t C, int32_t D, int32_t *out_labels,
+                            int64_t *out_counts, int64_t *out_offsets, uint32_t *out_perm)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "assign_build";
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    size_t rb;
+    if ((st = check_rows(ctx, base, dt, N, D, &rb)) != IVF_OK) return st;
+    if (!centroids || !out_counts || !out_offsets || (N > 0 && (!out_labels || !out_perm)))
+        return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(centroids) || !aligned16(out_counts) || !aligned16(out_offsets) ||
+        (out_labels && !aligned16(out_labels)) || (out_perm && !aligned16(out_perm)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t xb = (size_t)N * rb, cb = (size_t)C * D * 4;
+    const void *outs[4] = {out_labels, out_counts, out_offsets, out_perm};
+    const size_t osz[4] = {(size_t)N * 4, (size_t)C * 8, (size_t)(C + 1) * 8, (size_t)N * 4};
+    for (int i = 0; i < 4; ++i) {
+        if (overlap(outs[i], osz[i], base, xb) || overlap(outs[i], osz[i], centroids, cb))
+            return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    }
+    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus).bytes;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+
+    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
+    const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
+    if (N > 0 && (st = enqueue_assign(ctx, base, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK)
+        return st;
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
+    TIMED("build_lists", launch_build_lists(bp, out_labels, l.cntmat, out_counts, out_offsets, out_perm, ctx->stream));
+    return IVF_OK;
+}
+
+ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64_t C,
+                           int64_t *out_counts, int64_t *out_offsets, uint32_t *out_perm)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "build_lists";
+    if (C < 1) return fail(ctx, IVF_EINVAL, "C must be >= 1");
+    if (C > INT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "C must fit int32 ids");
+    if (N < 0) return fail(ctx, IVF_EINVAL, "N must be >= 0");
+    if (N > (int64_t)UINT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "N must be < 2^32");
+    if (!out_counts || !out_offsets || (N > 0 && (!labels || !out_perm)))
+        return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if ((labels && !aligned16(labels)) || !aligned16(out_counts) || !aligned16(out_offsets) ||
+        (out_perm && !aligned16(out_perm)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const void *outs[3] = {out_counts, out_offsets, out_perm};
+    const size_t osz[3] = {(size_t)C * 8, (size_t)(C + 1) * 8, (size_t)N * 4};
+    for (int i = 0; i < 3; ++i) {
+        if (overlap(outs[i], osz[i], labels, (size_t)N * 4)) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    }
+    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus).bytes;
+    ivf_status st;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
+    TIMED("build_lists", launch_build_lists(bp, labels, l.cntmat, out_counts, out_offsets, out_perm, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,127 @@
+// Internal declarations of the gfx950 IVF library: launch parameters shared
+// between the C-ABI layer (api.cpp) and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ivf {
+
+// ---- screening kernel geometry -------------------------------------------
+// One workgroup = kScreenWaves wave64s. Each wave owns 32 rows (queries or
+// data vectors) whose fp32 values live in registers as MFMA B fragments; all
+// waves share a chunk of kChunk centroids staged in LDS (double-buffered).
+constexpr int kChunk = 64;
+constexpr int kScreenWaves = 8;
+constexpr int kScreenThreads = kScreenWaves * 64;
+constexpr int kTileRows = kScreenWaves * 32;
+
+enum ScreenMode { kModeKeys = 0, kModeFilter = 1, kModeTop1 = 2 };
+enum RowType { kRowF32 = 0, kRowU8 = 1 };
+
+// Stats slots (uint64 each) in the workspace scalar area.
+enum StatSlot {
+    kStatFallback = 0,
+    kStatRefine2 = 1,
+    kStatCandidates = 2,
+    kStatOverflow = 3,
+    kStatSample = 4,
+    kNumStats = 8
+};
+
+struct ScreenArgs {
+    const void *rows;       // [nrows, D] fp32 or u8
+    int64_t nrows;
+    int D;
+    const float *cent;      // [C, D]
+    const float *cnorm;     // [C] fl32(||c||^2)
+    int64_t c_begin;        // first centroid of the range (multiple of kChunk)
+    int64_t c_end;          // one past the last centroid of the range
+    int64_t nchunks;        // ceil((c_end - c_begin) / kChunk)
+    int64_t ntiles;         // ceil(nrows / kTileRows)
+    int64_t units;          // ntiles * nchunks (keys / filter modes)
+    // keys mode
+    float *keys;            // [nrows, c_end - c_begin]
+    // filter mode
+    const float *tau;       // [nrows]
+    uint32_t *cand_cnt;     // [nrows]
+    uint2 *cand;            // [nrows, L] (key bits, centroid id)
+    int L;
+    // top-1 mode
+    const uint32_t *mc2_bits;  // max_j fl32(||c_j||^2) as float bits
+    double bound_coef;         // gamma_{DP+2} with u = 2^-23
+    int32_t *labels;           // [nrows]
+    int32_t *wl;               // fallback worklist
+    uint32_t *wl_cnt;
+    int64_t wl_cap;
+    unsigned long long *stats;
+    int force_fallback;
+};
+
+hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int grid,
+                         hipStream_t s);
+
+// ---- norms, selection, fallbacks (select.hip) -----------------------------
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_centroid_norms(const float *cent, int64_t C, int D, float *cnorm,
+                                 uint32_t *mc2_bits, hipStream_t s);
+hipError_t launch_row_norms(const float *rows, int64_t n, int D, double *out, hipStream_t s);
+
+struct RouteArgs {
+    const float *queries;  // [nq, D] (already offset to the batch)
+    int64_t nq;
+    const float *cent;
+    int64_t C;
+    int D;
+    int k;
+    int L;
+    int64_t Cs;             // centroids in the threshold sample [0, Cs)
+    int rank_j;
+    const float *keys;      // [nq, Cs]
+    float *tau;             // [nq]
+    uint32_t *cand_cnt;     // [nq]
+    uint2 *cand;            // [nq, L]
+    const double *qn2;      // [nq]
+    const uint32_t *mc2_bits;
+    double bound_coef;
+    int force_fallback;
+    int32_t *out_ids;       // [nq, k]
+    float *out_dist;        // [nq, k] or null
+    int32_t *wl;            // [nq]
+    uint32_t *wl_cnt;
+    unsigned long long *stats;
+};
+
+hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s);
+hipError_t launch_route_select(const RouteArgs &a, hipStream_t s);
+hipError_t launch_route_fallback(const RouteArgs &a, int grid, hipStream_t s);
+
+hipError_t launch_assign_fallback(const void *rows, int rowtype, int64_t N, int D,
+                                  const float *cent, int64_t C, int32_t *labels,
+                                  const int32_t *wl, const uint32_t *wl_cnt, int64_t wl_cap,
+                                  int grid, hipStream_t s);
+
+// ---- inverted-list build (lists.hip) ---------------------------------------
+constexpr int kSlice = 16384;    // buckets per workgroup (LDS counters)
+constexpr int kBuildThreads = 1024;
+constexpr int kSub = 4096;       // rows per scatter sub-chunk (4 per thread)
+
+struct BuildPlan {
+    int64_t N, C;
+    int nslices;
+    int nblocks;
+    int64_t R;               // rows per block (multiple of kSub)
+};
+BuildPlan plan_build(int64_t N, int64_t C, int num_cus);
+size_t build_scratch_bytes(const BuildPlan &p);  // count matrix bytes
+hipError_t launch_build_lists(const BuildPlan &p, const int32_t *labels, uint32_t *cntmat,
+                              int64_t *counts, int64_t *offsets, uint32_t *perm, hipStream_t s);
+
+// ---- k-means update (kmeans.hip) --------------------------------------------
+hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
+                                const float *cent_in, int64_t C, const int64_t *counts,
+                                const int64_t *offsets, const uint32_t *perm, uint64_t seed,
+                                int32_t iter, float *cent_out, double *jpart, double *objective,
+                                hipStream_t s);
+
+}  // namespace ivf

@@ -1,0 +1,136 @@
+// Lloyd mean update on gfx950 (k-means centroid training, Sec. "Fast Index
+// Construction"), run after the assignment and the list build.
+//
+// Cluster j's rows are perm[offsets[j] .. offsets[j+1]), ascending by row id
+// (the stable list build), so one wave per cluster sums them in exactly the
+// order "ascending row id": uint64 integer sums for uint8 data (exact), fp64
+// left-to-right sums for fp32 data. The new centroid is
+// (float)(sum / (double)count); an empty cluster takes training row
+//     r = SplitMix64 output (((iter << 32) | j) + 1) of a generator seeded with
+//         `seed`, mod N
+// (SplitMix64: Steele, Lea & Flood 2014). The wave also accumulates the
+// squared distances of its rows to the input centroid j; a one-workgroup
+// kernel adds the per-cluster parts in a fixed order into the objective.
+#include "ivf_internal.h"
+
+namespace ivf {
+namespace {
+
+__device__ __forceinline__ uint64_t splitmix_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ int64_t reseed_row(uint64_t seed, int32_t iter, int64_t j, int64_t N)
+{
+    const uint64_t key = ((uint64_t)(uint32_t)iter << 32) | (uint64_t)(uint32_t)j;
+    const uint64_t z = splitmix_mix(seed + (key + 1) * 0x9E3779B97F4A7C15ULL);
+    return (int64_t)(z % (uint64_t)N);
+}
+
+template <typename T> struct SumType;
+template <> struct SumType<uint8_t> { typedef unsigned long long type; };
+template <> struct SumType<float> { typedef double type; };
+
+constexpr int kMaxDimsPerLane = 4;  // D <= 256
+
+template <typename XT>
+__global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, int64_t N, int D,
+                                                     const float *__restrict__ cin, int64_t C,
+                                                     const int64_t *__restrict__ counts,
+                                                     const int64_t *__restrict__ offsets,
+                                                     const uint32_t *__restrict__ perm,
+                                                     uint64_t seed, int32_t iter,
+                                                     float *__restrict__ cout,
+                                                     double *__restrict__ jpart)
+{
+    typedef typename SumType<XT>::type S;
+    const int lane = threadIdx.x & 63;
+    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (j >= C) return;
+    const int64_t n = counts[j];
+    const int64_t o = offsets[j];
+    S sum[kMaxDimsPerLane];
+    double cj[kMaxDimsPerLane];
+#pragma unroll
+    for (int k = 0; k < kMaxDimsPerLane; ++k) {
+        sum[k] = 0;
+        const int d = lane + 64 * k;
+        cj[k] = d < D ? (double)cin[j * D + d] : 0.0;
+    }
+    double jp = 0.0;
+    for (int64_t t0 = 0; t0 < n; t0 += 64) {
+        const int64_t cnt = min((int64_t)64, n - t0);
+        const uint32_t myidx = lane < cnt ? perm[o + t0 + lane] : 0u;
+        for (int u = 0; u < cnt; ++u) {
+            const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, u);
+            const XT *x = X + i * D;
+#pragma unroll
+            for (int k = 0; k < kMaxDimsPerLane; ++k) {
+                const int d = lane + 64 * k;
+                if (d < D) {
+                    const XT v = x[d];
+                    sum[k] += (S)v;
+                    const double t = (double)v - cj[k];
+                    jp = fma(t, t, jp);
+                }
+            }
+        }
+    }
+    int64_t r = -1;
+    if (n == 0) r = reseed_row(seed, iter, j, N);
+#pragma unroll
+    for (int k = 0; k < kMaxDimsPerLane; ++k) {
+        const int d = lane + 64 * k;
+        if (d < D) {
+            float v;
+            if (n > 0)
+                v = (float)((double)sum[k] / (double)n);
+            else
+                v = (float)X[r * D + d];
+            cout[j * D + d] = v;
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) jp += __shfl_xor(jp, off);
+    if (lane == 0) jpart[j] = jp;
+}
+
+__global__ __launch_bounds__(1024) void sum_parts_kernel(const double *__restrict__ part,
+                                                         int64_t C, double *__restrict__ out)
+{
+    __shared__ double s[1024];
+    double acc = 0.0;
+    for (int64_t j = threadIdx.x; j < C; j += blockDim.x) acc += part[j];
+    s[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+        if (threadIdx.x < (unsigned)w) s[threadIdx.x] += s[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = s[0];
+}
+
+}  // namespace
+
+hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
+                                const float *cent_in, int64_t C, const int64_t *counts,
+                                const int64_t *offsets, const uint32_t *perm, uint64_t seed,
+                                int32_t iter, float *cent_out, double *jpart, double *objective,
+                                hipStream_t s)
+{
+    const unsigned grid = (unsigned)((C + 3) / 4);
+    if (rowtype == kRowU8)
+        hipLaunchKernelGGL(update_kernel<uint8_t>, dim3(grid), dim3(256), 0, s,
+                           (const uint8_t *)rows, N, D, cent_in, C, counts, offsets, perm, seed,
+                           iter, cent_out, jpart);
+    else
+        hipLaunchKernelGGL(update_kernel<float>, dim3(grid), dim3(256), 0, s, (const float *)rows,
+                           N, D, cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart);
+    if (objective)
+        hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(1024), 0, s, jpart, C, objective);
+    return hipGetLastError();
+}
+
+}  // namespace ivf

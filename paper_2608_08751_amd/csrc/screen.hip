@@ -1,0 +1,449 @@
+// Fused fp32-MFMA distance screening for gfx950.
+//
+// Computes, for a tile of rows x (queries or data vectors) against a range of
+// centroids c, the screening key
+//     key(x, c) = fl(fl32(||c||^2) - 2 * acc(x, c)),   acc = fp32 MFMA dot product,
+// i.e. Eq. (6) of the paper without the per-row constant ||x||^2 (it does not
+// change the order within a row), and consumes the keys in one of three
+// epilogues without ever writing the distance matrix:
+//   kModeKeys    write the keys (used for the routing threshold sample);
+//   kModeFilter  keep (key, id) whenever key <= tau(row) (routing candidates);
+//   kModeTop1    keep the three smallest keys per row (assignment), then
+//                certify the nearest centroid with a rounding-error bound and
+//                settle near-ties by exact fp64 re-evaluation.
+//
+// MFMA: v_mfma_f32_32x32x2_f32. A operand = centroids (M = 32 rows of a
+// chunk), B operand = rows (N = 32 rows of a wave), K split into two halves:
+// lane half h contributes dimensions [h*DP/2, (h+1)*DP/2), so every lane walks
+// contiguous memory and one ds_read_b128 feeds four K-steps. Output layout of
+// the 32x32 accumulator: lane l holds column l % 32 (one row x), register r
+// holds centroid 8*(r/4) + 4*(l/32) + r%4 of the block.
+#include "ivf_internal.h"
+
+#include <math.h>
+
+namespace ivf {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr float kInf = __builtin_huge_valf();
+
+__device__ __forceinline__ bool key_lt(float ka, int ia, float kb, int ib)
+{
+    return ka < kb || (ka == kb && ia < ib);
+}
+
+__device__ __forceinline__ bool dist_lt(double da, int ia, double db, int ib)
+{
+    return da < db || (da == db && ia < ib);
+}
+
+template <typename XT>
+__device__ __forceinline__ double exact_dist(const XT *__restrict__ x, const float *__restrict__ c,
+                                             int D)
+{
+    double s = 0.0;
+#pragma unroll 1
+    for (int d = 0; d < D; ++d) {
+        const double t = (double)x[d] - (double)c[d];
+        s = fma(t, t, s);
+    }
+    return s;
+}
+
+// Lane's half-row as fp32 B fragments: b[s] = x[row][h*KH + s], zero padded.
+template <int DP>
+__device__ __forceinline__ void load_row(const float *__restrict__ X, int64_t row, bool valid,
+                                         int D, int h, float (&b)[DP / 2])
+{
+    constexpr int KH = DP / 2;
+    const float *p = X + row * (int64_t)D + h * KH;
+#pragma unroll
+    for (int t = 0; t < KH / 4; ++t) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (valid && h * KH + 4 * t < D) v = *reinterpret_cast<const float4 *>(p + 4 * t);
+        b[4 * t + 0] = v.x;
+        b[4 * t + 1] = v.y;
+        b[4 * t + 2] = v.z;
+        b[4 * t + 3] = v.w;
+    }
+}
+
+template <int DP>
+__device__ __forceinline__ void load_row(const uint8_t *__restrict__ X, int64_t row, bool valid,
+                                         int D, int h, float (&b)[DP / 2])
+{
+    constexpr int KH = DP / 2;
+    const uint8_t *p = X + row * (int64_t)D + h * KH;
+#pragma unroll
+    for (int t = 0; t < KH / 4; ++t) {
+        uint32_t w = 0;
+        if (valid && h * KH + 4 * t < D) w = *reinterpret_cast<const uint32_t *>(p + 4 * t);
+        b[4 * t + 0] = (float)(w & 0xFFu);
+        b[4 * t + 1] = (float)((w >> 8) & 0xFFu);
+        b[4 * t + 2] = (float)((w >> 16) & 0xFFu);
+        b[4 * t + 3] = (float)(w >> 24);
+    }
+}
+
+// Per-thread registers holding one chunk on its way from HBM/L2 to LDS.
+template <int DP>
+struct ChunkRegs {
+    static constexpr int kVec = kChunk * DP / 4 / kScreenThreads;  // float4 per thread
+    float4 v[kVec];
+    float n;
+};
+
+template <int DP>
+__device__ __forceinline__ void chunk_fetch(const float *__restrict__ cent,
+                                            const float *__restrict__ cnorm, int64_t cbase,
+                                            int64_t c_end, int D, ChunkRegs<DP> &r)
+{
+    constexpr int V4 = DP / 4;
+#pragma unroll
+    for (int i = 0; i < ChunkRegs<DP>::kVec; ++i) {
+        const int idx = threadIdx.x + i * kScreenThreads;
+        const int rr = idx / V4, c4 = idx - rr * V4;
+        const int64_t row = cbase + rr;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < c_end && 4 * c4 < D)
+            v = *reinterpret_cast<const float4 *>(cent + row * (int64_t)D + 4 * c4);
+        r.v[i] = v;
+    }
+    r.n = 0.f;
+    if (threadIdx.x < kChunk) {
+        const int64_t row = cbase + threadIdx.x;
+        r.n = row < c_end ? cnorm[row] : kInf;
+    }
+}
+
+template <int DP>
+__device__ __forceinline__ void chunk_store(float *__restrict__ lc, float *__restrict__ ln,
+                                            const ChunkRegs<DP> &r)
+{
+    constexpr int V4 = DP / 4;
+    constexpr int LW = DP + 4;
+#pragma unroll
+    for (int i = 0; i < ChunkRegs<DP>::kVec; ++i) {
+        const int idx = threadIdx.x + i * kScreenThreads;
+        const int rr = idx / V4, c4 = idx - rr * V4;
+        *reinterpret_cast<float4 *>(lc + rr * LW + 4 * c4) = r.v[i];
+    }
+    if (threadIdx.x < kChunk) ln[threadIdx.x] = r.n;
+}
+
+// Per-row state of the top-1 epilogue: the three smallest keys, ids of two.
+struct Top3 {
+    float k1, k2, k3;
+    int i1, i2;
+};
+
+__device__ __forceinline__ void top3_insert(Top3 &t, float key, int id)
+{
+    if (key < t.k2) {
+        t.k3 = t.k2;
+        if (key < t.k1) {
+            t.k2 = t.k1;
+            t.i2 = t.i1;
+            t.k1 = key;
+            t.i1 = id;
+        } else {
+            t.k2 = key;
+            t.i2 = id;
+        }
+    } else {
+        t.k3 = key;
+    }
+}
+
+// Merges this lane's list with the partner lane's (both sorted by (key, id)).
+__device__ __forceinline__ Top3 top3_merge(Top3 a, Top3 b)
+{
+    if (key_lt(b.k1, b.i1, a.k1, a.i1)) {
+        Top3 t = a;
+        a = b;
+        b = t;
+    }
+    Top3 m;
+    m.k1 = a.k1;
+    m.i1 = a.i1;
+    if (key_lt(b.k1, b.i1, a.k2, a.i2)) {
+        m.k2 = b.k1;
+        m.i2 = b.i1;
+        m.k3 = fminf(a.k2, b.k2);
+    } else {
+        m.k2 = a.k2;
+        m.i2 = a.i2;
+        m.k3 = fminf(a.k3, b.k1);
+    }
+    return m;
+}
+
+// Rigorous bound on |key - (||c||^2 - 2 x.c)| for every centroid c:
+// gamma_{DP+2} * (M + 2 ||x|| sqrt(M)), M >= max ||c||^2 (slightly inflated to
+// cover the fp32 rounding of the stored norms), plus an absolute term for
+// possible flushes of subnormal products.
+__device__ __forceinline__ double key_bound(double coef, uint32_t mc2_bits, double xn2)
+{
+    const double M = (double)__uint_as_float(mc2_bits) * (1.0 + 0x1p-20);
+    return coef * (M + 2.0 * sqrt(xn2 * (1.0 + 0x1p-40)) * sqrt(M)) + 0x1p-100;
+}
+
+// Survivors of the filter epilogue are staged per wave in LDS and written out
+// 64 at a time: lane i of the flush takes staged entry i, reserves a slot in
+// its row's candidate list with one global atomic and stores (key, id).
+constexpr int kStage = 128;
+
+struct Stage {
+    uint2 kc[kScreenWaves][kStage];            // (key bits, centroid id)
+    unsigned char row[kScreenWaves][kStage];   // row within the tile
+};
+
+__device__ __forceinline__ void stage_flush(const ScreenArgs &a, Stage &st, int wave, int lane,
+                                            int64_t tile, int n)
+{
+    if (lane < n) {
+        const uint2 e = st.kc[wave][lane];
+        const int64_t row = tile * kTileRows + st.row[wave][lane];
+        const uint32_t slot = atomicAdd(a.cand_cnt + row, 1u);
+        if (slot < (uint32_t)a.L) a.cand[row * a.L + slot] = e;
+    }
+}
+
+template <int DP, typename XT, int MODE>
+__device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
+                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage &stg)
+{
+    constexpr int KH = DP / 2;
+    constexpr int LW = DP + 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row = tile * kTileRows + wave * 32 + jl;
+    const bool rvalid = row < a.nrows;
+
+    float b[KH];
+    load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
+
+    // this lane's half of ||x||^2 (exact fp32 values, fp64 sum); only the
+    // top-1 bound needs it, the routing bound uses separately computed norms
+    double xpart = 0.0;
+    if (MODE == kModeTop1) {
+#pragma unroll
+        for (int s = 0; s < KH; ++s) xpart = fma((double)b[s], (double)b[s], xpart);
+    }
+    float tau = -kInf;
+    if (MODE == kModeFilter && rvalid) tau = a.tau[row];
+    Top3 st{kInf, kInf, kInf, -1, -1};
+    int staged = 0;  // wave-uniform count of staged survivors
+
+    ChunkRegs<DP> cr;
+    chunk_fetch<DP>(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D, cr);
+    chunk_store<DP>(lds_c, lds_n, cr);
+    __syncthreads();
+
+    for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
+        const int buf = (int)((ch - ch_lo) & 1);
+        const bool more = ch + 1 < ch_hi;
+        const int64_t cbase = a.c_begin + ch * kChunk;
+        if (more) chunk_fetch<DP>(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D, cr);
+
+        const float *A0 = lds_c + buf * (kChunk * LW) + jl * LW + h * KH;
+        const float *A1 = A0 + 32 * LW;
+        f32x16 acc0 = {0.f}, acc1 = {0.f};
+        // one K-block (4 K-steps) of A fragments in flight ahead of the MFMAs;
+        // the scheduling barrier keeps the compiler from hoisting all LDS
+        // reads of the unrolled loop (which would cost ~2*DP registers)
+        float4 a0 = *reinterpret_cast<const float4 *>(A0);
+        float4 a1 = *reinterpret_cast<const float4 *>(A1);
+#pragma unroll
+        for (int t = 0; t < KH / 4; ++t) {
+            float4 n0 = a0, n1 = a1;
+            if (t + 1 < KH / 4) {
+                n0 = *reinterpret_cast<const float4 *>(A0 + 4 * (t + 1));
+                n1 = *reinterpret_cast<const float4 *>(A1 + 4 * (t + 1));
+            }
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.x, b[4 * t + 0], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.x, b[4 * t + 0], acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.y, b[4 * t + 1], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.y, b[4 * t + 1], acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.z, b[4 * t + 2], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.z, b[4 * t + 2], acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.w, b[4 * t + 3], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.w, b[4 * t + 3], acc1, 0, 0, 0);
+            a0 = n0;
+            a1 = n1;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+        // keys: key = fl(n_c - 2 acc), centroid of register r in block rb is
+        // rb*32 + 8*(r/4) + 4*h + r%4
+        const float *N = lds_n + buf * kChunk;
+        const int cb32 = (int)cbase + 4 * h;  // centroid ids fit int32
+        const int ce32 = (int)a.c_end;
+        float key[32];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 n0 = *reinterpret_cast<const float4 *>(N + 8 * g + 4 * h);
+            const float4 n1 = *reinterpret_cast<const float4 *>(N + 32 + 8 * g + 4 * h);
+            key[4 * g + 0] = fmaf(-2.0f, acc0[4 * g + 0], n0.x);
+            key[4 * g + 1] = fmaf(-2.0f, acc0[4 * g + 1], n0.y);
+            key[4 * g + 2] = fmaf(-2.0f, acc0[4 * g + 2], n0.z);
+            key[4 * g + 3] = fmaf(-2.0f, acc0[4 * g + 3], n0.w);
+            key[16 + 4 * g + 0] = fmaf(-2.0f, acc1[4 * g + 0], n1.x);
+            key[16 + 4 * g + 1] = fmaf(-2.0f, acc1[4 * g + 1], n1.y);
+            key[16 + 4 * g + 2] = fmaf(-2.0f, acc1[4 * g + 2], n1.z);
+            key[16 + 4 * g + 3] = fmaf(-2.0f, acc1[4 * g + 3], n1.w);
+        }
+
+        if (MODE == kModeKeys) {
+            if (rvalid) {
+                const int64_t ld = a.c_end - a.c_begin;
+                float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<float4 *>(out + rb * 32 + 8 * g) =
+                            make_float4(key[16 * rb + 4 * g + 0], key[16 * rb + 4 * g + 1],
+                                        key[16 * rb + 4 * g + 2], key[16 * rb + 4 * g + 3]);
+            }
+        } else if (MODE == kModeFilter) {
+#pragma unroll
+            for (int r = 0; r < 32; ++r) {
+                const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
+                const bool pass = rvalid && key[r] <= tau && cid < ce32;
+                const uint64_t mask = __ballot(pass);
+                if (mask != 0) {
+                    if (pass) {
+                        const int pos = staged + __builtin_amdgcn_mbcnt_hi(
+                            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+                        stg.kc[wave][pos] = make_uint2(__float_as_uint(key[r]), (uint32_t)cid);
+                        stg.row[wave][pos] = (unsigned char)(wave * 32 + jl);
+                    }
+                    staged += __popcll(mask);
+                    if (staged >= 64) {
+                        stage_flush(a, stg, wave, lane, tile, 64);
+                        if (lane < staged - 64) {
+                            stg.kc[wave][lane] = stg.kc[wave][64 + lane];
+                            stg.row[wave][lane] = stg.row[wave][64 + lane];
+                        }
+                        staged -= 64;
+                    }
+                }
+            }
+        } else {  // kModeTop1: ids visited in ascending order within a lane
+#pragma unroll
+            for (int r = 0; r < 32; ++r) {
+                const bool ins = key[r] < st.k3;
+                if (__ballot(ins) != 0) {
+                    if (ins) {
+                        const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
+                        top3_insert(st, key[r], cid);
+                    }
+                }
+            }
+        }
+
+        if (more) chunk_store<DP>(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk, cr);
+        __syncthreads();
+    }
+
+    if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
+
+    if (MODE == kModeTop1) {
+        const double xn2 = xpart + __shfl_xor(xpart, 32);
+        Top3 o;
+        o.k1 = __shfl_xor(st.k1, 32);
+        o.k2 = __shfl_xor(st.k2, 32);
+        o.k3 = __shfl_xor(st.k3, 32);
+        o.i1 = __shfl_xor(st.i1, 32);
+        o.i2 = __shfl_xor(st.i2, 32);
+        const Top3 m = top3_merge(st, o);
+        if (rvalid && h == 0) {
+            const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, xn2);
+            int label = -1;
+            if (!a.force_fallback) {
+                if ((double)m.k2 > (double)m.k1 + B2) {
+                    label = m.i1;
+                } else if ((double)m.k3 > (double)m.k1 + B2) {
+                    const XT *x = reinterpret_cast<const XT *>(a.rows) + row * (int64_t)a.D;
+                    const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
+                    const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
+                    label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
+                    atomicAdd(a.stats + kStatRefine2, 1ull);
+                }
+            }
+            if (label < 0) {
+                const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
+                if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
+                atomicAdd(a.stats + kStatFallback, 1ull);
+            }
+            a.labels[row] = label;
+        }
+    }
+}
+
+template <int DP, typename XT, int MODE>
+__global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a)
+{
+    __shared__ __attribute__((aligned(16))) float lds_c[2 * kChunk * (DP + 4)];
+    __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
+    __shared__ Stage stg;
+    if (MODE == kModeTop1) {
+        for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+            screen_range<DP, XT, MODE>(a, tile, 0, a.nchunks, lds_c, lds_n, stg);
+            __syncthreads();
+        }
+    } else {
+        // a contiguous range of (tile, chunk) units in tile-major order
+        int64_t u = a.units * blockIdx.x / gridDim.x;
+        const int64_t u1 = a.units * (blockIdx.x + 1) / gridDim.x;
+        while (u < u1) {
+            const int64_t tile = u / a.nchunks;
+            const int64_t ch = u - tile * a.nchunks;
+            const int64_t ch_end = min(a.nchunks, ch + (u1 - u));
+            screen_range<DP, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
+            u += ch_end - ch;
+            __syncthreads();
+        }
+    }
+}
+
+template <int DP, typename XT, int MODE>
+hipError_t launch_one(const ScreenArgs &a, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL((screen_kernel<DP, XT, MODE>), dim3(grid), dim3(kScreenThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int DP>
+hipError_t launch_dp(int mode, int rowtype, const ScreenArgs &a, int grid, hipStream_t s)
+{
+    if (mode == kModeTop1)
+        return rowtype == kRowU8 ? launch_one<DP, uint8_t, kModeTop1>(a, grid, s)
+                                 : launch_one<DP, float, kModeTop1>(a, grid, s);
+    if (rowtype != kRowF32) return hipErrorInvalidValue;
+    if (mode == kModeKeys) return launch_one<DP, float, kModeKeys>(a, grid, s);
+    return launch_one<DP, float, kModeFilter>(a, grid, s);
+}
+
+}  // namespace
+
+hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int grid,
+                         hipStream_t s)
+{
+    switch (DP) {
+    case 32: return launch_dp<32>(mode, rowtype, a, grid, s);
+    case 64: return launch_dp<64>(mode, rowtype, a, grid, s);
+    case 96: return launch_dp<96>(mode, rowtype, a, grid, s);
+    case 128: return launch_dp<128>(mode, rowtype, a, grid, s);
+    case 192: return launch_dp<192>(mode, rowtype, a, grid, s);
+    case 256: return launch_dp<256>(mode, rowtype, a, grid, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace ivf

@@ -1,0 +1,161 @@
+"""C-ABI contract on the CPU: the library loads, exports every symbol the
+header declares, and validates arguments before touching any device (a
+validation-only context, device -1, reports IVF_EDEVICE only after every
+check has passed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_08751_amd as ivf
+from paper_2608_08751_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ivf.h")
+
+BASE = 0x7F0000000000  # fake, 256-byte aligned device addresses (never dereferenced)
+GB = 1 << 30
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ivf_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ivf.load_library()
+
+
+@pytest.fixture()
+def vctx(lib):
+    ctx = ivf.Context(-1)
+    yield ctx
+    ctx.close()
+
+
+def P(off):
+    return ctypes.c_void_p(BASE + off)
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), "libivf.so does not export %s" % n
+    assert sorted(n for n, _, _ in B.SIGNATURES) == names
+
+
+def test_workspace_bytes(lib):
+    f = lib.ivf_workspace_bytes
+    assert f(B.IVF_OP_ROUTE, 1000, 1024, 128, 16) > 0
+    assert f(B.IVF_OP_ROUTE, 10000, 65536, 128, 64) > f(B.IVF_OP_ROUTE, 1000, 65536, 128, 64)
+    assert f(B.IVF_OP_KMEANS_STEP, 10**6, 4096, 128, 0) > f(B.IVF_OP_KMEANS_STEP, 10**5, 4096, 128, 0)
+    assert f(B.IVF_OP_ROUTE, 10, 0, 128, 1) == 0
+    assert f(B.IVF_OP_ROUTE, 10, 10, 128, 0) == 0
+    assert f(99, 10, 10, 128, 1) == 0
+
+
+def route(ctx, q=P(0), Q=1000, c=P(GB), C=4096, D=128, k=16, ids=P(2 * GB), dist=P(3 * GB)):
+    return ctx.lib.ivf_route(ctx.handle, q, Q, c, C, D, k, ids, dist)
+
+
+def with_ws(ctx, nbytes=4 * GB):
+    ctx.lib.ivf_set_workspace(ctx.handle, P(8 * GB), nbytes)
+
+
+def test_route_validation(vctx):
+    with_ws(vctx)
+    assert route(vctx) == B.IVF_EDEVICE  # every check passed
+    assert route(vctx, k=0) == B.IVF_EINVAL
+    assert route(vctx, k=4097, C=4096) == B.IVF_EINVAL
+    assert route(vctx, k=2000, C=4096) == B.IVF_EUNSUPPORTED
+    assert route(vctx, C=0) == B.IVF_EINVAL
+    assert route(vctx, Q=-1) == B.IVF_EINVAL
+    assert route(vctx, D=3) == B.IVF_EUNSUPPORTED
+    assert route(vctx, D=130) == B.IVF_EUNSUPPORTED
+    assert route(vctx, D=260) == B.IVF_EUNSUPPORTED
+    assert route(vctx, q=None) == B.IVF_EINVAL
+    assert route(vctx, ids=None) == B.IVF_EINVAL
+    assert route(vctx, q=P(4)) == B.IVF_EINVAL  # misaligned
+    assert "aligned" in vctx.error()
+    assert route(vctx, ids=P(0)) == B.IVF_EINVAL  # output overlaps queries
+    assert "overlap" in vctx.error()
+    assert route(vctx, dist=P(2 * GB)) == B.IVF_EINVAL  # outputs overlap each other
+    assert route(vctx, Q=0) == B.IVF_OK  # no-op
+    assert route(vctx, dist=None) == B.IVF_EDEVICE  # distances are optional
+
+
+def test_route_workspace_too_small(vctx):
+    need = vctx.lib.ivf_workspace_bytes(B.IVF_OP_ROUTE, 1000, 4096, 128, 16)
+    assert route(vctx) == B.IVF_ENOMEM
+    assert "required" in vctx.error() and str(need) in vctx.error()
+    with_ws(vctx, need - 1)
+    assert route(vctx) == B.IVF_ENOMEM
+    with_ws(vctx, need)
+    assert route(vctx) == B.IVF_EDEVICE
+    assert vctx.lib.ivf_set_workspace(vctx.handle, P(8 * GB + 16), need) == B.IVF_EINVAL
+
+
+def kstep(ctx, x=P(0), dt=B.IVF_U8, N=10**6, c=P(GB), C=4096, D=128, lab=P(2 * GB), cout=P(3 * GB),
+          cnt=P(4 * GB), obj=P(5 * GB)):
+    return ctx.lib.ivf_kmeans_step(ctx.handle, x, dt, N, c, C, D, 7, 0, lab, cout, cnt, obj)
+
+
+def test_kmeans_validation(vctx):
+    with_ws(vctx, 64 * GB)
+    assert kstep(vctx) == B.IVF_EDEVICE
+    assert kstep(vctx, dt=5) == B.IVF_EINVAL
+    assert kstep(vctx, N=-1) == B.IVF_EINVAL
+    assert kstep(vctx, N=2**32) == B.IVF_EUNSUPPORTED
+    assert kstep(vctx, N=0) == B.IVF_OK
+    assert kstep(vctx, cout=P(GB)) == B.IVF_EINVAL  # new centroids alias the input ones
+    assert kstep(vctx, lab=P(0)) == B.IVF_EINVAL
+    assert kstep(vctx, cnt=P(2 * GB)) == B.IVF_EINVAL
+    assert kstep(vctx, cnt=None, obj=None) == B.IVF_EDEVICE  # optional outputs
+    assert kstep(vctx, cout=None) == B.IVF_EINVAL
+    assert kstep(vctx, D=8, C=0) == B.IVF_EINVAL
+    with_ws(vctx, 1024)
+    assert kstep(vctx) == B.IVF_ENOMEM
+
+
+def test_assign_build_and_lists_validation(vctx):
+    lib, h = vctx.lib, vctx.handle
+    with_ws(vctx, 64 * GB)
+    ab = lambda **kw: lib.ivf_assign_build(h, kw.get("x", P(0)), B.IVF_U8, kw.get("N", 10**6), P(GB), 4096, 128,
+                                           kw.get("lab", P(2 * GB)), kw.get("cnt", P(3 * GB)),
+                                           kw.get("off", P(4 * GB)), kw.get("perm", P(5 * GB)))
+    assert ab() == B.IVF_EDEVICE
+    assert ab(perm=P(2 * GB)) == B.IVF_EINVAL
+    assert ab(off=None) == B.IVF_EINVAL
+    assert ab(N=2**32) == B.IVF_EUNSUPPORTED
+    bl = lambda **kw: lib.ivf_build_lists(h, kw.get("lab", P(0)), kw.get("N", 10**6), kw.get("C", 4096),
+                                          kw.get("cnt", P(GB)), kw.get("off", P(2 * GB)), kw.get("perm", P(3 * GB)))
+    assert bl() == B.IVF_EDEVICE
+    assert bl(C=0) == B.IVF_EINVAL
+    assert bl(perm=P(0)) == B.IVF_EINVAL
+    assert bl(N=0) == B.IVF_EDEVICE  # lists of zero rows still write counts/offsets
+
+
+def test_options_and_errors(vctx):
+    lib, h = vctx.lib, vctx.handle
+    assert lib.ivf_set_option(h, B.IVF_OPT_FORCE_FALLBACK, 1) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_SAMPLE_RANK, 16) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_SAMPLE_RANK, -3) == B.IVF_EINVAL
+    assert lib.ivf_set_option(h, 42, 0) == B.IVF_EINVAL
+    assert "unknown option" in vctx.error()
+    assert lib.ivf_sync(h) == B.IVF_OK
+    out = (ctypes.c_int64 * 8)()
+    assert lib.ivf_last_stats(h, out) == B.IVF_OK and list(out) == [0] * 8
+    assert lib.ivf_route(None, P(0), 1, P(GB), 1, 4, 1, P(2 * GB), None) == B.IVF_EINVAL
+
+
+def test_no_cpu_fallback_without_gpu():
+    import torch
+
+    if torch.cuda.is_available():
+        pytest.skip("GPU present")
+    with pytest.raises(Exception):
+        ivf.Context(0)

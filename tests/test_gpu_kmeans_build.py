@@ -1,0 +1,241 @@
+"""GPU parity of ivf_kmeans_step, ivf_assign_build and ivf_build_lists
+against the oracle: labels, counts, offsets, permutation and centroids must
+be bit-identical; the objective agrees to fp64 summation-order rounding."""
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+FULL = os.environ.get("IVF_FULL_SCALE", "0") == "1"
+
+
+@pytest.fixture(scope="module")
+def ivf_ctx():
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ctx = ivf.Context(0)
+    yield ctx
+    ctx.close()
+
+
+def to_dev(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_step(ctx, x, c, seed, it):
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    lab, cen, cnt, obj = ivf.ivf_kmeans_step(ctx, to_dev(x), to_dev(c), seed=seed, it=it)
+    torch.cuda.synchronize()
+    return lab.cpu().numpy(), cen.cpu().numpy(), cnt.cpu().numpy(), float(obj[0].cpu()), ctx.last_stats()
+
+
+def assert_step_equal(ctx, oracle_mod, x, c, seed, it):
+    lab, cen, cnt, obj, stats = gpu_step(ctx, x, c, seed, it)
+    olab, ocen, ocnt, oobj = oracle_mod.kmeans_step(x, c, seed=seed, it=it)
+    assert (lab == olab).all(), "labels differ at rows %s" % np.nonzero(lab != olab)[0][:10]
+    assert (cnt == ocnt).all()
+    assert (cen == ocen).all(), "centroids differ in clusters %s" % np.unique(np.nonzero(cen != ocen)[0])[:10]
+    assert abs(obj - oobj) <= 1e-12 * max(oobj, 1e-300)
+    return cen, obj, stats
+
+
+def test_kmeans_chain_uint8(ivf_ctx, oracle_mod):
+    """Four Lloyd iterations on 20,000 u8 rows (ragged tile), 300 clusters."""
+    means = synth.uniform_means(400, 128, seed=1)
+    x, _ = synth.mixture_rows_u8(means, 0, 20000, seed=1)
+    c = x[synth.kmeans_init(20000, 300, seed=1)].astype(np.float32)
+    objs = []
+    for it in range(4):
+        c, obj, stats = assert_step_equal(ivf_ctx, oracle_mod, x, c, 1, it)
+        objs.append(obj)
+    assert all(b <= a * (1 + 1e-9) for a, b in zip(objs, objs[1:]))
+
+
+def test_kmeans_float_rows(ivf_ctx, oracle_mod):
+    rng = np.random.default_rng(2)
+    x = (rng.standard_normal((6001, 64)) * 3 + rng.integers(0, 5, (6001, 1))).astype(np.float32)
+    c = x[rng.choice(6001, 100, replace=False)].copy()
+    for it in range(2):
+        c, _, _ = assert_step_equal(ivf_ctx, oracle_mod, x, c, 9, it)
+
+
+def test_kmeans_empty_clusters_reseed(ivf_ctx, oracle_mod):
+    rng = np.random.default_rng(4)
+    x = rng.integers(0, 60, (3000, 32)).astype(np.uint8)
+    c = np.vstack([x[:20].astype(np.float32), np.full((30, 32), 5000.0, np.float32)])
+    cen, _, _ = assert_step_equal(ivf_ctx, oracle_mod, x, c, 77, 5)
+    for j in range(20, 50):
+        assert (cen[j] == x[oracle_mod.reseed_row(77, 5, j, 3000)]).all()
+
+
+@pytest.mark.parametrize("N,C,D", [(1, 1, 4), (500, 1, 8), (257, 256, 16), (1000, 1000, 36)])
+def test_kmeans_small_shapes(ivf_ctx, oracle_mod, N, C, D):
+    rng = np.random.default_rng(N + C)
+    x = rng.integers(0, 256, (N, D)).astype(np.uint8)
+    c = rng.uniform(0, 255, (C, D)).astype(np.float32)
+    assert_step_equal(ivf_ctx, oracle_mod, x, c, 3, 1)
+
+
+def test_kmeans_forced_fallback_is_identical(ivf_ctx, oracle_mod):
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(100, 64, seed=6)
+    x, _ = synth.mixture_rows_u8(means, 0, 5000, seed=6)
+    c = x[synth.kmeans_init(5000, 80, seed=6)].astype(np.float32)
+    ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 1)
+    try:
+        _, _, stats = assert_step_equal(ivf_ctx, oracle_mod, x, c, 6, 0)
+        assert stats["fallback"] == 5000
+    finally:
+        ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 0)
+
+
+# ------------------------------------------------------------------ lists
+
+def gpu_lists(ctx, labels, C):
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    cnt, off, perm = ivf.ivf_build_lists(ctx, to_dev(labels), C)
+    torch.cuda.synchronize()
+    return cnt.cpu().numpy(), off.cpu().numpy(), perm.cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("N,C,skew", [
+    (0, 5, 0.0), (1, 1, 0.0), (1000, 1, 0.0), (12345, 300, 0.0), (100003, 20000, 0.0),
+    (2000001, 65536, 0.0), (1000000, 40000, 1.1), (300000, 3, 0.0), (4099, 70000, 0.0),
+])
+def test_build_lists_exact(ivf_ctx, oracle_mod, N, C, skew):
+    lab = synth.random_labels(N, C, seed=N + C, skew=skew)
+    cnt, off, perm = gpu_lists(ivf_ctx, lab, C)
+    ocnt, ooff, operm = oracle_mod.build_lists(lab, C)
+    assert (cnt == ocnt).all() and (off == ooff).all()
+    assert (perm == operm).all()
+
+
+def test_build_lists_single_list_all_rows(ivf_ctx, oracle_mod):
+    lab = np.full(200000, 7, np.int32)
+    cnt, off, perm = gpu_lists(ivf_ctx, lab, 20)
+    assert cnt[7] == 200000 and (perm == np.arange(200000, dtype=np.uint32)).all()
+
+
+@pytest.mark.parametrize("dt", ["u8", "f32"])
+def test_assign_build_small(ivf_ctx, oracle_mod, dt):
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(300, 128, seed=8)
+    x, _ = synth.mixture_rows_u8(means, 0, 30001, seed=8)
+    if dt == "f32":
+        x = x.astype(np.float32)
+    c = means[:250]
+    lab, cnt, off, perm = ivf.ivf_assign_build(ivf_ctx, to_dev(x), to_dev(c))
+    torch.cuda.synchronize()
+    olab = oracle_mod.assign(x, c)
+    ocnt, ooff, operm = oracle_mod.build_lists(olab, 250)
+    assert (lab.cpu().numpy() == olab).all()
+    assert (cnt.cpu().numpy() == ocnt).all() and (off.cpu().numpy() == ooff).all()
+    assert (perm.cpu().numpy().view(np.uint32) == operm).all()
+
+
+# ------------------------------------------------------- full-size workloads
+
+def test_kmeans_full_size_sampled(ivf_ctx, oracle_mod):
+    """10M u8 rows from the 65,536-component mixture, 65,536 centroids: the
+    first iteration's labels on a row sample match the oracle; counts are the
+    histogram of the labels; sampled clusters' centroids are their exact
+    means; the objective does not increase over three iterations."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    N, C, D = 10_000_000, 65536, 128
+    means = synth.uniform_means(C, D, seed=0)
+    md = to_dev(means)
+    x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
+    synth.device_mixture_rows_u8(md, 0, N, x, seed=0)
+    init = synth.kmeans_init(N, C, seed=0)
+    c = x[to_dev(init)].float().contiguous()
+    c0 = c.cpu().numpy()
+    objs = []
+    for it in range(3):
+        lab, cen, cnt, obj = ivf.ivf_kmeans_step(ivf_ctx, x, c, seed=0, it=it)
+        torch.cuda.synchronize()
+        stats = ivf_ctx.last_stats()
+        print("kmeans full-size iteration", it, stats)
+        objs.append(float(obj[0].cpu()))
+        if it == 0:
+            labh = lab.cpu().numpy()
+            rng = np.random.default_rng(7)
+            rows = np.sort(rng.choice(N, 384, replace=False))
+            xs = x[to_dev(rows)].cpu().numpy()
+            assert (labh[rows] == oracle_mod.assign(xs, c0)).all()
+            cnth = cnt.cpu().numpy()
+            assert (cnth == np.bincount(labh, minlength=C)).all()
+            order = np.argsort(labh, kind="stable")
+            starts = np.concatenate([[0], np.cumsum(cnth)])
+            cenh = cen.cpu().numpy()
+            for j in rng.choice(np.nonzero(cnth)[0], 64, replace=False):
+                members = order[starts[j]:starts[j + 1]]
+                xm = x[to_dev(members)].cpu().numpy()
+                want = xm.astype(np.float64).mean(axis=0).astype(np.float32)
+                assert (cenh[j] == want).all()
+            assert stats["fallback"] < N // 1000
+        c = cen
+    assert all(b <= a * (1 + 1e-9) for a, b in zip(objs, objs[1:]))
+
+
+@pytest.mark.parametrize("N", [16 * 2**20] + ([10**9] if FULL else []))
+def test_assign_build_full_generator_sampled(ivf_ctx, oracle_mod, N):
+    """u8 rows from the 65,536-component mixture generated on the device in
+    64M-row chunks, assigned to the 65,536 component means; sampled labels
+    match the oracle and the lists satisfy every invariant of the layout.
+    N = 1e9 (128 GB resident) runs with IVF_FULL_SCALE=1."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    C, D = 65536, 128
+    chunk = 64 * 2**20
+    means = synth.uniform_means(C, D, seed=0)
+    md = to_dev(means)
+    x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
+    for r0 in range(0, N, chunk):
+        synth.device_mixture_rows_u8(md, r0, min(chunk, N - r0), x[r0:r0 + chunk], seed=0)
+    lab, cnt, off, perm = ivf.ivf_assign_build(ivf_ctx, x, md)
+    torch.cuda.synchronize()
+    print("assign_build stats:", ivf_ctx.last_stats())
+    rng = np.random.default_rng(5)
+    rows = np.sort(rng.choice(N, 256, replace=False))
+    xs = x[to_dev(rows)].cpu().numpy()
+    labs = lab[to_dev(rows)].cpu().numpy()
+    assert (labs == oracle_mod.assign(xs, means)).all()
+    # layout invariants over the whole output
+    cnth = cnt.cpu().numpy()
+    offh = off.cpu().numpy()
+    assert cnth.sum() == N and offh[0] == 0 and (offh[1:] == np.cumsum(cnth)).all()
+    labd = lab.long()
+    assert (torch.bincount(labd, minlength=C).cpu().numpy() == cnth).all()
+    permd = perm.long() & 0xFFFFFFFF
+    lp = labd[permd]
+    assert bool((lp[1:] >= lp[:-1]).all())
+    same = lp[1:] == lp[:-1]
+    assert bool((permd[1:][same] > permd[:-1][same]).all())
+    seen = torch.zeros(N, dtype=torch.bool, device="cuda")
+    seen[permd] = True
+    assert bool(seen.all())
