@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the normalised routing extra")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--build-rows", type=int, default=1_000_000_000,
+                    help="rows for the separately timed list build at scale (0 = skip)")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="also run one device copy of this size (HBM counter calibration for rocprofv3)")
     return ap.parse_args()
@@ -182,7 +184,7 @@ def main():
         "route_queries_per_s": Q / (call_ms("route") * 1e-3),
         "route_tflops": 2.0 * Q * C * D / (call_ms("route") * 1e-3) / 1e12,
     }
-    build_ms = [ms for n, ms in timeline if n.endswith("/build_lists")]
+    build_ms = [ms for n, ms in timeline if "/build_" in n]
     # two builds per step: Nt rows (inside the k-means step) and Nb rows
     per_call["build_lists_gbs"] = 12.0 * (Nt + Nb) * args.steps / (sum(build_ms) * 1e-3) / 1e9
     per_call["build_lists_hbm_frac"] = per_call["build_lists_gbs"] / PEAK_HBM_GBS
@@ -221,11 +223,16 @@ def main():
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = n
 
-    if not args.no_extra:
-        result["extra"] = {"route_normalised": bench_route_normalised(ctx)}
-
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(x_train, c0, args.cpu_seconds)
+
+    if not args.no_extra:
+        result["extra"] = {"route_normalised": bench_route_normalised(ctx)}
+        if args.build_rows > 0:
+            # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
+            del x_train, x_base, lab_t, lab_b, perm_b
+            torch.cuda.empty_cache()
+            result["extra"]["build_lists_at_scale"] = bench_build(ctx, args.build_rows, C)
 
     print(json.dumps(result), flush=True)
 
@@ -265,6 +272,40 @@ def bench_route_normalised(ctx):
         "mfma_frac": flops / (t * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS,
         "screen_ms": filt,
         "stats": st,
+    }
+
+
+def bench_build(ctx, N, C):
+    """ivf_build_lists on N uniform device-generated labels over C lists:
+    median of 3 calls; algorithmic bytes = 12 per row (histogram reads a 4-byte
+    label; the scatter reads it again and writes a 4-byte id)."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    lab = torch.empty(N, dtype=torch.int32, device="cuda")
+    synth.device_labels(N, C, lab, seed=0)
+    cnt = torch.empty(C, dtype=torch.int64, device="cuda")
+    off = torch.empty(C + 1, dtype=torch.int64, device="cuda")
+    perm = torch.empty(N, dtype=torch.int32, device="cuda")
+    ivf.ivf_build_lists(ctx, lab, C, cnt, off, perm)
+    torch.cuda.synchronize()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    runs = []
+    for _ in range(3):
+        ivf.ivf_build_lists(ctx, lab, C, cnt, off, perm)
+        runs.append(ctx.kernel_times())
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    totals = [sum(ms for _, ms in r) for r in runs]
+    i = int(np.argsort(totals)[len(totals) // 2])
+    t = totals[i]
+    gbs = 12.0 * N / (t * 1e-3) / 1e9
+    return {
+        "rows": N, "lists": C, "ms": t, "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+        "kernels_ms": {n.split("/", 1)[1]: ms for n, ms in runs[i]},
     }
 
 

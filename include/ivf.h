@@ -170,11 +170,14 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *   IVF_OPT_SAMPLE_RANK     rank used for the routing threshold (0 = default);
  *                           changes speed only, never results or sizes
  *   IVF_OPT_PROFILE         1 = record a HIP event pair on the context stream
- *                           around every kernel launch of each call */
+ *                           around every kernel launch of each call
+ *   IVF_OPT_BUILD_BLOCKS    cap on the row blocks of the list build (0 =
+ *                           default); changes speed only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,
-    IVF_OPT_PROFILE = 2
+    IVF_OPT_PROFILE = 2,
+    IVF_OPT_BUILD_BLOCKS = 3
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

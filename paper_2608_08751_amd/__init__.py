@@ -21,6 +21,7 @@ from ._binding import (  # noqa: F401
     IVF_OP_BUILD_LISTS,
     IVF_OP_KMEANS_STEP,
     IVF_OP_ROUTE,
+    IVF_OPT_BUILD_BLOCKS,
     IVF_OPT_FORCE_FALLBACK,
     IVF_OPT_PROFILE,
     IVF_OPT_SAMPLE_RANK,

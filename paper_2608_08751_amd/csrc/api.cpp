@@ -27,6 +27,7 @@ struct ivf_ctx {
     std::string err;
     int force_fallback = 0;
     int sample_rank = 0;
+    int build_blocks = 0;
     unsigned long long *last_stats = nullptr;  // device, inside the workspace
     int64_t last_sample = 0;
     // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
@@ -344,6 +345,15 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     return IVF_OK;
 }
 
+ivf_status enqueue_build(ivf_ctx *ctx, const BuildPlan &bp, const int32_t *labels, uint32_t *cntmat,
+                         int64_t *counts, int64_t *offsets, uint32_t *perm)
+{
+    TIMED("build_hist", launch_build_hist(bp, labels, cntmat, ctx->stream));
+    TIMED("build_scan", launch_build_scan(bp, cntmat, counts, offsets, ctx->stream));
+    TIMED("build_scatter", launch_build_scatter(bp, labels, cntmat, offsets, perm, ctx->stream));
+    return IVF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -438,6 +448,10 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
         ctx->sample_rank = (int)value;
         return IVF_OK;
     case IVF_OPT_PROFILE: ctx->profile = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_BUILD_BLOCKS:
+        if (value < 0 || value > 65536) return fail(ctx, IVF_EINVAL, "build blocks out of range");
+        ctx->build_blocks = (int)value;
+        return IVF_OK;
     default: return fail(ctx, IVF_EINVAL, "unknown option %d", option);
     }
 }
@@ -626,9 +640,9 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
     const AssignLayout l = layout_assign(ctx->ws, N, C, true, true, ctx->num_cus);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
     int64_t *counts = out_counts ? out_counts : l.counts;
-    TIMED("build_lists", launch_build_lists(bp, out_labels, l.cntmat, counts, l.offsets, l.perm, ctx->stream));
+    if ((st = enqueue_build(ctx, bp, out_labels, l.cntmat, counts, l.offsets, l.perm)) != IVF_OK) return st;
     TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, centroids, C, counts, l.offsets, l.perm, seed,
                                  iter, out_centroids, l.jpart, out_objective, ctx->stream));
     return IVF_OK;
@@ -668,8 +682,8 @@ ivf_status ivf_assign_build(ivf_ctx *ctx, const void *base, int dt, int64_t N,
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if (N > 0 && (st = enqueue_assign(ctx, base, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK)
         return st;
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
-    TIMED("build_lists", launch_build_lists(bp, out_labels, l.cntmat, out_counts, out_offsets, out_perm, ctx->stream));
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
+    if ((st = enqueue_build(ctx, bp, out_labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
     return IVF_OK;
 }
 
@@ -701,8 +715,8 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
     const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus);
-    TIMED("build_lists", launch_build_lists(bp, labels, l.cntmat, out_counts, out_offsets, out_perm, ctx->stream));
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
+    if ((st = enqueue_build(ctx, bp, labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

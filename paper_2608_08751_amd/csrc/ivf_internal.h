@@ -112,10 +112,15 @@ struct BuildPlan {
     int nblocks;
     int64_t R;               // rows per block (multiple of kSub)
 };
-BuildPlan plan_build(int64_t N, int64_t C, int num_cus);
+// max_blocks > 0 caps the number of row blocks (fewer open write frontiers)
+BuildPlan plan_build(int64_t N, int64_t C, int num_cus, int max_blocks = 0);
 size_t build_scratch_bytes(const BuildPlan &p);  // count matrix bytes
-hipError_t launch_build_lists(const BuildPlan &p, const int32_t *labels, uint32_t *cntmat,
-                              int64_t *counts, int64_t *offsets, uint32_t *perm, hipStream_t s);
+hipError_t launch_build_hist(const BuildPlan &p, const int32_t *labels, uint32_t *cntmat,
+                             hipStream_t s);
+hipError_t launch_build_scan(const BuildPlan &p, uint32_t *cntmat, int64_t *counts, int64_t *offsets,
+                             hipStream_t s);
+hipError_t launch_build_scatter(const BuildPlan &p, const int32_t *labels, const uint32_t *cntmat,
+                                const int64_t *offsets, uint32_t *perm, hipStream_t s);
 
 // ---- k-means update (kmeans.hip) --------------------------------------------
 hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,

@@ -33,6 +33,18 @@ __device__ __forceinline__ void decode_block(int w, int nblocks, int nslices, in
     }
 }
 
+// Four consecutive labels starting at r (r % 4 == 0); -1 beyond r1.
+__device__ __forceinline__ int4 load_labels4(const int32_t *__restrict__ labels, int64_t r, int64_t r1)
+{
+    if (r + 3 < r1) return *reinterpret_cast<const int4 *>(labels + r);
+    int4 v;
+    v.x = r < r1 ? labels[r] : -1;
+    v.y = r + 1 < r1 ? labels[r + 1] : -1;
+    v.z = r + 2 < r1 ? labels[r + 2] : -1;
+    v.w = r + 3 < r1 ? labels[r + 3] : -1;
+    return v;
+}
+
 __global__ __launch_bounds__(kBuildThreads) void hist_kernel(const int32_t *__restrict__ labels,
                                                              int64_t N, int64_t R, int64_t C,
                                                              int nblocks, int nslices,
@@ -47,21 +59,19 @@ __global__ __launch_bounds__(kBuildThreads) void hist_kernel(const int32_t *__re
     __syncthreads();
     const int64_t r0 = (int64_t)b * R;
     const int64_t r1 = min(N, r0 + R);
-    for (int64_t r = r0 + 4 * (int64_t)threadIdx.x; r < r1; r += 4 * (int64_t)blockDim.x) {
-        int l[4];
-        if (r + 3 < r1) {
-            const int4 v = *reinterpret_cast<const int4 *>(labels + r);
-            l[0] = v.x;
-            l[1] = v.y;
-            l[2] = v.z;
-            l[3] = v.w;
-        } else {
-            for (int e = 0; e < 4; ++e) l[e] = r + e < r1 ? labels[r + e] : -1;
-        }
+    const int64_t step = 4 * (int64_t)blockDim.x;
+    for (int64_t r = r0 + 4 * (int64_t)threadIdx.x; r < r1; r += 4 * step) {
+        int4 v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t rel = (uint32_t)((int64_t)l[e] - j0);
-            if (l[e] >= 0 && rel < (uint32_t)width) atomicAdd(&cnt[rel], 1u);
+        for (int u = 0; u < 4; ++u) v[u] = load_labels4(labels, r + u * step, r1);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int l[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t rel = (uint32_t)((int64_t)l[e] - j0);
+                if (l[e] >= 0 && rel < (uint32_t)width) atomicAdd(&cnt[rel], 1u);
+            }
         }
     }
     __syncthreads();
@@ -134,18 +144,13 @@ __global__ __launch_bounds__(kBuildThreads) void scatter_kernel(
     const int64_t r0 = (int64_t)b * R;
     const int64_t r1 = min(N, r0 + R);
     const int t4 = 4 * threadIdx.x;
+    // labels of the next sub-chunk are loaded one sub-chunk ahead
+    int4 nxt = load_labels4(labels, r0 + t4, r1);
     for (int64_t base = r0; base < r1; base += kSub) {
         const int64_t r = base + t4;
-        int l[4];
-        if (r + 3 < r1) {
-            const int4 v = *reinterpret_cast<const int4 *>(labels + r);
-            l[0] = v.x;
-            l[1] = v.y;
-            l[2] = v.z;
-            l[3] = v.w;
-        } else {
-            for (int e = 0; e < 4; ++e) l[e] = r + e < r1 ? labels[r + e] : -1;
-        }
+        const int4 cur4 = nxt;
+        if (base + kSub < r1) nxt = load_labels4(labels, base + kSub + t4, r1);
+        const int l[4] = {cur4.x, cur4.y, cur4.z, cur4.w};
         uint32_t rel[4], old[4], m[4];
         bool mine[4];
 #pragma unroll
@@ -229,7 +234,7 @@ __global__ __launch_bounds__(kBuildThreads) void scatter_kernel(
 
 }  // namespace
 
-BuildPlan plan_build(int64_t N, int64_t C, int num_cus)
+BuildPlan plan_build(int64_t N, int64_t C, int num_cus, int max_blocks)
 {
     BuildPlan p;
     p.N = N;
@@ -237,6 +242,7 @@ BuildPlan plan_build(int64_t N, int64_t C, int num_cus)
     p.nslices = (int)((C + kSlice - 1) / kSlice);
     // one workgroup per CU in total: nblocks * nslices ~ num_cus
     int64_t nb = num_cus / p.nslices;
+    if (max_blocks > 0 && nb > max_blocks) nb = max_blocks;
     if (nb >= 8) nb -= nb % 8;
     if (nb < 1) nb = 1;
     int64_t R = (N + nb - 1) / nb;
@@ -253,19 +259,30 @@ size_t build_scratch_bytes(const BuildPlan &p)
     return (size_t)p.nblocks * (size_t)p.C * sizeof(uint32_t);
 }
 
-hipError_t launch_build_lists(const BuildPlan &p, const int32_t *labels, uint32_t *cntmat,
-                              int64_t *counts, int64_t *offsets, uint32_t *perm, hipStream_t s)
+hipError_t launch_build_hist(const BuildPlan &p, const int32_t *labels, uint32_t *cntmat,
+                             hipStream_t s)
 {
-    const int wgs = p.nblocks * p.nslices;
-    hipLaunchKernelGGL(hist_kernel, dim3(wgs), dim3(kBuildThreads), 0, s, labels, p.N, p.R, p.C,
-                       p.nblocks, p.nslices, cntmat);
+    hipLaunchKernelGGL(hist_kernel, dim3(p.nblocks * p.nslices), dim3(kBuildThreads), 0, s, labels,
+                       p.N, p.R, p.C, p.nblocks, p.nslices, cntmat);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_scan(const BuildPlan &p, uint32_t *cntmat, int64_t *counts, int64_t *offsets,
+                             hipStream_t s)
+{
     int g = (int)((p.C + 255) / 256);
     if (g > 4096) g = 4096;
     hipLaunchKernelGGL(colscan_kernel, dim3(g), dim3(256), 0, s, cntmat, p.C, p.nblocks, counts);
     hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(1024), 0, s, counts, p.C, offsets);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_scatter(const BuildPlan &p, const int32_t *labels, const uint32_t *cntmat,
+                                const int64_t *offsets, uint32_t *perm, hipStream_t s)
+{
     if (p.N > 0)
-        hipLaunchKernelGGL(scatter_kernel, dim3(wgs), dim3(kBuildThreads), 0, s, labels, p.N, p.R,
-                           p.C, p.nblocks, p.nslices, cntmat, offsets, perm);
+        hipLaunchKernelGGL(scatter_kernel, dim3(p.nblocks * p.nslices), dim3(kBuildThreads), 0, s,
+                           labels, p.N, p.R, p.C, p.nblocks, p.nslices, cntmat, offsets, perm);
     return hipGetLastError();
 }
 

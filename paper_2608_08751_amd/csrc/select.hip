@@ -132,17 +132,77 @@ __global__ __launch_bounds__(256) void row_norms_kernel(const float *__restrict_
     }
 }
 
+// Order-preserving map between non-NaN floats and uint32 keys.
+__device__ __forceinline__ uint32_t f2o(float f)
+{
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float o2f(uint32_t u)
+{
+    return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+
+// k-th smallest (1-based, k <= number of values) of the values spread over
+// the workgroup (thread t holds v[e] for e < nv): MSD radix select, four
+// passes of 8 bits with a 256-bin LDS histogram each; one wave locates the
+// bin that contains rank k with a prefix scan. Returns the exact value.
+template <int V>
+__device__ uint32_t block_select(const uint32_t (&v)[V], int nv, int k, uint32_t *hist,
+                                 uint32_t *sh)
+{
+    uint32_t prefix = 0, mask = 0, krem = (uint32_t)k;
+    const int lane = threadIdx.x & 63;
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            if (e < nv && (v[e] & mask) == prefix) atomicAdd(&hist[(v[e] >> shift) & 0xFFu], 1u);
+        __syncthreads();
+        if (threadIdx.x < 64) {
+            const uint32_t c0 = hist[4 * lane], c1 = hist[4 * lane + 1];
+            const uint32_t c2 = hist[4 * lane + 2], c3 = hist[4 * lane + 3];
+            const uint32_t own = c0 + c1 + c2 + c3;
+            uint32_t incl = own;
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t up = __shfl_up(incl, o);
+                if (lane >= o) incl += up;
+            }
+            const uint32_t before = incl - own;
+            if (before < krem && krem <= incl) {
+                uint32_t r = krem - before;
+                int bin = 4 * lane;
+                if (r > c0) { r -= c0; ++bin;
+                    if (r > c1) { r -= c1; ++bin;
+                        if (r > c2) { r -= c2; ++bin; } } }
+                sh[0] = (uint32_t)bin;
+                sh[1] = r;
+            }
+        }
+        __syncthreads();
+        prefix |= sh[0] << shift;
+        mask |= 0xFFu << shift;
+        krem = sh[1];
+        __syncthreads();
+    }
+    return prefix;
+}
+
 // Routing threshold from the sample keys [0, Cs) of one query: the keys are cut
 // into groups of 16 consecutive centroids, tau = the rank_j-th smallest group
 // minimum (so about rank_j sample keys lie at or below tau), and every sample
 // key <= tau is emitted as a candidate. With Cs == 0, tau = +inf.
 constexpr int kMaxGroups = 4096;
+constexpr int kGroupsPerThread = kMaxGroups / 256;
 
 __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
 {
     const int64_t q = blockIdx.x;
-    __shared__ float gm[kMaxGroups];
-    __shared__ int gid[kMaxGroups];
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sh[2];
     __shared__ uint32_t s_cnt;
     if (a.Cs == 0) {
         if (threadIdx.x == 0) {
@@ -152,30 +212,38 @@ __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
         return;
     }
     const int G = (int)(a.Cs / 16);
-    const int P = pow2_at_least(G);
     const float *kr = a.keys + q * a.Cs;
-    for (int g = threadIdx.x; g < P; g += blockDim.x) {
-        float m = kInfF;
+    uint32_t v[kGroupsPerThread];
+    int nv = 0;
+#pragma unroll
+    for (int e = 0; e < kGroupsPerThread; ++e) {
+        const int g = threadIdx.x + 256 * e;
+        v[e] = 0xFFFFFFFFu;
         if (g < G) {
             const float4 *p = reinterpret_cast<const float4 *>(kr + 16 * (int64_t)g);
+            float m = kInfF;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float4 v = p[i];
-                m = fminf(m, fminf(fminf(v.x, v.y), fminf(v.z, v.w)));
+                const float4 w = p[i];
+                m = fminf(m, fminf(fminf(w.x, w.y), fminf(w.z, w.w)));
             }
+            v[e] = f2o(m);
+            nv = e + 1;
         }
-        gm[g] = m;
-        gid[g] = g;
     }
     if (threadIdx.x == 0) s_cnt = 0;
-    __syncthreads();
-    bitonic_sort(gm, gid, P, key_lt);
-    const float th = gm[min(a.rank_j, G) - 1];
-    for (int64_t i = threadIdx.x; i < a.Cs; i += blockDim.x) {
-        const float k = kr[i];
-        if (k <= th) {
-            const uint32_t slot = atomicAdd(&s_cnt, 1u);
-            if (slot < (uint32_t)a.L) a.cand[q * a.L + slot] = make_uint2(__float_as_uint(k), (uint32_t)i);
+    const float th = o2f(block_select(v, nv, min(a.rank_j, G), hist, sh));
+    const float4 *k4 = reinterpret_cast<const float4 *>(kr);
+    for (int64_t i = threadIdx.x; i < a.Cs / 4; i += blockDim.x) {
+        const float4 w = k4[i];
+        const float kk[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (kk[e] <= th) {
+                const uint32_t slot = atomicAdd(&s_cnt, 1u);
+                if (slot < (uint32_t)a.L)
+                    a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[e]), (uint32_t)(4 * i + e));
+            }
         }
     }
     __syncthreads();
@@ -186,79 +254,81 @@ __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
 }
 
 // Certified selection of one query's top-k from its screened candidates.
-// Candidates = every centroid with key <= tau. Let kth = the k-th smallest key.
-// If tau >= kth + 2B, every centroid outside {key <= kth + 2B} is strictly
-// farther (exactly) than k candidates, so the exact top-k lies in that set;
-// its members are re-evaluated in fp64 and sorted by (distance, id).
-// Otherwise (or on overflow / underflow) the query goes to the fallback scan.
+// Candidates = every centroid with key <= tau. Let kth = the k-th smallest key
+// (radix select). If tau >= kth + 2B, every centroid outside
+// R = {key <= kth + 2B} is strictly farther (exactly) than k candidates, so the
+// exact top-k lies in R; R's members are re-evaluated in fp64 and ranked by
+// (distance, id). Otherwise (or on overflow / underflow) the query goes to
+// the fallback scan.
 constexpr int kMaxCand = 4096;
+constexpr int kCandPerThread = kMaxCand / 256;
+
+__device__ __forceinline__ void push_fallback(const RouteArgs &a, int64_t q, bool overflow)
+{
+    const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
+    a.wl[slot] = (int32_t)q;
+    atomicAdd(a.stats + kStatFallback, 1ull);
+    if (overflow) atomicAdd(a.stats + kStatOverflow, 1ull);
+}
 
 __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a)
 {
     const int64_t q = blockIdx.x;
-    __shared__ float sk[kMaxCand];
-    __shared__ int si[kMaxCand];
-    __shared__ double sd[kMaxCand];
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sh[2];
+    __shared__ int rid[kMaxCand];
+    __shared__ double rd[kMaxCand];
     __shared__ float qrow[256];
     __shared__ int s_nr;
     const uint32_t n = a.cand_cnt[q];
     if (threadIdx.x == 0) atomicAdd(a.stats + kStatCandidates, (unsigned long long)n);
     const bool overflow = n > (uint32_t)a.L;
     if (a.force_fallback || overflow || n < (uint32_t)a.k) {
-        if (threadIdx.x == 0) {
-            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
-            a.wl[slot] = (int32_t)q;
-            atomicAdd(a.stats + kStatFallback, 1ull);
-            if (overflow) atomicAdd(a.stats + kStatOverflow, 1ull);
-        }
+        if (threadIdx.x == 0) push_fallback(a, q, overflow);
         return;
     }
-    const int P = pow2_at_least((int)n);
-    for (int i = threadIdx.x; i < P; i += blockDim.x) {
+    uint32_t v[kCandPerThread];
+    int cid[kCandPerThread];
+    int nv = 0;
+#pragma unroll
+    for (int e = 0; e < kCandPerThread; ++e) {
+        const int i = threadIdx.x + 256 * e;
+        v[e] = 0xFFFFFFFFu;
+        cid[e] = 0;
         if (i < (int)n) {
             const uint2 c = a.cand[q * a.L + i];
-            sk[i] = __uint_as_float(c.x);
-            si[i] = (int)c.y;
-        } else {
-            sk[i] = kInfF;
-            si[i] = 0x7fffffff;
+            v[e] = f2o(__uint_as_float(c.x));
+            cid[e] = (int)c.y;
+            nv = e + 1;
         }
     }
     for (int d = threadIdx.x; d < a.D; d += blockDim.x) qrow[d] = a.queries[q * a.D + d];
     if (threadIdx.x == 0) s_nr = 0;
-    __syncthreads();
-    bitonic_sort(sk, si, P, key_lt);
-    const double kth = (double)sk[a.k - 1];
+    const double kth = (double)o2f(block_select(v, nv, a.k, hist, sh));
     const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, a.qn2[q]);
     if (!((double)a.tau[q] >= kth + B2)) {
-        if (threadIdx.x == 0) {
-            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
-            a.wl[slot] = (int32_t)q;
-            atomicAdd(a.stats + kStatFallback, 1ull);
-        }
+        if (threadIdx.x == 0) push_fallback(a, q, false);
         return;
     }
     const double thr = kth + B2;
-    int cnt = 0;
-    for (int i = threadIdx.x; i < (int)n; i += blockDim.x) cnt += ((double)sk[i] <= thr) ? 1 : 0;
-    atomicAdd(&s_nr, cnt);
+#pragma unroll
+    for (int e = 0; e < kCandPerThread; ++e)
+        if (e < nv && (double)o2f(v[e]) <= thr) rid[atomicAdd(&s_nr, 1)] = cid[e];
     __syncthreads();
-    const int nr = s_nr;  // a prefix of the sorted candidates, nr >= k
-    const int PR = pow2_at_least(nr);
-    // exact distances of the prefix (in place of the keys' storage order)
-    for (int i = threadIdx.x; i < PR; i += blockDim.x) {
-        if (i < nr) {
-            sd[i] = exact_dist(qrow, a.cent + (int64_t)si[i] * a.D, a.D);
-        } else {
-            sd[i] = kInfD;
-            si[i] = 0x7fffffff;
+    const int nr = s_nr;  // >= k
+    for (int i = threadIdx.x; i < nr; i += blockDim.x)
+        rd[i] = exact_dist(qrow, a.cent + (int64_t)rid[i] * a.D, a.D);
+    __syncthreads();
+    // rank of each re-evaluated candidate in (distance, id) order
+    for (int i = threadIdx.x; i < nr; i += blockDim.x) {
+        const double di = rd[i];
+        const int ii = rid[i];
+        int rank = 0;
+        for (int j = 0; j < nr; ++j) rank += dist_lt(rd[j], rid[j], di, ii) ? 1 : 0;
+        if (rank < a.k) {
+            a.out_ids[q * a.k + rank] = ii;
+            if (a.out_dist) a.out_dist[q * a.k + rank] = (float)di;
         }
-    }
-    __syncthreads();
-    bitonic_sort(sd, si, PR, dist_lt);
-    for (int i = threadIdx.x; i < a.k; i += blockDim.x) {
-        a.out_ids[q * a.k + i] = si[i];
-        if (a.out_dist) a.out_dist[q * a.k + i] = (float)sd[i];
     }
 }
 
@@ -319,50 +389,100 @@ __global__ __launch_bounds__(256) void route_fallback_kernel(RouteArgs a)
 }
 
 // Exact fp64 argmin over all centroids for rows whose top-1 could not be
-// certified. Rows come from the worklist, or, if it overflowed, from a scan of
-// the labels for the -1 marker.
-template <typename XT>
-__global__ __launch_bounds__(256) void assign_fallback_kernel(const XT *__restrict__ rows,
-                                                              int64_t N, int D,
-                                                              const float *__restrict__ cent,
-                                                              int64_t C, int32_t *labels,
-                                                              const int32_t *wl,
-                                                              const uint32_t *wl_cnt,
-                                                              int64_t wl_cap)
+// certified. Work items are 8 rows (8 worklist entries, or, if the worklist
+// overflowed, the -1 labels found in a 1024-row window). Centroids stream
+// through LDS in chunks of 128 rows (coalesced loads, row stride D+1 so that
+// lanes reading the same dimension of different centroids hit different
+// banks); thread (r, j) evaluates row r against chunk centroid j with the
+// exact operation sequence, keeps its best (distance, id), and the 128
+// threads of each row reduce in a fixed order.
+constexpr int kFbRows = 8;
+constexpr int kFbChunk = 128;
+constexpr int kFbThreads = kFbRows * kFbChunk;
+
+size_t assign_fallback_lds(int D)
 {
-    __shared__ double rd[4];
-    __shared__ int ri[4];
-    __shared__ int s_rows[256];
+    return (size_t)(kFbChunk + kFbRows) * (D + 1) * sizeof(float) + kFbThreads * sizeof(int) +
+           2 * kFbRows * (kFbChunk / 64) * sizeof(double);
+}
+
+template <typename XT>
+__global__ __launch_bounds__(kFbThreads) void assign_fallback_kernel(const XT *__restrict__ rows,
+                                                                     int64_t N, int D,
+                                                                     const float *__restrict__ cent,
+                                                                     int64_t C, int32_t *labels,
+                                                                     const int32_t *wl,
+                                                                     const uint32_t *wl_cnt,
+                                                                     int64_t wl_cap)
+{
+    extern __shared__ __attribute__((aligned(16))) unsigned char fb_lds[];
+    const int LW = D + 1;
+    float *cs = reinterpret_cast<float *>(fb_lds);          // [kFbChunk][LW]
+    float *xs = cs + kFbChunk * LW;                         // [kFbRows][LW]
+    int *found = reinterpret_cast<int *>(xs + kFbRows * LW); // [kFbThreads]
+    double *wd = reinterpret_cast<double *>(found + kFbThreads);  // [kFbRows][2]
+    int *wi = reinterpret_cast<int *>(wd + kFbRows * (kFbChunk / 64));
     __shared__ int s_n;
+
     const uint32_t total = *wl_cnt;
     const bool overflow = (int64_t)total > wl_cap;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t nitems = overflow ? (N + 255) / 256 : (int64_t)total;
-    for (int64_t w = blockIdx.x; w < nitems; w += gridDim.x) {
-        // gather the rows of this work item
+    const int r = threadIdx.x / kFbChunk;   // row slot of this thread
+    const int j = threadIdx.x % kFbChunk;   // centroid slot within a chunk
+    const int lane = threadIdx.x & 63;
+    const int64_t nwin = overflow ? (N + kFbThreads - 1) / kFbThreads : ((int64_t)total + kFbRows - 1) / kFbRows;
+
+    for (int64_t w = blockIdx.x; w < nwin; w += gridDim.x) {
+        // rows of this work window
         if (threadIdx.x == 0) s_n = 0;
         __syncthreads();
         if (overflow) {
-            const int64_t r = w * 256 + threadIdx.x;
-            if (r < N && labels[r] < 0) s_rows[atomicAdd(&s_n, 1)] = (int)r;
-        } else if (threadIdx.x == 0) {
-            s_rows[0] = wl[w];
-            s_n = 1;
+            const int64_t row = w * kFbThreads + threadIdx.x;
+            if (row < N && labels[row] < 0) found[atomicAdd(&s_n, 1)] = (int)row;
+        } else if (threadIdx.x < kFbRows) {
+            const int64_t e = w * kFbRows + threadIdx.x;
+            if (e < (int64_t)total) found[atomicAdd(&s_n, 1)] = wl[e];
         }
         __syncthreads();
-        const int nrow = s_n;
-        for (int t = 0; t < nrow; ++t) {
-            const int64_t r = s_rows[t];
-            const XT *x = rows + r * D;
+        const int nfound = s_n;
+        for (int g = 0; g < nfound; g += kFbRows) {
+            const int nr = min(kFbRows, nfound - g);
+            // stage the rows (exact as fp32: uint8 or fp32 values)
+            for (int i = threadIdx.x; i < kFbRows * D; i += blockDim.x) {
+                const int rr = i / D, d = i - rr * D;
+                xs[rr * LW + d] = rr < nr ? (float)rows[(int64_t)found[g + rr] * D + d] : 0.f;
+            }
             double bd = kInfD;
             int bi = 0x7fffffff;
-            for (int64_t c = threadIdx.x; c < C; c += blockDim.x) {
-                const double d = exact_dist(x, cent + c * D, D);
-                if (dist_lt(d, (int)c, bd, bi)) {
-                    bd = d;
-                    bi = (int)c;
+            for (int64_t base = 0; base < C; base += kFbChunk) {
+                __syncthreads();
+                const int nc = (int)min((int64_t)kFbChunk, C - base);
+                const int V4 = D / 4;
+                for (int i = threadIdx.x; i < nc * V4; i += blockDim.x) {
+                    const int cc = i / V4, d4 = i - cc * V4;
+                    const float4 v = *reinterpret_cast<const float4 *>(cent + (base + cc) * D + 4 * d4);
+                    float *dst = cs + cc * LW + 4 * d4;
+                    dst[0] = v.x;
+                    dst[1] = v.y;
+                    dst[2] = v.z;
+                    dst[3] = v.w;
+                }
+                __syncthreads();
+                if (r < nr && j < nc) {
+                    const float *xr = xs + r * LW;
+                    const float *cr = cs + j * LW;
+                    double acc = 0.0;
+                    for (int d = 0; d < D; ++d) {
+                        const double t = (double)xr[d] - (double)cr[d];
+                        acc = fma(t, t, acc);
+                    }
+                    const int id = (int)(base + j);
+                    if (dist_lt(acc, id, bd, bi)) {
+                        bd = acc;
+                        bi = id;
+                    }
                 }
             }
+            // reduce the 128 candidates of each row: two waves per row
             for (int o = 32; o > 0; o >>= 1) {
                 const double od = __shfl_xor(bd, o);
                 const int oi = __shfl_xor(bi, o);
@@ -372,17 +492,15 @@ __global__ __launch_bounds__(256) void assign_fallback_kernel(const XT *__restri
                 }
             }
             if (lane == 0) {
-                rd[wave] = bd;
-                ri[wave] = bi;
+                wd[r * 2 + j / 64] = bd;
+                wi[r * 2 + j / 64] = bi;
             }
             __syncthreads();
-            if (threadIdx.x == 0) {
-                for (int v = 1; v < 4; ++v)
-                    if (dist_lt(rd[v], ri[v], rd[0], ri[0])) {
-                        rd[0] = rd[v];
-                        ri[0] = ri[v];
-                    }
-                labels[r] = ri[0];
+            if (threadIdx.x < nr) {
+                const int rr = threadIdx.x;
+                double d0 = wd[rr * 2], d1 = wd[rr * 2 + 1];
+                int i0 = wi[rr * 2], i1 = wi[rr * 2 + 1];
+                labels[found[g + rr]] = dist_lt(d1, i1, d0, i0) ? i1 : i0;
             }
             __syncthreads();
         }
@@ -444,11 +562,12 @@ hipError_t launch_assign_fallback(const void *rows, int rowtype, int64_t N, int 
                                   const int32_t *wl, const uint32_t *wl_cnt, int64_t wl_cap,
                                   int grid, hipStream_t s)
 {
+    const size_t lds = assign_fallback_lds(D);
     if (rowtype == kRowU8)
-        hipLaunchKernelGGL(assign_fallback_kernel<uint8_t>, dim3(grid), dim3(256), 0, s,
+        hipLaunchKernelGGL(assign_fallback_kernel<uint8_t>, dim3(grid), dim3(kFbThreads), lds, s,
                            (const uint8_t *)rows, N, D, cent, C, labels, wl, wl_cnt, wl_cap);
     else
-        hipLaunchKernelGGL(assign_fallback_kernel<float>, dim3(grid), dim3(256), 0, s,
+        hipLaunchKernelGGL(assign_fallback_kernel<float>, dim3(grid), dim3(kFbThreads), lds, s,
                            (const float *)rows, N, D, cent, C, labels, wl, wl_cnt, wl_cap);
     return hipGetLastError();
 }

@@ -173,6 +173,9 @@ def _load_device():
                                        ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64,
                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         d.synth_mixture_u8.restype = ctypes.c_int
+        d.synth_labels_i32.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+        d.synth_labels_i32.restype = ctypes.c_int
         _dev = d
     return _dev
 
@@ -190,3 +193,22 @@ def device_mixture_rows_u8(means_dev, row0: int, nrows: int, out_dev, seed: int 
                             row0, nrows, out_dev.data_ptr(), ctypes.c_void_p(s.cuda_stream))
     if rc != 0:
         raise RuntimeError("synth_mixture_u8 failed (%d)" % rc)
+
+
+def device_labels(N: int, C: int, out_dev, seed: int = 0, stream=None):
+    """Fill out_dev (torch int32 [N] on the GPU) with uniform labels in [0, C):
+    label_i = SplitMix64 output (i + 1) of the label stream, mod C."""
+    import torch
+
+    d = _load_device()
+    assert out_dev.dtype == torch.int32 and out_dev.is_contiguous() and out_dev.numel() == N
+    s = stream if stream is not None else torch.cuda.current_stream()
+    rc = d.synth_labels_i32(_stream_seed(seed, _S_LABELS), C, N, out_dev.data_ptr(), ctypes.c_void_p(s.cuda_stream))
+    if rc != 0:
+        raise RuntimeError("synth_labels_i32 failed (%d)" % rc)
+
+
+def labels_host(N: int, C: int, seed: int = 0) -> np.ndarray:
+    """Host twin of device_labels (bit-identical: integer arithmetic only)."""
+    i = np.arange(N, dtype=np.uint64)
+    return (_nth(_stream_seed(seed, _S_LABELS), i + np.uint64(1)) % np.uint64(C)).astype(np.int32)

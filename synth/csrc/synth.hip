@@ -64,7 +64,25 @@ __global__ void mixture_rows_kernel(const float *__restrict__ means, int64_t C, 
     }
 }
 
+// Uniform labels in [0, C): label_i = SplitMix64 output (i + 1) mod C.
+__global__ void labels_kernel(uint64_t seed, int64_t C, int64_t n, int32_t *__restrict__ out)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        out[i] = (int32_t)(splitmix_mix(seed + (uint64_t)(i + 1) * kGamma) % (uint64_t)C);
+}
+
 } // namespace
+
+extern "C" int synth_labels_i32(uint64_t seed, int64_t C, int64_t n, int32_t *out, void *stream)
+{
+    if (C < 1 || n < 0 || (!out && n > 0)) return 1;
+    if (n == 0) return 0;
+    int64_t grid = (n + 255) / 256;
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(labels_kernel, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream, seed, C, n, out);
+    return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int synth_mixture_u8(const float *means, int64_t C, int D, uint64_t comp_seed,
                                 uint64_t noise_seed, int64_t row0, int64_t nrows, uint8_t *out,
