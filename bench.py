@@ -74,8 +74,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the sharding "
-              "design is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (queries, rows "
+              "or centroids would be sharded with one exchange each); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -169,7 +170,7 @@ def main():
         "peak": PEAK_FP32_MFMA_TFLOPS,
         "unit": "TFLOP/s",
         "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-        "traffic": None,
+        "traffic": measured_traffic(Nt),
         "kernel": "screen_kernel<128, uint8, top1>",
         "flops_per_launch": 2.0 * C * D * Nt,
         "avg_launch_ms": sum(top1) / len(top1),
@@ -235,6 +236,26 @@ def main():
             result["extra"]["build_lists_at_scale"] = bench_build(ctx, args.build_rows, C)
 
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(rows_per_launch):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (calibrated against a device
+    copy), if it was taken on the current kernel source and launch size;
+    otherwise None."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "screen_top1_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError, KeyError):
+        return None
+    if not sha.startswith(rec["source_sha256_prefix"]) or rec["rows_per_launch"] != rows_per_launch:
+        return None
+    return rec["traffic_bytes"]
 
 
 def bench_route_normalised(ctx):

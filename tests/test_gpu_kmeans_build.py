@@ -217,14 +217,17 @@ def test_assign_build_full_generator_sampled(ivf_ctx, oracle_mod, N):
     x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
     for r0 in range(0, N, chunk):
         synth.device_mixture_rows_u8(md, r0, min(chunk, N - r0), x[r0:r0 + chunk], seed=0)
+    torch.cuda.synchronize()
+    print("generated %d rows" % N, flush=True)
     lab, cnt, off, perm = ivf.ivf_assign_build(ivf_ctx, x, md)
     torch.cuda.synchronize()
-    print("assign_build stats:", ivf_ctx.last_stats())
+    print("assign_build stats:", ivf_ctx.last_stats(), flush=True)
     rng = np.random.default_rng(5)
     rows = np.sort(rng.choice(N, 256, replace=False))
     xs = x[to_dev(rows)].cpu().numpy()
     labs = lab[to_dev(rows)].cpu().numpy()
     assert (labs == oracle_mod.assign(xs, means)).all()
+    print("sampled labels match the oracle", flush=True)
     # layout invariants over the whole output
     cnth = cnt.cpu().numpy()
     offh = off.cpu().numpy()
