@@ -208,7 +208,12 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, bool need_build, bo
     l.cnorm = c.take<float>(C);
     l.wl_cap = worklist_cap(N);
     l.wl = c.take<int32_t>(l.wl_cap);
-    if (need_build) l.cntmat = c.take<uint32_t>(build_scratch_bytes(plan_build(N, C, num_cus)) / 4);
+    if (need_build) {
+        if (C <= kRadixMaxLists)
+            l.cntmat = (uint32_t *)c.take<unsigned char>(radix_scratch_bytes(plan_radix(N, C, num_cus)));
+        else
+            l.cntmat = c.take<uint32_t>(build_scratch_bytes(plan_build(N, C, num_cus)) / 4);
+    }
     if (need_lists) {
         l.counts = c.take<int64_t>(C);
         l.offsets = c.take<int64_t>(C + 1);
@@ -345,9 +350,28 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     return IVF_OK;
 }
 
-ivf_status enqueue_build(ivf_ctx *ctx, const BuildPlan &bp, const int32_t *labels, uint32_t *cntmat,
+// List build: the two-level radix partition for C <= 65,536 lists, the
+// single-pass per-block build otherwise. `scratch` is the build area of the
+// workspace.
+ivf_status enqueue_build(ivf_ctx *ctx, int64_t N, int64_t C, const int32_t *labels, void *scratch,
                          int64_t *counts, int64_t *offsets, uint32_t *perm)
 {
+    if (C <= kRadixMaxLists) {
+        const RadixPlan rp = plan_radix(N, C, ctx->num_cus);
+        const RadixScratch rs = carve_radix(rp, scratch);
+        if (N == 0) {
+            TIMED("fill", launch_fill_u32((uint32_t *)counts, 2 * C, 0u, ctx->stream));
+            TIMED("build_offsets", launch_offsets(counts, C, offsets, ctx->stream));
+            return IVF_OK;
+        }
+        TIMED("build_level0", launch_radix_level0(rp, labels, rs, ctx->stream));
+        TIMED("build_level1_counts", launch_radix_level1_counts(rp, rs, counts, ctx->stream));
+        TIMED("build_offsets", launch_offsets(counts, C, offsets, ctx->stream));
+        TIMED("build_level1_scatter", launch_radix_level1_scatter(rp, rs, offsets, perm, ctx->stream));
+        return IVF_OK;
+    }
+    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
+    uint32_t *cntmat = (uint32_t *)scratch;
     TIMED("build_hist", launch_build_hist(bp, labels, cntmat, ctx->stream));
     TIMED("build_scan", launch_build_scan(bp, cntmat, counts, offsets, ctx->stream));
     TIMED("build_scatter", launch_build_scatter(bp, labels, cntmat, offsets, perm, ctx->stream));
@@ -640,9 +664,8 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
     const AssignLayout l = layout_assign(ctx->ws, N, C, true, true, ctx->num_cus);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
     int64_t *counts = out_counts ? out_counts : l.counts;
-    if ((st = enqueue_build(ctx, bp, out_labels, l.cntmat, counts, l.offsets, l.perm)) != IVF_OK) return st;
+    if ((st = enqueue_build(ctx, N, C, out_labels, l.cntmat, counts, l.offsets, l.perm)) != IVF_OK) return st;
     TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, centroids, C, counts, l.offsets, l.perm, seed,
                                  iter, out_centroids, l.jpart, out_objective, ctx->stream));
     return IVF_OK;
@@ -682,8 +705,8 @@ ivf_status ivf_assign_build(ivf_ctx *ctx, const void *base, int dt, int64_t N,
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if (N > 0 && (st = enqueue_assign(ctx, base, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK)
         return st;
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
-    if ((st = enqueue_build(ctx, bp, out_labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
+    if ((st = enqueue_build(ctx, N, C, out_labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK)
+        return st;
     return IVF_OK;
 }
 
@@ -715,8 +738,7 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
     const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
-    const BuildPlan bp = plan_build(N, C, ctx->num_cus, ctx->build_blocks);
-    if ((st = enqueue_build(ctx, bp, labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
+    if ((st = enqueue_build(ctx, N, C, labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

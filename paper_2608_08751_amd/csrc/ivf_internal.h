@@ -122,6 +122,31 @@ hipError_t launch_build_scan(const BuildPlan &p, uint32_t *cntmat, int64_t *coun
 hipError_t launch_build_scatter(const BuildPlan &p, const int32_t *labels, const uint32_t *cntmat,
                                 const int64_t *offsets, uint32_t *perm, hipStream_t s);
 
+// ---- inverted-list build for C <= 65,536 (lists_radix.hip) -----------------
+constexpr int64_t kRadixMaxLists = 65536;
+
+struct RadixPlan {
+    int64_t N, C;
+    int64_t R0;      // rows per level-0 block (multiple of the 4,096-row tile)
+    int nblocks0;
+    int64_t R1;      // rows per level-1 sub-block
+    int max_sub1;    // upper bound on the number of level-1 sub-blocks
+};
+struct RadixScratch {
+    uint32_t *cnt0, *tot0, *astart, *sbstart, *cnt1, *tmp_ids;
+    uint8_t *tmp_lo;
+};
+RadixPlan plan_radix(int64_t N, int64_t C, int num_cus);
+size_t radix_scratch_bytes(const RadixPlan &p);
+RadixScratch carve_radix(const RadixPlan &p, void *base);
+hipError_t launch_radix_level0(const RadixPlan &p, const int32_t *labels, const RadixScratch &s,
+                               hipStream_t st);
+hipError_t launch_radix_level1_counts(const RadixPlan &p, const RadixScratch &s, int64_t *counts,
+                                      hipStream_t st);
+hipError_t launch_radix_level1_scatter(const RadixPlan &p, const RadixScratch &s, const int64_t *offsets,
+                                       uint32_t *perm, hipStream_t st);
+hipError_t launch_offsets(const int64_t *counts, int64_t C, int64_t *offsets, hipStream_t st);
+
 // ---- k-means update (kmeans.hip) --------------------------------------------
 hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
                                 const float *cent_in, int64_t C, const int64_t *counts,

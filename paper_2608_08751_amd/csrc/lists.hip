@@ -277,6 +277,12 @@ hipError_t launch_build_scan(const BuildPlan &p, uint32_t *cntmat, int64_t *coun
     return hipGetLastError();
 }
 
+hipError_t launch_offsets(const int64_t *counts, int64_t C, int64_t *offsets, hipStream_t st)
+{
+    hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(1024), 0, st, counts, C, offsets);
+    return hipGetLastError();
+}
+
 hipError_t launch_build_scatter(const BuildPlan &p, const int32_t *labels, const uint32_t *cntmat,
                                 const int64_t *offsets, uint32_t *perm, hipStream_t s)
 {

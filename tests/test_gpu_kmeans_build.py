@@ -118,6 +118,7 @@ def gpu_lists(ctx, labels, C):
 @pytest.mark.parametrize("N,C,skew", [
     (0, 5, 0.0), (1, 1, 0.0), (1000, 1, 0.0), (12345, 300, 0.0), (100003, 20000, 0.0),
     (2000001, 65536, 0.0), (1000000, 40000, 1.1), (300000, 3, 0.0), (4099, 70000, 0.0),
+    (20000003, 65536, 0.0), (9000000, 65536, 1.05),
 ])
 def test_build_lists_exact(ivf_ctx, oracle_mod, N, C, skew):
     lab = synth.random_labels(N, C, seed=N + C, skew=skew)
@@ -125,6 +126,14 @@ def test_build_lists_exact(ivf_ctx, oracle_mod, N, C, skew):
     ocnt, ooff, operm = oracle_mod.build_lists(lab, C)
     assert (cnt == ocnt).all() and (off == ooff).all()
     assert (perm == operm).all()
+
+
+def test_build_lists_deterministic(ivf_ctx):
+    """Several tiles per block and per sub-block: two runs are bit-identical."""
+    lab = synth.random_labels(12_000_000, 65536, seed=3)
+    a = gpu_lists(ivf_ctx, lab, 65536)
+    b = gpu_lists(ivf_ctx, lab, 65536)
+    assert all((x == y).all() for x, y in zip(a, b))
 
 
 def test_build_lists_single_list_all_rows(ivf_ctx, oracle_mod):
