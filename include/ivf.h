@@ -171,13 +171,16 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *                           changes speed only, never results or sizes
  *   IVF_OPT_PROFILE         1 = record a HIP event pair on the context stream
  *                           around every kernel launch of each call
- *   IVF_OPT_BUILD_BLOCKS    cap on the row blocks of the list build (0 =
- *                           default); changes speed only, never results */
+ *   IVF_OPT_BUILD_BLOCKS    cap on the row blocks of the single-pass list build
+ *                           (more than 65,536 lists; 0 = default); speed only
+ *   IVF_OPT_SCREEN_WAVES    wave64s per workgroup of the distance-screening
+ *                           kernel, 4 or 8; speed only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,
     IVF_OPT_PROFILE = 2,
-    IVF_OPT_BUILD_BLOCKS = 3
+    IVF_OPT_BUILD_BLOCKS = 3,
+    IVF_OPT_SCREEN_WAVES = 4
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

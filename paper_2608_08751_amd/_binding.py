@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libivf.so")
 IVF_OK, IVF_EINVAL, IVF_EUNSUPPORTED, IVF_ENOMEM, IVF_EDEVICE = range(5)
 IVF_F32, IVF_U8 = 0, 1
 IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS = range(4)
-IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE, IVF_OPT_BUILD_BLOCKS = range(4)
+IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE, IVF_OPT_BUILD_BLOCKS, IVF_OPT_SCREEN_WAVES = range(5)
 
 STATUS_NAMES = {0: "IVF_OK", 1: "IVF_EINVAL", 2: "IVF_EUNSUPPORTED", 3: "IVF_ENOMEM", 4: "IVF_EDEVICE"}
 

@@ -28,6 +28,7 @@ struct ivf_ctx {
     int force_fallback = 0;
     int sample_rank = 0;
     int build_blocks = 0;
+    int screen_waves = 8;
     unsigned long long *last_stats = nullptr;  // device, inside the workspace
     int64_t last_sample = 0;
     // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
@@ -331,8 +332,6 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     a.c_begin = 0;
     a.c_end = C;
     a.nchunks = (C + kChunk - 1) / kChunk;
-    a.ntiles = (N + kTileRows - 1) / kTileRows;
-    a.units = a.ntiles * a.nchunks;
     a.mc2_bits = l.sc.mc2_bits;
     a.bound_coef = bound_coef(DP);
     a.labels = labels;
@@ -341,8 +340,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     a.wl_cap = l.wl_cap;
     a.stats = l.sc.stats;
     a.force_fallback = ctx->force_fallback;
-    const int grid = (int)std::min<int64_t>(a.ntiles, (int64_t)ctx->num_cus);
-    TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, grid, s));
+    TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));
     TIMED("assign_fallback", launch_assign_fallback(rows, rowtype, N, D, cent, C, labels, l.wl, l.sc.wl_cnt, l.wl_cap,
                                    2 * ctx->num_cus, s));
     ctx->last_stats = l.sc.stats;
@@ -472,6 +470,10 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
         ctx->sample_rank = (int)value;
         return IVF_OK;
     case IVF_OPT_PROFILE: ctx->profile = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_SCREEN_WAVES:
+        if (value != 4 && value != 8) return fail(ctx, IVF_EINVAL, "screen waves must be 4 or 8");
+        ctx->screen_waves = (int)value;
+        return IVF_OK;
     case IVF_OPT_BUILD_BLOCKS:
         if (value < 0 || value > 65536) return fail(ctx, IVF_EINVAL, "build blocks out of range");
         ctx->build_blocks = (int)value;
@@ -563,15 +565,12 @@ ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float 
         a.D = D;
         a.cent = centroids;
         a.cnorm = l.cnorm;
-        a.ntiles = (nb + kTileRows - 1) / kTileRows;
         if (p.Cs > 0) {
             a.c_begin = 0;
             a.c_end = p.Cs;
             a.nchunks = p.Cs / kChunk;
-            a.units = a.ntiles * a.nchunks;
             a.keys = l.keys;
-            TIMED("screen_keys", launch_screen(kModeKeys, kRowF32, DP, a,
-                                  (int)std::min<int64_t>(a.units, ctx->num_cus), s));
+            TIMED("screen_keys", launch_screen(kModeKeys, kRowF32, DP, a, ctx->screen_waves, ctx->num_cus, s));
         }
         RouteArgs r{};
         r.queries = qrows;
@@ -601,14 +600,12 @@ ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float 
             a.c_begin = p.Cs;
             a.c_end = C;
             a.nchunks = (C - p.Cs + kChunk - 1) / kChunk;
-            a.units = a.ntiles * a.nchunks;
             a.keys = nullptr;
             a.tau = l.tau;
             a.cand_cnt = l.cand_cnt;
             a.cand = l.cand;
             a.L = p.L;
-            TIMED("screen_filter", launch_screen(kModeFilter, kRowF32, DP, a,
-                                  (int)std::min<int64_t>(a.units, ctx->num_cus), s));
+            TIMED("screen_filter", launch_screen(kModeFilter, kRowF32, DP, a, ctx->screen_waves, ctx->num_cus, s));
         }
         TIMED("route_select", launch_route_select(r, s));
         TIMED("route_fallback", launch_route_fallback(r, 2 * ctx->num_cus, s));

@@ -8,13 +8,11 @@
 namespace ivf {
 
 // ---- screening kernel geometry -------------------------------------------
-// One workgroup = kScreenWaves wave64s. Each wave owns 32 rows (queries or
-// data vectors) whose fp32 values live in registers as MFMA B fragments; all
-// waves share a chunk of kChunk centroids staged in LDS (double-buffered).
+// One workgroup = W wave64s (4 or 8). Each wave owns 32 rows (queries or data
+// vectors) whose fp32 values live in registers as MFMA B fragments; all waves
+// share a chunk of kChunk centroids staged in LDS (double-buffered). 8/W
+// workgroups run per CU (two waves per SIMD).
 constexpr int kChunk = 64;
-constexpr int kScreenWaves = 8;
-constexpr int kScreenThreads = kScreenWaves * 64;
-constexpr int kTileRows = kScreenWaves * 32;
 
 enum ScreenMode { kModeKeys = 0, kModeFilter = 1, kModeTop1 = 2 };
 enum RowType { kRowF32 = 0, kRowU8 = 1 };
@@ -38,8 +36,6 @@ struct ScreenArgs {
     int64_t c_begin;        // first centroid of the range (multiple of kChunk)
     int64_t c_end;          // one past the last centroid of the range
     int64_t nchunks;        // ceil((c_end - c_begin) / kChunk)
-    int64_t ntiles;         // ceil(nrows / kTileRows)
-    int64_t units;          // ntiles * nchunks (keys / filter modes)
     // keys mode
     float *keys;            // [nrows, c_end - c_begin]
     // filter mode
@@ -58,7 +54,8 @@ struct ScreenArgs {
     int force_fallback;
 };
 
-hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int grid,
+// waves: 4 or 8 per workgroup; the grid fills every CU with two waves per SIMD.
+hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int waves, int num_cus,
                          hipStream_t s);
 
 // ---- norms, selection, fallbacks (select.hip) -----------------------------

@@ -22,6 +22,8 @@
 
 #include <math.h>
 
+#include <algorithm>
+
 namespace ivf {
 namespace {
 
@@ -88,22 +90,22 @@ __device__ __forceinline__ void load_row(const uint8_t *__restrict__ X, int64_t 
 }
 
 // Per-thread registers holding one chunk on its way from HBM/L2 to LDS.
-template <int DP>
+template <int DP, int NT>
 struct ChunkRegs {
-    static constexpr int kVec = kChunk * DP / 4 / kScreenThreads;  // float4 per thread
+    static constexpr int kVec = kChunk * DP / 4 / NT;  // float4 per thread
     float4 v[kVec];
     float n;
 };
 
-template <int DP>
+template <int DP, int NT>
 __device__ __forceinline__ void chunk_fetch(const float *__restrict__ cent,
                                             const float *__restrict__ cnorm, int64_t cbase,
-                                            int64_t c_end, int D, ChunkRegs<DP> &r)
+                                            int64_t c_end, int D, ChunkRegs<DP, NT> &r)
 {
     constexpr int V4 = DP / 4;
 #pragma unroll
-    for (int i = 0; i < ChunkRegs<DP>::kVec; ++i) {
-        const int idx = threadIdx.x + i * kScreenThreads;
+    for (int i = 0; i < ChunkRegs<DP, NT>::kVec; ++i) {
+        const int idx = threadIdx.x + i * NT;
         const int rr = idx / V4, c4 = idx - rr * V4;
         const int64_t row = cbase + rr;
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -118,15 +120,15 @@ __device__ __forceinline__ void chunk_fetch(const float *__restrict__ cent,
     }
 }
 
-template <int DP>
+template <int DP, int NT>
 __device__ __forceinline__ void chunk_store(float *__restrict__ lc, float *__restrict__ ln,
-                                            const ChunkRegs<DP> &r)
+                                            const ChunkRegs<DP, NT> &r)
 {
     constexpr int V4 = DP / 4;
     constexpr int LW = DP + 4;
 #pragma unroll
-    for (int i = 0; i < ChunkRegs<DP>::kVec; ++i) {
-        const int idx = threadIdx.x + i * kScreenThreads;
+    for (int i = 0; i < ChunkRegs<DP, NT>::kVec; ++i) {
+        const int idx = threadIdx.x + i * NT;
         const int rr = idx / V4, c4 = idx - rr * V4;
         *reinterpret_cast<float4 *>(lc + rr * LW + 4 * c4) = r.v[i];
     }
@@ -195,33 +197,36 @@ __device__ __forceinline__ double key_bound(double coef, uint32_t mc2_bits, doub
 // its row's candidate list with one global atomic and stores (key, id).
 constexpr int kStage = 128;
 
+template <int W>
 struct Stage {
-    uint2 kc[kScreenWaves][kStage];            // (key bits, centroid id)
-    unsigned char row[kScreenWaves][kStage];   // row within the tile
+    uint2 kc[W][kStage];            // (key bits, centroid id)
+    unsigned char row[W][kStage];   // row within the tile
 };
 
-__device__ __forceinline__ void stage_flush(const ScreenArgs &a, Stage &st, int wave, int lane,
+template <int W>
+__device__ __forceinline__ void stage_flush(const ScreenArgs &a, Stage<W> &st, int wave, int lane,
                                             int64_t tile, int n)
 {
     if (lane < n) {
         const uint2 e = st.kc[wave][lane];
-        const int64_t row = tile * kTileRows + st.row[wave][lane];
+        const int64_t row = tile * (32 * W) + st.row[wave][lane];
         const uint32_t slot = atomicAdd(a.cand_cnt + row, 1u);
         if (slot < (uint32_t)a.L) a.cand[row * a.L + slot] = e;
     }
 }
 
-template <int DP, typename XT, int MODE>
+template <int DP, int W, typename XT, int MODE>
 __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
-                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage &stg)
+                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
 {
+    constexpr int NT = W * 64;
     constexpr int KH = DP / 2;
     constexpr int LW = DP + 4;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int h = lane >> 5;
     const int jl = lane & 31;
-    const int64_t row = tile * kTileRows + wave * 32 + jl;
+    const int64_t row = tile * (32 * W) + wave * 32 + jl;
     const bool rvalid = row < a.nrows;
 
     float b[KH];
@@ -239,16 +244,16 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     Top3 st{kInf, kInf, kInf, -1, -1};
     int staged = 0;  // wave-uniform count of staged survivors
 
-    ChunkRegs<DP> cr;
-    chunk_fetch<DP>(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D, cr);
-    chunk_store<DP>(lds_c, lds_n, cr);
+    ChunkRegs<DP, NT> cr;
+    chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D, cr);
+    chunk_store<DP, NT>(lds_c, lds_n, cr);
     __syncthreads();
 
     for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
         const int buf = (int)((ch - ch_lo) & 1);
         const bool more = ch + 1 < ch_hi;
         const int64_t cbase = a.c_begin + ch * kChunk;
-        if (more) chunk_fetch<DP>(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D, cr);
+        if (more) chunk_fetch<DP, NT>(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D, cr);
 
         const float *A0 = lds_c + buf * (kChunk * LW) + jl * LW + h * KH;
         const float *A1 = A0 + 32 * LW;
@@ -347,7 +352,7 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
             }
         }
 
-        if (more) chunk_store<DP>(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk, cr);
+        if (more) chunk_store<DP, NT>(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk, cr);
         __syncthreads();
     }
 
@@ -386,64 +391,77 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     }
 }
 
-template <int DP, typename XT, int MODE>
-__global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a)
+template <int DP, int W, typename XT, int MODE>
+__global__ __launch_bounds__(W * 64, 2) void screen_kernel(ScreenArgs a)
 {
     __shared__ __attribute__((aligned(16))) float lds_c[2 * kChunk * (DP + 4)];
     __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
-    __shared__ Stage stg;
+    __shared__ Stage<W> stg;
+    const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
     if (MODE == kModeTop1) {
-        for (int64_t tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
-            screen_range<DP, XT, MODE>(a, tile, 0, a.nchunks, lds_c, lds_n, stg);
+        for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+            screen_range<DP, W, XT, MODE>(a, tile, 0, a.nchunks, lds_c, lds_n, stg);
             __syncthreads();
         }
     } else {
         // a contiguous range of (tile, chunk) units in tile-major order
-        int64_t u = a.units * blockIdx.x / gridDim.x;
-        const int64_t u1 = a.units * (blockIdx.x + 1) / gridDim.x;
+        const int64_t units = ntiles * a.nchunks;
+        int64_t u = units * blockIdx.x / gridDim.x;
+        const int64_t u1 = units * (blockIdx.x + 1) / gridDim.x;
         while (u < u1) {
             const int64_t tile = u / a.nchunks;
             const int64_t ch = u - tile * a.nchunks;
             const int64_t ch_end = min(a.nchunks, ch + (u1 - u));
-            screen_range<DP, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
+            screen_range<DP, W, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
             u += ch_end - ch;
             __syncthreads();
         }
     }
 }
 
-template <int DP, typename XT, int MODE>
-hipError_t launch_one(const ScreenArgs &a, int grid, hipStream_t s)
+template <int DP, int W, typename XT, int MODE>
+hipError_t launch_one(const ScreenArgs &a, int num_cus, hipStream_t s)
 {
-    hipLaunchKernelGGL((screen_kernel<DP, XT, MODE>), dim3(grid), dim3(kScreenThreads), 0, s, a);
+    const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
+    const int64_t work = MODE == kModeTop1 ? ntiles : ntiles * a.nchunks;
+    const int per_cu = 8 / W;  // two waves per SIMD
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(work, (int64_t)per_cu * num_cus));
+    hipLaunchKernelGGL((screen_kernel<DP, W, XT, MODE>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
 }
 
-template <int DP>
-hipError_t launch_dp(int mode, int rowtype, const ScreenArgs &a, int grid, hipStream_t s)
+template <int DP, int W>
+hipError_t launch_dp(int mode, int rowtype, const ScreenArgs &a, int num_cus, hipStream_t s)
 {
     if (mode == kModeTop1)
-        return rowtype == kRowU8 ? launch_one<DP, uint8_t, kModeTop1>(a, grid, s)
-                                 : launch_one<DP, float, kModeTop1>(a, grid, s);
+        return rowtype == kRowU8 ? launch_one<DP, W, uint8_t, kModeTop1>(a, num_cus, s)
+                                 : launch_one<DP, W, float, kModeTop1>(a, num_cus, s);
     if (rowtype != kRowF32) return hipErrorInvalidValue;
-    if (mode == kModeKeys) return launch_one<DP, float, kModeKeys>(a, grid, s);
-    return launch_one<DP, float, kModeFilter>(a, grid, s);
+    if (mode == kModeKeys) return launch_one<DP, W, float, kModeKeys>(a, num_cus, s);
+    return launch_one<DP, W, float, kModeFilter>(a, num_cus, s);
+}
+
+template <int W>
+hipError_t launch_w(int mode, int rowtype, int DP, const ScreenArgs &a, int num_cus, hipStream_t s)
+{
+    switch (DP) {
+    case 32: return launch_dp<32, W>(mode, rowtype, a, num_cus, s);
+    case 64: return launch_dp<64, W>(mode, rowtype, a, num_cus, s);
+    case 96: return launch_dp<96, W>(mode, rowtype, a, num_cus, s);
+    case 128: return launch_dp<128, W>(mode, rowtype, a, num_cus, s);
+    case 192: return launch_dp<192, W>(mode, rowtype, a, num_cus, s);
+    case 256: return launch_dp<256, W>(mode, rowtype, a, num_cus, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
 
-hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int grid,
+hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int waves, int num_cus,
                          hipStream_t s)
 {
-    switch (DP) {
-    case 32: return launch_dp<32>(mode, rowtype, a, grid, s);
-    case 64: return launch_dp<64>(mode, rowtype, a, grid, s);
-    case 96: return launch_dp<96>(mode, rowtype, a, grid, s);
-    case 128: return launch_dp<128>(mode, rowtype, a, grid, s);
-    case 192: return launch_dp<192>(mode, rowtype, a, grid, s);
-    case 256: return launch_dp<256>(mode, rowtype, a, grid, s);
-    default: return hipErrorInvalidValue;
-    }
+    return waves == 4 ? launch_w<4>(mode, rowtype, DP, a, num_cus, s)
+                      : launch_w<8>(mode, rowtype, DP, a, num_cus, s);
 }
 
 }  // namespace ivf
