@@ -120,7 +120,8 @@ __device__ __forceinline__ void chunk_fetch(const float *__restrict__ cent,
     }
 }
 
-template <int DP, int NT>
+// NEG_HALF stages -||c||^2/2 instead of ||c||^2 (exact: a power-of-two scaling).
+template <int DP, int NT, bool NEG_HALF = false>
 __device__ __forceinline__ void chunk_store(float *__restrict__ lc, float *__restrict__ ln,
                                             const ChunkRegs<DP, NT> &r)
 {
@@ -132,7 +133,7 @@ __device__ __forceinline__ void chunk_store(float *__restrict__ lc, float *__res
         const int rr = idx / V4, c4 = idx - rr * V4;
         *reinterpret_cast<float4 *>(lc + rr * LW + 4 * c4) = r.v[i];
     }
-    if (threadIdx.x < kChunk) ln[threadIdx.x] = r.n;
+    if (threadIdx.x < kChunk) ln[threadIdx.x] = NEG_HALF ? -0.5f * r.n : r.n;
 }
 
 // Per-row state of the top-1 epilogue: the three smallest keys, ids of two.
@@ -140,24 +141,6 @@ struct Top3 {
     float k1, k2, k3;
     int i1, i2;
 };
-
-__device__ __forceinline__ void top3_insert(Top3 &t, float key, int id)
-{
-    if (key < t.k2) {
-        t.k3 = t.k2;
-        if (key < t.k1) {
-            t.k2 = t.k1;
-            t.i2 = t.i1;
-            t.k1 = key;
-            t.i1 = id;
-        } else {
-            t.k2 = key;
-            t.i2 = id;
-        }
-    } else {
-        t.k3 = key;
-    }
-}
 
 // Merges this lane's list with the partner lane's (both sorted by (key, id)).
 __device__ __forceinline__ Top3 top3_merge(Top3 a, Top3 b)
@@ -232,16 +215,8 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     float b[KH];
     load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
 
-    // this lane's half of ||x||^2 (exact fp32 values, fp64 sum); only the
-    // top-1 bound needs it, the routing bound uses separately computed norms
-    double xpart = 0.0;
-    if (MODE == kModeTop1) {
-#pragma unroll
-        for (int s = 0; s < KH; ++s) xpart = fma((double)b[s], (double)b[s], xpart);
-    }
     float tau = -kInf;
     if (MODE == kModeFilter && rvalid) tau = a.tau[row];
-    Top3 st{kInf, kInf, kInf, -1, -1};
     int staged = 0;  // wave-uniform count of staged survivors
 
     ChunkRegs<DP, NT> cr;
@@ -315,7 +290,7 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
                             make_float4(key[16 * rb + 4 * g + 0], key[16 * rb + 4 * g + 1],
                                         key[16 * rb + 4 * g + 2], key[16 * rb + 4 * g + 3]);
             }
-        } else if (MODE == kModeFilter) {
+        } else {  // kModeFilter
 #pragma unroll
             for (int r = 0; r < 32; ++r) {
                 const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
@@ -339,17 +314,6 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
                     }
                 }
             }
-        } else {  // kModeTop1: ids visited in ascending order within a lane
-#pragma unroll
-            for (int r = 0; r < 32; ++r) {
-                const bool ins = key[r] < st.k3;
-                if (__ballot(ins) != 0) {
-                    if (ins) {
-                        const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
-                        top3_insert(st, key[r], cid);
-                    }
-                }
-            }
         }
 
         if (more) chunk_store<DP, NT>(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk, cr);
@@ -357,38 +321,249 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     }
 
     if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
+}
 
-    if (MODE == kModeTop1) {
-        const double xn2 = xpart + __shfl_xor(xpart, 32);
-        Top3 o;
-        o.k1 = __shfl_xor(st.k1, 32);
-        o.k2 = __shfl_xor(st.k2, 32);
-        o.k3 = __shfl_xor(st.k3, 32);
-        o.i1 = __shfl_xor(st.i1, 32);
-        o.i2 = __shfl_xor(st.i2, 32);
-        const Top3 m = top3_merge(st, o);
-        if (rvalid && h == 0) {
-            const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, xn2);
-            int label = -1;
-            if (!a.force_fallback) {
-                if ((double)m.k2 > (double)m.k1 + B2) {
-                    label = m.i1;
-                } else if ((double)m.k3 > (double)m.k1 + B2) {
-                    const XT *x = reinterpret_cast<const XT *>(a.rows) + row * (int64_t)a.D;
-                    const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
-                    const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
-                    label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
-                    atomicAdd(a.stats + kStatRefine2, 1ull);
-                }
-            }
-            if (label < 0) {
-                const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
-                if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
-                atomicAdd(a.stats + kStatFallback, 1ull);
-            }
-            a.labels[row] = label;
-        }
+// ---------------------------------------------------------------- top-1 path
+//
+// The accumulators start from -fl32(||c||^2)/2 (staged in LDS instead of the
+// norms), so after the MFMAs an accumulator holds v = -key/2 exactly (scaling
+// by a power of two is exact) and the key never needs to be formed: the three
+// smallest keys are the three largest v. The epilogue of chunk j-1 (the
+// branch-free three-largest update) is interleaved with the MFMAs of chunk j,
+// so the matrix pipe keeps running while a wave consumes the previous
+// accumulators. Centroid data stays double-buffered; the norms take three
+// LDS slots because the first MFMAs of chunk j+1 read its norms while a slower
+// wave may still be loading chunk j's.
+
+// Inserts (v, id) into a lane's three largest values without branches (a
+// value <= v3 leaves the state unchanged): with v1 >= v2 >= v3,
+// med3(v, v2, v3) is the new third value and med3(v, v1, v2) the new second.
+// Strict comparisons keep the lower id on equal values because a lane visits
+// ids in ascending order.
+__device__ __forceinline__ void top3_push(Top3 &t, float v, int id)
+{
+    const bool gt1 = v > t.k1;
+    const bool gt2 = v > t.k2;
+    t.k3 = __builtin_amdgcn_fmed3f(v, t.k2, t.k3);
+    t.k2 = __builtin_amdgcn_fmed3f(v, t.k1, t.k2);
+    t.k1 = gt1 ? v : t.k1;
+    const int j2 = gt2 ? id : t.i2;
+    t.i2 = gt1 ? t.i1 : j2;
+    t.i1 = gt1 ? id : t.i1;
+}
+
+// max(a, b, c, d) in two instructions (fmaxf would first canonicalise each
+// operand for NaN handling; the values here are never NaN).
+__device__ __forceinline__ float max4(float a, float b, float c, float d)
+{
+    float m;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
+    asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(m), "v"(d));
+    return m;
+}
+
+// Group G (0..7) of the previous chunk's accumulators: block rb = G / 4 (p0
+// or p1), registers 4g..4g+3 with g = G % 4, centroids rb*32 + 8g + 4h + e.
+// Fp32 MFMA and other vector instructions share the SIMD, so every vector
+// instruction here costs matrix throughput: the group is first tested as a
+// whole (two instructions), and the insertion runs only when some lane of the
+// wave holds a value above its third largest.
+template <int G>
+__device__ __forceinline__ void top1_group(const f32x16 &p0, const f32x16 &p1, int idp, Top3 &st)
+{
+    constexpr int rb = G >> 2;
+    constexpr int g = G & 3;
+    constexpr int off = rb * 32 + 8 * g;  // centroid offset (h excluded)
+    const f32x16 &p = rb ? p1 : p0;
+    const float m = max4(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
+    if (__any(m > st.k3)) {
+        top3_push(st, p[4 * g + 0], idp + off + 0);
+        top3_push(st, p[4 * g + 1], idp + off + 1);
+        top3_push(st, p[4 * g + 2], idp + off + 2);
+        top3_push(st, p[4 * g + 3], idp + off + 3);
     }
+    // keeps the test at this point of the MFMA stream (the compiler would
+    // otherwise sink the whole epilogue below the chunk's last MFMA)
+    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2));
+}
+
+template <int G, int T, int KB>
+__device__ __forceinline__ void top1_groups_at(const f32x16 &p0, const f32x16 &p1, int idp, Top3 &st)
+{
+    if constexpr (G < 8) {
+        if constexpr (G * KB / 8 == T) top1_group<G>(p0, p1, idp, st);
+        top1_groups_at<G + 1, T, KB>(p0, p1, idp, st);
+    }
+}
+
+// MFMAs of one staged chunk into (c0, c1); with EP, the epilogue of the
+// previous chunk (p0, p1, first id idp) spread over the K-blocks.
+template <int DP, bool EP, int T = 0>
+__device__ __forceinline__ void top1_kblocks(const float *A0, const float *A1, const float (&b)[DP / 2],
+                                             f32x16 &c0, f32x16 &c1, float4 a0, float4 a1,
+                                             const f32x16 &p0, const f32x16 &p1, int idp, Top3 &st)
+{
+    constexpr int KB = DP / 8;
+    if constexpr (T < KB) {
+        float4 n0 = a0, n1 = a1;
+        if constexpr (T + 1 < KB) {
+            n0 = *reinterpret_cast<const float4 *>(A0 + 4 * (T + 1));
+            n1 = *reinterpret_cast<const float4 *>(A1 + 4 * (T + 1));
+        }
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.x, b[4 * T + 0], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.x, b[4 * T + 0], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.y, b[4 * T + 1], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.y, b[4 * T + 1], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.z, b[4 * T + 2], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.z, b[4 * T + 2], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.w, b[4 * T + 3], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.w, b[4 * T + 3], c1, 0, 0, 0);
+        if constexpr (EP) top1_groups_at<0, T, KB>(p0, p1, idp, st);
+        __builtin_amdgcn_sched_barrier(0);
+        top1_kblocks<DP, EP, T + 1>(A0, A1, b, c0, c1, n0, n1, p0, p1, idp, st);
+    }
+}
+
+// One chunk: A0 = this lane's row of the staged centroids, Nh = the staged
+// -||c||^2/2 values of the chunk offset by 4h.
+template <int DP, bool EP>
+__device__ __forceinline__ void top1_chunk(const float *A0, const float *Nh, const float (&b)[DP / 2],
+                                           f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1,
+                                           int idp, Top3 &st)
+{
+    const float *A1 = A0 + 32 * (DP + 4);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float4 u = *reinterpret_cast<const float4 *>(Nh + 8 * g);
+        const float4 w = *reinterpret_cast<const float4 *>(Nh + 32 + 8 * g);
+        c0[4 * g + 0] = u.x;
+        c0[4 * g + 1] = u.y;
+        c0[4 * g + 2] = u.z;
+        c0[4 * g + 3] = u.w;
+        c1[4 * g + 0] = w.x;
+        c1[4 * g + 1] = w.y;
+        c1[4 * g + 2] = w.z;
+        c1[4 * g + 3] = w.w;
+    }
+    const float4 a0 = *reinterpret_cast<const float4 *>(A0);
+    const float4 a1 = *reinterpret_cast<const float4 *>(A1);
+    top1_kblocks<DP, EP>(A0, A1, b, c0, c1, a0, a1, p0, p1, idp, st);
+}
+
+template <int G = 0>
+__device__ __forceinline__ void top1_drain(const f32x16 &p0, const f32x16 &p1, int idp, Top3 &st)
+{
+    if constexpr (G < 8) {
+        top1_group<G>(p0, p1, idp, st);
+        top1_drain<G + 1>(p0, p1, idp, st);
+    }
+}
+
+// Merges the two half-lanes of each row, certifies the nearest centroid with
+// the rounding-error bound, settles two-way near-ties exactly in fp64 and
+// queues everything else for the full fp64 fallback.
+template <typename XT>
+__device__ __forceinline__ void top1_finish(const ScreenArgs &a, int64_t row, bool rvalid, int h,
+                                            double xpart, const Top3 &st)
+{
+    const double xn2 = xpart + __shfl_xor(xpart, 32);
+    Top3 o;
+    o.k1 = __shfl_xor(st.k1, 32);
+    o.k2 = __shfl_xor(st.k2, 32);
+    o.k3 = __shfl_xor(st.k3, 32);
+    o.i1 = __shfl_xor(st.i1, 32);
+    o.i2 = __shfl_xor(st.i2, 32);
+    const Top3 m = top3_merge(st, o);
+    if (rvalid && h == 0) {
+        const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, xn2);
+        int label = -1;
+        if (!a.force_fallback) {
+            if ((double)m.k2 > (double)m.k1 + B2) {
+                label = m.i1;
+            } else if ((double)m.k3 > (double)m.k1 + B2) {
+                const XT *x = reinterpret_cast<const XT *>(a.rows) + row * (int64_t)a.D;
+                const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
+                const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
+                label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
+                atomicAdd(a.stats + kStatRefine2, 1ull);
+            }
+        }
+        if (label < 0) {
+            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
+            if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
+            atomicAdd(a.stats + kStatFallback, 1ull);
+        }
+        a.labels[row] = label;
+    }
+}
+
+template <int DP, int W, typename XT>
+__device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict__ lds_c,
+                            float *__restrict__ lds_n)
+{
+    constexpr int NT = W * 64;
+    constexpr int KH = DP / 2;
+    constexpr int CS = kChunk * (DP + 4);  // floats per staged chunk
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row = tile * (32 * W) + wave * 32 + jl;
+    const bool rvalid = row < a.nrows;
+
+    float b[KH];
+    load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
+    // this lane's half of ||x||^2 (exact fp32 values, fp64 sum) for the bound
+    double xpart = 0.0;
+#pragma unroll
+    for (int s = 0; s < KH; ++s) xpart = fma((double)b[s], (double)b[s], xpart);
+
+    Top3 st{-kInf, -kInf, -kInf, -1, -1};  // three largest v = -key/2
+    const int nch = (int)a.nchunks;         // < 2^25: centroid ids fit int32
+    const float *Ab = lds_c + jl * (DP + 4) + h * KH;  // this lane's A row in buffer 0
+    const float *Nb = lds_n + 4 * h;
+    const int idh = (int)a.c_begin + 4 * h;
+
+    ChunkRegs<DP, NT> cr;
+    chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin, a.c_end, a.D, cr);
+    chunk_store<DP, NT, true>(lds_c, lds_n, cr);
+    __syncthreads();
+
+    // chunk j of the range sits in buffer j & 1 (data and -||c||^2/2)
+    auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) {
+        const bool more = j + 1 < nch;
+        if (more)
+            chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + (int64_t)(j + 1) * kChunk, a.c_end, a.D, cr);
+        const int bj = j & 1;
+        top1_chunk<DP, true>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1, idh + (j - 1) * kChunk, st);
+        if (more) chunk_store<DP, NT, true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk, cr);
+        __syncthreads();
+    };
+
+    f32x16 x0, x1, y0, y1;
+    {
+        const bool more = nch > 1;
+        if (more) chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + kChunk, a.c_end, a.D, cr);
+        top1_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, st);
+        if (more) chunk_store<DP, NT, true>(lds_c + CS, lds_n + kChunk, cr);
+        __syncthreads();
+    }
+    int j = 1;
+    for (; j + 1 < nch; j += 2) {
+        step(j, y0, y1, x0, x1);
+        step(j + 1, x0, x1, y0, y1);
+    }
+    if (j < nch) {
+        step(j, y0, y1, x0, x1);
+        top1_drain(y0, y1, idh + j * kChunk, st);
+    } else {
+        top1_drain(x0, x1, idh + (j - 1) * kChunk, st);
+    }
+    // back to keys: key = -2 v exactly, ascending
+    st.k1 *= -2.0f;
+    st.k2 *= -2.0f;
+    st.k3 *= -2.0f;
+    top1_finish<XT>(a, row, rvalid, h, xpart, st);
 }
 
 template <int DP, int W, typename XT, int MODE>
@@ -396,14 +571,14 @@ __global__ __launch_bounds__(W * 64, 2) void screen_kernel(ScreenArgs a)
 {
     __shared__ __attribute__((aligned(16))) float lds_c[2 * kChunk * (DP + 4)];
     __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
-    __shared__ Stage<W> stg;
     const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
-    if (MODE == kModeTop1) {
+    if constexpr (MODE == kModeTop1) {
         for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-            screen_range<DP, W, XT, MODE>(a, tile, 0, a.nchunks, lds_c, lds_n, stg);
+            screen_top1<DP, W, XT>(a, tile, lds_c, lds_n);
             __syncthreads();
         }
     } else {
+        __shared__ Stage<W> stg;
         // a contiguous range of (tile, chunk) units in tile-major order
         const int64_t units = ntiles * a.nchunks;
         int64_t u = units * blockIdx.x / gridDim.x;
