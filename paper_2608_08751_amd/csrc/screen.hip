@@ -89,52 +89,64 @@ __device__ __forceinline__ void load_row(const uint8_t *__restrict__ X, int64_t 
     }
 }
 
-// Per-thread registers holding one chunk on its way from HBM/L2 to LDS.
+// Stages chunks of kChunk centroids (and their norms) from HBM/L2 into LDS.
+// Loads go through a buffer resource that spans only the chunk's valid rows:
+// reads past it return zeros, which gives the zero padding of a ragged last
+// chunk (and of the dimensions D..DP-1, whose offsets are pointed out of
+// range) without per-element bounds arithmetic. Per thread, the byte offsets
+// within a chunk and the LDS slots are fixed, so a chunk costs kVec loads.
 template <int DP, int NT>
-struct ChunkRegs {
-    static constexpr int kVec = kChunk * DP / 4 / NT;  // float4 per thread
+struct Stager {
+    static constexpr int V4 = DP / 4;
+    static constexpr int kVec = kChunk * V4 / NT;  // float4 per thread
+    static constexpr int kOut = 1 << 30;           // an offset past any chunk
+    int goff[kVec];  // byte offset of this thread's float4 in the chunk
+    int loff[kVec];  // float offset of its slot in a staged chunk
     float4 v[kVec];
-    float n;
+    float n;    // norm of centroid threadIdx.x of the chunk (threads < kChunk)
+    int valid;  // rows of the chunk below c_end
+
+    __device__ __forceinline__ void init(int D)
+    {
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) {
+            const int idx = threadIdx.x + i * NT;
+            const int rr = idx / V4, c4 = idx - rr * V4;
+            goff[i] = 4 * c4 < D ? (rr * D + 4 * c4) * 4 : kOut;
+            loff[i] = rr * (DP + 4) + 4 * c4;
+        }
+    }
+
+    __device__ __forceinline__ void fetch(const float *__restrict__ cent, const float *__restrict__ cnorm,
+                                          int64_t cbase, int64_t c_end, int D)
+    {
+        const int64_t left = c_end - cbase;  // <= 0 past the range: nothing is read
+        valid = (int)(left < 0 ? 0 : left < kChunk ? left : kChunk);
+        const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(cent + cbase * D), (short)0, valid * D * 4, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < kVec; ++i)
+            v[i] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rc, goff[i], 0, 0));
+        if (threadIdx.x < kChunk) {
+            const __amdgpu_buffer_rsrc_t rn = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<float *>(cnorm + cbase), (short)0, valid * 4, 0x00020000);
+            n = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rn, threadIdx.x * 4, 0, 0));
+        }
+    }
+
+    // NEG_HALF stages -||c||^2/2 instead of ||c||^2 (exact: a power-of-two scaling).
+    template <bool NEG_HALF = false>
+    __device__ __forceinline__ void store(float *__restrict__ lc, float *__restrict__ ln) const
+    {
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) *reinterpret_cast<float4 *>(lc + loff[i]) = v[i];
+        if (threadIdx.x < kChunk) {
+            // padded rows get an infinite norm, so they never win a selection
+            const float m = (int)threadIdx.x < valid ? n : kInf;
+            ln[threadIdx.x] = NEG_HALF ? -0.5f * m : m;
+        }
+    }
 };
-
-template <int DP, int NT>
-__device__ __forceinline__ void chunk_fetch(const float *__restrict__ cent,
-                                            const float *__restrict__ cnorm, int64_t cbase,
-                                            int64_t c_end, int D, ChunkRegs<DP, NT> &r)
-{
-    constexpr int V4 = DP / 4;
-#pragma unroll
-    for (int i = 0; i < ChunkRegs<DP, NT>::kVec; ++i) {
-        const int idx = threadIdx.x + i * NT;
-        const int rr = idx / V4, c4 = idx - rr * V4;
-        const int64_t row = cbase + rr;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row < c_end && 4 * c4 < D)
-            v = *reinterpret_cast<const float4 *>(cent + row * (int64_t)D + 4 * c4);
-        r.v[i] = v;
-    }
-    r.n = 0.f;
-    if (threadIdx.x < kChunk) {
-        const int64_t row = cbase + threadIdx.x;
-        r.n = row < c_end ? cnorm[row] : kInf;
-    }
-}
-
-// NEG_HALF stages -||c||^2/2 instead of ||c||^2 (exact: a power-of-two scaling).
-template <int DP, int NT, bool NEG_HALF = false>
-__device__ __forceinline__ void chunk_store(float *__restrict__ lc, float *__restrict__ ln,
-                                            const ChunkRegs<DP, NT> &r)
-{
-    constexpr int V4 = DP / 4;
-    constexpr int LW = DP + 4;
-#pragma unroll
-    for (int i = 0; i < ChunkRegs<DP, NT>::kVec; ++i) {
-        const int idx = threadIdx.x + i * NT;
-        const int rr = idx / V4, c4 = idx - rr * V4;
-        *reinterpret_cast<float4 *>(lc + rr * LW + 4 * c4) = r.v[i];
-    }
-    if (threadIdx.x < kChunk) ln[threadIdx.x] = NEG_HALF ? -0.5f * r.n : r.n;
-}
 
 // Per-row state of the top-1 epilogue: the three smallest keys, ids of two.
 struct Top3 {
@@ -219,16 +231,16 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     if (MODE == kModeFilter && rvalid) tau = a.tau[row];
     int staged = 0;  // wave-uniform count of staged survivors
 
-    ChunkRegs<DP, NT> cr;
-    chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D, cr);
-    chunk_store<DP, NT>(lds_c, lds_n, cr);
+    Stager<DP, NT> cr;
+    cr.init(a.D);
+    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
+    cr.store(lds_c, lds_n);
     __syncthreads();
 
     for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
         const int buf = (int)((ch - ch_lo) & 1);
-        const bool more = ch + 1 < ch_hi;
         const int64_t cbase = a.c_begin + ch * kChunk;
-        if (more) chunk_fetch<DP, NT>(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D, cr);
+        cr.fetch(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D);  // unconditional; see screen_top1
 
         const float *A0 = lds_c + buf * (kChunk * LW) + jl * LW + h * KH;
         const float *A1 = A0 + 32 * LW;
@@ -316,7 +328,7 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
             }
         }
 
-        if (more) chunk_store<DP, NT>(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk, cr);
+        cr.store(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk);
         __syncthreads();
     }
 
@@ -524,30 +536,28 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     const float *Nb = lds_n + 4 * h;
     const int idh = (int)a.c_begin + 4 * h;
 
-    ChunkRegs<DP, NT> cr;
-    chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin, a.c_end, a.D, cr);
-    chunk_store<DP, NT, true>(lds_c, lds_n, cr);
+    Stager<DP, NT> cr;
+    cr.init(a.D);
+    cr.fetch(a.cent, a.cnorm, a.c_begin, a.c_end, a.D);
+    cr.template store<true>(lds_c, lds_n);
     __syncthreads();
 
     // chunk j of the range sits in buffer j & 1 (data and -||c||^2/2)
+    // (the chunk after the last one is fetched and staged too: its loads read
+    // nothing and return zeros, which keeps every load unconditional)
     auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) {
-        const bool more = j + 1 < nch;
-        if (more)
-            chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + (int64_t)(j + 1) * kChunk, a.c_end, a.D, cr);
+        cr.fetch(a.cent, a.cnorm, a.c_begin + (int64_t)(j + 1) * kChunk, a.c_end, a.D);
         const int bj = j & 1;
         top1_chunk<DP, true>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1, idh + (j - 1) * kChunk, st);
-        if (more) chunk_store<DP, NT, true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk, cr);
+        cr.template store<true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk);
         __syncthreads();
     };
 
     f32x16 x0, x1, y0, y1;
-    {
-        const bool more = nch > 1;
-        if (more) chunk_fetch<DP, NT>(a.cent, a.cnorm, a.c_begin + kChunk, a.c_end, a.D, cr);
-        top1_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, st);
-        if (more) chunk_store<DP, NT, true>(lds_c + CS, lds_n + kChunk, cr);
-        __syncthreads();
-    }
+    cr.fetch(a.cent, a.cnorm, a.c_begin + kChunk, a.c_end, a.D);
+    top1_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, st);
+    cr.template store<true>(lds_c + CS, lds_n + kChunk);
+    __syncthreads();
     int j = 1;
     for (; j + 1 < nch; j += 2) {
         step(j, y0, y1, x0, x1);
