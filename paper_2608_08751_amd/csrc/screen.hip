@@ -210,131 +210,6 @@ __device__ __forceinline__ void stage_flush(const ScreenArgs &a, Stage<W> &st, i
     }
 }
 
-template <int DP, int W, typename XT, int MODE>
-__device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
-                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
-{
-    constexpr int NT = W * 64;
-    constexpr int KH = DP / 2;
-    constexpr int LW = DP + 4;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int h = lane >> 5;
-    const int jl = lane & 31;
-    const int64_t row = tile * (32 * W) + wave * 32 + jl;
-    const bool rvalid = row < a.nrows;
-
-    float b[KH];
-    load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
-
-    float tau = -kInf;
-    if (MODE == kModeFilter && rvalid) tau = a.tau[row];
-    int staged = 0;  // wave-uniform count of staged survivors
-
-    Stager<DP, NT> cr;
-    cr.init(a.D);
-    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
-    cr.store(lds_c, lds_n);
-    __syncthreads();
-
-    for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
-        const int buf = (int)((ch - ch_lo) & 1);
-        const int64_t cbase = a.c_begin + ch * kChunk;
-        cr.fetch(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D);  // unconditional; see screen_top1
-
-        const float *A0 = lds_c + buf * (kChunk * LW) + jl * LW + h * KH;
-        const float *A1 = A0 + 32 * LW;
-        f32x16 acc0 = {0.f}, acc1 = {0.f};
-        // one K-block (4 K-steps) of A fragments in flight ahead of the MFMAs;
-        // the scheduling barrier keeps the compiler from hoisting all LDS
-        // reads of the unrolled loop (which would cost ~2*DP registers)
-        float4 a0 = *reinterpret_cast<const float4 *>(A0);
-        float4 a1 = *reinterpret_cast<const float4 *>(A1);
-#pragma unroll
-        for (int t = 0; t < KH / 4; ++t) {
-            float4 n0 = a0, n1 = a1;
-            if (t + 1 < KH / 4) {
-                n0 = *reinterpret_cast<const float4 *>(A0 + 4 * (t + 1));
-                n1 = *reinterpret_cast<const float4 *>(A1 + 4 * (t + 1));
-            }
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.x, b[4 * t + 0], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.x, b[4 * t + 0], acc1, 0, 0, 0);
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.y, b[4 * t + 1], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.y, b[4 * t + 1], acc1, 0, 0, 0);
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.z, b[4 * t + 2], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.z, b[4 * t + 2], acc1, 0, 0, 0);
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.w, b[4 * t + 3], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.w, b[4 * t + 3], acc1, 0, 0, 0);
-            a0 = n0;
-            a1 = n1;
-            __builtin_amdgcn_sched_barrier(0);
-        }
-
-        // keys: key = fl(n_c - 2 acc), centroid of register r in block rb is
-        // rb*32 + 8*(r/4) + 4*h + r%4
-        const float *N = lds_n + buf * kChunk;
-        const int cb32 = (int)cbase + 4 * h;  // centroid ids fit int32
-        const int ce32 = (int)a.c_end;
-        float key[32];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const float4 n0 = *reinterpret_cast<const float4 *>(N + 8 * g + 4 * h);
-            const float4 n1 = *reinterpret_cast<const float4 *>(N + 32 + 8 * g + 4 * h);
-            key[4 * g + 0] = fmaf(-2.0f, acc0[4 * g + 0], n0.x);
-            key[4 * g + 1] = fmaf(-2.0f, acc0[4 * g + 1], n0.y);
-            key[4 * g + 2] = fmaf(-2.0f, acc0[4 * g + 2], n0.z);
-            key[4 * g + 3] = fmaf(-2.0f, acc0[4 * g + 3], n0.w);
-            key[16 + 4 * g + 0] = fmaf(-2.0f, acc1[4 * g + 0], n1.x);
-            key[16 + 4 * g + 1] = fmaf(-2.0f, acc1[4 * g + 1], n1.y);
-            key[16 + 4 * g + 2] = fmaf(-2.0f, acc1[4 * g + 2], n1.z);
-            key[16 + 4 * g + 3] = fmaf(-2.0f, acc1[4 * g + 3], n1.w);
-        }
-
-        if (MODE == kModeKeys) {
-            if (rvalid) {
-                const int64_t ld = a.c_end - a.c_begin;
-                float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
-#pragma unroll
-                for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g)
-                        *reinterpret_cast<float4 *>(out + rb * 32 + 8 * g) =
-                            make_float4(key[16 * rb + 4 * g + 0], key[16 * rb + 4 * g + 1],
-                                        key[16 * rb + 4 * g + 2], key[16 * rb + 4 * g + 3]);
-            }
-        } else {  // kModeFilter
-#pragma unroll
-            for (int r = 0; r < 32; ++r) {
-                const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
-                const bool pass = rvalid && key[r] <= tau && cid < ce32;
-                const uint64_t mask = __ballot(pass);
-                if (mask != 0) {
-                    if (pass) {
-                        const int pos = staged + __builtin_amdgcn_mbcnt_hi(
-                            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-                        stg.kc[wave][pos] = make_uint2(__float_as_uint(key[r]), (uint32_t)cid);
-                        stg.row[wave][pos] = (unsigned char)(wave * 32 + jl);
-                    }
-                    staged += __popcll(mask);
-                    if (staged >= 64) {
-                        stage_flush(a, stg, wave, lane, tile, 64);
-                        if (lane < staged - 64) {
-                            stg.kc[wave][lane] = stg.kc[wave][64 + lane];
-                            stg.row[wave][lane] = stg.row[wave][64 + lane];
-                        }
-                        staged -= 64;
-                    }
-                }
-            }
-        }
-
-        cr.store(lds_c + (buf ^ 1) * (kChunk * LW), lds_n + (buf ^ 1) * kChunk);
-        __syncthreads();
-    }
-
-    if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
-}
-
 // ---------------------------------------------------------------- top-1 path
 //
 // The accumulators start from -fl32(||c||^2)/2 (staged in LDS instead of the
@@ -439,7 +314,7 @@ __device__ __forceinline__ void top1_kblocks(const float *A0, const float *A1, c
 // One chunk: A0 = this lane's row of the staged centroids, Nh = the staged
 // -||c||^2/2 values of the chunk offset by 4h.
 template <int DP, bool EP>
-__device__ __forceinline__ void top1_chunk(const float *A0, const float *Nh, const float (&b)[DP / 2],
+__device__ __forceinline__ void mfma_chunk(const float *A0, const float *Nh, const float (&b)[DP / 2],
                                            f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1,
                                            int idp, Top3 &st)
 {
@@ -548,14 +423,14 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) {
         cr.fetch(a.cent, a.cnorm, a.c_begin + (int64_t)(j + 1) * kChunk, a.c_end, a.D);
         const int bj = j & 1;
-        top1_chunk<DP, true>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1, idh + (j - 1) * kChunk, st);
+        mfma_chunk<DP, true>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1, idh + (j - 1) * kChunk, st);
         cr.template store<true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk);
         __syncthreads();
     };
 
     f32x16 x0, x1, y0, y1;
     cr.fetch(a.cent, a.cnorm, a.c_begin + kChunk, a.c_end, a.D);
-    top1_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, st);
+    mfma_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, st);
     cr.template store<true>(lds_c + CS, lds_n + kChunk);
     __syncthreads();
     int j = 1;
@@ -574,6 +449,99 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     st.k2 *= -2.0f;
     st.k3 *= -2.0f;
     top1_finish<XT>(a, row, rvalid, h, xpart, st);
+}
+
+// Keys or filter over the chunks [ch_lo, ch_hi) of one tile. As on the
+// top-1 path the accumulators start from -||c||^2/2, so v = -key/2 exactly:
+// the keys mode writes -2v and the filter keeps v >= -tau/2 (the same test
+// as key <= tau). Padded centroids have v = -inf and the row threshold is
+// clamped to the lowest finite float, so they never pass.
+template <int DP, int W, typename XT, int MODE>
+__device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
+                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
+{
+    constexpr int NT = W * 64;
+    constexpr int KH = DP / 2;
+    constexpr int CS = kChunk * (DP + 4);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row = tile * (32 * W) + wave * 32 + jl;
+    const bool rvalid = row < a.nrows;
+
+    float b[KH];
+    load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
+
+    float tv = kInf;  // filter: keep v >= tv; rows past the end keep nothing
+    if (MODE == kModeFilter && rvalid) tv = fmaxf(-0.5f * a.tau[row], -__FLT_MAX__);
+    int staged = 0;  // wave-uniform count of staged survivors
+    Top3 unused{};
+
+    Stager<DP, NT> cr;
+    cr.init(a.D);
+    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
+    cr.template store<true>(lds_c, lds_n);
+    __syncthreads();
+
+    const float *Ab = lds_c + jl * (DP + 4) + h * KH;
+    const float *Nb = lds_n + 4 * h;
+    for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
+        const int buf = (int)((ch - ch_lo) & 1);
+        const int64_t cbase = a.c_begin + ch * kChunk;
+        cr.fetch(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D);  // unconditional; see screen_top1
+
+        f32x16 acc0, acc1;
+        mfma_chunk<DP, false>(Ab + buf * CS, Nb + buf * kChunk, b, acc0, acc1, acc0, acc1, 0, unused);
+
+        // register r of block rb holds centroid rb*32 + 8*(r/4) + 4*h + r%4
+        if (MODE == kModeKeys) {
+            if (rvalid) {
+                const int64_t ld = a.c_end - a.c_begin;  // a multiple of kChunk
+                float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    *reinterpret_cast<float4 *>(out + 8 * g) =
+                        make_float4(-2.0f * acc0[4 * g + 0], -2.0f * acc0[4 * g + 1],
+                                    -2.0f * acc0[4 * g + 2], -2.0f * acc0[4 * g + 3]);
+                    *reinterpret_cast<float4 *>(out + 32 + 8 * g) =
+                        make_float4(-2.0f * acc1[4 * g + 0], -2.0f * acc1[4 * g + 1],
+                                    -2.0f * acc1[4 * g + 2], -2.0f * acc1[4 * g + 3]);
+                }
+            }
+        } else {  // kModeFilter
+            const int cb32 = (int)cbase + 4 * h;  // centroid ids fit int32
+#pragma unroll
+            for (int r = 0; r < 32; ++r) {
+                const float v = r < 16 ? acc0[r] : acc1[r - 16];
+                const bool pass = v >= tv;
+                const uint64_t mask = __ballot(pass);
+                if (mask != 0) {
+                    if (pass) {
+                        const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
+                        const int pos = staged + __builtin_amdgcn_mbcnt_hi(
+                            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+                        stg.kc[wave][pos] = make_uint2(__float_as_uint(-2.0f * v), (uint32_t)cid);
+                        stg.row[wave][pos] = (unsigned char)(wave * 32 + jl);
+                    }
+                    staged += __popcll(mask);
+                    if (staged >= 64) {
+                        stage_flush(a, stg, wave, lane, tile, 64);
+                        if (lane < staged - 64) {
+                            stg.kc[wave][lane] = stg.kc[wave][64 + lane];
+                            stg.row[wave][lane] = stg.row[wave][64 + lane];
+                        }
+                        staged -= 64;
+                    }
+                }
+            }
+        }
+
+        cr.template store<true>(lds_c + (buf ^ 1) * CS, lds_n + (buf ^ 1) * kChunk);
+        __syncthreads();
+    }
+
+    if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
 }
 
 template <int DP, int W, typename XT, int MODE>
