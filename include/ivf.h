@@ -39,6 +39,8 @@
  *     share a context must not overlap on different streams.
  *   - Q, N == 0 is a no-op returning IVF_OK.
  *   - Supported shapes: 4 <= D <= 256 with D % 4 == 0 (else IVF_EUNSUPPORTED).
+ *   - Input values must be finite, with squared vector norms below FLT_MAX;
+ *     results are unspecified otherwise (inputs are not scanned for this).
  */
 #ifndef IVF_H
 #define IVF_H
@@ -174,7 +176,8 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *   IVF_OPT_BUILD_BLOCKS    cap on the row blocks of the single-pass list build
  *                           (more than 65,536 lists; 0 = default); speed only
  *   IVF_OPT_SCREEN_WAVES    wave64s per workgroup of the distance-screening
- *                           kernel, 4 or 8; speed only, never results */
+ *                           kernel, 4 or 8 (D > 128 always uses 4); speed
+ *                           only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,

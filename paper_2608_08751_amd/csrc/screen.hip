@@ -544,8 +544,17 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
     if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
 }
 
+// Waves per SIMD: two, so that one wave's staging and epilogue overlap the
+// other's MFMAs; one for DP >= 192, whose row fragments need the whole
+// register file (those sizes always run W = 4, one workgroup per CU).
+template <int DP>
+constexpr int waves_per_simd()
+{
+    return DP >= 192 ? 1 : 2;
+}
+
 template <int DP, int W, typename XT, int MODE>
-__global__ __launch_bounds__(W * 64, 2) void screen_kernel(ScreenArgs a)
+__global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(ScreenArgs a)
 {
     __shared__ __attribute__((aligned(16))) float lds_c[2 * kChunk * (DP + 4)];
     __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
@@ -577,7 +586,7 @@ hipError_t launch_one(const ScreenArgs &a, int num_cus, hipStream_t s)
 {
     const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
     const int64_t work = MODE == kModeTop1 ? ntiles : ntiles * a.nchunks;
-    const int per_cu = 8 / W;  // two waves per SIMD
+    const int per_cu = 4 * waves_per_simd<DP>() / W;
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(work, (int64_t)per_cu * num_cus));
     hipLaunchKernelGGL((screen_kernel<DP, W, XT, MODE>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
@@ -602,8 +611,8 @@ hipError_t launch_w(int mode, int rowtype, int DP, const ScreenArgs &a, int num_
     case 64: return launch_dp<64, W>(mode, rowtype, a, num_cus, s);
     case 96: return launch_dp<96, W>(mode, rowtype, a, num_cus, s);
     case 128: return launch_dp<128, W>(mode, rowtype, a, num_cus, s);
-    case 192: return launch_dp<192, W>(mode, rowtype, a, num_cus, s);
-    case 256: return launch_dp<256, W>(mode, rowtype, a, num_cus, s);
+    case 192: return launch_dp<192, 4>(mode, rowtype, a, num_cus, s);
+    case 256: return launch_dp<256, 4>(mode, rowtype, a, num_cus, s);
     default: return hipErrorInvalidValue;
     }
 }

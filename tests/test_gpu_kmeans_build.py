@@ -81,12 +81,22 @@ def test_kmeans_empty_clusters_reseed(ivf_ctx, oracle_mod):
         assert (cen[j] == x[oracle_mod.reseed_row(77, 5, j, 3000)]).all()
 
 
-@pytest.mark.parametrize("N,C,D", [(1, 1, 4), (500, 1, 8), (257, 256, 16), (1000, 1000, 36)])
+@pytest.mark.parametrize("N,C,D", [(1, 1, 4), (500, 1, 8), (257, 256, 16), (1000, 1000, 36),
+                                   (3000, 300, 200), (2000, 150, 256)])
 def test_kmeans_small_shapes(ivf_ctx, oracle_mod, N, C, D):
     rng = np.random.default_rng(N + C)
     x = rng.integers(0, 256, (N, D)).astype(np.uint8)
     c = rng.uniform(0, 255, (C, D)).astype(np.float32)
     assert_step_equal(ivf_ctx, oracle_mod, x, c, 3, 1)
+
+
+@pytest.mark.parametrize("D", [160, 256])
+def test_kmeans_wide_float_rows(ivf_ctx, oracle_mod, D):
+    """Wide rows run the screening kernel with one wave per SIMD."""
+    rng = np.random.default_rng(D)
+    x = (rng.standard_normal((2500, D)) * 2 + rng.integers(0, 4, (2500, 1))).astype(np.float32)
+    c = x[rng.choice(2500, 70, replace=False)].copy()
+    assert_step_equal(ivf_ctx, oracle_mod, x, c, 5, 0)
 
 
 def test_kmeans_forced_fallback_is_identical(ivf_ctx, oracle_mod):
