@@ -175,6 +175,11 @@ def main():
         "flops_per_launch": 2.0 * C * D * Nt,
         "avg_launch_ms": sum(top1) / len(top1),
     }
+    # the fp32 MFMA pipe as the library's probe kernel measures it on this
+    # GPU (register operands only), after the timed region
+    _, probe_tflops = ctx.mfma_probe()
+    roofline["measured_peak"] = probe_tflops
+    roofline["frac_of_measured_peak"] = achieved / probe_tflops
 
     def call_ms(call):
         return sum(ms for n, ms in timeline if n.startswith(call + "/")) / args.steps

@@ -187,6 +187,16 @@ typedef enum {
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 
+/* Measures the fp32 MFMA pipe for reporting: enqueues a probe kernel that
+ * runs only v_mfma_f32_32x32x2_f32 (register operands, two waves per SIMD on
+ * every CU) for `iters` rounds of 16 instructions per wave (after one
+ * untimed round that loads the kernel), waits for it
+ * (this call synchronises the context's stream), and stores its duration in
+ * *out_ms and its rate in *out_tflops (either may be NULL, not both).
+ * Errors: IVF_EINVAL (iters outside [1, 2^20], both outputs NULL),
+ * IVF_EUNSUPPORTED (validation-only context), IVF_EDEVICE. */
+ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tflops);
+
 /* Kernel timeline recorded while IVF_OPT_PROFILE is on, across calls, since
  * the last complete read: waits on the stream, then fills up to `max` entries
  * of names[] (strings owned by the context, valid until the next read) and

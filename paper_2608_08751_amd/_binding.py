@@ -38,6 +38,7 @@ SIGNATURES = [
     ("ivf_last_stats", _INT, [_P, ctypes.POINTER(_I64)]),
     ("ivf_set_option", _INT, [_P, _INT, _I64]),
     ("ivf_kernel_times", _INT, [_P, _INT, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
+    ("ivf_mfma_probe", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
 ]
 
 _lib = None
@@ -144,6 +145,15 @@ class Context:
         ms = (ctypes.c_float * max(n, 1))()
         self.lib.ivf_kernel_times(self.handle, n, names, ms)
         return [(names[i].decode(), float(ms[i])) for i in range(n)]
+
+    def mfma_probe(self, iters: int = 20000):
+        """(ms, TFLOP/s) of the fp32 MFMA throughput probe (synchronises)."""
+        ms = ctypes.c_float()
+        tf = ctypes.c_double()
+        self.bind_stream()
+        self.check(self.lib.ivf_mfma_probe(self.handle, iters, ctypes.byref(ms), ctypes.byref(tf)),
+                   "ivf_mfma_probe")
+        return float(ms.value), float(tf.value)
 
     def last_stats(self):
         out = (ctypes.c_int64 * 8)()

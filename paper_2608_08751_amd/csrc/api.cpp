@@ -521,6 +521,36 @@ int ivf_kernel_times(ivf_ctx *ctx, int max, const char **names, float *ms)
     return n;
 }
 
+ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tflops)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    if (iters < 1 || iters > (1 << 20)) return fail(ctx, IVF_EINVAL, "iters must be in [1, 2^20]");
+    if (!out_ms && !out_tflops) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (ctx->device < 0) return fail(ctx, IVF_EUNSUPPORTED, "validation-only context");
+    DeviceGuard g(ctx->device);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+        if (e0) (void)hipEventDestroy(e0);
+        return fail(ctx, IVF_EDEVICE, "hipEventCreate failed");
+    }
+    double flops = 0.0;
+    float ms = 0.f;
+    // an untimed short launch first: the first launch of a kernel also loads it
+    hipError_t e = launch_mfma_probe(1, ctx->num_cus, ctx->stream, &flops);
+    if (e == hipSuccess) e = hipEventRecord(e0, ctx->stream);
+    if (e == hipSuccess) e = launch_mfma_probe(iters, ctx->num_cus, ctx->stream, &flops);
+    if (e == hipSuccess) e = hipEventRecord(e1, ctx->stream);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (e != hipSuccess) return fail(ctx, IVF_EDEVICE, "MFMA probe: %s", hipGetErrorString(e));
+    if (out_ms) *out_ms = ms;
+    if (out_tflops) *out_tflops = ms > 0.f ? flops / (ms * 1e-3) / 1e12 : 0.0;
+    return IVF_OK;
+}
+
 ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
                      int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist)
 {

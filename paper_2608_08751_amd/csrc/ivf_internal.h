@@ -151,4 +151,8 @@ hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
                                 int32_t iter, float *cent_out, double *jpart, double *objective,
                                 hipStream_t s);
 
+// ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
+// Enqueues the probe kernel for `iters` rounds; *flops = the work it does.
+hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops);
+
 }  // namespace ivf

@@ -1,0 +1,45 @@
+// Throughput probe for the fp32 MFMA pipe of gfx950: every wave runs rounds
+// of sixteen v_mfma_f32_32x32x2_f32 on two independent accumulators with the
+// A and B operands in registers, two waves per SIMD on every CU. This is the
+// rate the screening kernels' MFMA stream could reach with no loads and no
+// other vector instructions; bench reports the screening kernels against it
+// next to the published peak.
+#include "ivf_internal.h"
+
+namespace ivf {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters, float a, float b, int write,
+                                                            float *sink)
+{
+    f32x16 acc0 = {0.f}, acc1 = {0.f};
+    const float av = a + threadIdx.x * 1e-7f;
+    const float bv = b - threadIdx.x * 1e-7f;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc1, 0, 0, 0);
+        }
+    }
+    float r = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) r += acc0[e] + acc1[e];
+    // the host passes write = 0: the store only keeps the MFMAs alive
+    if (write) sink[blockIdx.x * blockDim.x + threadIdx.x] = r;
+}
+
+}  // namespace
+
+hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops)
+{
+    const int grid = 2 * num_cus;  // 4 waves per workgroup: two waves per SIMD
+    hipLaunchKernelGGL(mfma_probe_kernel, dim3(grid), dim3(256), 0, s, iters, 1.0f, 2.0f, 0,
+                       (float *)nullptr);
+    *flops = (double)grid * 4 * iters * 16 * (2.0 * 32 * 32 * 2);
+    return hipGetLastError();
+}
+
+}  // namespace ivf

@@ -152,6 +152,16 @@ def test_options_and_errors(vctx):
     assert lib.ivf_route(None, P(0), 1, P(GB), 1, 4, 1, P(2 * GB), None) == B.IVF_EINVAL
 
 
+def test_mfma_probe_validation(vctx):
+    lib, h = vctx.lib, vctx.handle
+    ms, tf = ctypes.c_float(), ctypes.c_double()
+    assert lib.ivf_mfma_probe(h, 0, ctypes.byref(ms), ctypes.byref(tf)) == B.IVF_EINVAL
+    assert lib.ivf_mfma_probe(h, 1 << 21, ctypes.byref(ms), None) == B.IVF_EINVAL
+    assert lib.ivf_mfma_probe(h, 10, None, None) == B.IVF_EINVAL
+    assert lib.ivf_mfma_probe(h, 10, ctypes.byref(ms), None) == B.IVF_EUNSUPPORTED
+    assert lib.ivf_mfma_probe(None, 10, ctypes.byref(ms), None) == B.IVF_EINVAL
+
+
 def test_no_cpu_fallback_without_gpu():
     import torch
 
