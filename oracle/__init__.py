@@ -13,7 +13,8 @@ arrays through ctypes. Definitions followed:
 * ``assign``         nearest centroid per vector, ties to the lower id;
 * ``kmeans_update``  Lloyd mean update with deterministic reseed of empty clusters;
 * ``objective``      sum of squared distances of every vector to its assigned centroid;
-* ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation.
+* ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation;
+* ``list_major``     list-major copy of the vectors and their residuals x - c(x).
 
 Parity pins for each function are in ``tests/test_oracle_*.py``.
 """
@@ -72,6 +73,7 @@ def _load():
         lib.oracle_kmeans_step.argtypes = [p, ci, i64, p, i64, ci, u64, i32, p, p, p, p, ci]
         lib.oracle_build_lists.argtypes = [p, i64, i64, p, p, p]
         lib.oracle_num_threads.argtypes = [ci]
+        lib.oracle_list_major.argtypes = [p, ci, i64, p, i64, ci, p, p, i64, p, p]
         for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
                   lib.oracle_objective, lib.oracle_kmeans_step, lib.oracle_build_lists,
                   lib.oracle_num_threads):
@@ -189,6 +191,23 @@ def build_lists(labels, C: int):
     perm = np.empty(N, np.uint32)
     _check(_load().oracle_build_lists(_ptr(lab), N, C, _ptr(counts), _ptr(offsets), _ptr(perm)), "build_lists")
     return counts, offsets, perm
+
+
+def list_major(x, centroids, labels, perm, rows: bool = True, residuals: bool = True):
+    """List-major copy x[perm] (same dtype) and residuals x[perm] - c[labels[perm]]
+    (fp32, one fp32 subtraction per element); perm may be a slice of the
+    permutation. Returns (rows or None, residuals or None)."""
+    x, dt = _data(x)
+    c = _f32(centroids)
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    perm = np.ascontiguousarray(perm, dtype=np.uint32)
+    N, D = x.shape
+    n = perm.shape[0]
+    out_rows = np.empty((n, D), x.dtype) if rows else None
+    out_res = np.empty((n, D), np.float32) if residuals else None
+    _check(_load().oracle_list_major(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(lab), _ptr(perm), n,
+                                     _ptr(out_rows), _ptr(out_res)), "list_major")
+    return out_rows, out_res
 
 
 def assign_build(x, centroids, nthreads: int = 0):

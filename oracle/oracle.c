@@ -24,6 +24,9 @@
  *                        introduction and in "Fast Index Construction").
  *   oracle_build_lists   cluster-major inverted lists with offset, length and
  *                        vector ids (Sec. "System Architecture", index layout).
+ *   oracle_list_major    list-major copy of the vectors and their residuals
+ *                        x - c(x) (Sec. "List-major contiguous scans" and
+ *                        Sec. "Residual-PQ Candidate Reduction").
  *   oracle_reseed_row    deterministic choice of a training row for an empty
  *                        cluster; the paper is silent, the reading is SplitMix64
  *                        (Steele, Lea & Flood, OOPSLA 2014).
@@ -334,6 +337,49 @@ int oracle_build_lists(const int32_t *labels, int64_t n, int64_t nc, int64_t *ou
     memcpy(cursor, out_offsets, sizeof(int64_t) * (size_t)nc);
     for (int64_t i = 0; i < n; ++i) out_perm[cursor[labels[i]]++] = (uint32_t)i;
     free(cursor);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------ list-major layout */
+
+/* List-major copy of the base vectors and their residuals (Sec. "List-major
+ * contiguous scans": vectors stored in list order; Sec. "Residual-PQ
+ * Candidate Reduction", residual encoding: r = x - c(x) with c(x) the
+ * assigned centroid). For output position i, row = perm[i]:
+ *   out_rows[i]    = x[row]                       (same element type)
+ *   out_res[i][d]  = (float)x[row][d] - c[labels[row]][d]   (one fp32
+ *                    subtraction: the exact difference rounded once)
+ * Either output may be NULL. */
+int oracle_list_major(const void *x, int dtype, int64_t n_rows, const float *centroids, int64_t nc,
+                      int D, const int32_t *labels, const uint32_t *perm, int64_t n,
+                      void *out_rows, float *out_res)
+{
+    if (n_rows < 0 || n < 0 || nc < 1 || D < 1 || (dtype != ORACLE_F32 && dtype != ORACLE_U8))
+        return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        if ((int64_t)perm[i] >= n_rows) return ORACLE_EINVAL;
+        const int32_t l = labels[perm[i]];
+        if (l < 0 || l >= nc) return ORACLE_EINVAL;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        const int64_t row = (int64_t)perm[i];
+        const float *c = centroids + (int64_t)labels[row] * D;
+        for (int d = 0; d < D; ++d) {
+            float v;
+            if (dtype == ORACLE_U8) {
+                const uint8_t b = ((const uint8_t *)x)[row * D + d];
+                v = (float)b;
+                if (out_rows) ((uint8_t *)out_rows)[i * D + d] = b;
+            } else {
+                v = ((const float *)x)[row * D + d];
+                if (out_rows) ((float *)out_rows)[i * D + d] = v;
+            }
+            if (out_res) {
+                const float diff = v - c[d];
+                out_res[i * D + d] = diff;
+            }
+        }
+    }
     return ORACLE_OK;
 }
 

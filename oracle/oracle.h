@@ -45,6 +45,9 @@ int oracle_kmeans_step(const void *x, int dtype, int64_t n, const float *centroi
 int oracle_build_lists(const int32_t *labels, int64_t n, int64_t nc, int64_t *out_counts,
                        int64_t *out_offsets, uint32_t *out_perm);
 
+int oracle_list_major(const void *x, int dtype, int64_t n_rows, const float *centroids, int64_t nc,
+                      int D, const int32_t *labels, const uint32_t *perm, int64_t n,
+                      void *out_rows, float *out_res);
 int oracle_num_threads(int nthreads);
 
 #ifdef __cplusplus
