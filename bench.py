@@ -233,7 +233,8 @@ def main():
         result["cpu_baseline"] = cpu_baseline(x_train, c0, args.cpu_seconds)
 
     if not args.no_extra:
-        result["extra"] = {"route_normalised": bench_route_normalised(ctx)}
+        result["extra"] = {"route_normalised": bench_route_normalised(ctx),
+                           "list_major": bench_list_major(ctx, x_base, c1, off_b, perm_b)}
         if args.build_rows > 0:
             # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
             del x_train, x_base, lab_t, lab_b, perm_b
@@ -299,6 +300,36 @@ def bench_route_normalised(ctx):
         "screen_ms": filt,
         "stats": st,
     }
+
+
+def bench_list_major(ctx, x, cent, offsets, perm):
+    """ivf_list_major on the step's assign-build output (10M uint8 base rows,
+    65,536 lists): list-major copy plus fp32 residuals, median of 3 calls.
+    Algorithmic bytes per row: read the row and its id, write the row and
+    its residual (D + 4 + D + 4 D)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    N, D = x.shape
+    rows = torch.empty_like(x)
+    res = torch.empty((N, D), dtype=torch.float32, device=x.device)
+    ivf.ivf_list_major(ctx, x, cent, offsets, perm, out_rows=rows, out_residuals=res)
+    torch.cuda.synchronize()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    times = []
+    for _ in range(3):
+        ivf.ivf_list_major(ctx, x, cent, offsets, perm, out_rows=rows, out_residuals=res)
+        times.append(sum(ms for _, ms in ctx.kernel_times()))
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    t = float(np.median(times))
+    per_row = D + 4 + D + 4 * D
+    gbs = per_row * N / (t * 1e-3) / 1e9
+    del rows, res
+    return {"rows": N, "dim": D, "ms": t, "bytes_per_row": per_row, "GBps": gbs,
+            "hbm_frac": gbs / PEAK_HBM_GBS}
 
 
 def bench_build(ctx, N, C):

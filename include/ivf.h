@@ -187,6 +187,32 @@ typedef enum {
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 
+/* List-major layout of the base vectors and their residuals (Sec. "List-major
+ * contiguous scans": every IVF list is one contiguous range; Sec.
+ * "Residual-PQ Candidate Reduction": the residual x - c(x) to the assigned
+ * centroid is what residual PQ encodes).
+ *   base          [N, D] fp32 or uint8 (dt), N <= 2^32 - 1
+ *   centroids     [C, D] fp32
+ *   offsets       [C + 1] int64 list offsets and
+ *   perm          [N] uint32 list-major row ids, as ivf_assign_build returns
+ *                 them (offsets non-decreasing, offsets[0] = 0, offsets[C] = N)
+ *   pos0, n       the output covers list-major positions [pos0, pos0 + n)
+ *                 (batches of a large base), 0 <= pos0 <= pos0 + n <= N
+ *   out_rows      [n, D] same type as base: row perm[pos0 + i], may be NULL
+ *   out_residuals [n, D] fp32: that row minus the centroid of the list holding
+ *                 position pos0 + i, one fp32 subtraction per element (the
+ *                 exact difference rounded once), may be NULL (not both,
+ *                 unless n == 0, which is a no-op)
+ * A perm entry >= N yields a zero row and NaN residuals (nothing is read for
+ * it); offsets that are not a valid list layout give unspecified lists but no
+ * access outside the arrays. No workspace is used.
+ * Errors: IVF_EINVAL (sizes, positions, NULL pointers, misalignment,
+ * aliasing), IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */
+ivf_status ivf_list_major(ivf_ctx *ctx, const void *base, int dt, int64_t N,
+                          const float *centroids, int64_t C, int32_t D, const int64_t *offsets,
+                          const uint32_t *perm, int64_t pos0, int64_t n, void *out_rows,
+                          float *out_residuals);
+
 /* Measures the fp32 MFMA pipe for reporting: enqueues a probe kernel that
  * runs only v_mfma_f32_32x32x2_f32 (register operands, two waves per SIMD on
  * every CU) for `iters` rounds of 16 instructions per wave (after one

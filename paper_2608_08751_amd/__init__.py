@@ -34,6 +34,7 @@ from ._binding import (  # noqa: F401
     ivf_assign_build,
     ivf_build_lists,
     ivf_kmeans_step,
+    ivf_list_major,
     ivf_route,
     load_library,
 )

@@ -39,6 +39,7 @@ SIGNATURES = [
     ("ivf_set_option", _INT, [_P, _INT, _I64]),
     ("ivf_kernel_times", _INT, [_P, _INT, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
     ("ivf_mfma_probe", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
+    ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
 ]
 
 _lib = None
@@ -271,3 +272,28 @@ def ivf_build_lists(ctx: Context, labels, C: int, out_counts=None, out_offsets=N
     ctx.check(ctx.lib.ivf_build_lists(ctx.handle, _ptr(labels), N, C, _ptr(out_counts),
                                       _ptr(out_offsets), _ptr(out_perm)), "ivf_build_lists")
     return out_counts, out_offsets, out_perm
+
+
+def ivf_list_major(ctx: Context, base, centroids, offsets, perm, pos0: int = 0, n=None,
+                   rows: bool = True, residuals: bool = True, out_rows=None, out_residuals=None):
+    """List-major copy base[perm[pos0:pos0+n]] and residuals against each
+    position's list centroid (fp32). Returns (rows or None, residuals or None)."""
+    import torch
+
+    for t, name in ((base, "base"), (centroids, "centroids"), (offsets, "offsets"), (perm, "perm")):
+        _device_tensor(t, name)
+    N, D = base.shape
+    C = centroids.shape[0]
+    if n is None:
+        n = N - pos0
+    dev = base.device
+    if rows and out_rows is None:
+        out_rows = torch.empty((n, D), dtype=base.dtype, device=dev)
+    if residuals and out_residuals is None:
+        out_residuals = torch.empty((n, D), dtype=torch.float32, device=dev)
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_list_major(ctx.handle, _ptr(base), _dtype_code(base), N, _ptr(centroids), C, D,
+                                     _ptr(offsets), _ptr(perm), pos0, n,
+                                     _ptr(out_rows if rows else None),
+                                     _ptr(out_residuals if residuals else None)), "ivf_list_major")
+    return (out_rows if rows else None), (out_residuals if residuals else None)

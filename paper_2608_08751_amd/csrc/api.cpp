@@ -770,4 +770,40 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
     return IVF_OK;
 }
 
+ivf_status ivf_list_major(ivf_ctx *ctx, const void *base, int dt, int64_t N, const float *centroids,
+                          int64_t C, int32_t D, const int64_t *offsets, const uint32_t *perm,
+                          int64_t pos0, int64_t n, void *out_rows, float *out_residuals)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "list_major";
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    size_t rb;
+    if ((st = check_rows(ctx, base, dt, N, D, &rb)) != IVF_OK) return st;
+    if (pos0 < 0 || n < 0 || pos0 > N || n > N - pos0)
+        return fail(ctx, IVF_EINVAL, "positions [pos0, pos0 + n) must lie in [0, N)");
+    if (n == 0) return IVF_OK;
+    if (!out_rows && !out_residuals) return fail(ctx, IVF_EINVAL, "no output requested");
+    if (!centroids || !offsets || (N > 0 && !perm)) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(centroids) || !aligned16(offsets) || (perm && !aligned16(perm)) ||
+        (out_rows && !aligned16(out_rows)) || (out_residuals && !aligned16(out_residuals)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t ob[2] = {(size_t)n * rb, (size_t)n * D * 4};
+    const void *outs[2] = {out_rows, out_residuals};
+    const void *ins[4] = {base, centroids, offsets, perm};
+    const size_t ib[4] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)(C + 1) * 8, (size_t)N * 4};
+    for (int i = 0; i < 2; ++i)
+        for (int k = 0; k < 4; ++k)
+            if (overlap(outs[i], ob[i], ins[k], ib[k])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+    if (overlap(out_rows, ob[0], out_residuals, ob[1])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
+    TIMED("list_major", launch_list_major(base, rowtype, N, centroids, C, D, offsets, perm, pos0, n,
+                                          out_rows, out_residuals, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
 }  // extern "C"

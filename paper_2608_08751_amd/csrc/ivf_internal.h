@@ -151,6 +151,11 @@ hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
                                 int32_t iter, float *cent_out, double *jpart, double *objective,
                                 hipStream_t s);
 
+// ---- list-major layout and residuals (layout.hip) ----------------------------
+hipError_t launch_list_major(const void *base, int rowtype, int64_t N, const float *cent, int64_t C,
+                             int D, const int64_t *offsets, const uint32_t *perm, int64_t pos0,
+                             int64_t n, void *out_rows, float *out_res, hipStream_t s);
+
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.
 hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops);

@@ -162,6 +162,31 @@ def test_mfma_probe_validation(vctx):
     assert lib.ivf_mfma_probe(None, 10, ctypes.byref(ms), None) == B.IVF_EINVAL
 
 
+def test_list_major_validation(vctx):
+    lib, h = vctx.lib, vctx.handle
+    N, C, D = 1000, 10, 16
+    base, cent, off, perm, rows, res = P(0), P(GB), P(2 * GB), P(3 * GB), P(4 * GB), P(5 * GB)
+    call = lambda **k: lib.ivf_list_major(h, k.get("base", base), k.get("dt", B.IVF_U8), k.get("N", N),
+                                          k.get("cent", cent), k.get("C", C), k.get("D", D), k.get("off", off),
+                                          k.get("perm", perm), k.get("pos0", 0), k.get("n", N),
+                                          k.get("rows", rows), k.get("res", res))
+    assert call() == B.IVF_EDEVICE  # every check passed; no device behind the context
+    assert call(pos0=10, n=N - 10) == B.IVF_EDEVICE
+    assert call(pos0=10, n=N) == B.IVF_EINVAL
+    assert call(pos0=-1, n=1) == B.IVF_EINVAL
+    assert call(n=-1) == B.IVF_EINVAL
+    assert call(n=0) == B.IVF_OK and call(n=0, rows=None, res=None) == B.IVF_OK
+    assert call(rows=None, res=None) == B.IVF_EINVAL
+    assert call(rows=None) == B.IVF_EDEVICE and call(res=None) == B.IVF_EDEVICE
+    assert call(D=18) == B.IVF_EUNSUPPORTED
+    assert call(dt=7) == B.IVF_EINVAL
+    assert call(perm=None) == B.IVF_EINVAL and call(off=None) == B.IVF_EINVAL
+    assert call(rows=P(GB + 64)) == B.IVF_EINVAL  # overlaps the centroids
+    assert call(res=P(4 * GB + 1000)) == B.IVF_EINVAL  # overlaps out_rows
+    assert call(rows=P(4 * GB + 8)) == B.IVF_EINVAL  # misaligned
+    assert call(N=1 << 33, n=1) == B.IVF_EUNSUPPORTED
+
+
 def test_no_cpu_fallback_without_gpu():
     import torch
 
