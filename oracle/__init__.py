@@ -14,7 +14,9 @@ arrays through ctypes. Definitions followed:
 * ``kmeans_update``  Lloyd mean update with deterministic reseed of empty clusters;
 * ``objective``      sum of squared distances of every vector to its assigned centroid;
 * ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation;
-* ``list_major``     list-major copy of the vectors and their residuals x - c(x).
+* ``list_major``     list-major copy of the vectors and their residuals x - c(x);
+* ``pq_encode``      product-quantisation codes (nearest codeword per subspace);
+* ``pq_train_step``  one Lloyd step per subspace codebook.
 
 Parity pins for each function are in ``tests/test_oracle_*.py``.
 """
@@ -74,6 +76,8 @@ def _load():
         lib.oracle_build_lists.argtypes = [p, i64, i64, p, p, p]
         lib.oracle_num_threads.argtypes = [ci]
         lib.oracle_list_major.argtypes = [p, ci, i64, p, i64, ci, p, p, i64, p, p]
+        lib.oracle_pq_encode.argtypes = [p, i64, ci, ci, p, p, ci]
+        lib.oracle_pq_train_step.argtypes = [p, i64, ci, ci, p, u64, i32, p, p, p, ci]
         for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
                   lib.oracle_objective, lib.oracle_kmeans_step, lib.oracle_build_lists,
                   lib.oracle_num_threads):
@@ -208,6 +212,37 @@ def list_major(x, centroids, labels, perm, rows: bool = True, residuals: bool = 
     _check(_load().oracle_list_major(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(lab), _ptr(perm), n,
                                      _ptr(out_rows), _ptr(out_res)), "list_major")
     return out_rows, out_res
+
+
+PQ_K = 256
+
+
+def pq_encode(x, codebooks, nthreads: int = 0):
+    """PQ codes uint8 [N, M] of fp32 vectors x [N, D] with codebooks [M, 256, D/M]."""
+    x = _f32(x)
+    cb = _f32(codebooks)
+    N, D = x.shape
+    M = cb.shape[0]
+    assert cb.shape == (M, PQ_K, D // M)
+    codes = np.empty((N, M), np.uint8)
+    _check(_load().oracle_pq_encode(_ptr(x), N, D, M, _ptr(cb), _ptr(codes), nthreads), "pq_encode")
+    return codes
+
+
+def pq_train_step(x, codebooks, seed: int = 0, it: int = 0, nthreads: int = 0):
+    """One Lloyd step per subspace. Returns (codebooks f32 [M, 256, D/M],
+    counts int64 [M, 256], objectives f64 [M])."""
+    x = _f32(x)
+    cb = _f32(codebooks)
+    N, D = x.shape
+    M = cb.shape[0]
+    assert cb.shape == (M, PQ_K, D // M)
+    out = np.empty_like(cb)
+    cnt = np.empty((M, PQ_K), np.int64)
+    obj = np.zeros(M, np.float64)
+    _check(_load().oracle_pq_train_step(_ptr(x), N, D, M, _ptr(cb), seed & (2**64 - 1), it, _ptr(out),
+                                        _ptr(cnt), _ptr(obj), nthreads), "pq_train_step")
+    return out, cnt, obj
 
 
 def assign_build(x, centroids, nthreads: int = 0):

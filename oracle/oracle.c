@@ -27,6 +27,10 @@
  *   oracle_list_major    list-major copy of the vectors and their residuals
  *                        x - c(x) (Sec. "List-major contiguous scans" and
  *                        Sec. "Residual-PQ Candidate Reduction").
+ *   oracle_pq_encode,    product quantisation of vectors (residuals) and one
+ *   oracle_pq_train_step Lloyd step per subspace codebook (PQ encoding
+ *                        equation, Sec. "ANN Search and IVF"; Sec.
+ *                        "Residual-PQ Candidate Reduction").
  *   oracle_reseed_row    deterministic choice of a training row for an empty
  *                        cluster; the paper is silent, the reading is SplitMix64
  *                        (Steele, Lea & Flood, OOPSLA 2014).
@@ -381,6 +385,71 @@ int oracle_list_major(const void *x, int dtype, int64_t n_rows, const float *cen
         }
     }
     return ORACLE_OK;
+}
+
+/* --------------------------------------------------- product quantisation */
+
+/* Product quantisation (Sec. "ANN Search and IVF", the PQ encoding equation;
+ * applied to residuals in Sec. "Residual-PQ Candidate Reduction"): a vector
+ * of D dims is cut into M sub-vectors of D/M consecutive dims, subspace m
+ * has K = 256 codewords codebooks[m][j][.], and code m of a vector is the
+ * nearest codeword of its sub-vector by (distance, index). Training is one
+ * Lloyd step per subspace on the sub-vectors, exactly oracle_kmeans_step with
+ * seed + m (reseeding an empty codeword of subspace m from the sub-vectors).
+ * Both take the sub-vectors out of x into a contiguous copy first. */
+#define ORACLE_PQ_K 256
+
+static float *pq_slice(const float *x, int64_t n, int D, int m, int dsub)
+{
+    float *s = (float *)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1) * (size_t)dsub);
+    if (!s) return NULL;
+    for (int64_t i = 0; i < n; ++i)
+        for (int d = 0; d < dsub; ++d) s[i * dsub + d] = x[i * D + (int64_t)m * dsub + d];
+    return s;
+}
+
+int oracle_pq_encode(const float *x, int64_t n, int D, int M, const float *codebooks,
+                     uint8_t *out_codes, int nthreads)
+{
+    if (n < 0 || D < 1 || M < 1 || D % M != 0) return ORACLE_EINVAL;
+    const int dsub = D / M;
+    int32_t *lab = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    if (!lab) return ORACLE_EINVAL;
+    int rc = ORACLE_OK;
+    for (int m = 0; m < M && rc == ORACLE_OK; ++m) {
+        float *s = pq_slice(x, n, D, m, dsub);
+        if (!s) { rc = ORACLE_EINVAL; break; }
+        if (n > 0)
+            rc = oracle_assign(s, ORACLE_F32, n, codebooks + (int64_t)m * ORACLE_PQ_K * dsub, ORACLE_PQ_K,
+                               dsub, lab, NULL, nthreads);
+        for (int64_t i = 0; i < n && rc == ORACLE_OK; ++i) out_codes[i * M + m] = (uint8_t)lab[i];
+        free(s);
+    }
+    free(lab);
+    return rc;
+}
+
+int oracle_pq_train_step(const float *x, int64_t n, int D, int M, const float *codebooks,
+                         uint64_t seed, int32_t iter, float *out_codebooks, int64_t *out_counts,
+                         double *out_objective, int nthreads)
+{
+    if (n < 1 || D < 1 || M < 1 || D % M != 0) return ORACLE_EINVAL;
+    const int dsub = D / M;
+    int32_t *lab = (int32_t *)malloc(sizeof(int32_t) * (size_t)n);
+    if (!lab) return ORACLE_EINVAL;
+    int rc = ORACLE_OK;
+    for (int m = 0; m < M && rc == ORACLE_OK; ++m) {
+        float *s = pq_slice(x, n, D, m, dsub);
+        if (!s) { rc = ORACLE_EINVAL; break; }
+        const int64_t cb = (int64_t)m * ORACLE_PQ_K * dsub;
+        rc = oracle_kmeans_step(s, ORACLE_F32, n, codebooks + cb, ORACLE_PQ_K, dsub, seed + (uint64_t)m,
+                                iter, lab, out_codebooks + cb,
+                                out_counts ? out_counts + (int64_t)m * ORACLE_PQ_K : NULL,
+                                out_objective ? out_objective + m : NULL, nthreads);
+        free(s);
+    }
+    free(lab);
+    return rc;
 }
 
 int oracle_num_threads(int nthreads) { return resolve_threads(nthreads); }

@@ -48,6 +48,11 @@ int oracle_build_lists(const int32_t *labels, int64_t n, int64_t nc, int64_t *ou
 int oracle_list_major(const void *x, int dtype, int64_t n_rows, const float *centroids, int64_t nc,
                       int D, const int32_t *labels, const uint32_t *perm, int64_t n,
                       void *out_rows, float *out_res);
+int oracle_pq_encode(const float *x, int64_t n, int D, int M, const float *codebooks,
+                     uint8_t *out_codes, int nthreads);
+int oracle_pq_train_step(const float *x, int64_t n, int D, int M, const float *codebooks,
+                         uint64_t seed, int32_t iter, float *out_codebooks, int64_t *out_counts,
+                         double *out_objective, int nthreads);
 int oracle_num_threads(int nthreads);
 
 #ifdef __cplusplus
