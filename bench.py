@@ -35,6 +35,7 @@ if ROOT not in sys.path:
 
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix peak
 PEAK_HBM_GBS = 8000.0
+PEAK_FP64_VECTOR_TFLOPS = 78.6
 
 
 def parse():
@@ -233,8 +234,10 @@ def main():
         result["cpu_baseline"] = cpu_baseline(x_train, c0, args.cpu_seconds)
 
     if not args.no_extra:
-        result["extra"] = {"route_normalised": bench_route_normalised(ctx),
-                           "list_major": bench_list_major(ctx, x_base, c1, off_b, perm_b)}
+        lm, res = bench_list_major(ctx, x_base, c1, off_b, perm_b)
+        result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm,
+                           "pq": bench_pq(ctx, res)}
+        del res
         if args.build_rows > 0:
             # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
             del x_train, x_base, lab_t, lab_b, perm_b
@@ -327,9 +330,50 @@ def bench_list_major(ctx, x, cent, offsets, perm):
     t = float(np.median(times))
     per_row = D + 4 + D + 4 * D
     gbs = per_row * N / (t * 1e-3) / 1e9
-    del rows, res
-    return {"rows": N, "dim": D, "ms": t, "bytes_per_row": per_row, "GBps": gbs,
-            "hbm_frac": gbs / PEAK_HBM_GBS}
+    del rows
+    return ({"rows": N, "dim": D, "ms": t, "bytes_per_row": per_row, "GBps": gbs,
+             "hbm_frac": gbs / PEAK_HBM_GBS}, res)
+
+
+def bench_pq(ctx, res, M=16, train_rows=1 << 20):
+    """Residual PQ on the list-major residuals (10M x 128, M = 16 subspaces of
+    8 dims, 256 codewords): one codebook training step on the first 1M
+    residuals and the encoding of all of them, median of 3 calls each. The
+    encoding's algorithmic work is 3 flops (subtract, multiply, add) per
+    codeword and dim, in fp64: 3 * 256 * D per row, against the 78.6 TFLOP/s
+    fp64 vector peak."""
+    import numpy as np
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    N, D = res.shape
+    train = res[:train_rows]
+    rng = np.random.default_rng(0)
+    pick = torch.from_numpy(rng.choice(train_rows, 256, replace=False)).to(res.device)
+    cb0 = train[pick].reshape(256, M, D // M).permute(1, 0, 2).contiguous()
+    cb, cnt, obj = ivf.ivf_pq_train_step(ctx, train, cb0, seed=0, it=0)
+    codes = ivf.ivf_pq_encode(ctx, res, cb)
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+        ctx.kernel_times()
+        ts = []
+        for _ in range(3):
+            fn()
+            ts.append(sum(ms for _, ms in ctx.kernel_times()))
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+        return float(np.median(ts))
+
+    t_train = timed(lambda: ivf.ivf_pq_train_step(ctx, train, cb0, seed=0, it=0, out_codebooks=cb,
+                                                  out_counts=cnt, out_objective=obj))
+    t_enc = timed(lambda: ivf.ivf_pq_encode(ctx, res, cb, out_codes=codes))
+    flops = 3.0 * 256 * D * N
+    tf = flops / (t_enc * 1e-3) / 1e12
+    return {"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
+            "encode_ms": t_enc, "encode_rows_per_s": N / (t_enc * 1e-3), "encode_fp64_tflops": tf,
+            "encode_fp64_frac": tf / PEAK_FP64_VECTOR_TFLOPS}
 
 
 def bench_build(ctx, N, C):

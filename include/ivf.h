@@ -67,7 +67,8 @@ typedef enum {
     IVF_OP_ROUTE = 0,
     IVF_OP_KMEANS_STEP = 1,
     IVF_OP_ASSIGN_BUILD = 2,
-    IVF_OP_BUILD_LISTS = 3
+    IVF_OP_BUILD_LISTS = 3,
+    IVF_OP_PQ_TRAIN_STEP = 4
 } ivf_op;
 
 typedef struct ivf_ctx ivf_ctx;
@@ -92,6 +93,7 @@ ivf_status ivf_set_stream(ivf_ctx *ctx, void *hip_stream);
  *   IVF_OP_KMEANS_STEP  rows = N (k ignored)
  *   IVF_OP_ASSIGN_BUILD rows = N (k ignored)
  *   IVF_OP_BUILD_LISTS  rows = N (D, k ignored)
+ *   IVF_OP_PQ_TRAIN_STEP rows = n, C = M (D, k ignored)
  * Returns 0 for sizes that the op rejects. */
 size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k);
 
@@ -212,6 +214,40 @@ ivf_status ivf_list_major(ivf_ctx *ctx, const void *base, int dt, int64_t N,
                           const float *centroids, int64_t C, int32_t D, const int64_t *offsets,
                           const uint32_t *perm, int64_t pos0, int64_t n, void *out_rows,
                           float *out_residuals);
+
+/* Product quantisation (the PQ encoding equation, Sec. "ANN Search and IVF";
+ * applied to the residuals x - c(x), Sec. "Residual-PQ Candidate
+ * Reduction"). A D-dim vector is cut into M sub-vectors of D / M consecutive
+ * dims (M divides D, at most 16 dims per subspace); subspace m has 256
+ * codewords codebooks[m][j][0 .. D/M), fp32, [M, 256, D/M] row-major.
+ *
+ * ivf_pq_encode: out_codes [n, M] uint8, code m of row i = the codeword of
+ * subspace m nearest to sub-vector m of x[i] by (distance, index), the
+ * distance in fp64 as in the exactness contract.
+ *   x [n, D] fp32 (e.g. residuals from ivf_list_major); n == 0 is a no-op.
+ * No workspace. Errors: IVF_EINVAL (M does not divide D, NULL, misaligned,
+ * aliasing), IVF_EUNSUPPORTED (D, more than 16 dims per subspace). */
+ivf_status ivf_pq_encode(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int32_t M,
+                         const float *codebooks, uint8_t *out_codes);
+
+/* One Lloyd iteration of every subspace codebook (codebook training for
+ * residual PQ): subspace m runs exactly the ivf_kmeans_step definition on
+ * the sub-vectors x[.][m D/M .. (m+1) D/M) with 256 centroids and seed + m
+ * (fp64 sums in ascending row order; an empty codeword takes the
+ * sub-vector of the reseed row).
+ *   x              [n, D] fp32, 1 <= n <= 2^32 - 1
+ *   codebooks      [M, 256, D/M] input codebooks
+ *   out_codebooks  [M, 256, D/M], must not alias the input
+ *   out_counts     [M, 256] int64 codeword populations before reseeding,
+ *                  may be NULL
+ *   out_objective  [M] fp64 device array: per subspace, the sum over rows of
+ *                  the squared distance to the assigned input codeword, may
+ *                  be NULL
+ * Workspace: ivf_workspace_bytes(IVF_OP_PQ_TRAIN_STEP, n, M, D, 0).
+ * Errors: as ivf_pq_encode, plus IVF_ENOMEM. */
+ivf_status ivf_pq_train_step(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int32_t M,
+                             const float *codebooks, uint64_t seed, int32_t iter,
+                             float *out_codebooks, int64_t *out_counts, double *out_objective);
 
 /* Measures the fp32 MFMA pipe for reporting: enqueues a probe kernel that
  * runs only v_mfma_f32_32x32x2_f32 (register operands, two waves per SIMD on

@@ -20,6 +20,7 @@ from ._binding import (  # noqa: F401
     IVF_OP_ASSIGN_BUILD,
     IVF_OP_BUILD_LISTS,
     IVF_OP_KMEANS_STEP,
+    IVF_OP_PQ_TRAIN_STEP,
     IVF_OP_ROUTE,
     IVF_OPT_BUILD_BLOCKS,
     IVF_OPT_FORCE_FALLBACK,
@@ -35,6 +36,8 @@ from ._binding import (  # noqa: F401
     ivf_build_lists,
     ivf_kmeans_step,
     ivf_list_major,
+    ivf_pq_encode,
+    ivf_pq_train_step,
     ivf_route,
     load_library,
 )

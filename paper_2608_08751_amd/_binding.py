@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libivf.so")
 
 IVF_OK, IVF_EINVAL, IVF_EUNSUPPORTED, IVF_ENOMEM, IVF_EDEVICE = range(5)
 IVF_F32, IVF_U8 = 0, 1
-IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS = range(4)
+IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS, IVF_OP_PQ_TRAIN_STEP = range(5)
 IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE, IVF_OPT_BUILD_BLOCKS, IVF_OPT_SCREEN_WAVES = range(5)
 
 STATUS_NAMES = {0: "IVF_OK", 1: "IVF_EINVAL", 2: "IVF_EUNSUPPORTED", 3: "IVF_ENOMEM", 4: "IVF_EDEVICE"}
@@ -40,6 +40,8 @@ SIGNATURES = [
     ("ivf_kernel_times", _INT, [_P, _INT, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
     ("ivf_mfma_probe", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
+    ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
 ]
 
 _lib = None
@@ -297,3 +299,47 @@ def ivf_list_major(ctx: Context, base, centroids, offsets, perm, pos0: int = 0, 
                                      _ptr(out_rows if rows else None),
                                      _ptr(out_residuals if residuals else None)), "ivf_list_major")
     return (out_rows if rows else None), (out_residuals if residuals else None)
+
+
+PQ_K = 256
+
+
+def ivf_pq_encode(ctx: Context, x, codebooks, out_codes=None):
+    """PQ codes uint8 [n, M] of fp32 rows x [n, D] with codebooks [M, 256, D/M]."""
+    import torch
+
+    _device_tensor(x, "x")
+    _device_tensor(codebooks, "codebooks")
+    n, D = x.shape
+    M = codebooks.shape[0]
+    if out_codes is None:
+        out_codes = torch.empty((n, M), dtype=torch.uint8, device=x.device)
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_pq_encode(ctx.handle, _ptr(x), n, D, M, _ptr(codebooks), _ptr(out_codes)),
+              "ivf_pq_encode")
+    return out_codes
+
+
+def ivf_pq_train_step(ctx: Context, x, codebooks, seed: int = 0, it: int = 0, out_codebooks=None,
+                      out_counts=None, out_objective=None):
+    """One Lloyd step per subspace: (codebooks [M, 256, D/M], counts int64 [M, 256],
+    objectives fp64 [M])."""
+    import torch
+
+    _device_tensor(x, "x")
+    _device_tensor(codebooks, "codebooks")
+    n, D = x.shape
+    M = codebooks.shape[0]
+    dev = x.device
+    if out_codebooks is None:
+        out_codebooks = torch.empty_like(codebooks)
+    if out_counts is None:
+        out_counts = torch.empty((M, PQ_K), dtype=torch.int64, device=dev)
+    if out_objective is None:
+        out_objective = torch.empty(M, dtype=torch.float64, device=dev)
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_PQ_TRAIN_STEP, n, M, D, 0))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_pq_train_step(ctx.handle, _ptr(x), n, D, M, _ptr(codebooks), seed & (2**64 - 1), it,
+                                        _ptr(out_codebooks), _ptr(out_counts), _ptr(out_objective)),
+              "ivf_pq_train_step")
+    return out_codebooks, out_counts, out_objective

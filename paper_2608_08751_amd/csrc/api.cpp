@@ -198,6 +198,34 @@ struct AssignLayout {
     size_t bytes;
 };
 
+// Product-quantisation training step over M subspaces: labels [M][n], the
+// list build of each subspace's labels (256 lists; one radix scratch reused),
+// counts [M][256], offsets [M][257], permutations [M][n] and the update's
+// objective parts [M][256].
+struct PqLayout {
+    int32_t *labels;
+    void *radix;
+    int64_t *counts;
+    int64_t *offsets;
+    uint32_t *perm;
+    double *jpart;
+    size_t bytes;
+};
+
+PqLayout layout_pq(void *base, int64_t n, int M, int num_cus)
+{
+    Carver c(base);
+    PqLayout l{};
+    l.labels = c.take<int32_t>((size_t)n * M);
+    l.radix = c.take<unsigned char>(radix_scratch_bytes(plan_radix(n, kPqK, num_cus)));
+    l.counts = c.take<int64_t>((size_t)kPqK * M);
+    l.offsets = c.take<int64_t>((size_t)(kPqK + 1) * M);
+    l.perm = c.take<uint32_t>((size_t)n * M);
+    l.jpart = c.take<double>((size_t)kPqK * M);
+    l.bytes = c.off;
+    return l;
+}
+
 // need_lists: counts/offsets/perm live in the workspace (k-means step);
 // need_build: count matrix for the list build.
 AssignLayout layout_assign(void *base, int64_t N, int64_t C, bool need_build, bool need_lists,
@@ -435,6 +463,9 @@ size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
     case IVF_OP_BUILD_LISTS:
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+    case IVF_OP_PQ_TRAIN_STEP:  // C = M
+        if (C > kMaxD) return 0;
+        return layout_pq(nullptr, std::max<int64_t>(rows, 1), (int)C, num_cus).bytes;
     default:
         return 0;
     }
@@ -693,7 +724,7 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
     if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
     int64_t *counts = out_counts ? out_counts : l.counts;
     if ((st = enqueue_build(ctx, N, C, out_labels, l.cntmat, counts, l.offsets, l.perm)) != IVF_OK) return st;
-    TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, centroids, C, counts, l.offsets, l.perm, seed,
+    TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, D, centroids, C, counts, l.offsets, l.perm, seed,
                                  iter, out_centroids, l.jpart, out_objective, ctx->stream));
     return IVF_OK;
 }
@@ -802,6 +833,86 @@ ivf_status ivf_list_major(ivf_ctx *ctx, const void *base, int dt, int64_t N, con
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     TIMED("list_major", launch_list_major(base, rowtype, N, centroids, C, D, offsets, perm, pos0, n,
                                           out_rows, out_residuals, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
+static ivf_status check_pq(ivf_ctx *ctx, int32_t D, int32_t M, int *dsub)
+{
+    ivf_status st = check_common(ctx, kPqK, D);
+    if (st != IVF_OK) return st;
+    if (M < 1 || D % M != 0) return fail(ctx, IVF_EINVAL, "M must divide D (D = %d, M = %d)", D, M);
+    *dsub = D / M;
+    if (*dsub > kPqMaxSubDims)
+        return fail(ctx, IVF_EUNSUPPORTED, "at most %d dims per subspace (D / M = %d)", kPqMaxSubDims, *dsub);
+    return IVF_OK;
+}
+
+ivf_status ivf_pq_encode(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int32_t M,
+                         const float *codebooks, uint8_t *out_codes)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "pq_encode";
+    int dsub = 0;
+    ivf_status st = check_pq(ctx, D, M, &dsub);
+    if (st != IVF_OK) return st;
+    if (n < 0) return fail(ctx, IVF_EINVAL, "n must be >= 0");
+    if (n == 0) return IVF_OK;
+    if (!x || !codebooks || !out_codes) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(x) || !aligned16(codebooks) || !aligned16(out_codes))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t ob = (size_t)n * M;
+    if (overlap(out_codes, ob, x, (size_t)n * D * 4) || overlap(out_codes, ob, codebooks, (size_t)kPqK * D * 4))
+        return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    TIMED("pq_assign", launch_pq_assign(x, n, D, dsub, 0, M, codebooks, out_codes, M, nullptr, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
+ivf_status ivf_pq_train_step(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int32_t M,
+                             const float *codebooks, uint64_t seed, int32_t iter, float *out_codebooks,
+                             int64_t *out_counts, double *out_objective)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "pq_train_step";
+    int dsub = 0;
+    ivf_status st = check_pq(ctx, D, M, &dsub);
+    if (st != IVF_OK) return st;
+    if (n < 1) return fail(ctx, IVF_EINVAL, "n must be >= 1");
+    if (n > (int64_t)UINT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "n must be < 2^32");
+    if (!x || !codebooks || !out_codebooks) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(x) || !aligned16(codebooks) || !aligned16(out_codebooks) ||
+        (out_counts && !aligned16(out_counts)) || (out_objective && !aligned16(out_objective)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const size_t xb = (size_t)n * D * 4, cb = (size_t)kPqK * D * 4;
+    const void *outs[3] = {out_codebooks, out_counts, out_objective};
+    const size_t osz[3] = {cb, (size_t)M * kPqK * 8, (size_t)M * 8};
+    for (int i = 0; i < 3; ++i) {
+        if (overlap(outs[i], osz[i], x, xb) || overlap(outs[i], osz[i], codebooks, cb))
+            return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    }
+    const size_t need = layout_pq(nullptr, n, M, ctx->num_cus).bytes;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    const PqLayout l = layout_pq(ctx->ws, n, M, ctx->num_cus);
+    int64_t *counts = out_counts ? out_counts : l.counts;
+    // every subspace's labels, then each subspace's lists, then one update
+    // launch over all M x 256 codewords (group m = subspace m, seed + m)
+    TIMED("pq_assign", launch_pq_assign(x, n, D, dsub, 0, M, codebooks, nullptr, M, l.labels, ctx->stream));
+    for (int m = 0; m < M; ++m)
+        if ((st = enqueue_build(ctx, n, kPqK, l.labels + (int64_t)m * n, l.radix, counts + (int64_t)m * kPqK,
+                                l.offsets + (int64_t)m * (kPqK + 1), l.perm + (int64_t)m * n)) != IVF_OK)
+            return st;
+    TIMED("pq_update", launch_kmeans_update(x, kRowF32, n, dsub, D, codebooks, kPqK, counts, l.offsets, l.perm,
+                                            seed, iter, out_codebooks, l.jpart, out_objective, ctx->stream, M,
+                                            dsub));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

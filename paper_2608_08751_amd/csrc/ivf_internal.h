@@ -145,16 +145,29 @@ hipError_t launch_radix_level1_scatter(const RadixPlan &p, const RadixScratch &s
 hipError_t launch_offsets(const int64_t *counts, int64_t C, int64_t *offsets, hipStream_t st);
 
 // ---- k-means update (kmeans.hip) --------------------------------------------
-hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
+// `groups` independent problems in one launch (product-quantisation
+// subspaces): group g's rows start g * x_group elements further, its
+// centroids, counts, offsets, permutation and objective parts follow the
+// previous group's, its reseed uses seed + g, and objective[g] gets its sum.
+hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D, int64_t ld,
                                 const float *cent_in, int64_t C, const int64_t *counts,
                                 const int64_t *offsets, const uint32_t *perm, uint64_t seed,
                                 int32_t iter, float *cent_out, double *jpart, double *objective,
-                                hipStream_t s);
+                                hipStream_t s, int groups = 1, int64_t x_group = 0);
 
 // ---- list-major layout and residuals (layout.hip) ----------------------------
 hipError_t launch_list_major(const void *base, int rowtype, int64_t N, const float *cent, int64_t C,
                              int D, const int64_t *offsets, const uint32_t *perm, int64_t pos0,
                              int64_t n, void *out_rows, float *out_res, hipStream_t s);
+
+// ---- product quantisation (pq.hip) ------------------------------------------
+constexpr int kPqK = 256;         // codewords per subspace (8-bit codes)
+constexpr int kPqMaxSubDims = 16; // dims per subspace
+// Nearest codeword of every row in subspaces [m0, m1): codes [n, M] uint8
+// and/or labels [m1 - m0][n] int32.
+hipError_t launch_pq_assign(const float *X, int64_t n, int D, int dsub, int m0, int m1,
+                            const float *codebooks, uint8_t *codes, int M, int32_t *labels,
+                            hipStream_t s);
 
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.

@@ -11,6 +11,9 @@
 // (SplitMix64: Steele, Lea & Flood 2014). The wave also accumulates the
 // squared distances of its rows to the input centroid j; a one-workgroup
 // kernel adds the per-cluster parts in a fixed order into the objective.
+// Rows are D elements at a stride of ld elements (ld = D for whole vectors;
+// a subspace of product quantisation passes its first column and the full
+// row length).
 #include "ivf_internal.h"
 
 namespace ivf {
@@ -36,20 +39,36 @@ template <> struct SumType<float> { typedef double type; };
 
 constexpr int kMaxDimsPerLane = 4;  // D <= 256
 
+// Group g = blockIdx.y is an independent problem (a subspace of product
+// quantisation): its rows start g * gs.x elements further, its centroids
+// g * C * D floats, its counts, offsets and permutation g * C, g * (C + 1)
+// and g * N entries further, and its reseed uses seed + g.
 template <typename XT>
 __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, int64_t N, int D,
+                                                     int64_t ld,
                                                      const float *__restrict__ cin, int64_t C,
                                                      const int64_t *__restrict__ counts,
                                                      const int64_t *__restrict__ offsets,
                                                      const uint32_t *__restrict__ perm,
                                                      uint64_t seed, int32_t iter,
                                                      float *__restrict__ cout,
-                                                     double *__restrict__ jpart)
+                                                     double *__restrict__ jpart, int64_t x_group)
 {
     typedef typename SumType<XT>::type S;
     const int lane = threadIdx.x & 63;
     const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (j >= C) return;
+    {
+        const int64_t g = blockIdx.y;
+        X += g * x_group;
+        cin += g * C * D;
+        cout += g * C * D;
+        counts += g * C;
+        offsets += g * (C + 1);
+        perm += g * N;
+        jpart += g * C;
+        seed += (uint64_t)g;
+    }
     const int64_t n = counts[j];
     const int64_t o = offsets[j];
     S sum[kMaxDimsPerLane];
@@ -64,9 +83,36 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
     for (int64_t t0 = 0; t0 < n; t0 += 64) {
         const int64_t cnt = min((int64_t)64, n - t0);
         const uint32_t myidx = lane < cnt ? perm[o + t0 + lane] : 0u;
-        for (int u = 0; u < cnt; ++u) {
+        int u = 0;
+        // eight member rows in flight, then their values added in row order
+        for (; u + 8 <= cnt; u += 8) {
+            XT v[8][kMaxDimsPerLane];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, u + q);
+                const XT *x = X + i * ld;
+#pragma unroll
+                for (int k = 0; k < kMaxDimsPerLane; ++k) {
+                    const int d = lane + 64 * k;
+                    v[q][k] = d < D ? x[d] : (XT)0;
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+#pragma unroll
+                for (int k = 0; k < kMaxDimsPerLane; ++k) {
+                    const int d = lane + 64 * k;
+                    if (d < D) {
+                        sum[k] += (S)v[q][k];
+                        const double t = (double)v[q][k] - cj[k];
+                        jp = fma(t, t, jp);
+                    }
+                }
+            }
+        }
+        for (; u < cnt; ++u) {
             const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, u);
-            const XT *x = X + i * D;
+            const XT *x = X + i * ld;
 #pragma unroll
             for (int k = 0; k < kMaxDimsPerLane; ++k) {
                 const int d = lane + 64 * k;
@@ -89,7 +135,7 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
             if (n > 0)
                 v = (float)((double)sum[k] / (double)n);
             else
-                v = (float)X[r * D + d];
+                v = (float)X[r * ld + d];
             cout[j * D + d] = v;
         }
     }
@@ -97,10 +143,13 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
     if (lane == 0) jpart[j] = jp;
 }
 
+// Block g adds the C parts of group g in a fixed order into out[g].
 __global__ __launch_bounds__(1024) void sum_parts_kernel(const double *__restrict__ part,
                                                          int64_t C, double *__restrict__ out)
 {
     __shared__ double s[1024];
+    part += (int64_t)blockIdx.x * C;
+    out += blockIdx.x;
     double acc = 0.0;
     for (int64_t j = threadIdx.x; j < C; j += blockDim.x) acc += part[j];
     s[threadIdx.x] = acc;
@@ -114,22 +163,21 @@ __global__ __launch_bounds__(1024) void sum_parts_kernel(const double *__restric
 
 }  // namespace
 
-hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
+hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D, int64_t ld,
                                 const float *cent_in, int64_t C, const int64_t *counts,
                                 const int64_t *offsets, const uint32_t *perm, uint64_t seed,
                                 int32_t iter, float *cent_out, double *jpart, double *objective,
-                                hipStream_t s)
+                                hipStream_t s, int groups, int64_t x_group)
 {
-    const unsigned grid = (unsigned)((C + 3) / 4);
+    const dim3 grid((unsigned)((C + 3) / 4), (unsigned)groups);
     if (rowtype == kRowU8)
-        hipLaunchKernelGGL(update_kernel<uint8_t>, dim3(grid), dim3(256), 0, s,
-                           (const uint8_t *)rows, N, D, cent_in, C, counts, offsets, perm, seed,
-                           iter, cent_out, jpart);
+        hipLaunchKernelGGL(update_kernel<uint8_t>, grid, dim3(256), 0, s, (const uint8_t *)rows, N, D,
+                           ld, cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group);
     else
-        hipLaunchKernelGGL(update_kernel<float>, dim3(grid), dim3(256), 0, s, (const float *)rows,
-                           N, D, cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart);
+        hipLaunchKernelGGL(update_kernel<float>, grid, dim3(256), 0, s, (const float *)rows, N, D, ld,
+                           cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group);
     if (objective)
-        hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(1024), 0, s, jpart, C, objective);
+        hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)groups), dim3(1024), 0, s, jpart, C, objective);
     return hipGetLastError();
 }
 

@@ -187,6 +187,27 @@ def test_list_major_validation(vctx):
     assert call(N=1 << 33, n=1) == B.IVF_EUNSUPPORTED
 
 
+def test_pq_validation(vctx, lib):
+    h = vctx.handle
+    x, cb, out, cnt, obj = P(0), P(GB), P(2 * GB), P(3 * GB), P(4 * GB)
+    assert lib.ivf_pq_encode(h, x, 1000, 128, 16, cb, out) == B.IVF_EDEVICE
+    assert lib.ivf_pq_encode(h, x, 0, 128, 16, cb, out) == B.IVF_OK
+    assert lib.ivf_pq_encode(h, x, 1000, 128, 12, cb, out) == B.IVF_EINVAL  # 12 does not divide 128
+    assert lib.ivf_pq_encode(h, x, 1000, 128, 4, cb, out) == B.IVF_EUNSUPPORTED  # 32 dims per subspace
+    assert lib.ivf_pq_encode(h, x, 1000, 130, 10, cb, out) == B.IVF_EUNSUPPORTED  # D % 4
+    assert lib.ivf_pq_encode(h, x, 1000, 128, 16, None, out) == B.IVF_EINVAL
+    assert lib.ivf_pq_encode(h, x, 1000, 128, 16, cb, P(GB + 128)) == B.IVF_EINVAL  # overlaps codebooks
+    need = lib.ivf_workspace_bytes(B.IVF_OP_PQ_TRAIN_STEP, 1000, 16, 128, 0)
+    assert need > 1000 * 8
+    assert lib.ivf_pq_train_step(h, x, 1000, 128, 16, cb, 0, 0, out, cnt, obj) == B.IVF_ENOMEM
+    assert "workspace" in vctx.error()
+    assert lib.ivf_set_workspace(h, P(8 * GB), need) == B.IVF_OK
+    assert lib.ivf_pq_train_step(h, x, 1000, 128, 16, cb, 0, 0, out, cnt, obj) == B.IVF_EDEVICE
+    assert lib.ivf_pq_train_step(h, x, 1000, 128, 16, cb, 0, 0, out, None, None) == B.IVF_EDEVICE
+    assert lib.ivf_pq_train_step(h, x, 0, 128, 16, cb, 0, 0, out, cnt, obj) == B.IVF_EINVAL
+    assert lib.ivf_pq_train_step(h, x, 1000, 128, 16, cb, 0, 0, cb, cnt, obj) == B.IVF_EINVAL  # aliasing
+
+
 def test_no_cpu_fallback_without_gpu():
     import torch
 
