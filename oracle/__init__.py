@@ -11,6 +11,7 @@ arrays through ctypes. Definitions followed:
 * ``dist``           squared L2, the left-hand side of Eq. (6), evaluated directly;
 * ``route``          coarse search, Eq. (1): nprobe nearest centroids by (distance, id);
 * ``assign``         nearest centroid per vector, ties to the lower id;
+* ``assign_graph``   nearest among each vector's candidate centroids (fast construction);
 * ``kmeans_update``  Lloyd mean update with deterministic reseed of empty clusters;
 * ``objective``      sum of squared distances of every vector to its assigned centroid;
 * ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation;
@@ -77,6 +78,7 @@ def _load():
         lib.oracle_num_threads.argtypes = [ci]
         lib.oracle_list_major.argtypes = [p, ci, i64, p, i64, ci, p, p, i64, p, p]
         lib.oracle_pq_encode.argtypes = [p, i64, ci, ci, p, p, ci]
+        lib.oracle_assign_graph.argtypes = [p, ci, i64, p, i64, ci, p, ci, p, p, p, ci]
         lib.oracle_pq_train_step.argtypes = [p, i64, ci, ci, p, u64, i32, p, p, p, ci]
         for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
                   lib.oracle_objective, lib.oracle_kmeans_step, lib.oracle_build_lists,
@@ -139,6 +141,21 @@ def assign(x, centroids, nthreads: int = 0, return_dist: bool = False):
     labels = np.empty(N, np.int32)
     md = np.empty(N, np.float64) if return_dist else None
     _check(_load().oracle_assign(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(labels), _ptr(md), nthreads), "assign")
+    return (labels, md) if return_dist else labels
+
+
+def assign_graph(x, centroids, graph, prev, nthreads: int = 0, return_dist: bool = False):
+    """Candidate-restricted assignment: row i takes the nearest of the centroids
+    graph[prev[i]] by (distance, id); -1 (distance inf) when it has none."""
+    x, dt = _data(x)
+    c = _f32(centroids)
+    g = np.ascontiguousarray(graph, dtype=np.int32)
+    pv = np.ascontiguousarray(prev, dtype=np.int32)
+    N, D = x.shape
+    labels = np.empty(N, np.int32)
+    md = np.empty(N, np.float64) if return_dist else None
+    _check(_load().oracle_assign_graph(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(g), g.shape[1], _ptr(pv),
+                                       _ptr(labels), _ptr(md), nthreads), "assign_graph")
     return (labels, md) if return_dist else labels
 
 

@@ -24,6 +24,8 @@
  *                        introduction and in "Fast Index Construction").
  *   oracle_build_lists   cluster-major inverted lists with offset, length and
  *                        vector ids (Sec. "System Architecture", index layout).
+ *   oracle_assign_graph  candidate-restricted assignment (fast construction
+ *                        mode, Sec. "Fast Index Construction").
  *   oracle_list_major    list-major copy of the vectors and their residuals
  *                        x - c(x) (Sec. "List-major contiguous scans" and
  *                        Sec. "Residual-PQ Candidate Reduction").
@@ -212,6 +214,62 @@ int oracle_assign(const void *x, int dtype, int64_t n, const float *centroids, i
     if (n == 0) return ORACLE_OK;
     assign_ctx ctx = {x, dtype, centroids, nc, D, out_labels, out_mindist};
     parallel_for(n, nthreads, assign_range, &ctx);
+    return ORACLE_OK;
+}
+
+/* Candidate-restricted assignment (the fast construction mode of Sec. "Fast
+ * Index Construction", which scores every vector against a few candidate
+ * centroids only): the candidates of row i are graph[prev[i]][0 .. S), and
+ * label_i is the candidate of smallest distance by (distance, id). The paper
+ * draws its candidates from a CAGRA search over the centroids; here the
+ * graph is any [nc, S] table of centroid ids (e.g. each centroid's S nearest
+ * centroids) and prev[i] is the row's previous label. Candidate ids outside
+ * [0, nc) are skipped; a row with none gets label -1 and distance +inf. */
+typedef struct {
+    const void *x;
+    int dtype;
+    const float *c;
+    int64_t nc;
+    int D;
+    const int32_t *graph;
+    int S;
+    const int32_t *prev;
+    int32_t *labels;
+    double *mind;
+} graph_ctx;
+
+static void graph_range(void *vctx, int64_t begin, int64_t end)
+{
+    graph_ctx *a = (graph_ctx *)vctx;
+    for (int64_t i = begin; i < end; ++i) {
+        double best = INFINITY;
+        int64_t arg = -1;
+        const int32_t p = a->prev[i];
+        if (p >= 0 && p < a->nc) {
+            for (int s = 0; s < a->S; ++s) {
+                const int64_t j = a->graph[(int64_t)p * a->S + s];
+                if (j < 0 || j >= a->nc) continue;
+                const double d = oracle_dist_row(a->x, a->dtype, i, a->c + j * a->D, a->D);
+                if (arg < 0 || before(d, j, best, arg)) {
+                    best = d;
+                    arg = j;
+                }
+            }
+        }
+        a->labels[i] = (int32_t)arg;
+        if (a->mind) a->mind[i] = best;
+    }
+}
+
+int oracle_assign_graph(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc,
+                        int D, const int32_t *graph, int S, const int32_t *prev,
+                        int32_t *out_labels, double *out_mindist, int nthreads)
+{
+    if (n < 0 || nc < 1 || D < 1 || S < 1 || (dtype != ORACLE_F32 && dtype != ORACLE_U8))
+        return ORACLE_EINVAL;
+    if (n == 0) return ORACLE_OK;
+    graph_ctx ctx = {x, dtype, centroids, nc, D, graph, S, prev, out_labels, out_mindist};
+    parallel_for(n, nthreads, graph_range, &ctx);
     return ORACLE_OK;
 }
 

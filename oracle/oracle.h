@@ -28,6 +28,10 @@ int oracle_route(const float *queries, int64_t nq, const float *centroids, int64
 int oracle_assign(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc, int D,
                   int32_t *out_labels, double *out_mindist, int nthreads);
 
+int oracle_assign_graph(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc,
+                        int D, const int32_t *graph, int S, const int32_t *prev,
+                        int32_t *out_labels, double *out_mindist, int nthreads);
+
 uint64_t oracle_splitmix64_mix(uint64_t z);
 uint64_t oracle_splitmix64_nth(uint64_t seed, uint64_t n);
 int64_t oracle_reseed_row(uint64_t seed, int32_t iter, int64_t j, int64_t n);
