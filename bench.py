@@ -236,7 +236,9 @@ def main():
     if not args.no_extra:
         lm, res = bench_list_major(ctx, x_base, c1, off_b, perm_b)
         result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm,
-                           "pq": bench_pq(ctx, res)}
+                           "pq": bench_pq(ctx, res),
+                           "assign_graph": bench_assign_graph(ctx, x_train, c1, lab_t,
+                                                              kernels["kmeans_step/screen_top1"]["avg_ms"])}
         del res
         if args.build_rows > 0:
             # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
@@ -374,6 +376,45 @@ def bench_pq(ctx, res, M=16, train_rows=1 << 20):
     return {"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
             "encode_ms": t_enc, "encode_rows_per_s": N / (t_enc * 1e-3), "encode_fp64_tflops": tf,
             "encode_fp64_frac": tf / PEAK_FP64_VECTOR_TFLOPS}
+
+
+def bench_assign_graph(ctx, x, cent, prev, full_top1_ms, S=8):
+    """Candidate-restricted assignment (fast construction mode) of the step's
+    10M training rows to the new centroids: the 8-nearest-centroid graph from
+    ivf_route of the centroids against themselves, then each row scored
+    against the 8 neighbours of its previous centroid. Median of 3 calls.
+    HBM bytes per row: the row, its previous label, its label and distance
+    (centroid rows come from the cache)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    N, D = x.shape
+    C = cent.shape[0]
+    graph, _ = ivf.ivf_route(ctx, cent, cent, S, want_dist=False)
+    lab = torch.empty(N, dtype=torch.int32, device=x.device)
+    dist = torch.empty(N, dtype=torch.float32, device=x.device)
+    ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist)
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+        ctx.kernel_times()
+        ts = []
+        for _ in range(3):
+            fn()
+            ts.append(sum(ms for _, ms in ctx.kernel_times()))
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+        return float(np.median(ts))
+
+    t_graph = timed(lambda: ivf.ivf_route(ctx, cent, cent, S, out_ids=graph, want_dist=False))
+    t = timed(lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist))
+    per_row = D + 12
+    gbs = per_row * N / (t * 1e-3) / 1e9
+    return {"rows": N, "centroids": C, "degree": S, "graph_ms": t_graph, "assign_ms": t,
+            "rows_per_s": N / (t * 1e-3), "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+            "speedup_vs_full_assignment": full_top1_ms / t}
 
 
 def bench_build(ctx, N, C):

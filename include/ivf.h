@@ -189,6 +189,26 @@ typedef enum {
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 
+/* Candidate-restricted assignment (the fast construction mode of Sec. "Fast
+ * Index Construction": each vector is scored against a few candidate
+ * centroids only; the paper takes them from a CAGRA search over the
+ * centroids). The candidates of row i are graph[prev[i]][0 .. S): e.g. each
+ * centroid's S nearest centroids (ivf_route of the centroids against
+ * themselves with nprobe = S) and the row's previous label. out_labels[i] is
+ * the candidate of smallest distance by (distance, id), the distance exact as
+ * in the contract above; candidate ids outside [0, C) are skipped, and a row
+ * without any valid candidate (or with prev[i] outside [0, C)) gets -1 and an
+ * infinite distance. The result is exact for the candidate sets, not for the
+ * full centroid table.
+ *   rows       [N, D] fp32 or uint8 (dt), N <= 2^32 - 1
+ *   centroids  [C, D] fp32      graph [C, S] int32, 1 <= S <= 64
+ *   prev       [N] int32        out_labels [N] int32
+ *   out_dist   [N] fp32 squared distance (fp64 rounded), may be NULL
+ * No workspace. Errors: IVF_EINVAL, IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */
+ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
+                            const float *centroids, int64_t C, int32_t D, const int32_t *graph,
+                            int32_t S, const int32_t *prev, int32_t *out_labels, float *out_dist);
+
 /* List-major layout of the base vectors and their residuals (Sec. "List-major
  * contiguous scans": every IVF list is one contiguous range; Sec.
  * "Residual-PQ Candidate Reduction": the residual x - c(x) to the assigned

@@ -33,6 +33,7 @@ from ._binding import (  # noqa: F401
     Context,
     IvfError,
     ivf_assign_build,
+    ivf_assign_graph,
     ivf_build_lists,
     ivf_kmeans_step,
     ivf_list_major,

@@ -41,6 +41,7 @@ SIGNATURES = [
     ("ivf_mfma_probe", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
     ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
 ]
 
@@ -343,3 +344,25 @@ def ivf_pq_train_step(ctx: Context, x, codebooks, seed: int = 0, it: int = 0, ou
                                         _ptr(out_codebooks), _ptr(out_counts), _ptr(out_objective)),
               "ivf_pq_train_step")
     return out_codebooks, out_counts, out_objective
+
+
+def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None, out_dist=None,
+                     want_dist: bool = True):
+    """Nearest of each row's candidates graph[prev[i]] (int32 [C, S]):
+    labels int32 [N] and squared distances fp32 [N]."""
+    import torch
+
+    for t, name in ((rows, "rows"), (centroids, "centroids"), (graph, "graph"), (prev, "prev")):
+        _device_tensor(t, name)
+    N, D = rows.shape
+    C = centroids.shape[0]
+    S = graph.shape[1]
+    if out_labels is None:
+        out_labels = torch.empty(N, dtype=torch.int32, device=rows.device)
+    if want_dist and out_dist is None:
+        out_dist = torch.empty(N, dtype=torch.float32, device=rows.device)
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_assign_graph(ctx.handle, _ptr(rows), _dtype_code(rows), N, _ptr(centroids), C, D,
+                                       _ptr(graph), S, _ptr(prev), _ptr(out_labels),
+                                       _ptr(out_dist if want_dist else None)), "ivf_assign_graph")
+    return out_labels, (out_dist if want_dist else None)

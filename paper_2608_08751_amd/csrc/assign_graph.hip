@@ -1,0 +1,122 @@
+// Candidate-restricted assignment on gfx950 (the fast construction mode of
+// Sec. "Fast Index Construction": every vector is scored against a few
+// candidate centroids instead of all of them). The candidates of row i are
+// graph[prev[i]][0 .. S) (for instance each centroid's S nearest centroids,
+// from ivf_route of the centroids against themselves, and the row's previous
+// label); the label is the candidate of smallest exact distance by
+// (distance, id), the distance evaluated in fp64 exactly as everywhere in
+// this library (t = (double)x_d - (double)c_d; s = fma(t, t, s), d
+// ascending).
+//
+// A row owns a group of SP = next power of two >= S lanes of one wave; lane s
+// of the group evaluates candidate s with one sequential fma chain over the
+// dims (float4 loads of the centroid row; the lanes of a group read the same
+// row addresses, which the memory system merges), and a shuffle butterfly
+// inside the group takes the (distance, id) minimum.
+#include "ivf_internal.h"
+
+#include <limits.h>
+
+namespace ivf {
+namespace {
+
+constexpr int kAgThreads = 256;
+
+__device__ __forceinline__ void load4(const uint8_t *p, float (&v)[4])
+{
+    const uint32_t w = *reinterpret_cast<const uint32_t *>(p);
+    v[0] = (float)(w & 0xFFu);
+    v[1] = (float)((w >> 8) & 0xFFu);
+    v[2] = (float)((w >> 16) & 0xFFu);
+    v[3] = (float)(w >> 24);
+}
+
+__device__ __forceinline__ void load4(const float *p, float (&v)[4])
+{
+    const float4 w = *reinterpret_cast<const float4 *>(p);
+    v[0] = w.x;
+    v[1] = w.y;
+    v[2] = w.z;
+    v[3] = w.w;
+}
+
+template <typename XT>
+__global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
+    const XT *__restrict__ X, int64_t N, const float *__restrict__ cent, int64_t C, int D,
+    const int32_t *__restrict__ graph, int S, int sp_log2, const int32_t *__restrict__ prev,
+    int32_t *__restrict__ labels, float *__restrict__ dist)
+{
+    const int SP = 1 << sp_log2;
+    const int s = threadIdx.x & (SP - 1);
+    const int64_t i = ((int64_t)blockIdx.x * kAgThreads + threadIdx.x) >> sp_log2;
+    double d = __builtin_huge_val();
+    int id = INT_MAX;  // loses every comparison against a real candidate
+    if (i < N && s < S) {
+        const int32_t p = prev[i];
+        const int32_t j = (p >= 0 && p < C) ? graph[(int64_t)p * S + s] : -1;
+        if (j >= 0 && j < C) {
+            const XT *x = X + i * D;
+            const float *c = cent + (int64_t)j * D;
+            double acc = 0.0;
+            for (int k0 = 0; k0 < D; k0 += 32) {
+                // the loads of 32 dims first, then their fma chain in dim order
+                float xv[8][4], cv[8][4];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (k0 + 4 * q < D) {
+                        load4(x + k0 + 4 * q, xv[q]);
+                        load4(c + k0 + 4 * q, cv[q]);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (k0 + 4 * q < D) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const double t = (double)xv[q][e] - (double)cv[q][e];
+                            acc = fma(t, t, acc);
+                        }
+                    }
+                }
+            }
+            d = acc;
+            id = j;
+        }
+    }
+    // (distance, id) minimum over the SP lanes of the row's group
+    for (int off = SP >> 1; off > 0; off >>= 1) {
+        const double od = __shfl_xor(d, off);
+        const int oid = __shfl_xor(id, off);
+        if (od < d || (od == d && oid < id)) {
+            d = od;
+            id = oid;
+        }
+    }
+    if (i < N && s == 0) {
+        const bool none = id == INT_MAX;
+        labels[i] = none ? -1 : id;
+        if (dist) dist[i] = none ? __builtin_huge_valf() : (float)d;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C,
+                               int D, const int32_t *graph, int S, const int32_t *prev, int32_t *labels,
+                               float *dist, hipStream_t s)
+{
+    if (N <= 0) return hipSuccess;
+    int sp_log2 = 0;
+    while ((1 << sp_log2) < S) ++sp_log2;
+    const int64_t threads = N << sp_log2;
+    const unsigned grid = (unsigned)((threads + kAgThreads - 1) / kAgThreads);
+    if (rowtype == kRowU8)
+        hipLaunchKernelGGL(assign_graph_kernel<uint8_t>, dim3(grid), dim3(kAgThreads), 0, s,
+                           (const uint8_t *)rows, N, cent, C, D, graph, S, sp_log2, prev, labels, dist);
+    else
+        hipLaunchKernelGGL(assign_graph_kernel<float>, dim3(grid), dim3(kAgThreads), 0, s,
+                           (const float *)rows, N, cent, C, D, graph, S, sp_log2, prev, labels, dist);
+    return hipGetLastError();
+}
+
+}  // namespace ivf

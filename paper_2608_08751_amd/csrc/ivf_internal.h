@@ -169,6 +169,12 @@ hipError_t launch_pq_assign(const float *X, int64_t n, int D, int dsub, int m0, 
                             const float *codebooks, uint8_t *codes, int M, int32_t *labels,
                             hipStream_t s);
 
+// ---- candidate-restricted assignment (assign_graph.hip) ---------------------
+constexpr int kMaxGraphDegree = 64;
+hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C,
+                               int D, const int32_t *graph, int S, const int32_t *prev, int32_t *labels,
+                               float *dist, hipStream_t s);
+
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.
 hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops);

@@ -208,6 +208,22 @@ def test_pq_validation(vctx, lib):
     assert lib.ivf_pq_train_step(h, x, 1000, 128, 16, cb, 0, 0, cb, cnt, obj) == B.IVF_EINVAL  # aliasing
 
 
+def test_assign_graph_validation(vctx, lib):
+    h = vctx.handle
+    rows, cent, graph, prev, lab, dist = P(0), P(GB), P(2 * GB), P(3 * GB), P(4 * GB), P(5 * GB)
+    ok = lambda **k: lib.ivf_assign_graph(h, k.get("rows", rows), B.IVF_U8, k.get("N", 1000), cent, 100, 128,
+                                          k.get("graph", graph), k.get("S", 8), k.get("prev", prev),
+                                          k.get("lab", lab), k.get("dist", dist))
+    assert ok() == B.IVF_EDEVICE
+    assert ok(dist=None) == B.IVF_EDEVICE
+    assert ok(N=0) == B.IVF_OK
+    assert ok(S=0) == B.IVF_EINVAL and ok(S=65) == B.IVF_EINVAL
+    assert ok(graph=None) == B.IVF_EINVAL and ok(prev=None) == B.IVF_EINVAL and ok(lab=None) == B.IVF_EINVAL
+    assert ok(lab=P(3 * GB + 16)) == B.IVF_EINVAL  # overlaps prev
+    assert ok(dist=P(4 * GB + 64)) == B.IVF_EINVAL  # overlaps the labels
+    assert ok(dist=P(5 * GB + 4)) == B.IVF_EINVAL  # misaligned
+
+
 def test_no_cpu_fallback_without_gpu():
     import torch
 
