@@ -17,7 +17,8 @@ arrays through ctypes. Definitions followed:
 * ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation;
 * ``list_major``     list-major copy of the vectors and their residuals x - c(x);
 * ``pq_encode``      product-quantisation codes (nearest codeword per subspace);
-* ``pq_train_step``  one Lloyd step per subspace codebook.
+* ``pq_train_step``  one Lloyd step per subspace codebook;
+* ``adc_scan``       PQ approximate-distance scan of probed lists, k best per query.
 
 Parity pins for each function are in ``tests/test_oracle_*.py``.
 """
@@ -79,6 +80,7 @@ def _load():
         lib.oracle_list_major.argtypes = [p, ci, i64, p, i64, ci, p, p, i64, p, p]
         lib.oracle_pq_encode.argtypes = [p, i64, ci, ci, p, p, ci]
         lib.oracle_assign_graph.argtypes = [p, ci, i64, p, i64, ci, p, ci, p, p, p, ci]
+        lib.oracle_adc_scan.argtypes = [p, i64, ci, p, i64, p, ci, p, p, p, ci, p, ci, p, p]
         lib.oracle_pq_train_step.argtypes = [p, i64, ci, ci, p, u64, i32, p, p, p, ci]
         for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
                   lib.oracle_objective, lib.oracle_kmeans_step, lib.oracle_build_lists,
@@ -260,6 +262,27 @@ def pq_train_step(x, codebooks, seed: int = 0, it: int = 0, nthreads: int = 0):
     _check(_load().oracle_pq_train_step(_ptr(x), N, D, M, _ptr(cb), seed & (2**64 - 1), it, _ptr(out),
                                         _ptr(cnt), _ptr(obj), nthreads), "pq_train_step")
     return out, cnt, obj
+
+
+def adc_scan(queries, centroids, probes, offsets, perm, codes, codebooks, k: int):
+    """Residual-PQ ADC scan of each query's probed lists: the k smallest
+    (approximate distance, row id) pairs. Returns (ids uint32 [B, k],
+    distances float32 [B, k]); missing entries are 0xFFFFFFFF and inf."""
+    q = _f32(queries)
+    c = _f32(centroids)
+    pr = np.ascontiguousarray(probes, dtype=np.int32)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    pm = np.ascontiguousarray(perm, dtype=np.uint32)
+    cd = np.ascontiguousarray(codes, dtype=np.uint8)
+    cb = _f32(codebooks)
+    B, D = q.shape
+    M = cb.shape[0]
+    assert cd.shape[1] == M and cb.shape == (M, PQ_K, D // M)
+    ids = np.empty((B, k), np.uint32)
+    dd = np.empty((B, k), np.float32)
+    _check(_load().oracle_adc_scan(_ptr(q), B, D, _ptr(c), c.shape[0], _ptr(pr), pr.shape[1], _ptr(off), _ptr(pm),
+                                   _ptr(cd), M, _ptr(cb), k, _ptr(ids), _ptr(dd)), "adc_scan")
+    return ids, dd
 
 
 def assign_build(x, centroids, nthreads: int = 0):

@@ -26,6 +26,10 @@
  *                        vector ids (Sec. "System Architecture", index layout).
  *   oracle_assign_graph  candidate-restricted assignment (fast construction
  *                        mode, Sec. "Fast Index Construction").
+ *   oracle_adc_scan      residual-PQ approximate-distance scan of the probed
+ *                        lists with a bounded handoff (Sec. "Residual-PQ
+ *                        Candidate Reduction", Sec. "Compact PQ-Code
+ *                        Offloading").
  *   oracle_list_major    list-major copy of the vectors and their residuals
  *                        x - c(x) (Sec. "List-major contiguous scans" and
  *                        Sec. "Residual-PQ Candidate Reduction").
@@ -507,6 +511,87 @@ int oracle_pq_train_step(const float *x, int64_t n, int D, int M, const float *c
         free(s);
     }
     free(lab);
+    return rc;
+}
+
+/* ------------------------------------------------ residual-PQ ADC scan */
+
+/* Approximate-distance scan of the probed lists (Sec. "Residual-PQ Candidate
+ * Reduction": lookup table and ADC sum; Sec. "Compact PQ-Code Offloading":
+ * the bounded per-query handoff of N_rerank candidates). For query b and
+ * each probed list l = probes[b][s] (ids outside [0, nc) are skipped):
+ *   r[d]        = q[d] - c_l[d]                      (fp32 subtraction)
+ *   LUT[m][j]   = (float) dist(r^(m), cb[m][j])       (fp64 distance of the
+ *                 contract, rounded to fp32: the paper's fp32 LUTs)
+ *   d~(x)       = ((0 + LUT[0][a_0]) + LUT[1][a_1]) + ... + LUT[M-1][a_M-1]
+ *                 (fp32 additions in subspace order) for every position p of
+ *                 list l, a = codes[p], candidate id = perm[p]
+ * and out_ids/out_dist[b] are the k smallest candidates by (d~, id),
+ * ascending; missing entries are id 0xFFFFFFFF and +inf. */
+typedef struct {
+    float d;
+    uint32_t id;
+} adc_cand;
+
+static int adc_before(const void *pa, const void *pb)
+{
+    const adc_cand *a = (const adc_cand *)pa, *b = (const adc_cand *)pb;
+    if (a->d != b->d) return a->d < b->d ? -1 : 1;
+    return a->id < b->id ? -1 : (a->id > b->id ? 1 : 0);
+}
+
+int oracle_adc_scan(const float *queries, int64_t nq, int D, const float *centroids, int64_t nc,
+                    const int32_t *probes, int P, const int64_t *offsets, const uint32_t *perm,
+                    const uint8_t *codes, int M, const float *codebooks, int k,
+                    uint32_t *out_ids, float *out_dist)
+{
+    if (nq < 0 || D < 1 || nc < 1 || P < 1 || M < 1 || D % M != 0 || k < 1) return ORACLE_EINVAL;
+    const int dsub = D / M;
+    float *r = (float *)malloc(sizeof(float) * (size_t)D);
+    float *lut = (float *)malloc(sizeof(float) * (size_t)M * ORACLE_PQ_K);
+    if (!r || !lut) {
+        free(r);
+        free(lut);
+        return ORACLE_EINVAL;
+    }
+    int rc = ORACLE_OK;
+    for (int64_t b = 0; b < nq && rc == ORACLE_OK; ++b) {
+        int64_t total = 0;
+        for (int s = 0; s < P; ++s) {
+            const int32_t l = probes[b * P + s];
+            if (l >= 0 && l < nc) total += offsets[l + 1] - offsets[l];
+        }
+        adc_cand *cand = (adc_cand *)malloc(sizeof(adc_cand) * (size_t)(total > 0 ? total : 1));
+        if (!cand) {
+            rc = ORACLE_EINVAL;
+            break;
+        }
+        int64_t nc_b = 0;
+        for (int s = 0; s < P; ++s) {
+            const int32_t l = probes[b * P + s];
+            if (l < 0 || l >= nc) continue;
+            for (int d = 0; d < D; ++d) r[d] = queries[b * D + d] - centroids[(int64_t)l * D + d];
+            for (int m = 0; m < M; ++m)
+                for (int j = 0; j < ORACLE_PQ_K; ++j)
+                    lut[m * ORACLE_PQ_K + j] = (float)oracle_dist(
+                        r + m * dsub, codebooks + ((int64_t)m * ORACLE_PQ_K + j) * dsub, dsub);
+            for (int64_t p = offsets[l]; p < offsets[l + 1]; ++p) {
+                float acc = 0.0f;
+                for (int m = 0; m < M; ++m) acc = acc + lut[m * ORACLE_PQ_K + codes[p * M + m]];
+                cand[nc_b].d = acc;
+                cand[nc_b].id = perm[p];
+                ++nc_b;
+            }
+        }
+        qsort(cand, (size_t)nc_b, sizeof(adc_cand), adc_before);
+        for (int t = 0; t < k; ++t) {
+            out_ids[b * k + t] = t < nc_b ? cand[t].id : 0xFFFFFFFFu;
+            out_dist[b * k + t] = t < nc_b ? cand[t].d : INFINITY;
+        }
+        free(cand);
+    }
+    free(r);
+    free(lut);
     return rc;
 }
 

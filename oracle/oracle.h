@@ -57,6 +57,10 @@ int oracle_pq_encode(const float *x, int64_t n, int D, int M, const float *codeb
 int oracle_pq_train_step(const float *x, int64_t n, int D, int M, const float *codebooks,
                          uint64_t seed, int32_t iter, float *out_codebooks, int64_t *out_counts,
                          double *out_objective, int nthreads);
+int oracle_adc_scan(const float *queries, int64_t nq, int D, const float *centroids, int64_t nc,
+                    const int32_t *probes, int P, const int64_t *offsets, const uint32_t *perm,
+                    const uint8_t *codes, int M, const float *codebooks, int k,
+                    uint32_t *out_ids, float *out_dist);
 int oracle_num_threads(int nthreads);
 
 #ifdef __cplusplus
