@@ -235,11 +235,13 @@ def main():
 
     if not args.no_extra:
         lm, res = bench_list_major(ctx, x_base, c1, off_b, perm_b)
-        result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm,
-                           "pq": bench_pq(ctx, res),
+        pq, codes, cb = bench_pq(ctx, res)
+        del res
+        result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm, "pq": pq,
+                           "adc_scan": bench_adc(ctx, queries, c1, ids, off_b, perm_b, codes, cb),
                            "assign_graph": bench_assign_graph(ctx, x_train, c1, lab_t,
                                                               kernels["kmeans_step/screen_top1"]["avg_ms"])}
-        del res
+        del codes
         if args.build_rows > 0:
             # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
             del x_train, x_base, lab_t, lab_b, perm_b
@@ -373,9 +375,37 @@ def bench_pq(ctx, res, M=16, train_rows=1 << 20):
     t_enc = timed(lambda: ivf.ivf_pq_encode(ctx, res, cb, out_codes=codes))
     flops = 3.0 * 256 * D * N
     tf = flops / (t_enc * 1e-3) / 1e12
-    return {"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
-            "encode_ms": t_enc, "encode_rows_per_s": N / (t_enc * 1e-3), "encode_fp64_tflops": tf,
-            "encode_fp64_frac": tf / PEAK_FP64_VECTOR_TFLOPS}
+    return ({"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
+             "encode_ms": t_enc, "encode_rows_per_s": N / (t_enc * 1e-3), "encode_fp64_tflops": tf,
+             "encode_fp64_frac": tf / PEAK_FP64_VECTOR_TFLOPS}, codes, cb)
+
+
+def bench_adc(ctx, queries, cent, probes, offsets, perm, codes, cb, k=512):
+    """Residual-PQ ADC scan of the step's 10,000 routed queries (nprobe 64)
+    over the PQ codes of the 10M list-major base rows, handoff k = 512 per
+    query (the paper's N_rerank): median of 3 calls. Work per query: one
+    M x 256 LUT per probed list and M lookups per code of the probed lists."""
+    import numpy as np
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    Q, P = probes.shape
+    out_ids = torch.empty((Q, k), dtype=torch.int32, device=queries.device)
+    out_d = torch.empty((Q, k), dtype=torch.float32, device=queries.device)
+    ivf.ivf_adc_scan(ctx, queries, cent, probes, offsets, perm, codes, cb, k, out_ids=out_ids, out_dist=out_d)
+    torch.cuda.synchronize()
+    lens = (offsets[1:] - offsets[:-1])[probes.long()].sum().item()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    ts = []
+    for _ in range(3):
+        ivf.ivf_adc_scan(ctx, queries, cent, probes, offsets, perm, codes, cb, k, out_ids=out_ids, out_dist=out_d)
+        ts.append(sum(ms for _, ms in ctx.kernel_times()))
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    t = float(np.median(ts))
+    return {"queries": Q, "nprobe": P, "k": k, "subspaces": codes.shape[1], "codes_scanned": int(lens),
+            "ms": t, "queries_per_s": Q / (t * 1e-3), "codes_per_s": lens / (t * 1e-3)}
 
 
 def bench_assign_graph(ctx, x, cent, prev, full_top1_ms, S=8):

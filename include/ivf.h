@@ -68,7 +68,8 @@ typedef enum {
     IVF_OP_KMEANS_STEP = 1,
     IVF_OP_ASSIGN_BUILD = 2,
     IVF_OP_BUILD_LISTS = 3,
-    IVF_OP_PQ_TRAIN_STEP = 4
+    IVF_OP_PQ_TRAIN_STEP = 4,
+    IVF_OP_ADC_SCAN = 5
 } ivf_op;
 
 typedef struct ivf_ctx ivf_ctx;
@@ -94,6 +95,7 @@ ivf_status ivf_set_stream(ivf_ctx *ctx, void *hip_stream);
  *   IVF_OP_ASSIGN_BUILD rows = N (k ignored)
  *   IVF_OP_BUILD_LISTS  rows = N (D, k ignored)
  *   IVF_OP_PQ_TRAIN_STEP rows = n, C = M (D, k ignored)
+ *   IVF_OP_ADC_SCAN     rows = B queries, C = P probes per query, k = handoff
  * Returns 0 for sizes that the op rejects. */
 size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k);
 
@@ -268,6 +270,37 @@ ivf_status ivf_pq_encode(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int
 ivf_status ivf_pq_train_step(ivf_ctx *ctx, const float *x, int64_t n, int32_t D, int32_t M,
                              const float *codebooks, uint64_t seed, int32_t iter,
                              float *out_codebooks, int64_t *out_counts, double *out_objective);
+
+/* Residual-PQ approximate-distance scan of the probed lists (Sec.
+ * "Residual-PQ Candidate Reduction": per probed list, the query residual
+ * r = q - c_l, lookup tables LUT[m][j] = ||r^(m) - codeword_{m,j}||^2 and
+ * ADC sums; Sec. "Compact PQ-Code Offloading": chunked scan with local
+ * top-K and a hierarchical merge into a bounded handoff of N_rerank = k
+ * candidates per query for exact re-ranking).
+ * Definition: r = q - c_l in fp32; LUT[m][j] = the fp64 distance of the
+ * contract rounded to fp32; for every position p of list l,
+ * d~ = ((0 + LUT[0][a_0]) + LUT[1][a_1]) + ... in fp32 with a = codes[p];
+ * the output is each query's k smallest (d~, perm[p]) pairs, ascending, with
+ * missing entries id 0xFFFFFFFF and distance +inf. Exact: the kernels
+ * reproduce these operations and select by the (d~, id) order.
+ *   queries    [B, D] fp32          centroids [C, D] fp32
+ *   probes     [B, P] int32 list ids (e.g. ivf_route output); ids outside
+ *              [0, C) are skipped; the lists of a query must be distinct
+ *   offsets    [C + 1] int64, perm [N] uint32: the list layout
+ *              (ivf_assign_build)
+ *   codes      [N, M] uint8 PQ codes in list-major order (ivf_pq_encode of
+ *              the ivf_list_major residuals); M divides D, M <= 60
+ *   codebooks  [M, 256, D/M] fp32
+ *   k          handoff per query, 1 <= k <= 1024; P <= 4096
+ *   out_ids    [B, k] uint32 row ids     out_dist [B, k] fp32
+ * Workspace: ivf_workspace_bytes(IVF_OP_ADC_SCAN, B, P, D, k) = 8 B*P*k
+ * bytes (+256): large batches can be scanned in slices of queries.
+ * Errors: IVF_EINVAL, IVF_EUNSUPPORTED (D, M, N), IVF_ENOMEM, IVF_EDEVICE. */
+ivf_status ivf_adc_scan(ivf_ctx *ctx, const float *queries, int64_t B, int32_t D,
+                        const float *centroids, int64_t C, const int32_t *probes, int32_t P,
+                        const int64_t *offsets, const uint32_t *perm, int64_t N,
+                        const uint8_t *codes, int32_t M, const float *codebooks, int32_t k,
+                        uint32_t *out_ids, float *out_dist);
 
 /* Measures the fp32 MFMA pipe for reporting: enqueues a probe kernel that
  * runs only v_mfma_f32_32x32x2_f32 (register operands, two waves per SIMD on

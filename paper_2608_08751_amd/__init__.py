@@ -17,6 +17,7 @@ from ._binding import (  # noqa: F401
     IVF_EUNSUPPORTED,
     IVF_F32,
     IVF_OK,
+    IVF_OP_ADC_SCAN,
     IVF_OP_ASSIGN_BUILD,
     IVF_OP_BUILD_LISTS,
     IVF_OP_KMEANS_STEP,
@@ -33,6 +34,7 @@ from ._binding import (  # noqa: F401
     Context,
     IvfError,
     ivf_assign_build,
+    ivf_adc_scan,
     ivf_assign_graph,
     ivf_build_lists,
     ivf_kmeans_step,

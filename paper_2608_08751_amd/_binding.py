@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libivf.so")
 
 IVF_OK, IVF_EINVAL, IVF_EUNSUPPORTED, IVF_ENOMEM, IVF_EDEVICE = range(5)
 IVF_F32, IVF_U8 = 0, 1
-IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS, IVF_OP_PQ_TRAIN_STEP = range(5)
+IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS, IVF_OP_PQ_TRAIN_STEP, IVF_OP_ADC_SCAN = range(6)
 IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE, IVF_OPT_BUILD_BLOCKS, IVF_OPT_SCREEN_WAVES = range(5)
 
 STATUS_NAMES = {0: "IVF_OK", 1: "IVF_EINVAL", 2: "IVF_EUNSUPPORTED", 3: "IVF_ENOMEM", 4: "IVF_EDEVICE"}
@@ -42,6 +42,7 @@ SIGNATURES = [
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
+    ("ivf_adc_scan", _INT, [_P, _P, _I64, _I32, _P, _I64, _P, _I32, _P, _P, _I64, _P, _I32, _P, _I32, _P, _P]),
     ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
 ]
 
@@ -366,3 +367,29 @@ def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None
                                        _ptr(graph), S, _ptr(prev), _ptr(out_labels),
                                        _ptr(out_dist if want_dist else None)), "ivf_assign_graph")
     return out_labels, (out_dist if want_dist else None)
+
+
+def ivf_adc_scan(ctx: Context, queries, centroids, probes, offsets, perm, codes, codebooks, k: int,
+                 out_ids=None, out_dist=None):
+    """Residual-PQ ADC scan: each query's k best (approximate distance, row id)
+    over its probed lists. Returns (ids [B, k] uint32 bits in int32, dist [B, k])."""
+    import torch
+
+    for t, name in ((queries, "queries"), (centroids, "centroids"), (probes, "probes"), (offsets, "offsets"),
+                    (perm, "perm"), (codes, "codes"), (codebooks, "codebooks")):
+        _device_tensor(t, name)
+    B, D = queries.shape
+    C = centroids.shape[0]
+    P = probes.shape[1]
+    N, M = codes.shape
+    dev = queries.device
+    if out_ids is None:
+        out_ids = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if out_dist is None:
+        out_dist = torch.empty((B, k), dtype=torch.float32, device=dev)
+    ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_ADC_SCAN, B, P, D, k))
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_adc_scan(ctx.handle, _ptr(queries), B, D, _ptr(centroids), C, _ptr(probes), P,
+                                   _ptr(offsets), _ptr(perm), N, _ptr(codes), M, _ptr(codebooks), k,
+                                   _ptr(out_ids), _ptr(out_dist)), "ivf_adc_scan")
+    return out_ids, out_dist

@@ -463,6 +463,9 @@ size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
     case IVF_OP_BUILD_LISTS:
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+    case IVF_OP_ADC_SCAN:  // rows = B, C = P (probes per query), k = handoff
+        if (k < 1 || k > kAdcMaxK || C > kMaxAdcProbes) return 0;
+        return (size_t)rows * (size_t)C * (size_t)k * sizeof(uint64_t) + 256;
     case IVF_OP_PQ_TRAIN_STEP:  // C = M
         if (C > kMaxD) return 0;
         return layout_pq(nullptr, std::max<int64_t>(rows, 1), (int)C, num_cus).bytes;
@@ -868,6 +871,51 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N, c
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     TIMED("assign_graph", launch_assign_graph(rows, rowtype, N, centroids, C, D, graph, S, prev, out_labels,
                                               out_dist, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
+ivf_status ivf_adc_scan(ivf_ctx *ctx, const float *queries, int64_t B, int32_t D, const float *centroids,
+                        int64_t C, const int32_t *probes, int32_t P, const int64_t *offsets,
+                        const uint32_t *perm, int64_t N, const uint8_t *codes, int32_t M,
+                        const float *codebooks, int32_t k, uint32_t *out_ids, float *out_dist)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "adc_scan";
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    if (B < 0 || N < 0) return fail(ctx, IVF_EINVAL, "B and N must be >= 0");
+    if (N > (int64_t)UINT32_MAX) return fail(ctx, IVF_EUNSUPPORTED, "N must be < 2^32");
+    if (M < 1 || D % M != 0) return fail(ctx, IVF_EINVAL, "M must divide D (D = %d, M = %d)", D, M);
+    if (M > kAdcMaxM) return fail(ctx, IVF_EUNSUPPORTED, "at most %d subspaces", kAdcMaxM);
+    if (P < 1 || P > kMaxAdcProbes) return fail(ctx, IVF_EINVAL, "P must be in [1, %d]", kMaxAdcProbes);
+    if (k < 1 || k > kAdcMaxK) return fail(ctx, IVF_EINVAL, "k must be in [1, %d]", kAdcMaxK);
+    if (B == 0) return IVF_OK;
+    if (!queries || !centroids || !probes || !offsets || !codebooks || !out_ids || !out_dist ||
+        (N > 0 && (!perm || !codes)))
+        return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(queries) || !aligned16(centroids) || !aligned16(probes) || !aligned16(offsets) ||
+        (perm && !aligned16(perm)) || (codes && !aligned16(codes)) || !aligned16(codebooks) ||
+        !aligned16(out_ids) || !aligned16(out_dist))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const void *ins[7] = {queries, centroids, probes, offsets, perm, codes, codebooks};
+    const size_t ib[7] = {(size_t)B * D * 4, (size_t)C * D * 4, (size_t)B * P * 4, (size_t)(C + 1) * 8,
+                          (size_t)N * 4, (size_t)N * M, (size_t)kPqK * D * 4};
+    const void *outs[2] = {out_ids, out_dist};
+    const size_t ob = (size_t)B * k * 4;
+    for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 7; ++j)
+            if (overlap(outs[i], ob, ins[j], ib[j])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+    if (overlap(out_ids, ob, out_dist, ob)) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    const size_t need = (size_t)B * P * k * sizeof(uint64_t) + 256;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    Carver c(ctx->ws);
+    uint64_t *handoff = c.take<uint64_t>((size_t)B * P * k);
+    TIMED("adc_scan", launch_adc_scan(queries, B, D, centroids, C, probes, P, offsets, perm, N, codes, M,
+                                      codebooks, k, handoff, out_ids, out_dist, ctx->stream));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

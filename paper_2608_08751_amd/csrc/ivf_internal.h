@@ -175,6 +175,16 @@ hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const f
                                int D, const int32_t *graph, int S, const int32_t *prev, int32_t *labels,
                                float *dist, hipStream_t s);
 
+// ---- residual-PQ ADC scan (adc.hip) -----------------------------------------
+constexpr int kAdcMaxK = 1024;   // handoff per query (N_rerank)
+constexpr int kAdcMaxM = 60;     // subspaces (LUT of M x 256 floats in LDS, < 64 KiB)
+constexpr int kMaxAdcProbes = 4096;
+// handoff: [B * P * k] uint64 workspace; ids/dist [B, k].
+hipError_t launch_adc_scan(const float *Q, int64_t B, int D, const float *cent, int64_t C,
+                           const int32_t *probes, int P, const int64_t *offsets, const uint32_t *perm,
+                           int64_t N, const uint8_t *codes, int M, const float *codebooks, int k,
+                           uint64_t *handoff, uint32_t *ids, float *dist, hipStream_t s);
+
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.
 hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops);

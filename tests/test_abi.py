@@ -224,6 +224,27 @@ def test_assign_graph_validation(vctx, lib):
     assert ok(dist=P(5 * GB + 4)) == B.IVF_EINVAL  # misaligned
 
 
+def test_adc_scan_validation(vctx, lib):
+    h = vctx.handle
+    q, c, pr, off, perm, codes, cb, ids, dist = (P(i * GB) for i in range(9))
+    call = lambda **a: lib.ivf_adc_scan(h, q, a.get("B", 100), 128, c, 1000, pr, a.get("P", 64), off, perm,
+                                        a.get("N", 100000), codes, a.get("M", 16), cb, a.get("k", 512),
+                                        a.get("ids", ids), a.get("dist", dist))
+    need = lib.ivf_workspace_bytes(B.IVF_OP_ADC_SCAN, 100, 64, 128, 512)
+    assert need == 100 * 64 * 512 * 8 + 256
+    assert lib.ivf_workspace_bytes(B.IVF_OP_ADC_SCAN, 100, 64, 128, 2000) == 0
+    assert call() == B.IVF_ENOMEM
+    assert lib.ivf_set_workspace(h, P(20 * GB), need) == B.IVF_OK
+    assert call() == B.IVF_EDEVICE
+    assert call(B=0) == B.IVF_OK
+    assert call(k=0) == B.IVF_EINVAL and call(k=1025) == B.IVF_EINVAL
+    assert call(P=0) == B.IVF_EINVAL
+    assert call(M=12) == B.IVF_EINVAL and call(M=64) == B.IVF_EUNSUPPORTED
+    assert call(N=1 << 33) == B.IVF_EUNSUPPORTED
+    assert call(ids=None) == B.IVF_EINVAL
+    assert call(dist=P(7 * GB + 64)) == B.IVF_EINVAL  # overlaps the ids
+
+
 def test_no_cpu_fallback_without_gpu():
     import torch
 
