@@ -167,7 +167,8 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
  *   out[2] route: sum over queries of screened candidates kept
  *   out[3] route: queries whose candidate list overflowed
  *   out[4] route: centroids in the threshold sample
- *   out[5..7] reserved (0) */
+ *   out[5] assignment of uint8 rows: 1 when screened on int8 MFMA
+ *   out[6..7] reserved (0) */
 ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
 
 /* Test, tuning and profiling knobs (values persist on the context):
@@ -179,15 +180,21 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *                           around every kernel launch of each call
  *   IVF_OPT_BUILD_BLOCKS    cap on the row blocks of the single-pass list build
  *                           (more than 65,536 lists; 0 = default); speed only
- *   IVF_OPT_SCREEN_WAVES    wave64s per workgroup of the distance-screening
- *                           kernel, 4 or 8 (D > 128 always uses 4); speed
- *                           only, never results */
+ *   IVF_OPT_SCREEN_WAVES    wave64s per workgroup of the fp32 distance-
+ *                           screening kernel, 4 or 8 (D > 128 always uses 4);
+ *                           speed only, never results
+ *   IVF_OPT_FP32_SCREEN     1 = uint8 rows are screened on fp32 MFMA like
+ *                           fp32 rows (default 0: int8 MFMA whenever every
+ *                           centroid coordinate c has rint(256 (c - 128)) in
+ *                           [-32768, 32767], i.e. c in [0, 255.998]);
+ *                           speed only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,
     IVF_OPT_PROFILE = 2,
     IVF_OPT_BUILD_BLOCKS = 3,
-    IVF_OPT_SCREEN_WAVES = 4
+    IVF_OPT_SCREEN_WAVES = 4,
+    IVF_OPT_FP32_SCREEN = 5
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

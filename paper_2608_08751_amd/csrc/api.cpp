@@ -29,6 +29,7 @@ struct ivf_ctx {
     int sample_rank = 0;
     int build_blocks = 0;
     int screen_waves = 8;
+    int fp32_screen = 0;  // 1: uint8 rows also take the fp32 MFMA screen
     unsigned long long *last_stats = nullptr;  // device, inside the workspace
     int64_t last_sample = 0;
     // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
@@ -77,7 +78,8 @@ struct Carver {
 };
 
 // Scalar area at the start of every workspace: [0] max centroid norm bits,
-// [1] worklist counter, then kNumStats uint64 counters.
+// [1] worklist counter, [2] nonzero when some centroid does not quantise for
+// the int8 screen, then (from word 16) kNumStats uint64 counters.
 struct Scalars {
     uint32_t *mc2_bits;
     uint32_t *wl_cnt;
@@ -100,6 +102,14 @@ int padded_dim(int D)
     for (int dp : dps)
         if (D <= dp) return dp;
     return 0;
+}
+
+// Padded dimension of the quantised centroids kept for the int8 screen (the
+// largest when D is not a supported size: such calls fail validation anyway).
+int quant_dim(int D)
+{
+    const int dp = padded_dim(D);
+    return dp > 0 ? dp : 256;
 }
 
 double bound_coef(int DP)
@@ -187,6 +197,9 @@ int64_t worklist_cap(int64_t N) { return std::min<int64_t>(N, 4096 + N / 64); }
 struct AssignLayout {
     Scalars sc;
     float *cnorm;
+    // quantised centroids of the int8 screen (uint8 rows)
+    int8_t *qc;
+    int32_t *negb;
     int32_t *wl;
     int64_t wl_cap;
     // build
@@ -227,14 +240,19 @@ PqLayout layout_pq(void *base, int64_t n, int M, int num_cus)
 }
 
 // need_lists: counts/offsets/perm live in the workspace (k-means step);
-// need_build: count matrix for the list build.
-AssignLayout layout_assign(void *base, int64_t N, int64_t C, bool need_build, bool need_lists,
+// need_build: count matrix for the list build; qdp > 0: quantised centroids
+// of padded dimension qdp for the int8 screen.
+AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_build, bool need_lists,
                            int num_cus)
 {
     Carver c(base);
     AssignLayout l{};
     l.sc = take_scalars(c);
     l.cnorm = c.take<float>(C);
+    if (qdp > 0) {
+        l.qc = c.take<int8_t>((size_t)quantized_pad(C) * 2 * qdp);
+        l.negb = c.take<int32_t>(quantized_pad(C));
+    }
     l.wl_cap = worklist_cap(N);
     l.wl = c.take<int32_t>(l.wl_cap);
     if (need_build) {
@@ -368,6 +386,29 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     a.wl_cap = l.wl_cap;
     a.stats = l.sc.stats;
     a.force_fallback = ctx->force_fallback;
+    if (rowtype == kRowU8 && !ctx->fp32_screen) {
+        // int8 MFMA screen; the fp32 kernel runs only if some centroid does not quantise
+        uint32_t *q_bad = l.sc.mc2_bits + 2;
+        TIMED("quantize", launch_quantize_centroids(cent, C, D, DP, l.qc, l.negb, q_bad, s));
+        ScreenI8Args q{};
+        q.rows = (const uint8_t *)rows;
+        q.nrows = N;
+        q.D = D;
+        q.cent = cent;
+        q.qc = l.qc;
+        q.negb = l.negb;
+        q.cpad = quantized_pad(C);
+        q.nchunks = q.cpad / 64;
+        q.q_bad = q_bad;
+        q.labels = labels;
+        q.wl = l.wl;
+        q.wl_cnt = l.sc.wl_cnt;
+        q.wl_cap = l.wl_cap;
+        q.stats = l.sc.stats;
+        q.force_fallback = ctx->force_fallback;
+        TIMED("screen_top1_i8", launch_screen_i8(DP, q, 8, ctx->num_cus, s));
+        a.gate = q_bad;
+    }
     TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));
     TIMED("assign_fallback", launch_assign_fallback(rows, rowtype, N, D, cent, C, labels, l.wl, l.sc.wl_cnt, l.wl_cap,
                                    2 * ctx->num_cus, s));
@@ -446,7 +487,6 @@ ivf_status ivf_set_stream(ivf_ctx *ctx, void *hip_stream)
 size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k)
 {
     if (C < 1 || rows < 0) return 0;
-    (void)D;
     int num_cus = 256;
     int dev;
     hipDeviceProp_t prop;
@@ -458,11 +498,11 @@ size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k
         if (k < 1) return 0;
         return layout_route(nullptr, plan_route(rows, C, k, 0), C).bytes;
     case IVF_OP_KMEANS_STEP:
-        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, true, num_cus).bytes;
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, quant_dim(D), true, true, num_cus).bytes;
     case IVF_OP_ASSIGN_BUILD:
-        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, quant_dim(D), true, false, num_cus).bytes;
     case IVF_OP_BUILD_LISTS:
-        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, true, false, num_cus).bytes;
+        return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, 0, true, false, num_cus).bytes;
     case IVF_OP_ADC_SCAN:  // rows = B, C = P (probes per query), k = handoff
         if (k < 1 || k > kAdcMaxK || C > kMaxAdcProbes) return 0;
         return (size_t)rows * (size_t)C * (size_t)k * sizeof(uint64_t) + 256;
@@ -508,6 +548,7 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
         if (value != 4 && value != 8) return fail(ctx, IVF_EINVAL, "screen waves must be 4 or 8");
         ctx->screen_waves = (int)value;
         return IVF_OK;
+    case IVF_OPT_FP32_SCREEN: ctx->fp32_screen = value ? 1 : 0; return IVF_OK;
     case IVF_OPT_BUILD_BLOCKS:
         if (value < 0 || value > 65536) return fail(ctx, IVF_EINVAL, "build blocks out of range");
         ctx->build_blocks = (int)value;
@@ -717,12 +758,12 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
         for (int j = i + 1; j < 4; ++j)
             if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
     }
-    const size_t need = layout_assign(nullptr, N, C, true, true, ctx->num_cus).bytes;
+    const size_t need = layout_assign(nullptr, N, C, quant_dim(D), true, true, ctx->num_cus).bytes;
     if ((st = check_ws(ctx, need)) != IVF_OK) return st;
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
 
-    const AssignLayout l = layout_assign(ctx->ws, N, C, true, true, ctx->num_cus);
+    const AssignLayout l = layout_assign(ctx->ws, N, C, quant_dim(D), true, true, ctx->num_cus);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
     int64_t *counts = out_counts ? out_counts : l.counts;
@@ -757,12 +798,12 @@ ivf_status ivf_assign_build(ivf_ctx *ctx, const void *base, int dt, int64_t N,
         for (int j = i + 1; j < 4; ++j)
             if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
     }
-    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus).bytes;
+    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, quant_dim(D), true, false, ctx->num_cus).bytes;
     if ((st = check_ws(ctx, need)) != IVF_OK) return st;
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
 
-    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
+    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, quant_dim(D), true, false, ctx->num_cus);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     if (N > 0 && (st = enqueue_assign(ctx, base, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK)
         return st;
@@ -793,12 +834,12 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
         for (int j = i + 1; j < 3; ++j)
             if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
     }
-    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus).bytes;
+    const size_t need = layout_assign(nullptr, std::max<int64_t>(N, 1), C, 0, true, false, ctx->num_cus).bytes;
     ivf_status st;
     if ((st = check_ws(ctx, need)) != IVF_OK) return st;
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
-    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, true, false, ctx->num_cus);
+    const AssignLayout l = layout_assign(ctx->ws, std::max<int64_t>(N, 1), C, 0, true, false, ctx->num_cus);
     if ((st = enqueue_build(ctx, N, C, labels, l.cntmat, out_counts, out_offsets, out_perm)) != IVF_OK) return st;
     ctx->last_stats = nullptr;
     return IVF_OK;

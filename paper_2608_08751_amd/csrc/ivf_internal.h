@@ -24,6 +24,7 @@ enum StatSlot {
     kStatCandidates = 2,
     kStatOverflow = 3,
     kStatSample = 4,
+    kStatScreenI8 = 5,  // 1 when the uint8 rows were screened on int8 MFMA
     kNumStats = 8
 };
 
@@ -52,11 +53,39 @@ struct ScreenArgs {
     int64_t wl_cap;
     unsigned long long *stats;
     int force_fallback;
+    // top-1 only: when non-null and *gate == 0, the int8 screen has taken the
+    // call and this kernel returns at once
+    const uint32_t *gate;
 };
 
 // waves: 4 or 8 per workgroup; the grid fills every CU with two waves per SIMD.
 hipError_t launch_screen(int mode, int rowtype, int DP, const ScreenArgs &a, int waves, int num_cus,
                          hipStream_t s);
+
+// ---- int8 screening of uint8 rows (screen_i8.hip) ---------------------------
+// Quantised centroids: qc [cpad][2 * DP] int8 (plane H, then plane Ls), negb
+// [cpad] int32 (-B); cpad = C rounded up to 64, the padding scores lowest.
+struct ScreenI8Args {
+    const uint8_t *rows;   // [nrows, D]
+    int64_t nrows;
+    int D;
+    const float *cent;     // [C, D] (exact re-evaluation)
+    const int8_t *qc;
+    const int32_t *negb;
+    int64_t cpad;
+    int64_t nchunks;       // cpad / 64
+    const uint32_t *q_bad; // nonzero: some centroid did not quantise, fp32 takes over
+    int32_t *labels;
+    int32_t *wl;
+    uint32_t *wl_cnt;
+    int64_t wl_cap;
+    unsigned long long *stats;
+    int force_fallback;
+};
+int64_t quantized_pad(int64_t C);
+hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
+                                     uint32_t *q_bad, hipStream_t s);
+hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int waves, int num_cus, hipStream_t s);
 
 // ---- norms, selection, fallbacks (select.hip) -----------------------------
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);

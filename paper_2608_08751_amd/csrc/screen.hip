@@ -19,6 +19,7 @@
 // the 32x32 accumulator: lane l holds column l % 32 (one row x), register r
 // holds centroid 8*(r/4) + 4*(l/32) + r%4 of the block.
 #include "ivf_internal.h"
+#include "exact.h"
 
 #include <math.h>
 
@@ -34,24 +35,6 @@ constexpr float kInf = __builtin_huge_valf();
 __device__ __forceinline__ bool key_lt(float ka, int ia, float kb, int ib)
 {
     return ka < kb || (ka == kb && ia < ib);
-}
-
-__device__ __forceinline__ bool dist_lt(double da, int ia, double db, int ib)
-{
-    return da < db || (da == db && ia < ib);
-}
-
-template <typename XT>
-__device__ __forceinline__ double exact_dist(const XT *__restrict__ x, const float *__restrict__ c,
-                                             int D)
-{
-    double s = 0.0;
-#pragma unroll 1
-    for (int d = 0; d < D; ++d) {
-        const double t = (double)x[d] - (double)c[d];
-        s = fma(t, t, s);
-    }
-    return s;
 }
 
 // Lane's half-row as fp32 B fragments: b[s] = x[row][h*KH + s], zero padded.
@@ -560,6 +543,7 @@ __global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(Sc
     __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
     const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
     if constexpr (MODE == kModeTop1) {
+        if (a.gate && *a.gate == 0u) return;  // screened on int8 MFMA instead
         for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
             screen_top1<DP, W, XT>(a, tile, lds_c, lds_n);
             __syncthreads();

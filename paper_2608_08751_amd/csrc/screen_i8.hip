@@ -1,0 +1,517 @@
+// Nearest-centroid screening of uint8 rows on int8 MFMA (gfx950).
+//
+// The assignment step of Lloyd's iteration and of the base-vector assignment
+// (Sec. "Fast Index Construction") needs, per row x, the centroid c of least
+// ||x - c||^2. With x' = x - 128 and c' = c - 128 the distance is
+// ||x'||^2 + k(c) with k(c) = ||c'||^2 - 2 x'.c', so the nearest centroid is
+// the one of least k. Rows are integers in [0, 255], so x' is exact in int8;
+// centroids are quantised once per call to 16-bit fixed point,
+//     P = rint(256 c')  (-32768 <= P <= 32767),  P = 256 H + (Ls + 128),
+// with H = floor(P / 256) and Ls = (P mod 256) - 128 both in [-128, 127].
+// Two int8 MFMA products give exact int32 sums x'.H and x'.Ls, and the
+// screening score of a centroid is the exact integer
+//     s(c) = 256 x'.H + x'.Ls - B,   B = rint(128 ||c'||^2),
+// which equals -128 k(c) up to a per-row constant and an error e(c) with
+//     |e(c)| <= |128 ||c'||^2 - B| + sum_d |x'_d| |256 c'_d - P_d|
+//            <  1 + ||x'||_1 / 2 =: R - 1.
+// If the best score beats the second by more than 2R, its centroid is the
+// unique nearest; if it beats the third by more than 2R, the nearest is one of
+// the two best and an exact fp64 evaluation of both decides with the
+// (distance, id) order; otherwise the row goes to the exact fallback scan.
+// Labels therefore equal those of the fp64 definition, while the contraction
+// runs on int8 MFMA (v_mfma_i32_32x32x32_i8) instead of fp32 MFMA.
+//
+// Centroids whose quantisation would overflow (a coordinate c with
+// rint(256 (c - 128)) outside [-32768, 32767], i.e. roughly c outside
+// [0, 255.998], or a non-finite value) set a device flag; this kernel then does nothing and the
+// fp32 screening kernel, which reads the same flag, takes the call.
+//
+// MFMA operands: A = 32 centroids of a staged chunk (lane l supplies centroid
+// l % 32, bytes 16 (l / 32) .. +15 of a 32-byte K-step), B = 32 rows held in
+// registers (same byte mapping); accumulator register r of lane l holds
+// centroid 8 (r / 4) + 4 (l / 32) + r % 4 of the block for row l % 32.
+#include "exact.h"
+#include "ivf_internal.h"
+
+#include <algorithm>
+
+namespace ivf {
+namespace {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kQChunk = 64;          // centroids per staged chunk
+constexpr int kNoScore = INT32_MIN;  // score of a padded centroid (below any real score)
+
+// Row blocks of 32 rows per wave: two for DP <= 128 (each staged centroid
+// fragment then feeds two MFMAs), one above (register budget).
+template <int DP>
+constexpr int rows_blocks()
+{
+    return DP <= 128 ? 2 : 1;
+}
+
+// ------------------------------------------------------------ quantisation
+// One wave per centroid (grid-stride). Writes the two planes [H | Ls] of
+// DP bytes each (zero beyond D), the bias -B, and raises *q_bad on any value
+// that does not fit. Centroids C .. Cpad-1 are padding: zero planes and the
+// lowest score.
+__global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__ cent, int64_t C, int D,
+                                                       int DP, int64_t Cpad, int8_t *__restrict__ qc,
+                                                       int32_t *__restrict__ negb, uint32_t *__restrict__ q_bad)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t j = w0; j < Cpad; j += nw) {
+        double n2 = 0.0;
+        bool bad = false;
+        int8_t *q = qc + j * 2 * DP;
+        for (int d = lane; d < DP; d += 64) {
+            int hb = 0, lb = 0;
+            if (j < C && d < D) {
+                const double cp = (double)cent[j * D + d] - 128.0;
+                const double p = rint(256.0 * cp);
+                if (!(p >= -32768.0 && p <= 32767.0)) {  // also true for NaN
+                    bad = true;
+                } else {
+                    const int P = (int)p;
+                    const int H = P >> 8;  // floor(P / 256)
+                    hb = H;
+                    lb = P - 256 * H - 128;
+                    n2 = fma(cp, cp, n2);
+                }
+            }
+            q[d] = (int8_t)hb;
+            q[DP + d] = (int8_t)lb;
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) n2 += __shfl_xor(n2, o);
+        if (__any(bad) && lane == 0) *q_bad = 1u;
+        if (lane == 0) negb[j] = j < C ? -(int32_t)llrint(128.0 * n2) : kNoScore;
+    }
+}
+
+// ------------------------------------------------------------ staging
+// A chunk of kQChunk quantised centroids (both planes) and their biases,
+// copied from the padded global arrays into LDS with a row pitch of
+// 2 DP + 16 bytes (the 16 spread the rows over the banks). Loads go through a
+// buffer resource over the chunk, so the chunk after the last one reads
+// zeros and every load stays unconditional.
+template <int DP, int NT>
+struct QStager {
+    static constexpr int kRowU = DP / 8;            // 16-byte units per centroid
+    static constexpr int kU = kQChunk * kRowU;      // units per chunk
+    static constexpr int kUPT = (kU + NT - 1) / NT;
+    static constexpr int kPitch = 2 * DP + 16;
+    static constexpr int kBias = kQChunk * kPitch;  // byte offset of the biases
+    static constexpr int kBytes = kBias + 4 * kQChunk;
+    int goff[kUPT];
+    int loff[kUPT];
+    i32x4 v[kUPT];
+    i32x4 b;
+
+    __device__ __forceinline__ void init()
+    {
+#pragma unroll
+        for (int i = 0; i < kUPT; ++i) {
+            const int u = threadIdx.x + i * NT;
+            goff[i] = u < kU ? 16 * u : (1 << 30);
+            loff[i] = (u / kRowU) * kPitch + (u % kRowU) * 16;
+        }
+    }
+
+    __device__ __forceinline__ void fetch(const int8_t *__restrict__ qc, const int32_t *__restrict__ negb,
+                                          int64_t cbase, int64_t cpad)
+    {
+        const int64_t left = cpad - cbase;
+        const int valid = (int)(left < 0 ? 0 : left < kQChunk ? left : kQChunk);
+        const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<int8_t *>(qc + cbase * 2 * DP), (short)0, valid * 2 * DP, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < kUPT; ++i)
+            v[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, goff[i], 0, 0));
+        if (threadIdx.x < kQChunk / 4) {
+            const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<int32_t *>(negb + cbase), (short)0, valid * 4, 0x00020000);
+            b = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rb, 16 * threadIdx.x, 0, 0));
+        }
+    }
+
+    __device__ __forceinline__ void store(char *__restrict__ lds) const
+    {
+#pragma unroll
+        for (int i = 0; i < kUPT; ++i)
+            if (kU % NT == 0 || (int)threadIdx.x + i * NT < kU)
+                *reinterpret_cast<i32x4 *>(lds + loff[i]) = v[i];
+        if (threadIdx.x < kQChunk / 4) *reinterpret_cast<i32x4 *>(lds + kBias + 16 * threadIdx.x) = b;
+    }
+};
+
+// ------------------------------------------------------------ rows
+// Row block rb of this wave: K-step k of row (wave * RB + rb) * 32 + l % 32
+// as x' = x - 128 (a byte xor), dimensions >= D zero; l1 += sum |x'_d| over
+// the lane's bytes (v_sad_u8 against 128).
+template <int DP, int RB>
+__device__ __forceinline__ void load_rows(const uint8_t *__restrict__ X, int64_t row0, int64_t nrows, int D,
+                                          int wave, int jl, int h, i32x4 (&xf)[RB][DP / 32],
+                                          uint32_t (&l1)[RB])
+{
+    constexpr int KS = DP / 32;
+    const int64_t left = nrows - row0;
+    const int rows_here = (int)(left < 0 ? 0 : left < 2048 ? left : 2048);
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t *>(X + row0 * (int64_t)D), (short)0, rows_here * D, 0x00020000);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int base = ((wave * RB + rb) * 32 + jl) * D + 16 * h;
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const int d = 32 * k + 16 * h + 4 * w;
+                const uint32_t raw = __builtin_amdgcn_raw_buffer_load_b32(rr, base + 32 * k + 4 * w, 0, 0);
+                const bool ok = d < D;
+                xf[rb][k][w] = ok ? (int)(raw ^ 0x80808080u) : 0;
+                s = ok ? __builtin_amdgcn_sad_u8(raw, 0x80808080u, s) : s;
+            }
+        }
+        l1[rb] = s;
+    }
+}
+
+// ------------------------------------------------------------ top-1 epilogue
+// The three largest scores of a lane's row and the ids of two.
+struct Top3i {
+    int k1, k2, k3;
+    int i1, i2;
+};
+
+__device__ __forceinline__ int med3i(int a, int b, int c)
+{
+    int m;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
+    return m;
+}
+
+__device__ __forceinline__ int max4i(int a, int b, int c, int d)
+{
+    int m;
+    asm("v_max3_i32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
+    asm("v_max_i32 %0, %1, %2" : "=v"(m) : "v"(m), "v"(d));
+    return m;
+}
+
+// Branch-free insertion (v <= k3 leaves the state unchanged): with
+// k1 >= k2 >= k3, med3(v, k2, k3) is the new third and med3(v, k1, k2) the
+// new second; strict comparisons keep the lower id on equal scores because a
+// lane visits ids in ascending order.
+__device__ __forceinline__ void top3i_push(Top3i &t, int v, int id)
+{
+    const bool gt1 = v > t.k1;
+    const bool gt2 = v > t.k2;
+    t.k3 = med3i(v, t.k2, t.k3);
+    t.k2 = med3i(v, t.k1, t.k2);
+    t.k1 = gt1 ? v : t.k1;
+    const int j2 = gt2 ? id : t.i2;
+    t.i2 = gt1 ? t.i1 : j2;
+    t.i1 = gt1 ? id : t.i1;
+}
+
+__device__ __forceinline__ bool score_gt(int ka, int ia, int kb, int ib)
+{
+    return ka > kb || (ka == kb && ia < ib);
+}
+
+// Merges two lists sorted by (score descending, id ascending).
+__device__ __forceinline__ Top3i top3i_merge(Top3i a, Top3i b)
+{
+    if (score_gt(b.k1, b.i1, a.k1, a.i1)) {
+        const Top3i t = a;
+        a = b;
+        b = t;
+    }
+    Top3i m;
+    m.k1 = a.k1;
+    m.i1 = a.i1;
+    if (score_gt(b.k1, b.i1, a.k2, a.i2)) {
+        m.k2 = b.k1;
+        m.i2 = b.i1;
+        m.k3 = max(a.k2, b.k2);
+    } else {
+        m.k2 = a.k2;
+        m.i2 = a.i2;
+        m.k3 = max(a.k3, b.k1);
+    }
+    return m;
+}
+
+// Group g (0..3) of a finished tile: registers 4g .. 4g + 3, centroids
+// idp + 8g + e. The scores are formed (one shift-add each), tested as a group
+// against the third largest, and inserted only when some lane of the wave
+// needs it.
+template <int g>
+__device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+{
+    int v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e];
+    const int m = max4i(v[0], v[1], v[2], v[3]);
+    if (__any(m > st.k3)) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) top3i_push(st, v[e], idp + 8 * g + e);
+    }
+    // keeps the group at this point of the MFMA stream
+    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2));
+}
+
+template <int g, int T, int KS>
+__device__ __forceinline__ void i8_groups_at(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+{
+    if constexpr (g < 4) {
+        if constexpr (g * KS / 4 == T) i8_group<g>(pH, pL, idp, st);
+        i8_groups_at<g + 1, T, KS>(pH, pL, idp, st);
+    }
+}
+
+// The fragments of one staged 32-centroid block for every K-step: plane H at
+// Ar + 32k, plane Ls at Ar + DP + 32k (Ar = this lane's row, offset 16 h).
+template <int DP>
+struct Frags {
+    i32x4 h[DP / 32], l[DP / 32];
+};
+
+template <int DP>
+__device__ __forceinline__ void load_frags(const char *Ar, Frags<DP> &f)
+{
+#pragma unroll
+    for (int k = 0; k < DP / 32; ++k) {
+        f.h[k] = *reinterpret_cast<const i32x4 *>(Ar + 32 * k);
+        f.l[k] = *reinterpret_cast<const i32x4 *>(Ar + DP + 32 * k);
+    }
+}
+
+// K-steps T .. KS-1 of one tile: a 32-centroid block against one 32-row
+// block, both planes, into (cH, cL); at T = 0, cH starts from zero and cL
+// from the biases. With EP, the epilogue of the previous tile (pH, pL; ids
+// from idp; state sp) runs between the K-steps.
+template <int DP, bool EP, int T = 0>
+__device__ __forceinline__ void i8_tile(const Frags<DP> &f, const i32x4 (&x)[DP / 32], const i32x16 &bias,
+                                        i32x16 &cH, i32x16 &cL, const i32x16 &pH, const i32x16 &pL, int idp,
+                                        Top3i &sp)
+{
+    constexpr int KS = DP / 32;
+    if constexpr (T < KS) {
+        if constexpr (T == 0) {
+            const i32x16 zero = {0};
+            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x[0], zero, 0, 0, 0);
+            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[0], x[0], bias, 0, 0, 0);
+        } else {
+            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x[T], cH, 0, 0, 0);
+            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[T], x[T], cL, 0, 0, 0);
+        }
+        if constexpr (EP) i8_groups_at<0, T, KS>(pH, pL, idp, sp);
+        __builtin_amdgcn_sched_barrier(0);
+        i8_tile<DP, EP, T + 1>(f, x, bias, cH, cL, pH, pL, idp, sp);
+    }
+}
+
+template <int g = 0>
+__device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+{
+    if constexpr (g < 4) {
+        i8_group<g>(pH, pL, idp, st);
+        i8_drain<g + 1>(pH, pL, idp, st);
+    }
+}
+
+__device__ __forceinline__ i32x16 load_bias(const int *Bh)
+{
+    i32x16 bias;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const i32x4 u = *reinterpret_cast<const i32x4 *>(Bh + 8 * g);
+        bias[4 * g + 0] = u[0];
+        bias[4 * g + 1] = u[1];
+        bias[4 * g + 2] = u[2];
+        bias[4 * g + 3] = u[3];
+    }
+    return bias;
+}
+
+// Merges the two half-lanes of a row, certifies with the bound 2R = 4 + ||x'||_1,
+// settles two-way near-ties exactly in fp64 and queues the rest for the
+// full fp64 fallback.
+__device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, uint32_t l1part,
+                                          const Top3i &st)
+{
+    const uint32_t l1 = l1part + __shfl_xor(l1part, 32);
+    Top3i o;
+    o.k1 = __shfl_xor(st.k1, 32);
+    o.k2 = __shfl_xor(st.k2, 32);
+    o.k3 = __shfl_xor(st.k3, 32);
+    o.i1 = __shfl_xor(st.i1, 32);
+    o.i2 = __shfl_xor(st.i2, 32);
+    const Top3i m = top3i_merge(st, o);
+    if (rvalid && h == 0) {
+        const int64_t twoR = 4 + (int64_t)l1;
+        int label = -1;
+        if (!a.force_fallback) {
+            if ((int64_t)m.k1 - (int64_t)m.k2 > twoR) {
+                label = m.i1;
+            } else if ((int64_t)m.k1 - (int64_t)m.k3 > twoR) {
+                const uint8_t *x = a.rows + row * (int64_t)a.D;
+                const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
+                const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
+                label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
+                atomicAdd(a.stats + kStatRefine2, 1ull);
+            }
+        }
+        if (label < 0) {
+            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
+            if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
+            atomicAdd(a.stats + kStatFallback, 1ull);
+        }
+        a.labels[row] = label;
+    }
+}
+
+// One workgroup tile: W * 32 * RB rows against every centroid. Chunk j sits
+// in LDS buffer j & 1. Tiles (32 centroids x 32 rows) run in the order
+// (block 0, rows 0), (block 0, rows 1), (block 1, rows 0), (block 1, rows 1)
+// (RB = 2; with RB = 1 just the two blocks), alternating between the
+// accumulator sets T0 and T1, and each tile's K-steps carry the epilogue of
+// the tile before it. A block's fragments are read from LDS once for all RB
+// row blocks.
+template <int DP, int W>
+__device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
+{
+    constexpr int RB = rows_blocks<DP>();
+    constexpr int NT = W * 64;
+    using St = QStager<DP, NT>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row0 = tile * (W * 32 * RB);
+
+    i32x4 xf[RB][DP / 32];
+    uint32_t l1[RB];
+    load_rows<DP, RB>(a.rows, row0, a.nrows, a.D, wave, jl, h, xf, l1);
+
+    Top3i st[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1};
+
+    const char *A0 = lds + jl * St::kPitch + 16 * h;  // block 0 of buffer 0
+    const char *B0 = lds + St::kBias + 16 * h;        // biases of block 0 (4 h ints in)
+    const int idh = 4 * h;
+    const int nch = (int)a.nchunks;
+
+    St q;
+    q.init();
+    q.fetch(a.qc, a.negb, 0, a.cpad);
+    q.store(lds);
+    __syncthreads();
+
+    // T1 starts as a tile of lowest scores, so the first epilogue inserts nothing
+    i32x16 h0, l0, h1 = {0}, l1acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) l1acc[r] = kNoScore;
+    Frags<DP> f;
+    for (int j = 0; j < nch; ++j) {
+        q.fetch(a.qc, a.negb, (int64_t)(j + 1) * kQChunk, a.cpad);
+        const int bo = (j & 1) * CS;
+        const int c0 = idh + j * kQChunk;
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            load_frags<DP>(A0 + bo + cb * 32 * St::kPitch, f);
+            const i32x16 bias = load_bias(reinterpret_cast<const int *>(B0 + bo + cb * 128));
+            if constexpr (RB == 2) {
+                // (cb, rows 0) -> T0 while T1 = (cb - 1, rows 1) drains
+                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 + 32 * cb - 32, st[1]);
+                // (cb, rows 1) -> T1 while T0 = (cb, rows 0) drains
+                i8_tile<DP, true>(f, xf[RB - 1], bias, h1, l1acc, h0, l0, c0 + 32 * cb, st[0]);
+            } else if (cb == 0) {
+                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 - 32, st[0]);
+            } else {
+                i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, c0, st[0]);
+            }
+        }
+        q.store(lds + ((j + 1) & 1) * CS);
+        __syncthreads();
+    }
+    i8_drain(h1, l1acc, idh + (nch - 1) * kQChunk + 32, st[RB - 1]);
+
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
+        i8_finish(a, row, row < a.nrows, h, l1[rb], st[rb]);
+    }
+}
+
+template <int DP, int W>
+__global__ __launch_bounds__(W * 64, 2) void screen_i8_kernel(ScreenI8Args a)
+{
+    using St = QStager<DP, W * 64>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    __shared__ __attribute__((aligned(16))) char lds[2 * CS];
+    if (*a.q_bad) return;  // the fp32 screen takes this call
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.stats[kStatScreenI8] = 1ull;
+    constexpr int rows_per_tile = W * 32 * rows_blocks<DP>();
+    const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        screen_i8_tile<DP, W>(a, tile, lds);
+        __syncthreads();
+    }
+}
+
+template <int DP, int W>
+hipError_t launch_i8(const ScreenI8Args &a, int num_cus, hipStream_t s)
+{
+    constexpr int rows_per_tile = W * 32 * rows_blocks<DP>();
+    const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
+    const int per_cu = 8 / W;  // two waves per SIMD
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, (int64_t)per_cu * num_cus));
+    hipLaunchKernelGGL((screen_i8_kernel<DP, W>), dim3(grid), dim3(W * 64), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int W>
+hipError_t launch_i8_w(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s)
+{
+    switch (DP) {
+    case 32: return launch_i8<32, W>(a, num_cus, s);
+    case 64: return launch_i8<64, W>(a, num_cus, s);
+    case 96: return launch_i8<96, W>(a, num_cus, s);
+    case 128: return launch_i8<128, W>(a, num_cus, s);
+    case 192: return launch_i8<192, W>(a, num_cus, s);
+    case 256: return launch_i8<256, W>(a, num_cus, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+int64_t quantized_pad(int64_t C) { return (C + kQChunk - 1) / kQChunk * kQChunk; }
+
+hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
+                                     uint32_t *q_bad, hipStream_t s)
+{
+    const int64_t cpad = quantized_pad(C);
+    const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
+    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, qc, negb,
+                       q_bad);
+    return hipGetLastError();
+}
+
+hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int waves, int num_cus, hipStream_t s)
+{
+    if (a.nrows <= 0) return hipSuccess;
+    return waves == 4 ? launch_i8_w<4>(DP, a, num_cus, s) : launch_i8_w<8>(DP, a, num_cus, s);
+}
+
+}  // namespace ivf

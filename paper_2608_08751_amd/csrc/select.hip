@@ -8,6 +8,7 @@
 // at most B per key; the selection below only trusts them as far as B allows
 // and decides the final order with exact fp64 distances.
 #include "ivf_internal.h"
+#include "exact.h"
 
 #include <math.h>
 
@@ -17,27 +18,9 @@ namespace {
 constexpr float kInfF = __builtin_huge_valf();
 constexpr double kInfD = __builtin_huge_val();
 
-__device__ __forceinline__ bool dist_lt(double da, int ia, double db, int ib)
-{
-    return da < db || (da == db && ia < ib);
-}
-
 __device__ __forceinline__ bool key_lt(float ka, int ia, float kb, int ib)
 {
     return ka < kb || (ka == kb && ia < ib);
-}
-
-// The distance of the exactness contract: fp64, ascending dims, fma.
-template <typename XT>
-__device__ __forceinline__ double exact_dist(const XT *__restrict__ x, const float *__restrict__ c,
-                                             int D)
-{
-    double s = 0.0;
-    for (int d = 0; d < D; ++d) {
-        const double t = (double)x[d] - (double)c[d];
-        s = fma(t, t, s);
-    }
-    return s;
 }
 
 __device__ __forceinline__ double key_bound(double coef, uint32_t mc2_bits, double xn2)

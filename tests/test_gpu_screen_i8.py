@@ -1,0 +1,174 @@
+"""GPU parity of the int8-MFMA screen used for uint8 rows (assignment and the
+k-means step): labels must equal the oracle's exactly, on the int8 path and
+on the fp32 path the library takes when centroids do not quantise (or when
+IVF_OPT_FP32_SCREEN forces it), including near-ties that the quantised
+scores cannot separate."""
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ivf_ctx():
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ctx = ivf.Context(0)
+    yield ctx
+    ctx.close()
+
+
+def to_dev(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_assign(ctx, x, c, fp32_screen=False):
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 1 if fp32_screen else 0)
+    try:
+        lab, cnt, off, perm = ivf.ivf_assign_build(ctx, to_dev(x), to_dev(c))
+        torch.cuda.synchronize()
+        stats = ctx.last_stats()
+    finally:
+        ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 0)
+    return lab.cpu().numpy(), cnt.cpu().numpy(), off.cpu().numpy(), perm.cpu().numpy(), stats
+
+
+def check_assign(ctx, oracle_mod, x, c, expect_i8=True):
+    olab = oracle_mod.assign(x, c)
+    ocnt, ooff, operm = oracle_mod.build_lists(olab, c.shape[0])
+    out = {}
+    for fp32 in (False, True):
+        lab, cnt, off, perm, st = gpu_assign(ctx, x, c, fp32)
+        print("fp32_screen=%d stats %s" % (fp32, st), flush=True)
+        bad = np.nonzero(lab != olab)[0]
+        assert bad.size == 0, "fp32_screen=%d: labels differ at rows %s" % (fp32, bad[:10])
+        assert (cnt == ocnt).all() and (off == ooff).all() and (perm == operm).all()
+        assert st["screen_i8"] == (1 if (expect_i8 and not fp32) else 0)
+        out[fp32] = st
+    return out
+
+
+def rows_and_centroids(N, C, D, seed):
+    rng = np.random.default_rng(seed)
+    means = rng.uniform(0.0, 255.0, size=(max(C // 2, 1), D)).astype(np.float32)
+    x, _ = synth.mixture_rows_u8(means, 0, N, seed=seed)
+    if C <= N:
+        c = x[rng.choice(N, C, replace=False)].astype(np.float32)
+    else:
+        c = rng.uniform(0.0, 255.0, size=(C, D)).astype(np.float32)
+    c += rng.uniform(-0.5, 0.5, size=c.shape).astype(np.float32)  # fractional coordinates
+    np.clip(c, 0.0, 255.0, out=c)
+    return x, c
+
+
+@pytest.mark.parametrize(
+    "N,C,D",
+    [(5000, 1000, 128), (3001, 257, 100), (2500, 130, 36), (1500, 70, 200), (1200, 65, 256),
+     (700, 1, 32), (700, 2, 64), (701, 3, 96), (4099, 640, 252), (513, 64, 128), (1, 100, 128)],
+)
+def test_i8_parity_shapes(ivf_ctx, oracle_mod, N, C, D):
+    print("case N=%d C=%d D=%d" % (N, C, D), flush=True)
+    x, c = rows_and_centroids(N, C, D, seed=N + C + D)
+    check_assign(ivf_ctx, oracle_mod, x, c)
+
+
+def test_i8_near_ties(ivf_ctx, oracle_mod):
+    """Centroids that collide or nearly collide after quantisation (exact
+    duplicates, offsets of 1e-3 and of half a quantisation step) and rows on
+    or midway between them: the certificate must hand these to the exact
+    re-evaluation or the fallback, and the labels must still be exact."""
+    rng = np.random.default_rng(11)
+    D = 128
+    base = rng.integers(20, 236, size=(40, D)).astype(np.float32)
+    variants = [base, base.copy(), base + 1e-3, base - 1.0 / 512, base + 1.0 / 512, base + 0.5]
+    c = np.vstack(variants).astype(np.float32)
+    x = [np.rint(base), np.floor(base + 0.25), np.clip(np.rint(base + 1.0), 0, 255)]
+    mid = np.rint(base).copy()
+    mid[:, 0] += 1  # one unit off the tie
+    x.append(mid)
+    x.append(rng.integers(0, 256, size=(500, D)))
+    x = np.clip(np.vstack(x), 0, 255).astype(np.uint8)
+    st = check_assign(ivf_ctx, oracle_mod, x, c)
+    assert st[False]["refine2"] + st[False]["fallback"] > 0
+
+
+def test_i8_extreme_values(ivf_ctx, oracle_mod):
+    """Rows of all 0 / all 255 against centroids at the ends of the range:
+    the largest scores and bounds the int32 arithmetic has to hold."""
+    D = 256
+    rng = np.random.default_rng(3)
+    x = np.vstack([np.zeros((3, D)), np.full((3, D), 255), rng.integers(0, 256, size=(300, D))]).astype(np.uint8)
+    c = np.vstack([np.zeros((1, D)), np.full((1, D), 255.99), np.full((1, D), 127.5),
+                   rng.uniform(0, 255.99, size=(97, D))]).astype(np.float32)
+    check_assign(ivf_ctx, oracle_mod, x, c)
+
+
+@pytest.mark.parametrize("bad", [256.0, -0.5, 255.999, 300.0, -1e6])
+def test_i8_unquantisable_centroids_take_fp32(ivf_ctx, oracle_mod, bad):
+    """One coordinate outside what 16-bit fixed point around 128 holds: the
+    int8 kernel stands down and the fp32 screen gives the same exact labels."""
+    x, c = rows_and_centroids(3000, 200, 128, seed=5)
+    c[17, 5] = bad
+    check_assign(ivf_ctx, oracle_mod, x, c, expect_i8=False)
+
+
+def test_i8_edge_of_range_quantises(ivf_ctx, oracle_mod):
+    """255.998 and 0.0 still fit (-32768 <= rint(256 (c - 128)) <= 32767)."""
+    x, c = rows_and_centroids(2000, 100, 64, seed=8)
+    c[3, :] = 255.998
+    c[4, :] = 0.0
+    check_assign(ivf_ctx, oracle_mod, x, c)
+
+
+def test_i8_kmeans_step_both_paths(ivf_ctx, oracle_mod):
+    """Two Lloyd iterations from sampled rows (several centroids per mixture
+    component, so near-ties occur): both screens give the oracle's step."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(150, 128, seed=21)
+    x, _ = synth.mixture_rows_u8(means, 0, 12000, seed=21)
+    c = x[synth.kmeans_init(12000, 600, seed=21)].astype(np.float32)
+    for it in range(2):
+        olab, ocen, ocnt, oobj = oracle_mod.kmeans_step(x, c, seed=3, it=it)
+        for fp32 in (0, 1):
+            ivf_ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, fp32)
+            try:
+                lab, cen, cnt, obj = ivf.ivf_kmeans_step(ivf_ctx, to_dev(x), to_dev(c), seed=3, it=it)
+                torch.cuda.synchronize()
+                st = ivf_ctx.last_stats()
+            finally:
+                ivf_ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 0)
+            print("it %d fp32_screen=%d stats %s" % (it, fp32, st), flush=True)
+            assert st["screen_i8"] == 1 - fp32
+            assert (lab.cpu().numpy() == olab).all()
+            assert (cnt.cpu().numpy() == ocnt).all()
+            assert (cen.cpu().numpy() == ocen).all()
+        c = ocen
+
+
+def test_i8_forced_fallback_is_identical(ivf_ctx, oracle_mod):
+    import paper_2608_08751_amd as ivf
+
+    x, c = rows_and_centroids(1500, 90, 128, seed=13)
+    olab = oracle_mod.assign(x, c)
+    ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 1)
+    try:
+        lab, _, _, _, st = gpu_assign(ivf_ctx, x, c)
+    finally:
+        ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 0)
+    assert st["screen_i8"] == 1 and st["fallback"] == 1500
+    assert (lab == olab).all()

@@ -1,0 +1,114 @@
+"""Host model of the int8 screen's arithmetic (no GPU): the quantisation of
+centroids to P = rint(256 (c - 128)) = 256 H + Ls + 128 with int8 H and Ls,
+the integer score s = 256 x'.H + x'.Ls - rint(128 ||c'||^2), and the bound
+|s + 128 k + 128 sum(x')| < R - 1 = 1 + ||x'||_1 / 2 on which the kernel's
+certificate rests (k = ||c'||^2 - 2 x'.c', x' = x - 128, c' = c - 128).
+Distances are evaluated exactly with rational arithmetic on a subset."""
+from fractions import Fraction
+
+import numpy as np
+
+
+def quantise(c):
+    cp = c.astype(np.float64) - 128.0
+    P = np.rint(256.0 * cp)
+    assert np.all((P >= -32768) & (P <= 32767))
+    P = P.astype(np.int64)
+    H = P >> 8
+    Ls = P - 256 * H - 128
+    B = np.rint(128.0 * np.sum(cp * cp, axis=1)).astype(np.int64)
+    return P, H, Ls, B
+
+
+def score(x, H, Ls, B):
+    xp = x.astype(np.int64) - 128
+    return 256 * (xp @ H.T) + xp @ Ls.T - B[None, :]
+
+
+def centroids(rng, C, D):
+    c = rng.uniform(0.0, 255.99, size=(C, D)).astype(np.float32)
+    # values on and next to the rounding boundaries of the 1/256 grid
+    k = rng.integers(0, 256 * 255, size=(C // 4, D))
+    c[: C // 4] = ((k + 0.5) / 256.0).astype(np.float32)
+    c[C // 4: C // 2] = np.nextafter(((k + 0.5) / 256.0).astype(np.float32), np.float32(300))
+    c[0] = 0.0
+    c[1] = np.float32(255.998)
+    c[2] = np.float32(2.0 ** -60)  # c - 128 is not exact in fp64 (rounding slack of the bound)
+    return c
+
+
+def test_planes_are_int8_and_recompose():
+    rng = np.random.default_rng(0)
+    c = centroids(rng, 256, 64)
+    P, H, Ls, _ = quantise(c)
+    assert H.min() >= -128 and H.max() <= 127
+    assert Ls.min() >= -128 and Ls.max() <= 127
+    assert np.array_equal(256 * H + Ls + 128, P)
+
+
+def test_score_error_within_bound_exact_arithmetic():
+    rng = np.random.default_rng(1)
+    D, C = 16, 40
+    c = centroids(rng, C, D)
+    x = rng.integers(0, 256, size=(30, D))
+    x[0] = 0
+    x[1] = 255
+    _, H, Ls, B = quantise(c)
+    s = score(x, H, Ls, B)
+    cf = [[Fraction(float(v)) - 128 for v in row] for row in c]
+    worst = Fraction(0)
+    for i in range(x.shape[0]):
+        xp = [int(v) - 128 for v in x[i]]
+        sx = sum(xp)
+        R1 = 1 + Fraction(sum(abs(v) for v in xp), 2)
+        for j in range(C):
+            k = sum(v * v for v in cf[j]) - 2 * sum(a * b for a, b in zip(xp, cf[j]))
+            e = Fraction(int(s[i, j])) + 128 * k + 128 * sx
+            assert abs(e) < R1, (i, j, float(e), float(R1))
+            worst = max(worst, abs(e) / R1)
+    # the bound is not vacuous: errors reach a good part of it
+    assert worst > Fraction(1, 20)
+
+
+def test_certificate_never_excludes_the_nearest():
+    """On a wide random problem, whenever the best score beats the second by
+    more than 2R the best-scored centroid is the exact nearest (fp64 direct
+    distances), and whenever it beats the third by more than 2R the nearest
+    is one of the two best scored."""
+    rng = np.random.default_rng(2)
+    D, C, N = 128, 300, 400
+    c = centroids(rng, C, D)
+    base = np.rint(c[rng.integers(0, C, N)]).clip(0, 255)
+    x = np.clip(base + rng.integers(-3, 4, size=(N, D)), 0, 255).astype(np.int64)
+    _, H, Ls, B = quantise(c)
+    s = score(x, H, Ls, B)
+    d = ((x[:, None, :].astype(np.float64) - c[None, :, :].astype(np.float64)) ** 2).sum(axis=2)
+    l1 = np.abs(x - 128).sum(axis=1)
+    twoR = 4 + l1
+    order = np.argsort(-s, axis=1, kind="stable")
+    top = np.take_along_axis(s, order[:, :3], axis=1)
+    nearest = np.argmin(d, axis=1)
+    n1 = n2 = 0
+    for i in range(N):
+        if top[i, 0] - top[i, 1] > twoR[i]:
+            assert order[i, 0] == nearest[i]
+            n1 += 1
+        elif top[i, 0] - top[i, 2] > twoR[i]:
+            assert nearest[i] in order[i, :2]
+            n2 += 1
+    assert n1 > N // 2
+
+
+def test_int32_headroom_at_the_largest_dimension():
+    """D = 256 with every |x'| = 128 and P at both ends: the partial sums the
+    kernel forms (256 x'.H, x'.Ls - B, and their sum) stay inside int32."""
+    D = 256
+    c = np.full((2, D), 0.0, np.float32)
+    c[1] = np.float32(255.998)
+    x = np.zeros((1, D), np.int64)  # x' = -128 everywhere
+    _, H, Ls, B = quantise(c)
+    xp = x - 128
+    hi = 256 * (xp @ H.T)
+    lo = xp @ Ls.T - B[None, :]
+    for v in (hi, lo, hi + lo):
+        assert np.abs(v).max() < 2 ** 31
