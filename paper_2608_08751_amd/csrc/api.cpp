@@ -406,7 +406,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
         q.wl_cap = l.wl_cap;
         q.stats = l.sc.stats;
         q.force_fallback = ctx->force_fallback;
-        TIMED("screen_top1_i8", launch_screen_i8(DP, q, 8, ctx->num_cus, s));
+        TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
         a.gate = q_bad;
     }
     TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));

@@ -85,7 +85,8 @@ struct ScreenI8Args {
 int64_t quantized_pad(int64_t C);
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
                                      uint32_t *q_bad, hipStream_t s);
-hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int waves, int num_cus, hipStream_t s);
+// Eight waves per workgroup (two per SIMD), one workgroup per CU.
+hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
 
 // ---- norms, selection, fallbacks (select.hip) -----------------------------
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);

@@ -8,12 +8,12 @@
 // centroids are quantised once per call to 16-bit fixed point,
 //     P = rint(256 c')  (-32768 <= P <= 32767),  P = 256 H + (Ls + 128),
 // with H = floor(P / 256) and Ls = (P mod 256) - 128 both in [-128, 127].
-// Two int8 MFMA products give exact int32 sums x'.H and x'.Ls, and the
-// screening score of a centroid is the exact integer
-//     s(c) = 256 x'.H + x'.Ls - B,   B = rint(128 ||c'||^2),
+// Two int8 MFMA products give exact int32 sums, and the screening score of a
+// centroid is the exact integer
+//     s(c) = 256 (x'.H - Bh) + x'.Ls,   Bh = rint(||c'||^2 / 2),
 // which equals -128 k(c) up to a per-row constant and an error e(c) with
-//     |e(c)| <= |128 ||c'||^2 - B| + sum_d |x'_d| |256 c'_d - P_d|
-//            <  1 + ||x'||_1 / 2 =: R - 1.
+//     |e(c)| <= |128 ||c'||^2 - 256 Bh| + sum_d |x'_d| |256 c'_d - P_d|
+//            <  129 + ||x'||_1 / 2 < R := 131 + ||x'||_1 / 2.
 // If the best score beats the second by more than 2R, its centroid is the
 // unique nearest; if it beats the third by more than 2R, the nearest is one of
 // the two best and an exact fp64 evaluation of both decides with the
@@ -43,6 +43,7 @@ typedef int i32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kQChunk = 64;          // centroids per staged chunk
 constexpr int kNoScore = INT32_MIN;  // score of a padded centroid (below any real score)
+constexpr int kNoBias = -(1 << 23);  // H accumulator start of a padded centroid: s = kNoScore
 
 // Row blocks of 32 rows per wave: two for DP <= 128 (each staged centroid
 // fragment then feeds two MFMAs), one above (register budget).
@@ -54,7 +55,7 @@ constexpr int rows_blocks()
 
 // ------------------------------------------------------------ quantisation
 // One wave per centroid (grid-stride). Writes the two planes [H | Ls] of
-// DP bytes each (zero beyond D), the bias -B, and raises *q_bad on any value
+// DP bytes each (zero beyond D), the bias -Bh, and raises *q_bad on any value
 // that does not fit. Centroids C .. Cpad-1 are padding: zero planes and the
 // lowest score.
 __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__ cent, int64_t C, int D,
@@ -89,7 +90,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) n2 += __shfl_xor(n2, o);
         if (__any(bad) && lane == 0) *q_bad = 1u;
-        if (lane == 0) negb[j] = j < C ? -(int32_t)llrint(128.0 * n2) : kNoScore;
+        if (lane == 0) negb[j] = j < C ? -(int32_t)llrint(0.5 * n2) : kNoBias;
     }
 }
 
@@ -183,10 +184,13 @@ __device__ __forceinline__ void load_rows(const uint8_t *__restrict__ X, int64_t
 }
 
 // ------------------------------------------------------------ top-1 epilogue
-// The three largest scores of a lane's row and the ids of two.
+// The three largest scores of a lane's row and the ids of two; t3 is the
+// prefilter threshold on the H accumulators, (k3 - lmax) >> 8 with
+// lmax = 128 ||x'||_1 >= x'.Ls: an H value h <= t3 has s <= 256 h + lmax <= k3.
 struct Top3i {
     int k1, k2, k3;
     int i1, i2;
+    int t3, lmax;
 };
 
 __device__ __forceinline__ int med3i(int a, int b, int c)
@@ -249,22 +253,26 @@ __device__ __forceinline__ Top3i top3i_merge(Top3i a, Top3i b)
 }
 
 // Group g (0..3) of a finished tile: registers 4g .. 4g + 3, centroids
-// idp + 8g + e. The scores are formed (one shift-add each), tested as a group
-// against the third largest, and inserted only when some lane of the wave
-// needs it.
+// idp + 8g + e. The group's H values are tested against the prefilter
+// threshold (three instructions for four centroids); only when some lane of
+// the wave passes are the exact scores formed (one shift-add each), tested
+// against the third largest and inserted.
 template <int g>
 __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
 {
-    int v[4];
+    const int m = max4i(pH[4 * g], pH[4 * g + 1], pH[4 * g + 2], pH[4 * g + 3]);
+    if (__any(m > st.t3)) {
+        int v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e];
-    const int m = max4i(v[0], v[1], v[2], v[3]);
-    if (__any(m > st.k3)) {
+        for (int e = 0; e < 4; ++e) v[e] = (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e];
+        if (__any(max4i(v[0], v[1], v[2], v[3]) > st.k3)) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) top3i_push(st, v[e], idp + 8 * g + e);
+            for (int e = 0; e < 4; ++e) top3i_push(st, v[e], idp + 8 * g + e);
+            st.t3 = st.k3 > kNoScore ? (st.k3 - st.lmax) >> 8 : kNoScore;
+        }
     }
     // keeps the group at this point of the MFMA stream
-    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2));
+    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
 }
 
 template <int g, int T, int KS>
@@ -293,40 +301,6 @@ __device__ __forceinline__ void load_frags(const char *Ar, Frags<DP> &f)
     }
 }
 
-// K-steps T .. KS-1 of one tile: a 32-centroid block against one 32-row
-// block, both planes, into (cH, cL); at T = 0, cH starts from zero and cL
-// from the biases. With EP, the epilogue of the previous tile (pH, pL; ids
-// from idp; state sp) runs between the K-steps.
-template <int DP, bool EP, int T = 0>
-__device__ __forceinline__ void i8_tile(const Frags<DP> &f, const i32x4 (&x)[DP / 32], const i32x16 &bias,
-                                        i32x16 &cH, i32x16 &cL, const i32x16 &pH, const i32x16 &pL, int idp,
-                                        Top3i &sp)
-{
-    constexpr int KS = DP / 32;
-    if constexpr (T < KS) {
-        if constexpr (T == 0) {
-            const i32x16 zero = {0};
-            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x[0], zero, 0, 0, 0);
-            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[0], x[0], bias, 0, 0, 0);
-        } else {
-            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x[T], cH, 0, 0, 0);
-            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[T], x[T], cL, 0, 0, 0);
-        }
-        if constexpr (EP) i8_groups_at<0, T, KS>(pH, pL, idp, sp);
-        __builtin_amdgcn_sched_barrier(0);
-        i8_tile<DP, EP, T + 1>(f, x, bias, cH, cL, pH, pL, idp, sp);
-    }
-}
-
-template <int g = 0>
-__device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
-{
-    if constexpr (g < 4) {
-        i8_group<g>(pH, pL, idp, st);
-        i8_drain<g + 1>(pH, pL, idp, st);
-    }
-}
-
 __device__ __forceinline__ i32x16 load_bias(const int *Bh)
 {
     i32x16 bias;
@@ -341,13 +315,56 @@ __device__ __forceinline__ i32x16 load_bias(const int *Bh)
     return bias;
 }
 
-// Merges the two half-lanes of a row, certifies with the bound 2R = 4 + ||x'||_1,
+// K-steps T .. KS-1 of one tile: a 32-centroid block against one 32-row
+// block, both planes, into (cH, cL); at T = 0, cH starts from the biases and
+// cL from zero. With EP, the epilogue of the previous tile (pH, pL; ids from
+// idp; state sp) runs between the K-steps. With PF (the last tile that uses
+// this block's fragments), each fragment register is refilled from the next
+// block (nA, nB) as soon as its last MFMA has been issued, so the LDS reads
+// of the next block overlap this tile's MFMAs.
+template <int DP, bool PF, int T = 0>
+__device__ __forceinline__ void i8_tile(Frags<DP> &f, const i32x4 (&x)[DP / 32], i32x16 &bias, i32x16 &cH,
+                                        i32x16 &cL, const i32x16 &pH, const i32x16 &pL, int idp, Top3i &sp,
+                                        const char *nA, const int *nB)
+{
+    constexpr int KS = DP / 32;
+    if constexpr (T < KS) {
+        if constexpr (T == 0) {
+            const i32x16 zero = {0};
+            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x[0], bias, 0, 0, 0);
+            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[0], x[0], zero, 0, 0, 0);
+            if constexpr (PF) bias = load_bias(nB);
+        } else {
+            cH = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x[T], cH, 0, 0, 0);
+            cL = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.l[T], x[T], cL, 0, 0, 0);
+        }
+        if constexpr (PF) {
+            f.h[T] = *reinterpret_cast<const i32x4 *>(nA + 32 * T);
+            f.l[T] = *reinterpret_cast<const i32x4 *>(nA + DP + 32 * T);
+        }
+        i8_groups_at<0, T, KS>(pH, pL, idp, sp);
+        __builtin_amdgcn_sched_barrier(0);
+        i8_tile<DP, PF, T + 1>(f, x, bias, cH, cL, pH, pL, idp, sp, nA, nB);
+    }
+}
+
+template <int g = 0>
+__device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+{
+    if constexpr (g < 4) {
+        i8_group<g>(pH, pL, idp, st);
+        i8_drain<g + 1>(pH, pL, idp, st);
+    }
+}
+
+
+// Merges the two half-lanes of a row, certifies with the bound 2R = 262 + ||x'||_1,
 // settles two-way near-ties exactly in fp64 and queues the rest for the
 // full fp64 fallback.
 __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, uint32_t l1part,
                                           const Top3i &st)
 {
-    const uint32_t l1 = l1part + __shfl_xor(l1part, 32);
+    const uint32_t l1 = l1part;  // whole row (both half-lanes)
     Top3i o;
     o.k1 = __shfl_xor(st.k1, 32);
     o.k2 = __shfl_xor(st.k2, 32);
@@ -356,7 +373,7 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
     o.i2 = __shfl_xor(st.i2, 32);
     const Top3i m = top3i_merge(st, o);
     if (rvalid && h == 0) {
-        const int64_t twoR = 4 + (int64_t)l1;
+        const int64_t twoR = 262 + (int64_t)l1;
         int label = -1;
         if (!a.force_fallback) {
             if ((int64_t)m.k1 - (int64_t)m.k2 > twoR) {
@@ -379,12 +396,13 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
 }
 
 // One workgroup tile: W * 32 * RB rows against every centroid. Chunk j sits
-// in LDS buffer j & 1. Tiles (32 centroids x 32 rows) run in the order
-// (block 0, rows 0), (block 0, rows 1), (block 1, rows 0), (block 1, rows 1)
-// (RB = 2; with RB = 1 just the two blocks), alternating between the
-// accumulator sets T0 and T1, and each tile's K-steps carry the epilogue of
-// the tile before it. A block's fragments are read from LDS once for all RB
-// row blocks.
+// in LDS buffer j & 1. Tiles (32 centroids x 32 rows) run block by block and
+// within a block row block by row block, alternating between the
+// accumulator sets T0 and T1; each tile's K-steps carry the epilogue of the
+// tile before it, and the last tile of a block loads the next block's
+// fragments and biases. Chunk j + 1 is written to LDS between the two blocks
+// of chunk j (its buffer was last read before the previous such barrier) and
+// chunk j + 2 is fetched right after, a whole chunk ahead of its store.
 template <int DP, int W>
 __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
 {
@@ -392,6 +410,7 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
     constexpr int NT = W * 64;
     using St = QStager<DP, NT>;
     constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    constexpr int BLK = 32 * St::kPitch;  // bytes of one 32-centroid block
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int h = lane >> 5;
@@ -404,10 +423,13 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 
     Top3i st[RB];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1};
+    for (int rb = 0; rb < RB; ++rb) {
+        l1[rb] += __shfl_xor(l1[rb], 32);
+        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, (int)(128 * l1[rb])};
+    }
 
-    const char *A0 = lds + jl * St::kPitch + 16 * h;  // block 0 of buffer 0
-    const char *B0 = lds + St::kBias + 16 * h;        // biases of block 0 (4 h ints in)
+    const char *A0 = lds + jl * St::kPitch + 16 * h;             // block 0 of buffer 0
+    const char *B0 = lds + St::kBias + 16 * h;                   // its biases (4 h ints in)
     const int idh = 4 * h;
     const int nch = (int)a.nchunks;
 
@@ -416,33 +438,40 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
     q.fetch(a.qc, a.negb, 0, a.cpad);
     q.store(lds);
     __syncthreads();
+    q.fetch(a.qc, a.negb, kQChunk, a.cpad);
 
     // T1 starts as a tile of lowest scores, so the first epilogue inserts nothing
-    i32x16 h0, l0, h1 = {0}, l1acc;
+    i32x16 h0, l0, h1, l1acc = {0};
 #pragma unroll
-    for (int r = 0; r < 16; ++r) l1acc[r] = kNoScore;
+    for (int r = 0; r < 16; ++r) h1[r] = kNoBias;
     Frags<DP> f;
+    load_frags<DP>(A0, f);
+    i32x16 bias = load_bias(reinterpret_cast<const int *>(B0));
     for (int j = 0; j < nch; ++j) {
-        q.fetch(a.qc, a.negb, (int64_t)(j + 1) * kQChunk, a.cpad);
         const int bo = (j & 1) * CS;
+        const int bn = CS - bo;  // the other buffer
         const int c0 = idh + j * kQChunk;
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb) {
-            load_frags<DP>(A0 + bo + cb * 32 * St::kPitch, f);
-            const i32x16 bias = load_bias(reinterpret_cast<const int *>(B0 + bo + cb * 128));
+            // the block after this one: block 1 of this chunk, or block 0 of the next
+            const char *nA = cb == 0 ? A0 + bo + BLK : A0 + bn;
+            const int *nB = reinterpret_cast<const int *>(cb == 0 ? B0 + bo + 128 : B0 + bn);
             if constexpr (RB == 2) {
-                // (cb, rows 0) -> T0 while T1 = (cb - 1, rows 1) drains
-                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 + 32 * cb - 32, st[1]);
-                // (cb, rows 1) -> T1 while T0 = (cb, rows 0) drains
-                i8_tile<DP, true>(f, xf[RB - 1], bias, h1, l1acc, h0, l0, c0 + 32 * cb, st[0]);
+                // (cb, rows 0) -> T0 while T1 = the tile before drains
+                i8_tile<DP, false>(f, xf[0], bias, h0, l0, h1, l1acc, c0 + 32 * cb - 32, st[1], nA, nB);
+                // (cb, rows 1) -> T1 while T0 = (cb, rows 0) drains; loads the next block
+                i8_tile<DP, true>(f, xf[1], bias, h1, l1acc, h0, l0, c0 + 32 * cb, st[0], nA, nB);
             } else if (cb == 0) {
-                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 - 32, st[0]);
+                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 - 32, st[0], nA, nB);
             } else {
-                i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, c0, st[0]);
+                i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, c0, st[0], nA, nB);
+            }
+            if (cb == 0) {
+                q.store(lds + bn);
+                __syncthreads();
+                q.fetch(a.qc, a.negb, (int64_t)(j + 2) * kQChunk, a.cpad);
             }
         }
-        q.store(lds + ((j + 1) & 1) * CS);
-        __syncthreads();
     }
     i8_drain(h1, l1acc, idh + (nch - 1) * kQChunk + 32, st[RB - 1]);
 
@@ -508,10 +537,10 @@ hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP
     return hipGetLastError();
 }
 
-hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int waves, int num_cus, hipStream_t s)
+hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s)
 {
     if (a.nrows <= 0) return hipSuccess;
-    return waves == 4 ? launch_i8_w<4>(DP, a, num_cus, s) : launch_i8_w<8>(DP, a, num_cus, s);
+    return launch_i8_w<8>(DP, a, num_cus, s);
 }
 
 }  // namespace ivf

@@ -1,9 +1,11 @@
 """Host model of the int8 screen's arithmetic (no GPU): the quantisation of
 centroids to P = rint(256 (c - 128)) = 256 H + Ls + 128 with int8 H and Ls,
-the integer score s = 256 x'.H + x'.Ls - rint(128 ||c'||^2), and the bound
-|s + 128 k + 128 sum(x')| < R - 1 = 1 + ||x'||_1 / 2 on which the kernel's
-certificate rests (k = ||c'||^2 - 2 x'.c', x' = x - 128, c' = c - 128).
-Distances are evaluated exactly with rational arithmetic on a subset."""
+the integer score s = 256 (x'.H - Bh) + x'.Ls with Bh = rint(||c'||^2 / 2),
+the bound |s + 128 k + 128 sum(x')| < 129 + ||x'||_1 / 2 on which the
+kernel's certificate rests (k = ||c'||^2 - 2 x'.c', x' = x - 128,
+c' = c - 128), and the prefilter inequality s <= 256 h + 128 ||x'||_1 with
+h = x'.H - Bh. Distances are evaluated exactly with rational arithmetic on a
+subset."""
 from fractions import Fraction
 
 import numpy as np
@@ -16,13 +18,18 @@ def quantise(c):
     P = P.astype(np.int64)
     H = P >> 8
     Ls = P - 256 * H - 128
-    B = np.rint(128.0 * np.sum(cp * cp, axis=1)).astype(np.int64)
-    return P, H, Ls, B
+    Bh = np.rint(0.5 * np.sum(cp * cp, axis=1)).astype(np.int64)
+    return P, H, Ls, Bh
 
 
-def score(x, H, Ls, B):
+def hpart(x, H, Bh):
     xp = x.astype(np.int64) - 128
-    return 256 * (xp @ H.T) + xp @ Ls.T - B[None, :]
+    return xp @ H.T - Bh[None, :]
+
+
+def score(x, H, Ls, Bh):
+    xp = x.astype(np.int64) - 128
+    return 256 * hpart(x, H, Bh) + xp @ Ls.T
 
 
 def centroids(rng, C, D):
@@ -60,7 +67,7 @@ def test_score_error_within_bound_exact_arithmetic():
     for i in range(x.shape[0]):
         xp = [int(v) - 128 for v in x[i]]
         sx = sum(xp)
-        R1 = 1 + Fraction(sum(abs(v) for v in xp), 2)
+        R1 = 129 + Fraction(sum(abs(v) for v in xp), 2)
         for j in range(C):
             k = sum(v * v for v in cf[j]) - 2 * sum(a * b for a, b in zip(xp, cf[j]))
             e = Fraction(int(s[i, j])) + 128 * k + 128 * sx
@@ -84,7 +91,7 @@ def test_certificate_never_excludes_the_nearest():
     s = score(x, H, Ls, B)
     d = ((x[:, None, :].astype(np.float64) - c[None, :, :].astype(np.float64)) ** 2).sum(axis=2)
     l1 = np.abs(x - 128).sum(axis=1)
-    twoR = 4 + l1
+    twoR = 262 + l1
     order = np.argsort(-s, axis=1, kind="stable")
     top = np.take_along_axis(s, order[:, :3], axis=1)
     nearest = np.argmin(d, axis=1)
@@ -99,16 +106,38 @@ def test_certificate_never_excludes_the_nearest():
     assert n1 > N // 2
 
 
+def test_prefilter_never_rejects_a_larger_score():
+    """s <= 256 h + 128 ||x'||_1 for every row and centroid, so a group whose
+    H values are all <= (k3 - 128 ||x'||_1) >> 8 holds no score above k3."""
+    rng = np.random.default_rng(4)
+    D = 96
+    c = centroids(rng, 200, D)
+    x = rng.integers(0, 256, size=(300, D))
+    x[0] = 0
+    x[1] = 255
+    _, H, Ls, Bh = quantise(c)
+    s = score(x, H, Ls, Bh)
+    h = hpart(x, H, Bh)
+    lmax = 128 * np.abs(x - 128).sum(axis=1)
+    assert np.all(s <= 256 * h + lmax[:, None])
+    k3 = np.sort(s, axis=1)[:, -3]
+    t3 = (k3 - lmax) >> 8
+    above = s > k3[:, None]
+    assert np.all(h[above] > np.repeat(t3[:, None], s.shape[1], axis=1)[above])
+
+
 def test_int32_headroom_at_the_largest_dimension():
     """D = 256 with every |x'| = 128 and P at both ends: the partial sums the
-    kernel forms (256 x'.H, x'.Ls - B, and their sum) stay inside int32."""
+    kernel forms (x'.H - Bh shifted by 8, x'.Ls, and their sum) stay inside
+    int32, above the padding score -2^31."""
     D = 256
     c = np.full((2, D), 0.0, np.float32)
     c[1] = np.float32(255.998)
-    x = np.zeros((1, D), np.int64)  # x' = -128 everywhere
-    _, H, Ls, B = quantise(c)
-    xp = x - 128
-    hi = 256 * (xp @ H.T)
-    lo = xp @ Ls.T - B[None, :]
-    for v in (hi, lo, hi + lo):
-        assert np.abs(v).max() < 2 ** 31
+    for xv in (0, 255):
+        x = np.full((1, D), xv, np.int64)
+        _, H, Ls, Bh = quantise(c)
+        hi = 256 * hpart(x, H, Bh)
+        lo = (x - 128) @ Ls.T
+        for v in (hi, lo, hi + lo):
+            assert np.abs(v).max() < 2 ** 31 - 2 ** 24
+        assert hpart(x, H, Bh).min() > -(2 ** 23)
