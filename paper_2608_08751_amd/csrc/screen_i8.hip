@@ -184,14 +184,26 @@ __device__ __forceinline__ void load_rows(const uint8_t *__restrict__ X, int64_t
 }
 
 // ------------------------------------------------------------ top-1 epilogue
-// The three largest scores of a lane's row and the ids of two; t3 is the
-// prefilter threshold on the H accumulators, (k3 - lmax) >> 8 with
-// lmax = 128 ||x'||_1 >= x'.Ls: an H value h <= t3 has s <= 256 h + lmax <= k3.
+// The three largest scores a lane has kept for its row and the ids of two.
+// The certificate only asks whether the second and third scores are below
+// best - 2R, and the best only grows, so a lane keeps just the scores above
+// thr = max(k3, k1 - 2R - 1) at the time they are seen: every score that
+// ends up at or above final best - 2R is kept exactly, and every score kept
+// in its place or dropped lies below final best - 2R, so the decisions are
+// those of the exact three largest.
+// t3 = (thr - lmax) >> 8 is the prefilter threshold on the H accumulators
+// (lmax = 128 ||x'||_1 >= x'.Ls, so an H value h <= t3 has s <= thr);
+// twoR = 262 + ||x'||_1, so lmax = 128 (twoR - 262).
 struct Top3i {
     int k1, k2, k3;
     int i1, i2;
-    int t3, lmax;
+    int t3, twoR;
 };
+
+__device__ __forceinline__ int keep_threshold(const Top3i &st)
+{
+    return st.k1 > kNoScore ? max(st.k3, st.k1 - st.twoR - 1) : kNoScore;
+}
 
 __device__ __forceinline__ int med3i(int a, int b, int c)
 {
@@ -265,10 +277,11 @@ __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int
         int v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e];
-        if (__any(max4i(v[0], v[1], v[2], v[3]) > st.k3)) {
+        if (__any(max4i(v[0], v[1], v[2], v[3]) > keep_threshold(st))) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) top3i_push(st, v[e], idp + 8 * g + e);
-            st.t3 = st.k3 > kNoScore ? (st.k3 - st.lmax) >> 8 : kNoScore;
+            const int thr = keep_threshold(st);
+            st.t3 = thr > kNoScore ? (thr - ((st.twoR - 262) << 7)) >> 8 : kNoScore;
         }
     }
     // keeps the group at this point of the MFMA stream
@@ -361,10 +374,8 @@ __device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int
 // Merges the two half-lanes of a row, certifies with the bound 2R = 262 + ||x'||_1,
 // settles two-way near-ties exactly in fp64 and queues the rest for the
 // full fp64 fallback.
-__device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, uint32_t l1part,
-                                          const Top3i &st)
+__device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, const Top3i &st)
 {
-    const uint32_t l1 = l1part;  // whole row (both half-lanes)
     Top3i o;
     o.k1 = __shfl_xor(st.k1, 32);
     o.k2 = __shfl_xor(st.k2, 32);
@@ -373,7 +384,7 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
     o.i2 = __shfl_xor(st.i2, 32);
     const Top3i m = top3i_merge(st, o);
     if (rvalid && h == 0) {
-        const int64_t twoR = 262 + (int64_t)l1;
+        const int64_t twoR = st.twoR;
         int label = -1;
         if (!a.force_fallback) {
             if ((int64_t)m.k1 - (int64_t)m.k2 > twoR) {
@@ -400,9 +411,13 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
 // within a block row block by row block, alternating between the
 // accumulator sets T0 and T1; each tile's K-steps carry the epilogue of the
 // tile before it, and the last tile of a block loads the next block's
-// fragments and biases. Chunk j + 1 is written to LDS between the two blocks
-// of chunk j (its buffer was last read before the previous such barrier) and
-// chunk j + 2 is fetched right after, a whole chunk ahead of its store.
+// fragments and biases. Chunk j + 1 is written to LDS just before the last
+// tile of chunk j, the only one that reads it (its buffer was last read
+// before the previous such barrier), and chunk j + 2 is fetched right after,
+// a whole chunk ahead of its store. The loop is rotated so that an
+// iteration starts right after a barrier (no LDS read outstanding) with the
+// last tile of chunk j, then runs chunk j + 1 up to its last tile; all LDS
+// waits inside are then exact.
 template <int DP, int W>
 __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
 {
@@ -425,13 +440,15 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         l1[rb] += __shfl_xor(l1[rb], 32);
-        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, (int)(128 * l1[rb])};
+        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, (int)(262 + l1[rb])};
     }
 
-    const char *A0 = lds + jl * St::kPitch + 16 * h;             // block 0 of buffer 0
-    const char *B0 = lds + St::kBias + 16 * h;                   // its biases (4 h ints in)
+    const char *A0 = lds + jl * St::kPitch + 16 * h;  // block 0 of buffer 0
+    const char *B0 = lds + St::kBias + 16 * h;        // its biases (4 h ints in)
     const int idh = 4 * h;
     const int nch = (int)a.nchunks;
+    auto abuf = [&](int jj) { return A0 + (jj & 1) * CS; };
+    auto bbuf = [&](int jj) { return reinterpret_cast<const int *>(B0 + (jj & 1) * CS); };
 
     St q;
     q.init();
@@ -439,38 +456,60 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
     q.store(lds);
     __syncthreads();
     q.fetch(a.qc, a.negb, kQChunk, a.cpad);
+    // stores chunk jj into its buffer, then fetches chunk jj + 1
+    auto stage = [&](int jj) {
+        q.store(lds + (jj & 1) * CS);
+        __syncthreads();
+        q.fetch(a.qc, a.negb, (int64_t)(jj + 1) * kQChunk, a.cpad);
+    };
 
     // T1 starts as a tile of lowest scores, so the first epilogue inserts nothing
     i32x16 h0, l0, h1, l1acc = {0};
 #pragma unroll
     for (int r = 0; r < 16; ++r) h1[r] = kNoBias;
+    i32x16 bias = load_bias(bbuf(0));
     Frags<DP> f;
-    load_frags<DP>(A0, f);
-    i32x16 bias = load_bias(reinterpret_cast<const int *>(B0));
-    for (int j = 0; j < nch; ++j) {
-        const int bo = (j & 1) * CS;
-        const int bn = CS - bo;  // the other buffer
-        const int c0 = idh + j * kQChunk;
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            // the block after this one: block 1 of this chunk, or block 0 of the next
-            const char *nA = cb == 0 ? A0 + bo + BLK : A0 + bn;
-            const int *nB = reinterpret_cast<const int *>(cb == 0 ? B0 + bo + 128 : B0 + bn);
-            if constexpr (RB == 2) {
-                // (cb, rows 0) -> T0 while T1 = the tile before drains
-                i8_tile<DP, false>(f, xf[0], bias, h0, l0, h1, l1acc, c0 + 32 * cb - 32, st[1], nA, nB);
-                // (cb, rows 1) -> T1 while T0 = (cb, rows 0) drains; loads the next block
-                i8_tile<DP, true>(f, xf[1], bias, h1, l1acc, h0, l0, c0 + 32 * cb, st[0], nA, nB);
-            } else if (cb == 0) {
-                i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, c0 - 32, st[0], nA, nB);
-            } else {
-                i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, c0, st[0], nA, nB);
-            }
-            if (cb == 0) {
-                q.store(lds + bn);
-                __syncthreads();
-                q.fetch(a.qc, a.negb, (int64_t)(j + 2) * kQChunk, a.cpad);
-            }
+    load_frags<DP>(abuf(0), f);
+
+    if constexpr (RB == 2) {
+        // (jj, cb, rows 0) -> T0 while T1 = the tile before drains
+        auto rows0 = [&](int jj, int cb) {
+            i8_tile<DP, false>(f, xf[0], bias, h0, l0, h1, l1acc, idh + jj * kQChunk + 32 * cb - 32, st[1],
+                               nullptr, nullptr);
+        };
+        // (jj, cb, rows 1) -> T1 while T0 = (jj, cb, rows 0) drains; loads the next block
+        auto rows1 = [&](int jj, int cb, const char *nA, const int *nB) {
+            i8_tile<DP, true>(f, xf[1], bias, h1, l1acc, h0, l0, idh + jj * kQChunk + 32 * cb, st[0], nA, nB);
+        };
+        rows0(0, 0);
+        rows1(0, 0, abuf(0) + BLK, bbuf(0) + 32);
+        rows0(0, 1);
+        stage(1);
+        for (int j = 0;; ++j) {
+            rows1(j, 1, abuf(j + 1), bbuf(j + 1));
+            if (j + 1 == nch) break;
+            rows0(j + 1, 0);
+            rows1(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
+            rows0(j + 1, 1);
+            stage(j + 2);
+        }
+    } else {
+        // (jj, 0) -> T0 while T1 = (jj - 1, 1) drains; (jj, 1) -> T1 while T0 drains
+        auto blk0 = [&](int jj) {
+            i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, idh + jj * kQChunk - 32, st[0], abuf(jj) + BLK,
+                              bbuf(jj) + 32);
+        };
+        auto blk1 = [&](int jj) {
+            i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, idh + jj * kQChunk, st[0], abuf(jj + 1),
+                              bbuf(jj + 1));
+        };
+        blk0(0);
+        stage(1);
+        for (int j = 0;; ++j) {
+            blk1(j);
+            if (j + 1 == nch) break;
+            blk0(j + 1);
+            stage(j + 2);
         }
     }
     i8_drain(h1, l1acc, idh + (nch - 1) * kQChunk + 32, st[RB - 1]);
@@ -478,7 +517,7 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
-        i8_finish(a, row, row < a.nrows, h, l1[rb], st[rb]);
+        i8_finish(a, row, row < a.nrows, h, st[rb]);
     }
 }
 
