@@ -3,9 +3,10 @@
 
 One step = one pass of the whole hot path over one batch of synthetic input,
 on the 65,536-centroid, D = 128 index of the uint8-valued workloads:
-  1. ivf_kmeans_step  on 10M uint8 training rows (norms, fused fp32-MFMA
-                      screening with register top-1, certified fp64 refine,
-                      list build, Lloyd update with reseeding, objective);
+  1. ivf_kmeans_step  on 10M uint8 training rows (centroid quantisation,
+                      fused int8-MFMA screening with register top-1,
+                      certified fp64 refine, list build, Lloyd update with
+                      reseeding, objective);
   2. ivf_assign_build on a batch of 10M uint8 base rows with the new
                       centroids (full assignment + histogram / scan / stable
                       scatter into cluster-major lists);
@@ -34,6 +35,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix peak
+PEAK_INT8_MFMA_TOPS = 5000.0   # MI355X dense int8 matrix peak
 PEAK_HBM_GBS = 8000.0
 PEAK_FP64_VECTOR_TFLOPS = 78.6
 
@@ -53,6 +55,8 @@ def parse():
                     help="rows for the separately timed list build at scale (0 = skip)")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="also run one device copy of this size (HBM counter calibration for rocprofv3)")
+    ap.add_argument("--fp32-screen", action="store_true",
+                    help="screen the uint8 rows on fp32 MFMA (IVF_OPT_FP32_SCREEN) instead of int8")
     return ap.parse_args()
 
 
@@ -106,6 +110,9 @@ def main():
     log("inputs generated on the device in %.1f s" % (time.time() - t0))
 
     ctx = ivf.Context(0)
+    if args.fp32_screen:
+        ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 1)
+    top1_name = "screen_top1" if args.fp32_screen else "screen_top1_i8"
     lab_t = torch.empty(Nt, dtype=torch.int32, device=dev)
     c1 = torch.empty((C, D), dtype=torch.float32, device=dev)
     cnt_t = torch.empty(C, dtype=torch.int64, device=dev)
@@ -161,26 +168,48 @@ def main():
         a[1] += ms
     kernels = {n: {"launches": c, "avg_ms": t / c, "ms_per_step": t / args.steps} for n, (c, t) in agg.items()}
     # the dominant kernel: fused screening with top-1 (one launch on Nt rows,
-    # one on Nb rows per step); algorithmic flops = 2 * rows * C * D
-    top1 = [ms for n, ms in timeline if n.endswith("/screen_top1")]
-    flops_top1 = 2.0 * C * D * (Nt + Nb) * args.steps
-    achieved = flops_top1 / (sum(top1) * 1e-3) / 1e12
-    roofline = {
-        "bound": "mfma",
-        "achieved": achieved,
-        "peak": PEAK_FP32_MFMA_TFLOPS,
-        "unit": "TFLOP/s",
-        "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-        "traffic": measured_traffic(Nt),
-        "kernel": "screen_kernel<128, uint8, top1>",
-        "flops_per_launch": 2.0 * C * D * Nt,
-        "avg_launch_ms": sum(top1) / len(top1),
-    }
-    # the fp32 MFMA pipe as the library's probe kernel measures it on this
-    # GPU (register operands only), after the timed region
-    _, probe_tflops = ctx.mfma_probe()
-    roofline["measured_peak"] = probe_tflops
-    roofline["frac_of_measured_peak"] = achieved / probe_tflops
+    # one on Nb rows per step); algorithmic work = 2 * rows * C * D multiply
+    # and add operations (the -2 x.c contraction)
+    top1 = [ms for n, ms in timeline if n.endswith("/" + top1_name)]
+    ops_top1 = 2.0 * C * D * (Nt + Nb) * args.steps
+    achieved = ops_top1 / (sum(top1) * 1e-3) / 1e12
+    if args.fp32_screen:
+        roofline = {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_FP32_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+            "traffic": measured_traffic(Nt, "screen_top1_fp32_traffic.json"),
+            "kernel": "screen_kernel<128, uint8, top1> (fp32 MFMA)",
+            "ops_per_launch": 2.0 * C * D * Nt,
+            "avg_launch_ms": sum(top1) / len(top1),
+        }
+        _, probe = ctx.mfma_probe()
+    else:
+        # the int8 screen runs two int8 MFMA planes per centroid: it executes
+        # twice the algorithmic operations on the int8 pipe
+        roofline = {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_INT8_MFMA_TOPS,
+            "unit": "TOP/s",
+            "frac": achieved / PEAK_INT8_MFMA_TOPS,
+            "traffic": measured_traffic(Nt, "screen_top1_traffic.json"),
+            "kernel": "screen_i8_kernel<128, 8> (int8 MFMA)",
+            "ops_per_launch": 2.0 * C * D * Nt,
+            "executed_int8_ops_per_launch": 2 * 2.0 * C * D * Nt,
+            "executed_frac": 2 * achieved / PEAK_INT8_MFMA_TOPS,
+            "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+            "avg_launch_ms": sum(top1) / len(top1),
+        }
+        _, probe = ctx.mfma_probe_i8()
+    # the MFMA pipe as the library's probe kernel measures it on this GPU
+    # (register operands only), after the timed region
+    roofline["measured_peak"] = probe
+    roofline["frac_of_measured_peak"] = achieved / probe
+    if not args.fp32_screen:
+        roofline["executed_frac_of_measured_peak"] = 2 * achieved / probe
 
     def call_ms(call):
         return sum(ms for n, ms in timeline if n.startswith(call + "/")) / args.steps
@@ -195,7 +224,10 @@ def main():
     # two builds per step: Nt rows (inside the k-means step) and Nb rows
     per_call["build_lists_gbs"] = 12.0 * (Nt + Nb) * args.steps / (sum(build_ms) * 1e-3) / 1e9
     per_call["build_lists_hbm_frac"] = per_call["build_lists_gbs"] / PEAK_HBM_GBS
-    per_call["step_mfma_frac"] = 2.0 * C * D * vectors / (ms_per_step * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS
+    # the whole step's algorithmic rate against the fp32 MFMA peak (the uint8
+    # rows run on int8 MFMA, so this exceeds 1)
+    per_call["step_fp32_mfma_equivalent_frac"] = (2.0 * C * D * vectors / (ms_per_step * 1e-3) / 1e12
+                                                  / PEAK_FP32_MFMA_TFLOPS)
 
     result = {
         "metric": "routed queries/s and assigned vectors/s at 1 GPU; % of fp32 MFMA peak",
@@ -208,11 +240,13 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32" if args.fp32_screen else "i8",
         "data": "synthetic (seeded uint8 Gaussian mixture, 65,536 components, std 20, generated on the device)",
         "config": {
             "workload": "ivf_pipeline: kmeans_step(10M u8 rows) + assign_build(10M u8 rows) + route(10,000 queries, nprobe 64); C=65536, D=128",
             "train_rows": Nt, "base_rows": Nb, "queries": Q, "centroids": C, "dim": D, "nprobe": K,
+            "screen": ("fp32 MFMA" if args.fp32_screen else "int8 MFMA (two planes per centroid)")
+            + " for the uint8 rows, fp32 MFMA for the fp32 queries; exact fp64 re-evaluation of near-ties",
         },
         "roofline": roofline,
         "per_call": per_call,
@@ -240,7 +274,7 @@ def main():
         result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm, "pq": pq,
                            "adc_scan": bench_adc(ctx, queries, c1, ids, off_b, perm_b, codes, cb),
                            "assign_graph": bench_assign_graph(ctx, x_train, c1, lab_t,
-                                                              kernels["kmeans_step/screen_top1"]["avg_ms"])}
+                                                              kernels["kmeans_step/" + top1_name]["avg_ms"])}
         del codes
         if args.build_rows > 0:
             # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
@@ -251,14 +285,14 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def measured_traffic(rows_per_launch):
+def measured_traffic(rows_per_launch, record):
     """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary (calibrated against a device
     copy), if it was taken on the current kernel source and launch size;
     otherwise None."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", "screen_top1_traffic.json")
+    path = os.path.join(ROOT, "profiles", record)
     try:
         with open(path) as f:
             rec = json.load(f)

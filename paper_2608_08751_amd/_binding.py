@@ -39,6 +39,7 @@ SIGNATURES = [
     ("ivf_set_option", _INT, [_P, _INT, _I64]),
     ("ivf_kernel_times", _INT, [_P, _INT, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
     ("ivf_mfma_probe", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
+    ("ivf_mfma_probe_i8", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
@@ -159,6 +160,15 @@ class Context:
         self.check(self.lib.ivf_mfma_probe(self.handle, iters, ctypes.byref(ms), ctypes.byref(tf)),
                    "ivf_mfma_probe")
         return float(ms.value), float(tf.value)
+
+    def mfma_probe_i8(self, iters: int = 20000):
+        """(ms, TOP/s) of the int8 MFMA throughput probe (synchronises)."""
+        ms = ctypes.c_float()
+        tops = ctypes.c_double()
+        self.bind_stream()
+        self.check(self.lib.ivf_mfma_probe_i8(self.handle, iters, ctypes.byref(ms), ctypes.byref(tops)),
+                   "ivf_mfma_probe_i8")
+        return float(ms.value), float(tops.value)
 
     def last_stats(self):
         out = (ctypes.c_int64 * 8)()

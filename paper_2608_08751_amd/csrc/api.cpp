@@ -596,12 +596,19 @@ int ivf_kernel_times(ivf_ctx *ctx, int max, const char **names, float *ms)
     return n;
 }
 
-ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tflops)
+}  // extern "C"
+
+namespace {
+
+// Times one probe launch (after an untimed one that loads the kernel) and
+// reports its duration and rate in units of 1e12 operations per second.
+ivf_status run_probe(ivf_ctx *ctx, int32_t iters, hipError_t (*launch)(int, int, hipStream_t, double *),
+                     const char *what, float *out_ms, double *out_rate)
 {
     if (!ctx) return IVF_EINVAL;
     ctx->err.clear();
     if (iters < 1 || iters > (1 << 20)) return fail(ctx, IVF_EINVAL, "iters must be in [1, 2^20]");
-    if (!out_ms && !out_tflops) return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!out_ms && !out_rate) return fail(ctx, IVF_EINVAL, "null pointer argument");
     if (ctx->device < 0) return fail(ctx, IVF_EUNSUPPORTED, "validation-only context");
     DeviceGuard g(ctx->device);
     hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -609,21 +616,34 @@ ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *ou
         if (e0) (void)hipEventDestroy(e0);
         return fail(ctx, IVF_EDEVICE, "hipEventCreate failed");
     }
-    double flops = 0.0;
+    double ops = 0.0;
     float ms = 0.f;
-    // an untimed short launch first: the first launch of a kernel also loads it
-    hipError_t e = launch_mfma_probe(1, ctx->num_cus, ctx->stream, &flops);
+    hipError_t e = launch(1, ctx->num_cus, ctx->stream, &ops);
     if (e == hipSuccess) e = hipEventRecord(e0, ctx->stream);
-    if (e == hipSuccess) e = launch_mfma_probe(iters, ctx->num_cus, ctx->stream, &flops);
+    if (e == hipSuccess) e = launch(iters, ctx->num_cus, ctx->stream, &ops);
     if (e == hipSuccess) e = hipEventRecord(e1, ctx->stream);
     if (e == hipSuccess) e = hipEventSynchronize(e1);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
     (void)hipEventDestroy(e0);
     (void)hipEventDestroy(e1);
-    if (e != hipSuccess) return fail(ctx, IVF_EDEVICE, "MFMA probe: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return fail(ctx, IVF_EDEVICE, "%s: %s", what, hipGetErrorString(e));
     if (out_ms) *out_ms = ms;
-    if (out_tflops) *out_tflops = ms > 0.f ? flops / (ms * 1e-3) / 1e12 : 0.0;
+    if (out_rate) *out_rate = ms > 0.f ? ops / (ms * 1e-3) / 1e12 : 0.0;
     return IVF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tflops)
+{
+    return run_probe(ctx, iters, launch_mfma_probe, "fp32 MFMA probe", out_ms, out_tflops);
+}
+
+ivf_status ivf_mfma_probe_i8(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tops)
+{
+    return run_probe(ctx, iters, launch_mfma_probe_i8, "int8 MFMA probe", out_ms, out_tops);
 }
 
 ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,

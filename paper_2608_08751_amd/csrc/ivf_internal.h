@@ -218,5 +218,7 @@ hipError_t launch_adc_scan(const float *Q, int64_t B, int D, const float *cent, 
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.
 hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops);
+// The same for the int8 MFMA pipe; *ops = the int8 operations it does.
+hipError_t launch_mfma_probe_i8(int iters, int num_cus, hipStream_t s, double *ops);
 
 }  // namespace ivf

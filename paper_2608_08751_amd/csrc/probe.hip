@@ -1,9 +1,10 @@
-// Throughput probe for the fp32 MFMA pipe of gfx950: every wave runs rounds
-// of sixteen v_mfma_f32_32x32x2_f32 on two independent accumulators with the
-// A and B operands in registers, two waves per SIMD on every CU. This is the
-// rate the screening kernels' MFMA stream could reach with no loads and no
-// other vector instructions; bench reports the screening kernels against it
-// next to the published peak.
+// Throughput probes for the MFMA pipes of gfx950 that the screening kernels
+// use: every wave runs rounds of sixteen MFMAs (v_mfma_f32_32x32x2_f32, or
+// v_mfma_i32_32x32x32_i8) on two independent accumulators with the A and B
+// operands in registers, two waves per SIMD on every CU. This is the rate
+// the screening kernels' MFMA stream could reach with no loads and no other
+// vector instructions; bench reports the screening kernels against it next
+// to the published peak.
 #include "ivf_internal.h"
 
 namespace ivf {
@@ -31,7 +32,36 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters, float a, 
     if (write) sink[blockIdx.x * blockDim.x + threadIdx.x] = r;
 }
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(512, 2) void mfma_probe_i8_kernel(int iters, int a, int write, int *sink)
+{
+    i32x16 acc0 = {0}, acc1 = {0};
+    const i32x4 av = {a, a + 1, (int)threadIdx.x, a ^ 3};
+    const i32x4 bv = {a + 2, (int)threadIdx.x, a, 7};
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc1, 0, 0, 0);
+        }
+    }
+    int r = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) r += acc0[e] + acc1[e];
+    if (write) sink[blockIdx.x * blockDim.x + threadIdx.x] = r;
+}
+
 }  // namespace
+
+hipError_t launch_mfma_probe_i8(int iters, int num_cus, hipStream_t s, double *ops)
+{
+    const int grid = num_cus;  // 8 waves per workgroup: two waves per SIMD
+    hipLaunchKernelGGL(mfma_probe_i8_kernel, dim3(grid), dim3(512), 0, s, iters, 1, 0, (int *)nullptr);
+    *ops = (double)grid * 8 * iters * 16 * (2.0 * 32 * 32 * 32);
+    return hipGetLastError();
+}
 
 hipError_t launch_mfma_probe(int iters, int num_cus, hipStream_t s, double *flops)
 {

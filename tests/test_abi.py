@@ -152,14 +152,16 @@ def test_options_and_errors(vctx):
     assert lib.ivf_route(None, P(0), 1, P(GB), 1, 4, 1, P(2 * GB), None) == B.IVF_EINVAL
 
 
-def test_mfma_probe_validation(vctx):
+@pytest.mark.parametrize("fn", ["ivf_mfma_probe", "ivf_mfma_probe_i8"])
+def test_mfma_probe_validation(vctx, fn):
     lib, h = vctx.lib, vctx.handle
+    probe = getattr(lib, fn)
     ms, tf = ctypes.c_float(), ctypes.c_double()
-    assert lib.ivf_mfma_probe(h, 0, ctypes.byref(ms), ctypes.byref(tf)) == B.IVF_EINVAL
-    assert lib.ivf_mfma_probe(h, 1 << 21, ctypes.byref(ms), None) == B.IVF_EINVAL
-    assert lib.ivf_mfma_probe(h, 10, None, None) == B.IVF_EINVAL
-    assert lib.ivf_mfma_probe(h, 10, ctypes.byref(ms), None) == B.IVF_EUNSUPPORTED
-    assert lib.ivf_mfma_probe(None, 10, ctypes.byref(ms), None) == B.IVF_EINVAL
+    assert probe(h, 0, ctypes.byref(ms), ctypes.byref(tf)) == B.IVF_EINVAL
+    assert probe(h, 1 << 21, ctypes.byref(ms), None) == B.IVF_EINVAL
+    assert probe(h, 10, None, None) == B.IVF_EINVAL
+    assert probe(h, 10, ctypes.byref(ms), None) == B.IVF_EUNSUPPORTED
+    assert probe(None, 10, ctypes.byref(ms), None) == B.IVF_EINVAL
 
 
 def test_list_major_validation(vctx):
