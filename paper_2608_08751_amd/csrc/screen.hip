@@ -320,6 +320,19 @@ __device__ __forceinline__ void mfma_chunk(const float *A0, const float *Nh, con
     top1_kblocks<DP, EP>(A0, A1, b, c0, c1, a0, a1, p0, p1, idp, st);
 }
 
+// The group tests read accumulators through inline asm, which gets no wait
+// states after the MFMAs that write them; in the loop they read the previous
+// chunk's accumulators, many MFMAs later, but the last chunk's are drained
+// right after its MFMAs, so they are first copied by an add the compiler sees
+// (x + 0 is not folded: it turns -0 into +0, which the compares treat alike).
+__device__ __forceinline__ f32x16 settled(const f32x16 &p)
+{
+    f32x16 q;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) q[r] = p[r] + 0.0f;
+    return q;
+}
+
 template <int G = 0>
 __device__ __forceinline__ void top1_drain(const f32x16 &p0, const f32x16 &p1, int idp, Top3 &st)
 {
@@ -423,9 +436,9 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     }
     if (j < nch) {
         step(j, y0, y1, x0, x1);
-        top1_drain(y0, y1, idh + j * kChunk, st);
+        top1_drain(settled(y0), settled(y1), idh + j * kChunk, st);
     } else {
-        top1_drain(x0, x1, idh + (j - 1) * kChunk, st);
+        top1_drain(settled(x0), settled(x1), idh + (j - 1) * kChunk, st);
     }
     // back to keys: key = -2 v exactly, ascending
     st.k1 *= -2.0f;

@@ -205,19 +205,17 @@ __device__ __forceinline__ int keep_threshold(const Top3i &st)
     return st.k1 > kNoScore ? max(st.k3, st.k1 - st.twoR - 1) : kNoScore;
 }
 
+// Plain integer expressions (the compiler forms v_med3_i32 and v_max3_i32
+// from them): the operands include MFMA results, and only instructions the
+// compiler sees get the wait states that reading them requires.
 __device__ __forceinline__ int med3i(int a, int b, int c)
 {
-    int m;
-    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
-    return m;
+    return min(max(a, b), max(min(a, b), c));
 }
 
 __device__ __forceinline__ int max4i(int a, int b, int c, int d)
 {
-    int m;
-    asm("v_max3_i32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
-    asm("v_max_i32 %0, %1, %2" : "=v"(m) : "v"(m), "v"(d));
-    return m;
+    return max(max(max(a, b), c), d);
 }
 
 // Branch-free insertion (v <= k3 leaves the state unchanged): with
