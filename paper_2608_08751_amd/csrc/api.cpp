@@ -202,6 +202,8 @@ struct AssignLayout {
     int32_t *negb;
     int32_t *wl;
     int64_t wl_cap;
+    double *fb_d;   // split fallback partial results
+    int32_t *fb_i;
     // build
     uint32_t *cntmat;
     int64_t *counts;
@@ -255,6 +257,8 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_
     }
     l.wl_cap = worklist_cap(N);
     l.wl = c.take<int32_t>(l.wl_cap);
+    l.fb_d = c.take<double>(kFbSplitEntries);
+    l.fb_i = c.take<int32_t>(kFbSplitEntries);
     if (need_build) {
         if (C <= kRadixMaxLists)
             l.cntmat = (uint32_t *)c.take<unsigned char>(radix_scratch_bytes(plan_radix(N, C, num_cus)));
@@ -411,7 +415,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     }
     TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));
     TIMED("assign_fallback", launch_assign_fallback(rows, rowtype, N, D, cent, C, labels, l.wl, l.sc.wl_cnt, l.wl_cap,
-                                   2 * ctx->num_cus, s));
+                                                    l.fb_d, l.fb_i, 2 * ctx->num_cus, s));
     ctx->last_stats = l.sc.stats;
     ctx->last_sample = 0;
     return IVF_OK;

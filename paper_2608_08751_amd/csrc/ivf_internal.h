@@ -123,10 +123,17 @@ hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s);
 hipError_t launch_route_select(const RouteArgs &a, hipStream_t s);
 hipError_t launch_route_fallback(const RouteArgs &a, int grid, hipStream_t s);
 
+// Exact fp64 scan of the rows on the assignment worklist (labels -1). The
+// first kFbSplitWindows windows of 8 rows are split into kFbSeg centroid
+// segments over the whole grid; split_d / split_i hold their partial
+// results (kFbSplitWindows * kFbSeg * 8 entries each).
+constexpr int kFbSplitWindows = 256;
+constexpr int kFbSeg = 64;
+constexpr int64_t kFbSplitEntries = (int64_t)kFbSplitWindows * kFbSeg * 8;
 hipError_t launch_assign_fallback(const void *rows, int rowtype, int64_t N, int D,
                                   const float *cent, int64_t C, int32_t *labels,
                                   const int32_t *wl, const uint32_t *wl_cnt, int64_t wl_cap,
-                                  int grid, hipStream_t s);
+                                  double *split_d, int32_t *split_i, int grid, hipStream_t s);
 
 // ---- inverted-list build (lists.hip) ---------------------------------------
 constexpr int kSlice = 16384;    // buckets per workgroup (LDS counters)

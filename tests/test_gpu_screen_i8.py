@@ -160,15 +160,20 @@ def test_i8_kmeans_step_both_paths(ivf_ctx, oracle_mod):
         c = ocen
 
 
-def test_i8_forced_fallback_is_identical(ivf_ctx, oracle_mod):
+@pytest.mark.parametrize("N", [1500, 3000, 5000])
+def test_i8_forced_fallback_is_identical(ivf_ctx, oracle_mod, N):
+    """Every row through the exact fallback scan: 1,500 rows fit the
+    centroid-split windows, 3,000 also use the whole-row windows, and 5,000
+    overflow the worklist (min(N, 4096 + N / 64) entries), so the scan finds
+    the rows by their -1 labels."""
     import paper_2608_08751_amd as ivf
 
-    x, c = rows_and_centroids(1500, 90, 128, seed=13)
+    x, c = rows_and_centroids(N, 90, 128, seed=13)
     olab = oracle_mod.assign(x, c)
     ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 1)
     try:
         lab, _, _, _, st = gpu_assign(ivf_ctx, x, c)
     finally:
         ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 0)
-    assert st["screen_i8"] == 1 and st["fallback"] == 1500
+    assert st["screen_i8"] == 1 and st["fallback"] == N
     assert (lab == olab).all()
