@@ -1,0 +1,135 @@
+"""The two-plane int8 screening kernel (screen_i8.hip) built for the host
+against a wave64 emulation (tests/wave_emu: one host thread per lane, the int8
+MFMA's operand layout, barriers for the wave and the block) and run under
+AddressSanitizer: every row the screen settles carries the oracle's label,
+the others are exactly the fallback worklist, and no access leaves its
+allocation. No GPU is involved; this checks the kernel's arithmetic,
+indexing and synchronisation, not the compiled gfx950 code."""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import synth
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(os.path.dirname(HERE), "paper_2608_08751_amd", "csrc")
+CLANG = "/opt/rocm/llvm/bin/clang++"
+UNWRITTEN = 0x7F7F7F7F
+
+
+def strip_fences(src: str) -> str:
+    """The source without its empty asm statements (scheduling fences for the
+    GPU compiler; their register constraints do not exist on the host)."""
+    out, i = [], 0
+    while True:
+        j = src.find("asm volatile(", i)
+        if j < 0:
+            out.append(src[i:])
+            return "".join(out)
+        out.append(src[i:j])
+        k, depth = j + len("asm volatile("), 1
+        while depth:
+            depth += {"(": 1, ")": -1}.get(src[k], 0)
+            k += 1
+        assert src[k] == ";"
+        i = k + 1
+
+
+@pytest.fixture(scope="module")
+def emu_bin(tmp_path_factory):
+    if not os.path.exists(CLANG):
+        pytest.skip("clang++ of the ROCm toolchain not found")
+    d = tmp_path_factory.mktemp("wave_emu")
+    with open(os.path.join(CSRC, "screen_i8.hip")) as f:
+        src = strip_fences(f.read())
+    with open(d / "screen_i8_host_src.hip", "w") as f:
+        f.write(src)
+    exe = str(d / "screen_i8_host")
+    cmd = [CLANG, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer",
+           "-I", os.path.join(HERE, "wave_emu"), "-I", str(d), "-I", CSRC,
+           os.path.join(HERE, "wave_emu", "screen_i8_host.cpp"), "-o", exe, "-lpthread"]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stderr[-4000:]
+    return exe
+
+
+def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0):
+    N, D = x.shape
+    src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
+    with open(src, "wb") as f:
+        np.array([N, c.shape[0], D], np.int64).tofile(f)
+        np.ascontiguousarray(x, np.uint8).tofile(f)
+        np.ascontiguousarray(c, np.float32).tofile(f)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
+    r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback)], capture_output=True,
+                       text=True, timeout=900, env=env)
+    assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-6000:]
+    raw = np.fromfile(dst, np.uint8)
+    lab = raw[: 4 * N].view(np.int32)
+    n = int(raw[4 * N: 4 * N + 4].view(np.uint32)[0])
+    o = 4 * N + 4
+    wl = raw[o: o + 4 * n].view(np.int32)
+    o += 4 * n
+    stats = raw[o: o + 64].view(np.uint64)
+    q_bad = int(raw[o + 64: o + 68].view(np.uint32)[0])
+    return lab, wl, stats, q_bad
+
+
+def rows_and_centroids(N, C, D, seed):
+    rng = np.random.default_rng(seed)
+    means = rng.uniform(0.0, 255.0, size=(max(C // 2, 1), D)).astype(np.float32)
+    x, _ = synth.mixture_rows_u8(means, 0, N, seed=seed)
+    if C <= N:
+        c = x[rng.choice(N, C, replace=False)].astype(np.float32)
+    else:
+        c = rng.uniform(0.0, 255.0, size=(C, D)).astype(np.float32)
+    c += rng.uniform(-0.5, 0.5, size=c.shape).astype(np.float32)
+    np.clip(c, 0.0, 255.0, out=c)
+    return x, c
+
+
+def check(oracle_mod, lab, wl, stats, x, c):
+    olab = oracle_mod.assign(x, c)
+    assert not (lab == UNWRITTEN).any(), "labels never written"
+    fb = np.nonzero(lab == -1)[0]
+    assert np.array_equal(np.sort(wl), fb), "worklist differs from the unsettled rows"
+    settled = lab != -1
+    bad = np.nonzero(lab[settled] != olab[settled])[0]
+    assert bad.size == 0, "labels differ at rows %s" % np.nonzero(settled)[0][bad[:10]]
+    assert int(stats[0]) == fb.size and int(stats[5]) == 1
+
+
+@pytest.mark.parametrize("N,C,D,cus", [(1500, 130, 128, 3), (700, 3, 96, 2), (1100, 65, 256, 3), (600, 70, 36, 1)])
+def test_emulated_screen_matches_oracle(emu_bin, tmp_path, oracle_mod, N, C, D, cus):
+    """Several row tiles per workgroup (persistent loop), ragged last tiles,
+    C not a multiple of the 64-centroid chunk, and each padded width."""
+    x, c = rows_and_centroids(N, C, D, seed=N + C + D)
+    lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c, num_cus=cus)
+    assert q_bad == 0
+    check(oracle_mod, lab, wl, stats, x, c)
+
+
+def test_emulated_near_ties(emu_bin, tmp_path, oracle_mod):
+    """Pairs of nearly equal centroids (two candidates: the exact fp64
+    evaluation) and crowds of five (the fallback worklist)."""
+    rng = np.random.default_rng(11)
+    D = 64
+    pa = rng.integers(20, 236, size=(15, D)).astype(np.float32)
+    cr = rng.integers(20, 236, size=(15, D)).astype(np.float32)
+    c = np.vstack([pa, pa + 1e-3, cr, cr.copy(), cr + 1e-3, cr - 1.0 / 512, cr + 0.5]).astype(np.float32)
+    x = np.vstack([np.rint(pa), np.rint(pa + 0.25), np.rint(cr), rng.integers(0, 256, size=(200, D))])
+    x = np.clip(x, 0, 255).astype(np.uint8)
+    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c)
+    check(oracle_mod, lab, wl, stats, x, c)
+    assert int(stats[0]) > 0 and int(stats[1]) > 0
+
+
+def test_emulated_forced_fallback_and_unquantisable(emu_bin, tmp_path, oracle_mod):
+    x, c = rows_and_centroids(800, 40, 128, seed=5)
+    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c, force_fallback=1)
+    assert (lab == -1).all() and np.array_equal(np.sort(wl), np.arange(800)) and int(stats[0]) == 800
+    c[7, 3] = 256.0  # outside the 16-bit fixed point: the kernel stands down
+    lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c)
+    assert q_bad == 1 and (lab == UNWRITTEN).all() and wl.size == 0 and int(stats[5]) == 0

@@ -1,0 +1,208 @@
+// Host emulation of the HIP device environment used by the int8 screening
+// kernels (test infrastructure only; the library never runs on the host).
+// One host thread per lane; wave-collective operations (__shfl_xor, __any,
+// the int8 MFMA) exchange values through a per-wave barrier, __syncthreads is
+// a per-block barrier, and blocks of a grid run one after another. Buffer
+// loads honour the resource's byte range like the hardware (zero past the
+// end); every other access is a plain host access, so AddressSanitizer
+// reports any that leaves its allocation.
+#pragma once
+#include <stdint.h>
+#include <string.h>
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <algorithm>
+#include <atomic>
+#include <barrier>
+#include <thread>
+#include <vector>
+#include <functional>
+#include <climits>
+
+struct dim3 {
+    unsigned x = 1, y = 1, z = 1;
+    dim3() {}
+    dim3(unsigned a, unsigned b = 1, unsigned c = 1) : x(a), y(b), z(c) {}
+};
+struct uint2 {
+    unsigned x, y;
+};
+typedef int hipError_t;
+typedef void *hipStream_t;
+enum { hipSuccess = 0, hipErrorInvalidValue = 1 };
+inline hipError_t hipGetLastError() { return hipSuccess; }
+
+namespace emu {
+extern thread_local dim3 tid, bid;
+extern dim3 bdim, gdim;
+struct Wave {
+    std::barrier<> *bar;
+    unsigned char buf[64][128];
+};
+struct Block {
+    std::barrier<> *bar;
+    Wave waves[16];
+};
+extern Block *blk;
+inline Wave &wave() { return blk->waves[tid.x / 64]; }
+inline int lane() { return tid.x % 64; }
+}  // namespace emu
+
+#define threadIdx (emu::tid)
+#define blockIdx (emu::bid)
+#define blockDim (emu::bdim)
+#define gridDim (emu::gdim)
+#define __global__
+#define __device__
+#define __host__
+#define __forceinline__ inline
+#define __launch_bounds__(...)
+#define __shared__ static
+#define HIP_SYMBOL(x) (x)
+
+inline int max(int a, int b) { return a > b ? a : b; }
+inline int min(int a, int b) { return a < b ? a : b; }
+inline unsigned max(unsigned a, unsigned b) { return a > b ? a : b; }
+inline unsigned min(unsigned a, unsigned b) { return a < b ? a : b; }
+inline long long max(long long a, long long b) { return a > b ? a : b; }
+inline long long min(long long a, long long b) { return a < b ? a : b; }
+inline long max(long a, long b) { return a > b ? a : b; }
+inline long min(long a, long b) { return a < b ? a : b; }
+
+inline void __syncthreads() { emu::blk->bar->arrive_and_wait(); }
+
+template <typename T>
+inline T __shfl_xor(T v, int m)
+{
+    static_assert(sizeof(T) <= 128, "");
+    emu::Wave &w = emu::wave();
+    memcpy(w.buf[emu::lane()], &v, sizeof(T));
+    w.bar->arrive_and_wait();
+    T r;
+    memcpy(&r, w.buf[emu::lane() ^ m], sizeof(T));
+    w.bar->arrive_and_wait();
+    return r;
+}
+
+inline int __any(int p)
+{
+    emu::Wave &w = emu::wave();
+    w.buf[emu::lane()][0] = p ? 1 : 0;
+    w.bar->arrive_and_wait();
+    int r = 0;
+    for (int i = 0; i < 64; ++i) r |= w.buf[i][0];
+    w.bar->arrive_and_wait();
+    return r;
+}
+
+typedef int emu_i32x4 __attribute__((ext_vector_type(4)));
+typedef int emu_i32x16 __attribute__((ext_vector_type(16)));
+
+// v_mfma_i32_32x32x32_i8: lane l supplies A[l % 32][16 (l / 32) + 0..15] and
+// B[k][l % 32] for k = 16 (l / 32) + 0..15; output register r of lane l is
+// D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+inline emu_i32x16 __builtin_amdgcn_mfma_i32_32x32x32_i8(emu_i32x4 a, emu_i32x4 b, emu_i32x16 c, int, int, int)
+{
+    emu::Wave &w = emu::wave();
+    const int l = emu::lane();
+    memcpy(w.buf[l], &a, 16);
+    memcpy(w.buf[l] + 16, &b, 16);
+    w.bar->arrive_and_wait();
+    emu_i32x16 d;
+    for (int r = 0; r < 16; ++r) {
+        const int i = 8 * (r / 4) + 4 * (l / 32) + r % 4, j = l % 32;
+        int s = 0;
+        for (int k = 0; k < 32; ++k) {
+            const int8_t av = (int8_t)w.buf[i + 32 * (k / 16)][k % 16];
+            const int8_t bv = (int8_t)w.buf[j + 32 * (k / 16)][16 + k % 16];
+            s += (int)av * (int)bv;
+        }
+        d[r] = (int)((uint32_t)s + (uint32_t)c[r]);
+    }
+    w.bar->arrive_and_wait();
+    return d;
+}
+
+inline uint32_t __builtin_amdgcn_sad_u8(uint32_t a, uint32_t b, uint32_t c)
+{
+    for (int i = 0; i < 4; ++i) {
+        const int x = (a >> (8 * i)) & 255, y = (b >> (8 * i)) & 255;
+        c += x > y ? x - y : y - x;
+    }
+    return c;
+}
+
+struct __amdgpu_buffer_rsrc_t {
+    const char *base;
+    int64_t num;
+};
+inline __amdgpu_buffer_rsrc_t __builtin_amdgcn_make_buffer_rsrc(void *p, short, int num, int)
+{
+    return {(const char *)p, (int64_t)(unsigned)num};
+}
+// raw buffer loads: each dword past num_records reads zero (and is never touched)
+inline emu_i32x4 __builtin_amdgcn_raw_buffer_load_b128(__amdgpu_buffer_rsrc_t r, int off, int soff, int)
+{
+    emu_i32x4 v = {0, 0, 0, 0};
+    for (int i = 0; i < 4; ++i) {
+        const int64_t o = (int64_t)(unsigned)off + soff + 4 * i;
+        int t = 0;
+        if (o + 4 <= r.num) memcpy(&t, r.base + o, 4);
+        v[i] = t;
+    }
+    return v;
+}
+inline uint32_t __builtin_amdgcn_raw_buffer_load_b32(__amdgpu_buffer_rsrc_t r, int off, int soff, int)
+{
+    uint32_t v = 0;
+    const int64_t o = (int64_t)(unsigned)off + soff;
+    if (o + 4 <= r.num) memcpy(&v, r.base + o, 4);
+    return v;
+}
+inline void __builtin_amdgcn_sched_barrier(int) {}
+
+template <typename T>
+inline T atomicAdd(T *p, T v) { return __atomic_fetch_add(p, v, __ATOMIC_SEQ_CST); }
+inline unsigned long long atomicAdd(unsigned long long *p, unsigned long long v)
+{
+    return __atomic_fetch_add(p, v, __ATOMIC_SEQ_CST);
+}
+inline uint32_t atomicMax(uint32_t *p, uint32_t v)
+{
+    uint32_t o = __atomic_load_n(p, __ATOMIC_SEQ_CST);
+    while (o < v && !__atomic_compare_exchange_n(p, &o, v, false, __ATOMIC_SEQ_CST, __ATOMIC_SEQ_CST)) {}
+    return o;
+}
+
+namespace emu {
+// runs every block of the grid, one after another, with one host thread per lane
+template <typename K, typename... A>
+void launch(K kernel, dim3 grid, dim3 block, A... args)
+{
+    gdim = grid;
+    bdim = block;
+    const int nt = block.x;
+    for (unsigned b = 0; b < grid.x; ++b) {
+        Block B;
+        std::barrier<> bb(nt);
+        B.bar = &bb;
+        std::vector<std::barrier<> *> wb;
+        for (int w = 0; w < (nt + 63) / 64; ++w) {
+            wb.push_back(new std::barrier<>(std::min(64, nt - 64 * w)));
+            B.waves[w].bar = wb.back();
+        }
+        blk = &B;
+        std::vector<std::thread> th;
+        for (int t = 0; t < nt; ++t)
+            th.emplace_back([=]() {
+                tid = dim3(t);
+                bid = dim3(b);
+                kernel(args...);
+            });
+        for (auto &t : th) t.join();
+        for (auto *p : wb) delete p;
+    }
+}
+}  // namespace emu
+#define hipLaunchKernelGGL(k, g, b, sh, s, ...) emu::launch(k, g, b, __VA_ARGS__)

@@ -1,0 +1,86 @@
+// Runs the int8 screening kernels of screen_i8.hip on the host emulation, in
+// the order the library enqueues them for uint8 rows (quantisation, then the
+// screen), on one case file, with every array in an allocation of its own.
+// Writes the labels, the worklist and the statistics for the test to check
+// against the oracle; the fallback scan that follows in the library (another
+// source file) is not run, so rows it would settle keep the label -1.
+//   usage: screen_i8_host in.bin out.bin num_cus force_fallback
+//   in:  int64 N, C, D; uint8 rows [N][D]; float centroids [C][D]
+//   out: int32 labels [N]; uint32 worklist count; int32 worklist [count];
+//        uint64 stats [8]; uint32 quantisation flag
+#include "hip/hip_runtime.h"
+namespace emu {
+thread_local dim3 tid, bid;
+dim3 bdim, gdim;
+Block *blk;
+}  // namespace emu
+#include "screen_i8_host_src.hip"
+using namespace ivf;
+
+template <typename T>
+static T *alloc(size_t n, int fill)
+{
+    const size_t b = std::max<size_t>(n, 1) * sizeof(T);
+    T *p = (T *)malloc(b);
+    memset(p, fill, b);
+    return p;
+}
+
+int main(int argc, char **argv)
+{
+    if (argc < 5) return 2;
+    FILE *f = fopen(argv[1], "rb");
+    if (!f) return 2;
+    int64_t hdr[3];
+    if (fread(hdr, 8, 3, f) != 3) return 2;
+    const int64_t N = hdr[0], C = hdr[1];
+    const int D = (int)hdr[2];
+    uint8_t *x = alloc<uint8_t>(N * D, 0);
+    float *cent = alloc<float>(C * D, 0);
+    if (fread(x, 1, N * D, f) != (size_t)(N * D) || fread(cent, 4, C * D, f) != (size_t)(C * D)) return 2;
+    fclose(f);
+    const int num_cus = atoi(argv[3]);
+    int DP = 0;
+    for (int dp : {32, 64, 96, 128, 192, 256})
+        if (!DP && D <= dp) DP = dp;
+    if (!DP || D % 4) return 2;
+    const int64_t cpad = quantized_pad(C);
+    const int64_t wl_cap = std::min<int64_t>(N, 4096 + N / 64);
+    int8_t *qc = alloc<int8_t>(cpad * 2 * DP, 0);
+    int32_t *negb = alloc<int32_t>(cpad, 0);
+    uint32_t *q_bad = alloc<uint32_t>(1, 0);
+    uint32_t *wl_cnt = alloc<uint32_t>(1, 0);
+    int32_t *wl = alloc<int32_t>(wl_cap, 0);
+    int32_t *labels = alloc<int32_t>(N, 0x7f);  // 0x7f7f7f7f marks a label never written
+    unsigned long long *stats = alloc<unsigned long long>(8, 0);
+
+    launch_quantize_centroids(cent, C, D, DP, qc, negb, q_bad, nullptr);
+    ScreenI8Args a{};
+    a.rows = x;
+    a.nrows = N;
+    a.D = D;
+    a.cent = cent;
+    a.qc = qc;
+    a.negb = negb;
+    a.cpad = cpad;
+    a.nchunks = cpad / 64;
+    a.q_bad = q_bad;
+    a.labels = labels;
+    a.wl = wl;
+    a.wl_cnt = wl_cnt;
+    a.wl_cap = wl_cap;
+    a.stats = stats;
+    a.force_fallback = atoi(argv[4]);
+    launch_screen_i8(DP, a, num_cus, nullptr);
+
+    FILE *o = fopen(argv[2], "wb");
+    if (!o) return 2;
+    const uint32_t n = std::min<uint32_t>(*wl_cnt, (uint32_t)wl_cap);
+    fwrite(labels, 4, N, o);
+    fwrite(&n, 4, 1, o);
+    fwrite(wl, 4, n, o);
+    fwrite(stats, 8, 8, o);
+    fwrite(q_bad, 4, 1, o);
+    fclose(o);
+    return 0;
+}
