@@ -95,58 +95,71 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__
 }
 
 // ------------------------------------------------------------ staging
-// A chunk of kQChunk quantised centroids (both planes) and their biases,
-// copied from the padded global arrays into LDS with a row pitch of
-// 2 DP + 16 bytes (the 16 spread the rows over the banks). Loads go through a
-// buffer resource over the chunk, so the chunk after the last one reads
-// zeros and every load stays unconditional.
+// A chunk of kQChunk quantised centroids (both planes) and their biases is
+// copied from the padded global arrays straight into LDS by buffer loads with
+// an LDS destination (16 bytes per lane, a wave writes 1 KiB of consecutive
+// LDS per instruction): no register staging and no LDS stores by the vector
+// unit. LDS layout of a chunk: centroid rows with a pitch of 2 DP + 16 bytes
+// (the 16 spread the rows over the banks), then the 64 biases. Slot s
+// (16 bytes) of the row area holds unit s % (DP / 8 + 1) of row
+// s / (DP / 8 + 1); the pad unit and the bias instruction's lanes past the
+// biases read beyond the buffer range and receive zeros. Loads go through
+// buffer resources over the chunk's valid rows, so a ragged last chunk and
+// the chunk after the last one read zeros and every load is unconditional.
+// The loads of a chunk are complete (and visible to every wave) after the
+// next workgroup barrier, which waits for all outstanding vector memory
+// operations.
 template <int DP, int NT>
 struct QStager {
-    static constexpr int kRowU = DP / 8;            // 16-byte units per centroid
-    static constexpr int kU = kQChunk * kRowU;      // units per chunk
-    static constexpr int kUPT = (kU + NT - 1) / NT;
+    static constexpr int kRowU = DP / 8;                 // 16-byte units per centroid
     static constexpr int kPitch = 2 * DP + 16;
-    static constexpr int kBias = kQChunk * kPitch;  // byte offset of the biases
-    static constexpr int kBytes = kBias + 4 * kQChunk;
-    int goff[kUPT];
-    int loff[kUPT];
-    i32x4 v[kUPT];
-    i32x4 b;
+    static constexpr int kRowInst = kRowU + 1;           // 64 rows x (kRowU + 1) slots / 64 lanes
+    static constexpr int kInst = kRowInst + 1;           // plus one for the biases
+    static constexpr int kBias = kQChunk * kPitch;       // byte offset of the biases (= kRowInst KiB)
+    static constexpr int kBytes = kInst * 1024;
+    static constexpr int kW = NT / 64;
+    static constexpr int kIPW = (kInst + kW - 1) / kW;   // load instructions per wave
+    int voff[kIPW];
+    int wave;  // wave-uniform
 
     __device__ __forceinline__ void init()
     {
+        const int lane = threadIdx.x & 63;
+        wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 #pragma unroll
-        for (int i = 0; i < kUPT; ++i) {
-            const int u = threadIdx.x + i * NT;
-            goff[i] = u < kU ? 16 * u : (1 << 30);
-            loff[i] = (u / kRowU) * kPitch + (u % kRowU) * 16;
+        for (int i = 0; i < kIPW; ++i) {
+            const int inst = wave + i * kW;
+            int off = 1 << 30;  // beyond any buffer range: reads zero
+            if (inst < kRowInst) {
+                const int slot = 64 * inst + lane;
+                const int r = slot / (kRowU + 1), u = slot % (kRowU + 1);
+                if (u < kRowU) off = r * 2 * DP + 16 * u;
+            } else if (inst == kRowInst && lane < kQChunk / 4) {
+                off = 16 * lane;
+            }
+            voff[i] = off;
         }
     }
 
+    // Enqueues the loads of the chunk starting at centroid cbase into the LDS
+    // buffer buf.
     __device__ __forceinline__ void fetch(const int8_t *__restrict__ qc, const int32_t *__restrict__ negb,
-                                          int64_t cbase, int64_t cpad)
+                                          int64_t cbase, int64_t cpad, char *buf) const
     {
         const int64_t left = cpad - cbase;
         const int valid = (int)(left < 0 ? 0 : left < kQChunk ? left : kQChunk);
         const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<int8_t *>(qc + cbase * 2 * DP), (short)0, valid * 2 * DP, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<int32_t *>(negb + cbase), (short)0, valid * 4, 0x00020000);
 #pragma unroll
-        for (int i = 0; i < kUPT; ++i)
-            v[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, goff[i], 0, 0));
-        if (threadIdx.x < kQChunk / 4) {
-            const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-                const_cast<int32_t *>(negb + cbase), (short)0, valid * 4, 0x00020000);
-            b = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rb, 16 * threadIdx.x, 0, 0));
+        for (int i = 0; i < kIPW; ++i) {
+            const int inst = wave + i * kW;
+            if (inst < kInst)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(inst < kRowInst ? rq : rb,
+                                                         (__attribute__((address_space(3))) void *)(buf + inst * 1024),
+                                                         16, voff[i], 0, 0, 0);
         }
-    }
-
-    __device__ __forceinline__ void store(char *__restrict__ lds) const
-    {
-#pragma unroll
-        for (int i = 0; i < kUPT; ++i)
-            if (kU % NT == 0 || (int)threadIdx.x + i * NT < kU)
-                *reinterpret_cast<i32x4 *>(lds + loff[i]) = v[i];
-        if (threadIdx.x < kQChunk / 4) *reinterpret_cast<i32x4 *>(lds + kBias + 16 * threadIdx.x) = b;
     }
 };
 
@@ -409,10 +422,11 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
 // within a block row block by row block, alternating between the
 // accumulator sets T0 and T1; each tile's K-steps carry the epilogue of the
 // tile before it, and the last tile of a block loads the next block's
-// fragments and biases. Chunk j + 1 is written to LDS just before the last
-// tile of chunk j, the only one that reads it (its buffer was last read
-// before the previous such barrier), and chunk j + 2 is fetched right after,
-// a whole chunk ahead of its store. The loop is rotated so that an
+// fragments and biases. The barrier before the last tile of chunk j, the
+// first tile that reads chunk j + 1, completes the loads of chunk j + 1
+// (issued right after the previous such barrier) and ends every read of
+// chunk j's buffer, whose loads for chunk j + 2 are issued right after it, a
+// whole chunk ahead of their first use. The loop is rotated so that an
 // iteration starts right after a barrier (no LDS read outstanding) with the
 // last tile of chunk j, then runs chunk j + 1 up to its last tile; all LDS
 // waits inside are then exact.
@@ -450,15 +464,14 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 
     St q;
     q.init();
-    q.fetch(a.qc, a.negb, 0, a.cpad);
-    q.store(lds);
+    q.fetch(a.qc, a.negb, 0, a.cpad, lds);
     __syncthreads();
-    q.fetch(a.qc, a.negb, kQChunk, a.cpad);
-    // stores chunk jj into its buffer, then fetches chunk jj + 1
+    q.fetch(a.qc, a.negb, kQChunk, a.cpad, lds + CS);
+    // the barrier completes the loads of chunk jj (issued one stage earlier)
+    // and ends every read of the other buffer, which then receives chunk jj + 1
     auto stage = [&](int jj) {
-        q.store(lds + (jj & 1) * CS);
         __syncthreads();
-        q.fetch(a.qc, a.negb, (int64_t)(jj + 1) * kQChunk, a.cpad);
+        q.fetch(a.qc, a.negb, (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
     };
 
     // T1 starts as a tile of lowest scores, so the first epilogue inserts nothing

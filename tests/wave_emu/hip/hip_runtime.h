@@ -1,11 +1,14 @@
 // Host emulation of the HIP device environment used by the int8 screening
 // kernels (test infrastructure only; the library never runs on the host).
 // One host thread per lane; wave-collective operations (__shfl_xor, __any,
-// the int8 MFMA) exchange values through a per-wave barrier, __syncthreads is
-// a per-block barrier, and blocks of a grid run one after another. Buffer
-// loads honour the resource's byte range like the hardware (zero past the
-// end); every other access is a plain host access, so AddressSanitizer
-// reports any that leaves its allocation.
+// readfirstlane, the int8 MFMA) exchange values through a per-wave barrier,
+// __syncthreads is a per-block barrier, and blocks of a grid run one after
+// another. Buffer loads honour the resource's byte range like the hardware
+// (zero past the end); every other access is a plain host access, so
+// AddressSanitizer reports any that leaves its allocation. Buffer loads with
+// an LDS destination are asynchronous like on the device: the destination is
+// poisoned when the load is issued and receives its data only at the next
+// __syncthreads, so a read of it before that barrier sees the poison.
 #pragma once
 #include <stdint.h>
 #include <string.h>
@@ -19,6 +22,8 @@
 #include <vector>
 #include <functional>
 #include <climits>
+#include <array>
+#include <mutex>
 
 struct dim3 {
     unsigned x = 1, y = 1, z = 1;
@@ -40,11 +45,21 @@ struct Wave {
     std::barrier<> *bar;
     unsigned char buf[64][128];
 };
+struct DmaFlush {
+    void operator()() noexcept;
+};
 struct Block {
-    std::barrier<> *bar;
+    std::barrier<DmaFlush> *bar;
     Wave waves[16];
+    std::mutex mu;
+    std::vector<std::pair<char *, std::array<char, 16>>> pending;  // LDS writes of in-flight loads
 };
 extern Block *blk;
+inline void DmaFlush::operator()() noexcept
+{
+    for (auto &p : blk->pending) memcpy(p.first, p.second.data(), 16);
+    blk->pending.clear();
+}
 inline Wave &wave() { return blk->waves[tid.x / 64]; }
 inline int lane() { return tid.x % 64; }
 }  // namespace emu
@@ -160,6 +175,33 @@ inline uint32_t __builtin_amdgcn_raw_buffer_load_b32(__amdgpu_buffer_rsrc_t r, i
     if (o + 4 <= r.num) memcpy(&v, r.base + o, 4);
     return v;
 }
+// 16-byte buffer load into LDS: lane l writes lds + 16 l; the data lands at
+// the next __syncthreads, the destination holds a poison pattern until then
+template <typename P>
+inline void __builtin_amdgcn_raw_ptr_buffer_load_lds(__amdgpu_buffer_rsrc_t r, P lds, unsigned size, int off,
+                                                     int soff, int ioff, int)
+{
+    if (size != 16) abort();
+    const emu_i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0);
+    char *dst = (char *)(uintptr_t)lds + ioff + 16 * emu::lane();
+    std::array<char, 16> d;
+    memcpy(d.data(), &v, 16);
+    memset(dst, 0x5A, 16);
+    std::lock_guard<std::mutex> g(emu::blk->mu);
+    emu::blk->pending.push_back({dst, d});
+}
+
+inline int __builtin_amdgcn_readfirstlane(int v)
+{
+    emu::Wave &w = emu::wave();
+    memcpy(w.buf[emu::lane()], &v, sizeof(int));
+    w.bar->arrive_and_wait();
+    int r;
+    memcpy(&r, w.buf[0], sizeof(int));
+    w.bar->arrive_and_wait();
+    return r;
+}
+
 inline void __builtin_amdgcn_sched_barrier(int) {}
 
 template <typename T>
@@ -185,7 +227,7 @@ void launch(K kernel, dim3 grid, dim3 block, A... args)
     const int nt = block.x;
     for (unsigned b = 0; b < grid.x; ++b) {
         Block B;
-        std::barrier<> bb(nt);
+        std::barrier<DmaFlush> bb(nt);
         B.bar = &bb;
         std::vector<std::barrier<> *> wb;
         for (int w = 0; w < (nt + 63) / 64; ++w) {
