@@ -4,9 +4,10 @@
 One step = one pass of the whole hot path over one batch of synthetic input,
 on the 65,536-centroid, D = 128 index of the uint8-valued workloads:
   1. ivf_kmeans_step  on 10M uint8 training rows (centroid quantisation,
-                      fused int8-MFMA screening with register top-1,
-                      certified fp64 refine, list build, Lloyd update with
-                      reseeding, objective);
+                      fused single-plane int8-MFMA screening with register
+                      top-1, certified fp64 refine, two-plane int8 screen of
+                      the rows the single plane leaves, list build, Lloyd
+                      update with reseeding, objective);
   2. ivf_assign_build on a batch of 10M uint8 base rows with the new
                       centroids (full assignment + histogram / scan / stable
                       scatter into cluster-major lists);
@@ -57,6 +58,8 @@ def parse():
                     help="also run one device copy of this size (HBM counter calibration for rocprofv3)")
     ap.add_argument("--fp32-screen", action="store_true",
                     help="screen the uint8 rows on fp32 MFMA (IVF_OPT_FP32_SCREEN) instead of int8")
+    ap.add_argument("--two-plane", action="store_true",
+                    help="screen the uint8 rows on two int8 planes only (IVF_OPT_I8_TWO_PLANE_ONLY)")
     return ap.parse_args()
 
 
@@ -112,7 +115,12 @@ def main():
     ctx = ivf.Context(0)
     if args.fp32_screen:
         ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 1)
-    top1_name = "screen_top1" if args.fp32_screen else "screen_top1_i8"
+        top1_name = "screen_top1"
+    elif args.two_plane:
+        ctx.set_option(ivf.IVF_OPT_I8_TWO_PLANE_ONLY, 1)
+        top1_name = "screen_top1_i8"
+    else:
+        top1_name = "screen_top1_i8s"
     lab_t = torch.empty(Nt, dtype=torch.int32, device=dev)
     c1 = torch.empty((C, D), dtype=torch.float32, device=dev)
     cnt_t = torch.empty(C, dtype=torch.int64, device=dev)
@@ -186,9 +194,9 @@ def main():
             "avg_launch_ms": sum(top1) / len(top1),
         }
         _, probe = ctx.mfma_probe()
-    else:
-        # the int8 screen runs two int8 MFMA planes per centroid: it executes
-        # twice the algorithmic operations on the int8 pipe
+    elif args.two_plane:
+        # the two-plane int8 screen runs two int8 MFMA planes per centroid: it
+        # executes twice the algorithmic operations on the int8 pipe
         roofline = {
             "bound": "mfma",
             "achieved": achieved,
@@ -196,10 +204,26 @@ def main():
             "unit": "TOP/s",
             "frac": achieved / PEAK_INT8_MFMA_TOPS,
             "traffic": measured_traffic(Nt, "screen_top1_traffic.json"),
-            "kernel": "screen_i8_kernel<128, 8> (int8 MFMA)",
+            "kernel": "screen_i8_kernel<128, 8> (two-plane int8 MFMA)",
             "ops_per_launch": 2.0 * C * D * Nt,
             "executed_int8_ops_per_launch": 2 * 2.0 * C * D * Nt,
             "executed_frac": 2 * achieved / PEAK_INT8_MFMA_TOPS,
+            "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+            "avg_launch_ms": sum(top1) / len(top1),
+        }
+        _, probe = ctx.mfma_probe_i8()
+    else:
+        # the single-plane int8 screen executes exactly the algorithmic
+        # operations (one int8 plane per centroid)
+        roofline = {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_INT8_MFMA_TOPS,
+            "unit": "TOP/s",
+            "frac": achieved / PEAK_INT8_MFMA_TOPS,
+            "traffic": measured_traffic(Nt, "screen_top1_i8s_traffic.json"),
+            "kernel": "screen1_kernel<128, 8> (single-plane int8 MFMA)",
+            "ops_per_launch": 2.0 * C * D * Nt,
             "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
             "avg_launch_ms": sum(top1) / len(top1),
         }
@@ -208,7 +232,7 @@ def main():
     # (register operands only), after the timed region
     roofline["measured_peak"] = probe
     roofline["frac_of_measured_peak"] = achieved / probe
-    if not args.fp32_screen:
+    if args.two_plane:
         roofline["executed_frac_of_measured_peak"] = 2 * achieved / probe
 
     def call_ms(call):
@@ -245,7 +269,8 @@ def main():
         "config": {
             "workload": "ivf_pipeline: kmeans_step(10M u8 rows) + assign_build(10M u8 rows) + route(10,000 queries, nprobe 64); C=65536, D=128",
             "train_rows": Nt, "base_rows": Nb, "queries": Q, "centroids": C, "dim": D, "nprobe": K,
-            "screen": ("fp32 MFMA" if args.fp32_screen else "int8 MFMA (two planes per centroid)")
+            "screen": ("fp32 MFMA" if args.fp32_screen else "int8 MFMA (two planes per centroid)" if args.two_plane
+                       else "int8 MFMA (one plane per centroid; two planes for the rows it leaves)")
             + " for the uint8 rows, fp32 MFMA for the fp32 queries; exact fp64 re-evaluation of near-ties",
         },
         "roofline": roofline,

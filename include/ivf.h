@@ -168,7 +168,9 @@ ivf_status ivf_build_lists(ivf_ctx *ctx, const int32_t *labels, int64_t N, int64
  *   out[3] route: queries whose candidate list overflowed
  *   out[4] route: centroids in the threshold sample
  *   out[5] assignment of uint8 rows: 1 when screened on int8 MFMA
- *   out[6..7] reserved (0) */
+ *   out[6] assignment of uint8 rows: rows the single-plane int8 screen left
+ *          to the two-plane int8 screen
+ *   out[7] reserved (0) */
 ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
 
 /* Test, tuning and profiling knobs (values persist on the context):
@@ -187,6 +189,18 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *                           fp32 rows (default 0: int8 MFMA whenever every
  *                           centroid coordinate c has rint(256 (c - 128)) in
  *                           [-32768, 32767], i.e. c in [0, 255.998]);
+ *                           speed only, never results
+ *   IVF_OPT_I8_TWO_PLANE_ONLY  1 = no single-plane int8 pre-screen (default 0:
+ *                           for D <= 128, uint8 rows are first screened on one
+ *                           int8 plane rint(c - 128), which settles most rows
+ *                           with half the MFMA work, when every coordinate has
+ *                           rint(c - 128) in [-128, 127]); speed only
+ *   IVF_OPT_FORCE_RESCREEN  1 = the single-plane screen settles no row: every
+ *                           row goes on to the two-plane screen (results must
+ *                           not change)
+ *   IVF_OPT_RESCREEN_CAP    > 0: capacity of the single plane's list of rows
+ *                           for the two-plane screen (default 4,096 + N / 16;
+ *                           past it the two-plane screen takes every row);
  *                           speed only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
@@ -194,7 +208,10 @@ typedef enum {
     IVF_OPT_PROFILE = 2,
     IVF_OPT_BUILD_BLOCKS = 3,
     IVF_OPT_SCREEN_WAVES = 4,
-    IVF_OPT_FP32_SCREEN = 5
+    IVF_OPT_FP32_SCREEN = 5,
+    IVF_OPT_I8_TWO_PLANE_ONLY = 6,
+    IVF_OPT_FORCE_RESCREEN = 7,
+    IVF_OPT_RESCREEN_CAP = 8
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

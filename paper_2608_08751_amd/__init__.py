@@ -25,8 +25,11 @@ from ._binding import (  # noqa: F401
     IVF_OP_ROUTE,
     IVF_OPT_BUILD_BLOCKS,
     IVF_OPT_FORCE_FALLBACK,
+    IVF_OPT_FORCE_RESCREEN,
     IVF_OPT_FP32_SCREEN,
+    IVF_OPT_I8_TWO_PLANE_ONLY,
     IVF_OPT_PROFILE,
+    IVF_OPT_RESCREEN_CAP,
     IVF_OPT_SAMPLE_RANK,
     IVF_OPT_SCREEN_WAVES,
     IVF_U8,

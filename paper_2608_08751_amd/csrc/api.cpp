@@ -30,6 +30,9 @@ struct ivf_ctx {
     int build_blocks = 0;
     int screen_waves = 8;
     int fp32_screen = 0;  // 1: uint8 rows also take the fp32 MFMA screen
+    int two_plane_only = 0;  // 1: no single-plane int8 pre-screen
+    int force_rescreen = 0;  // 1: the single-plane screen lists every row
+    int64_t rescreen_cap = 0;  // > 0: smaller capacity of that list (tests)
     unsigned long long *last_stats = nullptr;  // device, inside the workspace
     int64_t last_sample = 0;
     // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
@@ -79,7 +82,10 @@ struct Carver {
 
 // Scalar area at the start of every workspace: [0] max centroid norm bits,
 // [1] worklist counter, [2] nonzero when some centroid does not quantise for
-// the int8 screen, then (from word 16) kNumStats uint64 counters.
+// the int8 screen, [3] the same for its single plane, [4] the single plane's
+// largest coordinate residual (float bits), [5] counter of the rows the
+// single plane leaves to the two planes, then (from word 16) kNumStats
+// uint64 counters.
 struct Scalars {
     uint32_t *mc2_bits;
     uint32_t *wl_cnt;
@@ -193,6 +199,9 @@ RouteLayout layout_route(void *base, const RoutePlan &p, int64_t C)
 }
 
 int64_t worklist_cap(int64_t N) { return std::min<int64_t>(N, 4096 + N / 64); }
+// rows the single-plane int8 screen may list for the two-plane screen
+// before that screen takes every row
+int64_t rescreen_cap(int64_t N) { return std::min<int64_t>(N, 4096 + N / 16); }
 
 struct AssignLayout {
     Scalars sc;
@@ -200,6 +209,11 @@ struct AssignLayout {
     // quantised centroids of the int8 screen (uint8 rows)
     int8_t *qc;
     int32_t *negb;
+    // single plane (padded dimension <= 128) and the rows it leaves
+    int8_t *qc1;
+    int32_t *negb1;
+    int32_t *list;
+    int64_t list_cap;
     int32_t *wl;
     int64_t wl_cap;
     double *fb_d;   // split fallback partial results
@@ -254,6 +268,12 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_
     if (qdp > 0) {
         l.qc = c.take<int8_t>((size_t)quantized_pad(C) * 2 * qdp);
         l.negb = c.take<int32_t>(quantized_pad(C));
+        if (qdp <= 128) {
+            l.qc1 = c.take<int8_t>((size_t)quantized_pad(C) * qdp);
+            l.negb1 = c.take<int32_t>(quantized_pad(C));
+            l.list_cap = rescreen_cap(N);
+            l.list = c.take<int32_t>(l.list_cap);
+        }
     }
     l.wl_cap = worklist_cap(N);
     l.wl = c.take<int32_t>(l.wl_cap);
@@ -391,7 +411,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     a.stats = l.sc.stats;
     a.force_fallback = ctx->force_fallback;
     if (rowtype == kRowU8 && !ctx->fp32_screen) {
-        // int8 MFMA screen; the fp32 kernel runs only if some centroid does not quantise
+        // int8 MFMA screens; the fp32 kernel runs only if some centroid does not quantise
         uint32_t *q_bad = l.sc.mc2_bits + 2;
         TIMED("quantize", launch_quantize_centroids(cent, C, D, DP, l.qc, l.negb, q_bad, s));
         ScreenI8Args q{};
@@ -410,6 +430,23 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
         q.wl_cap = l.wl_cap;
         q.stats = l.sc.stats;
         q.force_fallback = ctx->force_fallback;
+        q.ncent = C;
+        if (l.qc1 && !ctx->two_plane_only) {
+            // single plane first; the two planes then screen the rows it leaves
+            uint32_t *q_bad1 = l.sc.mc2_bits + 3;
+            uint32_t *e_bits = l.sc.mc2_bits + 4;
+            TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, s));
+            q.qc1 = l.qc1;
+            q.negb1 = l.negb1;
+            q.e_bits = e_bits;
+            q.q_bad1 = q_bad1;
+            q.list = l.list;
+            q.list_cnt = l.sc.mc2_bits + 5;
+            q.list_cap = ctx->rescreen_cap > 0 ? std::min<int64_t>(ctx->rescreen_cap, l.list_cap) : l.list_cap;
+            // a forced fallback passes every row on to the two planes, which send it on
+            q.force_rescreen = ctx->force_rescreen || ctx->force_fallback;
+            TIMED("screen_top1_i8s", launch_screen_i8_single(DP, q, ctx->num_cus, s));
+        }
         TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
         a.gate = q_bad;
     }
@@ -553,6 +590,12 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
         ctx->screen_waves = (int)value;
         return IVF_OK;
     case IVF_OPT_FP32_SCREEN: ctx->fp32_screen = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_I8_TWO_PLANE_ONLY: ctx->two_plane_only = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_FORCE_RESCREEN: ctx->force_rescreen = value ? 1 : 0; return IVF_OK;
+    case IVF_OPT_RESCREEN_CAP:
+        if (value < 0) return fail(ctx, IVF_EINVAL, "rescreen capacity must be >= 0");
+        ctx->rescreen_cap = value;
+        return IVF_OK;
     case IVF_OPT_BUILD_BLOCKS:
         if (value < 0 || value > 65536) return fail(ctx, IVF_EINVAL, "build blocks out of range");
         ctx->build_blocks = (int)value;

@@ -25,6 +25,7 @@ enum StatSlot {
     kStatOverflow = 3,
     kStatSample = 4,
     kStatScreenI8 = 5,  // 1 when the uint8 rows were screened on int8 MFMA
+    kStatRescreen = 6,  // rows the single-plane int8 screen left to the two-plane screen
     kNumStats = 8
 };
 
@@ -81,12 +82,32 @@ struct ScreenI8Args {
     int64_t wl_cap;
     unsigned long long *stats;
     int force_fallback;
+    // rows left by the single-plane screen (null: screen every row); when
+    // *q_bad1 is set or the list overflowed, every row is screened
+    const int32_t *list;
+    const uint32_t *list_cnt;
+    int64_t list_cap;
+    const uint32_t *q_bad1;
+    // single-plane screen (DP <= 128): plane [cpad][DP] int8, biases -b1,
+    // the largest coordinate residual (float bits), real centroid count, and
+    // a test knob that lists every row for the two-plane screen
+    const int8_t *qc1;
+    const int32_t *negb1;
+    const uint32_t *e_bits;
+    int64_t ncent;
+    int force_rescreen;
 };
 int64_t quantized_pad(int64_t C);
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
                                      uint32_t *q_bad, hipStream_t s);
 // Eight waves per workgroup (two per SIMD), one workgroup per CU.
 hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
+// Single-plane int8 screen (DP <= 128): plane rint(c - 128) [cpad][DP],
+// biases, *q_bad1 when some centroid does not fit, *e_bits = the largest
+// coordinate residual as float bits (both zeroed by the caller).
+hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
+                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s);
+hipError_t launch_screen_i8_single(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
 
 // ---- norms, selection, fallbacks (select.hip) -----------------------------
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);

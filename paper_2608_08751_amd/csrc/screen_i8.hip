@@ -99,20 +99,21 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__
 // copied from the padded global arrays straight into LDS by buffer loads with
 // an LDS destination (16 bytes per lane, a wave writes 1 KiB of consecutive
 // LDS per instruction): no register staging and no LDS stores by the vector
-// unit. LDS layout of a chunk: centroid rows with a pitch of 2 DP + 16 bytes
-// (the 16 spread the rows over the banks), then the 64 biases. Slot s
-// (16 bytes) of the row area holds unit s % (DP / 8 + 1) of row
-// s / (DP / 8 + 1); the pad unit and the bias instruction's lanes past the
+// unit. LDS layout of a chunk: centroid rows of PL planes with a pitch of
+// PL DP + 16 bytes (the 16 spread the rows over the banks), then the 64
+// biases. Slot s (16 bytes) of the row area holds unit s % (PL DP / 16 + 1)
+// of row s / (PL DP / 16 + 1); the pad unit and the bias instruction's lanes past the
 // biases read beyond the buffer range and receive zeros. Loads go through
 // buffer resources over the chunk's valid rows, so a ragged last chunk and
 // the chunk after the last one read zeros and every load is unconditional.
 // The loads of a chunk are complete (and visible to every wave) after the
 // next workgroup barrier, which waits for all outstanding vector memory
 // operations.
-template <int DP, int NT>
+template <int DP, int NT, int PL = 2>
 struct QStager {
-    static constexpr int kRowU = DP / 8;                 // 16-byte units per centroid
-    static constexpr int kPitch = 2 * DP + 16;
+    static constexpr int kRowB = PL * DP;                // bytes per centroid
+    static constexpr int kRowU = kRowB / 16;             // 16-byte units per centroid
+    static constexpr int kPitch = kRowB + 16;
     static constexpr int kRowInst = kRowU + 1;           // 64 rows x (kRowU + 1) slots / 64 lanes
     static constexpr int kInst = kRowInst + 1;           // plus one for the biases
     static constexpr int kBias = kQChunk * kPitch;       // byte offset of the biases (= kRowInst KiB)
@@ -133,7 +134,7 @@ struct QStager {
             if (inst < kRowInst) {
                 const int slot = 64 * inst + lane;
                 const int r = slot / (kRowU + 1), u = slot % (kRowU + 1);
-                if (u < kRowU) off = r * 2 * DP + 16 * u;
+                if (u < kRowU) off = r * kRowB + 16 * u;
             } else if (inst == kRowInst && lane < kQChunk / 4) {
                 off = 16 * lane;
             }
@@ -149,7 +150,7 @@ struct QStager {
         const int64_t left = cpad - cbase;
         const int valid = (int)(left < 0 ? 0 : left < kQChunk ? left : kQChunk);
         const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<int8_t *>(qc + cbase * 2 * DP), (short)0, valid * 2 * DP, 0x00020000);
+            const_cast<int8_t *>(qc + cbase * kRowB), (short)0, valid * kRowB, 0x00020000);
         const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<int32_t *>(negb + cbase), (short)0, valid * 4, 0x00020000);
 #pragma unroll
@@ -188,6 +189,37 @@ __device__ __forceinline__ void load_rows(const uint8_t *__restrict__ X, int64_t
                 const int d = 32 * k + 16 * h + 4 * w;
                 const uint32_t raw = __builtin_amdgcn_raw_buffer_load_b32(rr, base + 32 * k + 4 * w, 0, 0);
                 const bool ok = d < D;
+                xf[rb][k][w] = ok ? (int)(raw ^ 0x80808080u) : 0;
+                s = ok ? __builtin_amdgcn_sad_u8(raw, 0x80808080u, s) : s;
+            }
+        }
+        l1[rb] = s;
+    }
+}
+
+// The same for a list of rows: tile position t holds row ids[t] (t < n);
+// rowid[rb] receives this lane's row, or -1 past the end of the list.
+template <int DP, int RB>
+__device__ __forceinline__ void load_rows_ids(const uint8_t *__restrict__ X, int64_t N, const int32_t *__restrict__ ids,
+                                              int64_t t0, int64_t n, int D, int wave, int jl, int h,
+                                              i32x4 (&xf)[RB][DP / 32], uint32_t (&l1)[RB], int64_t (&rowid)[RB])
+{
+    constexpr int KS = DP / 32;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t t = t0 + (wave * RB + rb) * 32 + jl;
+        int64_t r = t < n ? (int64_t)ids[t] : -1;
+        if (r >= N) r = -1;
+        rowid[rb] = r;
+        const uint8_t *xr = X + (r < 0 ? 0 : r) * (int64_t)D + 16 * h;
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const int d = 32 * k + 16 * h + 4 * w;
+                const bool ok = r >= 0 && d < D;
+                const uint32_t raw = ok ? *reinterpret_cast<const uint32_t *>(xr + 32 * k + 4 * w) : 0x80808080u;
                 xf[rb][k][w] = ok ? (int)(raw ^ 0x80808080u) : 0;
                 s = ok ? __builtin_amdgcn_sad_u8(raw, 0x80808080u, s) : s;
             }
@@ -431,7 +463,8 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
 // last tile of chunk j, then runs chunk j + 1 up to its last tile; all LDS
 // waits inside are then exact.
 template <int DP, int W>
-__device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
+__device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds, const int32_t *ids,
+                               int64_t n)
 {
     constexpr int RB = rows_blocks<DP>();
     constexpr int NT = W * 64;
@@ -446,7 +479,17 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 
     i32x4 xf[RB][DP / 32];
     uint32_t l1[RB];
-    load_rows<DP, RB>(a.rows, row0, a.nrows, a.D, wave, jl, h, xf, l1);
+    int64_t rowid[RB];
+    if (ids) {
+        load_rows_ids<DP, RB>(a.rows, a.nrows, ids, row0, n, a.D, wave, jl, h, xf, l1, rowid);
+    } else {
+        load_rows<DP, RB>(a.rows, row0, a.nrows, a.D, wave, jl, h, xf, l1);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
+            rowid[rb] = row < a.nrows ? row : -1;
+        }
+    }
 
     Top3i st[RB];
 #pragma unroll
@@ -526,10 +569,7 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
     i8_drain(h1, l1acc, idh + (nch - 1) * kQChunk + 32, st[RB - 1]);
 
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
-        i8_finish(a, row, row < a.nrows, h, st[rb]);
-    }
+    for (int rb = 0; rb < RB; ++rb) i8_finish(a, rowid[rb], rowid[rb] >= 0, h, st[rb]);
 }
 
 template <int DP, int W>
@@ -540,10 +580,21 @@ __global__ __launch_bounds__(W * 64, 2) void screen_i8_kernel(ScreenI8Args a)
     __shared__ __attribute__((aligned(16))) char lds[2 * CS];
     if (*a.q_bad) return;  // the fp32 screen takes this call
     if (blockIdx.x == 0 && threadIdx.x == 0) a.stats[kStatScreenI8] = 1ull;
+    // after the single-plane screen: only the rows it left (its list), or
+    // every row when the list overflowed or the single plane did not apply
+    const int32_t *ids = nullptr;
+    int64_t n = a.nrows;
+    if (a.list && *a.q_bad1 == 0) {
+        const uint32_t c = *a.list_cnt;
+        if (c <= (uint64_t)a.list_cap) {
+            ids = a.list;
+            n = c;
+        }
+    }
     constexpr int rows_per_tile = W * 32 * rows_blocks<DP>();
-    const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
+    const int64_t ntiles = (n + rows_per_tile - 1) / rows_per_tile;
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        screen_i8_tile<DP, W>(a, tile, lds);
+        screen_i8_tile<DP, W>(a, tile, lds, ids, n);
         __syncthreads();
     }
 }
@@ -573,6 +624,297 @@ hipError_t launch_i8_w(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s
     }
 }
 
+// ============================================================ single plane
+// Screening on one int8 plane: half the MFMA work of the two planes. Every
+// centroid is quantised to H1 = rint(c') in [-128, 127] (c' = c - 128) with
+// the bias b1 = rint(||c'||^2 / 2), and the score of a centroid is the exact
+// integer
+//     s1(c) = x'.H1 - b1,
+// which differs from g(c) = x'.c' - ||c'||^2 / 2 = -k(c) / 2 by at most
+//     W = E ||x'||_1 + 1/2,   E = max_{c,d} |c'_d - H1_d|
+// (E = 0 for integer-valued centroids, such as rows sampled as the k-means
+// initialisation). With T >= 2W: if the best score beats the second by more
+// than T, its centroid is the unique nearest; if it beats the third by more
+// than T, the nearest is one of the two best and an exact fp64 evaluation
+// decides; otherwise the row is listed for the two-plane screen, whose bound
+// is 256 times finer. Centroids with rint(c') outside [-128, 127] set *q_bad1
+// and the two-plane screen takes every row.
+constexpr int kNoBias1 = -(1 << 26);  // bias of a padded centroid: below every real score (|s1| < 2^23)
+
+__global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict__ cent, int64_t C, int D, int DP,
+                                                        int64_t Cpad, int8_t *__restrict__ q1,
+                                                        int32_t *__restrict__ negb1, uint32_t *__restrict__ q_bad1,
+                                                        uint32_t *__restrict__ e_bits)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t j = w0; j < Cpad; j += nw) {
+        double n2 = 0.0, e = 0.0;
+        bool bad = false;
+        int8_t *q = q1 + j * DP;
+        for (int d = lane; d < DP; d += 64) {
+            int hb = 0;
+            if (j < C && d < D) {
+                const double cp = (double)cent[j * D + d] - 128.0;
+                const double p = rint(cp);
+                if (!(p >= -128.0 && p <= 127.0)) {  // also true for NaN
+                    bad = true;
+                } else {
+                    hb = (int)p;
+                    e = fmax(e, fabs(cp - p));
+                    n2 = fma(cp, cp, n2);
+                }
+            }
+            q[d] = (int8_t)hb;
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            n2 += __shfl_xor(n2, o);
+            e = fmax(e, __shfl_xor(e, o));
+        }
+        if (__any(bad) && lane == 0) *q_bad1 = 1u;
+        if (lane == 0) {
+            negb1[j] = j < C ? -(int32_t)llrint(0.5 * n2) : kNoBias1;
+            // non-negative floats order like their bit patterns; the read
+            // skips the atomic once a larger residual is recorded
+            const uint32_t eb = __float_as_uint(__double2float_ru(e));
+            if (j < C && e > 0.0 && eb > __atomic_load_n(e_bits, __ATOMIC_RELAXED)) atomicMax(e_bits, eb);
+        }
+    }
+}
+
+// The fragments of one staged 32-centroid block of the single plane.
+template <int DP>
+struct Frags1 {
+    i32x4 h[DP / 32];
+};
+
+template <int DP>
+__device__ __forceinline__ void load_frags1(const char *Ar, Frags1<DP> &f)
+{
+#pragma unroll
+    for (int k = 0; k < DP / 32; ++k) f.h[k] = *reinterpret_cast<const i32x4 *>(Ar + 32 * k);
+}
+
+// Group g (0..3) of a finished single-plane tile: registers 4g .. 4g + 3,
+// centroids idp + 8g + e. st.t3 holds the keep threshold (scores at or
+// below it cannot change the certificate's decision); only when some lane
+// of the wave has a score above it are the four values inserted.
+template <int g>
+__device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
+{
+    const int m = max4i(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
+    if (__any(m > st.t3)) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) top3i_push(st, p[4 * g + e], idp + 8 * g + e);
+        st.t3 = keep_threshold(st);
+    }
+    // keeps the group at this point of the MFMA stream
+    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
+}
+
+template <int g, int T, int KS>
+__device__ __forceinline__ void s1_groups_at(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
+{
+    if constexpr (g < 4) {
+        if constexpr (g * KS / 4 == T) {
+            s1_group<g>(p0, idp, s0);
+            s1_group<g>(p1, idp, s1);
+        }
+        s1_groups_at<g + 1, T, KS>(p0, p1, idp, s0, s1);
+    }
+}
+
+// K-steps T .. KS-1 of one 32-centroid block against both 32-row blocks of
+// the wave (c0 for rows 0, c1 for rows 1; two independent MFMA chains), both
+// starting from the biases at T = 0. The epilogue of the previous block
+// (p0, p1; ids from idp) runs between the K-steps, and each fragment
+// register is refilled from the next block (nA, nB) as soon as its last
+// MFMA has been issued.
+template <int DP, int T = 0>
+__device__ __forceinline__ void s1_pair(Frags1<DP> &f, const i32x4 (&x0)[DP / 32], const i32x4 (&x1)[DP / 32],
+                                        i32x16 &bias, i32x16 &c0, i32x16 &c1, const i32x16 &p0, const i32x16 &p1,
+                                        int idp, Top3i &s0, Top3i &s1, const char *nA, const int *nB)
+{
+    constexpr int KS = DP / 32;
+    if constexpr (T < KS) {
+        if constexpr (T == 0) {
+            c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x0[0], bias, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x1[0], bias, 0, 0, 0);
+            bias = load_bias(nB);
+        } else {
+            c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x0[T], c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x1[T], c1, 0, 0, 0);
+        }
+        f.h[T] = *reinterpret_cast<const i32x4 *>(nA + 32 * T);
+        s1_groups_at<0, T, KS>(p0, p1, idp, s0, s1);
+        __builtin_amdgcn_sched_barrier(0);
+        s1_pair<DP, T + 1>(f, x0, x1, bias, c0, c1, p0, p1, idp, s0, s1, nA, nB);
+    }
+}
+
+template <int g = 0>
+__device__ __forceinline__ void s1_drain(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
+{
+    if constexpr (g < 4) {
+        s1_group<g>(p0, idp, s0);
+        s1_group<g>(p1, idp, s1);
+        s1_drain<g + 1>(p0, p1, idp, s0, s1);
+    }
+}
+
+// Merges the two half-lanes of a row and certifies with the window T:
+// settled rows get their label (two-way near-ties decided in fp64), the
+// others are listed for the two-plane screen. A centroid id is used only
+// when it names a real centroid.
+__device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, const Top3i &st)
+{
+    Top3i o;
+    o.k1 = __shfl_xor(st.k1, 32);
+    o.k2 = __shfl_xor(st.k2, 32);
+    o.k3 = __shfl_xor(st.k3, 32);
+    o.i1 = __shfl_xor(st.i1, 32);
+    o.i2 = __shfl_xor(st.i2, 32);
+    const Top3i m = top3i_merge(st, o);
+    if (rvalid && h == 0) {
+        const int64_t T = st.twoR;
+        const bool ok1 = m.i1 >= 0 && m.i1 < a.ncent;
+        const bool ok2 = m.i2 >= 0 && m.i2 < a.ncent;
+        int label = -1;
+        if (!a.force_rescreen && ok1) {
+            if ((int64_t)m.k1 - (int64_t)m.k2 > T) {
+                label = m.i1;
+            } else if ((int64_t)m.k1 - (int64_t)m.k3 > T && ok2) {
+                const uint8_t *x = a.rows + row * (int64_t)a.D;
+                const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
+                const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
+                label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
+                atomicAdd(a.stats + kStatRefine2, 1ull);
+            }
+        }
+        if (label >= 0) {
+            a.labels[row] = label;
+        } else {
+            // past the list's capacity the two-plane screen takes every row
+            const uint32_t slot = atomicAdd(const_cast<uint32_t *>(a.list_cnt), 1u);
+            if (slot < (uint64_t)a.list_cap) const_cast<int32_t *>(a.list)[slot] = (int32_t)row;
+            atomicAdd(a.stats + kStatRescreen, 1ull);
+        }
+    }
+}
+
+// One workgroup tile of the single-plane screen: W * 64 rows (two 32-row
+// blocks per wave) against every centroid. A block's fragments feed both
+// row blocks; blocks alternate between the accumulator sets (a0, a1) and
+// (b0, b1), and each block's K-steps carry the epilogue of the block before
+// it. Staging and barriers as in the two-plane tile.
+template <int DP, int W>
+__device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
+{
+    static_assert(DP <= 128, "the single-plane screen keeps two row blocks per wave");
+    constexpr int RB = 2;
+    constexpr int NT = W * 64;
+    using St = QStager<DP, NT, 1>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    constexpr int BLK = 32 * St::kPitch;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row0 = tile * (W * 32 * RB);
+
+    i32x4 xf[RB][DP / 32];
+    uint32_t l1[RB];
+    load_rows<DP, RB>(a.rows, row0, a.nrows, a.D, wave, jl, h, xf, l1);
+
+    // T = ceil(2 E ||x'||_1 + 1) + 1 >= 2W (E rounded up; one unit of margin)
+    const double E = (double)__uint_as_float(*a.e_bits);
+    Top3i st[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        l1[rb] += __shfl_xor(l1[rb], 32);
+        const int T = (int)ceil(2.0 * E * (double)l1[rb]) + 2;
+        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, T};
+    }
+
+    const char *A0 = lds + jl * St::kPitch + 16 * h;
+    const char *B0 = lds + St::kBias + 16 * h;
+    const int idh = 4 * h;
+    const int nch = (int)a.nchunks;
+    auto abuf = [&](int jj) { return A0 + (jj & 1) * CS; };
+    auto bbuf = [&](int jj) { return reinterpret_cast<const int *>(B0 + (jj & 1) * CS); };
+
+    St q;
+    q.init();
+    q.fetch(a.qc1, a.negb1, 0, a.cpad, lds);
+    __syncthreads();
+    q.fetch(a.qc1, a.negb1, kQChunk, a.cpad, lds + CS);
+    auto stage = [&](int jj) {
+        __syncthreads();
+        q.fetch(a.qc1, a.negb1, (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
+    };
+
+    // (b0, b1) start as a block of lowest scores: the first epilogue inserts nothing
+    i32x16 a0, a1, b0, b1;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        b0[r] = kNoScore;
+        b1[r] = kNoScore;
+    }
+    i32x16 bias = load_bias(bbuf(0));
+    Frags1<DP> f;
+    load_frags1<DP>(abuf(0), f);
+
+    // block (jj, cb) into (a0, a1) while (b0, b1) = the block before drains
+    auto pairA = [&](int jj, int cb, const char *nA, const int *nB) {
+        s1_pair<DP>(f, xf[0], xf[1], bias, a0, a1, b0, b1, idh + jj * kQChunk + 32 * cb - 32, st[0], st[1], nA, nB);
+    };
+    auto pairB = [&](int jj, int cb, const char *nA, const int *nB) {
+        s1_pair<DP>(f, xf[0], xf[1], bias, b0, b1, a0, a1, idh + jj * kQChunk + 32 * cb - 32, st[0], st[1], nA, nB);
+    };
+    pairA(0, 0, abuf(0) + BLK, bbuf(0) + 32);
+    stage(1);
+    for (int j = 0;; ++j) {
+        pairB(j, 1, abuf(j + 1), bbuf(j + 1));
+        if (j + 1 == nch) break;
+        pairA(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
+        stage(j + 2);
+    }
+    s1_drain(b0, b1, idh + (nch - 1) * kQChunk + 32, st[0], st[1]);
+
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
+        s1_finish(a, row, row < a.nrows, h, st[rb]);
+    }
+}
+
+template <int DP, int W>
+__global__ __launch_bounds__(W * 64, 2) void screen1_kernel(ScreenI8Args a)
+{
+    using St = QStager<DP, W * 64, 1>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    __shared__ __attribute__((aligned(16))) char lds[2 * CS];
+    if (*a.q_bad || *a.q_bad1) return;  // another screen takes every row
+    constexpr int rows_per_tile = W * 64;
+    const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        screen1_tile<DP, W>(a, tile, lds);
+        __syncthreads();
+    }
+}
+
+template <int DP>
+hipError_t launch_s1(const ScreenI8Args &a, int num_cus, hipStream_t s)
+{
+    constexpr int W = 8;
+    const int64_t ntiles = (a.nrows + W * 64 - 1) / (W * 64);
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, (int64_t)num_cus));
+    hipLaunchKernelGGL((screen1_kernel<DP, W>), dim3(grid), dim3(W * 64), 0, s, a);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 int64_t quantized_pad(int64_t C) { return (C + kQChunk - 1) / kQChunk * kQChunk; }
@@ -585,6 +927,28 @@ hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP
     hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, qc, negb,
                        q_bad);
     return hipGetLastError();
+}
+
+hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
+                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s)
+{
+    const int64_t cpad = quantized_pad(C);
+    const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
+    hipLaunchKernelGGL(quantize1_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, q1, negb1,
+                       q_bad1, e_bits);
+    return hipGetLastError();
+}
+
+hipError_t launch_screen_i8_single(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s)
+{
+    if (a.nrows <= 0) return hipSuccess;
+    switch (DP) {
+    case 32: return launch_s1<32>(a, num_cus, s);
+    case 64: return launch_s1<64>(a, num_cus, s);
+    case 96: return launch_s1<96>(a, num_cus, s);
+    case 128: return launch_s1<128>(a, num_cus, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s)

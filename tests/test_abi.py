@@ -144,6 +144,10 @@ def test_options_and_errors(vctx):
     assert lib.ivf_set_option(h, B.IVF_OPT_FORCE_FALLBACK, 1) == B.IVF_OK
     assert lib.ivf_set_option(h, B.IVF_OPT_SAMPLE_RANK, 16) == B.IVF_OK
     assert lib.ivf_set_option(h, B.IVF_OPT_SAMPLE_RANK, -3) == B.IVF_EINVAL
+    assert lib.ivf_set_option(h, B.IVF_OPT_I8_TWO_PLANE_ONLY, 1) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_FORCE_RESCREEN, 1) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_RESCREEN_CAP, 5) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_RESCREEN_CAP, -1) == B.IVF_EINVAL
     assert lib.ivf_set_option(h, 42, 0) == B.IVF_EINVAL
     assert "unknown option" in vctx.error()
     assert lib.ivf_sync(h) == B.IVF_OK

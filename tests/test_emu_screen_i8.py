@@ -1,10 +1,12 @@
-"""The two-plane int8 screening kernel (screen_i8.hip) built for the host
-against a wave64 emulation (tests/wave_emu: one host thread per lane, the int8
-MFMA's operand layout, barriers for the wave and the block) and run under
-AddressSanitizer: every row the screen settles carries the oracle's label,
-the others are exactly the fallback worklist, and no access leaves its
-allocation. No GPU is involved; this checks the kernel's arithmetic,
-indexing and synchronisation, not the compiled gfx950 code."""
+"""The int8 screening kernels (screen_i8.hip: the two-plane screen alone, and
+the single-plane screen followed by the two-plane screen of the rows it
+leaves) built for the host against a wave64 emulation (tests/wave_emu: one
+host thread per lane, the int8 MFMA's operand layout, barriers for the wave
+and the block, asynchronous loads into LDS) and run under AddressSanitizer:
+every row the screens settle carries the oracle's label, the others are
+exactly the fallback worklist, and no access leaves its allocation. No GPU is
+involved; this checks the kernels' arithmetic, indexing and synchronisation,
+not the compiled gfx950 code."""
 import os
 import subprocess
 
@@ -55,7 +57,7 @@ def emu_bin(tmp_path_factory):
     return exe
 
 
-def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0):
+def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen=0, rescreen_cap=0):
     N, D = x.shape
     src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
     with open(src, "wb") as f:
@@ -63,8 +65,8 @@ def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0):
         np.ascontiguousarray(x, np.uint8).tofile(f)
         np.ascontiguousarray(c, np.float32).tofile(f)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
-    r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback)], capture_output=True,
-                       text=True, timeout=900, env=env)
+    r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback), str(mode),
+                        str(force_rescreen), str(rescreen_cap)], capture_output=True, text=True, timeout=900, env=env)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-6000:]
     raw = np.fromfile(dst, np.uint8)
     lab = raw[: 4 * N].view(np.int32)
@@ -74,6 +76,8 @@ def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0):
     o += 4 * n
     stats = raw[o: o + 64].view(np.uint64)
     q_bad = int(raw[o + 64: o + 68].view(np.uint32)[0])
+    run.q_bad1 = int(raw[o + 68: o + 72].view(np.uint32)[0])
+    run.listed = int(raw[o + 72: o + 76].view(np.uint32)[0])
     return lab, wl, stats, q_bad
 
 
@@ -101,17 +105,34 @@ def check(oracle_mod, lab, wl, stats, x, c):
     assert int(stats[0]) == fb.size and int(stats[5]) == 1
 
 
+@pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("N,C,D,cus", [(1500, 130, 128, 3), (700, 3, 96, 2), (1100, 65, 256, 3), (600, 70, 36, 1)])
-def test_emulated_screen_matches_oracle(emu_bin, tmp_path, oracle_mod, N, C, D, cus):
+def test_emulated_screen_matches_oracle(emu_bin, tmp_path, oracle_mod, N, C, D, cus, mode):
     """Several row tiles per workgroup (persistent loop), ragged last tiles,
-    C not a multiple of the 64-centroid chunk, and each padded width."""
+    C not a multiple of the 64-centroid chunk, and each padded width; mode 1
+    runs the single plane first (padded widths up to 128)."""
     x, c = rows_and_centroids(N, C, D, seed=N + C + D)
-    lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c, num_cus=cus)
+    lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c, num_cus=cus, mode=mode)
     assert q_bad == 0
     check(oracle_mod, lab, wl, stats, x, c)
+    if mode == 1 and D <= 128:
+        # non-integer centroids: some rows need the finer two planes
+        assert run.q_bad1 == 0 and run.listed == int(stats[6]) and run.listed < N
 
 
-def test_emulated_near_ties(emu_bin, tmp_path, oracle_mod):
+def test_emulated_single_plane_integer_centroids(emu_bin, tmp_path, oracle_mod):
+    """Integer-valued centroids (rows sampled as the k-means initialisation):
+    E = 0, the single plane settles every row that has no tie within one unit."""
+    x, _ = rows_and_centroids(1200, 90, 128, seed=3)
+    rng = np.random.default_rng(4)
+    c = x[rng.choice(1200, 90, replace=False)].astype(np.float32)
+    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c, mode=1)
+    check(oracle_mod, lab, wl, stats, x, c)
+    assert run.listed <= 12
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_emulated_near_ties(emu_bin, tmp_path, oracle_mod, mode):
     """Pairs of nearly equal centroids (two candidates: the exact fp64
     evaluation) and crowds of five (the fallback worklist)."""
     rng = np.random.default_rng(11)
@@ -121,9 +142,33 @@ def test_emulated_near_ties(emu_bin, tmp_path, oracle_mod):
     c = np.vstack([pa, pa + 1e-3, cr, cr.copy(), cr + 1e-3, cr - 1.0 / 512, cr + 0.5]).astype(np.float32)
     x = np.vstack([np.rint(pa), np.rint(pa + 0.25), np.rint(cr), rng.integers(0, 256, size=(200, D))])
     x = np.clip(x, 0, 255).astype(np.uint8)
-    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c)
+    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c, mode=mode)
     check(oracle_mod, lab, wl, stats, x, c)
     assert int(stats[0]) > 0 and int(stats[1]) > 0
+
+
+@pytest.mark.parametrize("force_rescreen,cap", [(1, 0), (0, 1), (1, 5)])
+def test_emulated_rescreen_forced_and_overflow(emu_bin, tmp_path, oracle_mod, force_rescreen, cap):
+    """Every row listed for the two planes; a list of one or five entries
+    that overflows (the two planes then screen every row)."""
+    x, c = rows_and_centroids(900, 75, 100, seed=8)
+    lab, wl, stats, _ = run(emu_bin, tmp_path, x, c, mode=1, force_rescreen=force_rescreen, rescreen_cap=cap)
+    check(oracle_mod, lab, wl, stats, x, c)
+    if force_rescreen:
+        assert run.listed == 900 and int(stats[6]) == 900
+    else:
+        assert run.listed > cap
+
+
+def test_emulated_single_plane_unquantisable(emu_bin, tmp_path, oracle_mod):
+    """A coordinate of 255.7 rounds to 128 on the single plane (outside int8)
+    but fits the two planes: the single plane stands down, the two planes
+    screen every row."""
+    x, c = rows_and_centroids(700, 50, 128, seed=9)
+    c[11, 5] = 255.7
+    lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c, mode=1)
+    assert q_bad == 0 and run.q_bad1 == 1 and run.listed == 0
+    check(oracle_mod, lab, wl, stats, x, c)
 
 
 def test_emulated_forced_fallback_and_unquantisable(emu_bin, tmp_path, oracle_mod):

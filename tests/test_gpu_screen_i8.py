@@ -1,8 +1,9 @@
-"""GPU parity of the int8-MFMA screen used for uint8 rows (assignment and the
-k-means step): labels must equal the oracle's exactly, on the int8 path and
-on the fp32 path the library takes when centroids do not quantise (or when
-IVF_OPT_FP32_SCREEN forces it), including near-ties that the quantised
-scores cannot separate."""
+"""GPU parity of the int8-MFMA screens used for uint8 rows (assignment and the
+k-means step): labels must equal the oracle's exactly on every path: the
+default (one int8 plane, then two int8 planes for the rows it leaves), two
+planes alone (IVF_OPT_I8_TWO_PLANE_ONLY), and the fp32 path the library takes
+when centroids do not quantise (or when IVF_OPT_FP32_SCREEN forces it),
+including near-ties that the quantised scores cannot separate."""
 import numpy as np
 import pytest
 
@@ -30,18 +31,29 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_assign(ctx, x, c, fp32_screen=False):
+# screen paths: (name, options)
+PATHS = {
+    "default": {},
+    "two_planes": {"IVF_OPT_I8_TWO_PLANE_ONLY": 1},
+    "fp32": {"IVF_OPT_FP32_SCREEN": 1},
+}
+
+
+def gpu_assign(ctx, x, c, path="default", **extra):
     import torch
 
     import paper_2608_08751_amd as ivf
 
-    ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 1 if fp32_screen else 0)
+    opts = dict(PATHS[path], **extra)
+    for k, v in opts.items():
+        ctx.set_option(getattr(ivf, k), v)
     try:
         lab, cnt, off, perm = ivf.ivf_assign_build(ctx, to_dev(x), to_dev(c))
         torch.cuda.synchronize()
         stats = ctx.last_stats()
     finally:
-        ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 0)
+        for k in opts:
+            ctx.set_option(getattr(ivf, k), 0)
     return lab.cpu().numpy(), cnt.cpu().numpy(), off.cpu().numpy(), perm.cpu().numpy(), stats
 
 
@@ -49,14 +61,16 @@ def check_assign(ctx, oracle_mod, x, c, expect_i8=True):
     olab = oracle_mod.assign(x, c)
     ocnt, ooff, operm = oracle_mod.build_lists(olab, c.shape[0])
     out = {}
-    for fp32 in (False, True):
-        lab, cnt, off, perm, st = gpu_assign(ctx, x, c, fp32)
-        print("fp32_screen=%d stats %s" % (fp32, st), flush=True)
+    for path in PATHS:
+        lab, cnt, off, perm, st = gpu_assign(ctx, x, c, path)
+        print("%s stats %s" % (path, st), flush=True)
         bad = np.nonzero(lab != olab)[0]
-        assert bad.size == 0, "fp32_screen=%d: labels differ at rows %s" % (fp32, bad[:10])
+        assert bad.size == 0, "%s: labels differ at rows %s" % (path, bad[:10])
         assert (cnt == ocnt).all() and (off == ooff).all() and (perm == operm).all()
-        assert st["screen_i8"] == (1 if (expect_i8 and not fp32) else 0)
-        out[fp32] = st
+        assert st["screen_i8"] == (1 if (expect_i8 and path != "fp32") else 0)
+        if path != "default" or not expect_i8:
+            assert st["rescreen"] == 0
+        out[path] = st
     return out
 
 
@@ -101,7 +115,9 @@ def test_i8_near_ties(ivf_ctx, oracle_mod):
     x.append(rng.integers(0, 256, size=(500, D)))
     x = np.clip(np.vstack(x), 0, 255).astype(np.uint8)
     st = check_assign(ivf_ctx, oracle_mod, x, c)
-    assert st[False]["refine2"] + st[False]["fallback"] > 0
+    assert st["default"]["refine2"] + st["default"]["fallback"] > 0
+    assert st["two_planes"]["refine2"] + st["two_planes"]["fallback"] > 0
+    assert st["default"]["rescreen"] > 0
 
 
 def test_i8_extreme_values(ivf_ctx, oracle_mod):
@@ -132,9 +148,11 @@ def test_i8_edge_of_range_quantises(ivf_ctx, oracle_mod):
     check_assign(ivf_ctx, oracle_mod, x, c)
 
 
-def test_i8_kmeans_step_both_paths(ivf_ctx, oracle_mod):
+def test_i8_kmeans_step_all_paths(ivf_ctx, oracle_mod):
     """Two Lloyd iterations from sampled rows (several centroids per mixture
-    component, so near-ties occur): both screens give the oracle's step."""
+    component, so near-ties occur): every screen gives the oracle's step. The
+    first iteration's centroids are integer rows, which the single plane
+    settles alone; the second's are means."""
     import torch
 
     import paper_2608_08751_amd as ivf
@@ -144,16 +162,20 @@ def test_i8_kmeans_step_both_paths(ivf_ctx, oracle_mod):
     c = x[synth.kmeans_init(12000, 600, seed=21)].astype(np.float32)
     for it in range(2):
         olab, ocen, ocnt, oobj = oracle_mod.kmeans_step(x, c, seed=3, it=it)
-        for fp32 in (0, 1):
-            ivf_ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, fp32)
+        for path, opts in PATHS.items():
+            for k, v in opts.items():
+                ivf_ctx.set_option(getattr(ivf, k), v)
             try:
                 lab, cen, cnt, obj = ivf.ivf_kmeans_step(ivf_ctx, to_dev(x), to_dev(c), seed=3, it=it)
                 torch.cuda.synchronize()
                 st = ivf_ctx.last_stats()
             finally:
-                ivf_ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 0)
-            print("it %d fp32_screen=%d stats %s" % (it, fp32, st), flush=True)
-            assert st["screen_i8"] == 1 - fp32
+                for k in opts:
+                    ivf_ctx.set_option(getattr(ivf, k), 0)
+            print("it %d %s stats %s" % (it, path, st), flush=True)
+            assert st["screen_i8"] == (0 if path == "fp32" else 1)
+            if path == "default" and it == 0:
+                assert st["rescreen"] <= 5
             assert (lab.cpu().numpy() == olab).all()
             assert (cnt.cpu().numpy() == ocnt).all()
             assert (cen.cpu().numpy() == ocen).all()
@@ -177,3 +199,43 @@ def test_i8_forced_fallback_is_identical(ivf_ctx, oracle_mod, N):
         ivf_ctx.set_option(ivf.IVF_OPT_FORCE_FALLBACK, 0)
     assert st["screen_i8"] == 1 and st["fallback"] == N
     assert (lab == olab).all()
+
+
+@pytest.mark.parametrize("N,C,D,cap", [(4000, 300, 128, 0), (2500, 130, 100, 7), (3000, 200, 64, 1)])
+def test_i8_single_plane_rescreen_forced_and_overflow(ivf_ctx, oracle_mod, N, C, D, cap):
+    """Every row handed from the single plane to the two planes
+    (IVF_OPT_FORCE_RESCREEN), or a list capacity of 7 or 1 that overflows so
+    that the two planes screen every row: the labels do not change."""
+    import paper_2608_08751_amd as ivf
+
+    x, c = rows_and_centroids(N, C, D, seed=N + C)
+    olab = oracle_mod.assign(x, c)
+    if cap == 0:
+        lab, _, _, _, st = gpu_assign(ivf_ctx, x, c, IVF_OPT_FORCE_RESCREEN=1)
+        assert st["rescreen"] == N
+    else:
+        lab, _, _, _, st = gpu_assign(ivf_ctx, x, c, IVF_OPT_RESCREEN_CAP=cap)
+        assert st["rescreen"] > cap
+    print("cap %d stats %s" % (cap, st), flush=True)
+    assert st["screen_i8"] == 1
+    assert (lab == olab).all()
+
+
+@pytest.mark.parametrize("bad", [255.5, 255.7, 255.99])
+def test_i8_single_plane_stands_down(ivf_ctx, oracle_mod, bad):
+    """A coordinate that rounds to 128 on the single plane (outside int8) but
+    fits the two planes: the two planes screen every row, exactly."""
+    x, c = rows_and_centroids(3000, 150, 128, seed=7)
+    c[9, 11] = bad
+    st = check_assign(ivf_ctx, oracle_mod, x, c)
+    assert st["default"]["rescreen"] == 0
+
+
+def test_i8_single_plane_integer_centroids(ivf_ctx, oracle_mod):
+    """Integer-valued centroids (sampled rows, as the k-means initialisation):
+    no rounding on the single plane, which settles (almost) every row."""
+    means = synth.uniform_means(200, 128, seed=31)
+    x, _ = synth.mixture_rows_u8(means, 0, 20000, seed=31)
+    c = x[synth.kmeans_init(20000, 700, seed=31)].astype(np.float32)
+    st = check_assign(ivf_ctx, oracle_mod, x, c)
+    assert st["default"]["rescreen"] <= 10

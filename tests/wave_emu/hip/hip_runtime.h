@@ -204,6 +204,26 @@ inline int __builtin_amdgcn_readfirstlane(int v)
 
 inline void __builtin_amdgcn_sched_barrier(int) {}
 
+inline uint32_t __float_as_uint(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    return u;
+}
+inline float __uint_as_float(uint32_t u)
+{
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+// double to float, rounded toward +infinity
+inline float __double2float_ru(double x)
+{
+    float f = (float)x;
+    if ((double)f < x) f = nextafterf(f, INFINITY);
+    return f;
+}
+
 template <typename T>
 inline T atomicAdd(T *p, T v) { return __atomic_fetch_add(p, v, __ATOMIC_SEQ_CST); }
 inline unsigned long long atomicAdd(unsigned long long *p, unsigned long long v)

@@ -1,13 +1,17 @@
 // Runs the int8 screening kernels of screen_i8.hip on the host emulation, in
-// the order the library enqueues them for uint8 rows (quantisation, then the
-// screen), on one case file, with every array in an allocation of its own.
-// Writes the labels, the worklist and the statistics for the test to check
-// against the oracle; the fallback scan that follows in the library (another
-// source file) is not run, so rows it would settle keep the label -1.
+// the order the library enqueues them for uint8 rows (quantisation, the
+// single-plane screen when the padded dimension is at most 128 and mode is 1,
+// then the two-plane screen over the rows it leaves), on one case file, with
+// every array in an allocation of its own. Writes the labels, the worklist
+// and the statistics for the test to check against the oracle; the fallback
+// scan that follows in the library (another source file) is not run, so rows
+// it would settle keep the label -1.
 //   usage: screen_i8_host in.bin out.bin num_cus force_fallback
+//                         [mode force_rescreen rescreen_cap]
 //   in:  int64 N, C, D; uint8 rows [N][D]; float centroids [C][D]
 //   out: int32 labels [N]; uint32 worklist count; int32 worklist [count];
-//        uint64 stats [8]; uint32 quantisation flag
+//        uint64 stats [8]; uint32 quantisation flag; uint32 single-plane
+//        quantisation flag; uint32 rescreen list count
 #include "hip/hip_runtime.h"
 namespace emu {
 thread_local dim3 tid, bid;
@@ -53,6 +57,15 @@ int main(int argc, char **argv)
     int32_t *wl = alloc<int32_t>(wl_cap, 0);
     int32_t *labels = alloc<int32_t>(N, 0x7f);  // 0x7f7f7f7f marks a label never written
     unsigned long long *stats = alloc<unsigned long long>(8, 0);
+    const int mode = argc > 5 ? atoi(argv[5]) : 0;
+    const bool single = mode == 1 && DP <= 128;
+    const int64_t list_cap = std::min<int64_t>(N, 4096 + N / 16);
+    int8_t *qc1 = single ? alloc<int8_t>(cpad * DP, 0) : nullptr;
+    int32_t *negb1 = single ? alloc<int32_t>(cpad, 0) : nullptr;
+    int32_t *list = single ? alloc<int32_t>(list_cap, 0) : nullptr;
+    uint32_t *q_bad1 = alloc<uint32_t>(1, 0);
+    uint32_t *e_bits = alloc<uint32_t>(1, 0);
+    uint32_t *list_cnt = alloc<uint32_t>(1, 0);
 
     launch_quantize_centroids(cent, C, D, DP, qc, negb, q_bad, nullptr);
     ScreenI8Args a{};
@@ -71,6 +84,20 @@ int main(int argc, char **argv)
     a.wl_cap = wl_cap;
     a.stats = stats;
     a.force_fallback = atoi(argv[4]);
+    a.ncent = C;
+    if (single) {
+        launch_quantize_centroids1(cent, C, D, DP, qc1, negb1, q_bad1, e_bits, nullptr);
+        a.qc1 = qc1;
+        a.negb1 = negb1;
+        a.e_bits = e_bits;
+        a.q_bad1 = q_bad1;
+        a.list = list;
+        a.list_cnt = list_cnt;
+        const int64_t cap = argc > 7 ? atoll(argv[7]) : 0;
+        a.list_cap = cap > 0 ? std::min<int64_t>(cap, list_cap) : list_cap;
+        a.force_rescreen = argc > 6 ? atoi(argv[6]) : 0;
+        launch_screen_i8_single(DP, a, num_cus, nullptr);
+    }
     launch_screen_i8(DP, a, num_cus, nullptr);
 
     FILE *o = fopen(argv[2], "wb");
@@ -81,6 +108,8 @@ int main(int argc, char **argv)
     fwrite(wl, 4, n, o);
     fwrite(stats, 8, 8, o);
     fwrite(q_bad, 4, 1, o);
+    fwrite(q_bad1, 4, 1, o);
+    fwrite(list_cnt, 4, 1, o);
     fclose(o);
     return 0;
 }
