@@ -258,6 +258,8 @@ __device__ __forceinline__ int med3i(int a, int b, int c)
     return min(max(a, b), max(min(a, b), c));
 }
 
+__device__ __forceinline__ int max3i(int a, int b, int c) { return max(max(a, b), c); }
+
 __device__ __forceinline__ int max4i(int a, int b, int c, int d)
 {
     return max(max(max(a, b), c), d);
@@ -700,12 +702,14 @@ __device__ __forceinline__ void load_frags1(const char *Ar, Frags1<DP> &f)
 // Group g (0..3) of a finished single-plane tile: registers 4g .. 4g + 3,
 // centroids idp + 8g + e. st.t3 holds the keep threshold (scores at or
 // below it cannot change the certificate's decision); only when some lane
-// of the wave has a score above it are the four values inserted.
+// of the wave has a score above it are the four values inserted. The
+// insertion is rare once a row has met its nearest centroids, so it is laid
+// out off the straight-line path.
 template <int g>
 __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
 {
     const int m = max4i(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
-    if (__any(m > st.t3)) {
+    if (__builtin_expect(__any(m > st.t3), 0)) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) top3i_push(st, p[4 * g + e], idp + 8 * g + e);
         st.t3 = keep_threshold(st);
@@ -714,16 +718,27 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
     asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
 }
 
-template <int g, int T, int KS>
+// A whole finished tile of one row block (16 scores per lane) in one test:
+// only when some lane of the wave has a score above its keep threshold are
+// the four groups tested and inserted one by one.
+__device__ __forceinline__ void s1_tile_test(const i32x16 &p, int idp, Top3i &st)
+{
+    const int m = max(max(max3i(max3i(p[0], p[1], p[2]), max3i(p[3], p[4], p[5]), max3i(p[6], p[7], p[8])),
+                          max3i(max3i(p[9], p[10], p[11]), max3i(p[12], p[13], p[14]), p[15])),
+                      kNoScore);
+    if (__builtin_expect(__any(m > st.t3), 0)) {
+        s1_group<0>(p, idp, st);
+        s1_group<1>(p, idp, st);
+        s1_group<2>(p, idp, st);
+        s1_group<3>(p, idp, st);
+    }
+}
+
+template <int T, int KS>
 __device__ __forceinline__ void s1_groups_at(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
 {
-    if constexpr (g < 4) {
-        if constexpr (g * KS / 4 == T) {
-            s1_group<g>(p0, idp, s0);
-            s1_group<g>(p1, idp, s1);
-        }
-        s1_groups_at<g + 1, T, KS>(p0, p1, idp, s0, s1);
-    }
+    if constexpr (T == 0) s1_tile_test(p0, idp, s0);
+    if constexpr (T == KS / 2) s1_tile_test(p1, idp, s1);
 }
 
 // K-steps T .. KS-1 of one 32-centroid block against both 32-row blocks of
@@ -742,26 +757,26 @@ __device__ __forceinline__ void s1_pair(Frags1<DP> &f, const i32x4 (&x0)[DP / 32
         if constexpr (T == 0) {
             c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x0[0], bias, 0, 0, 0);
             c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x1[0], bias, 0, 0, 0);
+            // an empty use of the biases after both MFMAs: neither is their last
+            // reader, so the compiler gives both a separate destination instead
+            // of copying the biases into one accumulator first
+            asm volatile("" ::"v"(bias));
             bias = load_bias(nB);
         } else {
             c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x0[T], c0, 0, 0, 0);
             c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x1[T], c1, 0, 0, 0);
         }
         f.h[T] = *reinterpret_cast<const i32x4 *>(nA + 32 * T);
-        s1_groups_at<0, T, KS>(p0, p1, idp, s0, s1);
+        s1_groups_at<T, KS>(p0, p1, idp, s0, s1);
         __builtin_amdgcn_sched_barrier(0);
         s1_pair<DP, T + 1>(f, x0, x1, bias, c0, c1, p0, p1, idp, s0, s1, nA, nB);
     }
 }
 
-template <int g = 0>
 __device__ __forceinline__ void s1_drain(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
 {
-    if constexpr (g < 4) {
-        s1_group<g>(p0, idp, s0);
-        s1_group<g>(p1, idp, s1);
-        s1_drain<g + 1>(p0, p1, idp, s0, s1);
-    }
+    s1_tile_test(p0, idp, s0);
+    s1_tile_test(p1, idp, s1);
 }
 
 // Merges the two half-lanes of a row and certifies with the window T:
