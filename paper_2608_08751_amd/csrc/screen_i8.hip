@@ -712,7 +712,11 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
     if (__builtin_expect(__any(m > st.t3), 0)) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) top3i_push(st, p[4 * g + e], idp + 8 * g + e);
-        st.t3 = keep_threshold(st);
+        // the two half-lanes of a row share their best score: the row's best
+        // only grows, so scores at or below (best of both) - T - 1 are
+        // irrelevant to the certificate of the merged lists as well
+        const int kb = max(st.k1, __shfl_xor(st.k1, 32));
+        st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
     }
     // keeps the group at this point of the MFMA stream
     asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
