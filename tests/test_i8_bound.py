@@ -5,7 +5,11 @@ the bound |s + 128 k + 128 sum(x')| < 129 + ||x'||_1 / 2 on which the
 kernel's certificate rests (k = ||c'||^2 - 2 x'.c', x' = x - 128,
 c' = c - 128), and the prefilter inequality s <= 256 h + 128 ||x'||_1 with
 h = x'.H - Bh. Distances are evaluated exactly with rational arithmetic on a
-subset."""
+subset. The single-plane screen's arithmetic: one int8 plane H1 = rint(c'),
+the score s1 = x'.H1 - b1 with b1 = rint(||c'||^2 / 2), and the bound
+|g - s1| <= E ||x'||_1 + 1/2 with g = x'.c' - ||c'||^2 / 2 = -k / 2 and E the
+largest coordinate residual |c' - H1|, on which its window
+T = ceil(2 E ||x'||_1) + 2 rests."""
 from fractions import Fraction
 
 import numpy as np
@@ -141,3 +145,112 @@ def test_int32_headroom_at_the_largest_dimension():
         for v in (hi, lo, hi + lo):
             assert np.abs(v).max() < 2 ** 31 - 2 ** 24
         assert hpart(x, H, Bh).min() > -(2 ** 23)
+
+
+# ---------------------------------------------------------------- single plane
+
+def quantise1(c):
+    """One int8 plane, its biases and E rounded up to fp32 (as the kernel)."""
+    cp = c.astype(np.float64) - 128.0
+    H1 = np.rint(cp)
+    assert np.all((H1 >= -128) & (H1 <= 127))
+    b1 = np.rint(0.5 * np.sum(cp * cp, axis=1)).astype(np.int64)
+    e = float(np.max(np.abs(cp - H1))) if c.size else 0.0
+    E = float(np.nextafter(np.float32(e), np.float32(1))) if np.float32(e) < e else float(np.float32(e))
+    return H1.astype(np.int64), b1, E
+
+
+def window(x, E):
+    l1 = np.abs(x.astype(np.int64) - 128).sum(axis=1)
+    return np.ceil(2.0 * E * l1).astype(np.int64) + 2
+
+
+def test_single_plane_range_and_integer_centroids():
+    """rint(c - 128) fits int8 for c in [-0.5, 255.5); integer centroids have
+    E = 0; 255.5 rounds (half to even) to 128 and does not fit."""
+    rng = np.random.default_rng(5)
+    c = rng.uniform(-0.49, 255.49, size=(300, 40)).astype(np.float32)
+    H1, _, E = quantise1(c)
+    assert H1.min() >= -128 and H1.max() <= 127 and 0.0 < E <= 0.5
+    ci = rng.integers(0, 256, size=(50, 40)).astype(np.float32)
+    assert quantise1(ci)[2] == 0.0
+    assert np.rint(np.float64(np.float32(255.5)) - 128.0) == 128.0
+
+
+def test_single_plane_error_within_bound_exact_arithmetic():
+    """|g - s1| <= E ||x'||_1 + 1/2 in exact rational arithmetic, including
+    centroids on and next to the half-unit rounding boundaries, and the
+    kernel's window T exceeds twice that error."""
+    rng = np.random.default_rng(6)
+    D, C = 16, 40
+    c = rng.uniform(0.0, 255.4, size=(C, D)).astype(np.float32)
+    k = rng.integers(0, 255, size=(C // 4, D))
+    c[: C // 4] = (k + 0.5).astype(np.float32)
+    c[C // 4: C // 2] = np.nextafter((k + 0.5).astype(np.float32), np.float32(300))
+    c[0] = 0.0
+    c[1] = np.float32(2.0 ** -60)
+    x = rng.integers(0, 256, size=(30, D))
+    x[0] = 0
+    x[1] = 255
+    H1, b1, E = quantise1(c)
+    s1 = (x - 128) @ H1.T - b1[None, :]
+    T = window(x, E)
+    cf = [[Fraction(float(v)) - 128 for v in row] for row in c]
+    worst = Fraction(0)
+    for i in range(x.shape[0]):
+        xp = [int(v) - 128 for v in x[i]]
+        W = Fraction(E) * sum(abs(v) for v in xp) + Fraction(1, 2)
+        for j in range(C):
+            g = sum(a * b for a, b in zip(xp, cf[j])) - sum(v * v for v in cf[j]) / 2
+            e = g - int(s1[i, j])
+            assert abs(e) <= W, (i, j, float(e), float(W))
+            assert 2 * abs(e) < int(T[i])
+            worst = max(worst, abs(e) / W)
+    assert worst > Fraction(1, 20)
+
+
+def test_single_plane_certificate_never_excludes_the_nearest():
+    """The kernel's decision on the single plane: the best-scored centroid
+    when it beats the second by more than T, the nearest of the two best
+    (fp64) when it beats the third by more than T, the two-plane screen
+    otherwise. Settled rows carry the exact nearest centroid, for mean-like
+    centroids (E near 1/2) and for integer ones (E = 0)."""
+    rng = np.random.default_rng(7)
+    D, C, N = 128, 300, 500
+    for integer in (False, True):
+        c = rng.uniform(0.0, 255.0, size=(C, D))
+        c[1::3] = c[0::3][: len(c[1::3])] + rng.normal(0, 2.0, size=c[1::3].shape)  # near pairs
+        c = np.clip(c, 0, 255).astype(np.float32)
+        if integer:
+            c = np.rint(c).astype(np.float32)
+        base = np.rint(c[rng.integers(0, C, N)])
+        x = np.clip(base + rng.integers(-20, 21, size=(N, D)), 0, 255).astype(np.int64)
+        H1, b1, E = quantise1(c)
+        s1 = (x - 128) @ H1.T - b1[None, :]
+        T = window(x, E)
+        d = ((x[:, None, :].astype(np.float64) - c[None, :, :].astype(np.float64)) ** 2).sum(axis=2)
+        nearest = np.argmin(d, axis=1)
+        order = np.argsort(-s1, axis=1, kind="stable")
+        top = np.take_along_axis(s1, order[:, :3], axis=1)
+        settled = 0
+        for i in range(N):
+            if top[i, 0] - top[i, 1] > T[i]:
+                assert order[i, 0] == nearest[i]
+                settled += 1
+            elif top[i, 0] - top[i, 2] > T[i]:
+                a, b = order[i, 0], order[i, 1]
+                assert nearest[i] == (a if (d[i, a], a) <= (d[i, b], b) else b)
+                settled += 1
+        assert settled > N // 2
+
+
+def test_single_plane_int32_headroom():
+    """D = 128 with |x'| = 128 and H1 at both ends: |s1| < 2^23 (the padding
+    bias -2^26 stays below every real score) and well inside int32."""
+    D = 128
+    c = np.stack([np.zeros(D), np.full(D, 255.4)]).astype(np.float32)
+    H1, b1, _ = quantise1(c)
+    for xv in (0, 255):
+        x = np.full((1, D), xv, np.int64)
+        s1 = (x - 128) @ H1.T - b1[None, :]
+        assert np.abs(s1).max() < 2 ** 23
