@@ -29,8 +29,14 @@ namespace ivf {
 namespace {
 
 constexpr int kRThreads = 256;           // 4 waves
-constexpr int kRTile = 4096;             // rows per tile
-constexpr int kRItems = kRTile / kRThreads;  // 16 rows per thread
+constexpr int kRTile = 4096;             // rows per tile of level 1
+constexpr int kRTile0 = 8192;            // rows per tile of level 0 (longer runs per digit)
+
+template <bool FIRST>
+constexpr int tile_rows()
+{
+    return FIRST ? kRTile0 : kRTile;
+}
 
 // Exclusive scan of v over the 256 threads of the block; returns the prefix.
 __device__ __forceinline__ uint32_t block_exscan256(uint32_t v, uint32_t *wsum)
@@ -49,6 +55,7 @@ __device__ __forceinline__ uint32_t block_exscan256(uint32_t v, uint32_t *wsum)
     return before + incl - v;
 }
 
+template <int RT>
 struct TileLds {
     unsigned long long peers[4][256];  // per-wave match-any scratch (lane bits per digit)
     uint32_t wcnt[4][256];   // per-wave digit counts, then their exclusive prefix
@@ -56,29 +63,31 @@ struct TileLds {
     uint32_t gbase[256];     // global start of this tile's digit run
     uint32_t run[256];       // block running offset per digit
     uint32_t wsum[4];
-    uint32_t sid[kRTile];    // staged row ids
-    uint8_t slo[kRTile];     // staged low bytes (level 0)
-    uint8_t sdig[kRTile];    // staged digits
+    uint32_t sid[RT];        // staged row ids
+    uint8_t slo[RT];         // staged low bytes (level 0)
+    uint8_t sdig[RT];        // staged digits
 };
 
-// A tile's inputs, loaded one tile ahead: row r = base + wave*1024 + e*64 + lane.
+// A tile's inputs, loaded one tile ahead: row r = base + wave*RT/4 + e*64 + lane.
+template <int RT>
 struct TileIn {
-    uint32_t v[kRItems];       // level 0: label; level 1: row id
-    uint32_t lo4[kRItems / 4]; // level 1: low bytes, four per word
+    static constexpr int kItems = RT / kRThreads;  // rows per thread
+    uint32_t v[kItems];        // level 0: label; level 1: row id
+    uint32_t lo4[kItems / 4];  // level 1: low bytes, four per word
 };
 
-template <bool FIRST, bool FULL>
-__device__ __forceinline__ void load_tile(TileIn &in, int64_t base, int64_t end,
+template <bool FIRST, bool FULL, int RT = tile_rows<FIRST>()>
+__device__ __forceinline__ void load_tile(TileIn<RT> &in, int64_t base, int64_t end,
                                           const int32_t *__restrict__ labels,
                                           const uint32_t *__restrict__ in_ids,
                                           const uint8_t *__restrict__ in_lo)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int e = 0; e < kRItems / 4; ++e) in.lo4[e] = 0;
+    for (int e = 0; e < TileIn<RT>::kItems / 4; ++e) in.lo4[e] = 0;
 #pragma unroll
-    for (int e = 0; e < kRItems; ++e) {
-        const int64_t r = base + wave * 1024 + e * 64 + lane;
+    for (int e = 0; e < TileIn<RT>::kItems; ++e) {
+        const int64_t r = base + wave * (RT / 4) + e * 64 + lane;
         const bool ok = FULL || r < end;
         if (FIRST) {
             in.v[e] = ok ? (uint32_t)labels[r] : 0xFFFFFFFFu;
@@ -92,17 +101,18 @@ __device__ __forceinline__ void load_tile(TileIn &in, int64_t base, int64_t end,
 // One tile: rank, stage and write. Level 0 (FIRST): the digit is label >> 8,
 // the payload is (row id, label & 255). Level 1: the digit is the stored low
 // byte, the payload is the stored row id.
-template <bool FIRST, bool FULL>
-__device__ void radix_tile(TileLds &t, const TileIn &in, int64_t base, int64_t end, int C,
+template <bool FIRST, bool FULL, int RT = tile_rows<FIRST>()>
+__device__ void radix_tile(TileLds<RT> &t, const TileIn<RT> &in, int64_t base, int64_t end, int C,
                            uint32_t *__restrict__ out_ids, uint8_t *__restrict__ out_lo)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint32_t dp[kRItems];  // (digit << 16) | position in the wave's run, 0xFFFF = none
+    constexpr int kItems = TileIn<RT>::kItems;
+    uint32_t dp[kItems];  // (digit << 16) | position in the wave's run, 0xFFFF = none
     // rank column by column
 #pragma unroll
-    for (int e = 0; e < kRItems; ++e) {
-        const int64_t r = base + wave * 1024 + e * 64 + lane;
+    for (int e = 0; e < kItems; ++e) {
+        const int64_t r = base + wave * (RT / 4) + e * 64 + lane;
         bool valid = FULL || r < end;
         uint32_t d;
         if (FIRST) {
@@ -145,11 +155,11 @@ __device__ void radix_tile(TileLds &t, const TileIn &in, int64_t base, int64_t e
     __syncthreads();
     // stage in (digit, row) order
 #pragma unroll
-    for (int e = 0; e < kRItems; ++e) {
+    for (int e = 0; e < kItems; ++e) {
         if ((dp[e] & 0xFFFFu) != 0xFFFFu) {
             const uint32_t d = dp[e] >> 16;
             const uint32_t li = t.start[d] + t.wcnt[wave][d] + (dp[e] & 0xFFFFu);
-            t.sid[li] = FIRST ? (uint32_t)(base + wave * 1024 + e * 64 + lane) : in.v[e];
+            t.sid[li] = FIRST ? (uint32_t)(base + wave * (RT / 4) + e * 64 + lane) : in.v[e];
             t.sdig[li] = (uint8_t)d;
             if (FIRST) t.slo[li] = (uint8_t)(in.v[e] & 0xFFu);
         }
@@ -159,7 +169,7 @@ __device__ void radix_tile(TileLds &t, const TileIn &in, int64_t base, int64_t e
     // addresses
     const uint32_t total = t.start[255] + (t.run[255] - t.gbase[255]);
 #pragma unroll
-    for (int e = 0; e < kRItems; ++e) {
+    for (int e = 0; e < kItems; ++e) {
         const uint32_t i = threadIdx.x + e * kRThreads;
         if (i < total) {
             const uint32_t d = t.sdig[i];
@@ -174,7 +184,8 @@ __device__ void radix_tile(TileLds &t, const TileIn &in, int64_t base, int64_t e
     __syncthreads();
 }
 
-__device__ __forceinline__ void init_run(TileLds &t)
+template <int RT>
+__device__ __forceinline__ void init_run(TileLds<RT> &t)
 {
     for (int i = threadIdx.x; i < 256; i += kRThreads) {
         t.wcnt[0][i] = t.wcnt[1][i] = t.wcnt[2][i] = t.wcnt[3][i] = 0;
@@ -254,27 +265,28 @@ __global__ __launch_bounds__(kRThreads) void starts0_kernel(const uint32_t *__re
     if (d == 255) astart[256] = st + v;
 }
 
-__global__ __launch_bounds__(kRThreads, 4) void scatter0_kernel(const int32_t *__restrict__ labels, int64_t N,
+__global__ __launch_bounds__(kRThreads, 2) void scatter0_kernel(const int32_t *__restrict__ labels, int64_t N,
                                                              int64_t R0, int C, int nblocks,
                                                              const uint32_t *__restrict__ base0,
                                                              const uint32_t *__restrict__ astart,
                                                              uint32_t *__restrict__ tmp_ids,
                                                              uint8_t *__restrict__ tmp_lo)
 {
-    __shared__ TileLds t;
+    constexpr int RT = kRTile0;
+    __shared__ TileLds<RT> t;
     init_run(t);
     t.run[threadIdx.x] = astart[threadIdx.x] + base0[(int64_t)threadIdx.x * nblocks + blockIdx.x];
     __syncthreads();
     const int64_t r0 = (int64_t)blockIdx.x * R0, r1 = min(N, r0 + R0);
-    TileIn cur, nxt;
-    if (r0 + kRTile <= r1) load_tile<true, true>(cur, r0, r1, labels, nullptr, nullptr);
+    TileIn<RT> cur, nxt;
+    if (r0 + RT <= r1) load_tile<true, true>(cur, r0, r1, labels, nullptr, nullptr);
     else load_tile<true, false>(cur, r0, r1, labels, nullptr, nullptr);
-    for (int64_t base = r0; base < r1; base += kRTile) {
-        const int64_t nb = base + kRTile;
-        if (nb + kRTile <= r1) load_tile<true, true>(nxt, nb, r1, labels, nullptr, nullptr);
+    for (int64_t base = r0; base < r1; base += RT) {
+        const int64_t nb = base + RT;
+        if (nb + RT <= r1) load_tile<true, true>(nxt, nb, r1, labels, nullptr, nullptr);
         else if (nb < r1) load_tile<true, false>(nxt, nb, r1, labels, nullptr, nullptr);
-        if (base + kRTile <= r1)
-            radix_tile<true, true>(t, cur, base, base + kRTile, C, tmp_ids, tmp_lo);
+        if (base + RT <= r1)
+            radix_tile<true, true>(t, cur, base, base + RT, C, tmp_ids, tmp_lo);
         else
             radix_tile<true, false>(t, cur, base, r1, C, tmp_ids, tmp_lo);
         cur = nxt;
@@ -359,7 +371,7 @@ __global__ __launch_bounds__(kRThreads) void scatter1_kernel(const uint32_t *__r
                                                              const int64_t *__restrict__ offsets, int C,
                                                              uint32_t *__restrict__ perm)
 {
-    __shared__ TileLds t;
+    __shared__ TileLds<kRTile> t;
     int bucket;
     int64_t lo, hi;
     if (!locate_sub(sbstart, astart, R1, blockIdx.x, bucket, lo, hi)) return;
@@ -370,7 +382,7 @@ __global__ __launch_bounds__(kRThreads) void scatter1_kernel(const uint32_t *__r
         t.run[d] = j < C ? (uint32_t)offsets[j] + base1[(int64_t)blockIdx.x * 256 + d] : 0u;
     }
     __syncthreads();
-    TileIn cur, nxt;
+    TileIn<kRTile> cur, nxt;
     if (lo + kRTile <= hi) load_tile<false, true>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
     else load_tile<false, false>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
     for (int64_t base = lo; base < hi; base += kRTile) {
@@ -396,11 +408,11 @@ RadixPlan plan_radix(int64_t N, int64_t C, int num_cus)
     p.N = N;
     p.C = C;
     int64_t R0 = (N + 8 * (int64_t)num_cus - 1) / (8 * (int64_t)num_cus);
-    R0 = (R0 + kRTile - 1) / kRTile * kRTile;
-    R0 = std::min<int64_t>(std::max<int64_t>(R0, kRTile), 16 * (int64_t)kRTile);
+    R0 = (R0 + kRTile0 - 1) / kRTile0 * kRTile0;
+    R0 = std::min<int64_t>(std::max<int64_t>(R0, kRTile0), 16 * (int64_t)kRTile0);
     p.R0 = R0;
     p.nblocks0 = (int)std::max<int64_t>(1, (N + R0 - 1) / R0);
-    p.R1 = R0;
+    p.R1 = std::min<int64_t>(R0, 16 * (int64_t)kRTile);
     p.max_sub1 = (int)((N + p.R1 - 1) / p.R1) + 256;
     return p;
 }
