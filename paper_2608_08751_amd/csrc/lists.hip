@@ -93,30 +93,70 @@ __global__ __launch_bounds__(256) void colscan_kernel(uint32_t *__restrict__ cnt
     }
 }
 
-// Exclusive scan of counts by one workgroup: each thread sums a contiguous
-// piece, the piece sums are scanned in LDS, then each piece is written out.
+// Exclusive scan of counts by one workgroup of 1,024 threads, in passes of
+// 16,384 counts: each thread loads 16 consecutive counts at once (one memory
+// latency per pass), scans them in registers, and the thread totals are
+// scanned across the wave (shuffles) and the 16 waves (LDS); a carry links
+// the passes.
+constexpr int kOffPer = 16;
+
 __global__ __launch_bounds__(1024) void offsets_kernel(const int64_t *__restrict__ counts,
                                                        int64_t C, int64_t *__restrict__ offsets)
 {
-    __shared__ int64_t part[1024];
-    const int64_t per = (C + blockDim.x - 1) / blockDim.x;
-    const int64_t lo = min(C, per * threadIdx.x), hi = min(C, lo + per);
-    int64_t sum = 0;
-    for (int64_t j = lo; j < hi; ++j) sum += counts[j];
-    part[threadIdx.x] = sum;
-    __syncthreads();
-    for (int o = 1; o < (int)blockDim.x; o <<= 1) {
-        const int64_t v = threadIdx.x >= (unsigned)o ? part[threadIdx.x - o] : 0;
+    __shared__ int64_t wtot[16];
+    __shared__ int64_t carry_s;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t carry = 0;
+    for (int64_t base = 0; base < C; base += 1024 * kOffPer) {
+        const int64_t j0 = base + (int64_t)threadIdx.x * kOffPer;
+        int64_t v[kOffPer];
+        if (j0 + kOffPer <= C) {
+#pragma unroll
+            for (int k = 0; k < kOffPer; k += 2) {
+                const longlong2 u = *reinterpret_cast<const longlong2 *>(counts + j0 + k);
+                v[k] = u.x;
+                v[k + 1] = u.y;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kOffPer; ++k) v[k] = j0 + k < C ? counts[j0 + k] : 0;
+        }
+        int64_t tot = 0;
+#pragma unroll
+        for (int k = 0; k < kOffPer; ++k) tot += v[k];
+        // inclusive scan of the thread totals over the wave
+        int64_t incl = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t up = __shfl_up(incl, o);
+            if (lane >= o) incl += up;
+        }
+        if (lane == 63) wtot[wave] = incl;
         __syncthreads();
-        part[threadIdx.x] += v;
+        int64_t before = carry;
+        for (int w = 0; w < wave; ++w) before += wtot[w];
+        if (threadIdx.x == 1023) carry_s = before + incl;
+        int64_t run = before + incl - tot;
+        if (j0 + kOffPer <= C && ((j0 & 1) == 0)) {
+#pragma unroll
+            for (int k = 0; k < kOffPer; k += 2) {
+                longlong2 u;
+                u.x = run;
+                u.y = run + v[k];
+                run += v[k] + v[k + 1];
+                *reinterpret_cast<longlong2 *>(offsets + j0 + k) = u;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kOffPer; ++k) {
+                if (j0 + k < C) offsets[j0 + k] = run;
+                run += v[k];
+            }
+        }
         __syncthreads();
+        carry = carry_s;
     }
-    int64_t run = threadIdx.x == 0 ? 0 : part[threadIdx.x - 1];
-    for (int64_t j = lo; j < hi; ++j) {
-        offsets[j] = run;
-        run += counts[j];
-    }
-    if (threadIdx.x == blockDim.x - 1) offsets[C] = part[threadIdx.x];
+    if (threadIdx.x == 0) offsets[C] = carry;
 }
 
 constexpr int kLinearDupMax = 128;
