@@ -708,15 +708,25 @@ __device__ __forceinline__ void load_frags1(const char *Ar, Frags1<DP> &f)
 template <int g>
 __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
 {
-    const int m = max4i(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
+    const int v0 = p[4 * g], v1 = p[4 * g + 1], v2 = p[4 * g + 2], v3 = p[4 * g + 3];
+    const int m = max4i(v0, v1, v2, v3);
     if (__builtin_expect(__any(m > st.t3), 0)) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) top3i_push(st, p[4 * g + e], idp + 8 * g + e);
-        // the two half-lanes of a row share their best score: the row's best
-        // only grows, so scores at or below (best of both) - T - 1 are
-        // irrelevant to the certificate of the merged lists as well
-        const int kb = max(st.k1, __shfl_xor(st.k1, 32));
+        // the group's best (the lowest position among equal scores) first
+        const int e1 = v0 == m ? 0 : v1 == m ? 1 : v2 == m ? 2 : 3;
+        top3i_push(st, m, idp + 8 * g + e1);
+        int kb = max(st.k1, __shfl_xor(st.k1, 32));
         st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
+        // the other three only when some lane still needs one of them
+        const int r0 = e1 == 0 ? kNoScore : v0, r1 = e1 == 1 ? kNoScore : v1;
+        const int r2 = e1 == 2 ? kNoScore : v2, r3 = e1 == 3 ? kNoScore : v3;
+        if (__builtin_expect(__any(max4i(r0, r1, r2, r3) > st.t3), 0)) {
+            top3i_push(st, r0, idp + 8 * g);
+            top3i_push(st, r1, idp + 8 * g + 1);
+            top3i_push(st, r2, idp + 8 * g + 2);
+            top3i_push(st, r3, idp + 8 * g + 3);
+            kb = max(st.k1, __shfl_xor(st.k1, 32));
+            st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
+        }
     }
     // keeps the group at this point of the MFMA stream
     asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
