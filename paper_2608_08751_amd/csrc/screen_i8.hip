@@ -728,8 +728,6 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
             st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
         }
     }
-    // keeps the group at this point of the MFMA stream
-    asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
 }
 
 // A whole finished tile of one row block (16 scores per lane) in one test:
@@ -748,49 +746,44 @@ __device__ __forceinline__ void s1_tile_test(const i32x16 &p, int idp, Top3i &st
     }
 }
 
-template <int T, int KS>
-__device__ __forceinline__ void s1_groups_at(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
+template <int RB, int T, int KS, int rb = 0>
+__device__ __forceinline__ void s1_tests_at(const i32x16 (&p)[RB], int idp, Top3i (&st)[RB])
 {
-    if constexpr (T == 0) s1_tile_test(p0, idp, s0);
-    if constexpr (T == KS / 2) s1_tile_test(p1, idp, s1);
+    if constexpr (rb < RB) {
+        if constexpr (rb * KS / RB == T) s1_tile_test(p[rb], idp, st[rb]);
+        s1_tests_at<RB, T, KS, rb + 1>(p, idp, st);
+    }
 }
 
-// K-steps T .. KS-1 of one 32-centroid block against both 32-row blocks of
-// the wave (c0 for rows 0, c1 for rows 1; two independent MFMA chains), both
-// starting from the biases at T = 0. The epilogue of the previous block
-// (p0, p1; ids from idp) runs between the K-steps, and each fragment
-// register is refilled from the next block (nA, nB) as soon as its last
-// MFMA has been issued.
-template <int DP, int T = 0>
-__device__ __forceinline__ void s1_pair(Frags1<DP> &f, const i32x4 (&x0)[DP / 32], const i32x4 (&x1)[DP / 32],
-                                        i32x16 &bias, i32x16 &c0, i32x16 &c1, const i32x16 &p0, const i32x16 &p1,
-                                        int idp, Top3i &s0, Top3i &s1, const char *nA, const int *nB)
+// K-steps T .. KS-1 of one 32-centroid block against the RB 32-row blocks of
+// the wave (c[rb]: RB independent MFMA chains), all starting from the biases
+// at T = 0. The epilogue of the previous block (p; ids from idp) runs between
+// the K-steps, and each fragment register is refilled from the next block
+// (nA, nB) as soon as its last MFMA has been issued.
+template <int DP, int RB, int T = 0>
+__device__ __forceinline__ void s1_block(Frags1<DP> &f, const i32x4 (&x)[RB][DP / 32], i32x16 &bias,
+                                         i32x16 (&c)[RB], const i32x16 (&p)[RB], int idp, Top3i (&st)[RB],
+                                         const char *nA, const int *nB)
 {
     constexpr int KS = DP / 32;
     if constexpr (T < KS) {
         if constexpr (T == 0) {
-            c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x0[0], bias, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x1[0], bias, 0, 0, 0);
-            // an empty use of the biases after both MFMAs: neither is their last
-            // reader, so the compiler gives both a separate destination instead
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) c[rb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[0], x[rb][0], bias, 0, 0, 0);
+            // an empty use of the biases after the MFMAs: none is their last
+            // reader, so the compiler gives each a separate destination instead
             // of copying the biases into one accumulator first
             asm volatile("" ::"v"(bias));
             bias = load_bias(nB);
         } else {
-            c0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x0[T], c0, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x1[T], c1, 0, 0, 0);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) c[rb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.h[T], x[rb][T], c[rb], 0, 0, 0);
         }
         f.h[T] = *reinterpret_cast<const i32x4 *>(nA + 32 * T);
-        s1_groups_at<T, KS>(p0, p1, idp, s0, s1);
+        s1_tests_at<RB, T, KS>(p, idp, st);
         __builtin_amdgcn_sched_barrier(0);
-        s1_pair<DP, T + 1>(f, x0, x1, bias, c0, c1, p0, p1, idp, s0, s1, nA, nB);
+        s1_block<DP, RB, T + 1>(f, x, bias, c, p, idp, st, nA, nB);
     }
-}
-
-__device__ __forceinline__ void s1_drain(const i32x16 &p0, const i32x16 &p1, int idp, Top3i &s0, Top3i &s1)
-{
-    s1_tile_test(p0, idp, s0);
-    s1_tile_test(p1, idp, s1);
 }
 
 // Merges the two half-lanes of a row and certifies with the window T:
@@ -833,16 +826,25 @@ __device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bo
     }
 }
 
-// One workgroup tile of the single-plane screen: W * 64 rows (two 32-row
-// blocks per wave) against every centroid. A block's fragments feed both
-// row blocks; blocks alternate between the accumulator sets (a0, a1) and
-// (b0, b1), and each block's K-steps carry the epilogue of the block before
-// it. Staging and barriers as in the two-plane tile.
+// Row blocks of 32 rows per wave in the single-plane screen: three at
+// DP = 128 (a block's fragments and biases feed three MFMA chains, within
+// the register file), two below.
+template <int DP>
+constexpr int s1_row_blocks()
+{
+    return DP == 128 ? 3 : 2;
+}
+
+// One workgroup tile of the single-plane screen: W * 32 * RB rows against
+// every centroid. A block's fragments feed every row block of the wave;
+// blocks alternate between the accumulator sets A and B, and each block's
+// K-steps carry the epilogue of the block before it. Staging and barriers as
+// in the two-plane tile.
 template <int DP, int W>
 __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
 {
-    static_assert(DP <= 128, "the single-plane screen keeps two row blocks per wave");
-    constexpr int RB = 2;
+    static_assert(DP <= 128, "the single-plane screen keeps several row blocks per wave");
+    constexpr int RB = s1_row_blocks<DP>();
     constexpr int NT = W * 64;
     using St = QStager<DP, NT, 1>;
     constexpr int CS = (St::kBytes + 15) / 16 * 16;
@@ -884,33 +886,33 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
         q.fetch(a.qc1, a.negb1, (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
     };
 
-    // (b0, b1) start as a block of lowest scores: the first epilogue inserts nothing
-    i32x16 a0, a1, b0, b1;
+    // set B starts as a block of lowest scores: the first epilogue inserts nothing
+    i32x16 sa[RB], sb[RB];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        b0[r] = kNoScore;
-        b1[r] = kNoScore;
-    }
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sb[rb][r] = kNoScore;
     i32x16 bias = load_bias(bbuf(0));
     Frags1<DP> f;
     load_frags1<DP>(abuf(0), f);
 
-    // block (jj, cb) into (a0, a1) while (b0, b1) = the block before drains
-    auto pairA = [&](int jj, int cb, const char *nA, const int *nB) {
-        s1_pair<DP>(f, xf[0], xf[1], bias, a0, a1, b0, b1, idh + jj * kQChunk + 32 * cb - 32, st[0], st[1], nA, nB);
+    // block (jj, cb) into set A while set B = the block before drains, and back
+    auto blockA = [&](int jj, int cb, const char *nA, const int *nB) {
+        s1_block<DP, RB>(f, xf, bias, sa, sb, idh + jj * kQChunk + 32 * cb - 32, st, nA, nB);
     };
-    auto pairB = [&](int jj, int cb, const char *nA, const int *nB) {
-        s1_pair<DP>(f, xf[0], xf[1], bias, b0, b1, a0, a1, idh + jj * kQChunk + 32 * cb - 32, st[0], st[1], nA, nB);
+    auto blockB = [&](int jj, int cb, const char *nA, const int *nB) {
+        s1_block<DP, RB>(f, xf, bias, sb, sa, idh + jj * kQChunk + 32 * cb - 32, st, nA, nB);
     };
-    pairA(0, 0, abuf(0) + BLK, bbuf(0) + 32);
+    blockA(0, 0, abuf(0) + BLK, bbuf(0) + 32);
     stage(1);
     for (int j = 0;; ++j) {
-        pairB(j, 1, abuf(j + 1), bbuf(j + 1));
+        blockB(j, 1, abuf(j + 1), bbuf(j + 1));
         if (j + 1 == nch) break;
-        pairA(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
+        blockA(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
         stage(j + 2);
     }
-    s1_drain(b0, b1, idh + (nch - 1) * kQChunk + 32, st[0], st[1]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) s1_tile_test(sb[rb], idh + (nch - 1) * kQChunk + 32, st[rb]);
 
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -926,7 +928,7 @@ __global__ __launch_bounds__(W * 64, 2) void screen1_kernel(ScreenI8Args a)
     constexpr int CS = (St::kBytes + 15) / 16 * 16;
     __shared__ __attribute__((aligned(16))) char lds[2 * CS];
     if (*a.q_bad || *a.q_bad1) return;  // another screen takes every row
-    constexpr int rows_per_tile = W * 64;
+    constexpr int rows_per_tile = W * 32 * s1_row_blocks<DP>();
     const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         screen1_tile<DP, W>(a, tile, lds);
@@ -938,7 +940,8 @@ template <int DP>
 hipError_t launch_s1(const ScreenI8Args &a, int num_cus, hipStream_t s)
 {
     constexpr int W = 8;
-    const int64_t ntiles = (a.nrows + W * 64 - 1) / (W * 64);
+    constexpr int rows_per_tile = W * 32 * s1_row_blocks<DP>();
+    const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, (int64_t)num_cus));
     hipLaunchKernelGGL((screen1_kernel<DP, W>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
