@@ -313,19 +313,22 @@ def main():
 def measured_traffic(rows_per_launch, record):
     """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary (calibrated against a device
-    copy), if it was taken on the current kernel source and launch size;
-    otherwise None."""
+    copy), if it was taken on the current kernel sources (the record's
+    `sources`, hashed in order) and launch size; otherwise None."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", record)
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
-    except (OSError, ValueError, KeyError):
+        h = hashlib.sha256()
+        for src in rec["sources"]:
+            with open(os.path.join(ROOT, src), "rb") as f:
+                h.update(f.read())
+        sha = h.hexdigest()
+    except (OSError, ValueError, KeyError, TypeError):
         return None
-    if not sha.startswith(rec["source_sha256_prefix"]) or rec["rows_per_launch"] != rows_per_launch:
+    if not sha.startswith(rec["sources_sha256_prefix"]) or rec["rows_per_launch"] != rows_per_launch:
         return None
     return rec["traffic_bytes"]
 
