@@ -211,7 +211,7 @@ def main():
             "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
             "avg_launch_ms": sum(top1) / len(top1),
         }
-        _, probe = ctx.mfma_probe_i8()
+        _, probe = ctx.mfma_probe_i8(200000)
     else:
         # the single-plane int8 screen executes exactly the algorithmic
         # operations (one int8 plane per centroid)
@@ -227,9 +227,11 @@ def main():
             "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
             "avg_launch_ms": sum(top1) / len(top1),
         }
-        _, probe = ctx.mfma_probe_i8()
+        _, probe = ctx.mfma_probe_i8(200000)
     # the MFMA pipe as the library's probe kernel measures it on this GPU
-    # (register operands only), after the timed region
+    # (register operands only; for int8, pseudo-random operands over about
+    # 0.1 s, which the part runs at its power-limited clock), after the timed
+    # region
     roofline["measured_peak"] = probe
     roofline["frac_of_measured_peak"] = achieved / probe
     if args.two_plane:

@@ -337,9 +337,11 @@ ivf_status ivf_adc_scan(ivf_ctx *ctx, const float *queries, int64_t B, int32_t D
 ivf_status ivf_mfma_probe(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tflops);
 
 /* The same measurement for the int8 MFMA pipe that screens uint8 rows:
- * v_mfma_i32_32x32x32_i8 with register operands, two waves per SIMD on every
- * CU; *out_tops in 1e12 int8 operations per second. Same arguments, errors
- * and synchronisation as ivf_mfma_probe. */
+ * v_mfma_i32_32x32x32_i8 with register operands holding pseudo-random bytes
+ * (the part runs the int8 pipe at a power-limited clock on data that
+ * toggles, well below the published peak), two waves per SIMD on every CU;
+ * *out_tops in 1e12 int8 operations per second. Same arguments, errors and
+ * synchronisation as ivf_mfma_probe. */
 ivf_status ivf_mfma_probe_i8(ivf_ctx *ctx, int32_t iters, float *out_ms, double *out_tops);
 
 /* Kernel timeline recorded while IVF_OPT_PROFILE is on, across calls, since

@@ -4,7 +4,10 @@
 // operands in registers, two waves per SIMD on every CU. This is the rate
 // the screening kernels' MFMA stream could reach with no loads and no other
 // vector instructions; bench reports the screening kernels against it next
-// to the published peak.
+// to the published peak. The int8 probe feeds pseudo-random operands (four
+// register sets per operand, rotated): with data that toggles like real
+// rows and centroids the part runs the int8 pipe at a lower, power-limited
+// clock than with constant operands.
 #include "ivf_internal.h"
 
 namespace ivf {
@@ -35,22 +38,34 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters, float a, 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 
-__global__ __launch_bounds__(512, 2) void mfma_probe_i8_kernel(int iters, int a, int write, int *sink)
+__global__ __launch_bounds__(512, 2) void mfma_probe_i8_kernel(int iters, int seed, int write, int *sink)
 {
     i32x16 acc0 = {0}, acc1 = {0};
-    const i32x4 av = {a, a + 1, (int)threadIdx.x, a ^ 3};
-    const i32x4 bv = {a + 2, (int)threadIdx.x, a, 7};
+    i32x4 av[4], bv[4];
+    uint32_t s = (uint32_t)seed * 2654435761u + threadIdx.x * 40503u + blockIdx.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            s = s * 1664525u + 1013904223u;  // LCG (Numerical Recipes constants)
+            av[i][j] = (int)s;
+            s = s * 1664525u + 1013904223u;
+            bv[i][j] = (int)s;
+        }
     for (int i = 0; i < iters; ++i) {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc1, 0, 0, 0);
+        for (int r = 0; r < 2; ++r) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av[k], bv[(k + r) & 3], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(av[(k + 1) & 3], bv[(k + r + 2) & 3], acc1, 0, 0, 0);
+            }
         }
     }
-    int r = 0;
+    int t = 0;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) r += acc0[e] + acc1[e];
-    if (write) sink[blockIdx.x * blockDim.x + threadIdx.x] = r;
+    for (int e = 0; e < 16; ++e) t += acc0[e] + acc1[e];
+    if (write) sink[blockIdx.x * blockDim.x + threadIdx.x] = t;
 }
 
 }  // namespace
