@@ -269,8 +269,8 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_
         l.qc = c.take<int8_t>((size_t)quantized_pad(C) * 2 * qdp);
         l.negb = c.take<int32_t>(quantized_pad(C));
         if (qdp <= 128) {
-            l.qc1 = c.take<int8_t>((size_t)quantized_pad(C) * qdp);
-            l.negb1 = c.take<int32_t>(quantized_pad(C));
+            l.qc1 = c.take<int8_t>((size_t)quantized_pad1(C) * qdp);
+            l.negb1 = c.take<int32_t>(quantized_pad1(C));
             l.list_cap = rescreen_cap(N);
             l.list = c.take<int32_t>(l.list_cap);
         }

@@ -88,7 +88,8 @@ struct ScreenI8Args {
     const uint32_t *list_cnt;
     int64_t list_cap;
     const uint32_t *q_bad1;
-    // single-plane screen (DP <= 128): plane [cpad][DP] int8, biases -b1,
+    // single-plane screen (DP <= 128): plane [quantized_pad1(ncent)][DP]
+    // int8, biases -b1 (the launcher sets its own cpad and nchunks from ncent),
     // the largest coordinate residual (float bits), real centroid count, and
     // a test knob that lists every row for the two-plane screen
     const int8_t *qc1;
@@ -98,11 +99,13 @@ struct ScreenI8Args {
     int force_rescreen;
 };
 int64_t quantized_pad(int64_t C);
+// the single plane (qc1, negb1) is padded to whole staged chunks of 256
+int64_t quantized_pad1(int64_t C);
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
                                      uint32_t *q_bad, hipStream_t s);
 // Eight waves per workgroup (two per SIMD), one workgroup per CU.
 hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
-// Single-plane int8 screen (DP <= 128): plane rint(c - 128) [cpad][DP],
+// Single-plane int8 screen (DP <= 128): plane rint(c - 128) [quantized_pad1(C)][DP],
 // biases, *q_bad1 when some centroid does not fit, *e_bits = the largest
 // coordinate residual as float bits (both zeroed by the caller).
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,

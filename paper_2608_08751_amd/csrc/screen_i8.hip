@@ -34,6 +34,7 @@
 #include "ivf_internal.h"
 
 #include <algorithm>
+#include <utility>
 
 namespace ivf {
 namespace {
@@ -41,7 +42,9 @@ namespace {
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kQChunk = 64;          // centroids per staged chunk
+constexpr int kQChunk = 64;          // centroids per staged chunk (sub-chunk of the single plane)
+constexpr int kS1Sub = 4;            // 64-centroid sub-chunks per staged chunk of the single plane
+constexpr int kS1Chunk = kS1Sub * kQChunk;
 constexpr int kNoScore = INT32_MIN;  // score of a padded centroid (below any real score)
 constexpr int kNoBias = -(1 << 23);  // H accumulator start of a padded centroid: s = kNoScore
 
@@ -835,11 +838,21 @@ constexpr int s1_row_blocks()
     return DP == 128 ? 3 : 2;
 }
 
+template <class F, int... I>
+__device__ __forceinline__ void for_each_index(F &&f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
 // One workgroup tile of the single-plane screen: W * 32 * RB rows against
 // every centroid. A block's fragments feed every row block of the wave;
 // blocks alternate between the accumulator sets A and B, and each block's
-// K-steps carry the epilogue of the block before it. Staging and barriers as
-// in the two-plane tile.
+// K-steps carry the epilogue of the block before it. A staged chunk holds
+// kS1Sub sub-chunks of 64 centroids in the two-plane tile's LDS layout (2 *
+// kS1Sub blocks of 32 per workgroup barrier); two chunk buffers alternate.
+// The barrier before the last block of chunk j makes chunk j + 1 visible
+// (that block refills its fragments from it) and then chunk j + 2 is
+// fetched into chunk j's buffer, which no wave reads any more.
 template <int DP, int W>
 __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restrict__ lds)
 {
@@ -847,7 +860,9 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
     constexpr int RB = s1_row_blocks<DP>();
     constexpr int NT = W * 64;
     using St = QStager<DP, NT, 1>;
-    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;  // one 64-centroid sub-chunk
+    constexpr int SB = kS1Sub * CS;                  // one staged chunk
+    constexpr int NB = 2 * kS1Sub;                   // 32-centroid blocks per staged chunk
     constexpr int BLK = 32 * St::kPitch;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -873,18 +888,23 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
     const char *B0 = lds + St::kBias + 16 * h;
     const int idh = 4 * h;
     const int nch = (int)a.nchunks;
-    auto abuf = [&](int jj) { return A0 + (jj & 1) * CS; };
-    auto bbuf = [&](int jj) { return reinterpret_cast<const int *>(B0 + (jj & 1) * CS); };
+    // block b (0 .. NB - 1) of staged chunk jj
+    auto abuf = [&](int jj, int b) { return A0 + (jj & 1) * SB + (b >> 1) * CS + (b & 1) * BLK; };
+    auto bbuf = [&](int jj, int b) {
+        return reinterpret_cast<const int *>(B0 + (jj & 1) * SB + (b >> 1) * CS) + 32 * (b & 1);
+    };
 
     St q;
     q.init();
-    q.fetch(a.qc1, a.negb1, 0, a.cpad, lds);
-    __syncthreads();
-    q.fetch(a.qc1, a.negb1, kQChunk, a.cpad, lds + CS);
-    auto stage = [&](int jj) {
-        __syncthreads();
-        q.fetch(a.qc1, a.negb1, (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
+    auto fetch = [&](int jj) {
+        char *buf = lds + (jj & 1) * SB;
+#pragma unroll
+        for (int u = 0; u < kS1Sub; ++u)
+            q.fetch(a.qc1, a.negb1, (int64_t)jj * kS1Chunk + u * kQChunk, a.cpad, buf + u * CS);
     };
+    fetch(0);
+    __syncthreads();
+    fetch(1);
 
     // set B starts as a block of lowest scores: the first epilogue inserts nothing
     i32x16 sa[RB], sb[RB];
@@ -892,27 +912,31 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sb[rb][r] = kNoScore;
-    i32x16 bias = load_bias(bbuf(0));
+    i32x16 bias = load_bias(bbuf(0, 0));
     Frags1<DP> f;
-    load_frags1<DP>(abuf(0), f);
+    load_frags1<DP>(abuf(0, 0), f);
 
-    // block (jj, cb) into set A while set B = the block before drains, and back
-    auto blockA = [&](int jj, int cb, const char *nA, const int *nB) {
-        s1_block<DP, RB>(f, xf, bias, sa, sb, idh + jj * kQChunk + 32 * cb - 32, st, nA, nB);
+    // block b of chunk jj into set A (b even) or B while the other set (the
+    // block before) drains; fragments refill from the next block
+    auto block = [&](int jj, auto bc) {
+        constexpr int b = decltype(bc)::value;
+        const char *nA = b + 1 < NB ? abuf(jj, b + 1) : abuf(jj + 1, 0);
+        const int *nB = b + 1 < NB ? bbuf(jj, b + 1) : bbuf(jj + 1, 0);
+        const int idp = idh + jj * kS1Chunk + 32 * b - 32;
+        if constexpr (b % 2 == 0)
+            s1_block<DP, RB>(f, xf, bias, sa, sb, idp, st, nA, nB);
+        else
+            s1_block<DP, RB>(f, xf, bias, sb, sa, idp, st, nA, nB);
     };
-    auto blockB = [&](int jj, int cb, const char *nA, const int *nB) {
-        s1_block<DP, RB>(f, xf, bias, sb, sa, idh + jj * kQChunk + 32 * cb - 32, st, nA, nB);
-    };
-    blockA(0, 0, abuf(0) + BLK, bbuf(0) + 32);
-    stage(1);
     for (int j = 0;; ++j) {
-        blockB(j, 1, abuf(j + 1), bbuf(j + 1));
+        for_each_index([&](auto bc) { block(j, bc); }, std::make_integer_sequence<int, NB - 1>{});
+        __syncthreads();
+        fetch(j + 2);
+        block(j, std::integral_constant<int, NB - 1>{});
         if (j + 1 == nch) break;
-        blockA(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
-        stage(j + 2);
     }
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) s1_tile_test(sb[rb], idh + (nch - 1) * kQChunk + 32, st[rb]);
+    for (int rb = 0; rb < RB; ++rb) s1_tile_test(sb[rb], idh + (nch - 1) * kS1Chunk + 32 * (NB - 1), st[rb]);
 
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -926,7 +950,7 @@ __global__ __launch_bounds__(W * 64, 2) void screen1_kernel(ScreenI8Args a)
 {
     using St = QStager<DP, W * 64, 1>;
     constexpr int CS = (St::kBytes + 15) / 16 * 16;
-    __shared__ __attribute__((aligned(16))) char lds[2 * CS];
+    __shared__ __attribute__((aligned(16))) char lds[2 * kS1Sub * CS];
     if (*a.q_bad || *a.q_bad1) return;  // another screen takes every row
     constexpr int rows_per_tile = W * 32 * s1_row_blocks<DP>();
     const int64_t ntiles = (a.nrows + rows_per_tile - 1) / rows_per_tile;
@@ -951,6 +975,8 @@ hipError_t launch_s1(const ScreenI8Args &a, int num_cus, hipStream_t s)
 
 int64_t quantized_pad(int64_t C) { return (C + kQChunk - 1) / kQChunk * kQChunk; }
 
+int64_t quantized_pad1(int64_t C) { return (C + kS1Chunk - 1) / kS1Chunk * kS1Chunk; }
+
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
                                      uint32_t *q_bad, hipStream_t s)
 {
@@ -964,16 +990,20 @@ hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
                                       uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s)
 {
-    const int64_t cpad = quantized_pad(C);
+    const int64_t cpad = quantized_pad1(C);
     const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
     hipLaunchKernelGGL(quantize1_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, q1, negb1,
                        q_bad1, e_bits);
     return hipGetLastError();
 }
 
-hipError_t launch_screen_i8_single(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s)
+hipError_t launch_screen_i8_single(int DP, const ScreenI8Args &a0, int num_cus, hipStream_t s)
 {
-    if (a.nrows <= 0) return hipSuccess;
+    if (a0.nrows <= 0) return hipSuccess;
+    // the single plane is padded to whole staged chunks
+    ScreenI8Args a = a0;
+    a.cpad = quantized_pad1(a0.ncent);
+    a.nchunks = a.cpad / kS1Chunk;
     switch (DP) {
     case 32: return launch_s1<32>(a, num_cus, s);
     case 64: return launch_s1<64>(a, num_cus, s);

@@ -106,11 +106,13 @@ def check(oracle_mod, lab, wl, stats, x, c):
 
 
 @pytest.mark.parametrize("mode", [0, 1])
-@pytest.mark.parametrize("N,C,D,cus", [(1500, 130, 128, 3), (700, 3, 96, 2), (1100, 65, 256, 3), (600, 70, 36, 1)])
+@pytest.mark.parametrize("N,C,D,cus", [(1500, 130, 128, 3), (700, 3, 96, 2), (1100, 65, 256, 3), (600, 70, 36, 1),
+                                       (900, 530, 64, 2)])
 def test_emulated_screen_matches_oracle(emu_bin, tmp_path, oracle_mod, N, C, D, cus, mode):
     """Several row tiles per workgroup (persistent loop), ragged last tiles,
     C not a multiple of the 64-centroid chunk, and each padded width; mode 1
-    runs the single plane first (padded widths up to 128)."""
+    runs the single plane first (padded widths up to 128; C = 530 spans three
+    of its 256-centroid staged chunks, the last one ragged)."""
     x, c = rows_and_centroids(N, C, D, seed=N + C + D)
     lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c, num_cus=cus, mode=mode)
     assert q_bad == 0

@@ -60,8 +60,9 @@ int main(int argc, char **argv)
     const int mode = argc > 5 ? atoi(argv[5]) : 0;
     const bool single = mode == 1 && DP <= 128;
     const int64_t list_cap = std::min<int64_t>(N, 4096 + N / 16);
-    int8_t *qc1 = single ? alloc<int8_t>(cpad * DP, 0) : nullptr;
-    int32_t *negb1 = single ? alloc<int32_t>(cpad, 0) : nullptr;
+    const int64_t cpad1 = quantized_pad1(C);
+    int8_t *qc1 = single ? alloc<int8_t>(cpad1 * DP, 0) : nullptr;
+    int32_t *negb1 = single ? alloc<int32_t>(cpad1, 0) : nullptr;
     int32_t *list = single ? alloc<int32_t>(list_cap, 0) : nullptr;
     uint32_t *q_bad1 = alloc<uint32_t>(1, 0);
     uint32_t *e_bits = alloc<uint32_t>(1, 0);
