@@ -143,6 +143,93 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
     if (lane == 0) jpart[j] = jp;
 }
 
+// uint8 rows with D = 16 U (U = 1, 2, 4, 8 or 16 lanes per row) and 16-byte
+// aligned rows: lane l reads the 16 bytes of dimensions 16 (l % U) .. + 15 of
+// member l / U of each group of 64 / U members (one 16-byte load per lane,
+// 64 / U rows per wave instruction), P groups in flight. The per-dimension
+// sums are exact integers, so their order does not matter and the means are
+// those of the byte-wise kernel bit for bit; the objective is the same fp64
+// sum in another order.
+template <int U>
+__global__ __launch_bounds__(256) void update_u8v_kernel(const uint8_t *__restrict__ X, int64_t N, int D,
+                                                         int64_t ld, const float *__restrict__ cin, int64_t C,
+                                                         const int64_t *__restrict__ counts,
+                                                         const int64_t *__restrict__ offsets,
+                                                         const uint32_t *__restrict__ perm, uint64_t seed,
+                                                         int32_t iter, float *__restrict__ cout,
+                                                         double *__restrict__ jpart, int64_t x_group)
+{
+    constexpr int R = 64 / U;  // members per wave load
+    constexpr int P = 4;       // loads in flight per lane
+    const int lane = threadIdx.x & 63;
+    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (j >= C) return;
+    {
+        const int64_t g = blockIdx.y;
+        X += g * x_group;
+        cin += g * C * D;
+        cout += g * C * D;
+        counts += g * C;
+        offsets += g * (C + 1);
+        perm += g * N;
+        jpart += g * C;
+        seed += (uint64_t)g;
+    }
+    const int64_t n = counts[j];
+    const int64_t o = offsets[j];
+    const int u = lane % U, r = lane / U;
+    double cj[16];
+    unsigned long long sum[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        cj[e] = (double)cin[j * D + 16 * u + e];
+        sum[e] = 0;
+    }
+    double jp = 0.0;
+    for (int64_t t0 = 0; t0 < n; t0 += 64) {
+        const int cnt = (int)min((int64_t)64, n - t0);
+        const uint32_t myidx = lane < cnt ? perm[o + t0 + lane] : 0u;
+        for (int q0 = 0; q0 < cnt; q0 += P * R) {
+            uint4 v[P];
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+                const int m = q0 + p * R + r;  // member within the chunk of 64
+                const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, m & 63);
+                v[p] = m < cnt ? *reinterpret_cast<const uint4 *>(X + i * ld + 16 * u) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+                if (q0 + p * R + r < cnt) {
+                    const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const uint32_t b = (w[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+                        sum[e] += b;
+                        const double t = (double)b - cj[e];
+                        jp = fma(t, t, jp);
+                    }
+                }
+            }
+        }
+    }
+    // lanes with the same dimensions (same l % U) add their partial sums
+#pragma unroll
+    for (int off = U; off < 64; off <<= 1)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sum[e] += __shfl_xor(sum[e], off);
+    int64_t rr = -1;
+    if (n == 0) rr = reseed_row(seed, iter, j, N);
+    if (r == 0) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int d = 16 * u + e;
+            cout[j * D + d] = n > 0 ? (float)((double)sum[e] / (double)n) : (float)X[rr * ld + d];
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) jp += __shfl_xor(jp, off);
+    if (lane == 0) jpart[j] = jp;
+}
+
 // Block g adds the C parts of group g in a fixed order into out[g].
 __global__ __launch_bounds__(1024) void sum_parts_kernel(const double *__restrict__ part,
                                                          int64_t C, double *__restrict__ out)
@@ -170,7 +257,15 @@ hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
                                 hipStream_t s, int groups, int64_t x_group)
 {
     const dim3 grid((unsigned)((C + 3) / 4), (unsigned)groups);
-    if (rowtype == kRowU8)
+    const int U = D / 16;
+    const bool vec = rowtype == kRowU8 && D % 16 == 0 && (U == 1 || U == 2 || U == 4 || U == 8 || U == 16) &&
+                     ld % 16 == 0 && x_group % 16 == 0 && (uintptr_t)rows % 16 == 0;
+    if (vec) {
+        auto k = U == 1 ? update_u8v_kernel<1> : U == 2 ? update_u8v_kernel<2> : U == 4 ? update_u8v_kernel<4>
+                 : U == 8 ? update_u8v_kernel<8> : update_u8v_kernel<16>;
+        hipLaunchKernelGGL(k, grid, dim3(256), 0, s, (const uint8_t *)rows, N, D, ld, cent_in, C, counts, offsets,
+                           perm, seed, iter, cent_out, jpart, x_group);
+    } else if (rowtype == kRowU8)
         hipLaunchKernelGGL(update_kernel<uint8_t>, grid, dim3(256), 0, s, (const uint8_t *)rows, N, D,
                            ld, cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group);
     else

@@ -82,7 +82,8 @@ def test_kmeans_empty_clusters_reseed(ivf_ctx, oracle_mod):
 
 
 @pytest.mark.parametrize("N,C,D", [(1, 1, 4), (500, 1, 8), (257, 256, 16), (1000, 1000, 36),
-                                   (3000, 300, 200), (2000, 150, 256)])
+                                   (3000, 300, 200), (2000, 150, 256), (1200, 90, 32), (4000, 40, 64),
+                                   (300, 400, 128)])
 def test_kmeans_small_shapes(ivf_ctx, oracle_mod, N, C, D):
     rng = np.random.default_rng(N + C)
     x = rng.integers(0, 256, (N, D)).astype(np.uint8)
