@@ -223,3 +223,48 @@ def test_build_edge_cases(oracle_mod):
         oracle_mod.build_lists(np.array([0, 3]), 3)
     with pytest.raises(ValueError):
         oracle_mod.build_lists(np.array([-1]), 3)
+
+
+def test_update_f32_order_golden(oracle_mod):
+    """fp32 rows: the cluster sums are fp64 sums in ascending row order. The
+    golden rows make that order and that precision visible: a reversed or
+    exact sum, fp32 or extended-precision accumulation each change a mean."""
+    rows, labels, want = [], [], {}
+    for line in open(os.path.join(GOLDEN, "kmeans_update_f32_order.txt")):
+        f = line.split("#")[0].split()
+        if not f:
+            continue
+        if f[0] == "row":
+            v = int(f[1])
+            assert float(np.float32(v)) == v  # every row value is an fp32 number
+            rows.append(v)
+            labels.append(int(f[2]))
+        elif f[0] == "centroid":
+            want[int(f[1])] = float(f[2])
+    x = np.array(rows, np.float32).reshape(-1, 1)
+    lab = np.array(labels, np.int32)
+    cent, cnt = oracle_mod.kmeans_update(x, lab, 4)
+    assert (cnt == np.bincount(lab, minlength=4)).all()
+    for j in range(4):
+        assert float(cent[j, 0]) == want[j], (j, float(cent[j, 0]), want[j])
+
+    # the reading, worked out in exact arithmetic with one fp64 rounding per
+    # addition (float(Fraction) is correctly rounded), gives the golden means;
+    # the other readings give different ones in the clusters built for them
+    def mean(vals, acc="f64", order=1):
+        s = Fraction(0)
+        for v in vals[::order]:
+            if acc == "f64":
+                s = Fraction(float(s + v))
+            elif acc == "f32":
+                s = Fraction(float(np.float32(float(s + v))))
+            else:
+                s = s + v
+        return float(np.float32(float(Fraction(float(s)) / len(vals))))
+
+    members = {j: [Fraction(v) for v, l in zip(rows, labels) if l == j] for j in range(4)}
+    for j in range(4):
+        assert mean(members[j]) == want[j]
+    assert mean(members[0], order=-1) != want[0] and mean(members[0], acc="exact") != want[0]
+    assert mean(members[1], order=-1) != want[1] and mean(members[1], acc="exact") != want[1]
+    assert mean(members[2], acc="f32") != want[2]
