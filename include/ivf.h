@@ -6,10 +6,10 @@
  *   - coarse search, Eq. (1), Sec. "ANN Search and IVF": for each query the
  *     nprobe centroids of smallest squared L2 distance;
  *   - the distances are evaluated as in Eq. (6), Sec. "GPU coarse search"
- *     (||q||^2 + ||c||^2 - 2 q.c, the -2 q.c term as a dense fp32 MFMA
- *     contraction over LDS-staged tiles), with the row-wise top-P selected on
- *     the device so that only O(B*P) ids and distances are produced
- *     ("On-device list selection", same section);
+ *     (||q||^2 + ||c||^2 - 2 q.c, the -2 q.c term as a dense MFMA contraction
+ *     over LDS-staged centroid tiles, never written to memory), with the
+ *     row-wise top-P selected on the device so that only O(B*P) ids and
+ *     distances are produced ("On-device list selection", same section);
  *   - IVF construction, Sec. "System Architecture" (index layout) and
  *     Sec. "Fast Index Construction": Lloyd k-means iterations (assignment +
  *     mean update) and the assignment of every base vector to its nearest
@@ -19,9 +19,23 @@
  * exactly what the definition gives with distances evaluated in fp64 as
  *     s = 0; for d = 0..D-1: t = (double)x_d - (double)c_d; s = fma(t, t, s)
  * and ties broken by the lower centroid id. Returned distances are that s
- * rounded to fp32. The fp32 MFMA pass only screens candidates; a rigorous
- * rounding-error bound decides which candidates are re-evaluated in fp64 and
- * when a query or row falls back to an exact fp64 scan of all centroids.
+ * rounded to fp32. The MFMA contraction only screens candidates; a rigorous
+ * error bound decides which candidates are re-evaluated in fp64 and when a
+ * query or row falls back to an exact fp64 scan of all centroids. Which
+ * matrix unit screens depends on the data type:
+ *   - fp32 queries and rows: fp32 MFMA (v_mfma_f32_32x32x2_f32); the bound is
+ *     the fp32 dot-product rounding bound for any summation order;
+ *   - uint8 rows (k-means and assignment): int8 MFMA
+ *     (v_mfma_i32_32x32x32_i8) on rows x - 128 against quantised centroids,
+ *     whose integer scores are exact; the bound is the quantisation error
+ *     alone. For D <= 128 one int8 plane rint(c - 128) screens first and
+ *     settles most rows; the rows it leaves are screened on two int8 planes
+ *     of the 16-bit fixed-point value rint(256 (c - 128)). A call whose
+ *     centroids have a coordinate outside [0, 255.998] (which does not
+ *     quantise) is screened on fp32 MFMA instead; the switch happens on the
+ *     device, without a host synchronisation.
+ * Either way the results are the exact ones above; the screen chosen changes
+ * speed only.
  *
  * Conventions shared by every call:
  *   - Array arguments are DEVICE pointers on the context's device, row-major,
@@ -38,7 +52,11 @@
  *     IVF_ENOMEM with the required size in ivf_last_error(). Two calls that
  *     share a context must not overlap on different streams.
  *   - Q, N == 0 is a no-op returning IVF_OK.
- *   - Supported shapes: 4 <= D <= 256 with D % 4 == 0 (else IVF_EUNSUPPORTED).
+ *   - Supported shapes: 4 <= D <= 256 with D % 4 == 0 (else IVF_EUNSUPPORTED);
+ *     the row-major register tiles of the screens hold at most 256 dims.
+ *   - Row counts N up to 2^32 - 1 (row ids are uint32 in the permutation);
+ *     the assignment screens rows in slices of 2^28, so row ids inside a
+ *     launch always fit int32.
  *   - Input values must be finite, with squared vector norms below FLT_MAX;
  *     results are unspecified otherwise (inputs are not scanned for this).
  */
@@ -201,7 +219,10 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *   IVF_OPT_RESCREEN_CAP    > 0: capacity of the single plane's list of rows
  *                           for the two-plane screen (default 4,096 + N / 16;
  *                           past it the two-plane screen takes every row);
- *                           speed only, never results */
+ *                           speed only, never results
+ *   IVF_OPT_ASSIGN_SLICE    > 0: rows per assignment slice, below the
+ *                           default 2^28 (each slice is screened with its own
+ *                           worklists); speed only, never results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,
@@ -211,7 +232,8 @@ typedef enum {
     IVF_OPT_FP32_SCREEN = 5,
     IVF_OPT_I8_TWO_PLANE_ONLY = 6,
     IVF_OPT_FORCE_RESCREEN = 7,
-    IVF_OPT_RESCREEN_CAP = 8
+    IVF_OPT_RESCREEN_CAP = 8,
+    IVF_OPT_ASSIGN_SLICE = 9
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

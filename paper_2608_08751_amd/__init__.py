@@ -23,6 +23,7 @@ from ._binding import (  # noqa: F401
     IVF_OP_KMEANS_STEP,
     IVF_OP_PQ_TRAIN_STEP,
     IVF_OP_ROUTE,
+    IVF_OPT_ASSIGN_SLICE,
     IVF_OPT_BUILD_BLOCKS,
     IVF_OPT_FORCE_FALLBACK,
     IVF_OPT_FORCE_RESCREEN,

@@ -33,6 +33,7 @@ struct ivf_ctx {
     int two_plane_only = 0;  // 1: no single-plane int8 pre-screen
     int force_rescreen = 0;  // 1: the single-plane screen lists every row
     int64_t rescreen_cap = 0;  // > 0: smaller capacity of that list (tests)
+    int64_t assign_slice = 0;  // > 0: shorter assignment slices (tests)
     unsigned long long *last_stats = nullptr;  // device, inside the workspace
     int64_t last_sample = 0;
     // kernel timing (IVF_OPT_PROFILE): an event pair per launch of the last call
@@ -54,6 +55,8 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kRouteBatch = 16384;
 constexpr int kMaxNprobe = 1024;
 constexpr int kMaxD = 256;
+// Rows per assignment slice (row ids inside a slice fit int32).
+constexpr int64_t kAssignSlice = (int64_t)1 << 28;
 
 ivf_status fail(ivf_ctx *ctx, ivf_status st, const char *fmt, ...)
 {
@@ -271,11 +274,11 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_
         if (qdp <= 128) {
             l.qc1 = c.take<int8_t>((size_t)quantized_pad1(C) * qdp);
             l.negb1 = c.take<int32_t>(quantized_pad1(C));
-            l.list_cap = rescreen_cap(N);
+            l.list_cap = rescreen_cap(std::min(N, kAssignSlice));
             l.list = c.take<int32_t>(l.list_cap);
         }
     }
-    l.wl_cap = worklist_cap(N);
+    l.wl_cap = worklist_cap(std::min(N, kAssignSlice));
     l.wl = c.take<int32_t>(l.wl_cap);
     l.fb_d = c.take<double>(kFbSplitEntries);
     l.fb_i = c.take<int32_t>(kFbSplitEntries);
@@ -385,74 +388,96 @@ ivf_status check_common(ivf_ctx *ctx, int64_t C, int32_t D)
 }
 
 // Assignment of N rows (top-1 with certification and fallback) into labels.
+// The centroid preparation (norms, quantised planes) runs once; the rows are
+// then screened in slices of at most `slice` rows, each with its own
+// worklists, so that the row ids the screens and the fallback pass around
+// (int32, relative to the slice) stay below 2^31 for any N <= 2^32 - 1.
 ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N,
                           const float *cent, int64_t C, int D, int32_t *labels,
                           const AssignLayout &l)
 {
     hipStream_t s = ctx->stream;
     const int DP = padded_dim(D);
+    const size_t rb = (size_t)D * (rowtype == kRowU8 ? 1 : 4);
+    const int64_t slice = ctx->assign_slice > 0 ? std::min<int64_t>(ctx->assign_slice, kAssignSlice) : kAssignSlice;
     TIMED("fill", launch_fill_u32(l.sc.mc2_bits, 64, 0u, s));
     TIMED("centroid_norms", launch_centroid_norms(cent, C, D, l.cnorm, l.sc.mc2_bits, s));
-    ScreenArgs a{};
-    a.rows = rows;
-    a.nrows = N;
-    a.D = D;
-    a.cent = cent;
-    a.cnorm = l.cnorm;
-    a.c_begin = 0;
-    a.c_end = C;
-    a.nchunks = (C + kChunk - 1) / kChunk;
-    a.mc2_bits = l.sc.mc2_bits;
-    a.bound_coef = bound_coef(DP);
-    a.labels = labels;
-    a.wl = l.wl;
-    a.wl_cnt = l.sc.wl_cnt;
-    a.wl_cap = l.wl_cap;
-    a.stats = l.sc.stats;
-    a.force_fallback = ctx->force_fallback;
-    if (rowtype == kRowU8 && !ctx->fp32_screen) {
+    const bool int8 = rowtype == kRowU8 && !ctx->fp32_screen;
+    const bool single = int8 && l.qc1 && !ctx->two_plane_only;
+    uint32_t *q_bad = l.sc.mc2_bits + 2;
+    uint32_t *q_bad1 = l.sc.mc2_bits + 3;
+    uint32_t *e_bits = l.sc.mc2_bits + 4;
+    uint32_t *list_cnt = l.sc.mc2_bits + 5;
+    if (int8) {
         // int8 MFMA screens; the fp32 kernel runs only if some centroid does not quantise
-        uint32_t *q_bad = l.sc.mc2_bits + 2;
         TIMED("quantize", launch_quantize_centroids(cent, C, D, DP, l.qc, l.negb, q_bad, s));
-        ScreenI8Args q{};
-        q.rows = (const uint8_t *)rows;
-        q.nrows = N;
-        q.D = D;
-        q.cent = cent;
-        q.qc = l.qc;
-        q.negb = l.negb;
-        q.cpad = quantized_pad(C);
-        q.nchunks = q.cpad / 64;
-        q.q_bad = q_bad;
-        q.labels = labels;
-        q.wl = l.wl;
-        q.wl_cnt = l.sc.wl_cnt;
-        q.wl_cap = l.wl_cap;
-        q.stats = l.sc.stats;
-        q.force_fallback = ctx->force_fallback;
-        q.ncent = C;
-        if (l.qc1 && !ctx->two_plane_only) {
-            // single plane first; the two planes then screen the rows it leaves
-            uint32_t *q_bad1 = l.sc.mc2_bits + 3;
-            uint32_t *e_bits = l.sc.mc2_bits + 4;
+        if (single)
             TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, s));
-            q.qc1 = l.qc1;
-            q.negb1 = l.negb1;
-            q.e_bits = e_bits;
-            q.q_bad1 = q_bad1;
-            q.list = l.list;
-            q.list_cnt = l.sc.mc2_bits + 5;
-            q.list_cap = ctx->rescreen_cap > 0 ? std::min<int64_t>(ctx->rescreen_cap, l.list_cap) : l.list_cap;
-            // a forced fallback passes every row on to the two planes, which send it on
-            q.force_rescreen = ctx->force_rescreen || ctx->force_fallback;
-            TIMED("screen_top1_i8s", launch_screen_i8_single(DP, q, ctx->num_cus, s));
-        }
-        TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
-        a.gate = q_bad;
     }
-    TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));
-    TIMED("assign_fallback", launch_assign_fallback(rows, rowtype, N, D, cent, C, labels, l.wl, l.sc.wl_cnt, l.wl_cap,
-                                                    l.fb_d, l.fb_i, 2 * ctx->num_cus, s));
+    for (int64_t r0 = 0; r0 < N; r0 += slice) {
+        const int64_t n = std::min(slice, N - r0);
+        const void *xr = (const char *)rows + (size_t)r0 * rb;
+        int32_t *lab = labels + r0;
+        if (r0 > 0) {
+            // the worklist and the single plane's list start empty for every slice
+            TIMED("fill", launch_fill_u32(l.sc.wl_cnt, 1, 0u, s));
+            if (single) TIMED("fill", launch_fill_u32(list_cnt, 1, 0u, s));
+        }
+        ScreenArgs a{};
+        a.rows = xr;
+        a.nrows = n;
+        a.D = D;
+        a.cent = cent;
+        a.cnorm = l.cnorm;
+        a.c_begin = 0;
+        a.c_end = C;
+        a.nchunks = (C + kChunk - 1) / kChunk;
+        a.mc2_bits = l.sc.mc2_bits;
+        a.bound_coef = bound_coef(DP);
+        a.labels = lab;
+        a.wl = l.wl;
+        a.wl_cnt = l.sc.wl_cnt;
+        a.wl_cap = l.wl_cap;
+        a.stats = l.sc.stats;
+        a.force_fallback = ctx->force_fallback;
+        if (int8) {
+            ScreenI8Args q{};
+            q.rows = (const uint8_t *)xr;
+            q.nrows = n;
+            q.D = D;
+            q.cent = cent;
+            q.qc = l.qc;
+            q.negb = l.negb;
+            q.cpad = quantized_pad(C);
+            q.nchunks = q.cpad / 64;
+            q.q_bad = q_bad;
+            q.labels = lab;
+            q.wl = l.wl;
+            q.wl_cnt = l.sc.wl_cnt;
+            q.wl_cap = l.wl_cap;
+            q.stats = l.sc.stats;
+            q.force_fallback = ctx->force_fallback;
+            q.ncent = C;
+            if (single) {
+                // single plane first; the two planes then screen the rows it leaves
+                q.qc1 = l.qc1;
+                q.negb1 = l.negb1;
+                q.e_bits = e_bits;
+                q.q_bad1 = q_bad1;
+                q.list = l.list;
+                q.list_cnt = list_cnt;
+                q.list_cap = ctx->rescreen_cap > 0 ? std::min<int64_t>(ctx->rescreen_cap, l.list_cap) : l.list_cap;
+                // a forced fallback passes every row on to the two planes, which send it on
+                q.force_rescreen = ctx->force_rescreen || ctx->force_fallback;
+                TIMED("screen_top1_i8s", launch_screen_i8_single(DP, q, ctx->num_cus, s));
+            }
+            TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
+            a.gate = q_bad;
+        }
+        TIMED("screen_top1", launch_screen(kModeTop1, rowtype, DP, a, ctx->screen_waves, ctx->num_cus, s));
+        TIMED("assign_fallback", launch_assign_fallback(xr, rowtype, n, D, cent, C, lab, l.wl, l.sc.wl_cnt,
+                                                        l.wl_cap, l.fb_d, l.fb_i, 2 * ctx->num_cus, s));
+    }
     ctx->last_stats = l.sc.stats;
     ctx->last_sample = 0;
     return IVF_OK;
@@ -595,6 +620,10 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
     case IVF_OPT_RESCREEN_CAP:
         if (value < 0) return fail(ctx, IVF_EINVAL, "rescreen capacity must be >= 0");
         ctx->rescreen_cap = value;
+        return IVF_OK;
+    case IVF_OPT_ASSIGN_SLICE:
+        if (value < 0) return fail(ctx, IVF_EINVAL, "assignment slice must be >= 0");
+        ctx->assign_slice = value;
         return IVF_OK;
     case IVF_OPT_BUILD_BLOCKS:
         if (value < 0 || value > 65536) return fail(ctx, IVF_EINVAL, "build blocks out of range");

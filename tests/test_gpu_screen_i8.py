@@ -239,3 +239,26 @@ def test_i8_single_plane_integer_centroids(ivf_ctx, oracle_mod):
     c = x[synth.kmeans_init(20000, 700, seed=31)].astype(np.float32)
     st = check_assign(ivf_ctx, oracle_mod, x, c)
     assert st["default"]["rescreen"] <= 10
+
+
+@pytest.mark.parametrize("slice_rows,extra", [(1000, {}), (997, {"IVF_OPT_FORCE_RESCREEN": 1}),
+                                              (4096, {"IVF_OPT_FORCE_FALLBACK": 1}),
+                                              (1500, {"IVF_OPT_RESCREEN_CAP": 3})])
+@pytest.mark.parametrize("path", ["default", "fp32"])
+def test_assignment_in_row_slices(ivf_ctx, oracle_mod, slice_rows, extra, path):
+    """The assignment screens rows in slices (2^28 rows by default, so that
+    row ids inside a launch fit int32); short slices (IVF_OPT_ASSIGN_SLICE)
+    with ragged last slices, every row handed on, every row in the fallback,
+    or an overflowing list: the labels, counts, offsets and permutation do not
+    change, and the statistics add up over the slices."""
+    x, c = rows_and_centroids(12345, 333, 128, seed=71)
+    olab = oracle_mod.assign(x, c)
+    ocnt, ooff, operm = oracle_mod.build_lists(olab, c.shape[0])
+    lab, cnt, off, perm, st = gpu_assign(ivf_ctx, x, c, path, IVF_OPT_ASSIGN_SLICE=slice_rows, **extra)
+    print("slice %d %s %s stats %s" % (slice_rows, path, extra, st), flush=True)
+    assert (lab == olab).all()
+    assert (cnt == ocnt).all() and (off == ooff).all() and (perm == operm).all()
+    if "IVF_OPT_FORCE_FALLBACK" in extra:
+        assert st["fallback"] == 12345
+    if "IVF_OPT_FORCE_RESCREEN" in extra and path == "default":
+        assert st["rescreen"] == 12345
