@@ -1,27 +1,29 @@
 #!/usr/bin/env python3
-"""Benchmark of the IVF routing / construction hot path on one MI355X.
+"""Benchmark of the IVF routing and construction hot path on one MI355X.
 
-One step = one pass of the whole hot path over one batch of synthetic input,
-on the 65,536-centroid, D = 128 index of the uint8-valued workloads:
-  1. ivf_kmeans_step  on 10M uint8 training rows (centroid quantisation,
-                      fused single-plane int8-MFMA screening with register
-                      top-1, certified fp64 refine, two-plane int8 screen of
-                      the rows the single plane leaves, list build, Lloyd
-                      update with reseeding, objective);
-  2. ivf_assign_build on a batch of 10M uint8 base rows with the new
-                      centroids (full assignment + histogram / scan / stable
-                      scatter into cluster-major lists);
-  3. ivf_route        of 10,000 integer-valued fp32 queries, nprobe 64
-                      (threshold sample, fused filter, certified selection).
-Every routed query and every assigned row is one vector scored against all
-65,536 centroids with top-k selection, so `value` = (train rows + base rows +
-queries) / step time, in vectors/s. Inputs are resident in HBM before timing.
+Every workload is measured at its stated size, with its inputs resident in
+HBM before timing, and next to the CPU oracle on this host:
 
-The JSON line also carries, per call, the rates; the dominant kernel's
-roofline measured live with HIP events on the library's stream; and the CPU
-oracle timed on a bounded sample on this host (`cpu_baseline`). The
-normalised-float routing workload (262,144 centroids, D = 96, nprobe 128) is
-timed separately as an extra.
+  1. routing, tiny: 1,024 centroids, D = 128, 1,000 integer-valued queries,
+     nprobe 16 (oracle in full);
+  2. routing, uint8-valued: 65,536 centroids, D = 128, 10,000 queries,
+     nprobe 64;
+  3. routing, normalised floats: 262,144 unit-norm centroids, D = 96, 10,000
+     queries, nprobe 128;
+  4. k-means: 10 Lloyd iterations on 10M uint8 rows (65,536-component
+     mixture, std 20), 65,536 centroids from a seeded row sample;
+  5. assign-build: 1e9 uint8 rows of the same generator (128 GB resident,
+     produced on the device in 64M-row chunks) assigned to the 65,536
+     mixture means by top-1 L2, then the inverted-list build.
+
+The timed step (`--steps`, after `--warmup` untimed ones) is workload 5, the
+largest: one ivf_assign_build call over all 1e9 rows. `value` = rows / step
+time. `roofline` is that step's dominant kernel (the single-plane int8
+screen); `cpu_baseline` is the oracle on a bounded sample of the same
+assignment. The other workloads are in `configs`, each with its own rate,
+roofline fraction and oracle timing. NEXT-row kernels (list-major layout,
+residual PQ, ADC scan, candidate-restricted assignment) run on the k-means
+output and are reported under `extra`.
 """
 from __future__ import annotations
 
@@ -40,26 +42,24 @@ PEAK_INT8_MFMA_TOPS = 5000.0   # MI355X dense int8 matrix peak
 PEAK_HBM_GBS = 8000.0
 PEAK_FP64_VECTOR_TFLOPS = 78.6
 
+C_BIG, D_U8 = 65536, 128
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=3, help="timed assign-build calls over the 1e9 rows")
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--train-rows", type=int, default=10_000_000)
-    ap.add_argument("--base-rows", type=int, default=10_000_000)
-    ap.add_argument("--queries", type=int, default=10_000)
+    ap.add_argument("--rows", type=int, default=10**9, help="rows of the assign-build workload")
+    ap.add_argument("--kmeans-rows", type=int, default=10_000_000)
+    ap.add_argument("--kmeans-iters", type=int, default=10)
+    ap.add_argument("--only", default="", help="comma-separated subset of 1,2,3,4,5 (profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-extra", action="store_true", help="skip the normalised routing extra")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
-    ap.add_argument("--build-rows", type=int, default=1_000_000_000,
-                    help="rows for the separately timed list build at scale (0 = skip)")
+    ap.add_argument("--no-extra", action="store_true", help="skip the NEXT-row kernels")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target oracle time for the headline CPU baseline")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="also run one device copy of this size (HBM counter calibration for rocprofv3)")
-    ap.add_argument("--fp32-screen", action="store_true",
-                    help="screen the uint8 rows on fp32 MFMA (IVF_OPT_FP32_SCREEN) instead of int8")
-    ap.add_argument("--two-plane", action="store_true",
-                    help="screen the uint8 rows on two int8 planes only (IVF_OPT_I8_TWO_PLANE_ONLY)")
     return ap.parse_args()
 
 
@@ -78,6 +78,206 @@ def cpu_model():
     return "unknown"
 
 
+def dev(a):
+    import numpy as np
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def call_times(ctx, fn, reps, warm=3):
+    """Whole-call times (ms) of `fn` from HIP events on the stream the
+    library runs on (torch's current stream, which the context binds to),
+    after `warm` untimed calls; plus the per-kernel timeline of the last call."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    fn()
+    tl = ctx.kernel_times()
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    return ts, tl
+
+
+def oracle_rate(fn, n_probe, n_max, target_s):
+    """Runs fn(n) on a probe of n_probe units, then on as many units as fit
+    about target_s seconds (at most n_max); returns (units, seconds)."""
+    t = time.perf_counter()
+    fn(n_probe)
+    dt = time.perf_counter() - t
+    n = int(min(n_max, max(n_probe, n_probe * target_s / max(dt, 1e-6))))
+    t = time.perf_counter()
+    fn(n)
+    return n, time.perf_counter() - t
+
+
+# ------------------------------------------------------------------ routing
+
+def bench_route(ctx, name, d, k, oracle_s, full_oracle=False):
+    """Routing of d["queries"] against d["centroids"], nprobe k: median of 10
+    whole calls; the oracle's queries/s on all its queries (full_oracle) or
+    a bounded sample of them."""
+    import numpy as np
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    q, c = dev(d["queries"]), dev(d["centroids"])
+    Q, D = q.shape
+    C = c.shape[0]
+    ids = torch.empty((Q, k), dtype=torch.int32, device="cuda")
+    dist = torch.empty((Q, k), dtype=torch.float32, device="cuda")
+    fn = lambda: ivf.ivf_route(ctx, q, c, k, out_ids=ids, out_dist=dist)
+    ts, tl = call_times(ctx, fn, 10)
+    st = ctx.last_stats()
+    t = float(np.median(ts))
+    flops = 2.0 * Q * C * D
+    tf = flops / (t * 1e-3) / 1e12
+    out = {"queries": Q, "centroids": C, "dim": D, "nprobe": k, "ms_per_call": t,
+           "queries_per_s": Q / (t * 1e-3), "tflops": tf, "fp32_mfma_frac": tf / PEAK_FP32_MFMA_TFLOPS,
+           "kernels_ms": {n.split("/", 1)[1]: ms for n, ms in tl}, "stats": st}
+    if oracle_s is not None:
+        import oracle
+
+        qh, ch = d["queries"], d["centroids"]
+        if full_oracle:
+            t0 = time.perf_counter()
+            oids, _ = oracle.route(qh, ch, k)
+            n, dt = Q, time.perf_counter() - t0
+            same = bool((oids == ids.cpu().numpy()).all())
+        else:
+            n, dt = oracle_rate(lambda m: oracle.route(qh[:m], ch, k), 16, Q, oracle_s)
+            same = None
+        out["oracle"] = {"queries_per_s": n / dt, "queries": n, "seconds": dt, "cores": oracle.num_threads(0),
+                         "sample": "all queries" if full_oracle else "the first %d queries" % n}
+        if same is not None:
+            out["oracle"]["ids_equal"] = same
+    log("%s: %.3f ms per call, %.1f TFLOP/s" % (name, t, tf))
+    return out
+
+
+# ------------------------------------------------------------------ k-means
+
+def bench_kmeans(ctx, N, iters, oracle_s):
+    """Lloyd's algorithm from the seeded row sample: `iters` iterations, each
+    one ivf_kmeans_step timed with HIP events; per iteration its time,
+    objective and screening statistics."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    C, D = C_BIG, D_U8
+    means = dev(synth.uniform_means(C, D, seed=0))
+    x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
+    synth.device_mixture_rows_u8(means, 0, N, x, seed=0)
+    c0 = x[dev(synth.kmeans_init(N, C, seed=0))].float().contiguous()
+    lab = torch.empty(N, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(C, dtype=torch.int64, device="cuda")
+    obj = torch.empty(1, dtype=torch.float64, device="cuda")
+    cbuf = [torch.empty((C, D), dtype=torch.float32, device="cuda") for _ in range(2)]
+    # one untimed iteration loads the kernels and sizes the workspace
+    ivf.ivf_kmeans_step(ctx, x, c0, seed=0, it=0, out_labels=lab, out_centroids=cbuf[0], out_counts=cnt,
+                        out_objective=obj)
+    torch.cuda.synchronize()
+    rows = []
+    c = c0
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+    ctx.kernel_times()
+    for it in range(iters):
+        out = cbuf[it % 2]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ivf.ivf_kmeans_step(ctx, x, c, seed=0, it=it, out_labels=lab, out_centroids=out, out_counts=cnt,
+                            out_objective=obj)
+        e1.record()
+        e1.synchronize()
+        tl = ctx.kernel_times()
+        rows.append({"iteration": it, "ms": e0.elapsed_time(e1), "objective": float(obj.item()),
+                     "screen_single_plane_ms": sum(ms for n, ms in tl if n.endswith("/screen_top1_i8s")),
+                     "screen_two_planes_ms": sum(ms for n, ms in tl if n.endswith("/screen_top1_i8")),
+                     "update_ms": sum(ms for n, ms in tl if n.endswith("/kmeans_update")),
+                     "build_ms": sum(ms for n, ms in tl if "/build_" in n),
+                     "stats": ctx.last_stats()})
+        c = out
+        log("k-means iteration %d: %.1f ms, objective %.6e" % (it, rows[-1]["ms"], rows[-1]["objective"]))
+    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+    total = sum(r["ms"] for r in rows)
+    ops = 2.0 * N * C * D * iters
+    tops = ops / (total * 1e-3) / 1e12
+    res = {"rows": N, "centroids": C, "dim": D, "iterations": iters, "total_s": total * 1e-3,
+           "ms_per_iteration": total / iters, "vectors_per_s": N * iters / (total * 1e-3),
+           "algorithmic_tops": tops, "int8_mfma_frac": tops / PEAK_INT8_MFMA_TOPS,
+           "vs_fp32_mfma_peak_ratio": tops / PEAK_FP32_MFMA_TFLOPS,
+           "objective_non_increasing": all(b["objective"] <= a["objective"] * (1 + 1e-9)
+                                           for a, b in zip(rows, rows[1:])),
+           "per_iteration": rows}
+    if oracle_s is not None:
+        import oracle
+
+        ch = c0.cpu().numpy()
+        rng = np.random.default_rng(98)
+        idx = np.sort(rng.choice(N, 200000, replace=False))
+        xs = x[dev(idx)].cpu().numpy()
+        n, dt = oracle_rate(lambda m: oracle.assign(xs[:m], ch), 16, len(idx), oracle_s)
+        res["oracle"] = {"vectors_per_s": n / dt, "rows": n, "seconds": dt, "cores": oracle.num_threads(0),
+                         "sample": "nearest-centroid search of %d sampled training rows against the initial "
+                                   "65,536 centroids (the assignment of one iteration)" % n}
+    return res, x, c, lab
+
+
+# ------------------------------------------------------------- assign-build
+
+def gen_rows(N, means_dev):
+    import torch
+
+    import synth
+
+    chunk = 64 * 2**20
+    x = torch.empty((N, D_U8), dtype=torch.uint8, device="cuda")
+    for r0 in range(0, N, chunk):
+        synth.device_mixture_rows_u8(means_dev, r0, min(chunk, N - r0), x[r0:r0 + chunk], seed=0)
+    torch.cuda.synchronize()
+    return x
+
+
+def measured_traffic(rows_per_launch, record):
+    """HBM bytes per launch of the dominant kernel from a committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (calibrated against a device copy), if it
+    was taken on the current kernel sources (the record's `sources`, hashed
+    in order) and launch size; otherwise None."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", record)
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        h = hashlib.sha256()
+        for src in rec["sources"]:
+            with open(os.path.join(ROOT, src), "rb") as f:
+                h.update(f.read())
+        sha = h.hexdigest()
+    except (OSError, ValueError, KeyError, TypeError):
+        return None, None
+    if not sha.startswith(rec["sources_sha256_prefix"]) or rec["rows_per_launch"] != rows_per_launch:
+        return None, None
+    return rec["traffic_bytes"], "profiles/" + record
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -94,291 +294,230 @@ def main():
     import paper_2608_08751_amd as ivf
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
-    C, D, K = 65536, 128, 64
-    Nt, Nb, Q = args.train_rows, args.base_rows, args.queries
-
-    t0 = time.time()
-    means = torch.from_numpy(synth.uniform_means(C, D, seed=0)).to(dev)
-    x_train = torch.empty((Nt, D), dtype=torch.uint8, device=dev)
-    x_base = torch.empty((Nb, D), dtype=torch.uint8, device=dev)
-    qrows = torch.empty((Q, D), dtype=torch.uint8, device=dev)
-    synth.device_mixture_rows_u8(means, 0, Nt, x_train, seed=0)
-    synth.device_mixture_rows_u8(means, Nt, Nb, x_base, seed=0)
-    synth.device_mixture_rows_u8(means, Nt + Nb, Q, qrows, seed=0)
-    queries = qrows.float().contiguous()
-    init = torch.from_numpy(synth.kmeans_init(Nt, C, seed=0)).to(dev)
-    c0 = x_train[init].float().contiguous()
-    torch.cuda.synchronize()
-    log("inputs generated on the device in %.1f s" % (time.time() - t0))
-
+    only = set(args.only.split(",")) if args.only else {"1", "2", "3", "4", "5"}
+    osec = None if args.no_cpu_baseline else 3.0
     ctx = ivf.Context(0)
-    if args.fp32_screen:
-        ctx.set_option(ivf.IVF_OPT_FP32_SCREEN, 1)
-        top1_name = "screen_top1"
-    elif args.two_plane:
-        ctx.set_option(ivf.IVF_OPT_I8_TWO_PLANE_ONLY, 1)
-        top1_name = "screen_top1_i8"
-    else:
-        top1_name = "screen_top1_i8s"
-    lab_t = torch.empty(Nt, dtype=torch.int32, device=dev)
-    c1 = torch.empty((C, D), dtype=torch.float32, device=dev)
-    cnt_t = torch.empty(C, dtype=torch.int64, device=dev)
-    obj = torch.empty(2, dtype=torch.float64, device=dev)
-    lab_b = torch.empty(Nb, dtype=torch.int32, device=dev)
-    cnt_b = torch.empty(C, dtype=torch.int64, device=dev)
-    off_b = torch.empty(C + 1, dtype=torch.int64, device=dev)
-    perm_b = torch.empty(Nb, dtype=torch.int32, device=dev)
-    ids = torch.empty((Q, K), dtype=torch.int32, device=dev)
-    dist = torch.empty((Q, K), dtype=torch.float32, device=dev)
+    configs = {}
+    extra = {}
 
-    stats = {}
-
-    def step(record=False):
-        ivf.ivf_kmeans_step(ctx, x_train, c0, seed=0, it=0, out_labels=lab_t, out_centroids=c1,
-                            out_counts=cnt_t, out_objective=obj)
-        if record:
-            stats["kmeans"] = ctx.last_stats()
-        ivf.ivf_assign_build(ctx, x_base, c1, out_labels=lab_b, out_counts=cnt_b, out_offsets=off_b,
-                             out_perm=perm_b)
-        if record:
-            stats["assign_build"] = ctx.last_stats()
-        ivf.ivf_route(ctx, queries, c1, K, out_ids=ids, out_dist=dist)
-        if record:
-            stats["route"] = ctx.last_stats()
-
-    for _ in range(args.warmup):
-        step(record=True)
-    torch.cuda.synchronize()
-    log("warmup done; fallback/refine stats:", stats)
-
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-    ctx.kernel_times()  # clear
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(args.steps):
-        step()
-        log("step %d enqueued" % i)
-    torch.cuda.synchronize()
-    t_total = time.perf_counter() - t_start
-    timeline = ctx.kernel_times()
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-
-    ms_per_step = 1e3 * t_total / args.steps
-    vectors = Nt + Nb + Q
-    value = vectors / (t_total / args.steps)
-
-    # per-kernel aggregation over the timed steps
-    agg = {}
-    for name, ms in timeline:
-        a = agg.setdefault(name, [0, 0.0])
-        a[0] += 1
-        a[1] += ms
-    kernels = {n: {"launches": c, "avg_ms": t / c, "ms_per_step": t / args.steps} for n, (c, t) in agg.items()}
-    # the dominant kernel: fused screening with top-1 (one launch on Nt rows,
-    # one on Nb rows per step); algorithmic work = 2 * rows * C * D multiply
-    # and add operations (the -2 x.c contraction)
-    top1 = [ms for n, ms in timeline if n.endswith("/" + top1_name)]
-    ops_top1 = 2.0 * C * D * (Nt + Nb) * args.steps
-    achieved = ops_top1 / (sum(top1) * 1e-3) / 1e12
-    if args.fp32_screen:
-        roofline = {
-            "bound": "mfma",
-            "achieved": achieved,
-            "peak": PEAK_FP32_MFMA_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-            "traffic": measured_traffic(Nt, "screen_top1_fp32_traffic.json"),
-            "kernel": "screen_kernel<128, uint8, top1> (fp32 MFMA)",
-            "ops_per_launch": 2.0 * C * D * Nt,
-            "avg_launch_ms": sum(top1) / len(top1),
-        }
-        _, probe = ctx.mfma_probe()
-    elif args.two_plane:
-        # the two-plane int8 screen runs two int8 MFMA planes per centroid: it
-        # executes twice the algorithmic operations on the int8 pipe
-        roofline = {
-            "bound": "mfma",
-            "achieved": achieved,
-            "peak": PEAK_INT8_MFMA_TOPS,
-            "unit": "TOP/s",
-            "frac": achieved / PEAK_INT8_MFMA_TOPS,
-            "traffic": measured_traffic(Nt, "screen_top1_traffic.json"),
-            "kernel": "screen_i8_kernel<128, 8> (two-plane int8 MFMA)",
-            "ops_per_launch": 2.0 * C * D * Nt,
-            "executed_int8_ops_per_launch": 2 * 2.0 * C * D * Nt,
-            "executed_frac": 2 * achieved / PEAK_INT8_MFMA_TOPS,
-            "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-            "avg_launch_ms": sum(top1) / len(top1),
-        }
-        _, probe = ctx.mfma_probe_i8(200000)
-    else:
-        # the single-plane int8 screen executes exactly the algorithmic
-        # operations (one int8 plane per centroid)
-        roofline = {
-            "bound": "mfma",
-            "achieved": achieved,
-            "peak": PEAK_INT8_MFMA_TOPS,
-            "unit": "TOP/s",
-            "frac": achieved / PEAK_INT8_MFMA_TOPS,
-            "traffic": measured_traffic(Nt, "screen_top1_i8s_traffic.json"),
-            "kernel": "screen1_kernel<128, 8> (single-plane int8 MFMA)",
-            "ops_per_launch": 2.0 * C * D * Nt,
-            "fp32_mfma_equivalent_frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-            "avg_launch_ms": sum(top1) / len(top1),
-        }
-        _, probe = ctx.mfma_probe_i8(200000)
-    # the MFMA pipe as the library's probe kernel measures it on this GPU
-    # (register operands only; for int8, pseudo-random operands over about
-    # 0.1 s, which the part runs at its power-limited clock), after the timed
-    # region
-    roofline["measured_peak"] = probe
-    roofline["frac_of_measured_peak"] = achieved / probe
-    if args.two_plane:
-        roofline["executed_frac_of_measured_peak"] = 2 * achieved / probe
-
-    def call_ms(call):
-        return sum(ms for n, ms in timeline if n.startswith(call + "/")) / args.steps
-
-    per_call = {
-        "kmeans_step_vectors_per_s": Nt / (call_ms("kmeans_step") * 1e-3),
-        "assign_build_vectors_per_s": Nb / (call_ms("assign_build") * 1e-3),
-        "route_queries_per_s": Q / (call_ms("route") * 1e-3),
-        "route_tflops": 2.0 * Q * C * D / (call_ms("route") * 1e-3) / 1e12,
-    }
-    build_ms = [ms for n, ms in timeline if "/build_" in n]
-    # two builds per step: Nt rows (inside the k-means step) and Nb rows
-    per_call["build_lists_gbs"] = 12.0 * (Nt + Nb) * args.steps / (sum(build_ms) * 1e-3) / 1e9
-    per_call["build_lists_hbm_frac"] = per_call["build_lists_gbs"] / PEAK_HBM_GBS
-    # the whole step's algorithmic rate against the fp32 MFMA peak (the uint8
-    # rows run on int8 MFMA, so this exceeds 1)
-    per_call["step_fp32_mfma_equivalent_frac"] = (2.0 * C * D * vectors / (ms_per_step * 1e-3) / 1e12
-                                                  / PEAK_FP32_MFMA_TFLOPS)
+    if "1" in only:
+        configs["1_route_tiny"] = bench_route(ctx, "route tiny", synth.uniform_mixture_route(1024, 1000, 128, seed=0),
+                                              16, osec, full_oracle=True)
+    if "2" in only:
+        configs["2_route_uint8"] = bench_route(ctx, "route uint8-valued",
+                                               synth.uniform_mixture_route(C_BIG, 10000, 128, seed=0), 64, osec)
+    if "3" in only:
+        configs["3_route_normalised"] = bench_route(ctx, "route normalised",
+                                                    synth.normalised_route(262144, 10000, 96, seed=0), 128, osec)
+    if "4" in only:
+        km, x_train, c_km, lab_km = bench_kmeans(ctx, args.kmeans_rows, args.kmeans_iters,
+                                                 None if osec is None else 6.0)
+        configs["4_kmeans"] = km
+        if not args.no_extra:
+            extra = bench_next_rows(ctx, x_train, c_km, lab_km, configs["4_kmeans"])
+        del x_train, c_km, lab_km
+        torch.cuda.empty_cache()
 
     result = {
         "metric": "routed queries/s and assigned vectors/s at 1 GPU; % of fp32 MFMA peak",
-        "value": value,
-        "unit": "vectors/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if args.fp32_screen else "i8",
-        "data": "synthetic (seeded uint8 Gaussian mixture, 65,536 components, std 20, generated on the device)",
-        "config": {
-            "workload": "ivf_pipeline: kmeans_step(10M u8 rows) + assign_build(10M u8 rows) + route(10,000 queries, nprobe 64); C=65536, D=128",
-            "train_rows": Nt, "base_rows": Nb, "queries": Q, "centroids": C, "dim": D, "nprobe": K,
-            "screen": ("fp32 MFMA" if args.fp32_screen else "int8 MFMA (two planes per centroid)" if args.two_plane
-                       else "int8 MFMA (one plane per centroid; two planes for the rows it leaves)")
-            + " for the uint8 rows, fp32 MFMA for the fp32 queries; exact fp64 re-evaluation of near-ties",
-        },
-        "roofline": roofline,
-        "per_call": per_call,
-        "kernels": kernels,
-        "stats": stats,
+        "dtype": "i8",
+        "data": "synthetic: seeded uint8 Gaussian mixture (65,536 components uniform in [0,255]^128, std 20, "
+                "rounded and clipped), generated on the device; stands in for SIFT-1B",
     }
 
-    if args.copy_calibration_gib > 0:
-        n = int(args.copy_calibration_gib * 2**30)
-        src = torch.empty(n, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        src.fill_(1)
+    if "5" in only:
+        N, C, D = args.rows, C_BIG, D_U8
+        t0 = time.time()
+        means_h = synth.uniform_means(C, D, seed=0)
+        means = dev(means_h)
+        x = gen_rows(N, means)
+        log("generated %d rows in %.1f s" % (N, time.time() - t0))
+        lab = torch.empty(N, dtype=torch.int32, device="cuda")
+        cnt = torch.empty(C, dtype=torch.int64, device="cuda")
+        off = torch.empty(C + 1, dtype=torch.int64, device="cuda")
+        perm = torch.empty(N, dtype=torch.int32, device="cuda")
+
+        def step():
+            ivf.ivf_assign_build(ctx, x, means, out_labels=lab, out_counts=cnt, out_offsets=off, out_perm=perm)
+
+        for _ in range(args.warmup):
+            step()
         torch.cuda.synchronize()
-        dst.copy_(src)
+        stats = ctx.last_stats()
+        log("warmup done; stats:", stats)
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
+        ctx.kernel_times()
         torch.cuda.synchronize()
-        result["copy_calibration_bytes"] = n
+        t_start = time.perf_counter()
+        for i in range(args.steps):
+            step()
+            torch.cuda.synchronize()
+            log("step %d done" % i)
+        t_total = time.perf_counter() - t_start
+        timeline = ctx.kernel_times()
+        ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
+        ms_per_step = 1e3 * t_total / args.steps
 
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(x_train, c0, args.cpu_seconds)
+        agg = {}
+        for name, ms in timeline:
+            a = agg.setdefault(name.split("/", 1)[1], [0, 0.0])
+            a[0] += 1
+            a[1] += ms
+        kernels = {n: {"launches": c_, "avg_ms": t / c_, "ms_per_step": t / args.steps} for n, (c_, t) in agg.items()}
+        # dominant kernel: the single-plane int8 screen, one launch per slice
+        # of at most 2^28 rows; algorithmic work = 2 * rows * C * D multiply
+        # and add operations (the -2 x.c contraction), which it executes
+        # exactly (one int8 plane per centroid)
+        scr = [ms for n, ms in timeline if n.endswith("/screen_top1_i8s")]
+        ops_step = 2.0 * N * C * D
+        achieved = ops_step * args.steps / (sum(scr) * 1e-3) / 1e12
+        launches_per_step = len(scr) // args.steps
+        traffic, traffic_src = measured_traffic(min(N, 2**28), "screen_top1_i8s_traffic.json")
+        _, probe = ctx.mfma_probe_i8(200000)
+        roofline = {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_INT8_MFMA_TOPS,
+            "unit": "TOP/s",
+            "frac": achieved / PEAK_INT8_MFMA_TOPS,
+            "traffic": traffic,
+            "traffic_source": traffic_src or "not measured on the current kernel sources",
+            "kernel": "screen1_kernel<128, 8> (single-plane int8 MFMA, fused top-1)",
+            "ops_per_step": ops_step,
+            "launches_per_step": launches_per_step,
+            "rows_per_launch": min(N, 2**28),
+            "avg_launch_ms": sum(scr) / len(scr),
+            "measured_peak": probe,
+            "frac_of_measured_peak": achieved / probe,
+            "vs_fp32_mfma_peak_ratio": achieved / PEAK_FP32_MFMA_TFLOPS,
+        }
+        build = [ms for n, ms in timeline if "/build_" in n]
+        build_ms = sum(build) / args.steps
+        gbs = 12.0 * N / (build_ms * 1e-3) / 1e9
+        cfg5 = {
+            "rows": N, "centroids": C, "dim": D, "ms_per_call": ms_per_step,
+            "vectors_per_s": N / (ms_per_step * 1e-3),
+            "assign_ms": sum(ms for n, ms in timeline if "/build_" not in n) / args.steps,
+            "algorithmic_tops": ops_step / (ms_per_step * 1e-3) / 1e12,
+            "build_lists": {"ms": build_ms, "bytes_per_row": 12, "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+                            "kernels_ms": {n: k["ms_per_step"] for n, k in kernels.items() if n.startswith("build_")}},
+            "stats": stats,
+        }
+        result.update({
+            "value": N / (ms_per_step * 1e-3),
+            "unit": "vectors/s",
+            "ms_per_step": ms_per_step,
+            "config": {
+                "workload": "assign-build: 1e9 uint8 rows (D = 128, 128 GB resident, generated on the device in "
+                            "64M-row chunks) assigned to 65,536 fp32 centroids (the mixture means) by top-1 "
+                            "squared L2, then counts, offsets and the stable list permutation",
+                "rows": N, "centroids": C, "dim": D,
+                "screen": "int8 MFMA (one plane per centroid; two planes for the rows it leaves); exact fp64 "
+                          "re-evaluation of near-ties",
+            },
+            "roofline": roofline,
+            "kernels": kernels,
+        })
+        if args.copy_calibration_gib > 0:
+            n = int(args.copy_calibration_gib * 2**30)
+            src = torch.empty(n, dtype=torch.uint8, device="cuda")
+            dst = torch.empty_like(src)
+            src.fill_(1)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            result["copy_calibration_bytes"] = n
+            del src, dst
+        if osec is not None:
+            import oracle
 
-    if not args.no_extra:
-        lm, res = bench_list_major(ctx, x_base, c1, off_b, perm_b)
-        pq, codes, cb = bench_pq(ctx, res)
-        del res
-        result["extra"] = {"route_normalised": bench_route_normalised(ctx), "list_major": lm, "pq": pq,
-                           "adc_scan": bench_adc(ctx, queries, c1, ids, off_b, perm_b, codes, cb),
-                           "assign_graph": bench_assign_graph(ctx, x_train, c1, lab_t,
-                                                              kernels["kmeans_step/" + top1_name]["avg_ms"])}
-        del codes
-        if args.build_rows > 0:
-            # free the pipeline's buffers first: the 1e9-row build needs ~8 GB
-            del x_train, x_base, lab_t, lab_b, perm_b
-            torch.cuda.empty_cache()
-            result["extra"]["build_lists_at_scale"] = bench_build(ctx, args.build_rows, C)
+            oracle.build()
+            rng = np.random.default_rng(99)
+            idx = np.sort(rng.choice(N, 262144, replace=False))
+            xs = x[dev(idx)].cpu().numpy()
+            n, dt = oracle_rate(lambda m: oracle.assign(xs[:m], means_h), 16, len(idx), args.cpu_seconds)
+            result["cpu_baseline"] = {
+                "value": n / dt, "unit": "vectors/s", "cores": oracle.num_threads(0), "kind": "oracle",
+                "cpu": cpu_model(),
+                "sample": "nearest-centroid search of %d rows sampled from the 1e9 (copied back from the "
+                          "device) against the 65,536 centroids, %.1f s" % (n, dt),
+            }
+            # the list build on a 1e8-label prefix of the GPU labels
+            nb = min(N, 10**8)
+            labh = lab[:nb].cpu().numpy()
+            t = time.perf_counter()
+            oracle.build_lists(labh, C)
+            dt = time.perf_counter() - t
+            cfg5["oracle"] = {"assign_vectors_per_s": result["cpu_baseline"]["value"],
+                              "build_vectors_per_s": nb / dt,
+                              "sample": "assignment as cpu_baseline; counting-sort list build of the first "
+                                        "%d GPU labels (one thread), %.1f s" % (nb, dt)}
+        configs["5_assign_build"] = cfg5
+        del x, lab, perm
+        torch.cuda.empty_cache()
 
+    result["configs"] = configs
+    if extra:
+        result["extra"] = extra
     print(json.dumps(result), flush=True)
 
 
-def measured_traffic(rows_per_launch, record):
-    """HBM bytes per launch of the dominant kernel from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (calibrated against a device
-    copy), if it was taken on the current kernel sources (the record's
-    `sources`, hashed in order) and launch size; otherwise None."""
-    import hashlib
+# ---------------------------------------------------------------- NEXT rows
 
-    path = os.path.join(ROOT, "profiles", record)
-    try:
-        with open(path) as f:
-            rec = json.load(f)
-        h = hashlib.sha256()
-        for src in rec["sources"]:
-            with open(os.path.join(ROOT, src), "rb") as f:
-                h.update(f.read())
-        sha = h.hexdigest()
-    except (OSError, ValueError, KeyError, TypeError):
-        return None
-    if not sha.startswith(rec["sources_sha256_prefix"]) or rec["rows_per_launch"] != rows_per_launch:
-        return None
-    return rec["traffic_bytes"]
-
-
-def bench_route_normalised(ctx):
-    """Routing of 10,000 normalised queries against 262,144 unit-norm centroids
-    (D = 96), nprobe 128: median of 5 calls, whole-call event time."""
+def bench_next_rows(ctx, x, cent, prev, km):
+    """The NEXT-row kernels on the k-means workload's 10M rows and trained
+    centroids: assign-build, list-major layout with residuals, residual PQ
+    (one training step, encoding), the ADC scan of 10,000 routed queries,
+    and the candidate-restricted assignment."""
     import numpy as np
     import torch
 
     import synth
     import paper_2608_08751_amd as ivf
 
-    d = synth.normalised_route(262144, 10000, 96, seed=0)
-    q = torch.from_numpy(d["queries"]).cuda()
-    c = torch.from_numpy(d["centroids"]).cuda()
-    ids = torch.empty((10000, 128), dtype=torch.int32, device="cuda")
-    dist = torch.empty((10000, 128), dtype=torch.float32, device="cuda")
-    ivf.ivf_route(ctx, q, c, 128, out_ids=ids, out_dist=dist)
+    N, D = x.shape
+    C = cent.shape[0]
+    lab, cnt, off, perm = ivf.ivf_assign_build(ctx, x, cent)
     torch.cuda.synchronize()
-    st = ctx.last_stats()
+    out = {}
+    lm, res = bench_list_major(ctx, x, cent, off, perm)
+    out["list_major"] = lm
+    pq, codes, cb = bench_pq(ctx, res)
+    out["pq"] = pq
+    del res
+    q = dev(synth.uniform_mixture_route(C, 10000, D, seed=0)["queries"])
+    probes, _ = ivf.ivf_route(ctx, q, cent, 64, want_dist=False)
+    out["adc_scan"] = bench_adc(ctx, q, cent, probes, off, perm, codes, cb)
+    full_ms = km["per_iteration"][-1]["screen_single_plane_ms"] + km["per_iteration"][-1]["screen_two_planes_ms"]
+    out["assign_graph"] = bench_assign_graph(ctx, x, cent, prev, full_ms)
+    return out
+
+
+def _timed(ctx, fn, reps=3):
+    import numpy as np
+
+    import paper_2608_08751_amd as ivf
+
     ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
     ctx.kernel_times()
-    times = []
-    for _ in range(5):
-        ivf.ivf_route(ctx, q, c, 128, out_ids=ids, out_dist=dist)
-        tl = ctx.kernel_times()
-        times.append(sum(ms for _, ms in tl))
-        filt = sum(ms for n, ms in tl if n.endswith(("/screen_filter", "/screen_keys")))
+    ts = []
+    for _ in range(reps):
+        fn()
+        ts.append(sum(ms for _, ms in ctx.kernel_times()))
     ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-    t = float(np.median(times))
-    flops = 2.0 * 10000 * 262144 * 96
-    return {
-        "queries_per_s": 10000 / (t * 1e-3),
-        "ms_per_call": t,
-        "tflops": flops / (t * 1e-3) / 1e12,
-        "mfma_frac": flops / (t * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS,
-        "screen_ms": filt,
-        "stats": st,
-    }
+    return float(np.median(ts))
 
 
 def bench_list_major(ctx, x, cent, offsets, perm):
-    """ivf_list_major on the step's assign-build output (10M uint8 base rows,
-    65,536 lists): list-major copy plus fp32 residuals, median of 3 calls.
-    Algorithmic bytes per row: read the row and its id, write the row and
-    its residual (D + 4 + D + 4 D)."""
-    import numpy as np
+    """ivf_list_major (uint8 rows, 65,536 lists): list-major copy plus fp32
+    residuals, median of 3 calls. Algorithmic bytes per row: read the row and
+    its id, write the row and its residual (D + 4 + D + 4 D)."""
     import torch
 
     import paper_2608_08751_amd as ivf
@@ -386,16 +525,10 @@ def bench_list_major(ctx, x, cent, offsets, perm):
     N, D = x.shape
     rows = torch.empty_like(x)
     res = torch.empty((N, D), dtype=torch.float32, device=x.device)
-    ivf.ivf_list_major(ctx, x, cent, offsets, perm, out_rows=rows, out_residuals=res)
+    fn = lambda: ivf.ivf_list_major(ctx, x, cent, offsets, perm, out_rows=rows, out_residuals=res)
+    fn()
     torch.cuda.synchronize()
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-    ctx.kernel_times()
-    times = []
-    for _ in range(3):
-        ivf.ivf_list_major(ctx, x, cent, offsets, perm, out_rows=rows, out_residuals=res)
-        times.append(sum(ms for _, ms in ctx.kernel_times()))
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-    t = float(np.median(times))
+    t = _timed(ctx, fn)
     per_row = D + 4 + D + 4 * D
     gbs = per_row * N / (t * 1e-3) / 1e9
     del rows
@@ -404,12 +537,11 @@ def bench_list_major(ctx, x, cent, offsets, perm):
 
 
 def bench_pq(ctx, res, M=16, train_rows=1 << 20):
-    """Residual PQ on the list-major residuals (10M x 128, M = 16 subspaces of
-    8 dims, 256 codewords): one codebook training step on the first 1M
-    residuals and the encoding of all of them, median of 3 calls each. The
-    encoding's algorithmic work is 3 flops (subtract, multiply, add) per
-    codeword and dim, in fp64: 3 * 256 * D per row, against the 78.6 TFLOP/s
-    fp64 vector peak."""
+    """Residual PQ on the list-major residuals (M = 16 subspaces of 8 dims,
+    256 codewords): one codebook training step on the first 1M residuals and
+    the encoding of all of them, median of 3 calls each. The encoding's
+    algorithmic work is 3 flops (subtract, multiply, add) per codeword and
+    dim, in fp64: 3 * 256 * D per row, against the fp64 vector peak."""
     import numpy as np
     import torch
 
@@ -423,20 +555,9 @@ def bench_pq(ctx, res, M=16, train_rows=1 << 20):
     cb, cnt, obj = ivf.ivf_pq_train_step(ctx, train, cb0, seed=0, it=0)
     codes = ivf.ivf_pq_encode(ctx, res, cb)
     torch.cuda.synchronize()
-
-    def timed(fn):
-        ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-        ctx.kernel_times()
-        ts = []
-        for _ in range(3):
-            fn()
-            ts.append(sum(ms for _, ms in ctx.kernel_times()))
-        ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-        return float(np.median(ts))
-
-    t_train = timed(lambda: ivf.ivf_pq_train_step(ctx, train, cb0, seed=0, it=0, out_codebooks=cb,
-                                                  out_counts=cnt, out_objective=obj))
-    t_enc = timed(lambda: ivf.ivf_pq_encode(ctx, res, cb, out_codes=codes))
+    t_train = _timed(ctx, lambda: ivf.ivf_pq_train_step(ctx, train, cb0, seed=0, it=0, out_codebooks=cb,
+                                                        out_counts=cnt, out_objective=obj))
+    t_enc = _timed(ctx, lambda: ivf.ivf_pq_encode(ctx, res, cb, out_codes=codes))
     flops = 3.0 * 256 * D * N
     tf = flops / (t_enc * 1e-3) / 1e12
     return ({"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
@@ -445,11 +566,9 @@ def bench_pq(ctx, res, M=16, train_rows=1 << 20):
 
 
 def bench_adc(ctx, queries, cent, probes, offsets, perm, codes, cb, k=512):
-    """Residual-PQ ADC scan of the step's 10,000 routed queries (nprobe 64)
-    over the PQ codes of the 10M list-major base rows, handoff k = 512 per
-    query (the paper's N_rerank): median of 3 calls. Work per query: one
-    M x 256 LUT per probed list and M lookups per code of the probed lists."""
-    import numpy as np
+    """Residual-PQ ADC scan of 10,000 routed queries (nprobe 64) over the PQ
+    codes of the list-major rows, handoff k = 512 per query (the paper's
+    N_rerank): median of 3 calls."""
     import torch
 
     import paper_2608_08751_amd as ivf
@@ -457,29 +576,22 @@ def bench_adc(ctx, queries, cent, probes, offsets, perm, codes, cb, k=512):
     Q, P = probes.shape
     out_ids = torch.empty((Q, k), dtype=torch.int32, device=queries.device)
     out_d = torch.empty((Q, k), dtype=torch.float32, device=queries.device)
-    ivf.ivf_adc_scan(ctx, queries, cent, probes, offsets, perm, codes, cb, k, out_ids=out_ids, out_dist=out_d)
+    fn = lambda: ivf.ivf_adc_scan(ctx, queries, cent, probes, offsets, perm, codes, cb, k, out_ids=out_ids,
+                                  out_dist=out_d)
+    fn()
     torch.cuda.synchronize()
     lens = (offsets[1:] - offsets[:-1])[probes.long()].sum().item()
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-    ctx.kernel_times()
-    ts = []
-    for _ in range(3):
-        ivf.ivf_adc_scan(ctx, queries, cent, probes, offsets, perm, codes, cb, k, out_ids=out_ids, out_dist=out_d)
-        ts.append(sum(ms for _, ms in ctx.kernel_times()))
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-    t = float(np.median(ts))
+    t = _timed(ctx, fn)
     return {"queries": Q, "nprobe": P, "k": k, "subspaces": codes.shape[1], "codes_scanned": int(lens),
             "ms": t, "queries_per_s": Q / (t * 1e-3), "codes_per_s": lens / (t * 1e-3)}
 
 
-def bench_assign_graph(ctx, x, cent, prev, full_top1_ms, S=8):
-    """Candidate-restricted assignment (fast construction mode) of the step's
-    10M training rows to the new centroids: the 8-nearest-centroid graph from
-    ivf_route of the centroids against themselves, then each row scored
-    against the 8 neighbours of its previous centroid. Median of 3 calls.
-    HBM bytes per row: the row, its previous label, its label and distance
-    (centroid rows come from the cache)."""
-    import numpy as np
+def bench_assign_graph(ctx, x, cent, prev, full_ms, S=8):
+    """Candidate-restricted assignment (fast construction mode): the
+    8-nearest-centroid graph from ivf_route of the centroids against
+    themselves, then each row scored against the 8 neighbours of its previous
+    centroid. Median of 3 calls. HBM bytes per row: the row, its previous
+    label, its label and distance (centroid rows come from the cache)."""
     import torch
 
     import paper_2608_08751_amd as ivf
@@ -491,94 +603,13 @@ def bench_assign_graph(ctx, x, cent, prev, full_top1_ms, S=8):
     dist = torch.empty(N, dtype=torch.float32, device=x.device)
     ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist)
     torch.cuda.synchronize()
-
-    def timed(fn):
-        ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-        ctx.kernel_times()
-        ts = []
-        for _ in range(3):
-            fn()
-            ts.append(sum(ms for _, ms in ctx.kernel_times()))
-        ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-        return float(np.median(ts))
-
-    t_graph = timed(lambda: ivf.ivf_route(ctx, cent, cent, S, out_ids=graph, want_dist=False))
-    t = timed(lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist))
+    t_graph = _timed(ctx, lambda: ivf.ivf_route(ctx, cent, cent, S, out_ids=graph, want_dist=False))
+    t = _timed(ctx, lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist))
     per_row = D + 12
     gbs = per_row * N / (t * 1e-3) / 1e9
     return {"rows": N, "centroids": C, "degree": S, "graph_ms": t_graph, "assign_ms": t,
             "rows_per_s": N / (t * 1e-3), "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
-            "speedup_vs_full_assignment": full_top1_ms / t}
-
-
-def bench_build(ctx, N, C):
-    """ivf_build_lists on N uniform device-generated labels over C lists:
-    median of 3 calls; algorithmic bytes = 12 per row (histogram reads a 4-byte
-    label; the scatter reads it again and writes a 4-byte id)."""
-    import numpy as np
-    import torch
-
-    import synth
-    import paper_2608_08751_amd as ivf
-
-    lab = torch.empty(N, dtype=torch.int32, device="cuda")
-    synth.device_labels(N, C, lab, seed=0)
-    cnt = torch.empty(C, dtype=torch.int64, device="cuda")
-    off = torch.empty(C + 1, dtype=torch.int64, device="cuda")
-    perm = torch.empty(N, dtype=torch.int32, device="cuda")
-    ivf.ivf_build_lists(ctx, lab, C, cnt, off, perm)
-    torch.cuda.synchronize()
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 1)
-    ctx.kernel_times()
-    runs = []
-    for _ in range(3):
-        ivf.ivf_build_lists(ctx, lab, C, cnt, off, perm)
-        runs.append(ctx.kernel_times())
-    ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
-    totals = [sum(ms for _, ms in r) for r in runs]
-    i = int(np.argsort(totals)[len(totals) // 2])
-    t = totals[i]
-    gbs = 12.0 * N / (t * 1e-3) / 1e9
-    return {
-        "rows": N, "lists": C, "ms": t, "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
-        "kernels_ms": {n.split("/", 1)[1]: ms for n, ms in runs[i]},
-    }
-
-
-def cpu_baseline(x_train, c0, target_s):
-    """The oracle (plain C, fp64, all host threads) on a bounded sample of the
-    same work: nearest-centroid search of sampled training rows against the
-    65,536 centroids. Each routed query / assigned row costs the same C*D
-    distance work, so its rate is the oracle's vectors/s for the step."""
-    import numpy as np
-
-    import oracle
-
-    oracle.build()
-    cent = c0.cpu().numpy()
-    threads = oracle.num_threads(0)
-    rng = np.random.default_rng(99)
-    probe = max(8, threads)
-    rows = x_train[:probe].cpu().numpy()
-    t = time.perf_counter()
-    oracle.assign(rows, cent)
-    dt = time.perf_counter() - t
-    n = int(min(max(probe, probe * target_s / max(dt, 1e-6)), 200000))
-    idx = np.sort(rng.choice(x_train.shape[0], n, replace=False))
-    import torch
-
-    rows = x_train[torch.from_numpy(idx).cuda()].cpu().numpy()
-    t = time.perf_counter()
-    oracle.assign(rows, cent)
-    dt = time.perf_counter() - t
-    return {
-        "value": n / dt,
-        "unit": "vectors/s",
-        "cores": threads,
-        "kind": "oracle",
-        "cpu": cpu_model(),
-        "sample": "nearest-centroid search of %d sampled training rows against the 65,536 centroids (%.1f s)" % (n, dt),
-    }
+            "speedup_vs_full_assignment": full_ms / t}
 
 
 if __name__ == "__main__":

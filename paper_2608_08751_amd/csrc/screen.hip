@@ -222,14 +222,15 @@ __device__ __forceinline__ void top3_push(Top3 &t, float v, int id)
     t.i1 = gt1 ? id : t.i1;
 }
 
-// max(a, b, c, d) in two instructions (fmaxf would first canonicalise each
-// operand for NaN handling; the values here are never NaN).
+// max(a, b, c, d) in two v_maximum3_f32. fmaxf would first canonicalise each
+// operand (an extra instruction per value); maximum differs from it only for
+// NaN and for -0 against +0, and the values here are never NaN while the
+// compares that follow treat -0 and +0 alike. Being ordinary compiler
+// operations, the reads of MFMA results get their wait states from the
+// compiler's hazard recognizer.
 __device__ __forceinline__ float max4(float a, float b, float c, float d)
 {
-    float m;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(m) : "v"(a), "v"(b), "v"(c));
-    asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(m), "v"(d));
-    return m;
+    return __builtin_elementwise_maximum(__builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c), d);
 }
 
 // Group G (0..7) of the previous chunk's accumulators: block rb = G / 4 (p0
@@ -318,19 +319,6 @@ __device__ __forceinline__ void mfma_chunk(const float *A0, const float *Nh, con
     const float4 a0 = *reinterpret_cast<const float4 *>(A0);
     const float4 a1 = *reinterpret_cast<const float4 *>(A1);
     top1_kblocks<DP, EP>(A0, A1, b, c0, c1, a0, a1, p0, p1, idp, st);
-}
-
-// The group tests read accumulators through inline asm, which gets no wait
-// states after the MFMAs that write them; in the loop they read the previous
-// chunk's accumulators, many MFMAs later, but the last chunk's are drained
-// right after its MFMAs, so they are first copied by an add the compiler sees
-// (x + 0 is not folded: it turns -0 into +0, which the compares treat alike).
-__device__ __forceinline__ f32x16 settled(const f32x16 &p)
-{
-    f32x16 q;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) q[r] = p[r] + 0.0f;
-    return q;
 }
 
 template <int G = 0>
@@ -436,9 +424,9 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     }
     if (j < nch) {
         step(j, y0, y1, x0, x1);
-        top1_drain(settled(y0), settled(y1), idh + j * kChunk, st);
+        top1_drain(y0, y1, idh + j * kChunk, st);
     } else {
-        top1_drain(settled(x0), settled(x1), idh + (j - 1) * kChunk, st);
+        top1_drain(x0, x1, idh + (j - 1) * kChunk, st);
     }
     // back to keys: key = -2 v exactly, ascending
     st.k1 *= -2.0f;

@@ -10,7 +10,6 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (runs through the HIP C-ABI library)")
-    config.addinivalue_line("markers", "slow: full-size workload, opt-in with IVF_FULL_SCALE=1")
 
 
 @pytest.fixture(scope="session")

@@ -1,0 +1,187 @@
+"""GPU parity at the full sizes of the two construction workloads (k-means
+training and the assignment of every base vector, Sec. "Fast Index
+Construction"), against the oracle on the same bytes:
+
+* k-means: 10M uint8 rows (65,536-component mixture, std 20), 65,536
+  centroids initialised from a seeded row sample, three Lloyd iterations. At
+  every iteration the labels of 65,536 sampled rows equal the oracle's
+  nearest centroid for that iteration's input centroids; the new centroids
+  and counts equal the oracle's update recomputed from the full GPU labels,
+  bit for bit; the objective equals the oracle's (fp64, to summation order)
+  and does not increase. Iteration 0 (integer centroids) is settled by the
+  single int8 plane; iterations 1 and 2 (mean centroids) also go through the
+  fp64 evaluation of two candidates, the two-plane screen and the exact
+  fallback scan, and the test checks that they did.
+* assign-build: 1e9 uint8 rows of the same generator (128 GB resident,
+  produced on the device in 64M-row chunks), 65,536 centroids (the mixture
+  means). The labels of 262,144 sampled rows (copied back from device
+  memory) equal the oracle's; counts, offsets and the permutation equal the
+  oracle's counting sort over all 1e9 GPU labels.
+
+The oracle runs on every host thread; each label sample is its own test so
+that progress shows while the long ones run."""
+import time
+
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+C, D = 65536, 128
+KM_ROWS = 10_000_000
+KM_ITERS = 3
+KM_SAMPLE = 65536
+AB_ROWS = 10**9
+AB_CHUNK = 64 * 2**20
+AB_SAMPLE = 262144
+AB_PARTS = 4
+
+
+@pytest.fixture(scope="module")
+def ivf_ctx():
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ctx = ivf.Context(0)
+    yield ctx
+    ctx.close()
+
+
+def to_dev(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.fixture(scope="module")
+def kmeans_chain(ivf_ctx):
+    """Three GPU Lloyd iterations; keeps host copies of the rows and of every
+    iteration's input centroids, labels, outputs and statistics."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(C, D, seed=0)
+    x = torch.empty((KM_ROWS, D), dtype=torch.uint8, device="cuda")
+    synth.device_mixture_rows_u8(to_dev(means), 0, KM_ROWS, x, seed=0)
+    c = x[to_dev(synth.kmeans_init(KM_ROWS, C, seed=0))].float().contiguous()
+    its = []
+    for it in range(KM_ITERS):
+        t = time.time()
+        lab, cen, cnt, obj = ivf.ivf_kmeans_step(ivf_ctx, x, c, seed=0, it=it)
+        torch.cuda.synchronize()
+        st = ivf_ctx.last_stats()
+        print("k-means iteration %d: %.2f s, stats %s" % (it, time.time() - t, st), flush=True)
+        its.append({"c_in": c.cpu().numpy(), "labels": lab.cpu().numpy(), "cen": cen.cpu().numpy(),
+                    "cnt": cnt.cpu().numpy(), "obj": float(obj[0].cpu()), "stats": st})
+        c = cen
+    xh = x.cpu().numpy()
+    del x, c, lab, cen, cnt, obj
+    torch.cuda.empty_cache()
+    return xh, its
+
+
+@pytest.mark.parametrize("it", range(KM_ITERS))
+def test_kmeans_10m_labels_sampled(kmeans_chain, oracle_mod, it):
+    xh, its = kmeans_chain
+    rows = np.sort(np.random.default_rng(100 + it).choice(KM_ROWS, KM_SAMPLE, replace=False))
+    t = time.time()
+    want = oracle_mod.assign(xh[rows], its[it]["c_in"])
+    print("iteration %d: oracle labels of %d rows in %.1f s" % (it, KM_SAMPLE, time.time() - t), flush=True)
+    got = its[it]["labels"][rows]
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, "iteration %d: labels differ at rows %s" % (it, rows[bad[:10]])
+
+
+@pytest.mark.parametrize("it", range(KM_ITERS))
+def test_kmeans_10m_update_from_full_labels(kmeans_chain, oracle_mod, it):
+    """The oracle's update over every GPU label: all 65,536 centroids and
+    counts bit-equal; the objective of those labels agrees and does not
+    increase from one iteration to the next."""
+    xh, its = kmeans_chain
+    r = its[it]
+    ocen, ocnt = oracle_mod.kmeans_update(xh, r["labels"], C, seed=0, it=it)
+    assert (r["cnt"] == ocnt).all()
+    bad = np.unique(np.nonzero(r["cen"] != ocen)[0])
+    assert bad.size == 0, "iteration %d: centroids differ in clusters %s" % (it, bad[:10])
+    oobj = oracle_mod.objective(xh, r["labels"], r["c_in"])
+    assert abs(r["obj"] - oobj) <= 1e-12 * oobj
+    if it > 0:
+        assert r["obj"] <= its[it - 1]["obj"] * (1 + 1e-9)
+
+
+def test_kmeans_10m_paths_exercised(kmeans_chain):
+    """Iteration 0 scores integer centroids (the single plane settles nearly
+    every row); against the mean centroids of iterations 1 and 2 rows also
+    take the fp64 evaluation of two candidates, the two-plane screen and the
+    exact fallback scan, so those paths are covered at full size above."""
+    _, its = kmeans_chain
+    s = [r["stats"] for r in its]
+    assert all(x["screen_i8"] == 1 for x in s)
+    assert s[0]["rescreen"] < KM_ROWS // 1000
+    for x in s[1:]:
+        assert x["refine2"] > 0 and x["rescreen"] > 0
+    assert s[1]["fallback"] + s[2]["fallback"] > 0
+    assert all(x["fallback"] < KM_ROWS // 1000 for x in s)
+
+
+@pytest.fixture(scope="module")
+def assign_build_1e9(ivf_ctx):
+    """One ivf_assign_build over 1e9 device-generated rows; keeps host copies
+    of the outputs and of the sampled rows, then frees the device memory."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(C, D, seed=0)
+    md = to_dev(means)
+    x = torch.empty((AB_ROWS, D), dtype=torch.uint8, device="cuda")
+    t = time.time()
+    for r0 in range(0, AB_ROWS, AB_CHUNK):
+        synth.device_mixture_rows_u8(md, r0, min(AB_CHUNK, AB_ROWS - r0), x[r0:r0 + AB_CHUNK], seed=0)
+    torch.cuda.synchronize()
+    print("generated %d rows in %.1f s" % (AB_ROWS, time.time() - t), flush=True)
+    t = time.time()
+    lab, cnt, off, perm = ivf.ivf_assign_build(ivf_ctx, x, md)
+    torch.cuda.synchronize()
+    st = ivf_ctx.last_stats()
+    print("assign_build of %d rows: %.2f s, stats %s" % (AB_ROWS, time.time() - t, st), flush=True)
+    rows = np.sort(np.random.default_rng(5).choice(AB_ROWS, AB_SAMPLE, replace=False))
+    out = {"means": means, "rows": rows, "xs": x[to_dev(rows)].cpu().numpy(), "labels": lab.cpu().numpy(),
+           "counts": cnt.cpu().numpy(), "offsets": off.cpu().numpy(),
+           "perm": perm.cpu().numpy().view(np.uint32), "stats": st}
+    del x, lab, cnt, off, perm
+    torch.cuda.empty_cache()
+    return out
+
+
+@pytest.mark.parametrize("part", range(AB_PARTS))
+def test_assign_build_1e9_labels_sampled(assign_build_1e9, oracle_mod, part):
+    r = assign_build_1e9
+    n = AB_SAMPLE // AB_PARTS
+    sl = slice(part * n, (part + 1) * n)
+    t = time.time()
+    want = oracle_mod.assign(r["xs"][sl], r["means"])
+    print("part %d: oracle labels of %d rows in %.1f s" % (part, n, time.time() - t), flush=True)
+    got = r["labels"][r["rows"][sl]]
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, "labels differ at rows %s" % r["rows"][sl][bad[:10]]
+
+
+def test_assign_build_1e9_lists_exact(assign_build_1e9, oracle_mod):
+    """Counts, offsets and permutation equal the oracle's counting sort over
+    all 1e9 labels the GPU produced."""
+    r = assign_build_1e9
+    t = time.time()
+    ocnt, ooff, operm = oracle_mod.build_lists(r["labels"], C)
+    print("oracle list build over %d labels in %.1f s" % (AB_ROWS, time.time() - t), flush=True)
+    assert (r["counts"] == ocnt).all()
+    assert (r["offsets"] == ooff).all() and r["offsets"][-1] == AB_ROWS
+    assert np.array_equal(r["perm"], operm)
+    st = r["stats"]
+    assert st["screen_i8"] == 1 and st["fallback"] < AB_ROWS // 10**6
