@@ -137,6 +137,22 @@ ivf_status ivf_sync(ivf_ctx *ctx);
 ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
                      int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist);
 
+/* ivf_route for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * same arguments, results and errors as ivf_route, but no workspace is used
+ * and nothing is allocated (no hipMalloc, hipFree, event or library
+ * allocation; IVF_OPT_PROFILE records nothing for it). The scratch memory is
+ * a static device array of 64 MiB held on every device the library runs on
+ * until the process ends; queries are processed in batches that fit it
+ * (smaller batches than ivf_route's, so throughput can be lower). Sizes that
+ * need more than 64 MiB for a single query (C above about 16M, or nprobe and
+ * C giving a larger candidate layout) are refused with IVF_EUNSUPPORTED.
+ * Every call on a device shares that device's array and leaves its contents
+ * behind (the call clears what it needs itself): two calls that overlap on
+ * one device, from any contexts or streams, race and give undefined results. */
+ivf_status ivf_route_noalloc(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
+                             int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist);
+
 /* One Lloyd iteration of k-means (k-means training, Sec. "Fast Index
  * Construction"): assignment against `centroids`, then the mean update.
  *   train          [N, D] fp32 or uint8 (dt), N >= 1

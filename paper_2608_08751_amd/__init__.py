@@ -47,6 +47,7 @@ from ._binding import (  # noqa: F401
     ivf_pq_encode,
     ivf_pq_train_step,
     ivf_route,
+    ivf_route_noalloc,
     load_library,
 )
 

@@ -34,6 +34,7 @@ SIGNATURES = [
     ("ivf_set_workspace", _INT, [_P, _P, _SZ]),
     ("ivf_sync", _INT, [_P]),
     ("ivf_route", _INT, [_P, _P, _I64, _P, _I64, _I32, _I32, _P, _P]),
+    ("ivf_route_noalloc", _INT, [_P, _P, _I64, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_kmeans_step", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _U64, _I32, _P, _P, _P, _P]),
     ("ivf_assign_build", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _P, _P]),
     ("ivf_build_lists", _INT, [_P, _P, _I64, _I64, _P, _P, _P]),
@@ -213,6 +214,20 @@ def ivf_route(ctx: Context, queries, centroids, nprobe: int, out_ids=None, out_d
     ctx.bind_stream()
     ctx.check(ctx.lib.ivf_route(ctx.handle, _ptr(queries), Q, _ptr(centroids), C, D, nprobe,
                                 _ptr(out_ids), _ptr(out_dist)), "ivf_route")
+    return out_ids, out_dist
+
+
+def ivf_route_noalloc(ctx: Context, queries, centroids, nprobe: int, out_ids, out_dist=None):
+    """ivf_route without a workspace: the library's static device scratch is
+    used and nothing is allocated by the call (out_ids / out_dist are the
+    caller's). Calls that overlap on one device race."""
+    _device_tensor(queries, "queries")
+    _device_tensor(centroids, "centroids")
+    Q, D = queries.shape
+    C = centroids.shape[0]
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_route_noalloc(ctx.handle, _ptr(queries), Q, _ptr(centroids), C, D, nprobe,
+                                        _ptr(out_ids), _ptr(out_dist)), "ivf_route_noalloc")
     return out_ids, out_dist
 
 

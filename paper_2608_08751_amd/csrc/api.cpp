@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -57,6 +58,36 @@ constexpr int kMaxNprobe = 1024;
 constexpr int kMaxD = 256;
 // Rows per assignment slice (row ids inside a slice fit int32).
 constexpr int64_t kAssignSlice = (int64_t)1 << 28;
+
+// Scratch memory of ivf_route_noalloc, for callers that cannot allocate
+// device memory: one copy per device, held while the library is loaded. In
+// host code `scratch` names a host-side stand-in; kernels get the device
+// address that hipGetSymbolAddress returns for each device.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Looks up (once per device, with that device current) the device address of
+// `scratch`; nullptr on failure.
+void *static_scratch(int device)
+{
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        int prev = -1;
+        if (hipGetDevice(&prev) != hipSuccess) return nullptr;
+        if (prev != device && hipSetDevice(device) != hipSuccess) return nullptr;
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (prev != device) (void)hipSetDevice(prev);
+        if (e != hipSuccess) return nullptr;
+        g_scratch_ptr[device] = ptr;
+    }
+    return g_scratch_ptr[device];
+}
 
 ivf_status fail(ivf_ctx *ctx, ivf_status st, const char *fmt, ...)
 {
@@ -531,6 +562,8 @@ ivf_status ivf_create(int device, void *hip_stream, ivf_ctx **out)
     if (device < 0 || device >= n) return IVF_EINVAL;
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, device) != hipSuccess) return IVF_EDEVICE;
+    // the static scratch of ivf_route_noalloc: its address on this device
+    if (!static_scratch(device)) return IVF_EDEVICE;
     ivf_ctx *c = new ivf_ctx();
     c->device = device;
     c->stream = (hipStream_t)hip_stream;
@@ -722,19 +755,26 @@ ivf_status ivf_mfma_probe_i8(ivf_ctx *ctx, int32_t iters, float *out_ms, double 
     return run_probe(ctx, iters, launch_mfma_probe_i8, "int8 MFMA probe", out_ms, out_tops);
 }
 
-ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
-                     int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist)
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by ivf_route and ivf_route_noalloc (nothing is
+// enqueued). *done is set when Q == 0 (a no-op).
+ivf_status check_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids, int64_t C,
+                       int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist, bool *done)
 {
-    if (!ctx) return IVF_EINVAL;
-    ctx->err.clear();
-    ctx->cur_call = "route";
+    *done = false;
     if (Q < 0) return fail(ctx, IVF_EINVAL, "Q must be >= 0");
     ivf_status st = check_common(ctx, C, D);
     if (st != IVF_OK) return st;
     if (nprobe < 1 || nprobe > C)
         return fail(ctx, IVF_EINVAL, "nprobe must be in [1, C] (got %d, C = %lld)", nprobe, (long long)C);
     if (nprobe > kMaxNprobe) return fail(ctx, IVF_EUNSUPPORTED, "nprobe > %d", kMaxNprobe);
-    if (Q == 0) return IVF_OK;
+    if (Q == 0) {
+        *done = true;
+        return IVF_OK;
+    }
     if (!queries || !centroids || !out_ids) return fail(ctx, IVF_EINVAL, "null pointer argument");
     if (!aligned16(queries) || !aligned16(centroids) || !aligned16(out_ids) ||
         (out_dist && !aligned16(out_dist)))
@@ -744,13 +784,16 @@ ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float 
         overlap(out_dist, ob, queries, qb) || overlap(out_dist, ob, centroids, cb) ||
         overlap(out_ids, ob, out_dist, ob))
         return fail(ctx, IVF_EINVAL, "outputs overlap inputs or each other");
-    const RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
-    const size_t need = layout_route(nullptr, p, C).bytes;
-    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
-    DeviceGuard g(ctx->device);
-    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    return IVF_OK;
+}
 
-    const RouteLayout l = layout_route(ctx->ws, p, C);
+// Enqueues the routing kernels, queries in batches of p.QB, with the scratch
+// memory laid out by layout_route at `ws`.
+ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids, int64_t C,
+                         int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist, const RoutePlan &p,
+                         void *ws)
+{
+    const RouteLayout l = layout_route(ws, p, C);
     hipStream_t s = ctx->stream;
     const int DP = padded_dim(D);
     TIMED("fill", launch_fill_u32(l.sc.mc2_bits, 64, 0u, s));
@@ -814,6 +857,65 @@ ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float 
     ctx->last_stats = l.sc.stats;
     ctx->last_sample = p.Cs;
     return IVF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
+                     int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "route";
+    bool done = false;
+    ivf_status st = check_route(ctx, queries, Q, centroids, C, D, nprobe, out_ids, out_dist, &done);
+    if (st != IVF_OK || done) return st;
+    const RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
+    const size_t need = layout_route(nullptr, p, C).bytes;
+    if ((st = check_ws(ctx, need)) != IVF_OK) return st;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    return enqueue_route(ctx, queries, Q, centroids, C, D, nprobe, out_ids, out_dist, p, ctx->ws);
+}
+
+ivf_status ivf_route_noalloc(ivf_ctx *ctx, const float *queries, int64_t Q, const float *centroids,
+                             int64_t C, int32_t D, int32_t nprobe, int32_t *out_ids, float *out_dist)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "route_noalloc";
+    bool done = false;
+    ivf_status st = check_route(ctx, queries, Q, centroids, C, D, nprobe, out_ids, out_dist, &done);
+    if (st != IVF_OK || done) return st;
+    // the batch of queries shrinks until the layout fits the static scratch;
+    // sizes that do not fit with a single query are refused
+    RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
+    const size_t one = [&] {
+        RoutePlan q1 = p;
+        q1.QB = 1;
+        return layout_route(nullptr, q1, C).bytes;
+    }();
+    if (one > kStaticScratchBytes)
+        return fail(ctx, IVF_EUNSUPPORTED,
+                    "route_noalloc: C = %lld, nprobe = %d need %zu bytes of scratch for one query; the static "
+                    "scratch holds %zu", (long long)C, nprobe, one, kStaticScratchBytes);
+    const size_t per_query = layout_route(nullptr, RoutePlan{2, p.Cs, p.L, p.rank_j}, C).bytes - one;
+    const int64_t fit = 1 + (int64_t)((kStaticScratchBytes - one) / std::max<size_t>(per_query, 1));
+    if (p.QB > fit) p.QB = fit >= 64 ? fit / 32 * 32 : fit;
+    while (p.QB > 1 && layout_route(nullptr, p, C).bytes > kStaticScratchBytes) --p.QB;
+    if (ctx->device < 0) return fail(ctx, IVF_EDEVICE, "no usable device (validation-only context)");
+    void *scratch_ptr = static_scratch(ctx->device);
+    if (!scratch_ptr) return fail(ctx, IVF_EDEVICE, "static scratch of device %d is not available", ctx->device);
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    // no event objects are created for this call, even when profiling is on
+    const int prof = ctx->profile;
+    ctx->profile = 0;
+    st = enqueue_route(ctx, queries, Q, centroids, C, D, nprobe, out_ids, out_dist, p, scratch_ptr);
+    ctx->profile = prof;
+    return st;
 }
 
 static ivf_status check_rows(ivf_ctx *ctx, const void *rows, int dt, int64_t N, int32_t D,

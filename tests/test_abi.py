@@ -164,6 +164,24 @@ def test_row_counts_above_int32(vctx):
     assert lib.ivf_set_option(h, B.IVF_OPT_ASSIGN_SLICE, 0) == B.IVF_OK
 
 
+def test_route_noalloc_validation(vctx):
+    """Routing with the static scratch: same argument checks as ivf_route, and
+    sizes whose layout for one query exceeds the 64 MiB scratch are refused
+    (before any device use)."""
+    lib, h = vctx.lib, vctx.handle
+    rn = lambda Q=1000, C=4096, D=128, k=16, ids=P(2 * GB): lib.ivf_route_noalloc(h, P(0), Q, P(GB), C, D, k, ids,
+                                                                                 None)
+    assert rn() == B.IVF_EDEVICE  # valid; no device behind this context
+    assert rn(Q=0) == B.IVF_OK
+    assert rn(k=0) == B.IVF_EINVAL
+    assert rn(k=2000, C=5000) == B.IVF_EUNSUPPORTED
+    assert rn(D=6) == B.IVF_EUNSUPPORTED
+    assert rn(ids=P(0)) == B.IVF_EINVAL
+    assert rn(C=20_000_000, D=4, ids=P(8 * GB)) == B.IVF_EUNSUPPORTED
+    assert "static scratch" in vctx.error()
+    assert rn(C=2_000_000, D=4, k=8, ids=P(8 * GB)) == B.IVF_EDEVICE
+
+
 def test_options_and_errors(vctx):
     lib, h = vctx.lib, vctx.handle
     assert lib.ivf_set_option(h, B.IVF_OPT_FORCE_FALLBACK, 1) == B.IVF_OK
