@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libivf.so")
 
-SOURCES = ["api.cpp", "screen.hip", "screen_i8.hip", "select.hip", "lists.hip", "lists_radix.hip", "kmeans.hip", "layout.hip", "pq.hip", "assign_graph.hip", "adc.hip", "probe.hip"]
+SOURCES = ["api.cpp", "screen.hip", "screen_i8.hip", "select.hip", "fallback.hip", "lists.hip", "lists_radix.hip", "kmeans.hip", "layout.hip", "pq.hip", "assign_graph.hip", "adc.hip", "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -39,6 +39,17 @@ def strip_fences(src: str) -> str:
         i = k + 1
 
 
+def dynamic_lds(src: str) -> str:
+    """The source with each dynamic LDS array (extern __shared__) bound to the
+    emulator's per-block dynamic LDS allocation."""
+    import re
+
+    pat = re.compile(r"extern __shared__ __attribute__\(\(aligned\(16\)\)\) unsigned char (\w+)\[\];")
+    out, n = pat.subn(lambda m: "unsigned char *%s = emu::dyn_lds;" % m.group(1), src)
+    assert n > 0
+    return out
+
+
 @pytest.fixture(scope="module")
 def emu_bin(tmp_path_factory):
     if not os.path.exists(CLANG):
@@ -48,16 +59,22 @@ def emu_bin(tmp_path_factory):
         src = strip_fences(f.read())
     with open(d / "screen_i8_host_src.hip", "w") as f:
         f.write(src)
+    with open(os.path.join(CSRC, "fallback.hip")) as f:
+        src = dynamic_lds(f.read())
+    with open(d / "fallback_host_src.hip", "w") as f:
+        f.write(src)
     exe = str(d / "screen_i8_host")
     cmd = [CLANG, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer",
            "-I", os.path.join(HERE, "wave_emu"), "-I", str(d), "-I", CSRC,
-           os.path.join(HERE, "wave_emu", "screen_i8_host.cpp"), "-o", exe, "-lpthread"]
+           os.path.join(HERE, "wave_emu", "screen_i8_host.cpp"), os.path.join(HERE, "wave_emu", "fallback_host.cpp"),
+           "-o", exe, "-lpthread"]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stderr[-4000:]
     return exe
 
 
-def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen=0, rescreen_cap=0):
+def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen=0, rescreen_cap=0,
+        run_fallback=0, wl_cap=0):
     N, D = x.shape
     src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
     with open(src, "wb") as f:
@@ -66,7 +83,8 @@ def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen
         np.ascontiguousarray(c, np.float32).tofile(f)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
     r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback), str(mode),
-                        str(force_rescreen), str(rescreen_cap)], capture_output=True, text=True, timeout=900, env=env)
+                        str(force_rescreen), str(rescreen_cap), str(run_fallback), str(wl_cap)],
+                       capture_output=True, text=True, timeout=900, env=env)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-6000:]
     raw = np.fromfile(dst, np.uint8)
     lab = raw[: 4 * N].view(np.int32)
@@ -180,3 +198,35 @@ def test_emulated_forced_fallback_and_unquantisable(emu_bin, tmp_path, oracle_mo
     c[7, 3] = 256.0  # outside the 16-bit fixed point: the kernel stands down
     lab, wl, stats, q_bad = run(emu_bin, tmp_path, x, c)
     assert q_bad == 1 and (lab == UNWRITTEN).all() and wl.size == 0 and int(stats[5]) == 0
+
+
+@pytest.mark.parametrize("mode,force_fallback,wl_cap,N", [
+    (0, 0, 3, 300),   # the worklist overflows: the scan for labels of -1 finds the rows
+    (0, 1, 0, 120),   # every row listed: centroid-split windows and their merge
+    (1, 1, 5, 300),   # every row through both planes, overflowing worklist
+])
+def test_emulated_pipeline_with_fallback(emu_bin, tmp_path, oracle_mod, mode, force_fallback, wl_cap, N):
+    """The screens followed by the exact fallback scan (fallback.hip), in the
+    library's order: every row ends with the oracle's label. The worklist
+    either holds every row the screens hand on, or overflows (capacity 1, 3,
+    5 or 100), in which case the fallback finds the rows by their labels of
+    -1; every row forced through the fallback covers the centroid-split
+    windows, their merge and the whole-row windows. Under AddressSanitizer,
+    with the dynamic LDS of every block a fresh allocation."""
+    rng = np.random.default_rng(N + wl_cap)
+    D = 64
+    pa = rng.integers(20, 236, size=(20, D)).astype(np.float32)
+    c = np.vstack([pa, pa + 1e-3, pa + 0.5, rng.uniform(0, 255, size=(97, D))]).astype(np.float32)
+    x = np.vstack([np.rint(pa), np.rint(pa + 0.25), rng.integers(0, 256, size=(N - 40, D))])
+    x = np.clip(x, 0, 255).astype(np.uint8)
+    lab, wl, st, _ = run(emu_bin, tmp_path, x, c, num_cus=2, force_fallback=force_fallback, mode=mode,
+                         run_fallback=1, wl_cap=wl_cap)
+    handed = int(st[0])  # rows the screens handed to the fallback
+    assert handed > 0
+    if wl_cap:
+        assert handed > wl_cap  # the worklist overflowed
+    if force_fallback:
+        assert handed == N
+    olab = oracle_mod.assign(x, c)
+    bad = np.nonzero(lab != olab)[0]
+    assert bad.size == 0, "labels differ at rows %s" % bad[:10]

@@ -33,6 +33,9 @@ struct dim3 {
 struct uint2 {
     unsigned x, y;
 };
+struct float4 {
+    float x, y, z, w;
+};
 typedef int hipError_t;
 typedef void *hipStream_t;
 enum { hipSuccess = 0, hipErrorInvalidValue = 1 };
@@ -55,6 +58,8 @@ struct Block {
     std::vector<std::pair<char *, std::array<char, 16>>> pending;  // LDS writes of in-flight loads
 };
 extern Block *blk;
+// dynamic LDS of the running block (the launch's shared-memory bytes)
+extern unsigned char *dyn_lds;
 inline void DmaFlush::operator()() noexcept
 {
     for (auto &p : blk->pending) memcpy(p.first, p.second.data(), 16);
@@ -240,12 +245,16 @@ inline uint32_t atomicMax(uint32_t *p, uint32_t v)
 namespace emu {
 // runs every block of the grid, one after another, with one host thread per lane
 template <typename K, typename... A>
-void launch(K kernel, dim3 grid, dim3 block, A... args)
+void launch(K kernel, dim3 grid, dim3 block, size_t shared_bytes, A... args)
 {
     gdim = grid;
     bdim = block;
     const int nt = block.x;
     for (unsigned b = 0; b < grid.x; ++b) {
+        // a fresh allocation per block, filled with a pattern, so that reads
+        // of LDS the block did not write are seen and overruns are reported
+        std::vector<unsigned char> lds(std::max<size_t>(shared_bytes, 1), 0xA5);
+        dyn_lds = shared_bytes ? lds.data() : nullptr;
         Block B;
         std::barrier<DmaFlush> bb(nt);
         B.bar = &bb;
@@ -267,4 +276,4 @@ void launch(K kernel, dim3 grid, dim3 block, A... args)
     }
 }
 }  // namespace emu
-#define hipLaunchKernelGGL(k, g, b, sh, s, ...) emu::launch(k, g, b, __VA_ARGS__)
+#define hipLaunchKernelGGL(k, g, b, sh, s, ...) emu::launch(k, g, b, (size_t)(sh), __VA_ARGS__)

@@ -2,12 +2,12 @@
 // the order the library enqueues them for uint8 rows (quantisation, the
 // single-plane screen when the padded dimension is at most 128 and mode is 1,
 // then the two-plane screen over the rows it leaves), on one case file, with
-// every array in an allocation of its own. Writes the labels, the worklist
-// and the statistics for the test to check against the oracle; the fallback
-// scan that follows in the library (another source file) is not run, so rows
-// it would settle keep the label -1.
+// every array in an allocation of its own; optionally followed by the exact
+// fallback scan of fallback.hip (built as its own translation unit), which
+// settles the rows the screens hand on. Writes the labels, the worklist and
+// the statistics for the test to check against the oracle.
 //   usage: screen_i8_host in.bin out.bin num_cus force_fallback
-//                         [mode force_rescreen rescreen_cap]
+//                         [mode force_rescreen rescreen_cap run_fallback wl_cap]
 //   in:  int64 N, C, D; uint8 rows [N][D]; float centroids [C][D]
 //   out: int32 labels [N]; uint32 worklist count; int32 worklist [count];
 //        uint64 stats [8]; uint32 quantisation flag; uint32 single-plane
@@ -17,6 +17,7 @@ namespace emu {
 thread_local dim3 tid, bid;
 dim3 bdim, gdim;
 Block *blk;
+unsigned char *dyn_lds;
 }  // namespace emu
 #include "screen_i8_host_src.hip"
 using namespace ivf;
@@ -49,7 +50,8 @@ int main(int argc, char **argv)
         if (!DP && D <= dp) DP = dp;
     if (!DP || D % 4) return 2;
     const int64_t cpad = quantized_pad(C);
-    const int64_t wl_cap = std::min<int64_t>(N, 4096 + N / 64);
+    const int64_t wl_cap_arg = argc > 9 ? atoll(argv[9]) : 0;
+    const int64_t wl_cap = wl_cap_arg > 0 ? std::min<int64_t>(wl_cap_arg, N) : std::min<int64_t>(N, 4096 + N / 64);
     int8_t *qc = alloc<int8_t>(cpad * 2 * DP, 0);
     int32_t *negb = alloc<int32_t>(cpad, 0);
     uint32_t *q_bad = alloc<uint32_t>(1, 0);
@@ -96,10 +98,19 @@ int main(int argc, char **argv)
         a.list_cnt = list_cnt;
         const int64_t cap = argc > 7 ? atoll(argv[7]) : 0;
         a.list_cap = cap > 0 ? std::min<int64_t>(cap, list_cap) : list_cap;
-        a.force_rescreen = argc > 6 ? atoi(argv[6]) : 0;
+        // as the library: a forced fallback passes every row on to the two planes
+        a.force_rescreen = (argc > 6 ? atoi(argv[6]) : 0) || a.force_fallback;
         launch_screen_i8_single(DP, a, num_cus, nullptr);
     }
     launch_screen_i8(DP, a, num_cus, nullptr);
+    if (argc > 8 && atoi(argv[8])) {
+        double *split_d = alloc<double>(kFbSplitEntries, 0);
+        int32_t *split_i = alloc<int32_t>(kFbSplitEntries, 0);
+        launch_assign_fallback(x, kRowU8, N, D, cent, C, labels, wl, wl_cnt, wl_cap, split_d, split_i,
+                               2 * num_cus, nullptr);
+        free(split_d);
+        free(split_i);
+    }
 
     FILE *o = fopen(argv[2], "wb");
     if (!o) return 2;
