@@ -435,6 +435,225 @@ __device__ void screen_top1(const ScreenArgs &a, int64_t tile, float *__restrict
     top1_finish<XT>(a, row, rvalid, h, xpart, st);
 }
 
+// ------------------------------------------------------------ filter path
+//
+// The filter's epilogue runs like the top-1 one: the previous chunk's
+// accumulators are tested group by group between the MFMAs of the current
+// chunk. A group of four values is tested as a whole (max and one compare);
+// only when some lane of the wave holds a survivor are its values staged.
+template <int W>
+struct FilterState {
+    uint32_t *cand_cnt;  // the candidate lists (copies of the launch
+    uint2 *cand;         // arguments: a pointer to the arguments themselves
+    int L;               // would put them in private memory)
+    Stage<W> *stg;
+    int64_t tile;
+    float tv;    // keep v >= tv
+    int staged;  // wave-uniform count of staged survivors
+    int wave, lane, rl;
+};
+
+// stage_flush for the filter path
+template <int W>
+__device__ __forceinline__ void filter_flush(FilterState<W> &fs, int n)
+{
+    if (fs.lane < n) {
+        const uint2 e = fs.stg->kc[fs.wave][fs.lane];
+        const int64_t row = fs.tile * (32 * W) + fs.stg->row[fs.wave][fs.lane];
+        const uint32_t slot = atomicAdd(fs.cand_cnt + row, 1u);
+        if (slot < (uint32_t)fs.L) fs.cand[row * fs.L + slot] = e;
+    }
+}
+
+// Stages (v, id) for the lanes where v passes; flushes 64 entries whenever
+// the wave has staged that many (so at most 127 are ever staged: the buffer
+// holds 128).
+template <int W>
+__device__ __forceinline__ void filter_value(float v, int id, FilterState<W> &fs)
+{
+    const bool pass = v >= fs.tv;
+    const uint64_t mask = __ballot(pass);
+    if (mask == 0) return;
+    if (pass) {
+        const int pos = fs.staged + __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+        fs.stg->kc[fs.wave][pos] = make_uint2(__float_as_uint(-2.0f * v), (uint32_t)id);
+        fs.stg->row[fs.wave][pos] = (unsigned char)fs.rl;
+    }
+    fs.staged += __popcll(mask);
+    if (fs.staged >= 64) {
+        filter_flush(fs, 64);
+        if (fs.lane < fs.staged - 64) {
+            fs.stg->kc[fs.wave][fs.lane] = fs.stg->kc[fs.wave][64 + fs.lane];
+            fs.stg->row[fs.wave][fs.lane] = fs.stg->row[fs.wave][64 + fs.lane];
+        }
+        fs.staged -= 64;
+    }
+}
+
+template <int G, int W>
+__device__ __forceinline__ void filter_group(const f32x16 &p0, const f32x16 &p1, int idp, FilterState<W> &fs)
+{
+    constexpr int rb = G >> 2;
+    constexpr int g = G & 3;
+    constexpr int off = rb * 32 + 8 * g;  // centroid offset (h excluded)
+    const f32x16 &p = rb ? p1 : p0;
+    const float m = max4(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
+    if (__any(m >= fs.tv)) {
+        filter_value(p[4 * g + 0], idp + off + 0, fs);
+        filter_value(p[4 * g + 1], idp + off + 1, fs);
+        filter_value(p[4 * g + 2], idp + off + 2, fs);
+        filter_value(p[4 * g + 3], idp + off + 3, fs);
+    }
+    // keeps the test at this point of the MFMA stream
+    asm volatile("" : "+v"(fs.tv));
+}
+
+template <int G, int T, int KB, int W>
+__device__ __forceinline__ void filter_groups_at(const f32x16 &p0, const f32x16 &p1, int idp, FilterState<W> &fs)
+{
+    if constexpr (G < 8) {
+        if constexpr (G * KB / 8 == T) filter_group<G, W>(p0, p1, idp, fs);
+        filter_groups_at<G + 1, T, KB, W>(p0, p1, idp, fs);
+    }
+}
+
+template <int DP, bool EP, int W, int T = 0>
+__device__ __forceinline__ void filter_kblocks(const float *A0, const float *A1, const float (&b)[DP / 2],
+                                               f32x16 &c0, f32x16 &c1, float4 a0, float4 a1,
+                                               const f32x16 &p0, const f32x16 &p1, int idp, FilterState<W> &fs)
+{
+    constexpr int KB = DP / 8;
+    if constexpr (T < KB) {
+        float4 n0 = a0, n1 = a1;
+        if constexpr (T + 1 < KB) {
+            n0 = *reinterpret_cast<const float4 *>(A0 + 4 * (T + 1));
+            n1 = *reinterpret_cast<const float4 *>(A1 + 4 * (T + 1));
+        }
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.x, b[4 * T + 0], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.x, b[4 * T + 0], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.y, b[4 * T + 1], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.y, b[4 * T + 1], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.z, b[4 * T + 2], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.z, b[4 * T + 2], c1, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0.w, b[4 * T + 3], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1.w, b[4 * T + 3], c1, 0, 0, 0);
+        if constexpr (EP) filter_groups_at<0, T, KB, W>(p0, p1, idp, fs);
+        __builtin_amdgcn_sched_barrier(0);
+        filter_kblocks<DP, EP, W, T + 1>(A0, A1, b, c0, c1, n0, n1, p0, p1, idp, fs);
+    }
+}
+
+// One chunk into (c0, c1) with the filter epilogue of the previous chunk
+// (p0, p1, first id idp) spread over its K-blocks.
+template <int DP, int W>
+__device__ __forceinline__ void filter_chunk(const float *A0, const float *Nh, const float (&b)[DP / 2],
+                                             f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1,
+                                             int idp, FilterState<W> &fs)
+{
+    const float *A1 = A0 + 32 * (DP + 4);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float4 u = *reinterpret_cast<const float4 *>(Nh + 8 * g);
+        const float4 w = *reinterpret_cast<const float4 *>(Nh + 32 + 8 * g);
+        c0[4 * g + 0] = u.x;
+        c0[4 * g + 1] = u.y;
+        c0[4 * g + 2] = u.z;
+        c0[4 * g + 3] = u.w;
+        c1[4 * g + 0] = w.x;
+        c1[4 * g + 1] = w.y;
+        c1[4 * g + 2] = w.z;
+        c1[4 * g + 3] = w.w;
+    }
+    const float4 a0 = *reinterpret_cast<const float4 *>(A0);
+    const float4 a1 = *reinterpret_cast<const float4 *>(A1);
+    filter_kblocks<DP, true, W>(A0, A1, b, c0, c1, a0, a1, p0, p1, idp, fs);
+}
+
+template <int G = 0, int W>
+__device__ __forceinline__ void filter_drain(const f32x16 &p0, const f32x16 &p1, int idp, FilterState<W> &fs)
+{
+    if constexpr (G < 8) {
+        filter_group<G, W>(p0, p1, idp, fs);
+        filter_drain<G + 1, W>(p0, p1, idp, fs);
+    }
+}
+
+// Filter over the chunks [ch_lo, ch_hi) of one tile: chunk j's MFMAs carry
+// chunk j-1's epilogue; the last chunk's accumulators are drained after.
+template <int DP, int W>
+__device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
+                                    float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
+{
+    constexpr int NT = W * 64;
+    constexpr int KH = DP / 2;
+    constexpr int CS = kChunk * (DP + 4);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row = tile * (32 * W) + wave * 32 + jl;
+    const bool rvalid = row < a.nrows;
+
+    float b[KH];
+    load_row<DP>(reinterpret_cast<const float *>(a.rows), row, rvalid, a.D, h, b);
+
+    FilterState<W> fs;
+    fs.cand_cnt = a.cand_cnt;
+    fs.cand = a.cand;
+    fs.L = a.L;
+    fs.stg = &stg;
+    fs.tile = tile;
+    fs.tv = kInf;  // rows past the end keep nothing
+    if (rvalid) fs.tv = fmaxf(-0.5f * a.tau[row], -__FLT_MAX__);
+    fs.staged = 0;
+    fs.wave = wave;
+    fs.lane = lane;
+    fs.rl = wave * 32 + jl;
+
+    const float *Ab = lds_c + jl * (DP + 4) + h * KH;
+    const float *Nb = lds_n + 4 * h;
+    // centroid ids fit int32; the id of register r of block rb of a chunk at
+    // cbase is cbase + 4h + rb*32 + 8*(r/4) + r%4
+    const int idh = (int)a.c_begin + 4 * h;
+    const int nch = (int)(ch_hi - ch_lo);
+
+    Stager<DP, NT> cr;
+    cr.init(a.D);
+    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
+    cr.template store<true>(lds_c, lds_n);
+    __syncthreads();
+
+    Top3 unused{};
+    f32x16 x0, x1, y0, y1;
+    cr.fetch(a.cent, a.cnorm, a.c_begin + (ch_lo + 1) * kChunk, a.c_end, a.D);
+    mfma_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, unused);
+    cr.template store<true>(lds_c + CS, lds_n + kChunk);
+    __syncthreads();
+
+    // chunk j (relative to ch_lo) sits in buffer j & 1
+    auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) {
+        cr.fetch(a.cent, a.cnorm, a.c_begin + (ch_lo + j + 1) * kChunk, a.c_end, a.D);
+        const int bj = j & 1;
+        filter_chunk<DP, W>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1,
+                            idh + (int)(ch_lo + j - 1) * kChunk, fs);
+        cr.template store<true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk);
+        __syncthreads();
+    };
+    int j = 1;
+    for (; j + 1 < nch; j += 2) {
+        step(j, y0, y1, x0, x1);
+        step(j + 1, x0, x1, y0, y1);
+    }
+    if (j < nch) {
+        step(j, y0, y1, x0, x1);
+        filter_drain(y0, y1, idh + (int)(ch_lo + j) * kChunk, fs);
+    } else {
+        filter_drain(x0, x1, idh + (int)(ch_lo + j - 1) * kChunk, fs);
+    }
+    if (fs.staged > 0) filter_flush(fs, fs.staged);
+}
+
 // Keys or filter over the chunks [ch_lo, ch_hi) of one tile. As on the
 // top-1 path the accumulators start from -||c||^2/2, so v = -key/2 exactly:
 // the keys mode writes -2v and the filter keeps v >= -tau/2 (the same test
@@ -559,7 +778,10 @@ __global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(Sc
             const int64_t tile = u / a.nchunks;
             const int64_t ch = u - tile * a.nchunks;
             const int64_t ch_end = min(a.nchunks, ch + (u1 - u));
-            screen_range<DP, W, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
+            if constexpr (MODE == kModeFilter)
+                screen_filter_range<DP, W>(a, tile, ch, ch_end, lds_c, lds_n, stg);
+            else
+                screen_range<DP, W, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
             u += ch_end - ch;
             __syncthreads();
         }
