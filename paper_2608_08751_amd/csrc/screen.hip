@@ -347,11 +347,15 @@ __device__ __forceinline__ void top1_finish(const ScreenArgs &a, int64_t row, bo
     const Top3 m = top3_merge(st, o);
     if (rvalid && h == 0) {
         const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, xn2);
+        // a centroid id is used only when it names a real centroid; any other
+        // state sends the row to the exact fallback scan
+        const bool ok1 = m.i1 >= a.c_begin && m.i1 < a.c_end;
+        const bool ok2 = m.i2 >= a.c_begin && m.i2 < a.c_end;
         int label = -1;
-        if (!a.force_fallback) {
+        if (!a.force_fallback && ok1) {
             if ((double)m.k2 > (double)m.k1 + B2) {
                 label = m.i1;
-            } else if ((double)m.k3 > (double)m.k1 + B2) {
+            } else if ((double)m.k3 > (double)m.k1 + B2 && ok2) {
                 const XT *x = reinterpret_cast<const XT *>(a.rows) + row * (int64_t)a.D;
                 const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
                 const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);

@@ -433,11 +433,15 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
     const Top3i m = top3i_merge(st, o);
     if (rvalid && h == 0) {
         const int64_t twoR = st.twoR;
+        // a centroid id is used only when it names a real centroid; any other
+        // state sends the row to the exact fallback scan
+        const bool ok1 = m.i1 >= 0 && m.i1 < a.ncent;
+        const bool ok2 = m.i2 >= 0 && m.i2 < a.ncent;
         int label = -1;
-        if (!a.force_fallback) {
+        if (!a.force_fallback && ok1) {
             if ((int64_t)m.k1 - (int64_t)m.k2 > twoR) {
                 label = m.i1;
-            } else if ((int64_t)m.k1 - (int64_t)m.k3 > twoR) {
+            } else if ((int64_t)m.k1 - (int64_t)m.k3 > twoR && ok2) {
                 const uint8_t *x = a.rows + row * (int64_t)a.D;
                 const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
                 const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
