@@ -12,6 +12,7 @@ arrays through ctypes. Definitions followed:
 * ``route``          coarse search, Eq. (1): nprobe nearest centroids by (distance, id);
 * ``assign``         nearest centroid per vector, ties to the lower id;
 * ``assign_graph``   nearest among each vector's candidate centroids (fast construction);
+* ``assign_cells``   nearest among a coarse cell's member centroids, then a greedy graph walk;
 * ``kmeans_update``  Lloyd mean update with deterministic reseed of empty clusters;
 * ``objective``      sum of squared distances of every vector to its assigned centroid;
 * ``build_lists``    cluster-major inverted lists: counts, offsets, stable permutation;
@@ -84,6 +85,7 @@ def _load():
         lib.oracle_list_major.argtypes = [p, ci, i64, p, i64, ci, p, p, i64, p, p]
         lib.oracle_pq_encode.argtypes = [p, i64, ci, ci, p, p, ci]
         lib.oracle_assign_graph.argtypes = [p, ci, i64, p, i64, ci, p, ci, p, p, p, ci]
+        lib.oracle_assign_cells.argtypes = [p, ci, i64, p, i64, ci, p, i64, p, p, i64, p, ci, ci, p, p, ci]
         lib.oracle_adc_scan.argtypes = [p, i64, ci, p, i64, p, ci, p, p, p, ci, p, ci, p, p]
         lib.oracle_pq_train_step.argtypes = [p, i64, ci, ci, p, u64, i32, p, p, p, ci]
         for f in (lib.oracle_route, lib.oracle_assign, lib.oracle_kmeans_update,
@@ -162,6 +164,27 @@ def assign_graph(x, centroids, graph, prev, nthreads: int = 0, return_dist: bool
     md = np.empty(N, np.float64) if return_dist else None
     _check(_load().oracle_assign_graph(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(g), g.shape[1], _ptr(pv),
                                        _ptr(labels), _ptr(md), nthreads), "assign_graph")
+    return (labels, md) if return_dist else labels
+
+
+def assign_cells(x, centroids, cell, cell_offsets, cell_members, graph=None, hops: int = 0,
+                 nthreads: int = 0, return_dist: bool = False):
+    """Row i takes the nearest member of its coarse cell cell[i] by (distance,
+    id), then walks graph[b] greedily up to `hops` times while a neighbour is
+    nearer; -1 (distance inf) when its cell holds no valid member."""
+    x, dt = _data(x)
+    c = _f32(centroids)
+    cl = np.ascontiguousarray(cell, dtype=np.int32)
+    off = np.ascontiguousarray(cell_offsets, dtype=np.int64)
+    mem = np.ascontiguousarray(cell_members, dtype=np.uint32)
+    g = None if graph is None else np.ascontiguousarray(graph, dtype=np.int32)
+    N, D = x.shape
+    labels = np.empty(N, np.int32)
+    md = np.empty(N, np.float64) if return_dist else None
+    _check(_load().oracle_assign_cells(_ptr(x), dt, N, _ptr(c), c.shape[0], D, _ptr(cl), off.shape[0] - 1,
+                                       _ptr(off), _ptr(mem), mem.shape[0], _ptr(g),
+                                       0 if g is None else g.shape[1], hops, _ptr(labels), _ptr(md),
+                                       nthreads), "assign_cells")
     return (labels, md) if return_dist else labels
 
 

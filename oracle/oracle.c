@@ -26,6 +26,10 @@
  *                        vector ids (Sec. "System Architecture", index layout).
  *   oracle_assign_graph  candidate-restricted assignment (fast construction
  *                        mode, Sec. "Fast Index Construction").
+ *   oracle_assign_cells  candidates for rows without a previous label: the
+ *                        members of the row's coarse cell, then a greedy walk
+ *                        over a centroid graph (Sec. "Fast Index Building
+ *                        Details", graph-assisted assignment of the base).
  *   oracle_adc_scan      residual-PQ approximate-distance scan of the probed
  *                        lists with a bounded handoff (Sec. "Residual-PQ
  *                        Candidate Reduction", Sec. "Compact PQ-Code
@@ -274,6 +278,96 @@ int oracle_assign_graph(const void *x, int dtype, int64_t n, const float *centro
     if (n == 0) return ORACLE_OK;
     graph_ctx ctx = {x, dtype, centroids, nc, D, graph, S, prev, out_labels, out_mindist};
     parallel_for(n, nthreads, graph_range, &ctx);
+    return ORACLE_OK;
+}
+
+/* Candidate source for rows that have no previous label (the graph-assisted
+ * assignment of the full base set, Sec. "Fast Index Building Details"): a
+ * coarse partition of the centroid table into G cells (each centroid a member
+ * of one cell) gives the first candidates, and a greedy walk over a graph of
+ * centroids refines them. Row i is given its cell cell[i] (e.g. its nearest
+ * coarse centroid). Its first choice b is the member of that cell of smallest
+ * (distance, id); members are members[offsets[c] .. offsets[c + 1]), the two
+ * offsets clamped into [0, n_members] (the second at least the first), and
+ * member ids outside [0, nc) are skipped. Then up to `hops` times: among the
+ * valid ids graph[b][0 .. S) take the one of smallest (distance, id); if it
+ * comes before b in (distance, id) order it becomes b, otherwise the walk
+ * stops. The label is the final b; a row whose cell lies outside [0, G) or
+ * holds no valid member gets -1 and distance +inf. */
+typedef struct {
+    const void *x;
+    int dtype;
+    const float *c;
+    int64_t nc;
+    int D;
+    const int32_t *cell;
+    int64_t G;
+    const int64_t *offsets;
+    const uint32_t *members;
+    int64_t n_members;
+    const int32_t *graph;
+    int S;
+    int hops;
+    int32_t *labels;
+    double *mind;
+} cells_ctx;
+
+static void cells_range(void *vctx, int64_t begin, int64_t end)
+{
+    cells_ctx *a = (cells_ctx *)vctx;
+    for (int64_t i = begin; i < end; ++i) {
+        double best = INFINITY;
+        int64_t arg = -1;
+        const int32_t g = a->cell[i];
+        if (g >= 0 && g < a->G) {
+            int64_t m0 = a->offsets[g], m1 = a->offsets[g + 1];
+            if (m0 < 0) m0 = 0;
+            if (m0 > a->n_members) m0 = a->n_members;
+            if (m1 < m0) m1 = m0;
+            if (m1 > a->n_members) m1 = a->n_members;
+            for (int64_t e = m0; e < m1; ++e) {
+                const int64_t j = a->members[e];
+                if (j >= a->nc) continue;
+                const double d = oracle_dist_row(a->x, a->dtype, i, a->c + j * a->D, a->D);
+                if (arg < 0 || before(d, j, best, arg)) {
+                    best = d;
+                    arg = j;
+                }
+            }
+        }
+        for (int h = 0; arg >= 0 && a->graph && h < a->hops; ++h) {
+            double nb = INFINITY;
+            int64_t narg = -1;
+            for (int s = 0; s < a->S; ++s) {
+                const int64_t j = a->graph[arg * a->S + s];
+                if (j < 0 || j >= a->nc) continue;
+                const double d = oracle_dist_row(a->x, a->dtype, i, a->c + j * a->D, a->D);
+                if (narg < 0 || before(d, j, nb, narg)) {
+                    nb = d;
+                    narg = j;
+                }
+            }
+            if (narg < 0 || !before(nb, narg, best, arg)) break;
+            best = nb;
+            arg = narg;
+        }
+        a->labels[i] = (int32_t)arg;
+        if (a->mind) a->mind[i] = best;
+    }
+}
+
+int oracle_assign_cells(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc, int D,
+                        const int32_t *cell, int64_t G, const int64_t *cell_offsets,
+                        const uint32_t *cell_members, int64_t n_members, const int32_t *graph, int S,
+                        int hops, int32_t *out_labels, double *out_mindist, int nthreads)
+{
+    if (n < 0 || nc < 1 || D < 1 || G < 1 || n_members < 0 || hops < 0 || (graph && S < 1) ||
+        (dtype != ORACLE_F32 && dtype != ORACLE_U8))
+        return ORACLE_EINVAL;
+    if (n == 0) return ORACLE_OK;
+    cells_ctx ctx = {x, dtype, centroids, nc, D, cell, G, cell_offsets, cell_members, n_members,
+                     graph, S, hops, out_labels, out_mindist};
+    parallel_for(n, nthreads, cells_range, &ctx);
     return ORACLE_OK;
 }
 

@@ -32,6 +32,11 @@ int oracle_assign_graph(const void *x, int dtype, int64_t n, const float *centro
                         int D, const int32_t *graph, int S, const int32_t *prev,
                         int32_t *out_labels, double *out_mindist, int nthreads);
 
+int oracle_assign_cells(const void *x, int dtype, int64_t n, const float *centroids, int64_t nc, int D,
+                        const int32_t *cell, int64_t G, const int64_t *cell_offsets,
+                        const uint32_t *cell_members, int64_t n_members, const int32_t *graph, int S,
+                        int hops, int32_t *out_labels, double *out_mindist, int nthreads);
+
 uint64_t oracle_splitmix64_mix(uint64_t z);
 uint64_t oracle_splitmix64_nth(uint64_t seed, uint64_t n);
 int64_t oracle_reseed_row(uint64_t seed, int32_t iter, int64_t j, int64_t n);
