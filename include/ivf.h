@@ -273,6 +273,41 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
                             const float *centroids, int64_t C, int32_t D, const int32_t *graph,
                             int32_t S, const int32_t *prev, int32_t *out_labels, float *out_dist);
 
+/* Candidates for rows that have no previous label (the graph-assisted
+ * assignment of the full base set, Sec. "Fast Index Building Details": the
+ * paper retrieves a few candidate centroids per vector from a CAGRA search
+ * over the centroid table). Here the candidates come from a coarse partition
+ * of the centroids into G cells and a greedy walk over a centroid graph:
+ * row i first takes the member of its cell cell[i] of smallest (distance, id)
+ * (cell_members[cell_offsets[c] .. cell_offsets[c + 1]), both offsets clamped
+ * into [0, M], the second to at least the first), then, up to `hops` times,
+ * moves to the neighbour graph[b][0 .. S) of smallest (distance, id) if that
+ * neighbour comes before the current choice b in (distance, id) order, and
+ * stops otherwise. Distances are exact as in the contract above; ids outside
+ * [0, C) are skipped; a row whose cell lies outside [0, G) or holds no valid
+ * member gets -1 and an infinite distance. The result is exact for that
+ * procedure, not for the full centroid table. Typical inputs: the cells from
+ * ivf_assign_build of the centroids (as fp32 rows) against a coarse table of
+ * G centroids (its offsets and permutation are cell_offsets and
+ * cell_members), the rows' cells from ivf_assign_build of the rows against
+ * the same table, and the graph from ivf_route of the centroids against
+ * themselves.
+ *   rows          [N, D] fp32 or uint8 (dt), N <= 2^32 - 1
+ *   centroids     [C, D] fp32
+ *   cell          [N] int32, cell of each row
+ *   cell_offsets  [G + 1] int64, 1 <= G <= 2^31 - 1
+ *   cell_members  [M] uint32 centroid ids grouped by cell (may be NULL when M = 0)
+ *   graph         [C, S] int32 or NULL (no walk), 1 <= S <= 64
+ *   hops          0 <= hops <= 1024
+ *   out_labels    [N] int32;  out_dist [N] fp32 squared distance or NULL
+ * No workspace. Errors: IVF_EINVAL (sizes, NULL pointers, misalignment,
+ * aliasing), IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */
+ivf_status ivf_assign_cells(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
+                            const float *centroids, int64_t C, int32_t D, const int32_t *cell,
+                            int64_t G, const int64_t *cell_offsets, const uint32_t *cell_members,
+                            int64_t M, const int32_t *graph, int32_t S, int32_t hops,
+                            int32_t *out_labels, float *out_dist);
+
 /* List-major layout of the base vectors and their residuals (Sec. "List-major
  * contiguous scans": every IVF list is one contiguous range; Sec.
  * "Residual-PQ Candidate Reduction": the residual x - c(x) to the assigned

@@ -40,6 +40,7 @@ from ._binding import (  # noqa: F401
     IvfError,
     ivf_assign_build,
     ivf_adc_scan,
+    ivf_assign_cells,
     ivf_assign_graph,
     ivf_build_lists,
     ivf_kmeans_step,

@@ -46,6 +46,7 @@ SIGNATURES = [
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
+    ("ivf_assign_cells", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I64, _P, _P, _I64, _P, _I32, _I32, _P, _P]),
     ("ivf_adc_scan", _INT, [_P, _P, _I64, _I32, _P, _I64, _P, _I32, _P, _P, _I64, _P, _I32, _P, _I32, _P, _P]),
     ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
 ]
@@ -393,6 +394,35 @@ def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None
     ctx.check(ctx.lib.ivf_assign_graph(ctx.handle, _ptr(rows), _dtype_code(rows), N, _ptr(centroids), C, D,
                                        _ptr(graph), S, _ptr(prev), _ptr(out_labels),
                                        _ptr(out_dist if want_dist else None)), "ivf_assign_graph")
+    return out_labels, (out_dist if want_dist else None)
+
+
+def ivf_assign_cells(ctx: Context, rows, centroids, cell, cell_offsets, cell_members, graph=None, hops: int = 0,
+                     out_labels=None, out_dist=None, want_dist: bool = True):
+    """Nearest member of each row's coarse cell, then up to `hops` greedy
+    moves over graph (int32 [C, S] or None): labels int32 [N] and squared
+    distances fp32 [N]."""
+    import torch
+
+    for t, name in ((rows, "rows"), (centroids, "centroids"), (cell, "cell"), (cell_offsets, "cell_offsets"),
+                    (cell_members, "cell_members")):
+        _device_tensor(t, name)
+    if graph is not None:
+        _device_tensor(graph, "graph")
+    N, D = rows.shape
+    C = centroids.shape[0]
+    G = cell_offsets.shape[0] - 1
+    M = cell_members.shape[0]
+    S = graph.shape[1] if graph is not None else 0
+    if out_labels is None:
+        out_labels = torch.empty(N, dtype=torch.int32, device=rows.device)
+    if want_dist and out_dist is None:
+        out_dist = torch.empty(N, dtype=torch.float32, device=rows.device)
+    ctx.bind_stream()
+    ctx.check(ctx.lib.ivf_assign_cells(ctx.handle, _ptr(rows), _dtype_code(rows), N, _ptr(centroids), C, D,
+                                       _ptr(cell), G, _ptr(cell_offsets), _ptr(cell_members) if M else None, M,
+                                       _ptr(graph) if graph is not None else None, S, hops, _ptr(out_labels),
+                                       _ptr(out_dist if want_dist else None)), "ivf_assign_cells")
     return out_labels, (out_dist if want_dist else None)
 
 

@@ -56,6 +56,7 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kRouteBatch = 16384;
 constexpr int kMaxNprobe = 1024;
 constexpr int kMaxD = 256;
+constexpr int kMaxHops = 1024;  // greedy moves of ivf_assign_cells
 // Rows per assignment slice (row ids inside a slice fit int32).
 constexpr int64_t kAssignSlice = (int64_t)1 << 28;
 
@@ -1110,6 +1111,49 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N, c
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     TIMED("assign_graph", launch_assign_graph(rows, rowtype, N, centroids, C, D, graph, S, prev, out_labels,
                                               out_dist, ctx->stream));
+    ctx->last_stats = nullptr;
+    return IVF_OK;
+}
+
+ivf_status ivf_assign_cells(ivf_ctx *ctx, const void *rows, int dt, int64_t N, const float *centroids,
+                            int64_t C, int32_t D, const int32_t *cell, int64_t G, const int64_t *cell_offsets,
+                            const uint32_t *cell_members, int64_t M, const int32_t *graph, int32_t S,
+                            int32_t hops, int32_t *out_labels, float *out_dist)
+{
+    if (!ctx) return IVF_EINVAL;
+    ctx->err.clear();
+    ctx->cur_call = "assign_cells";
+    ivf_status st = check_common(ctx, C, D);
+    if (st != IVF_OK) return st;
+    size_t rb;
+    if ((st = check_rows(ctx, rows, dt, N, D, &rb)) != IVF_OK) return st;
+    if (G < 1 || G > INT32_MAX) return fail(ctx, IVF_EINVAL, "G must be in [1, 2^31 - 1] (got %lld)", (long long)G);
+    if (M < 0) return fail(ctx, IVF_EINVAL, "M must be >= 0");
+    if (hops < 0 || hops > kMaxHops) return fail(ctx, IVF_EINVAL, "hops must be in [0, %d] (got %d)", kMaxHops, hops);
+    if (graph && (S < 1 || S > kMaxGraphDegree))
+        return fail(ctx, IVF_EINVAL, "S must be in [1, %d] (got %d)", kMaxGraphDegree, S);
+    if (N == 0) return IVF_OK;
+    if (!centroids || !cell || !cell_offsets || (M > 0 && !cell_members) || !out_labels)
+        return fail(ctx, IVF_EINVAL, "null pointer argument");
+    if (!aligned16(centroids) || !aligned16(cell) || !aligned16(cell_offsets) ||
+        (cell_members && !aligned16(cell_members)) || (graph && !aligned16(graph)) || !aligned16(out_labels) ||
+        (out_dist && !aligned16(out_dist)))
+        return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
+    const void *ins[6] = {rows, centroids, cell, cell_offsets, cell_members, graph};
+    const size_t ib[6] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)N * 4, (size_t)(G + 1) * 8, (size_t)M * 4,
+                          graph ? (size_t)C * S * 4 : 0};
+    const void *outs[2] = {out_labels, out_dist};
+    const size_t ob[2] = {(size_t)N * 4, (size_t)N * 4};
+    for (int i = 0; i < 2; ++i)
+        for (int k = 0; k < 6; ++k)
+            if (overlap(outs[i], ob[i], ins[k], ib[k])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
+    if (overlap(out_labels, ob[0], out_dist, ob[1])) return fail(ctx, IVF_EINVAL, "outputs overlap");
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
+    const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
+    TIMED("assign_cells", launch_assign_cells(rows, rowtype, N, centroids, C, D, cell, G, cell_offsets, cell_members,
+                                              M, graph, graph ? S : 0, hops, out_labels, out_dist, ctx->num_cus,
+                                              ctx->stream));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

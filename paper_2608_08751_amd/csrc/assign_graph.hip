@@ -14,8 +14,11 @@
 // row addresses, which the memory system merges), and a shuffle butterfly
 // inside the group takes the (distance, id) minimum.
 #include "ivf_internal.h"
+#include "exact.h"
 
 #include <limits.h>
+
+#include <algorithm>
 
 namespace ivf {
 namespace {
@@ -99,6 +102,122 @@ __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
     }
 }
 
+// Cell-and-walk assignment: candidates for rows that have no previous label
+// (the graph-assisted assignment of the full base set, Sec. "Fast Index
+// Building Details"). Row i first takes the member of its coarse cell
+// cell[i] of smallest (distance, id) (members[offsets[c] .. offsets[c + 1]),
+// both offsets clamped into [0, M]), then up to `hops` times moves to the
+// graph neighbour of smallest (distance, id) while that neighbour comes
+// before the current choice. Ids outside [0, C) are skipped; a row without a
+// valid member gets -1 and an infinite distance.
+//
+// One wave per row: the row goes to the wave's LDS slot as fp32 (exact for
+// uint8), lane l evaluates members l, l + 64, ... and, on a hop, neighbour l,
+// each with the exact sequential fp64 chain (ds_read_b128 of the row is a
+// broadcast), and a butterfly takes the wave's (distance, id) minimum.
+constexpr int kAcWaves = 4;
+
+__device__ __forceinline__ double dist_lds(const float *__restrict__ xs, const float *__restrict__ c, int D)
+{
+    double acc = 0.0;
+    for (int k0 = 0; k0 < D; k0 += 32) {
+        float4 xv[8], cv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (k0 + 4 * q < D) {
+                xv[q] = *reinterpret_cast<const float4 *>(xs + k0 + 4 * q);
+                cv[q] = *reinterpret_cast<const float4 *>(c + k0 + 4 * q);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (k0 + 4 * q < D) {
+                const float xa[4] = {xv[q].x, xv[q].y, xv[q].z, xv[q].w};
+                const float ca[4] = {cv[q].x, cv[q].y, cv[q].z, cv[q].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double t = (double)xa[e] - (double)ca[e];
+                    acc = fma(t, t, acc);
+                }
+            }
+        }
+    }
+    return acc;
+}
+
+__device__ __forceinline__ void wave_min(double &d, int &id)
+{
+    for (int off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_xor(d, off);
+        const int oid = __shfl_xor(id, off);
+        if (dist_lt(od, oid, d, id)) {
+            d = od;
+            id = oid;
+        }
+    }
+}
+
+template <typename XT>
+__global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
+    const XT *__restrict__ X, int64_t N, const float *__restrict__ cent, int64_t C, int D,
+    const int32_t *__restrict__ cell, int64_t G, const int64_t *__restrict__ offsets,
+    const uint32_t *__restrict__ members, int64_t M, const int32_t *__restrict__ graph, int S, int hops,
+    int32_t *__restrict__ labels, float *__restrict__ dist)
+{
+    __shared__ __attribute__((aligned(16))) float xs_all[kAcWaves][kCellsMaxDim];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    float *xs = xs_all[wave];
+    for (int64_t i = (int64_t)blockIdx.x * kAcWaves + wave; i < N; i += (int64_t)gridDim.x * kAcWaves) {
+        // the row into this wave's slot; the wave's own LDS operations run in
+        // order, the fence keeps the compiler from moving reads above writes
+        __builtin_amdgcn_wave_barrier();
+        for (int d = lane; d < D; d += 64) xs[d] = (float)X[i * D + d];
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+
+        double bd = __builtin_huge_val();
+        int bi = INT_MAX;  // loses every comparison against a real candidate
+        const int32_t g = cell[i];
+        if (g >= 0 && g < G) {
+            int64_t m0 = offsets[g], m1 = offsets[g + 1];
+            m0 = min(max(m0, (int64_t)0), M);
+            m1 = min(max(m1, m0), M);
+            for (int64_t e = m0 + lane; e < m1; e += 64) {
+                const uint32_t j = members[e];
+                if ((int64_t)j < C) {
+                    const double d = dist_lds(xs, cent + (int64_t)j * D, D);
+                    if (dist_lt(d, (int)j, bd, bi)) {
+                        bd = d;
+                        bi = (int)j;
+                    }
+                }
+            }
+        }
+        wave_min(bd, bi);
+        for (int h = 0; bi != INT_MAX && graph && h < hops; ++h) {
+            double nd = __builtin_huge_val();
+            int ni = INT_MAX;
+            if (lane < S) {
+                const int32_t j = graph[(int64_t)bi * S + lane];
+                if (j >= 0 && j < C) {
+                    nd = dist_lds(xs, cent + (int64_t)j * D, D);
+                    ni = j;
+                }
+            }
+            wave_min(nd, ni);
+            if (ni == INT_MAX || !dist_lt(nd, ni, bd, bi)) break;
+            bd = nd;
+            bi = ni;
+        }
+        if (lane == 0) {
+            const bool none = bi == INT_MAX;
+            labels[i] = none ? -1 : bi;
+            if (dist) dist[i] = none ? __builtin_huge_valf() : (float)bd;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C,
@@ -116,6 +235,29 @@ hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const f
     else
         hipLaunchKernelGGL(assign_graph_kernel<float>, dim3(grid), dim3(kAgThreads), 0, s,
                            (const float *)rows, N, cent, C, D, graph, S, sp_log2, prev, labels, dist);
+    return hipGetLastError();
+}
+
+}  // namespace ivf
+
+namespace ivf {
+
+hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C, int D,
+                               const int32_t *cell, int64_t G, const int64_t *offsets, const uint32_t *members,
+                               int64_t M, const int32_t *graph, int S, int hops, int32_t *labels, float *dist,
+                               int num_cus, hipStream_t s)
+{
+    if (N <= 0) return hipSuccess;
+    const int64_t blocks = (N + kAcWaves - 1) / kAcWaves;
+    const unsigned grid = (unsigned)std::min<int64_t>(blocks, (int64_t)num_cus * 32);
+    if (rowtype == kRowU8)
+        hipLaunchKernelGGL(assign_cells_kernel<uint8_t>, dim3(grid), dim3(kAcWaves * 64), 0, s,
+                           (const uint8_t *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
+                           labels, dist);
+    else
+        hipLaunchKernelGGL(assign_cells_kernel<float>, dim3(grid), dim3(kAcWaves * 64), 0, s,
+                           (const float *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
+                           labels, dist);
     return hipGetLastError();
 }
 

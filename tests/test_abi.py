@@ -273,6 +273,28 @@ def test_assign_graph_validation(vctx, lib):
     assert ok(dist=P(5 * GB + 4)) == B.IVF_EINVAL  # misaligned
 
 
+def test_assign_cells_validation(vctx, lib):
+    h = vctx.handle
+    rows, cent, cell, off, mem, graph, lab, dist = (P(i * GB) for i in range(8))
+    ok = lambda **k: lib.ivf_assign_cells(h, rows, B.IVF_U8, k.get("N", 1000), cent, 100, k.get("D", 128),
+                                          k.get("cell", cell), k.get("G", 10), k.get("off", off),
+                                          k.get("mem", mem), k.get("M", 100), k.get("graph", graph),
+                                          k.get("S", 8), k.get("hops", 4), k.get("lab", lab), k.get("dist", dist))
+    assert ok() == B.IVF_EDEVICE
+    assert ok(graph=None, S=0) == B.IVF_EDEVICE and ok(dist=None) == B.IVF_EDEVICE
+    assert ok(mem=None, M=0) == B.IVF_EDEVICE
+    assert ok(N=0) == B.IVF_OK
+    assert ok(G=0) == B.IVF_EINVAL and ok(M=-1) == B.IVF_EINVAL
+    assert ok(hops=-1) == B.IVF_EINVAL and ok(hops=1025) == B.IVF_EINVAL
+    assert ok(S=0) == B.IVF_EINVAL and ok(S=65) == B.IVF_EINVAL
+    assert ok(D=260) == B.IVF_EUNSUPPORTED and ok(N=1 << 32) == B.IVF_EUNSUPPORTED
+    assert ok(cell=None) == B.IVF_EINVAL and ok(off=None) == B.IVF_EINVAL and ok(mem=None) == B.IVF_EINVAL
+    assert ok(lab=None) == B.IVF_EINVAL
+    assert ok(lab=P(2 * GB + 16)) == B.IVF_EINVAL  # overlaps cell
+    assert ok(dist=P(6 * GB + 64)) == B.IVF_EINVAL  # overlaps the labels
+    assert ok(off=P(3 * GB + 8)) == B.IVF_EINVAL  # misaligned
+
+
 def test_adc_scan_validation(vctx, lib):
     h = vctx.handle
     q, c, pr, off, perm, codes, cb, ids, dist = (P(i * GB) for i in range(9))
