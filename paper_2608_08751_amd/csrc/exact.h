@@ -46,4 +46,33 @@ __device__ __forceinline__ double exact_dist(const XT *__restrict__ x, const flo
     return s;
 }
 
+// The same distance for a row staged in LDS (fp32) and a centroid row whose
+// address is 16-byte aligned (D % 4 == 0): the centroid is read 64 dims at a
+// time in 16-byte loads, all issued before their fma chain.
+__device__ __forceinline__ double exact_dist_lds4(const float *__restrict__ x, const float *__restrict__ c, int D)
+{
+    double s = 0.0;
+#pragma unroll 1
+    for (int d0 = 0; d0 < D; d0 += 64) {
+        float4 cv[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            if (d0 + 4 * q < D) cv[q] = *reinterpret_cast<const float4 *>(c + d0 + 4 * q);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            if (d0 + 4 * q < D) {
+                const float4 xv = *reinterpret_cast<const float4 *>(x + d0 + 4 * q);
+                const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
+                const float ca[4] = {cv[q].x, cv[q].y, cv[q].z, cv[q].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double t = (double)xa[e] - (double)ca[e];
+                    s = fma(t, t, s);
+                }
+            }
+        }
+    }
+    return s;
+}
+
 }  // namespace ivf

@@ -170,28 +170,25 @@ __device__ __forceinline__ double key_bound(double coef, uint32_t mc2_bits, doub
     return coef * (M + 2.0 * sqrt(xn2 * (1.0 + 0x1p-40)) * sqrt(M)) + 0x1p-100;
 }
 
-// Survivors of the filter epilogue are staged per wave in LDS and written out
-// 64 at a time: lane i of the flush takes staged entry i, reserves a slot in
-// its row's candidate list with one global atomic and stores (key, id).
-constexpr int kStage = 128;
-
+// Survivors of the filter epilogue: a lane whose group of four values holds
+// one at or above its threshold queues the whole group (the four values and
+// the first id) in LDS, entry i of lane l of a wave at [wave][i][l] so that
+// the lanes of one store hit consecutive addresses; one 16-byte and one
+// 4-byte store per group, no per-value work on the MFMA path. A flush (before
+// a lane's queue would overflow, and at the end of a range) keeps the values
+// that pass: a lane's entries all belong to its own row, so one atomic on the
+// row's counter reserves room for all of them.
 template <int W>
-struct Stage {
-    uint2 kc[W][kStage];            // (key bits, centroid id)
-    unsigned char row[W][kStage];   // row within the tile
-};
-
-template <int W>
-__device__ __forceinline__ void stage_flush(const ScreenArgs &a, Stage<W> &st, int wave, int lane,
-                                            int64_t tile, int n)
+constexpr int filter_queue_cap()
 {
-    if (lane < n) {
-        const uint2 e = st.kc[wave][lane];
-        const int64_t row = tile * (32 * W) + st.row[wave][lane];
-        const uint32_t slot = atomicAdd(a.cand_cnt + row, 1u);
-        if (slot < (uint32_t)a.L) a.cand[row * a.L + slot] = e;
-    }
+    return W == 8 ? 8 : 4;  // 80 KiB (8 waves) or 20 KiB (4 waves, wide rows)
 }
+
+template <int W>
+struct FilterQueue {
+    float4 v[W][filter_queue_cap<W>()][64];  // the group's four values
+    int id[W][filter_queue_cap<W>()][64];    // id of its first value
+};
 
 // ---------------------------------------------------------------- top-1 path
 //
@@ -450,49 +447,43 @@ struct FilterState {
     uint32_t *cand_cnt;  // the candidate lists (copies of the launch
     uint2 *cand;         // arguments: a pointer to the arguments themselves
     int L;               // would put them in private memory)
-    Stage<W> *stg;
-    int64_t tile;
-    float tv;    // keep v >= tv
-    int staged;  // wave-uniform count of staged survivors
-    int wave, lane, rl;
+    FilterQueue<W> *q;
+    int64_t row;  // this lane's row
+    float tv;     // keep v >= tv
+    int qn;       // entries in this lane's queue
+    int wave, lane;
 };
 
-// stage_flush for the filter path
+// Moves every lane's queued values that pass into its row's candidate list:
+// one atomic per lane reserves their number of slots (entries past the
+// list's capacity are dropped; the selection sees the count and sends the
+// row to the fallback). Keys are -2v, exactly.
 template <int W>
-__device__ __forceinline__ void filter_flush(FilterState<W> &fs, int n)
+__device__ __forceinline__ void filter_flush(FilterState<W> &fs)
 {
-    if (fs.lane < n) {
-        const uint2 e = fs.stg->kc[fs.wave][fs.lane];
-        const int64_t row = fs.tile * (32 * W) + fs.stg->row[fs.wave][fs.lane];
-        const uint32_t slot = atomicAdd(fs.cand_cnt + row, 1u);
-        if (slot < (uint32_t)fs.L) fs.cand[row * fs.L + slot] = e;
-    }
-}
-
-// Stages (v, id) for the lanes where v passes; flushes 64 entries whenever
-// the wave has staged that many (so at most 127 are ever staged: the buffer
-// holds 128).
-template <int W>
-__device__ __forceinline__ void filter_value(float v, int id, FilterState<W> &fs)
-{
-    const bool pass = v >= fs.tv;
-    const uint64_t mask = __ballot(pass);
-    if (mask == 0) return;
-    if (pass) {
-        const int pos = fs.staged + __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-        fs.stg->kc[fs.wave][pos] = make_uint2(__float_as_uint(-2.0f * v), (uint32_t)id);
-        fs.stg->row[fs.wave][pos] = (unsigned char)fs.rl;
-    }
-    fs.staged += __popcll(mask);
-    if (fs.staged >= 64) {
-        filter_flush(fs, 64);
-        if (fs.lane < fs.staged - 64) {
-            fs.stg->kc[fs.wave][fs.lane] = fs.stg->kc[fs.wave][64 + fs.lane];
-            fs.stg->row[fs.wave][fs.lane] = fs.stg->row[fs.wave][64 + fs.lane];
+    if (fs.qn > 0) {
+        uint32_t n = 0;
+        for (int i = 0; i < fs.qn; ++i) {
+            const float4 v = fs.q->v[fs.wave][i][fs.lane];
+            n += (v.x >= fs.tv) + (v.y >= fs.tv) + (v.z >= fs.tv) + (v.w >= fs.tv);
         }
-        fs.staged -= 64;
+        const uint32_t slot = atomicAdd(fs.cand_cnt + fs.row, n);
+        uint2 *dst = fs.cand + fs.row * fs.L;
+        uint32_t k = slot;
+        for (int i = 0; i < fs.qn; ++i) {
+            const float4 v4 = fs.q->v[fs.wave][i][fs.lane];
+            const int id = fs.q->id[fs.wave][i][fs.lane];
+            const float va[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (va[e] >= fs.tv) {
+                    if (k < (uint32_t)fs.L) dst[k] = make_uint2(__float_as_uint(-2.0f * va[e]), (uint32_t)(id + e));
+                    ++k;
+                }
+            }
+        }
     }
+    fs.qn = 0;
 }
 
 template <int G, int W>
@@ -503,11 +494,14 @@ __device__ __forceinline__ void filter_group(const f32x16 &p0, const f32x16 &p1,
     constexpr int off = rb * 32 + 8 * g;  // centroid offset (h excluded)
     const f32x16 &p = rb ? p1 : p0;
     const float m = max4(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
-    if (__any(m >= fs.tv)) {
-        filter_value(p[4 * g + 0], idp + off + 0, fs);
-        filter_value(p[4 * g + 1], idp + off + 1, fs);
-        filter_value(p[4 * g + 2], idp + off + 2, fs);
-        filter_value(p[4 * g + 3], idp + off + 3, fs);
+    const bool pass = m >= fs.tv;
+    if (__any(pass)) {
+        if (__any(fs.qn >= filter_queue_cap<W>())) filter_flush(fs);
+        if (pass) {
+            fs.q->v[fs.wave][fs.qn][fs.lane] = make_float4(p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]);
+            fs.q->id[fs.wave][fs.qn][fs.lane] = idp + off;
+            ++fs.qn;
+        }
     }
     // keeps the test at this point of the MFMA stream
     asm volatile("" : "+v"(fs.tv));
@@ -587,7 +581,7 @@ __device__ __forceinline__ void filter_drain(const f32x16 &p0, const f32x16 &p1,
 // chunk j-1's epilogue; the last chunk's accumulators are drained after.
 template <int DP, int W>
 __device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
-                                    float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
+                                    float *__restrict__ lds_c, float *__restrict__ lds_n, FilterQueue<W> &fq)
 {
     constexpr int NT = W * 64;
     constexpr int KH = DP / 2;
@@ -606,14 +600,13 @@ __device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t
     fs.cand_cnt = a.cand_cnt;
     fs.cand = a.cand;
     fs.L = a.L;
-    fs.stg = &stg;
-    fs.tile = tile;
+    fs.q = &fq;
+    fs.row = row;
     fs.tv = kInf;  // rows past the end keep nothing
     if (rvalid) fs.tv = fmaxf(-0.5f * a.tau[row], -__FLT_MAX__);
-    fs.staged = 0;
+    fs.qn = 0;
     fs.wave = wave;
     fs.lane = lane;
-    fs.rl = wave * 32 + jl;
 
     const float *Ab = lds_c + jl * (DP + 4) + h * KH;
     const float *Nb = lds_n + 4 * h;
@@ -655,17 +648,16 @@ __device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t
     } else {
         filter_drain(x0, x1, idh + (int)(ch_lo + j - 1) * kChunk, fs);
     }
-    if (fs.staged > 0) filter_flush(fs, fs.staged);
+    filter_flush(fs);
 }
 
-// Keys or filter over the chunks [ch_lo, ch_hi) of one tile. As on the
-// top-1 path the accumulators start from -||c||^2/2, so v = -key/2 exactly:
-// the keys mode writes -2v and the filter keeps v >= -tau/2 (the same test
-// as key <= tau). Padded centroids have v = -inf and the row threshold is
-// clamped to the lowest finite float, so they never pass.
-template <int DP, int W, typename XT, int MODE>
-__device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
-                             float *__restrict__ lds_c, float *__restrict__ lds_n, Stage<W> &stg)
+// Keys over the chunks [ch_lo, ch_hi) of one tile (the routing threshold
+// sample). As on the top-1 path the accumulators start from -||c||^2/2, so
+// v = -key/2 exactly and the key written is -2v. Padded centroids have v =
+// -inf, i.e. an infinite key.
+template <int DP, int W, typename XT>
+__device__ void screen_keys_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
+                                  float *__restrict__ lds_c, float *__restrict__ lds_n)
 {
     constexpr int NT = W * 64;
     constexpr int KH = DP / 2;
@@ -679,10 +671,6 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
 
     float b[KH];
     load_row<DP>(reinterpret_cast<const XT *>(a.rows), row, rvalid, a.D, h, b);
-
-    float tv = kInf;  // filter: keep v >= tv; rows past the end keep nothing
-    if (MODE == kModeFilter && rvalid) tv = fmaxf(-0.5f * a.tau[row], -__FLT_MAX__);
-    int staged = 0;  // wave-uniform count of staged survivors
     Top3 unused{};
 
     Stager<DP, NT> cr;
@@ -702,53 +690,23 @@ __device__ void screen_range(const ScreenArgs &a, int64_t tile, int64_t ch_lo, i
         mfma_chunk<DP, false>(Ab + buf * CS, Nb + buf * kChunk, b, acc0, acc1, acc0, acc1, 0, unused);
 
         // register r of block rb holds centroid rb*32 + 8*(r/4) + 4*h + r%4
-        if (MODE == kModeKeys) {
-            if (rvalid) {
-                const int64_t ld = a.c_end - a.c_begin;  // a multiple of kChunk
-                float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
+        if (rvalid) {
+            const int64_t ld = a.c_end - a.c_begin;  // a multiple of kChunk
+            float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    *reinterpret_cast<float4 *>(out + 8 * g) =
-                        make_float4(-2.0f * acc0[4 * g + 0], -2.0f * acc0[4 * g + 1],
-                                    -2.0f * acc0[4 * g + 2], -2.0f * acc0[4 * g + 3]);
-                    *reinterpret_cast<float4 *>(out + 32 + 8 * g) =
-                        make_float4(-2.0f * acc1[4 * g + 0], -2.0f * acc1[4 * g + 1],
-                                    -2.0f * acc1[4 * g + 2], -2.0f * acc1[4 * g + 3]);
-                }
-            }
-        } else {  // kModeFilter
-            const int cb32 = (int)cbase + 4 * h;  // centroid ids fit int32
-#pragma unroll
-            for (int r = 0; r < 32; ++r) {
-                const float v = r < 16 ? acc0[r] : acc1[r - 16];
-                const bool pass = v >= tv;
-                const uint64_t mask = __ballot(pass);
-                if (mask != 0) {
-                    if (pass) {
-                        const int cid = cb32 + (r >> 4) * 32 + 8 * ((r & 15) >> 2) + (r & 3);
-                        const int pos = staged + __builtin_amdgcn_mbcnt_hi(
-                            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-                        stg.kc[wave][pos] = make_uint2(__float_as_uint(-2.0f * v), (uint32_t)cid);
-                        stg.row[wave][pos] = (unsigned char)(wave * 32 + jl);
-                    }
-                    staged += __popcll(mask);
-                    if (staged >= 64) {
-                        stage_flush(a, stg, wave, lane, tile, 64);
-                        if (lane < staged - 64) {
-                            stg.kc[wave][lane] = stg.kc[wave][64 + lane];
-                            stg.row[wave][lane] = stg.row[wave][64 + lane];
-                        }
-                        staged -= 64;
-                    }
-                }
+            for (int g = 0; g < 4; ++g) {
+                *reinterpret_cast<float4 *>(out + 8 * g) =
+                    make_float4(-2.0f * acc0[4 * g + 0], -2.0f * acc0[4 * g + 1],
+                                -2.0f * acc0[4 * g + 2], -2.0f * acc0[4 * g + 3]);
+                *reinterpret_cast<float4 *>(out + 32 + 8 * g) =
+                    make_float4(-2.0f * acc1[4 * g + 0], -2.0f * acc1[4 * g + 1],
+                                -2.0f * acc1[4 * g + 2], -2.0f * acc1[4 * g + 3]);
             }
         }
 
         cr.template store<true>(lds_c + (buf ^ 1) * CS, lds_n + (buf ^ 1) * kChunk);
         __syncthreads();
     }
-
-    if (MODE == kModeFilter && staged > 0) stage_flush(a, stg, wave, lane, tile, staged);
 }
 
 // Waves per SIMD: two, so that one wave's staging and epilogue overlap the
@@ -773,7 +731,6 @@ __global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(Sc
             __syncthreads();
         }
     } else {
-        __shared__ Stage<W> stg;
         // a contiguous range of (tile, chunk) units in tile-major order
         const int64_t units = ntiles * a.nchunks;
         int64_t u = units * blockIdx.x / gridDim.x;
@@ -782,10 +739,12 @@ __global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(Sc
             const int64_t tile = u / a.nchunks;
             const int64_t ch = u - tile * a.nchunks;
             const int64_t ch_end = min(a.nchunks, ch + (u1 - u));
-            if constexpr (MODE == kModeFilter)
-                screen_filter_range<DP, W>(a, tile, ch, ch_end, lds_c, lds_n, stg);
-            else
-                screen_range<DP, W, XT, MODE>(a, tile, ch, ch_end, lds_c, lds_n, stg);
+            if constexpr (MODE == kModeFilter) {
+                __shared__ FilterQueue<W> fq;
+                screen_filter_range<DP, W>(a, tile, ch, ch_end, lds_c, lds_n, fq);
+            } else {
+                screen_keys_range<DP, W, XT>(a, tile, ch, ch_end, lds_c, lds_n);
+            }
             u += ch_end - ch;
             __syncthreads();
         }

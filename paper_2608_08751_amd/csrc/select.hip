@@ -69,8 +69,9 @@ __global__ void fill_u32_kernel(uint32_t *p, int64_t n, uint32_t v)
         p[i] = v;
 }
 
-// fl32(||c||^2) per centroid (fp64 accumulation, one wave per row) and the
-// maximum over all rows (as float bits; floats >= 0 order like their bits).
+// fl32(||c||^2) per centroid (fp64 accumulation in dimension order, one
+// thread per row, 16-byte loads; D % 4 == 0) and the maximum over all rows
+// (as float bits; floats >= 0 order like their bits).
 __global__ __launch_bounds__(256) void centroid_norms_kernel(const float *__restrict__ cent,
                                                              int64_t C, int D,
                                                              float *__restrict__ cnorm,
@@ -80,17 +81,29 @@ __global__ __launch_bounds__(256) void centroid_norms_kernel(const float *__rest
     const int wave = threadIdx.x >> 6;
     __shared__ uint32_t wmax[4];
     uint32_t mx = 0;
-    for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < C; r += (int64_t)gridDim.x * 4) {
+    for (int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x; r < C; r += (int64_t)gridDim.x * 256) {
+        const float4 *p = reinterpret_cast<const float4 *>(cent + r * D);
         double s = 0.0;
-        for (int d = lane; d < D; d += 64) {
-            const double v = (double)cent[r * D + d];
-            s = fma(v, v, s);
+        for (int d4 = 0; d4 < D / 4; d4 += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (d4 + u < D / 4) v[u] = p[d4 + u];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                if (d4 + u < D / 4) {
+                    s = fma((double)v[u].x, (double)v[u].x, s);
+                    s = fma((double)v[u].y, (double)v[u].y, s);
+                    s = fma((double)v[u].z, (double)v[u].z, s);
+                    s = fma((double)v[u].w, (double)v[u].w, s);
+                }
+            }
         }
-        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
         const float n = (float)s;
-        if (lane == 0) cnorm[r] = n;
+        cnorm[r] = n;
         mx = max(mx, __float_as_uint(n));
     }
+    for (int o = 32; o > 0; o >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
     if (lane == 0) wmax[wave] = mx;
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -236,6 +249,65 @@ __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
     }
 }
 
+// The same threshold with the query's sample keys read once: thread t keeps
+// groups t, t + 256, ... (GPT of them, 16 keys each) in registers, takes
+// their minima for the selection and then emits its own keys <= tau. Used
+// when the sample has at most 256 * GPT groups.
+template <int GPT>
+__global__ __launch_bounds__(256) void route_threshold_reg_kernel(RouteArgs a)
+{
+    const int64_t q = blockIdx.x;
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sh[2];
+    __shared__ uint32_t s_cnt;
+    const int G = (int)(a.Cs / 16);
+    const float4 *k4 = reinterpret_cast<const float4 *>(a.keys + q * a.Cs);
+    float4 w[GPT][4];
+    uint32_t v[GPT];
+    int nv = 0;
+#pragma unroll
+    for (int e = 0; e < GPT; ++e) {
+        const int g = threadIdx.x + 256 * e;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w[e][i] = g < G ? k4[4 * (int64_t)g + i] : make_float4(kInfF, kInfF, kInfF, kInfF);
+    }
+#pragma unroll
+    for (int e = 0; e < GPT; ++e) {
+        float m = kInfF;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fminf(m, fminf(fminf(w[e][i].x, w[e][i].y), fminf(w[e][i].z, w[e][i].w)));
+        v[e] = 0xFFFFFFFFu;
+        if (threadIdx.x + 256 * e < G) {
+            v[e] = f2o(m);
+            nv = e + 1;
+        }
+    }
+    if (threadIdx.x == 0) s_cnt = 0;
+    const float th = o2f(block_select(v, nv, min(a.rank_j, G), hist, sh));
+#pragma unroll
+    for (int e = 0; e < GPT; ++e) {
+        const int g = threadIdx.x + 256 * e;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float kk[4] = {w[e][i].x, w[e][i].y, w[e][i].z, w[e][i].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if (g < G && kk[c] <= th) {
+                    const uint32_t slot = atomicAdd(&s_cnt, 1u);
+                    if (slot < (uint32_t)a.L)
+                        a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[c]), (uint32_t)(16 * g + 4 * i + c));
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a.tau[q] = th;
+        a.cand_cnt[q] = s_cnt;
+    }
+}
+
 // Certified selection of one query's top-k from its screened candidates.
 // Candidates = every centroid with key <= tau. Let kth = the k-th smallest key
 // (radix select). If tau >= kth + 2B, every centroid outside
@@ -259,12 +331,13 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a)
     const int64_t q = blockIdx.x;
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh[2];
-    __shared__ int rid[kMaxCand];
-    __shared__ double rd[kMaxCand];
-    __shared__ float qrow[256];
+    __shared__ __attribute__((aligned(16))) float qrow[256];
     __shared__ int s_nr;
+    // R (at most L <= kMaxCand entries): fp64 distances, then ids
+    extern __shared__ __attribute__((aligned(16))) unsigned char sel_lds[];
+    double *rd = reinterpret_cast<double *>(sel_lds);
+    int *rid = reinterpret_cast<int *>(rd + a.L);
     const uint32_t n = a.cand_cnt[q];
-    if (threadIdx.x == 0) atomicAdd(a.stats + kStatCandidates, (unsigned long long)n);
     const bool overflow = n > (uint32_t)a.L;
     if (a.force_fallback || overflow || n < (uint32_t)a.k) {
         if (threadIdx.x == 0) push_fallback(a, q, overflow);
@@ -324,6 +397,21 @@ __global__ __launch_bounds__(256) void route_fallback_kernel(RouteArgs a)
     __shared__ int bi[2048];
     __shared__ float qrow[256];
     __shared__ uint32_t s_cnt;
+    __shared__ unsigned long long s_sum[4];
+    {
+        // the candidate total of the batch for the statistics (one atomic
+        // per workgroup instead of one per query)
+        unsigned long long sum = 0;
+        for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < a.nq; q += (int64_t)gridDim.x * blockDim.x)
+            sum += a.cand_cnt[q];
+        for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+        if ((threadIdx.x & 63) == 0) s_sum[threadIdx.x >> 6] = sum;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const unsigned long long t = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
+            if (t) atomicAdd(a.stats + kStatCandidates, t);
+        }
+    }
     const uint32_t total = *a.wl_cnt;
     int K2 = 256;
     while (K2 < a.k) K2 <<= 1;
@@ -391,7 +479,7 @@ hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s)
 hipError_t launch_centroid_norms(const float *cent, int64_t C, int D, float *cnorm,
                                  uint32_t *mc2_bits, hipStream_t s)
 {
-    hipLaunchKernelGGL(centroid_norms_kernel, dim3(grid_for(C, 4, 2048)), dim3(256), 0, s, cent, C, D,
+    hipLaunchKernelGGL(centroid_norms_kernel, dim3(grid_for(C, 256, 4096)), dim3(256), 0, s, cent, C, D,
                        cnorm, mc2_bits);
     return hipGetLastError();
 }
@@ -405,13 +493,22 @@ hipError_t launch_row_norms(const float *rows, int64_t n, int D, double *out, hi
 
 hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(route_threshold_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    const int64_t G = a.Cs / 16;
+    if (a.Cs > 0 && G <= 256)
+        hipLaunchKernelGGL(route_threshold_reg_kernel<1>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    else if (a.Cs > 0 && G <= 512)
+        hipLaunchKernelGGL(route_threshold_reg_kernel<2>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    else if (a.Cs > 0 && G <= 1024)
+        hipLaunchKernelGGL(route_threshold_reg_kernel<4>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(route_threshold_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_route_select(const RouteArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(route_select_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    const size_t lds = (size_t)a.L * (sizeof(double) + sizeof(int));
+    hipLaunchKernelGGL(route_select_kernel, dim3((unsigned)a.nq), dim3(256), lds, s, a);
     return hipGetLastError();
 }
 
