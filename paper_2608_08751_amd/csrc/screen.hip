@@ -20,6 +20,7 @@
 // holds centroid 8*(r/4) + 4*(l/32) + r%4 of the block.
 #include "ivf_internal.h"
 #include "exact.h"
+#include "wave_ops.h"
 
 #include <math.h>
 
@@ -342,13 +343,14 @@ __device__ __forceinline__ void top1_finish(const ScreenArgs &a, int64_t row, bo
     o.i1 = __shfl_xor(st.i1, 32);
     o.i2 = __shfl_xor(st.i2, 32);
     const Top3 m = top3_merge(st, o);
+    int label = -1;
+    bool refined = false;
     if (rvalid && h == 0) {
         const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, xn2);
         // a centroid id is used only when it names a real centroid; any other
         // state sends the row to the exact fallback scan
         const bool ok1 = m.i1 >= a.c_begin && m.i1 < a.c_end;
         const bool ok2 = m.i2 >= a.c_begin && m.i2 < a.c_end;
-        int label = -1;
         if (!a.force_fallback && ok1) {
             if ((double)m.k2 > (double)m.k1 + B2) {
                 label = m.i1;
@@ -357,16 +359,17 @@ __device__ __forceinline__ void top1_finish(const ScreenArgs &a, int64_t row, bo
                 const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
                 const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
                 label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
-                atomicAdd(a.stats + kStatRefine2, 1ull);
+                refined = true;
             }
-        }
-        if (label < 0) {
-            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
-            if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
-            atomicAdd(a.stats + kStatFallback, 1ull);
         }
         a.labels[row] = label;
     }
+    // statistics and worklist slots: one atomic per wave
+    const bool to_fallback = rvalid && h == 0 && label < 0;
+    wave_count(a.stats + kStatRefine2, refined);
+    wave_count(a.stats + kStatFallback, to_fallback);
+    const uint32_t slot = wave_append(a.wl_cnt, to_fallback);
+    if (to_fallback && slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
 }
 
 template <int DP, int W, typename XT>

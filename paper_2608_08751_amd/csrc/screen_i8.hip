@@ -31,6 +31,7 @@
 // registers (same byte mapping); accumulator register r of lane l holds
 // centroid 8 (r / 4) + 4 (l / 32) + r % 4 of the block for row l % 32.
 #include "exact.h"
+#include "wave_ops.h"
 #include "ivf_internal.h"
 
 #include <algorithm>
@@ -431,13 +432,14 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
     o.i1 = __shfl_xor(st.i1, 32);
     o.i2 = __shfl_xor(st.i2, 32);
     const Top3i m = top3i_merge(st, o);
+    int label = -1;
+    bool refined = false;
     if (rvalid && h == 0) {
         const int64_t twoR = st.twoR;
         // a centroid id is used only when it names a real centroid; any other
         // state sends the row to the exact fallback scan
         const bool ok1 = m.i1 >= 0 && m.i1 < a.ncent;
         const bool ok2 = m.i2 >= 0 && m.i2 < a.ncent;
-        int label = -1;
         if (!a.force_fallback && ok1) {
             if ((int64_t)m.k1 - (int64_t)m.k2 > twoR) {
                 label = m.i1;
@@ -446,16 +448,17 @@ __device__ __forceinline__ void i8_finish(const ScreenI8Args &a, int64_t row, bo
                 const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
                 const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
                 label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
-                atomicAdd(a.stats + kStatRefine2, 1ull);
+                refined = true;
             }
-        }
-        if (label < 0) {
-            const uint32_t slot = atomicAdd(a.wl_cnt, 1u);
-            if (slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
-            atomicAdd(a.stats + kStatFallback, 1ull);
         }
         a.labels[row] = label;
     }
+    // statistics and worklist slots: one atomic per wave
+    const bool to_fallback = rvalid && h == 0 && label < 0;
+    wave_count(a.stats + kStatRefine2, refined);
+    wave_count(a.stats + kStatFallback, to_fallback);
+    const uint32_t slot = wave_append(a.wl_cnt, to_fallback);
+    if (to_fallback && slot < (uint64_t)a.wl_cap) a.wl[slot] = (int32_t)row;
 }
 
 // One workgroup tile: W * 32 * RB rows against every centroid. Chunk j sits
@@ -806,11 +809,12 @@ __device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bo
     o.i1 = __shfl_xor(st.i1, 32);
     o.i2 = __shfl_xor(st.i2, 32);
     const Top3i m = top3i_merge(st, o);
+    int label = -1;
+    bool refined = false;
     if (rvalid && h == 0) {
         const int64_t T = st.twoR;
         const bool ok1 = m.i1 >= 0 && m.i1 < a.ncent;
         const bool ok2 = m.i2 >= 0 && m.i2 < a.ncent;
-        int label = -1;
         if (!a.force_rescreen && ok1) {
             if ((int64_t)m.k1 - (int64_t)m.k2 > T) {
                 label = m.i1;
@@ -819,18 +823,18 @@ __device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bo
                 const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
                 const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
                 label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
-                atomicAdd(a.stats + kStatRefine2, 1ull);
+                refined = true;
             }
         }
-        if (label >= 0) {
-            a.labels[row] = label;
-        } else {
-            // past the list's capacity the two-plane screen takes every row
-            const uint32_t slot = atomicAdd(const_cast<uint32_t *>(a.list_cnt), 1u);
-            if (slot < (uint64_t)a.list_cap) const_cast<int32_t *>(a.list)[slot] = (int32_t)row;
-            atomicAdd(a.stats + kStatRescreen, 1ull);
-        }
+        if (label >= 0) a.labels[row] = label;
     }
+    // statistics and list slots: one atomic per wave; past the list's
+    // capacity the two-plane screen takes every row
+    const bool listed = rvalid && h == 0 && label < 0;
+    wave_count(a.stats + kStatRefine2, refined);
+    wave_count(a.stats + kStatRescreen, listed);
+    const uint32_t slot = wave_append(const_cast<uint32_t *>(a.list_cnt), listed);
+    if (listed && slot < (uint64_t)a.list_cap) const_cast<int32_t *>(a.list)[slot] = (int32_t)row;
 }
 
 // Row blocks of 32 rows per wave in the single-plane screen: three at

@@ -116,6 +116,47 @@ inline int __any(int p)
     return r;
 }
 
+inline unsigned long long __ballot(int p)
+{
+    emu::Wave &w = emu::wave();
+    w.buf[emu::lane()][0] = p ? 1 : 0;
+    w.bar->arrive_and_wait();
+    unsigned long long r = 0;
+    for (int i = 0; i < 64; ++i) r |= (unsigned long long)w.buf[i][0] << i;
+    w.bar->arrive_and_wait();
+    return r;
+}
+
+template <typename T>
+inline T __shfl(T v, int src)
+{
+    static_assert(sizeof(T) <= 128, "");
+    emu::Wave &w = emu::wave();
+    memcpy(w.buf[emu::lane()], &v, sizeof(T));
+    w.bar->arrive_and_wait();
+    T r;
+    memcpy(&r, w.buf[src & 63], sizeof(T));
+    w.bar->arrive_and_wait();
+    return r;
+}
+
+inline int __ffsll(unsigned long long m) { return __builtin_ffsll((long long)m); }
+inline int __popcll(unsigned long long m) { return __builtin_popcountll(m); }
+
+// lanes below this one among the mask's low (lanes 0-31) and high (32-63) halves
+inline unsigned __builtin_amdgcn_mbcnt_lo(unsigned m, unsigned acc)
+{
+    const int l = emu::lane();
+    const unsigned below = l >= 32 ? 0xFFFFFFFFu : ((1u << l) - 1u);
+    return acc + (unsigned)__builtin_popcount(m & below);
+}
+inline unsigned __builtin_amdgcn_mbcnt_hi(unsigned m, unsigned acc)
+{
+    const int l = emu::lane();
+    const unsigned below = l < 32 ? 0u : ((1u << (l - 32)) - 1u);
+    return acc + (unsigned)__builtin_popcount(m & below);
+}
+
 typedef int emu_i32x4 __attribute__((ext_vector_type(4)));
 typedef int emu_i32x16 __attribute__((ext_vector_type(16)));
 
