@@ -335,15 +335,31 @@ __global__ __launch_bounds__(kRThreads) void hist1_kernel(const uint8_t *__restr
                                                           const uint32_t *__restrict__ sbstart, int64_t R1,
                                                           uint32_t *__restrict__ cnt1)
 {
-    __shared__ uint32_t h[256];
+    __shared__ uint32_t h[4][256];  // one histogram per wave
     int bucket;
     int64_t lo, hi;
     if (!locate_sub(sbstart, astart, R1, blockIdx.x, bucket, lo, hi)) return;
-    h[threadIdx.x] = 0;
+    const int wave = threadIdx.x >> 6;
+    for (int w = 0; w < 4; ++w) h[w][threadIdx.x] = 0;
     __syncthreads();
-    for (int64_t r = lo + threadIdx.x; r < hi; r += kRThreads) atomicAdd(&h[tmp_lo[r]], 1u);
+    // 16-byte loads over the aligned middle, single bytes at the two ends
+    const int64_t a0 = min(hi, (lo + 15) & ~(int64_t)15);
+    const int64_t a1 = max(a0, hi & ~(int64_t)15);
+    for (int64_t r = lo + threadIdx.x; r < a0; r += kRThreads) atomicAdd(&h[wave][tmp_lo[r]], 1u);
+    for (int64_t r = a1 + threadIdx.x; r < hi; r += kRThreads) atomicAdd(&h[wave][tmp_lo[r]], 1u);
+    const uint4 *v = reinterpret_cast<const uint4 *>(tmp_lo + a0);
+    const int64_t n16 = (a1 - a0) >> 4;
+    for (int64_t i = threadIdx.x; i < n16; i += kRThreads) {
+        const uint4 w4 = v[i];
+        const uint32_t ws[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) atomicAdd(&h[wave][(ws[k] >> (8 * b)) & 0xFFu], 1u);
+    }
     __syncthreads();
-    cnt1[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
+    cnt1[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[0][threadIdx.x] + h[1][threadIdx.x] + h[2][threadIdx.x] +
+                                                    h[3][threadIdx.x];
 }
 
 // Per bucket b and low byte d: prefix of cnt1 over the bucket's sub-blocks;
