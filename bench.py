@@ -494,6 +494,7 @@ def bench_next_rows(ctx, x, cent, prev, km):
     q = dev(synth.uniform_mixture_route(C, 10000, D, seed=0)["queries"])
     probes, _ = ivf.ivf_route(ctx, q, cent, 64, want_dist=False)
     out["adc_scan"] = bench_adc(ctx, q, cent, probes, off, perm, codes, cb)
+    out["adc_scan_zipf"] = bench_adc_zipf(ctx, q, cent, codes, cb)
     full_ms = km["per_iteration"][-1]["screen_single_plane_ms"] + km["per_iteration"][-1]["screen_two_planes_ms"]
     out["assign_graph"] = bench_assign_graph(ctx, x, cent, prev, full_ms)
     out["assign_cells"] = bench_assign_cells(ctx, x, cent, lab, full_ms)
@@ -585,6 +586,39 @@ def bench_adc(ctx, queries, cent, probes, offsets, perm, codes, cb, k=512):
     t = _timed(ctx, fn)
     return {"queries": Q, "nprobe": P, "k": k, "subspaces": codes.shape[1], "codes_scanned": int(lens),
             "ms": t, "queries_per_s": Q / (t * 1e-3), "codes_per_s": lens / (t * 1e-3)}
+
+
+def bench_adc_zipf(ctx, queries, cent, codes, cb, k=512, P=64, skew=1.0):
+    """The same scan over a Zipf-skewed list layout (list sizes ~ 1/rank over
+    the 65,536 lists, so the largest holds about 8 % of the codes): the
+    codes are reassigned to seeded Zipf labels, and every query probes 64
+    distinct random lists. Median of 3 calls."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    N = codes.shape[0]
+    C = cent.shape[0]
+    lab = synth.random_labels(N, C, seed=7, skew=skew)
+    perm = dev(np.argsort(lab, kind="stable").astype(np.int32))
+    cnt = np.bincount(lab, minlength=C)
+    off = dev(np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64))
+    rng = np.random.default_rng(8)
+    Q = queries.shape[0]
+    probes = dev(np.stack([rng.choice(C, P, replace=False) for _ in range(Q)]).astype(np.int32))
+    out_ids = torch.empty((Q, k), dtype=torch.int32, device=queries.device)
+    out_d = torch.empty((Q, k), dtype=torch.float32, device=queries.device)
+    fn = lambda: ivf.ivf_adc_scan(ctx, queries, cent, probes, off, perm, codes, cb, k, out_ids=out_ids,
+                                  out_dist=out_d)
+    fn()
+    torch.cuda.synchronize()
+    lens = (off[1:] - off[:-1])[probes.long()].sum().item()
+    t = _timed(ctx, fn)
+    return {"queries": Q, "nprobe": P, "k": k, "lists": C, "zipf_exponent": skew,
+            "largest_list": int(cnt.max()), "codes_scanned": int(lens), "ms": t,
+            "queries_per_s": Q / (t * 1e-3), "codes_per_s": lens / (t * 1e-3)}
 
 
 def bench_assign_graph(ctx, x, cent, prev, full_ms, S=8):

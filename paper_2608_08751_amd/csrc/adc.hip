@@ -1,7 +1,8 @@
 // Residual-PQ approximate-distance scan on gfx950 (Sec. "Residual-PQ
 // Candidate Reduction": lookup tables and ADC sums; Sec. "Compact PQ-Code
-// Offloading": chunked scan with local top-K, hierarchical merge to a
-// bounded per-query handoff of N_rerank candidates).
+// Offloading": GPU-side task setup, chunked scan with local top-K, fused
+// first merge, hierarchical merge to a bounded per-query handoff of N_rerank
+// candidates).
 //
 // For query b and probed list l: r = q - c_l (fp32), LUT[m][j] = the fp64
 // distance of the contract between r^(m) and codeword j of subspace m,
@@ -10,20 +11,37 @@
 // with candidate id perm[p]. Candidates are ordered by (d~, id) through one
 // 64-bit key: (order-preserving bits of d~) << 32 | id.
 //
-// Level 1 (adc_list_kernel): one workgroup per (query, probe slot) builds
-// the LUT in LDS, scans the list in chunks of kAdcChunk codes and keeps its
-// k smallest keys in an LDS pool (an exact MSD radix select trims the pool
-// whenever it holds more than k), then hands them to the workspace. Level 2
-// (adc_merge_kernel): one workgroup per query runs the same pool over its
-// P * k handed-over keys and sorts the k smallest. Ids are unique within a
-// query (lists are disjoint), so "the k smallest keys" is exact.
+// Work decomposition. Every probed list is cut into chunks of kAdcChunk
+// codes (the last one partial); the chunks of a list are taken in runs of
+// G_b (the group size of query b, max(kAdcMinGroup, ceil(chunks_b / P))), so a
+// short list is one group and a long one is spread over several groups, and a
+// query has at most 2P groups (the workspace holds 2P * k handoff keys per
+// query).
+//   adc_setup_kernel   one workgroup per query: the chunk counts of its
+//                      probed lists, G_b, the groups of every list and their
+//                      exclusive scan over the probes (each group's slot),
+//                      and one descriptor per group (list, code range);
+//   adc_group_kernel   one workgroup per group slot (slots past the query's
+//                      group count return at once): builds the list's LUT,
+//                      scans the group's chunks and keeps the k smallest keys
+//                      in an LDS pool (an exact MSD radix select trims it
+//                      whenever it holds more than k), then hands over those k
+//                      keys: the chunk scan and the first merge are one
+//                      kernel, chunk-level candidates never leave LDS;
+//   adc_merge_kernel   one workgroup per query merges its groups' keys into
+//                      the k smallest and sorts them.
+// Ids are unique within a query (lists are disjoint), so "the k smallest
+// keys" is exact whatever the grouping.
 #include "ivf_internal.h"
+
+#include <algorithm>
 
 namespace ivf {
 namespace {
 
 constexpr int kAdcThreads = 256;
-constexpr int kAdcChunk = 1024;                          // codes appended per round
+constexpr int kAdcChunk = 1024;                          // codes per chunk (appended per round)
+constexpr int kAdcMinGroup = 8;                          // chunks per group at least
 constexpr int kAdcPool = kAdcMaxK + kAdcChunk;            // LDS pool capacity (keys)
 constexpr int kAdcKeysPerThread = kAdcPool / kAdcThreads;
 constexpr uint64_t kNoKey = ~0ull;
@@ -115,50 +133,126 @@ __device__ void pool_trim(PoolLds &P, int k)
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kAdcThreads) void adc_list_kernel(
-    const float *__restrict__ Q, int D, const float *__restrict__ cent, int64_t C,
-    const int32_t *__restrict__ probes, int P, const int64_t *__restrict__ offsets,
-    const uint32_t *__restrict__ perm, int64_t N, const uint8_t *__restrict__ codes, int M,
-    const float *__restrict__ codebooks, int k, uint64_t *__restrict__ handoff)
+// Positions [o0, o1) of list l, kept inside [0, N) whatever the offsets hold;
+// an id outside [0, C) is an empty list.
+__device__ __forceinline__ void list_range(const int64_t *__restrict__ offsets, int64_t C, int64_t N, int32_t l,
+                                           int64_t &o0, int64_t &o1)
+{
+    if (l < 0 || l >= C) {
+        o0 = o1 = 0;
+        return;
+    }
+    o0 = min(max(offsets[l], (int64_t)0), N);
+    o1 = min(max(offsets[l + 1], o0), N);
+}
+
+// Task setup of query b: the group size, the groups of each probed list
+// (prefix over the probes gives each group's slot j < 2P), and for every
+// group its list and code range: dl[b][j], dpos[b][j] = (first, end).
+__global__ __launch_bounds__(kAdcThreads) void adc_setup_kernel(const int32_t *__restrict__ probes, int P,
+                                                                const int64_t *__restrict__ offsets, int64_t C,
+                                                                int64_t N, int32_t *__restrict__ gcnt,
+                                                                int32_t *__restrict__ dl,
+                                                                longlong2 *__restrict__ dpos)
+{
+    __shared__ int32_t wsum[kAdcThreads / 64];
+    __shared__ int32_t s_g;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t b = blockIdx.x;
+    // thread t takes the contiguous probes [t * per, (t + 1) * per)
+    const int per = (P + kAdcThreads - 1) / kAdcThreads;  // <= 16
+    int32_t nch[16];
+    int64_t o0s[16], o1s[16];
+    int32_t tot = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int p = t * per + e;
+        nch[e] = 0;
+        o0s[e] = o1s[e] = 0;
+        if (e < per && p < P) {
+            list_range(offsets, C, N, probes[b * P + p], o0s[e], o1s[e]);
+            nch[e] = (int32_t)((o1s[e] - o0s[e] + kAdcChunk - 1) / kAdcChunk);
+        }
+        tot += nch[e];
+    }
+    // chunks of the query -> group size
+    int32_t s = tot;
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) wsum[wave] = s;
+    __syncthreads();
+    if (t == 0) {
+        int32_t n = 0;
+        for (int w = 0; w < kAdcThreads / 64; ++w) n += wsum[w];
+        s_g = max(kAdcMinGroup, (n + P - 1) / P);
+    }
+    __syncthreads();
+    const int32_t G = s_g;
+    // groups per list and their exclusive scan over the probes
+    int32_t ng = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ng += (nch[e] + G - 1) / G;
+    int32_t incl = ng;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int32_t up = __shfl_up(incl, o);
+        if (lane >= o) incl += up;
+    }
+    __syncthreads();
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int32_t j = incl - ng;
+    for (int w = 0; w < wave; ++w) j += wsum[w];
+    const int64_t base = b * 2 * (int64_t)P;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        if (nch[e] == 0) continue;
+        const int32_t l = probes[b * P + t * per + e];
+        for (int64_t f = o0s[e]; f < o1s[e]; f += (int64_t)G * kAdcChunk, ++j) {
+            dl[base + j] = l;
+            dpos[base + j] = make_longlong2(f, min(o1s[e], f + (int64_t)G * kAdcChunk));
+        }
+    }
+    if (t == kAdcThreads - 1) gcnt[b] = j;  // the last thread ends past every group
+}
+
+// Group slot (b, j) of every query (grid B * 2P).
+__global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
+    const float *__restrict__ Q, int D, const float *__restrict__ cent, int P, const uint32_t *__restrict__ perm,
+    const uint8_t *__restrict__ codes, int M, const float *__restrict__ codebooks, int k,
+    const int32_t *__restrict__ gcnt, const int32_t *__restrict__ dl, const longlong2 *__restrict__ dpos,
+    uint64_t *__restrict__ handoff)
 {
     extern __shared__ float dyn[];  // r [D] then LUT [M][256]
     __shared__ PoolLds pool;
     float *r = dyn;
     float *lut = dyn + D;
     const int t = threadIdx.x;
-    const int64_t b = blockIdx.x / P;
-    const int s = (int)(blockIdx.x - b * P);
-    uint64_t *out = handoff + (int64_t)blockIdx.x * k;
-    const int32_t l = probes[b * P + s];
-    if (l < 0 || l >= C) {  // not a list: hand over nothing
-        for (int i = t; i < k; i += kAdcThreads) out[i] = kNoKey;
-        return;
-    }
+    const int64_t b = blockIdx.x / (2 * P);
+    const int j = (int)(blockIdx.x - b * 2 * P);
+    if (j >= gcnt[b]) return;  // no such group
+    const int64_t slot = b * 2 * (int64_t)P + j;
+    const int32_t l = dl[slot];
+    const longlong2 range = dpos[slot];
     const int dsub = D / M;
     for (int d = t; d < D; d += kAdcThreads) r[d] = Q[b * D + d] - cent[(int64_t)l * D + d];
     if (t == 0) pool.n = 0;
     __syncthreads();
     for (int e = t; e < M * kPqK; e += kAdcThreads) {
-        const int m = e >> 8;
-        const float *w = codebooks + (int64_t)e * dsub;
-        const float *rm = r + m * dsub;
+        const float *wr = codebooks + (int64_t)e * dsub;
+        const float *rm = r + (e >> 8) * dsub;
         double acc = 0.0;
         for (int d = 0; d < dsub; ++d) {
-            const double u = (double)rm[d] - (double)w[d];
-            acc = fma(u, u, acc);
+            const double v = (double)rm[d] - (double)wr[d];
+            acc = fma(v, v, acc);
         }
         lut[e] = (float)acc;
     }
     __syncthreads();
-    // positions of list l, kept inside [0, N) whatever the offsets hold
-    const int64_t o0 = min(max(offsets[l], (int64_t)0), N);
-    const int64_t o1 = min(max(offsets[l + 1], o0), N);
-    for (int64_t c0 = o0; c0 < o1; c0 += kAdcChunk) {
-        const int len = (int)min((int64_t)kAdcChunk, o1 - c0);
+    for (int64_t c0 = range.x; c0 < range.y; c0 += kAdcChunk) {
+        const int len = (int)min((int64_t)kAdcChunk, range.y - c0);
         const int base = (int)pool.n;
         for (int i = t; i < len; i += kAdcThreads) {
-            const int64_t p = c0 + i;
-            const uint8_t *a = codes + p * M;
+            const int64_t pos = c0 + i;
+            const uint8_t *a = codes + pos * M;
             float acc = 0.0f;
             if ((M & 3) == 0) {
                 for (int m = 0; m < M; m += 4) {
@@ -171,26 +265,27 @@ __global__ __launch_bounds__(kAdcThreads) void adc_list_kernel(
             } else {
                 for (int m = 0; m < M; ++m) acc = acc + lut[m * kPqK + a[m]];
             }
-            pool.key[base + i] = ((uint64_t)f2o(acc) << 32) | perm[p];
+            pool.key[base + i] = ((uint64_t)f2o(acc) << 32) | perm[pos];
         }
         __syncthreads();
         if (t == 0) pool.n = (uint32_t)(base + len);
         __syncthreads();
         if ((int)pool.n > k) pool_trim(pool, k);
     }
+    uint64_t *out = handoff + slot * k;
     const int n = (int)pool.n;
     for (int i = t; i < k; i += kAdcThreads) out[i] = i < n ? pool.key[i] : kNoKey;
 }
 
 __global__ __launch_bounds__(kAdcThreads) void adc_merge_kernel(const uint64_t *__restrict__ handoff,
-                                                               int P, int k, uint32_t *__restrict__ ids,
-                                                               float *__restrict__ dist)
+                                                               int P, int k, const int32_t *__restrict__ gcnt,
+                                                               uint32_t *__restrict__ ids, float *__restrict__ dist)
 {
     __shared__ PoolLds pool;
     const int t = threadIdx.x;
     const int64_t b = blockIdx.x;
-    const uint64_t *in = handoff + b * (int64_t)P * k;
-    const int64_t total = (int64_t)P * k;
+    const uint64_t *in = handoff + b * 2 * (int64_t)P * k;
+    const int64_t total = (int64_t)gcnt[b] * k;  // the query's groups
     if (t == 0) pool.n = 0;
     __syncthreads();
     for (int64_t c0 = 0; c0 < total; c0 += kAdcChunk) {
@@ -238,15 +333,19 @@ __global__ __launch_bounds__(kAdcThreads) void adc_merge_kernel(const uint64_t *
 hipError_t launch_adc_scan(const float *Q, int64_t B, int D, const float *cent, int64_t C,
                            const int32_t *probes, int P, const int64_t *offsets, const uint32_t *perm,
                            int64_t N, const uint8_t *codes, int M, const float *codebooks, int k,
-                           uint64_t *handoff, uint32_t *ids, float *dist, hipStream_t s)
+                           const AdcScratch &w, uint32_t *ids, float *dist, hipStream_t s)
 {
     if (B <= 0) return hipSuccess;
-    const size_t lds = (size_t)(D + M * kPqK) * sizeof(float);
-    hipLaunchKernelGGL(adc_list_kernel, dim3((unsigned)(B * P)), dim3(kAdcThreads), lds, s, Q, D, cent, C,
-                       probes, P, offsets, perm, N, codes, M, codebooks, k, handoff);
+    hipLaunchKernelGGL(adc_setup_kernel, dim3((unsigned)B), dim3(kAdcThreads), 0, s, probes, P, offsets, C, N,
+                       w.gcnt, w.dl, w.dpos);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(adc_merge_kernel, dim3((unsigned)B), dim3(kAdcThreads), 0, s, handoff, P, k, ids, dist);
+    const size_t lds = (size_t)(D + M * kPqK) * sizeof(float);
+    hipLaunchKernelGGL(adc_group_kernel, dim3((unsigned)(B * 2 * P)), dim3(kAdcThreads), lds, s, Q, D, cent, P,
+                       perm, codes, M, codebooks, k, w.gcnt, w.dl, w.dpos, w.handoff);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(adc_merge_kernel, dim3((unsigned)B), dim3(kAdcThreads), 0, s, w.handoff, P, k, w.gcnt,
+                       ids, dist);
     return hipGetLastError();
 }
 

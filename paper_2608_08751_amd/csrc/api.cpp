@@ -115,6 +115,20 @@ struct Carver {
     }
 };
 
+// Workspace of ivf_adc_scan for B queries, P probes, handoff k (layout only
+// when base is null); returns the bytes used.
+size_t layout_adc(void *base, int64_t B, int64_t P, int64_t k, AdcScratch *w)
+{
+    Carver c(base);
+    AdcScratch s;
+    s.handoff = c.take<uint64_t>((size_t)B * 2 * P * k);
+    s.dl = c.take<int32_t>((size_t)B * 2 * P);
+    s.dpos = c.take<longlong2>((size_t)B * 2 * P);
+    s.gcnt = c.take<int32_t>((size_t)B);
+    if (w) *w = s;
+    return c.off + kAlign;
+}
+
 // Scalar area at the start of every workspace: [0] max centroid norm bits,
 // [1] worklist counter, [2] nonzero when some centroid does not quantise for
 // the int8 screen, [3] the same for its single plane, [4] the single plane's
@@ -604,8 +618,8 @@ size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k
     case IVF_OP_BUILD_LISTS:
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, 0, true, false, num_cus).bytes;
     case IVF_OP_ADC_SCAN:  // rows = B, C = P (probes per query), k = handoff
-        if (k < 1 || k > kAdcMaxK || C > kMaxAdcProbes) return 0;
-        return (size_t)rows * (size_t)C * (size_t)k * sizeof(uint64_t) + 256;
+        if (k < 1 || k > kAdcMaxK || C < 1 || C > kMaxAdcProbes) return 0;
+        return layout_adc(nullptr, rows, C, k, nullptr);
     case IVF_OP_PQ_TRAIN_STEP:  // C = M
         if (C > kMaxD) return 0;
         return layout_pq(nullptr, std::max<int64_t>(rows, 1), (int)C, num_cus).bytes;
@@ -1191,14 +1205,14 @@ ivf_status ivf_adc_scan(ivf_ctx *ctx, const float *queries, int64_t B, int32_t D
         for (int j = 0; j < 7; ++j)
             if (overlap(outs[i], ob, ins[j], ib[j])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
     if (overlap(out_ids, ob, out_dist, ob)) return fail(ctx, IVF_EINVAL, "outputs overlap");
-    const size_t need = (size_t)B * P * k * sizeof(uint64_t) + 256;
+    const size_t need = layout_adc(nullptr, B, P, k, nullptr);
     if ((st = check_ws(ctx, need)) != IVF_OK) return st;
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
-    Carver c(ctx->ws);
-    uint64_t *handoff = c.take<uint64_t>((size_t)B * P * k);
+    AdcScratch w;
+    layout_adc(ctx->ws, B, P, k, &w);
     TIMED("adc_scan", launch_adc_scan(queries, B, D, centroids, C, probes, P, offsets, perm, N, codes, M,
-                                      codebooks, k, handoff, out_ids, out_dist, ctx->stream));
+                                      codebooks, k, w, out_ids, out_dist, ctx->stream));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

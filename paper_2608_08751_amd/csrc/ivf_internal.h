@@ -248,11 +248,19 @@ hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const f
 constexpr int kAdcMaxK = 1024;   // handoff per query (N_rerank)
 constexpr int kAdcMaxM = 60;     // subspaces (LUT of M x 256 floats in LDS, < 64 KiB)
 constexpr int kMaxAdcProbes = 4096;
-// handoff: [B * P * k] uint64 workspace; ids/dist [B, k].
+// Workspace of the scan: at most 2P groups per query, each with a handoff of
+// k keys and a descriptor (list id, code range), and each query's group count.
+struct AdcScratch {
+    uint64_t *handoff;  // [B * 2P * k]
+    int32_t *dl;        // [B * 2P] list of the group
+    longlong2 *dpos;    // [B * 2P] first and end code position of the group
+    int32_t *gcnt;      // [B] groups of the query
+};
+// ids/dist [B, k].
 hipError_t launch_adc_scan(const float *Q, int64_t B, int D, const float *cent, int64_t C,
                            const int32_t *probes, int P, const int64_t *offsets, const uint32_t *perm,
                            int64_t N, const uint8_t *codes, int M, const float *codebooks, int k,
-                           uint64_t *handoff, uint32_t *ids, float *dist, hipStream_t s);
+                           const AdcScratch &w, uint32_t *ids, float *dist, hipStream_t s);
 
 // ---- fp32 MFMA throughput probe (probe.hip) ---------------------------------
 // Enqueues the probe kernel for `iters` rounds; *flops = the work it does.

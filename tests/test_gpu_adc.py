@@ -71,6 +71,37 @@ def test_adc_scan_exact(ivf_ctx, oracle_mod, B, C, D, M, N, P, k, skew):
     assert (dist.view(np.uint32) == odist.view(np.uint32)).all()
 
 
+@pytest.mark.parametrize("B,C,D,M,N,P,k,skew", [
+    (3, 8, 64, 16, 120000, 4, 512, 2.0),      # one list far longer than the rest: spread over groups
+    (4, 6, 32, 8, 60000, 1, 256, 0.0),        # one probe: a single group of every chunk
+    (5, 2000, 64, 16, 200000, 64, 512, 1.2),  # Zipf-skewed lists, 64 probes
+    (2, 5, 32, 8, 50000, 5, 1000, 0.0),       # every list probed
+])
+def test_adc_scan_chunk_groups(ivf_ctx, oracle_mod, B, C, D, M, N, P, k, skew):
+    """Lists cut into 1,024-code chunks and grouped per query (at most P
+    groups): long lists spread over several groups, many short lists
+    packed into one."""
+    q, c, probes, off, perm, codes, cb = setup(7 * B + C + N, B, C, D, M, N, P, skew)
+    ids, dist = gpu_adc(ivf_ctx, q, c, probes, off, perm, codes, cb, k)
+    oids, odist = oracle_mod.adc_scan(q, c, probes, off, perm, codes, cb, k)
+    assert (ids == oids).all()
+    assert (dist.view(np.uint32) == odist.view(np.uint32)).all()
+
+
+def test_adc_scan_queries_without_candidates(ivf_ctx, oracle_mod):
+    """Queries whose probed lists are all empty or invalid have no chunk and
+    no group; their handoff is all padding."""
+    q, c, probes, off, perm, codes, cb = setup(11, 4, 50, 32, 8, 5000, 3)
+    probes[0, :] = -1
+    off[7] = off[8] = off[6]  # list 7 empty (offsets stay non-decreasing)
+    off[9:] = np.maximum(off[9:], off[8])
+    probes[1, :] = [7, -5, 51]
+    ids, dist = gpu_adc(ivf_ctx, q, c, probes, off, perm, codes, cb, 64)
+    oids, odist = oracle_mod.adc_scan(q, c, probes, off, perm, codes, cb, 64)
+    assert (ids == oids).all() and (dist.view(np.uint32) == odist.view(np.uint32)).all()
+    assert (ids[:2] == 0xFFFFFFFF).all() and np.isinf(dist[:2]).all()
+
+
 def test_adc_scan_invalid_probes(ivf_ctx, oracle_mod):
     q, c, probes, off, perm, codes, cb = setup(5, 6, 40, 32, 8, 10000, 6)
     probes[:, 2] = -1
