@@ -497,7 +497,7 @@ def bench_next_rows(ctx, x, cent, prev, km):
     out["adc_scan_zipf"] = bench_adc_zipf(ctx, q, cent, codes, cb)
     full_ms = km["per_iteration"][-1]["screen_single_plane_ms"] + km["per_iteration"][-1]["screen_two_planes_ms"]
     out["assign_graph"] = bench_assign_graph(ctx, x, cent, prev, full_ms)
-    out["assign_cells"] = bench_assign_cells(ctx, x, cent, lab, full_ms)
+    out["assign_cells"] = bench_assign_cells(ctx)
     return out
 
 
@@ -648,46 +648,60 @@ def bench_assign_graph(ctx, x, cent, prev, full_ms, S=8):
 
 
 
-def bench_assign_cells(ctx, x, cent, exact, full_ms, G=1024, S=8, hops=8):
+def bench_assign_cells(ctx, N=10_000_000, G=1024, S=8, hops=8):
     """Candidates for rows without a previous label (graph-assisted assignment
-    of the base set): a coarse table of 1,024 centroids (three Lloyd steps
-    over the centroid table), the cells of the centroids and of the rows
-    against it (ivf_assign_build), the 8-nearest-centroid graph, then the
-    nearest member of each row's cell and up to 8 greedy graph moves. Median
-    of 3 calls of each timed part; agreement with the exact labels."""
+    of the base set) on the assign-build workload's generator: 10M base rows,
+    the 65,536 mixture means as centroids. A coarse table of 1,024 centroids
+    (three Lloyd steps over the centroid table), the cells of the centroids
+    and of the rows against it (ivf_assign_build), the 8-nearest-centroid
+    graph, then the nearest member of each row's cell and up to 8 greedy
+    graph moves, rows taken in cell order. Median of 3 calls of each timed
+    part; agreement with, and time against, the exact assignment of the same
+    rows."""
     import torch
 
     import synth
     import paper_2608_08751_amd as ivf
 
-    N, D = x.shape
-    C = cent.shape[0]
+    C, D = C_BIG, D_U8
+    cent = dev(synth.uniform_means(C, D, seed=0))
+    x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
+    synth.device_mixture_rows_u8(cent, 0, N, x, seed=0)
+    exact, _, _, _ = ivf.ivf_assign_build(ctx, x, cent)
+    t_full = _timed(ctx, lambda: ivf.ivf_assign_build(ctx, x, cent, out_labels=exact))
     coarse = cent[dev(synth.kmeans_init(C, G, seed=1))].contiguous()
     t_coarse = 0.0
     for it in range(3):
         t_coarse += _timed(ctx, lambda: ivf.ivf_kmeans_step(ctx, cent, coarse, seed=1, it=it), reps=1)
         _, coarse, _, _ = ivf.ivf_kmeans_step(ctx, cent, coarse, seed=1, it=it)
-    _, _, c_off, c_mem = ivf.ivf_assign_build(ctx, cent, coarse)
+    _, c_cnt, c_off, c_mem = ivf.ivf_assign_build(ctx, cent, coarse)
     t_members = _timed(ctx, lambda: ivf.ivf_assign_build(ctx, cent, coarse))
     graph, _ = ivf.ivf_route(ctx, cent, cent, S, want_dist=False)
     t_graph = _timed(ctx, lambda: ivf.ivf_route(ctx, cent, cent, S, out_ids=graph, want_dist=False))
-    cell = torch.empty(N, dtype=torch.int32, device=x.device)
-    t_cell = _timed(ctx, lambda: ivf.ivf_kmeans_step(ctx, x, coarse, seed=1, it=0, out_labels=cell))
+    cell, _, _, by_cell = ivf.ivf_assign_build(ctx, x, coarse)
+    t_cell = _timed(ctx, lambda: ivf.ivf_assign_build(ctx, x, coarse, out_labels=cell, out_perm=by_cell))
     lab = torch.empty(N, dtype=torch.int32, device=x.device)
     dist = torch.empty(N, dtype=torch.float32, device=x.device)
-    fn = lambda: ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, graph, hops, out_labels=lab,
-                                      out_dist=dist)
+    fn = lambda: ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, graph, hops, order=by_cell,
+                                      out_labels=lab, out_dist=dist)
     fn()
     torch.cuda.synchronize()
     t = _timed(ctx, fn)
     agree = float((lab == exact).float().mean())
-    ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, None, 0, out_labels=lab, out_dist=dist)
+    ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, None, 0, order=by_cell, out_labels=lab,
+                         out_dist=dist)
     agree0 = float((lab == exact).float().mean())
+    members_per_row = float(c_cnt[cell.long()].double().mean())
     per_row = t + t_cell
-    return {"rows": N, "centroids": C, "cells": G, "degree": S, "hops": hops, "coarse_train_ms": t_coarse,
-            "members_ms": t_members, "graph_ms": t_graph, "row_cells_ms": t_cell, "assign_ms": t,
-            "rows_per_s": N / (per_row * 1e-3), "agreement_with_exact": agree,
-            "agreement_first_choice_only": agree0, "speedup_vs_full_assignment": full_ms / per_row}
+    out = {"rows": N, "centroids": C, "cells": G, "degree": S, "hops": hops, "coarse_train_ms": t_coarse,
+           "members_ms": t_members, "graph_ms": t_graph, "row_cells_ms": t_cell, "assign_ms": t,
+           "members_per_cell_max": int(c_cnt.max()), "members_per_row_mean": members_per_row,
+           "rows_per_s": N / (per_row * 1e-3), "agreement_with_exact": agree,
+           "agreement_first_choice_only": agree0, "exact_assignment_ms": t_full,
+           "speedup_vs_exact_assignment": t_full / per_row}
+    del x
+    torch.cuda.empty_cache()
+    return out
 
 
 if __name__ == "__main__":

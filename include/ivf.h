@@ -299,6 +299,12 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
  *   cell_members  [M] uint32 centroid ids grouped by cell (may be NULL when M = 0)
  *   graph         [C, S] int32 or NULL (no walk), 1 <= S <= 64
  *   hops          0 <= hops <= 1024
+ *   order         [N] uint32 processing order, or NULL (row order): results
+ *                 do not depend on it, speed does (rows of one cell next to
+ *                 each other share their members' loads; the permutation
+ *                 from ivf_assign_build of the rows against the coarse table
+ *                 is that order). Entries >= N are skipped; a row that order
+ *                 does not list keeps whatever out_labels/out_dist held.
  *   out_labels    [N] int32;  out_dist [N] fp32 squared distance or NULL
  * No workspace. Errors: IVF_EINVAL (sizes, NULL pointers, misalignment,
  * aliasing), IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */
@@ -306,7 +312,7 @@ ivf_status ivf_assign_cells(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
                             const float *centroids, int64_t C, int32_t D, const int32_t *cell,
                             int64_t G, const int64_t *cell_offsets, const uint32_t *cell_members,
                             int64_t M, const int32_t *graph, int32_t S, int32_t hops,
-                            int32_t *out_labels, float *out_dist);
+                            const uint32_t *order, int32_t *out_labels, float *out_dist);
 
 /* List-major layout of the base vectors and their residuals (Sec. "List-major
  * contiguous scans": every IVF list is one contiguous range; Sec.

@@ -46,7 +46,7 @@ SIGNATURES = [
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
-    ("ivf_assign_cells", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I64, _P, _P, _I64, _P, _I32, _I32, _P, _P]),
+    ("ivf_assign_cells", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I64, _P, _P, _I64, _P, _I32, _I32, _P, _P, _P]),
     ("ivf_adc_scan", _INT, [_P, _P, _I64, _I32, _P, _I64, _P, _I32, _P, _P, _I64, _P, _I32, _P, _I32, _P, _P]),
     ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
 ]
@@ -398,10 +398,11 @@ def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None
 
 
 def ivf_assign_cells(ctx: Context, rows, centroids, cell, cell_offsets, cell_members, graph=None, hops: int = 0,
-                     out_labels=None, out_dist=None, want_dist: bool = True):
+                     order=None, out_labels=None, out_dist=None, want_dist: bool = True):
     """Nearest member of each row's coarse cell, then up to `hops` greedy
     moves over graph (int32 [C, S] or None): labels int32 [N] and squared
-    distances fp32 [N]."""
+    distances fp32 [N]. `order` (int32 [N] or None) only sets the processing
+    order."""
     import torch
 
     for t, name in ((rows, "rows"), (centroids, "centroids"), (cell, "cell"), (cell_offsets, "cell_offsets"),
@@ -409,6 +410,8 @@ def ivf_assign_cells(ctx: Context, rows, centroids, cell, cell_offsets, cell_mem
         _device_tensor(t, name)
     if graph is not None:
         _device_tensor(graph, "graph")
+    if order is not None:
+        _device_tensor(order, "order")
     N, D = rows.shape
     C = centroids.shape[0]
     G = cell_offsets.shape[0] - 1
@@ -421,7 +424,8 @@ def ivf_assign_cells(ctx: Context, rows, centroids, cell, cell_offsets, cell_mem
     ctx.bind_stream()
     ctx.check(ctx.lib.ivf_assign_cells(ctx.handle, _ptr(rows), _dtype_code(rows), N, _ptr(centroids), C, D,
                                        _ptr(cell), G, _ptr(cell_offsets), _ptr(cell_members) if M else None, M,
-                                       _ptr(graph) if graph is not None else None, S, hops, _ptr(out_labels),
+                                       _ptr(graph) if graph is not None else None, S, hops,
+                                       _ptr(order) if order is not None else None, _ptr(out_labels),
                                        _ptr(out_dist if want_dist else None)), "ivf_assign_cells")
     return out_labels, (out_dist if want_dist else None)
 

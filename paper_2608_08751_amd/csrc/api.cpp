@@ -1132,7 +1132,7 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N, c
 ivf_status ivf_assign_cells(ivf_ctx *ctx, const void *rows, int dt, int64_t N, const float *centroids,
                             int64_t C, int32_t D, const int32_t *cell, int64_t G, const int64_t *cell_offsets,
                             const uint32_t *cell_members, int64_t M, const int32_t *graph, int32_t S,
-                            int32_t hops, int32_t *out_labels, float *out_dist)
+                            int32_t hops, const uint32_t *order, int32_t *out_labels, float *out_dist)
 {
     if (!ctx) return IVF_EINVAL;
     ctx->err.clear();
@@ -1150,24 +1150,24 @@ ivf_status ivf_assign_cells(ivf_ctx *ctx, const void *rows, int dt, int64_t N, c
     if (!centroids || !cell || !cell_offsets || (M > 0 && !cell_members) || !out_labels)
         return fail(ctx, IVF_EINVAL, "null pointer argument");
     if (!aligned16(centroids) || !aligned16(cell) || !aligned16(cell_offsets) ||
-        (cell_members && !aligned16(cell_members)) || (graph && !aligned16(graph)) || !aligned16(out_labels) ||
-        (out_dist && !aligned16(out_dist)))
+        (cell_members && !aligned16(cell_members)) || (graph && !aligned16(graph)) || (order && !aligned16(order)) ||
+        !aligned16(out_labels) || (out_dist && !aligned16(out_dist)))
         return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
-    const void *ins[6] = {rows, centroids, cell, cell_offsets, cell_members, graph};
-    const size_t ib[6] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)N * 4, (size_t)(G + 1) * 8, (size_t)M * 4,
-                          graph ? (size_t)C * S * 4 : 0};
+    const void *ins[7] = {rows, centroids, cell, cell_offsets, cell_members, graph, order};
+    const size_t ib[7] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)N * 4, (size_t)(G + 1) * 8, (size_t)M * 4,
+                          graph ? (size_t)C * S * 4 : 0, order ? (size_t)N * 4 : 0};
     const void *outs[2] = {out_labels, out_dist};
     const size_t ob[2] = {(size_t)N * 4, (size_t)N * 4};
     for (int i = 0; i < 2; ++i)
-        for (int k = 0; k < 6; ++k)
+        for (int k = 0; k < 7; ++k)
             if (overlap(outs[i], ob[i], ins[k], ib[k])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
     if (overlap(out_labels, ob[0], out_dist, ob[1])) return fail(ctx, IVF_EINVAL, "outputs overlap");
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
     TIMED("assign_cells", launch_assign_cells(rows, rowtype, N, centroids, C, D, cell, G, cell_offsets, cell_members,
-                                              M, graph, graph ? S : 0, hops, out_labels, out_dist, ctx->num_cus,
-                                              ctx->stream));
+                                              M, graph, graph ? S : 0, hops, order, out_labels, out_dist,
+                                              ctx->num_cus, ctx->stream));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

@@ -162,13 +162,19 @@ __global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
     const XT *__restrict__ X, int64_t N, const float *__restrict__ cent, int64_t C, int D,
     const int32_t *__restrict__ cell, int64_t G, const int64_t *__restrict__ offsets,
     const uint32_t *__restrict__ members, int64_t M, const int32_t *__restrict__ graph, int S, int hops,
-    int32_t *__restrict__ labels, float *__restrict__ dist)
+    const uint32_t *__restrict__ order, int32_t *__restrict__ labels, float *__restrict__ dist)
 {
     __shared__ __attribute__((aligned(16))) float xs_all[kAcWaves][kCellsMaxDim];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     float *xs = xs_all[wave];
-    for (int64_t i = (int64_t)blockIdx.x * kAcWaves + wave; i < N; i += (int64_t)gridDim.x * kAcWaves) {
+    // a contiguous range of processing positions per workgroup: with rows in
+    // cell order, consecutive rows of a workgroup read the same members
+    const int64_t per = ((N + gridDim.x - 1) / gridDim.x + kAcWaves - 1) / kAcWaves * kAcWaves;
+    const int64_t p0 = (int64_t)blockIdx.x * per, p1 = min(N, p0 + per);
+    for (int64_t p = p0 + wave; p < p1; p += kAcWaves) {
+        const int64_t i = order ? (int64_t)order[p] : p;
+        if (i >= N) continue;  // not a row
         // the row into this wave's slot; the wave's own LDS operations run in
         // order, the fence keeps the compiler from moving reads above writes
         __builtin_amdgcn_wave_barrier();
@@ -244,8 +250,8 @@ namespace ivf {
 
 hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C, int D,
                                const int32_t *cell, int64_t G, const int64_t *offsets, const uint32_t *members,
-                               int64_t M, const int32_t *graph, int S, int hops, int32_t *labels, float *dist,
-                               int num_cus, hipStream_t s)
+                               int64_t M, const int32_t *graph, int S, int hops, const uint32_t *order,
+                               int32_t *labels, float *dist, int num_cus, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
     const int64_t blocks = (N + kAcWaves - 1) / kAcWaves;
@@ -253,11 +259,11 @@ hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const f
     if (rowtype == kRowU8)
         hipLaunchKernelGGL(assign_cells_kernel<uint8_t>, dim3(grid), dim3(kAcWaves * 64), 0, s,
                            (const uint8_t *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
-                           labels, dist);
+                           order, labels, dist);
     else
         hipLaunchKernelGGL(assign_cells_kernel<float>, dim3(grid), dim3(kAcWaves * 64), 0, s,
                            (const float *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
-                           labels, dist);
+                           order, labels, dist);
     return hipGetLastError();
 }
 

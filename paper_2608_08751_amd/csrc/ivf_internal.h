@@ -241,8 +241,8 @@ hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const f
 constexpr int kCellsMaxDim = 256;
 hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C, int D,
                                const int32_t *cell, int64_t G, const int64_t *offsets, const uint32_t *members,
-                               int64_t M, const int32_t *graph, int S, int hops, int32_t *labels, float *dist,
-                               int num_cus, hipStream_t s);
+                               int64_t M, const int32_t *graph, int S, int hops, const uint32_t *order,
+                               int32_t *labels, float *dist, int num_cus, hipStream_t s);
 
 // ---- residual-PQ ADC scan (adc.hip) -----------------------------------------
 constexpr int kAdcMaxK = 1024;   // handoff per query (N_rerank)

@@ -275,14 +275,17 @@ def test_assign_graph_validation(vctx, lib):
 
 def test_assign_cells_validation(vctx, lib):
     h = vctx.handle
-    rows, cent, cell, off, mem, graph, lab, dist = (P(i * GB) for i in range(8))
+    rows, cent, cell, off, mem, graph, lab, dist, order = (P(i * GB) for i in range(9))
     ok = lambda **k: lib.ivf_assign_cells(h, rows, B.IVF_U8, k.get("N", 1000), cent, 100, k.get("D", 128),
                                           k.get("cell", cell), k.get("G", 10), k.get("off", off),
                                           k.get("mem", mem), k.get("M", 100), k.get("graph", graph),
-                                          k.get("S", 8), k.get("hops", 4), k.get("lab", lab), k.get("dist", dist))
+                                          k.get("S", 8), k.get("hops", 4), k.get("order", order),
+                                          k.get("lab", lab), k.get("dist", dist))
     assert ok() == B.IVF_EDEVICE
     assert ok(graph=None, S=0) == B.IVF_EDEVICE and ok(dist=None) == B.IVF_EDEVICE
-    assert ok(mem=None, M=0) == B.IVF_EDEVICE
+    assert ok(mem=None, M=0) == B.IVF_EDEVICE and ok(order=None) == B.IVF_EDEVICE
+    assert ok(order=P(8 * GB + 4)) == B.IVF_EINVAL  # misaligned
+    assert ok(lab=P(8 * GB + 64)) == B.IVF_EINVAL  # overlaps the order
     assert ok(N=0) == B.IVF_OK
     assert ok(G=0) == B.IVF_EINVAL and ok(M=-1) == B.IVF_EINVAL
     assert ok(hops=-1) == B.IVF_EINVAL and ok(hops=1025) == B.IVF_EINVAL

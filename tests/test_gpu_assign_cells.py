@@ -33,14 +33,15 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def run(ctx, x, c, cell, offsets, members, graph, hops):
+def run(ctx, x, c, cell, offsets, members, graph, hops, order=None):
     import torch
 
     import paper_2608_08751_amd as ivf
 
     lab, dist = ivf.ivf_assign_cells(ctx, to_dev(x), to_dev(c), to_dev(cell.astype(np.int32)),
                                      to_dev(offsets.astype(np.int64)), to_dev(members.view(np.int32)),
-                                     None if graph is None else to_dev(graph.astype(np.int32)), hops)
+                                     None if graph is None else to_dev(graph.astype(np.int32)), hops,
+                                     order=None if order is None else to_dev(order.astype(np.int32)))
     torch.cuda.synchronize()
     return lab.cpu().numpy(), dist.cpu().numpy()
 
@@ -71,10 +72,42 @@ def test_assign_cells_exact(ivf_ctx, oracle_mod, N, C, D, G, S, hops, dt):
     offsets, members = random_cells(rng, C, G)
     graph = rng.integers(0, C, (C, S)).astype(np.int32)
     cell = rng.integers(0, G, N).astype(np.int32)
-    lab, dist = run(ivf_ctx, x, c, cell, offsets, members, graph, hops)
     olab, od = oracle_mod.assign_cells(x, c, cell, offsets, members, graph, hops, return_dist=True)
-    assert (lab == olab).all()
-    assert (dist == od.astype(np.float32)).all()
+    # any processing order gives the same result: row order, a random
+    # permutation, and rows grouped by cell
+    for order in (None, rng.permutation(N), np.argsort(cell, kind="stable")):
+        lab, dist = run(ivf_ctx, x, c, cell, offsets, members, graph, hops, order)
+        assert (lab == olab).all()
+        assert (dist == od.astype(np.float32)).all()
+
+
+def test_assign_cells_order_skips_and_leaves_rows(ivf_ctx, oracle_mod):
+    """Order entries past N are skipped; rows the order does not list keep
+    the output buffer's contents."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    rng = np.random.default_rng(6)
+    N, C, D, G = 500, 40, 32, 5
+    x = rng.integers(0, 256, (N, D)).astype(np.uint8)
+    c = rng.uniform(0, 255, (C, D)).astype(np.float32)
+    offsets, members = random_cells(rng, C, G)
+    cell = rng.integers(0, G, N).astype(np.int32)
+    order = rng.permutation(N).astype(np.int64)
+    order[:7] = N + np.arange(7)  # not rows
+    left = np.setdiff1d(np.arange(N), order)
+    lab = torch.full((N,), -77, dtype=torch.int32, device="cuda")
+    dist = torch.full((N,), 5.0, dtype=torch.float32, device="cuda")
+    ivf.ivf_assign_cells(ivf_ctx, to_dev(x), to_dev(c), to_dev(cell), to_dev(offsets), to_dev(members.view(np.int32)),
+                         None, 0, order=to_dev(order.astype(np.uint32).view(np.int32)), out_labels=lab,
+                         out_dist=dist)
+    torch.cuda.synchronize()
+    olab, od = oracle_mod.assign_cells(x, c, cell, offsets, members, None, 0, return_dist=True)
+    lab, dist = lab.cpu().numpy(), dist.cpu().numpy()
+    done = np.setdiff1d(np.arange(N), left)
+    assert (lab[done] == olab[done]).all() and (dist[done] == od[done].astype(np.float32)).all()
+    assert (lab[left] == -77).all() and (dist[left] == 5.0).all()
 
 
 def test_assign_cells_ties_invalid_and_no_graph(ivf_ctx, oracle_mod):
@@ -133,10 +166,10 @@ def test_assign_cells_base_full_size(ivf_ctx, oracle_mod):
     for it in range(3):
         _, coarse, _, _ = ivf.ivf_kmeans_step(ivf_ctx, cent, coarse, seed=1, it=it)
     _, _, c_off, c_mem = ivf.ivf_assign_build(ivf_ctx, cent, coarse)
-    cell, _, _, _ = ivf.ivf_assign_build(ivf_ctx, x, coarse)
+    cell, _, _, by_cell = ivf.ivf_assign_build(ivf_ctx, x, coarse)
     graph, _ = ivf.ivf_route(ivf_ctx, cent, cent, S)
-    lab, dist = ivf.ivf_assign_cells(ivf_ctx, x, cent, cell, c_off, c_mem, graph, hops)
-    first, fdist = ivf.ivf_assign_cells(ivf_ctx, x, cent, cell, c_off, c_mem, None, 0)
+    lab, dist = ivf.ivf_assign_cells(ivf_ctx, x, cent, cell, c_off, c_mem, graph, hops, order=by_cell)
+    first, fdist = ivf.ivf_assign_cells(ivf_ctx, x, cent, cell, c_off, c_mem, None, 0, order=by_cell)
     exact, _, _, _ = ivf.ivf_assign_build(ivf_ctx, x, cent)
     torch.cuda.synchronize()
     rng = np.random.default_rng(11)
