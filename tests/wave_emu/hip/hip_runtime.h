@@ -36,6 +36,9 @@ struct uint2 {
 struct float4 {
     float x, y, z, w;
 };
+struct longlong2 {
+    long long x, y;
+};
 typedef int hipError_t;
 typedef void *hipStream_t;
 enum { hipSuccess = 0, hipErrorInvalidValue = 1 };
