@@ -53,7 +53,8 @@ def parse():
     ap.add_argument("--rows", type=int, default=10**9, help="rows of the assign-build workload")
     ap.add_argument("--kmeans-rows", type=int, default=10_000_000)
     ap.add_argument("--kmeans-iters", type=int, default=10)
-    ap.add_argument("--only", default="", help="comma-separated subset of 1,2,3,4,5 (profiling runs)")
+    ap.add_argument("--only", default="", help="comma-separated subset of 1,2,3,4,5 and b (the list build "
+                                               "alone on 1e9 labels; profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the NEXT-row kernels")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -424,16 +425,6 @@ def main():
             "roofline": roofline,
             "kernels": kernels,
         })
-        if args.copy_calibration_gib > 0:
-            n = int(args.copy_calibration_gib * 2**30)
-            src = torch.empty(n, dtype=torch.uint8, device="cuda")
-            dst = torch.empty_like(src)
-            src.fill_(1)
-            torch.cuda.synchronize()
-            dst.copy_(src)
-            torch.cuda.synchronize()
-            result["copy_calibration_bytes"] = n
-            del src, dst
         if osec is not None:
             import oracle
 
@@ -462,10 +453,50 @@ def main():
         del x, lab, perm
         torch.cuda.empty_cache()
 
+    if "b" in only:
+        configs["list_build"] = bench_build(ctx, args.rows)
+    if args.copy_calibration_gib > 0:
+        # one device copy of known size, for scaling rocprofv3 byte counters
+        n = int(args.copy_calibration_gib * 2**30)
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n
+        del src, dst
     result["configs"] = configs
     if extra:
         result["extra"] = extra
     print(json.dumps(result), flush=True)
+
+
+def bench_build(ctx, N):
+    """ivf_build_lists alone on N uniform labels over 65,536 lists (device
+    generator): median of 3 calls, per-kernel times; 12 algorithmic bytes per
+    row against the HBM peak."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_08751_amd as ivf
+
+    C = C_BIG
+    lab = torch.empty(N, dtype=torch.int32, device="cuda")
+    synth.device_labels(N, C, lab, seed=3)
+    cnt = torch.empty(C, dtype=torch.int64, device="cuda")
+    off = torch.empty(C + 1, dtype=torch.int64, device="cuda")
+    perm = torch.empty(N, dtype=torch.int32, device="cuda")
+    fn = lambda: ivf.ivf_build_lists(ctx, lab, C, out_counts=cnt, out_offsets=off, out_perm=perm)
+    ts, tl = call_times(ctx, fn, 3, warm=1)
+    t = float(np.median(ts))
+    gbs = 12.0 * N / (t * 1e-3) / 1e9
+    log("list build of %d labels: %.3f ms" % (N, t))
+    del lab, perm
+    torch.cuda.empty_cache()
+    return {"labels": N, "lists": C, "ms_per_call": t, "bytes_per_row": 12, "GBps": gbs,
+            "hbm_frac": gbs / PEAK_HBM_GBS, "kernels_ms": {n.split("/", 1)[1]: ms for n, ms in tl}}
 
 
 # ---------------------------------------------------------------- NEXT rows
