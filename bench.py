@@ -656,7 +656,8 @@ def bench_assign_graph(ctx, x, cent, prev, full_ms, S=8):
     """Candidate-restricted assignment (fast construction mode): the
     8-nearest-centroid graph from ivf_route of the centroids against
     themselves, then each row scored against the 8 neighbours of its previous
-    centroid. Median of 3 calls. HBM bytes per row: the row, its previous
+    centroid, rows taken grouped by previous label (and, for comparison, in
+    row order). Median of 3 calls. HBM bytes per row: the row, its previous
     label, its label and distance (centroid rows come from the cache)."""
     import torch
 
@@ -667,13 +668,19 @@ def bench_assign_graph(ctx, x, cent, prev, full_ms, S=8):
     graph, _ = ivf.ivf_route(ctx, cent, cent, S, want_dist=False)
     lab = torch.empty(N, dtype=torch.int32, device=x.device)
     dist = torch.empty(N, dtype=torch.float32, device=x.device)
-    ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist)
+    # rows grouped by previous label (that label's list permutation): rows
+    # next to each other share their candidates
+    _, _, order = ivf.ivf_build_lists(ctx, prev, C)
+    ivf.ivf_assign_graph(ctx, x, cent, graph, prev, order=order, out_labels=lab, out_dist=dist)
     torch.cuda.synchronize()
     t_graph = _timed(ctx, lambda: ivf.ivf_route(ctx, cent, cent, S, out_ids=graph, want_dist=False))
-    t = _timed(ctx, lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist))
+    t_rows = _timed(ctx, lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, out_labels=lab, out_dist=dist))
+    t = _timed(ctx, lambda: ivf.ivf_assign_graph(ctx, x, cent, graph, prev, order=order, out_labels=lab,
+                                                 out_dist=dist))
     per_row = D + 12
     gbs = per_row * N / (t * 1e-3) / 1e9
     return {"rows": N, "centroids": C, "degree": S, "graph_ms": t_graph, "assign_ms": t,
+            "assign_ms_row_order": t_rows,
             "rows_per_s": N / (t * 1e-3), "GBps": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
             "speedup_vs_full_assignment": full_ms / t}
 

@@ -267,11 +267,17 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
  *   rows       [N, D] fp32 or uint8 (dt), N <= 2^32 - 1
  *   centroids  [C, D] fp32      graph [C, S] int32, 1 <= S <= 64
  *   prev       [N] int32        out_labels [N] int32
+ *   order      [N] uint32 processing order, or NULL (row order): results do
+ *              not depend on it, speed does (rows with the same previous
+ *              label next to each other share their candidates' loads; the
+ *              previous step's list permutation is that order). Entries >= N
+ *              are skipped; a row that order does not list is left untouched.
  *   out_dist   [N] fp32 squared distance (fp64 rounded), may be NULL
  * No workspace. Errors: IVF_EINVAL, IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */
 ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N,
                             const float *centroids, int64_t C, int32_t D, const int32_t *graph,
-                            int32_t S, const int32_t *prev, int32_t *out_labels, float *out_dist);
+                            int32_t S, const int32_t *prev, const uint32_t *order,
+                            int32_t *out_labels, float *out_dist);
 
 /* Candidates for rows that have no previous label (the graph-assisted
  * assignment of the full base set, Sec. "Fast Index Building Details": the

@@ -45,7 +45,7 @@ SIGNATURES = [
     ("ivf_mfma_probe_i8", _INT, [_P, _I32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]),
     ("ivf_list_major", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _I64, _I64, _P, _P]),
     ("ivf_pq_encode", _INT, [_P, _P, _I64, _I32, _I32, _P, _P]),
-    ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P]),
+    ("ivf_assign_graph", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I32, _P, _P, _P, _P]),
     ("ivf_assign_cells", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _I64, _P, _P, _I64, _P, _I32, _I32, _P, _P, _P]),
     ("ivf_adc_scan", _INT, [_P, _P, _I64, _I32, _P, _I64, _P, _I32, _P, _P, _I64, _P, _I32, _P, _I32, _P, _P]),
     ("ivf_pq_train_step", _INT, [_P, _P, _I64, _I32, _I32, _P, _U64, _I32, _P, _P, _P]),
@@ -375,10 +375,11 @@ def ivf_pq_train_step(ctx: Context, x, codebooks, seed: int = 0, it: int = 0, ou
     return out_codebooks, out_counts, out_objective
 
 
-def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None, out_dist=None,
+def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, order=None, out_labels=None, out_dist=None,
                      want_dist: bool = True):
     """Nearest of each row's candidates graph[prev[i]] (int32 [C, S]):
-    labels int32 [N] and squared distances fp32 [N]."""
+    labels int32 [N] and squared distances fp32 [N]. `order` (int32 [N] or
+    None) only sets the processing order."""
     import torch
 
     for t, name in ((rows, "rows"), (centroids, "centroids"), (graph, "graph"), (prev, "prev")):
@@ -391,9 +392,12 @@ def ivf_assign_graph(ctx: Context, rows, centroids, graph, prev, out_labels=None
     if want_dist and out_dist is None:
         out_dist = torch.empty(N, dtype=torch.float32, device=rows.device)
     ctx.bind_stream()
+    if order is not None:
+        _device_tensor(order, "order")
     ctx.check(ctx.lib.ivf_assign_graph(ctx.handle, _ptr(rows), _dtype_code(rows), N, _ptr(centroids), C, D,
-                                       _ptr(graph), S, _ptr(prev), _ptr(out_labels),
-                                       _ptr(out_dist if want_dist else None)), "ivf_assign_graph")
+                                       _ptr(graph), S, _ptr(prev), _ptr(order) if order is not None else None,
+                                       _ptr(out_labels), _ptr(out_dist if want_dist else None)),
+              "ivf_assign_graph")
     return out_labels, (out_dist if want_dist else None)
 
 

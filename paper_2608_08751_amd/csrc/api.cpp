@@ -1096,7 +1096,7 @@ ivf_status ivf_list_major(ivf_ctx *ctx, const void *base, int dt, int64_t N, con
 
 ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N, const float *centroids,
                             int64_t C, int32_t D, const int32_t *graph, int32_t S, const int32_t *prev,
-                            int32_t *out_labels, float *out_dist)
+                            const uint32_t *order, int32_t *out_labels, float *out_dist)
 {
     if (!ctx) return IVF_EINVAL;
     ctx->err.clear();
@@ -1109,22 +1109,23 @@ ivf_status ivf_assign_graph(ivf_ctx *ctx, const void *rows, int dt, int64_t N, c
         return fail(ctx, IVF_EINVAL, "S must be in [1, %d] (got %d)", kMaxGraphDegree, S);
     if (N == 0) return IVF_OK;
     if (!centroids || !graph || !prev || !out_labels) return fail(ctx, IVF_EINVAL, "null pointer argument");
-    if (!aligned16(centroids) || !aligned16(graph) || !aligned16(prev) || !aligned16(out_labels) ||
-        (out_dist && !aligned16(out_dist)))
+    if (!aligned16(centroids) || !aligned16(graph) || !aligned16(prev) || (order && !aligned16(order)) ||
+        !aligned16(out_labels) || (out_dist && !aligned16(out_dist)))
         return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
-    const void *ins[4] = {rows, centroids, graph, prev};
-    const size_t ib[4] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)C * S * 4, (size_t)N * 4};
+    const void *ins[5] = {rows, centroids, graph, prev, order};
+    const size_t ib[5] = {(size_t)N * rb, (size_t)C * D * 4, (size_t)C * S * 4, (size_t)N * 4,
+                          order ? (size_t)N * 4 : 0};
     const void *outs[2] = {out_labels, out_dist};
     const size_t ob[2] = {(size_t)N * 4, (size_t)N * 4};
     for (int i = 0; i < 2; ++i)
-        for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < 5; ++k)
             if (overlap(outs[i], ob[i], ins[k], ib[k])) return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
     if (overlap(out_labels, ob[0], out_dist, ob[1])) return fail(ctx, IVF_EINVAL, "outputs overlap");
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, IVF_EDEVICE, "no usable device (context device %d)", ctx->device);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
-    TIMED("assign_graph", launch_assign_graph(rows, rowtype, N, centroids, C, D, graph, S, prev, out_labels,
-                                              out_dist, ctx->stream));
+    TIMED("assign_graph", launch_assign_graph(rows, rowtype, N, centroids, C, D, graph, S, prev, order,
+                                              out_labels, out_dist, ctx->stream));
     ctx->last_stats = nullptr;
     return IVF_OK;
 }

@@ -47,14 +47,18 @@ template <typename XT>
 __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
     const XT *__restrict__ X, int64_t N, const float *__restrict__ cent, int64_t C, int D,
     const int32_t *__restrict__ graph, int S, int sp_log2, const int32_t *__restrict__ prev,
-    int32_t *__restrict__ labels, float *__restrict__ dist)
+    const uint32_t *__restrict__ order, int32_t *__restrict__ labels, float *__restrict__ dist)
 {
     const int SP = 1 << sp_log2;
     const int s = threadIdx.x & (SP - 1);
-    const int64_t i = ((int64_t)blockIdx.x * kAgThreads + threadIdx.x) >> sp_log2;
+    // processing position -> row (rows with the same previous label next to
+    // each other share their candidates' loads); order entries >= N are skipped
+    const int64_t pos = ((int64_t)blockIdx.x * kAgThreads + threadIdx.x) >> sp_log2;
+    const int64_t i = (order && pos < N) ? (int64_t)order[pos] : pos;
+    const bool live = pos < N && i < N;
     double d = __builtin_huge_val();
     int id = INT_MAX;  // loses every comparison against a real candidate
-    if (i < N && s < S) {
+    if (live && s < S) {
         const int32_t p = prev[i];
         const int32_t j = (p >= 0 && p < C) ? graph[(int64_t)p * S + s] : -1;
         if (j >= 0 && j < C) {
@@ -95,7 +99,7 @@ __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
             id = oid;
         }
     }
-    if (i < N && s == 0) {
+    if (live && s == 0) {
         const bool none = id == INT_MAX;
         labels[i] = none ? -1 : id;
         if (dist) dist[i] = none ? __builtin_huge_valf() : (float)d;
@@ -227,8 +231,8 @@ __global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
 }  // namespace
 
 hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C,
-                               int D, const int32_t *graph, int S, const int32_t *prev, int32_t *labels,
-                               float *dist, hipStream_t s)
+                               int D, const int32_t *graph, int S, const int32_t *prev, const uint32_t *order,
+                               int32_t *labels, float *dist, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
     int sp_log2 = 0;
@@ -237,10 +241,10 @@ hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const f
     const unsigned grid = (unsigned)((threads + kAgThreads - 1) / kAgThreads);
     if (rowtype == kRowU8)
         hipLaunchKernelGGL(assign_graph_kernel<uint8_t>, dim3(grid), dim3(kAgThreads), 0, s,
-                           (const uint8_t *)rows, N, cent, C, D, graph, S, sp_log2, prev, labels, dist);
+                           (const uint8_t *)rows, N, cent, C, D, graph, S, sp_log2, prev, order, labels, dist);
     else
         hipLaunchKernelGGL(assign_graph_kernel<float>, dim3(grid), dim3(kAgThreads), 0, s,
-                           (const float *)rows, N, cent, C, D, graph, S, sp_log2, prev, labels, dist);
+                           (const float *)rows, N, cent, C, D, graph, S, sp_log2, prev, order, labels, dist);
     return hipGetLastError();
 }
 

@@ -233,8 +233,8 @@ hipError_t launch_pq_assign(const float *X, int64_t n, int D, int dsub, int m0, 
 // ---- candidate-restricted assignment (assign_graph.hip) ---------------------
 constexpr int kMaxGraphDegree = 64;
 hipError_t launch_assign_graph(const void *rows, int rowtype, int64_t N, const float *cent, int64_t C,
-                               int D, const int32_t *graph, int S, const int32_t *prev, int32_t *labels,
-                               float *dist, hipStream_t s);
+                               int D, const int32_t *graph, int S, const int32_t *prev, const uint32_t *order,
+                               int32_t *labels, float *dist, hipStream_t s);
 // Cell-and-walk assignment (rows without a previous label): nearest member of
 // the row's coarse cell, then up to `hops` greedy moves over graph [C, S]
 // (graph may be null). D <= kCellsMaxDim.

@@ -259,10 +259,10 @@ def test_pq_validation(vctx, lib):
 
 def test_assign_graph_validation(vctx, lib):
     h = vctx.handle
-    rows, cent, graph, prev, lab, dist = P(0), P(GB), P(2 * GB), P(3 * GB), P(4 * GB), P(5 * GB)
+    rows, cent, graph, prev, lab, dist, order = P(0), P(GB), P(2 * GB), P(3 * GB), P(4 * GB), P(5 * GB), P(6 * GB)
     ok = lambda **k: lib.ivf_assign_graph(h, k.get("rows", rows), B.IVF_U8, k.get("N", 1000), cent, 100, 128,
                                           k.get("graph", graph), k.get("S", 8), k.get("prev", prev),
-                                          k.get("lab", lab), k.get("dist", dist))
+                                          k.get("order", order), k.get("lab", lab), k.get("dist", dist))
     assert ok() == B.IVF_EDEVICE
     assert ok(dist=None) == B.IVF_EDEVICE
     assert ok(N=0) == B.IVF_OK
@@ -271,6 +271,8 @@ def test_assign_graph_validation(vctx, lib):
     assert ok(lab=P(3 * GB + 16)) == B.IVF_EINVAL  # overlaps prev
     assert ok(dist=P(4 * GB + 64)) == B.IVF_EINVAL  # overlaps the labels
     assert ok(dist=P(5 * GB + 4)) == B.IVF_EINVAL  # misaligned
+    assert ok(order=None) == B.IVF_EDEVICE and ok(order=P(6 * GB + 4)) == B.IVF_EINVAL
+    assert ok(lab=P(6 * GB + 16)) == B.IVF_EINVAL  # overlaps the order
 
 
 def test_assign_cells_validation(vctx, lib):

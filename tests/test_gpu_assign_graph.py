@@ -30,12 +30,13 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def run(ctx, x, c, graph, prev):
+def run(ctx, x, c, graph, prev, order=None):
     import torch
 
     import paper_2608_08751_amd as ivf
 
-    lab, dist = ivf.ivf_assign_graph(ctx, to_dev(x), to_dev(c), to_dev(graph), to_dev(prev))
+    lab, dist = ivf.ivf_assign_graph(ctx, to_dev(x), to_dev(c), to_dev(graph), to_dev(prev),
+                                     order=None if order is None else to_dev(order.astype(np.int32)))
     torch.cuda.synchronize()
     return lab.cpu().numpy(), dist.cpu().numpy()
 
@@ -54,10 +55,12 @@ def test_assign_graph_exact(ivf_ctx, oracle_mod, N, C, D, S, dt):
         c = rng.standard_normal((C, D)).astype(np.float32)
     graph = rng.integers(0, C, (C, S)).astype(np.int32)
     prev = rng.integers(0, C, N).astype(np.int32)
-    lab, dist = run(ivf_ctx, x, c, graph, prev)
     olab, od = oracle_mod.assign_graph(x, c, graph, prev, return_dist=True)
-    assert (lab == olab).all()
-    assert (dist == od.astype(np.float32)).all()
+    # any processing order gives the same result
+    for order in (None, rng.permutation(N), np.argsort(prev, kind="stable")):
+        lab, dist = run(ivf_ctx, x, c, graph, prev, order)
+        assert (lab == olab).all()
+        assert (dist == od.astype(np.float32)).all()
 
 
 def test_assign_graph_ties_duplicates_and_invalid(ivf_ctx, oracle_mod):
@@ -91,7 +94,8 @@ def test_fast_kmeans_iteration_full_size(ivf_ctx, oracle_mod):
     c0 = x[to_dev(synth.kmeans_init(N, C, seed=0))].float().contiguous()
     lab0, c1, _, _ = ivf.ivf_kmeans_step(ivf_ctx, x, c0, seed=0, it=0)
     graph, _ = ivf.ivf_route(ivf_ctx, c1, c1, S)
-    lab, dist = ivf.ivf_assign_graph(ivf_ctx, x, c1, graph, lab0)
+    _, _, by_prev = ivf.ivf_build_lists(ivf_ctx, lab0, C)
+    lab, dist = ivf.ivf_assign_graph(ivf_ctx, x, c1, graph, lab0, order=by_prev)
     exact, _, _, _ = ivf.ivf_kmeans_step(ivf_ctx, x, c1, seed=0, it=1)
     torch.cuda.synchronize()
     rng = np.random.default_rng(9)
