@@ -15,12 +15,15 @@
 //   per-list counts and each sub-block's start per digit; the offsets are the
 //   exclusive scan of the counts; scatter1 writes the row ids into the
 //   permutation.
-// Inside a block, rows are taken in 4,096-row tiles: wave w ranks its 1,024
-// rows column by column (64 consecutive rows per column) with an LDS
-// match-any on the digit, the 4 waves' digit counts are combined with a prefix, the tile
-// is staged in LDS in (digit, row) order and written out so that consecutive
-// threads store consecutive addresses of one digit run. Both levels keep row
-// order within a digit, so the final order is (label, row id).
+// Inside a block, rows are taken in tiles (8,192 rows at level 0, 4,096 at
+// level 1): wave w ranks its quarter column by column (64 consecutive rows per
+// column) with an LDS match-any on the digit, keeping cumulative per-wave
+// digit counts; after one workgroup barrier every wave reads all four waves'
+// counts and derives the tile's digit starts itself (no further barrier), the
+// tile is staged in LDS in (digit, row) order and, after a second barrier,
+// written out so that consecutive threads store consecutive addresses of one
+// digit run. Both levels keep row order within a digit, so the final order is
+// (label, row id).
 #include "ivf_internal.h"
 
 #include <algorithm>
@@ -28,15 +31,16 @@
 namespace ivf {
 namespace {
 
-constexpr int kRThreads = 256;           // 4 waves
-constexpr int kRTile = 4096;             // rows per tile of level 1
-constexpr int kRTile0 = 8192;            // rows per tile of level 0 (longer runs per digit)
-
-template <bool FIRST>
-constexpr int tile_rows()
-{
-    return FIRST ? kRTile0 : kRTile;
-}
+constexpr int kRThreads = 256;           // 4 waves (histogram and scan kernels)
+// Partition kernels: one workgroup of kPW waves per CU, each wave ranking
+// kItems0 / kItems1 columns of 64 rows per tile. Long tiles give long write
+// runs per digit, and few blocks in flight keep the runs being filled (about
+// 256 per block) within the L2 until their cache lines are complete.
+constexpr int kPW = 12;
+constexpr int kRTile0 = kPW * 64 * 32;   // rows per tile of level 0 (24,576)
+constexpr int kRTile = kPW * 64 * 16;    // rows per tile of level 1 (12,288)
+constexpr int kPosBits = 15;             // tile position bits of a staged level-0 entry
+static_assert(kRTile0 <= (1 << kPosBits), "tile positions must fit the staged entry");
 
 // Exclusive scan of v over the 256 threads of the block; returns the prefix.
 __device__ __forceinline__ uint32_t block_exscan256(uint32_t v, uint32_t *wsum)
@@ -55,39 +59,40 @@ __device__ __forceinline__ uint32_t block_exscan256(uint32_t v, uint32_t *wsum)
     return before + incl - v;
 }
 
-template <int RT>
+// LDS of one partition workgroup. Ranking state is per wave; the combine is
+// done by every wave for itself (each lane owns digits 4 lane .. 4 lane + 3),
+// so a tile needs two workgroup barriers: after the ranking (the digit counts
+// of all waves are complete) and after the staging (the tile is in LDS).
+template <bool FIRST, int RT, int W>
 struct TileLds {
-    unsigned long long peers[4][256];  // per-wave match-any scratch (lane bits per digit)
-    uint32_t wcnt[4][256];   // per-wave digit counts, then their exclusive prefix
-    uint32_t start[256];     // digit start inside the tile
-    uint32_t gbase[256];     // global start of this tile's digit run
-    uint32_t run[256];       // block running offset per digit
-    uint32_t wsum[4];
-    uint32_t sid[RT];        // staged row ids
-    uint8_t slo[RT];         // staged low bytes (level 0)
-    uint8_t sdig[RT];        // staged digits
+    unsigned long long peers[W][256];  // per-wave match-any scratch (lane bits per digit), zero between columns
+    uint32_t wcnt[W][256];   // entries of each digit ranked by each wave in this tile
+    uint32_t wbase[W][256];  // wave w: staged index of its first digit-d entry of the tile
+    uint32_t woff[W][256];   // wave w's copy: global index of staged index 0 of digit d (mod 2^32)
+    uint32_t sw[RT];         // staged entries: level 0 (label << kPosBits | tile position), level 1 row id
+    uint8_t sdig[FIRST ? 4 : RT];  // level 1: staged digits
 };
 
-// A tile's inputs, loaded one tile ahead: row r = base + wave*RT/4 + e*64 + lane.
-template <int RT>
+// A tile's inputs: row r = base + wave*RT/W + e*64 + lane.
+template <int RT, int W>
 struct TileIn {
-    static constexpr int kItems = RT / kRThreads;  // rows per thread
+    static constexpr int kItems = RT / (W * 64);  // rows per thread
     uint32_t v[kItems];        // level 0: label; level 1: row id
     uint32_t lo4[kItems / 4];  // level 1: low bytes, four per word
 };
 
-template <bool FIRST, bool FULL, int RT = tile_rows<FIRST>()>
-__device__ __forceinline__ void load_tile(TileIn<RT> &in, int64_t base, int64_t end,
+template <bool FIRST, bool FULL, int RT, int W>
+__device__ __forceinline__ void load_tile(TileIn<RT, W> &in, int64_t base, int64_t end,
                                           const int32_t *__restrict__ labels,
                                           const uint32_t *__restrict__ in_ids,
                                           const uint8_t *__restrict__ in_lo)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int e = 0; e < TileIn<RT>::kItems / 4; ++e) in.lo4[e] = 0;
+    for (int e = 0; e < TileIn<RT, W>::kItems / 4; ++e) in.lo4[e] = 0;
 #pragma unroll
-    for (int e = 0; e < TileIn<RT>::kItems; ++e) {
-        const int64_t r = base + wave * (RT / 4) + e * 64 + lane;
+    for (int e = 0; e < TileIn<RT, W>::kItems; ++e) {
+        const int64_t r = base + wave * (RT / W) + e * 64 + lane;
         const bool ok = FULL || r < end;
         if (FIRST) {
             in.v[e] = ok ? (uint32_t)labels[r] : 0xFFFFFFFFu;
@@ -100,97 +105,140 @@ __device__ __forceinline__ void load_tile(TileIn<RT> &in, int64_t base, int64_t 
 
 // One tile: rank, stage and write. Level 0 (FIRST): the digit is label >> 8,
 // the payload is (row id, label & 255). Level 1: the digit is the stored low
-// byte, the payload is the stored row id.
-template <bool FIRST, bool FULL, int RT = tile_rows<FIRST>()>
-__device__ void radix_tile(TileLds<RT> &t, const TileIn<RT> &in, int64_t base, int64_t end, int C,
-                           uint32_t *__restrict__ out_ids, uint8_t *__restrict__ out_lo)
+// byte, the payload is the stored row id. Outputs are written only below
+// n_out. `next` loads the following tile into `in` once the tile no longer
+// needs it (after the ranking at level 0, after the staging at level 1), so
+// its loads overlap the rest of the tile.
+template <bool FIRST, bool FULL, int RT, int W, class Next>
+__device__ void radix_tile(TileLds<FIRST, RT, W> &t, uint32_t (&run)[4], TileIn<RT, W> &in, int64_t base, int64_t end,
+                           int C, uint32_t n_out, uint32_t *__restrict__ out_ids, uint8_t *__restrict__ out_lo,
+                           Next &&next)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    constexpr int kItems = TileIn<RT>::kItems;
-    uint32_t dp[kItems];  // (digit << 16) | position in the wave's run, 0xFFFF = none
-    // rank column by column
+    constexpr int kItems = TileIn<RT, W>::kItems;
+    // (label << 16 | rank) at level 0, (digit << 16 | rank) at level 1, where
+    // rank is the entry's position among the wave's digit-d entries of the
+    // tile; ~0 = none
+    uint32_t dp[kItems];
+    // this wave's counts start from zero (every wave has read them in the
+    // previous tile's combine, before its second barrier)
+    *reinterpret_cast<uint4 *>(&t.wcnt[wave][4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
+    // rank column by column: the lanes of a column with the same digit OR
+    // their bits into peers[wave][d] and read the union back; the group's
+    // lowest lane adds the group to the wave's count and clears the entry.
+    // (A wave's LDS instructions execute in order, for all lanes at once.)
 #pragma unroll
     for (int e = 0; e < kItems; ++e) {
-        const int64_t r = base + wave * (RT / 4) + e * 64 + lane;
+        const int64_t r = base + wave * (RT / W) + e * 64 + lane;
         bool valid = FULL || r < end;
-        uint32_t d;
+        uint32_t d, key;
         if (FIRST) {
             const int32_t l = (int32_t)in.v[e];
             valid = valid && l >= 0 && l < C;  // labels outside [0, C) are skipped
             d = valid ? ((uint32_t)l >> 8) : 0u;
+            key = (uint32_t)l;
         } else {
             d = (in.lo4[e / 4] >> (8 * (e % 4))) & 0xFFu;
+            key = d;
         }
-        // lanes of this wave with the same digit: every lane ORs its bit into
-        // peers[wave][d], reads the union back, and the group leader clears it
-        uint16_t p = 0xFFFFu;
+        uint32_t rk = 0xFFFFFFFFu;
         if (valid) {
             atomicOr(&t.peers[wave][d], 1ull << lane);
             const uint64_t m = t.peers[wave][d];
             const uint32_t b = t.wcnt[wave][d];
-            p = (uint16_t)(b + (uint32_t)__popcll(m & lt));
+            rk = (key << 16) | (b + (uint32_t)__popcll(m & lt));
             if ((m & lt) == 0) {
                 t.wcnt[wave][d] = b + (uint32_t)__popcll(m);
                 t.peers[wave][d] = 0ull;
             }
         }
-        dp[e] = (d << 16) | p;
+        dp[e] = rk;
     }
+    if (FIRST) next();
     __syncthreads();
-    // combine the waves: per digit (one thread per digit)
+    // combine, in every wave: the tile's count of each digit, their exclusive
+    // scan over the digits, this wave's staging base per digit and the global
+    // offsets
+    uint32_t total;
     {
-        const int d = threadIdx.x;
-        const uint32_t c0 = t.wcnt[0][d], c1 = t.wcnt[1][d], c2 = t.wcnt[2][d], c3 = t.wcnt[3][d];
-        const uint32_t tot = c0 + c1 + c2 + c3;
-        t.wcnt[0][d] = 0;
-        t.wcnt[1][d] = c0;
-        t.wcnt[2][d] = c0 + c1;
-        t.wcnt[3][d] = c0 + c1 + c2;
-        const uint32_t st = block_exscan256(tot, t.wsum);
-        t.start[d] = st;
-        t.gbase[d] = t.run[d];
-        t.run[d] += tot;
+        uint32_t tot[4] = {0u, 0u, 0u, 0u}, before[4] = {0u, 0u, 0u, 0u}, s = 0;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(&t.wcnt[w][4 * lane]);
+            const uint32_t c[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                tot[j] += c[j];
+                before[j] += w < wave ? c[j] : 0u;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s += tot[j];
+        uint32_t incl = s;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t up = __shfl_up(incl, o);
+            if (lane >= o) incl += up;
+        }
+        total = __shfl(incl, 63);
+        uint32_t st = incl - s;
+        uint32_t wb[4], wo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            wb[j] = st + before[j];
+            wo[j] = run[j] - st;
+            run[j] += tot[j];
+            st += tot[j];
+        }
+        *reinterpret_cast<uint4 *>(&t.wbase[wave][4 * lane]) = make_uint4(wb[0], wb[1], wb[2], wb[3]);
+        *reinterpret_cast<uint4 *>(&t.woff[wave][4 * lane]) = make_uint4(wo[0], wo[1], wo[2], wo[3]);
     }
-    __syncthreads();
-    // stage in (digit, row) order
+    // stage in (digit, row) order (wbase of this wave was written by this wave)
 #pragma unroll
     for (int e = 0; e < kItems; ++e) {
-        if ((dp[e] & 0xFFFFu) != 0xFFFFu) {
-            const uint32_t d = dp[e] >> 16;
-            const uint32_t li = t.start[d] + t.wcnt[wave][d] + (dp[e] & 0xFFFFu);
-            t.sid[li] = FIRST ? (uint32_t)(base + wave * (RT / 4) + e * 64 + lane) : in.v[e];
-            t.sdig[li] = (uint8_t)d;
-            if (FIRST) t.slo[li] = (uint8_t)(in.v[e] & 0xFFu);
+        if (dp[e] != 0xFFFFFFFFu) {
+            const uint32_t key = dp[e] >> 16;
+            const uint32_t d = FIRST ? key >> 8 : key;
+            const uint32_t li = t.wbase[wave][d] + (dp[e] & 0xFFFFu);
+            if (li < (uint32_t)RT) {
+                if (FIRST) {
+                    t.sw[li] = (key << kPosBits) | (uint32_t)(wave * (RT / W) + e * 64 + lane);
+                } else {
+                    t.sw[li] = in.v[e];
+                    t.sdig[li] = (uint8_t)d;
+                }
+            }
         }
     }
+    if (!FIRST) next();
     __syncthreads();
     // write the runs: consecutive staged entries of a digit go to consecutive
     // addresses
-    const uint32_t total = t.start[255] + (t.run[255] - t.gbase[255]);
-#pragma unroll
+#pragma unroll 8
     for (int e = 0; e < kItems; ++e) {
-        const uint32_t i = threadIdx.x + e * kRThreads;
+        const uint32_t i = threadIdx.x + e * (W * 64);
         if (i < total) {
-            const uint32_t d = t.sdig[i];
-            const uint32_t g = t.gbase[d] + (i - t.start[d]);
-            out_ids[g] = t.sid[i];
-            if (FIRST) out_lo[g] = t.slo[i];
+            const uint32_t w = t.sw[i];
+            const uint32_t d = FIRST ? (w >> (kPosBits + 8)) & 0xFFu : t.sdig[i];
+            const uint32_t g = t.woff[wave][d] + i;
+            if (g < n_out) {
+                if (FIRST) {
+                    out_ids[g] = (uint32_t)base + (w & ((1u << kPosBits) - 1));
+                    out_lo[g] = (uint8_t)(w >> kPosBits);
+                } else {
+                    out_ids[g] = w;
+                }
+            }
         }
     }
-    // the next tile counts from zero (nothing reads wcnt in this phase; the
-    // barrier below orders the reset before the next tile's ranking)
-    t.wcnt[0][threadIdx.x] = t.wcnt[1][threadIdx.x] = t.wcnt[2][threadIdx.x] = t.wcnt[3][threadIdx.x] = 0;
-    __syncthreads();
 }
 
-template <int RT>
-__device__ __forceinline__ void init_run(TileLds<RT> &t)
+// Zeroes the match-any scratch (the caller's next barrier publishes it).
+template <bool FIRST, int RT, int W>
+__device__ __forceinline__ void init_block(TileLds<FIRST, RT, W> &t)
 {
-    for (int i = threadIdx.x; i < 256; i += kRThreads) {
-        t.wcnt[0][i] = t.wcnt[1][i] = t.wcnt[2][i] = t.wcnt[3][i] = 0;
-        t.peers[0][i] = t.peers[1][i] = t.peers[2][i] = t.peers[3][i] = 0ull;
-    }
+    for (int i = threadIdx.x; i < W * 256; i += W * 64) (&t.peers[0][0])[i] = 0ull;
 }
 
 // ---- level 0 ----------------------------------------------------------------
@@ -265,31 +313,39 @@ __global__ __launch_bounds__(kRThreads) void starts0_kernel(const uint32_t *__re
     if (d == 255) astart[256] = st + v;
 }
 
-__global__ __launch_bounds__(kRThreads, 2) void scatter0_kernel(const int32_t *__restrict__ labels, int64_t N,
+__global__ __launch_bounds__(kPW * 64) void scatter0_kernel(const int32_t *__restrict__ labels, int64_t N,
                                                              int64_t R0, int C, int nblocks,
                                                              const uint32_t *__restrict__ base0,
                                                              const uint32_t *__restrict__ astart,
                                                              uint32_t *__restrict__ tmp_ids,
                                                              uint8_t *__restrict__ tmp_lo)
 {
-    constexpr int RT = kRTile0;
-    __shared__ TileLds<RT> t;
-    init_run(t);
-    t.run[threadIdx.x] = astart[threadIdx.x] + base0[(int64_t)threadIdx.x * nblocks + blockIdx.x];
+    constexpr int RT = kRTile0, W = kPW;
+    __shared__ TileLds<true, RT, W> t;
+    uint32_t run[4];  // running global offsets of this lane's digits 4 lane .. 4 lane + 3
+    init_block(t);
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int d = 4 * lane + j;
+        run[j] = astart[d] + base0[(int64_t)d * nblocks + blockIdx.x];
+    }
     __syncthreads();
+    const uint32_t n_out = (uint32_t)N;
     const int64_t r0 = (int64_t)blockIdx.x * R0, r1 = min(N, r0 + R0);
-    TileIn<RT> cur, nxt;
-    if (r0 + RT <= r1) load_tile<true, true>(cur, r0, r1, labels, nullptr, nullptr);
-    else load_tile<true, false>(cur, r0, r1, labels, nullptr, nullptr);
+    TileIn<RT, W> cur;
+    if (r0 + RT <= r1) load_tile<true, true, RT, W>(cur, r0, r1, labels, nullptr, nullptr);
+    else load_tile<true, false, RT, W>(cur, r0, r1, labels, nullptr, nullptr);
     for (int64_t base = r0; base < r1; base += RT) {
         const int64_t nb = base + RT;
-        if (nb + RT <= r1) load_tile<true, true>(nxt, nb, r1, labels, nullptr, nullptr);
-        else if (nb < r1) load_tile<true, false>(nxt, nb, r1, labels, nullptr, nullptr);
+        auto next = [&]() {
+            if (nb + RT <= r1) load_tile<true, true, RT, W>(cur, nb, r1, labels, nullptr, nullptr);
+            else if (nb < r1) load_tile<true, false, RT, W>(cur, nb, r1, labels, nullptr, nullptr);
+        };
         if (base + RT <= r1)
-            radix_tile<true, true>(t, cur, base, base + RT, C, tmp_ids, tmp_lo);
+            radix_tile<true, true, RT, W>(t, run, cur, base, base + RT, C, n_out, tmp_ids, tmp_lo, next);
         else
-            radix_tile<true, false>(t, cur, base, r1, C, tmp_ids, tmp_lo);
-        cur = nxt;
+            radix_tile<true, false, RT, W>(t, run, cur, base, r1, C, n_out, tmp_ids, tmp_lo, next);
     }
 }
 
@@ -379,7 +435,7 @@ __global__ __launch_bounds__(kRThreads) void scan1_kernel(uint32_t *__restrict__
     if (j < C) counts[j] = run;
 }
 
-__global__ __launch_bounds__(kRThreads) void scatter1_kernel(const uint32_t *__restrict__ tmp_ids,
+__global__ __launch_bounds__(kPW * 64) void scatter1_kernel(const uint32_t *__restrict__ tmp_ids,
                                                              const uint8_t *__restrict__ tmp_lo,
                                                              const uint32_t *__restrict__ astart,
                                                              const uint32_t *__restrict__ sbstart,
@@ -387,29 +443,35 @@ __global__ __launch_bounds__(kRThreads) void scatter1_kernel(const uint32_t *__r
                                                              const int64_t *__restrict__ offsets, int C,
                                                              uint32_t *__restrict__ perm)
 {
-    __shared__ TileLds<kRTile> t;
+    constexpr int RT = kRTile, W = kPW;
+    __shared__ TileLds<false, RT, W> t;
     int bucket;
     int64_t lo, hi;
     if (!locate_sub(sbstart, astart, R1, blockIdx.x, bucket, lo, hi)) return;
-    init_run(t);
-    {
-        const int d = threadIdx.x;
-        const int j = bucket * 256 + d;
-        t.run[d] = j < C ? (uint32_t)offsets[j] + base1[(int64_t)blockIdx.x * 256 + d] : 0u;
+    uint32_t run[4];  // running global offsets of this lane's digits 4 lane .. 4 lane + 3
+    init_block(t);
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int d = 4 * lane + j;
+        const int l = bucket * 256 + d;
+        run[j] = l < C ? (uint32_t)offsets[l] + base1[(int64_t)blockIdx.x * 256 + d] : 0u;
     }
     __syncthreads();
-    TileIn<kRTile> cur, nxt;
-    if (lo + kRTile <= hi) load_tile<false, true>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
-    else load_tile<false, false>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
-    for (int64_t base = lo; base < hi; base += kRTile) {
-        const int64_t nb = base + kRTile;
-        if (nb + kRTile <= hi) load_tile<false, true>(nxt, nb, hi, nullptr, tmp_ids, tmp_lo);
-        else if (nb < hi) load_tile<false, false>(nxt, nb, hi, nullptr, tmp_ids, tmp_lo);
-        if (base + kRTile <= hi)
-            radix_tile<false, true>(t, cur, base, base + kRTile, C, perm, nullptr);
+    const uint32_t n_out = astart[256];
+    TileIn<RT, W> cur;
+    if (lo + RT <= hi) load_tile<false, true, RT, W>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
+    else load_tile<false, false, RT, W>(cur, lo, hi, nullptr, tmp_ids, tmp_lo);
+    for (int64_t base = lo; base < hi; base += RT) {
+        const int64_t nb = base + RT;
+        auto next = [&]() {
+            if (nb + RT <= hi) load_tile<false, true, RT, W>(cur, nb, hi, nullptr, tmp_ids, tmp_lo);
+            else if (nb < hi) load_tile<false, false, RT, W>(cur, nb, hi, nullptr, tmp_ids, tmp_lo);
+        };
+        if (base + RT <= hi)
+            radix_tile<false, true, RT, W>(t, run, cur, base, base + RT, C, n_out, perm, nullptr, next);
         else
-            radix_tile<false, false>(t, cur, base, hi, C, perm, nullptr);
-        cur = nxt;
+            radix_tile<false, false, RT, W>(t, run, cur, base, hi, C, n_out, perm, nullptr, next);
     }
 }
 
@@ -472,7 +534,7 @@ hipError_t launch_radix_level0(const RadixPlan &p, const int32_t *labels, const 
                        p.nblocks0, s.cnt0);
     hipLaunchKernelGGL(scan0_kernel, dim3(256), dim3(kRThreads), 0, st, s.cnt0, p.nblocks0, s.tot0);
     hipLaunchKernelGGL(starts0_kernel, dim3(1), dim3(kRThreads), 0, st, s.tot0, s.astart);
-    hipLaunchKernelGGL(scatter0_kernel, dim3(p.nblocks0), dim3(kRThreads), 0, st, labels, p.N, p.R0, (int)p.C,
+    hipLaunchKernelGGL(scatter0_kernel, dim3(p.nblocks0), dim3(kPW * 64), 0, st, labels, p.N, p.R0, (int)p.C,
                        p.nblocks0, s.cnt0, s.astart, s.tmp_ids, s.tmp_lo);
     return hipGetLastError();
 }
@@ -491,7 +553,7 @@ hipError_t launch_radix_level1_counts(const RadixPlan &p, const RadixScratch &s,
 hipError_t launch_radix_level1_scatter(const RadixPlan &p, const RadixScratch &s, const int64_t *offsets,
                                        uint32_t *perm, hipStream_t st)
 {
-    hipLaunchKernelGGL(scatter1_kernel, dim3(p.max_sub1), dim3(kRThreads), 0, st, s.tmp_ids, s.tmp_lo,
+    hipLaunchKernelGGL(scatter1_kernel, dim3(p.max_sub1), dim3(kPW * 64), 0, st, s.tmp_ids, s.tmp_lo,
                        s.astart, s.sbstart, p.R1, s.cnt1, offsets, (int)p.C, perm);
     return hipGetLastError();
 }
