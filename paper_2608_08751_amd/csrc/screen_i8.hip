@@ -756,11 +756,20 @@ __device__ __forceinline__ void s1_tile_test(const i32x16 &p, int idp, Top3i &st
     }
 }
 
+// K-step at which the previous block's row block rb is tested: one step
+// after an even spread, so that the test does not read an accumulator whose
+// last MFMA was issued just before (no wait states for its result).
+template <int RB, int KS, int rb>
+constexpr int s1_test_step()
+{
+    return rb * KS / RB + 1 < KS ? rb * KS / RB + 1 : KS - 1;
+}
+
 template <int RB, int T, int KS, int rb = 0>
 __device__ __forceinline__ void s1_tests_at(const i32x16 (&p)[RB], int idp, Top3i (&st)[RB])
 {
     if constexpr (rb < RB) {
-        if constexpr (rb * KS / RB == T) s1_tile_test(p[rb], idp, st[rb]);
+        if constexpr (s1_test_step<RB, KS, rb>() == T) s1_tile_test(p[rb], idp, st[rb]);
         s1_tests_at<RB, T, KS, rb + 1>(p, idp, st);
     }
 }
