@@ -34,6 +34,13 @@
  *     centroids have a coordinate outside [0, 255.998] (which does not
  *     quantise) is screened on fp32 MFMA instead; the switch happens on the
  *     device, without a host synchronisation.
+ *   - uint8-valued fp32 queries (every value an integer in [0, 255]) routed
+ *     against more than 2,048 centroids: the threshold-sample keys and the
+ *     candidate filter run on the two int8 planes (x - 128 against
+ *     rint(256 (c - 128))), with a bound of (390 + ||x - 128||_1) / 2 in the
+ *     planes' key units; any other value in the call, or a centroid that does
+ *     not quantise, sends the call to the fp32 kernels (device flag, no host
+ *     synchronisation). IVF_OPT_FP32_SCREEN forces the fp32 kernels.
  * Either way the results are the exact ones above; the screen chosen changes
  * speed only.
  *
@@ -219,8 +226,9 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *   IVF_OPT_SCREEN_WAVES    wave64s per workgroup of the fp32 distance-
  *                           screening kernel, 4 or 8 (D > 128 always uses 4);
  *                           speed only, never results
- *   IVF_OPT_FP32_SCREEN     1 = uint8 rows are screened on fp32 MFMA like
- *                           fp32 rows (default 0: int8 MFMA whenever every
+ *   IVF_OPT_FP32_SCREEN     1 = uint8 rows, and uint8-valued queries in
+ *                           ivf_route, are screened on fp32 MFMA like fp32
+ *                           data (default 0: int8 MFMA whenever every
  *                           centroid coordinate c has rint(256 (c - 128)) in
  *                           [-32768, 32767], i.e. c in [0, 255.998]);
  *                           speed only, never results

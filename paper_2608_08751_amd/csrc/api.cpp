@@ -186,12 +186,14 @@ struct RoutePlan {
     int64_t Cs;   // threshold sample size (centroids [0, Cs)), 0 = none
     int L;        // candidate capacity per query
     int rank_j;
+    int qdp;      // padded dimension of the int8 route planes; 0 = fp32 kernels only
 };
 
-RoutePlan plan_route(int64_t Q, int64_t C, int k, int rank_override)
+RoutePlan plan_route(int64_t Q, int64_t C, int k, int rank_override, int D)
 {
     RoutePlan p;
     p.QB = std::max<int64_t>(1, std::min<int64_t>(Q, kRouteBatch));
+    p.qdp = quant_dim(D);
     if (C <= 2048) {
         p.Cs = 0;
         p.L = pow2_ceil(std::max<int64_t>(C, k));
@@ -228,6 +230,11 @@ struct RouteLayout {
     uint2 *cand;
     float *keys;
     int32_t *wl;
+    // int8 route planes (plan.qdp > 0): two planes [quantized_pad(C)][2 qdp],
+    // biases, per-query bounds
+    int8_t *qc;
+    int32_t *negb;
+    float *qbound;
     size_t bytes;
 };
 
@@ -243,6 +250,14 @@ RouteLayout layout_route(void *base, const RoutePlan &p, int64_t C)
     l.cand = c.take<uint2>((size_t)p.QB * p.L);
     l.keys = c.take<float>((size_t)p.QB * p.Cs);
     l.wl = c.take<int32_t>(p.QB);
+    l.qc = nullptr;
+    l.negb = nullptr;
+    l.qbound = nullptr;
+    if (p.qdp > 0) {
+        l.qc = c.take<int8_t>((size_t)quantized_pad(C) * 2 * p.qdp);
+        l.negb = c.take<int32_t>(quantized_pad(C));
+        l.qbound = c.take<float>(p.QB);
+    }
     l.bytes = c.off + kAlign;
     return l;
 }
@@ -610,7 +625,7 @@ size_t ivf_workspace_bytes(int op, int64_t rows, int64_t C, int32_t D, int32_t k
     switch (op) {
     case IVF_OP_ROUTE:
         if (k < 1) return 0;
-        return layout_route(nullptr, plan_route(rows, C, k, 0), C).bytes;
+        return layout_route(nullptr, plan_route(rows, C, k, 0, D), C).bytes;
     case IVF_OP_KMEANS_STEP:
         return layout_assign(nullptr, std::max<int64_t>(rows, 1), C, quant_dim(D), true, true, num_cus).bytes;
     case IVF_OP_ASSIGN_BUILD:
@@ -813,6 +828,18 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
     const int DP = padded_dim(D);
     TIMED("fill", launch_fill_u32(l.sc.mc2_bits, 64, 0u, s));
     TIMED("centroid_norms", launch_centroid_norms(centroids, C, D, l.cnorm, l.sc.mc2_bits, s));
+    // uint8-valued queries are routed on the two int8 planes; the fp32
+    // kernels run instead (device flag, no host synchronisation) when a query
+    // or a centroid does not fit them. Tables small enough to be candidates
+    // whole (no threshold sample) stay on the fp32 kernels: there the screen
+    // only copies every centroid into the candidate list.
+    const bool i8 = p.qdp > 0 && p.Cs > 0 && !ctx->fp32_screen;
+    uint32_t *q_bad = l.sc.mc2_bits + 2;
+    uint32_t *i8_off = l.sc.mc2_bits + 6;
+    if (i8) {
+        TIMED("route_i8_check", launch_route_i8_check(queries, Q, D, i8_off, s));
+        TIMED("quantize", launch_quantize_centroids(centroids, C, D, p.qdp, l.qc, l.negb, q_bad, s, i8_off));
+    }
     for (int64_t q0 = 0; q0 < Q; q0 += p.QB) {
         const int64_t nb = std::min(p.QB, Q - q0);
         const float *qrows = queries + q0 * D;
@@ -824,11 +851,29 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         a.D = D;
         a.cent = centroids;
         a.cnorm = l.cnorm;
+        a.gate = i8 ? i8_off : nullptr;
+        RouteI8Args ra{};
+        ra.queries = qrows;
+        ra.nq = nb;
+        ra.D = D;
+        ra.qc = l.qc;
+        ra.negb = l.negb;
+        ra.cpad = quantized_pad(C);
+        ra.off = i8_off;
+        ra.stats = l.sc.stats;
+        if (i8) TIMED("route_i8_bound", launch_route_i8_bound(qrows, nb, D, q_bad, i8_off, l.qbound, s));
         if (p.Cs > 0) {
             a.c_begin = 0;
             a.c_end = p.Cs;
             a.nchunks = p.Cs / kChunk;
             a.keys = l.keys;
+            if (i8) {
+                ra.c_begin = 0;
+                ra.c_end = p.Cs;
+                ra.nchunks = p.Cs / kQuantChunk;
+                ra.keys = l.keys;
+                TIMED("route_i8_keys", launch_route_i8(kRouteKeys, p.qdp, ra, ctx->num_cus, s));
+            }
             TIMED("screen_keys", launch_screen(kModeKeys, kRowF32, DP, a, ctx->screen_waves, ctx->num_cus, s));
         }
         RouteArgs r{};
@@ -854,6 +899,8 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         r.wl = l.wl;
         r.wl_cnt = l.sc.wl_cnt;
         r.stats = l.sc.stats;
+        r.i8_off = i8 ? i8_off : nullptr;
+        r.qbound = l.qbound;
         TIMED("route_threshold", launch_route_threshold(r, s));
         if (p.Cs < C) {
             a.c_begin = p.Cs;
@@ -864,6 +911,17 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
             a.cand_cnt = l.cand_cnt;
             a.cand = l.cand;
             a.L = p.L;
+            if (i8) {
+                ra.c_begin = p.Cs;
+                ra.c_end = C;
+                ra.nchunks = (C - p.Cs + kQuantChunk - 1) / kQuantChunk;
+                ra.keys = nullptr;
+                ra.tau = l.tau;
+                ra.cand_cnt = l.cand_cnt;
+                ra.cand = l.cand;
+                ra.L = p.L;
+                TIMED("route_i8_filter", launch_route_i8(kRouteFilter, p.qdp, ra, ctx->num_cus, s));
+            }
             TIMED("screen_filter", launch_screen(kModeFilter, kRowF32, DP, a, ctx->screen_waves, ctx->num_cus, s));
         }
         TIMED("route_select", launch_route_select(r, s));
@@ -887,7 +945,7 @@ ivf_status ivf_route(ivf_ctx *ctx, const float *queries, int64_t Q, const float 
     bool done = false;
     ivf_status st = check_route(ctx, queries, Q, centroids, C, D, nprobe, out_ids, out_dist, &done);
     if (st != IVF_OK || done) return st;
-    const RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
+    const RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank, D);
     const size_t need = layout_route(nullptr, p, C).bytes;
     if ((st = check_ws(ctx, need)) != IVF_OK) return st;
     DeviceGuard g(ctx->device);
@@ -906,17 +964,21 @@ ivf_status ivf_route_noalloc(ivf_ctx *ctx, const float *queries, int64_t Q, cons
     if (st != IVF_OK || done) return st;
     // the batch of queries shrinks until the layout fits the static scratch;
     // sizes that do not fit with a single query are refused
-    RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank);
-    const size_t one = [&] {
+    RoutePlan p = plan_route(Q, C, nprobe, ctx->sample_rank, D);
+    auto one_query = [&] {
         RoutePlan q1 = p;
         q1.QB = 1;
         return layout_route(nullptr, q1, C).bytes;
-    }();
+    };
+    // the int8 route planes are left out (fp32 kernels only) when they do not
+    // fit beside one query
+    if (one_query() > kStaticScratchBytes) p.qdp = 0;
+    const size_t one = one_query();
     if (one > kStaticScratchBytes)
         return fail(ctx, IVF_EUNSUPPORTED,
                     "route_noalloc: C = %lld, nprobe = %d need %zu bytes of scratch for one query; the static "
                     "scratch holds %zu", (long long)C, nprobe, one, kStaticScratchBytes);
-    const size_t per_query = layout_route(nullptr, RoutePlan{2, p.Cs, p.L, p.rank_j}, C).bytes - one;
+    const size_t per_query = layout_route(nullptr, RoutePlan{2, p.Cs, p.L, p.rank_j, p.qdp}, C).bytes - one;
     const int64_t fit = 1 + (int64_t)((kStaticScratchBytes - one) / std::max<size_t>(per_query, 1));
     if (p.QB > fit) p.QB = fit >= 64 ? fit / 32 * 32 : fit;
     while (p.QB > 1 && layout_route(nullptr, p, C).bytes > kStaticScratchBytes) --p.QB;

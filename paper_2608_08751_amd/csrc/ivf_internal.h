@@ -54,8 +54,8 @@ struct ScreenArgs {
     int64_t wl_cap;
     unsigned long long *stats;
     int force_fallback;
-    // top-1 only: when non-null and *gate == 0, the int8 screen has taken the
-    // call and this kernel returns at once
+    // when non-null and *gate == 0, the int8 screen has taken the call and
+    // this kernel returns at once
     const uint32_t *gate;
 };
 
@@ -101,8 +101,9 @@ struct ScreenI8Args {
 int64_t quantized_pad(int64_t C);
 // the single plane (qc1, negb1) is padded to whole staged chunks of 256
 int64_t quantized_pad1(int64_t C);
+// skip (may be null): when *skip is nonzero the kernel does nothing
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
-                                     uint32_t *q_bad, hipStream_t s);
+                                     uint32_t *q_bad, hipStream_t s, const uint32_t *skip = nullptr);
 // Eight waves per workgroup (two per SIMD), one workgroup per CU.
 hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
 // Single-plane int8 screen (DP <= 128): plane rint(c - 128) [quantized_pad1(C)][DP],
@@ -141,9 +142,42 @@ struct RouteArgs {
     int32_t *wl;            // [nq]
     uint32_t *wl_cnt;
     unsigned long long *stats;
+    // keys from the int8 route kernels while *i8_off == 0 (null: fp32 only):
+    // their per-query bound qbound replaces the fp32 key bound
+    const uint32_t *i8_off;
+    const float *qbound;    // [nq]
 };
 
 hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s);
+// Int8 routing of uint8-valued queries on the two quantised planes
+// (screen_i8.hip): keys of the threshold sample and the candidate filter,
+// run only while *off == 0; route_i8_check raises *off when some query value
+// is not an integer in [0, 255], route_i8_bound when *q_bad is set, and
+// writes the per-query bound of the int8 keys.
+constexpr int kQuantChunk = 64;  // centroids per staged chunk of the two-plane kernels
+constexpr int kRouteKeys = 0;
+constexpr int kRouteFilter = 1;
+struct RouteI8Args {
+    const float *queries;   // [nq, D]
+    int64_t nq;
+    int D;
+    const int8_t *qc;       // two planes [cpad][2 DP] and biases [cpad] (quantize_kernel)
+    const int32_t *negb;
+    int64_t cpad;
+    int64_t c_begin, c_end; // centroid range; chunks of 64 from c_begin
+    int64_t nchunks;
+    const uint32_t *off;
+    float *keys;            // keys mode: [nq, c_end - c_begin]
+    const float *tau;       // filter mode: [nq], lists [nq, L]
+    uint32_t *cand_cnt;
+    uint2 *cand;
+    int L;
+    unsigned long long *stats;  // [kStatScreenI8] = 1 when the int8 filter ran
+};
+hipError_t launch_route_i8_check(const float *queries, int64_t nq, int D, uint32_t *off, hipStream_t s);
+hipError_t launch_route_i8_bound(const float *queries, int64_t nq, int D, const uint32_t *q_bad, uint32_t *off,
+                                 float *qbound, hipStream_t s);
+hipError_t launch_route_i8(int mode, int DP, const RouteI8Args &a, int num_cus, hipStream_t s);
 hipError_t launch_route_select(const RouteArgs &a, hipStream_t s);
 hipError_t launch_route_fallback(const RouteArgs &a, int grid, hipStream_t s);
 

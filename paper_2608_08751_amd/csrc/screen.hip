@@ -727,8 +727,8 @@ __global__ __launch_bounds__(W * 64, waves_per_simd<DP>()) void screen_kernel(Sc
     __shared__ __attribute__((aligned(16))) float lds_c[2 * kChunk * (DP + 4)];
     __shared__ __attribute__((aligned(16))) float lds_n[2 * kChunk];
     const int64_t ntiles = (a.nrows + 32 * W - 1) / (32 * W);
+    if (a.gate && *a.gate == 0u) return;  // screened on int8 MFMA instead
     if constexpr (MODE == kModeTop1) {
-        if (a.gate && *a.gate == 0u) return;  // screened on int8 MFMA instead
         for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
             screen_top1<DP, W, XT>(a, tile, lds_c, lds_n);
             __syncthreads();

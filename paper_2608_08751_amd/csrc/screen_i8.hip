@@ -35,6 +35,7 @@
 #include "ivf_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 #include <utility>
 
 namespace ivf {
@@ -43,7 +44,7 @@ namespace {
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kQChunk = 64;          // centroids per staged chunk (sub-chunk of the single plane)
+constexpr int kQChunk = kQuantChunk;  // centroids per staged chunk (sub-chunk of the single plane)
 constexpr int kS1Sub = 4;            // 64-centroid sub-chunks per staged chunk of the single plane
 constexpr int kS1Chunk = kS1Sub * kQChunk;
 constexpr int kNoScore = INT32_MIN;  // score of a padded centroid (below any real score)
@@ -64,8 +65,10 @@ constexpr int rows_blocks()
 // lowest score.
 __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__ cent, int64_t C, int D,
                                                        int DP, int64_t Cpad, int8_t *__restrict__ qc,
-                                                       int32_t *__restrict__ negb, uint32_t *__restrict__ q_bad)
+                                                       int32_t *__restrict__ negb, uint32_t *__restrict__ q_bad,
+                                                       const uint32_t *__restrict__ skip)
 {
+    if (skip && *skip) return;  // no int8 screen reads the planes in this call
     const int lane = threadIdx.x & 63;
     const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
@@ -337,8 +340,92 @@ __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int
     asm volatile("" : "+v"(st.k1), "+v"(st.k2), "+v"(st.k3), "+v"(st.i1), "+v"(st.i2), "+v"(st.t3));
 }
 
-template <int g, int T, int KS>
-__device__ __forceinline__ void i8_groups_at(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+// Routing epilogues of the two-plane tile (uint8-valued queries): keys of
+// the threshold sample, or the filter that lists every centroid whose key is
+// at most the query's threshold. The key of a centroid is -(float)s, which
+// orders the centroids like their distances up to the bound of the routing
+// certificate (the screening error of s plus the rounding to fp32).
+struct RouteKeysState {
+    float *krow;      // the row's keys, indexed by centroid id - c_begin; null: no row
+    int64_t c_begin, c_end;
+};
+
+// Candidates are queued per thread and row block in LDS (kRouteQueue
+// entries (s, id); entry e of thread t at q[e * threads + t] of the row
+// block's queue) and moved to the query's list with one atomic per thread
+// when some lane of the wave could overflow its queue and at the end of the
+// range. The queue takes every score with s >= sthr, a necessary condition
+// for -(float)s <= tau; the flush keeps the exact ones.
+constexpr int kRouteQueue = 12;
+
+struct RouteFilterState {
+    int t3;           // prefilter on the H accumulators: a key <= tau needs H >= t3
+    int sthr;         // and s >= sthr
+    float tau;
+    int64_t row;      // -1: no row
+    uint32_t *cand_cnt;
+    uint2 *cand;
+    int L;
+    uint2 *q;         // this thread's queue (stride qstride)
+    int qstride;
+    int qn;
+};
+
+__device__ __forceinline__ void route_flush(RouteFilterState &st)
+{
+    if (st.qn > 0 && st.row >= 0) {
+        uint32_t n = 0;
+        for (int i = 0; i < st.qn; ++i) n += -(float)(int)st.q[i * st.qstride].x <= st.tau ? 1u : 0u;
+        if (n) {
+            uint32_t slot = atomicAdd(st.cand_cnt + st.row, n);
+            uint2 *dst = st.cand + st.row * st.L;
+            for (int i = 0; i < st.qn; ++i) {
+                const uint2 e = st.q[i * st.qstride];
+                const float k = -(float)(int)e.x;
+                if (k <= st.tau) {
+                    if (slot < (uint32_t)st.L) dst[slot] = make_uint2(__float_as_uint(k), e.y);
+                    ++slot;
+                }
+            }
+        }
+    }
+    st.qn = 0;
+}
+
+template <int g>
+__device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int idp, RouteKeysState &st)
+{
+    const int64_t id0 = (int64_t)idp + 8 * g;
+    if (st.krow && id0 >= st.c_begin && id0 + 3 < st.c_end) {
+        float k[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) k[e] = -(float)((int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e]);
+        *reinterpret_cast<float4 *>(st.krow + (id0 - st.c_begin)) = make_float4(k[0], k[1], k[2], k[3]);
+    }
+}
+
+template <int g>
+__device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int idp, RouteFilterState &st)
+{
+    const int m = max4i(pH[4 * g], pH[4 * g + 1], pH[4 * g + 2], pH[4 * g + 3]);
+    if (__any(m >= st.t3)) {
+        if (__any(st.qn > kRouteQueue - 4)) route_flush(st);
+        // branch-free: every value is written at the queue's end, which
+        // advances only for those that pass (sthr excludes rows past the
+        // queries and padded centroids, whose score is INT_MIN)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int v = (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e];
+            st.q[st.qn * st.qstride] = make_uint2((uint32_t)v, (uint32_t)(idp + 8 * g + e));
+            st.qn += v >= st.sthr ? 1 : 0;
+        }
+    }
+    // keeps the group at this point of the MFMA stream
+    asm volatile("" : "+v"(st.t3), "+v"(st.qn));
+}
+
+template <int g, int T, int KS, class S>
+__device__ __forceinline__ void i8_groups_at(const i32x16 &pH, const i32x16 &pL, int idp, S &st)
 {
     if constexpr (g < 4) {
         if constexpr (g * KS / 4 == T) i8_group<g>(pH, pL, idp, st);
@@ -384,9 +471,9 @@ __device__ __forceinline__ i32x16 load_bias(const int *Bh)
 // this block's fragments), each fragment register is refilled from the next
 // block (nA, nB) as soon as its last MFMA has been issued, so the LDS reads
 // of the next block overlap this tile's MFMAs.
-template <int DP, bool PF, int T = 0>
+template <int DP, bool PF, int T = 0, class S>
 __device__ __forceinline__ void i8_tile(Frags<DP> &f, const i32x4 (&x)[DP / 32], i32x16 &bias, i32x16 &cH,
-                                        i32x16 &cL, const i32x16 &pH, const i32x16 &pL, int idp, Top3i &sp,
+                                        i32x16 &cL, const i32x16 &pH, const i32x16 &pL, int idp, S &sp,
                                         const char *nA, const int *nB)
 {
     constexpr int KS = DP / 32;
@@ -410,8 +497,8 @@ __device__ __forceinline__ void i8_tile(Frags<DP> &f, const i32x4 (&x)[DP / 32],
     }
 }
 
-template <int g = 0>
-__device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int idp, Top3i &st)
+template <int g = 0, class S>
+__device__ __forceinline__ void i8_drain(const i32x16 &pH, const i32x16 &pL, int idp, S &st)
 {
     if constexpr (g < 4) {
         i8_group<g>(pH, pL, idp, st);
@@ -632,6 +719,283 @@ hipError_t launch_i8_w(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s
     case 128: return launch_i8<128, W>(a, num_cus, s);
     case 192: return launch_i8<192, W>(a, num_cus, s);
     case 256: return launch_i8<256, W>(a, num_cus, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+// ============================================================ routing
+// Routing of uint8-valued queries (integers in [0, 255] stored as fp32) on
+// the two planes: x' = q - 128 is exact in int8, and the key -(float)s of a
+// centroid differs from 128 k(c) minus a per-query constant by less than
+// R + 64 (R = 131 + ||x'||_1 / 2 from the screening, 64 from rounding s to
+// fp32), so the routing certificate of the fp32 path holds with the bound
+// B = R + 64 in these key units (Sec. "GPU coarse search": the routing
+// contraction; the exactness argument is that of the assignment screens).
+// route_i8_check checks every query value before the centroids are
+// quantised, route_i8_bound writes B per query; when some value is not an
+// integer in [0, 255] or some centroid does not quantise (*q_bad), *off is
+// raised and the fp32 kernels, which check the same flag, take the call.
+
+// Raises *off when some value of the nq queries is not an integer in
+// [0, 255] (one wave per query, grid-stride).
+__global__ __launch_bounds__(256) void route_i8_check_kernel(const float *__restrict__ Q, int64_t nq, int D,
+                                                             uint32_t *__restrict__ off)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    bool bad = false;
+    for (int64_t q = w0; q < nq; q += nw) {
+        for (int d = lane; d < D; d += 64) {
+            const float v = Q[q * D + d];
+            if (!(v >= 0.0f && v <= 255.0f && v == rintf(v))) bad = true;  // also true for NaN
+        }
+    }
+    if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(off, 1u);  // one atomic per workgroup
+}
+
+// Per query of a batch (one wave each): qbound[q] = B = (390 + ||x'||_1) / 2;
+// raises *off when *q_bad (a centroid outside the two planes' range) is set.
+__global__ __launch_bounds__(256) void route_i8_bound_kernel(const float *__restrict__ Q, int64_t nq, int D,
+                                                             const uint32_t *__restrict__ q_bad,
+                                                             uint32_t *__restrict__ off, float *__restrict__ qbound)
+{
+    if (*off) return;  // the fp32 kernels take this call
+    const int lane = threadIdx.x & 63;
+    const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    if (w0 == 0 && lane == 0 && *q_bad) atomicOr(off, 1u);
+    for (int64_t q = w0; q < nq; q += nw) {
+        uint32_t l1 = 0;
+        for (int d = lane; d < D; d += 64) {
+            const int x = (int)Q[q * D + d] - 128;
+            l1 += (uint32_t)(x < 0 ? -x : x);
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) l1 += __shfl_xor(l1, o);
+        if (lane == 0) qbound[q] = 0.5f * (float)(390u + l1);
+    }
+}
+
+// Row block rb of this wave from fp32 queries that hold integers in
+// [0, 255]: x' = q - 128 as int8 (dimensions >= D zero), l1 = ||x'||_1 of
+// the lane's half (the caller adds the other half).
+template <int DP, int RB>
+__device__ __forceinline__ void load_queries(const float *__restrict__ Q, int64_t row0, int64_t nrows, int D,
+                                             int wave, int jl, int h, i32x4 (&xf)[RB][DP / 32],
+                                             uint32_t (&l1)[RB], int64_t (&rowid)[RB])
+{
+    constexpr int KS = DP / 32;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
+        const bool rv = row < nrows;
+        rowid[rb] = rv ? row : -1;
+        const float *qr = Q + (rv ? row : 0) * (int64_t)D + 16 * h;
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const int d = 32 * k + 16 * h + 4 * w;
+                uint32_t packed = 0;
+                if (rv && d < D) {
+                    const float4 v = *reinterpret_cast<const float4 *>(qr + 32 * k + 4 * w);
+                    const float va[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int x = (int)va[e] - 128;
+                        packed |= ((uint32_t)x & 0xFFu) << (8 * e);
+                        s += (uint32_t)(x < 0 ? -x : x);
+                    }
+                }
+                xf[rb][k][w] = (int)packed;
+            }
+        }
+        l1[rb] = s;
+    }
+}
+
+// Chunks [ch_lo, ch_hi) of the range's 64-centroid chunks (chunk j starts at
+// centroid c_begin + 64 j) against one tile of queries, with the keys or
+// the filter epilogue; the staging and the MFMA stream are those of
+// screen_i8_tile.
+template <int DP, int W, int MODE>
+__device__ void route_i8_range(const RouteI8Args &a, int64_t tile, int64_t ch_lo, int64_t ch_hi,
+                               char *__restrict__ lds, uint2 *__restrict__ queue)
+{
+    constexpr int RB = rows_blocks<DP>();
+    constexpr int NT = W * 64;
+    using St = QStager<DP, NT>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    constexpr int BLK = 32 * St::kPitch;
+    using S = typename std::conditional<MODE == kRouteKeys, RouteKeysState, RouteFilterState>::type;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int h = lane >> 5;
+    const int jl = lane & 31;
+    const int64_t row0 = tile * (W * 32 * RB);
+
+    i32x4 xf[RB][DP / 32];
+    uint32_t l1[RB];
+    int64_t rowid[RB];
+    load_queries<DP, RB>(a.queries, row0, a.nq, a.D, wave, jl, h, xf, l1, rowid);
+
+    S st[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        l1[rb] += __shfl_xor(l1[rb], 32);
+        const int64_t row = rowid[rb];
+        if constexpr (MODE == kRouteKeys) {
+            st[rb].krow = row >= 0 ? a.keys + row * (a.c_end - a.c_begin) : nullptr;
+            st[rb].c_begin = a.c_begin;
+            st[rb].c_end = a.c_end;
+        } else {
+            st[rb].row = row;
+            st[rb].cand_cnt = a.cand_cnt;
+            st[rb].cand = a.cand;
+            st[rb].L = a.L;
+            st[rb].tau = row >= 0 ? a.tau[row] : -__builtin_huge_valf();
+            // a key <= tau needs s >= -tau - 64, and s <= 256 H + 128 ||x'||_1
+            const double t = floor((-(double)st[rb].tau - 64.0 - 128.0 * (double)l1[rb]) / 256.0);
+            st[rb].t3 = row < 0 || !(t <= 2147483647.0) ? INT_MAX : t < -2147483648.0 ? INT_MIN : (int)t;
+            // s > INT_MIN for every real centroid: padded ones (s = INT_MIN) never pass
+            const double u = ceil(-(double)st[rb].tau - 64.0);
+            st[rb].sthr = row < 0 || !(u <= 2147483647.0) ? INT_MAX : u < -2147483647.0 ? INT_MIN + 1 : (int)u;
+            st[rb].q = queue + rb * kRouteQueue * NT + threadIdx.x;
+            st[rb].qstride = NT;
+            st[rb].qn = 0;
+        }
+    }
+
+    const char *A0 = lds + jl * St::kPitch + 16 * h;
+    const char *B0 = lds + St::kBias + 16 * h;
+    const int64_t cb0 = a.c_begin + ch_lo * kQChunk;  // first centroid of the range's chunk 0
+    const int idh = (int)cb0 + 4 * h;
+    const int nch = (int)(ch_hi - ch_lo);
+    auto abuf = [&](int jj) { return A0 + (jj & 1) * CS; };
+    auto bbuf = [&](int jj) { return reinterpret_cast<const int *>(B0 + (jj & 1) * CS); };
+
+    St q;
+    q.init();
+    q.fetch(a.qc, a.negb, cb0, a.cpad, lds);
+    __syncthreads();
+    q.fetch(a.qc, a.negb, cb0 + kQChunk, a.cpad, lds + CS);
+    auto stage = [&](int jj) {
+        __syncthreads();
+        q.fetch(a.qc, a.negb, cb0 + (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
+    };
+
+    // T1 starts as a tile of lowest scores: the first epilogue keeps nothing
+    // (its ids lie before the range)
+    i32x16 h0, l0, h1, l1acc = {0};
+#pragma unroll
+    for (int r = 0; r < 16; ++r) h1[r] = kNoBias;
+    i32x16 bias = load_bias(bbuf(0));
+    Frags<DP> f;
+    load_frags<DP>(abuf(0), f);
+    // the block before the range: keys are written only inside the range and
+    // the filter's first drain sees only lowest scores
+    S none = st[RB - 1];
+    if constexpr (MODE == kRouteKeys) {
+        none.krow = nullptr;
+    } else {
+        none.row = -1;
+        none.sthr = INT_MAX;
+    }
+
+    if constexpr (RB == 2) {
+        auto rows0 = [&](int jj, int cb, S &sp) {
+            i8_tile<DP, false>(f, xf[0], bias, h0, l0, h1, l1acc, idh + jj * kQChunk + 32 * cb - 32, sp,
+                               nullptr, nullptr);
+        };
+        auto rows1 = [&](int jj, int cb, const char *nA, const int *nB) {
+            i8_tile<DP, true>(f, xf[1], bias, h1, l1acc, h0, l0, idh + jj * kQChunk + 32 * cb, st[0], nA, nB);
+        };
+        rows0(0, 0, none);
+        rows1(0, 0, abuf(0) + BLK, bbuf(0) + 32);
+        rows0(0, 1, st[1]);
+        stage(1);
+        for (int j = 0;; ++j) {
+            rows1(j, 1, abuf(j + 1), bbuf(j + 1));
+            if (j + 1 == nch) break;
+            rows0(j + 1, 0, st[1]);
+            rows1(j + 1, 0, abuf(j + 1) + BLK, bbuf(j + 1) + 32);
+            rows0(j + 1, 1, st[1]);
+            stage(j + 2);
+        }
+    } else {
+        auto blk0 = [&](int jj, S &sp) {
+            i8_tile<DP, true>(f, xf[0], bias, h0, l0, h1, l1acc, idh + jj * kQChunk - 32, sp, abuf(jj) + BLK,
+                              bbuf(jj) + 32);
+        };
+        auto blk1 = [&](int jj) {
+            i8_tile<DP, true>(f, xf[0], bias, h1, l1acc, h0, l0, idh + jj * kQChunk, st[0], abuf(jj + 1),
+                              bbuf(jj + 1));
+        };
+        blk0(0, none);
+        stage(1);
+        for (int j = 0;; ++j) {
+            blk1(j);
+            if (j + 1 == nch) break;
+            blk0(j + 1, st[0]);
+            stage(j + 2);
+        }
+    }
+    i8_drain(h1, l1acc, idh + (nch - 1) * kQChunk + 32, st[RB - 1]);
+    if constexpr (MODE == kRouteFilter) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) route_flush(st[rb]);
+    }
+}
+
+template <int DP, int W, int MODE>
+__global__ __launch_bounds__(W * 64, 2) void route_i8_kernel(RouteI8Args a)
+{
+    using St = QStager<DP, W * 64>;
+    constexpr int CS = (St::kBytes + 15) / 16 * 16;
+    __shared__ __attribute__((aligned(16))) char lds[2 * CS];
+    __shared__ uint2 queue[MODE == kRouteFilter ? rows_blocks<DP>() * kRouteQueue * W * 64 : 1];
+    if (*a.off) return;  // the fp32 kernels take this call
+    if (MODE == kRouteFilter && blockIdx.x == 0 && threadIdx.x == 0 && a.stats) a.stats[kStatScreenI8] = 1ull;
+    constexpr int rows_per_tile = W * 32 * rows_blocks<DP>();
+    const int64_t ntiles = (a.nq + rows_per_tile - 1) / rows_per_tile;
+    // a contiguous range of (tile, chunk) units in tile-major order
+    const int64_t units = ntiles * a.nchunks;
+    int64_t u = units * blockIdx.x / gridDim.x;
+    const int64_t u1 = units * (blockIdx.x + 1) / gridDim.x;
+    while (u < u1) {
+        const int64_t tile = u / a.nchunks;
+        const int64_t ch = u - tile * a.nchunks;
+        const int64_t ch_end = min(a.nchunks, ch + (u1 - u));
+        route_i8_range<DP, W, MODE>(a, tile, ch, ch_end, lds, queue);
+        u += ch_end - ch;
+        __syncthreads();
+    }
+}
+
+template <int DP, int MODE>
+hipError_t launch_route_i8_dp(const RouteI8Args &a, int num_cus, hipStream_t s)
+{
+    constexpr int W = 8;
+    constexpr int rows_per_tile = W * 32 * rows_blocks<DP>();
+    const int64_t ntiles = (a.nq + rows_per_tile - 1) / rows_per_tile;
+    const int64_t units = ntiles * a.nchunks;
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(units, (int64_t)num_cus));
+    hipLaunchKernelGGL((route_i8_kernel<DP, W, MODE>), dim3(grid), dim3(W * 64), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_route_i8_mode(int DP, const RouteI8Args &a, int num_cus, hipStream_t s)
+{
+    switch (DP) {
+    case 32: return launch_route_i8_dp<32, MODE>(a, num_cus, s);
+    case 64: return launch_route_i8_dp<64, MODE>(a, num_cus, s);
+    case 96: return launch_route_i8_dp<96, MODE>(a, num_cus, s);
+    case 128: return launch_route_i8_dp<128, MODE>(a, num_cus, s);
+    case 192: return launch_route_i8_dp<192, MODE>(a, num_cus, s);
+    case 256: return launch_route_i8_dp<256, MODE>(a, num_cus, s);
     default: return hipErrorInvalidValue;
     }
 }
@@ -995,12 +1359,12 @@ int64_t quantized_pad(int64_t C) { return (C + kQChunk - 1) / kQChunk * kQChunk;
 int64_t quantized_pad1(int64_t C) { return (C + kS1Chunk - 1) / kS1Chunk * kS1Chunk; }
 
 hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP, int8_t *qc, int32_t *negb,
-                                     uint32_t *q_bad, hipStream_t s)
+                                     uint32_t *q_bad, hipStream_t s, const uint32_t *skip)
 {
     const int64_t cpad = quantized_pad(C);
-    const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
+    const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 8192);
     hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, qc, negb,
-                       q_bad);
+                       q_bad, skip);
     return hipGetLastError();
 }
 
@@ -1034,6 +1398,31 @@ hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStrea
 {
     if (a.nrows <= 0) return hipSuccess;
     return launch_i8_w<8>(DP, a, num_cus, s);
+}
+
+hipError_t launch_route_i8_check(const float *queries, int64_t nq, int D, uint32_t *off, hipStream_t s)
+{
+    if (nq <= 0) return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((nq + 3) / 4, 1024);
+    hipLaunchKernelGGL(route_i8_check_kernel, dim3((unsigned)blocks), dim3(256), 0, s, queries, nq, D, off);
+    return hipGetLastError();
+}
+
+hipError_t launch_route_i8_bound(const float *queries, int64_t nq, int D, const uint32_t *q_bad, uint32_t *off,
+                                 float *qbound, hipStream_t s)
+{
+    if (nq <= 0) return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((nq + 3) / 4, 65536);
+    hipLaunchKernelGGL(route_i8_bound_kernel, dim3((unsigned)blocks), dim3(256), 0, s, queries, nq, D, q_bad, off,
+                       qbound);
+    return hipGetLastError();
+}
+
+hipError_t launch_route_i8(int mode, int DP, const RouteI8Args &a, int num_cus, hipStream_t s)
+{
+    if (a.nq <= 0 || a.nchunks <= 0) return hipSuccess;
+    return mode == kRouteKeys ? launch_route_i8_mode<kRouteKeys>(DP, a, num_cus, s)
+                              : launch_route_i8_mode<kRouteFilter>(DP, a, num_cus, s);
 }
 
 }  // namespace ivf

@@ -361,7 +361,8 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a)
     for (int d = threadIdx.x; d < a.D; d += blockDim.x) qrow[d] = a.queries[q * a.D + d];
     if (threadIdx.x == 0) s_nr = 0;
     const double kth = (double)o2f(block_select(v, nv, a.k, hist, sh));
-    const double B2 = 2.0 * key_bound(a.bound_coef, *a.mc2_bits, a.qn2[q]);
+    const double B2 = a.i8_off && *a.i8_off == 0u ? 2.0 * (double)a.qbound[q]
+                                                  : 2.0 * key_bound(a.bound_coef, *a.mc2_bits, a.qn2[q]);
     if (!((double)a.tau[q] >= kth + B2)) {
         if (threadIdx.x == 0) push_fallback(a, q, false);
         return;

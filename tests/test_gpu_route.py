@@ -144,11 +144,23 @@ def _sampled_full_size(ctx, oracle_mod, d, k, nsample):
 
 
 def test_route_uint8_full_size_sampled(ivf_ctx, oracle_mod):
-    """65,536 centroids, 10,000 queries, nprobe 64: 150 sampled queries + plants."""
-    d = synth.uniform_mixture_route(65536, 10000, 128, seed=0)
-    stats = _sampled_full_size(ivf_ctx, oracle_mod, d, 64, 150)
+    """65,536 centroids, 10,000 integer-valued queries, nprobe 64 (the int8
+    planes): 200 sampled queries against the oracle."""
+    d = synth.uniform_mixture_route(65536, 10000, 128, seed=0, plants=0)
+    stats = _sampled_full_size(ivf_ctx, oracle_mod, d, 64, 200)
     print("route u8 full-size stats:", stats)
+    assert stats["screen_i8"] == 1
     assert stats["fallback"] < 100  # < 1% of queries
+
+
+def test_route_uint8_full_size_with_plants_sampled(ivf_ctx, oracle_mod):
+    """The same workload with 16 queries replaced by (non-integral) centroids:
+    the call takes the fp32 kernels; the plants route to their centroid at
+    distance 0."""
+    d = synth.uniform_mixture_route(65536, 10000, 128, seed=0)
+    stats = _sampled_full_size(ivf_ctx, oracle_mod, d, 64, 100)
+    assert stats["screen_i8"] == 0
+    assert stats["fallback"] < 100
 
 
 def test_route_normalised_full_size_sampled(ivf_ctx, oracle_mod):
@@ -157,3 +169,61 @@ def test_route_normalised_full_size_sampled(ivf_ctx, oracle_mod):
     stats = _sampled_full_size(ivf_ctx, oracle_mod, d, 128, 60)
     print("route normalised full-size stats:", stats)
     assert stats["fallback"] < 100
+
+
+def _route_with_option(ctx, q, c, k, option, value):
+    import paper_2608_08751_amd as ivf
+
+    ctx.set_option(option, value)
+    try:
+        return run_route(ctx, q, c, k)
+    finally:
+        ctx.set_option(option, 0)
+
+
+@pytest.mark.parametrize("C,Q,D,k", [(9000, 700, 128, 64), (2100, 130, 64, 16), (2500, 50, 96, 30),
+                                     (4500, 300, 256, 40), (3001, 77, 36, 5)])
+def test_route_int8_and_fp32_paths_agree(ivf_ctx, oracle_mod, C, Q, D, k):
+    """Uint8-valued queries are routed on the two int8 planes (tables above
+    2,048 centroids); forcing the fp32 kernels must give the same ids and
+    distances (both exact)."""
+    import paper_2608_08751_amd as ivf
+
+    d = synth.uniform_mixture_route(C, Q, D, seed=C + D, plants=0)
+    stats = assert_route_equal(ivf_ctx, oracle_mod, d["queries"], d["centroids"], k)
+    assert stats["screen_i8"] == 1
+    ids, dist, _ = run_route(ivf_ctx, d["queries"], d["centroids"], k)
+    fids, fdist, fstats = _route_with_option(ivf_ctx, d["queries"], d["centroids"], k, ivf.IVF_OPT_FP32_SCREEN, 1)
+    assert fstats["screen_i8"] == 0
+    assert (ids == fids).all() and (dist == fdist).all()
+
+
+@pytest.mark.parametrize("where", ["query", "centroid_high", "centroid_low"])
+def test_route_values_outside_the_int8_path_take_fp32(ivf_ctx, oracle_mod, where):
+    """A non-integral query value or a centroid outside the two planes'
+    range sends the whole call to the fp32 kernels, with exact results."""
+    d = synth.uniform_mixture_route(6000, 200, 128, seed=7, plants=0)
+    q, c = d["queries"].copy(), d["centroids"].copy()
+    if where == "query":
+        q[123, 45] += 0.5
+    elif where == "centroid_high":
+        c[4321, 7] = 300.0
+    else:
+        c[17, 100] = -2.0
+    stats = assert_route_equal(ivf_ctx, oracle_mod, q, c, 32)
+    assert stats["screen_i8"] == 0
+
+
+def test_route_int8_forced_fallback_and_extreme_ranks(ivf_ctx, oracle_mod):
+    """The int8 keys and filter feed the same certified selection: too tight
+    or too loose thresholds and forced fallbacks stay exact."""
+    import paper_2608_08751_amd as ivf
+
+    d = synth.uniform_mixture_route(20000, 150, 128, seed=21, plants=0)
+    for opt, val in ((ivf.IVF_OPT_SAMPLE_RANK, 1), (ivf.IVF_OPT_SAMPLE_RANK, 400), (ivf.IVF_OPT_FORCE_FALLBACK, 1)):
+        ivf_ctx.set_option(opt, val)
+        try:
+            stats = assert_route_equal(ivf_ctx, oracle_mod, d["queries"], d["centroids"], 64)
+            assert stats["screen_i8"] == 1
+        finally:
+            ivf_ctx.set_option(opt, 0)

@@ -254,3 +254,61 @@ def test_single_plane_int32_headroom():
         x = np.full((1, D), xv, np.int64)
         s1 = (x - 128) @ H1.T - b1[None, :]
         assert np.abs(s1).max() < 2 ** 23
+
+
+def _f32(v):
+    return float(np.float32(v))
+
+
+def test_route_key_bound_exact_arithmetic():
+    """Routing of uint8-valued queries keys each centroid by -(float)s: its
+    distance to 128 k + 128 sum(x') stays below B = (390 + ||x'||_1) / 2
+    (the screening bound R = 131 + ||x'||_1 / 2 plus 64 for rounding s to
+    fp32), including scores beyond 2^24 where the rounding is not exact."""
+    rng = np.random.default_rng(7)
+    for D in (16, 256):
+        C = 24
+        c = centroids(rng, C, D)
+        c[3] = 0.0     # large ||c'||^2 and x'.c' magnitudes
+        c[4] = 255.99
+        x = rng.integers(0, 256, size=(12, D))
+        x[0] = 0
+        x[1] = 255
+        _, H, Ls, Bh = quantise(c)
+        s = score(x, H, Ls, Bh)
+        assert np.abs(s).max() > 2 ** 24  # the fp32 rounding of s is exercised
+        cf = [[Fraction(float(v)) - 128 for v in row] for row in c]
+        for i in range(x.shape[0]):
+            xp = [int(v) - 128 for v in x[i]]
+            B = Fraction(390 + sum(abs(v) for v in xp), 2)
+            for j in range(C):
+                k = sum(v * v for v in cf[j]) - 2 * sum(a * b for a, b in zip(xp, cf[j]))
+                key = Fraction(-_f32(int(s[i, j])))
+                assert abs(key - (128 * k + 128 * sum(xp))) < B
+
+
+def test_route_filter_thresholds_are_necessary():
+    """The filter keeps -(float)s <= tau; its integer test s >= ceil(-tau - 64)
+    and its prefilter h >= floor((-tau - 64 - 128 ||x'||_1) / 256) on the H
+    plane (h = x'.H - Bh) never reject a score that passes."""
+    import math
+
+    rng = np.random.default_rng(8)
+    D, C = 128, 64
+    c = centroids(rng, C, D)
+    x = rng.integers(0, 256, size=(8, D))
+    _, H, Ls, Bh = quantise(c)
+    s = score(x, H, Ls, Bh)
+    h = hpart(x, H, Bh)
+    l1 = np.abs(x.astype(np.int64) - 128).sum(axis=1)
+    for i in range(x.shape[0]):
+        for j in range(C):
+            key = -_f32(int(s[i, j]))
+            # thresholds at, just above and just below the key (fp32 grid)
+            for tau in (key, _f32(np.nextafter(np.float32(key), np.float32(np.inf))),
+                        _f32(np.nextafter(np.float32(key), np.float32(-np.inf)))):
+                passes = key <= tau
+                sthr = math.ceil(-tau - 64.0)
+                t3 = math.floor((-tau - 64.0 - 128.0 * float(l1[i])) / 256.0)
+                if passes:
+                    assert int(s[i, j]) >= sthr and int(h[i, j]) >= t3

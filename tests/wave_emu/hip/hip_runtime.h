@@ -36,6 +36,8 @@ struct uint2 {
 struct float4 {
     float x, y, z, w;
 };
+inline uint2 make_uint2(unsigned x, unsigned y) { return uint2{x, y}; }
+inline float4 make_float4(float x, float y, float z, float w) { return float4{x, y, z, w}; }
 struct longlong2 {
     long long x, y;
 };
@@ -59,6 +61,7 @@ struct Block {
     Wave waves[16];
     std::mutex mu;
     std::vector<std::pair<char *, std::array<char, 16>>> pending;  // LDS writes of in-flight loads
+    std::atomic<int> or_acc{0};  // __syncthreads_or
 };
 extern Block *blk;
 // dynamic LDS of the running block (the launch's shared-memory bytes)
@@ -94,6 +97,18 @@ inline long max(long a, long b) { return a > b ? a : b; }
 inline long min(long a, long b) { return a < b ? a : b; }
 
 inline void __syncthreads() { emu::blk->bar->arrive_and_wait(); }
+
+// block-wide OR of p, a barrier like __syncthreads
+inline int __syncthreads_or(int p)
+{
+    if (p) emu::blk->or_acc.fetch_or(1);
+    __syncthreads();
+    const int r = emu::blk->or_acc.load();
+    __syncthreads();
+    if (emu::tid.x == 0) emu::blk->or_acc.store(0);
+    __syncthreads();
+    return r;
+}
 
 template <typename T>
 inline T __shfl_xor(T v, int m)
@@ -279,6 +294,7 @@ inline unsigned long long atomicAdd(unsigned long long *p, unsigned long long v)
 {
     return __atomic_fetch_add(p, v, __ATOMIC_SEQ_CST);
 }
+inline uint32_t atomicOr(uint32_t *p, uint32_t v) { return __atomic_fetch_or(p, v, __ATOMIC_SEQ_CST); }
 inline uint32_t atomicMax(uint32_t *p, uint32_t v)
 {
     uint32_t o = __atomic_load_n(p, __ATOMIC_SEQ_CST);
