@@ -912,9 +912,10 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
             a.cand = l.cand;
             a.L = p.L;
             if (i8) {
-                ra.c_begin = p.Cs;
+                // the int8 threshold emits no sample candidates: the filter covers every centroid
+                ra.c_begin = 0;
                 ra.c_end = C;
-                ra.nchunks = (C - p.Cs + kQuantChunk - 1) / kQuantChunk;
+                ra.nchunks = (C + kQuantChunk - 1) / kQuantChunk;
                 ra.keys = nullptr;
                 ra.tau = l.tau;
                 ra.cand_cnt = l.cand_cnt;

@@ -167,7 +167,7 @@ struct RouteI8Args {
     int64_t c_begin, c_end; // centroid range; chunks of 64 from c_begin
     int64_t nchunks;
     const uint32_t *off;
-    float *keys;            // keys mode: [nq, c_end - c_begin]
+    float *keys;            // keys mode: group minima [nq, (c_end - c_begin) / 16] (c_begin, c_end multiples of 16)
     const float *tau;       // filter mode: [nq], lists [nq, L]
     uint32_t *cand_cnt;
     uint2 *cand;

@@ -345,9 +345,13 @@ __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int
 // at most the query's threshold. The key of a centroid is -(float)s, which
 // orders the centroids like their distances up to the bound of the routing
 // certificate (the screening error of s plus the rounding to fp32).
+// The keys pass writes, per row, the minimum key of every 16 consecutive
+// centroids of the sample (the two half-lanes of a row each hold 8 of them),
+// which is all the threshold needs.
 struct RouteKeysState {
-    float *krow;      // the row's keys, indexed by centroid id - c_begin; null: no row
+    float *krow;      // the row's group minima, indexed by (centroid id - c_begin) / 16; null: no row
     int64_t c_begin, c_end;
+    int acc;          // largest score of the current group of 16 on this half-lane
 };
 
 // Candidates are queued per thread and row block in LDS (kRouteQueue
@@ -395,12 +399,19 @@ __device__ __forceinline__ void route_flush(RouteFilterState &st)
 template <int g>
 __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int idp, RouteKeysState &st)
 {
-    const int64_t id0 = (int64_t)idp + 8 * g;
-    if (st.krow && id0 >= st.c_begin && id0 + 3 < st.c_end) {
-        float k[4];
+    // registers of groups 2m and 2m + 1 hold, over both half-lanes, the
+    // centroids 16m .. 16m + 15 of the 32-centroid block at idp - 4h
+    int m = (int)((uint32_t)pH[4 * g] << 8) + pL[4 * g];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) k[e] = -(float)((int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e]);
-        *reinterpret_cast<float4 *>(st.krow + (id0 - st.c_begin)) = make_float4(k[0], k[1], k[2], k[3]);
+    for (int e = 1; e < 4; ++e) m = max(m, (int)((uint32_t)pH[4 * g + e] << 8) + pL[4 * g + e]);
+    if constexpr (g % 2 == 0) {
+        st.acc = m;
+    } else {
+        m = max(m, st.acc);
+        m = max(m, __shfl_xor(m, 32));
+        const int64_t id0 = (int64_t)(idp & ~31) + 16 * (g / 2);
+        if (st.krow && (threadIdx.x & 32) == 0 && id0 >= st.c_begin && id0 + 15 < st.c_end)
+            st.krow[(id0 - st.c_begin) >> 4] = -(float)m;
     }
 }
 
@@ -847,9 +858,10 @@ __device__ void route_i8_range(const RouteI8Args &a, int64_t tile, int64_t ch_lo
         l1[rb] += __shfl_xor(l1[rb], 32);
         const int64_t row = rowid[rb];
         if constexpr (MODE == kRouteKeys) {
-            st[rb].krow = row >= 0 ? a.keys + row * (a.c_end - a.c_begin) : nullptr;
+            st[rb].krow = row >= 0 ? a.keys + row * ((a.c_end - a.c_begin) / 16) : nullptr;
             st[rb].c_begin = a.c_begin;
             st[rb].c_end = a.c_end;
+            st[rb].acc = INT_MIN;
         } else {
             st[rb].row = row;
             st[rb].cand_cnt = a.cand_cnt;

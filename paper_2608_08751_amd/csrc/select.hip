@@ -194,8 +194,12 @@ __device__ uint32_t block_select(const uint32_t (&v)[V], int nv, int k, uint32_t
 constexpr int kMaxGroups = 4096;
 constexpr int kGroupsPerThread = kMaxGroups / 256;
 
+// true when the int8 route kernels produce this call's keys (group minima)
+__device__ __forceinline__ bool int8_keys(const RouteArgs &a) { return a.i8_off && *a.i8_off == 0u; }
+
 __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
 {
+    if (int8_keys(a)) return;
     const int64_t q = blockIdx.x;
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh[2];
@@ -256,6 +260,7 @@ __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
 template <int GPT>
 __global__ __launch_bounds__(256) void route_threshold_reg_kernel(RouteArgs a)
 {
+    if (int8_keys(a)) return;
     const int64_t q = blockIdx.x;
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh[2];
@@ -305,6 +310,36 @@ __global__ __launch_bounds__(256) void route_threshold_reg_kernel(RouteArgs a)
     if (threadIdx.x == 0) {
         a.tau[q] = th;
         a.cand_cnt[q] = s_cnt;
+    }
+}
+
+// The threshold when the int8 route kernels ran: the keys buffer holds the
+// sample's group minima [nq, Cs / 16] directly, tau = the rank_j-th smallest,
+// and the sample's centroids are left to the filter, which then covers every
+// centroid (the candidate list starts empty).
+__global__ __launch_bounds__(256) void route_threshold_min_kernel(RouteArgs a)
+{
+    if (!int8_keys(a)) return;
+    const int64_t q = blockIdx.x;
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sh[2];
+    const int G = (int)(a.Cs / 16);
+    const float *kr = a.keys + q * G;
+    uint32_t v[kGroupsPerThread];
+    int nv = 0;
+#pragma unroll
+    for (int e = 0; e < kGroupsPerThread; ++e) {
+        const int g = threadIdx.x + 256 * e;
+        v[e] = 0xFFFFFFFFu;
+        if (g < G) {
+            v[e] = f2o(kr[g]);
+            nv = e + 1;
+        }
+    }
+    const float th = o2f(block_select(v, nv, min(a.rank_j, G), hist, sh));
+    if (threadIdx.x == 0) {
+        a.tau[q] = th;
+        a.cand_cnt[q] = 0;
     }
 }
 
@@ -495,6 +530,7 @@ hipError_t launch_row_norms(const float *rows, int64_t n, int D, double *out, hi
 hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s)
 {
     const int64_t G = a.Cs / 16;
+    if (a.i8_off && a.Cs > 0) hipLaunchKernelGGL(route_threshold_min_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
     if (a.Cs > 0 && G <= 256)
         hipLaunchKernelGGL(route_threshold_reg_kernel<1>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
     else if (a.Cs > 0 && G <= 512)
