@@ -771,7 +771,8 @@ __global__ __launch_bounds__(256) void route_i8_bound_kernel(const float *__rest
                                                              const uint32_t *__restrict__ q_bad,
                                                              uint32_t *__restrict__ off, float *__restrict__ qbound)
 {
-    if (*off) return;  // the fp32 kernels take this call
+    // (the bounds are written whatever *off says: a wave must not read the
+    // flag this kernel itself raises to decide whether to take part)
     const int lane = threadIdx.x & 63;
     const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
@@ -779,7 +780,8 @@ __global__ __launch_bounds__(256) void route_i8_bound_kernel(const float *__rest
     for (int64_t q = w0; q < nq; q += nw) {
         uint32_t l1 = 0;
         for (int d = lane; d < D; d += 64) {
-            const int x = (int)Q[q * D + d] - 128;
+            const float v = Q[q * D + d];  // (a value outside [0, 255] has raised *off already)
+            const int x = v >= 0.0f && v <= 255.0f ? (int)v - 128 : 0;
             l1 += (uint32_t)(x < 0 ? -x : x);
         }
 #pragma unroll

@@ -54,12 +54,15 @@ def test_route_noalloc_matches_route_twice(ivf_ctx):
     # first call: 65,536 centroids, 4,000 queries (several batches of the
     # static scratch); second call: fewer centroids and queries, so stale
     # contents of the scratch from the first call lie beyond what it writes
-    cases = [(synth.uniform_mixture_route(65536, 4000, 128, seed=3), 64),
-             (synth.uniform_mixture_route(3000, 300, 64, seed=4), 16)]
-    for d, k in cases:
+    # (the first call has integer-valued queries only, so it routes on the
+    # int8 planes; the planted queries of the second send it to fp32)
+    cases = [(synth.uniform_mixture_route(65536, 4000, 128, seed=3, plants=0), 64, 1),
+             (synth.uniform_mixture_route(3000, 300, 64, seed=4), 16, 0)]
+    for d, k, i8 in cases:
         ids, dist, rids, rdist, st = route_both(ivf_ctx, d, k)
         print("noalloc route Q=%d C=%d k=%d stats %s" % (d["queries"].shape[0], d["centroids"].shape[0], k, st),
               flush=True)
+        assert st["screen_i8"] == i8
         assert np.array_equal(ids, rids)
         assert np.array_equal(dist.view(np.uint32), rdist.view(np.uint32))
         for qi, ci in zip(d["plant_q"], d["plant_c"]):
