@@ -183,10 +183,11 @@ def bench_route(ctx, name, d, k, oracle_s, full_oracle=False):
 
 # ------------------------------------------------------------------ k-means
 
-def bench_kmeans(ctx, N, iters, oracle_s):
+def bench_kmeans(ctx, N, iters, oracle_s, hints=True):
     """Lloyd's algorithm from the seeded row sample: `iters` iterations, each
-    one ivf_kmeans_step timed with HIP events; per iteration its time,
-    objective and screening statistics."""
+    one ivf_kmeans_step timed with HIP events (from the second on with the
+    previous iteration's labels as hints); per iteration its time, objective
+    and screening statistics."""
     import numpy as np
     import torch
 
@@ -198,7 +199,8 @@ def bench_kmeans(ctx, N, iters, oracle_s):
     x = torch.empty((N, D), dtype=torch.uint8, device="cuda")
     synth.device_mixture_rows_u8(means, 0, N, x, seed=0)
     c0 = x[dev(synth.kmeans_init(N, C, seed=0))].float().contiguous()
-    lab = torch.empty(N, dtype=torch.int32, device="cuda")
+    labs = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(2)]
+    lab = labs[0]
     cnt = torch.empty(C, dtype=torch.int64, device="cuda")
     obj = torch.empty(1, dtype=torch.float64, device="cuda")
     cbuf = [torch.empty((C, D), dtype=torch.float32, device="cuda") for _ in range(2)]
@@ -213,9 +215,11 @@ def bench_kmeans(ctx, N, iters, oracle_s):
     for it in range(iters):
         out = cbuf[it % 2]
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        lab = labs[it % 2]
+        hint = labs[(it + 1) % 2] if hints and it > 0 else None
         e0.record()
         ivf.ivf_kmeans_step(ctx, x, c, seed=0, it=it, out_labels=lab, out_centroids=out, out_counts=cnt,
-                            out_objective=obj)
+                            out_objective=obj, hint_labels=hint)
         e1.record()
         e1.synchronize()
         tl = ctx.kernel_times()
@@ -231,7 +235,8 @@ def bench_kmeans(ctx, N, iters, oracle_s):
     total = sum(r["ms"] for r in rows)
     ops = 2.0 * N * C * D * iters
     tops = ops / (total * 1e-3) / 1e12
-    res = {"rows": N, "centroids": C, "dim": D, "iterations": iters, "total_s": total * 1e-3,
+    res = {"rows": N, "centroids": C, "dim": D, "iterations": iters, "label_hints": bool(hints),
+           "total_s": total * 1e-3,
            "ms_per_iteration": total / iters, "vectors_per_s": N * iters / (total * 1e-3),
            "algorithmic_tops": tops, "int8_mfma_frac": tops / PEAK_INT8_MFMA_TOPS,
            "vs_fp32_mfma_peak_ratio": tops / PEAK_FP32_MFMA_TFLOPS,

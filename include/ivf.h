@@ -176,11 +176,17 @@ ivf_status ivf_route_noalloc(ivf_ctx *ctx, const float *queries, int64_t Q, cons
  *   out_counts     [C] int64 cluster sizes before reseeding, may be NULL
  *   out_objective  device fp64 scalar: sum over rows of the squared distance
  *                  to the assigned input centroid, may be NULL
+ *   hint_labels    [N] int32 or NULL: a label per row from an earlier step
+ *                  (the previous iteration's out_labels). Speed only: the
+ *                  single-plane int8 screen starts each row's keep threshold
+ *                  from the hinted centroid's score, so fewer centroids met
+ *                  early in the scan are inserted; results never depend on it.
+ *                  Entries outside [0, C) are ignored. Must not alias an output.
  * Errors: as ivf_route; N > 2^32 - 1 is IVF_EUNSUPPORTED. */
 ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
                            const float *centroids, int64_t C, int32_t D, uint64_t seed,
                            int32_t iter, int32_t *out_labels, float *out_centroids,
-                           int64_t *out_counts, double *out_objective);
+                           int64_t *out_counts, double *out_objective, const int32_t *hint_labels);
 
 /* Full assignment and inverted-list build (Sec. "System Architecture", index
  * layout: cluster-major lists with offset, length and vector ids).

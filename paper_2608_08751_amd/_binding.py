@@ -35,7 +35,7 @@ SIGNATURES = [
     ("ivf_sync", _INT, [_P]),
     ("ivf_route", _INT, [_P, _P, _I64, _P, _I64, _I32, _I32, _P, _P]),
     ("ivf_route_noalloc", _INT, [_P, _P, _I64, _P, _I64, _I32, _I32, _P, _P]),
-    ("ivf_kmeans_step", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _U64, _I32, _P, _P, _P, _P]),
+    ("ivf_kmeans_step", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _U64, _I32, _P, _P, _P, _P, _P]),
     ("ivf_assign_build", _INT, [_P, _P, _INT, _I64, _P, _I64, _I32, _P, _P, _P, _P]),
     ("ivf_build_lists", _INT, [_P, _P, _I64, _I64, _P, _P, _P]),
     ("ivf_last_stats", _INT, [_P, ctypes.POINTER(_I64)]),
@@ -233,9 +233,11 @@ def ivf_route_noalloc(ctx: Context, queries, centroids, nprobe: int, out_ids, ou
 
 
 def ivf_kmeans_step(ctx: Context, train, centroids, seed: int = 0, it: int = 0, out_labels=None,
-                    out_centroids=None, out_counts=None, out_objective=None):
+                    out_centroids=None, out_counts=None, out_objective=None, hint_labels=None):
     """One Lloyd iteration: labels [N] int32, new centroids [C, D] fp32,
-    counts [C] int64 (before reseeding), objective (device fp64 scalar)."""
+    counts [C] int64 (before reseeding), objective (device fp64 scalar).
+    `hint_labels` (int32 [N], e.g. the previous iteration's labels) only
+    changes the speed."""
     import torch
 
     _device_tensor(train, "train")
@@ -251,11 +253,14 @@ def ivf_kmeans_step(ctx: Context, train, centroids, seed: int = 0, it: int = 0, 
         out_counts = torch.empty(C, dtype=torch.int64, device=dev)
     if out_objective is None:
         out_objective = torch.empty(2, dtype=torch.float64, device=dev)
+    if hint_labels is not None:
+        _device_tensor(hint_labels, "hint_labels")
     ctx.ensure_workspace(ctx.lib.ivf_workspace_bytes(IVF_OP_KMEANS_STEP, N, C, D, 0))
     ctx.bind_stream()
     ctx.check(ctx.lib.ivf_kmeans_step(ctx.handle, _ptr(train), _dtype_code(train), N, _ptr(centroids),
                                       C, D, seed & (2**64 - 1), it, _ptr(out_labels),
-                                      _ptr(out_centroids), _ptr(out_counts), _ptr(out_objective)),
+                                      _ptr(out_centroids), _ptr(out_counts), _ptr(out_objective),
+                                      _ptr(hint_labels) if hint_labels is not None else None),
               "ivf_kmeans_step")
     return out_labels, out_centroids, out_counts, out_objective
 

@@ -455,7 +455,7 @@ ivf_status check_common(ivf_ctx *ctx, int64_t C, int32_t D)
 // (int32, relative to the slice) stay below 2^31 for any N <= 2^32 - 1.
 ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N,
                           const float *cent, int64_t C, int D, int32_t *labels,
-                          const AssignLayout &l)
+                          const AssignLayout &l, const int32_t *hint = nullptr)
 {
     hipStream_t s = ctx->stream;
     const int DP = padded_dim(D);
@@ -530,6 +530,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
                 q.list_cap = ctx->rescreen_cap > 0 ? std::min<int64_t>(ctx->rescreen_cap, l.list_cap) : l.list_cap;
                 // a forced fallback passes every row on to the two planes, which send it on
                 q.force_rescreen = ctx->force_rescreen || ctx->force_fallback;
+                q.hint = hint ? hint + r0 : nullptr;
                 TIMED("screen_top1_i8s", launch_screen_i8_single(DP, q, ctx->num_cus, s));
             }
             TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
@@ -1011,7 +1012,7 @@ static ivf_status check_rows(ivf_ctx *ctx, const void *rows, int dt, int64_t N, 
 ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
                            const float *centroids, int64_t C, int32_t D, uint64_t seed,
                            int32_t iter, int32_t *out_labels, float *out_centroids,
-                           int64_t *out_counts, double *out_objective)
+                           int64_t *out_counts, double *out_objective, const int32_t *hint_labels)
 {
     if (!ctx) return IVF_EINVAL;
     ctx->err.clear();
@@ -1023,13 +1024,15 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
     if (N == 0) return IVF_OK;
     if (!centroids || !out_labels || !out_centroids) return fail(ctx, IVF_EINVAL, "null pointer argument");
     if (!aligned16(centroids) || !aligned16(out_labels) || !aligned16(out_centroids) ||
-        (out_counts && !aligned16(out_counts)) || (out_objective && !aligned16(out_objective)))
+        (out_counts && !aligned16(out_counts)) || (out_objective && !aligned16(out_objective)) ||
+        (hint_labels && !aligned16(hint_labels)))
         return fail(ctx, IVF_EINVAL, "arrays must be 16-byte aligned");
     const size_t xb = (size_t)N * rb, cb = (size_t)C * D * 4, lb = (size_t)N * 4, nb = (size_t)C * 8;
     const void *outs[4] = {out_labels, out_centroids, out_counts, out_objective};
     const size_t osz[4] = {lb, cb, nb, 8};
     for (int i = 0; i < 4; ++i) {
-        if (overlap(outs[i], osz[i], train, xb) || overlap(outs[i], osz[i], centroids, cb))
+        if (overlap(outs[i], osz[i], train, xb) || overlap(outs[i], osz[i], centroids, cb) ||
+            overlap(outs[i], osz[i], hint_labels, hint_labels ? lb : 0))
             return fail(ctx, IVF_EINVAL, "outputs overlap inputs");
         for (int j = i + 1; j < 4; ++j)
             if (overlap(outs[i], osz[i], outs[j], osz[j])) return fail(ctx, IVF_EINVAL, "outputs overlap");
@@ -1041,7 +1044,8 @@ ivf_status ivf_kmeans_step(ivf_ctx *ctx, const void *train, int dt, int64_t N,
 
     const AssignLayout l = layout_assign(ctx->ws, N, C, quant_dim(D), true, true, ctx->num_cus);
     const int rowtype = dt == IVF_U8 ? kRowU8 : kRowF32;
-    if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l)) != IVF_OK) return st;
+    if ((st = enqueue_assign(ctx, train, rowtype, N, centroids, C, D, out_labels, l, hint_labels)) != IVF_OK)
+        return st;
     int64_t *counts = out_counts ? out_counts : l.counts;
     if ((st = enqueue_build(ctx, N, C, out_labels, l.cntmat, counts, l.offsets, l.perm)) != IVF_OK) return st;
     TIMED("kmeans_update", launch_kmeans_update(train, rowtype, N, D, D, centroids, C, counts, l.offsets, l.perm, seed,

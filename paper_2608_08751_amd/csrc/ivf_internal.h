@@ -97,6 +97,9 @@ struct ScreenI8Args {
     const uint32_t *e_bits;
     int64_t ncent;
     int force_rescreen;
+    // single plane: a label per row from an earlier step, or null; the row's
+    // keep threshold starts from that centroid's score (speed only)
+    const int32_t *hint;
 };
 int64_t quantized_pad(int64_t C);
 // the single plane (qc1, negb1) is padded to whole staged chunks of 256

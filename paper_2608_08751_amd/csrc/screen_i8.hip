@@ -250,6 +250,7 @@ struct Top3i {
     int k1, k2, k3;
     int i1, i2;
     int t3, twoR;
+    int ks;  // single plane: score of the row's hinted centroid (kNoScore: none)
 };
 
 __device__ __forceinline__ int keep_threshold(const Top3i &st)
@@ -605,7 +606,7 @@ __device__ void screen_i8_tile(const ScreenI8Args &a, int64_t tile, char *__rest
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         l1[rb] += __shfl_xor(l1[rb], 32);
-        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, (int)(262 + l1[rb])};
+        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, (int)(262 + l1[rb]), kNoScore};
     }
 
     const char *A0 = lds + jl * St::kPitch + 16 * h;  // block 0 of buffer 0
@@ -1102,7 +1103,7 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
         // the group's best (the lowest position among equal scores) first
         const int e1 = v0 == m ? 0 : v1 == m ? 1 : v2 == m ? 2 : 3;
         top3i_push(st, m, idp + 8 * g + e1);
-        int kb = max(st.k1, __shfl_xor(st.k1, 32));
+        int kb = max(max(st.k1, __shfl_xor(st.k1, 32)), st.ks);
         st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
         // the other three only when some lane still needs one of them
         const int r0 = e1 == 0 ? kNoScore : v0, r1 = e1 == 1 ? kNoScore : v1;
@@ -1112,7 +1113,7 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
             top3i_push(st, r1, idp + 8 * g + 1);
             top3i_push(st, r2, idp + 8 * g + 2);
             top3i_push(st, r3, idp + 8 * g + 3);
-            kb = max(st.k1, __shfl_xor(st.k1, 32));
+            kb = max(max(st.k1, __shfl_xor(st.k1, 32)), st.ks);
             st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
         }
     }
@@ -1276,7 +1277,36 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
     for (int rb = 0; rb < RB; ++rb) {
         l1[rb] += __shfl_xor(l1[rb], 32);
         const int T = (int)ceil(2.0 * E * (double)l1[rb]) + 2;
-        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, T};
+        st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, T, kNoScore};
+    }
+    // A hinted label (an earlier step's) starts the keep threshold from that
+    // centroid's exact score s_h <= the row's best: every score the
+    // certificate needs (at or above best - T) still lies above s_h - T - 1,
+    // and the scan meets far fewer new bests. The score is the plane row's
+    // dot with x' (the two half-lanes' halves added) plus its bias, the same
+    // integer the MFMA chain produces.
+    if (a.hint) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int64_t row = row0 + (wave * RB + rb) * 32 + jl;
+            const int hl = row < a.nrows ? a.hint[row] : -1;
+            const bool ok = hl >= 0 && hl < a.ncent;
+            int dot = 0;
+            if (ok) {
+                const int8_t *qr = a.qc1 + (int64_t)hl * DP + 16 * h;
+#pragma unroll
+                for (int k = 0; k < DP / 32; ++k) {
+                    const i32x4 v = *reinterpret_cast<const i32x4 *>(qr + 32 * k);
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) dot = __builtin_amdgcn_sdot4(v[w], xf[rb][k][w], dot, false);
+                }
+            }
+            dot += __shfl_xor(dot, 32);
+            if (ok) {
+                st[rb].ks = dot + a.negb1[hl];
+                st[rb].t3 = st[rb].ks - st[rb].twoR - 1;
+            }
+        }
     }
 
     const char *A0 = lds + jl * St::kPitch + 16 * h;

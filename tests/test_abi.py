@@ -100,8 +100,8 @@ def test_route_workspace_too_small(vctx):
 
 
 def kstep(ctx, x=P(0), dt=B.IVF_U8, N=10**6, c=P(GB), C=4096, D=128, lab=P(2 * GB), cout=P(3 * GB),
-          cnt=P(4 * GB), obj=P(5 * GB)):
-    return ctx.lib.ivf_kmeans_step(ctx.handle, x, dt, N, c, C, D, 7, 0, lab, cout, cnt, obj)
+          cnt=P(4 * GB), obj=P(5 * GB), hint=None):
+    return ctx.lib.ivf_kmeans_step(ctx.handle, x, dt, N, c, C, D, 7, 0, lab, cout, cnt, obj, hint)
 
 
 def test_kmeans_validation(vctx):
@@ -117,6 +117,9 @@ def test_kmeans_validation(vctx):
     assert kstep(vctx, cnt=None, obj=None) == B.IVF_EDEVICE  # optional outputs
     assert kstep(vctx, cout=None) == B.IVF_EINVAL
     assert kstep(vctx, D=8, C=0) == B.IVF_EINVAL
+    assert kstep(vctx, hint=P(6 * GB)) == B.IVF_EDEVICE  # hint labels (speed only)
+    assert kstep(vctx, hint=P(6 * GB + 4)) == B.IVF_EINVAL  # misaligned
+    assert kstep(vctx, hint=P(2 * GB + 64)) == B.IVF_EINVAL  # overlaps the labels
     with_ws(vctx, 1024)
     assert kstep(vctx) == B.IVF_ENOMEM
 

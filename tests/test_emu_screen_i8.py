@@ -74,16 +74,21 @@ def emu_bin(tmp_path_factory):
 
 
 def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen=0, rescreen_cap=0,
-        run_fallback=0, wl_cap=0):
+        run_fallback=0, wl_cap=0, hints=None):
     N, D = x.shape
     src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
     with open(src, "wb") as f:
         np.array([N, c.shape[0], D], np.int64).tofile(f)
         np.ascontiguousarray(x, np.uint8).tofile(f)
         np.ascontiguousarray(c, np.float32).tofile(f)
+    extra = []
+    if hints is not None:
+        hp = tmp_path / "hints.bin"
+        np.ascontiguousarray(hints, np.int32).tofile(hp)
+        extra = [str(hp)]
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
     r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback), str(mode),
-                        str(force_rescreen), str(rescreen_cap), str(run_fallback), str(wl_cap)],
+                        str(force_rescreen), str(rescreen_cap), str(run_fallback), str(wl_cap)] + extra,
                        capture_output=True, text=True, timeout=900, env=env)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-6000:]
     raw = np.fromfile(dst, np.uint8)
@@ -230,3 +235,23 @@ def test_emulated_pipeline_with_fallback(emu_bin, tmp_path, oracle_mod, mode, fo
     olab = oracle_mod.assign(x, c)
     bad = np.nonzero(lab != olab)[0]
     assert bad.size == 0, "labels differ at rows %s" % bad[:10]
+
+
+def test_emulated_single_plane_with_hints(emu_bin, tmp_path, oracle_mod):
+    """Hinted labels (speed only) start each row's keep threshold from the
+    hinted centroid's score: the exact labels, garbage hints (out of range,
+    negative, random) and a mix give the same settled labels, worklist and
+    rescreen list as no hints."""
+    x, c = rows_and_centroids(900, 140, 128, seed=12)
+    lab0, wl0, st0, _ = run(emu_bin, tmp_path, x, c, mode=1)
+    listed0 = run.listed
+    check(oracle_mod, lab0, wl0, st0, x, c)
+    olab = oracle_mod.assign(x, c).astype(np.int32)
+    rng = np.random.default_rng(13)
+    garbage = rng.integers(-5, 200, size=900).astype(np.int32)
+    garbage[:10] = np.iinfo(np.int32).min
+    for hints in (olab, garbage, np.where(rng.random(900) < 0.5, olab, garbage).astype(np.int32)):
+        lab, wl, st, _ = run(emu_bin, tmp_path, x, c, mode=1, hints=hints)
+        check(oracle_mod, lab, wl, st, x, c)
+        assert np.array_equal(lab, lab0) and np.array_equal(np.sort(wl), np.sort(wl0))
+        assert run.listed == listed0 and int(st[1]) == int(st0[1])

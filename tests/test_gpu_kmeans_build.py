@@ -167,3 +167,34 @@ def test_assign_build_small(ivf_ctx, oracle_mod, dt):
     assert (lab.cpu().numpy() == olab).all()
     assert (cnt.cpu().numpy() == ocnt).all() and (off.cpu().numpy() == ooff).all()
     assert (perm.cpu().numpy().view(np.uint32) == operm).all()
+
+
+@pytest.mark.parametrize("N,C,D", [(30000, 700, 128), (9000, 300, 64), (12000, 520, 96)])
+def test_kmeans_label_hints_change_nothing(ivf_ctx, oracle_mod, N, C, D):
+    """Hint labels only seed the single plane's keep threshold: the previous
+    iteration's labels, garbage (negative, >= C, random) and a mix give the
+    same labels, centroids, counts and objective as no hints, and the oracle's
+    step."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(max(C // 2, 1), D, seed=N)
+    x, _ = synth.mixture_rows_u8(means, 0, N, seed=N)
+    c0 = x[synth.kmeans_init(N, C, seed=1)].astype(np.float32)
+    xd = to_dev(x)
+    lab0, c1, _, _ = ivf.ivf_kmeans_step(ivf_ctx, xd, to_dev(c0), seed=0, it=0)
+    ref = ivf.ivf_kmeans_step(ivf_ctx, xd, c1, seed=0, it=1)
+    torch.cuda.synchronize()
+    ref = [t.cpu().numpy() for t in ref]
+    olab, ocen, ocnt, _ = oracle_mod.kmeans_step(x, c1.cpu().numpy(), seed=0, it=1)
+    assert (ref[0] == olab).all() and (ref[1] == ocen).all() and (ref[2] == ocnt).all()
+    rng = np.random.default_rng(N + C)
+    garbage = rng.integers(-3, C + 50, size=N).astype(np.int32)
+    mix = np.where(rng.random(N) < 0.5, lab0.cpu().numpy(), garbage).astype(np.int32)
+    for hint in (lab0, to_dev(garbage), to_dev(mix)):
+        out = ivf.ivf_kmeans_step(ivf_ctx, xd, c1, seed=0, it=1, hint_labels=hint)
+        torch.cuda.synchronize()
+        out = [t.cpu().numpy() for t in out]
+        assert (out[0] == ref[0]).all() and (out[1] == ref[1]).all() and (out[2] == ref[2]).all()
+        assert out[3][0] == ref[3][0]

@@ -203,6 +203,13 @@ inline emu_i32x16 __builtin_amdgcn_mfma_i32_32x32x32_i8(emu_i32x4 a, emu_i32x4 b
     return d;
 }
 
+// v_dot4_i32_i8 without clamping: c + the dot of the four signed bytes
+inline int __builtin_amdgcn_sdot4(int a, int b, int c, bool)
+{
+    for (int i = 0; i < 4; ++i) c += (int)(int8_t)(a >> (8 * i)) * (int)(int8_t)(b >> (8 * i));
+    return c;
+}
+
 inline uint32_t __builtin_amdgcn_sad_u8(uint32_t a, uint32_t b, uint32_t c)
 {
     for (int i = 0; i < 4; ++i) {

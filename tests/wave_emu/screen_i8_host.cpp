@@ -7,7 +7,8 @@
 // settles the rows the screens hand on. Writes the labels, the worklist and
 // the statistics for the test to check against the oracle.
 //   usage: screen_i8_host in.bin out.bin num_cus force_fallback
-//                         [mode force_rescreen rescreen_cap run_fallback wl_cap]
+//                         [mode force_rescreen rescreen_cap run_fallback wl_cap hints.bin]
+//   hints.bin (optional): int32 hint labels [N] for the single plane
 //   in:  int64 N, C, D; uint8 rows [N][D]; float centroids [C][D]
 //   out: int32 labels [N]; uint32 worklist count; int32 worklist [count];
 //        uint64 stats [8]; uint32 quantisation flag; uint32 single-plane
@@ -100,6 +101,14 @@ int main(int argc, char **argv)
         a.list_cap = cap > 0 ? std::min<int64_t>(cap, list_cap) : list_cap;
         // as the library: a forced fallback passes every row on to the two planes
         a.force_rescreen = (argc > 6 ? atoi(argv[6]) : 0) || a.force_fallback;
+        int32_t *hint = nullptr;
+        if (argc > 10) {
+            hint = alloc<int32_t>(N, 0);
+            FILE *hf = fopen(argv[10], "rb");
+            if (!hf || fread(hint, 4, N, hf) != (size_t)N) return 2;
+            fclose(hf);
+        }
+        a.hint = hint;
         launch_screen_i8_single(DP, a, num_cus, nullptr);
     }
     launch_screen_i8(DP, a, num_cus, nullptr);
