@@ -246,6 +246,17 @@ __device__ __forceinline__ void load_rows_ids(const uint8_t *__restrict__ X, int
 // t3 = (thr - lmax) >> 8 is the prefilter threshold on the H accumulators
 // (lmax = 128 ||x'||_1 >= x'.Ls, so an H value h <= t3 has s <= thr);
 // twoR = 262 + ||x'||_1, so lmax = 128 (twoR - 262).
+// Largest value over the two half-lanes of a row (lanes l and l ^ 32).
+// v_permlane32_swap exchanges the upper 32 lanes of its first operand with
+// the lower 32 lanes of its second; with v in both, each lane finds v of
+// lanes l and l ^ 32 in its two results. A VALU exchange, where a shuffle
+// would take a round trip through the LDS crossbar.
+__device__ __forceinline__ int halves_max(int v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    return max((int)r[0], (int)r[1]);
+}
+
 struct Top3i {
     int k1, k2, k3;
     int i1, i2;
@@ -409,7 +420,7 @@ __device__ __forceinline__ void i8_group(const i32x16 &pH, const i32x16 &pL, int
         st.acc = m;
     } else {
         m = max(m, st.acc);
-        m = max(m, __shfl_xor(m, 32));
+        m = halves_max(m);
         const int64_t id0 = (int64_t)(idp & ~31) + 16 * (g / 2);
         if (st.krow && (threadIdx.x & 32) == 0 && id0 >= st.c_begin && id0 + 15 < st.c_end)
             st.krow[(id0 - st.c_begin) >> 4] = -(float)m;
@@ -1103,7 +1114,7 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
         // the group's best (the lowest position among equal scores) first
         const int e1 = v0 == m ? 0 : v1 == m ? 1 : v2 == m ? 2 : 3;
         top3i_push(st, m, idp + 8 * g + e1);
-        int kb = max(max(st.k1, __shfl_xor(st.k1, 32)), st.ks);
+        int kb = max(halves_max(st.k1), st.ks);
         st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
         // the other three only when some lane still needs one of them
         const int r0 = e1 == 0 ? kNoScore : v0, r1 = e1 == 1 ? kNoScore : v1;
@@ -1113,7 +1124,7 @@ __device__ __forceinline__ void s1_group(const i32x16 &p, int idp, Top3i &st)
             top3i_push(st, r1, idp + 8 * g + 1);
             top3i_push(st, r2, idp + 8 * g + 2);
             top3i_push(st, r3, idp + 8 * g + 3);
-            kb = max(max(st.k1, __shfl_xor(st.k1, 32)), st.ks);
+            kb = max(halves_max(st.k1), st.ks);
             st.t3 = kb > kNoScore ? max(st.k3, kb - st.twoR - 1) : kNoScore;
         }
     }

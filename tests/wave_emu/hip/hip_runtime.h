@@ -123,6 +123,27 @@ inline T __shfl_xor(T v, int m)
     return r;
 }
 
+// v_permlane32_swap_b32 (the two results of the builtin): the upper 32
+// lanes of the first operand trade places with the lower 32 lanes of the
+// second (lane layout checked on the device).
+struct PermlanePair {
+    uint32_t v[2];
+    uint32_t operator[](int i) const { return v[i]; }
+};
+inline PermlanePair __builtin_amdgcn_permlane32_swap(uint32_t old, uint32_t src, bool, bool)
+{
+    emu::Wave &w = emu::wave();
+    const int l = emu::lane();
+    const uint32_t in[2] = {old, src};
+    memcpy(w.buf[l], in, sizeof in);
+    w.bar->arrive_and_wait();
+    PermlanePair r;
+    memcpy(&r.v[0], w.buf[l < 32 ? l : l - 32] + (l < 32 ? 0 : 4), 4);
+    memcpy(&r.v[1], w.buf[l < 32 ? l + 32 : l] + (l < 32 ? 0 : 4), 4);
+    w.bar->arrive_and_wait();
+    return r;
+}
+
 inline int __any(int p)
 {
     emu::Wave &w = emu::wave();
