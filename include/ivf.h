@@ -252,7 +252,13 @@ ivf_status ivf_last_stats(ivf_ctx *ctx, int64_t out[8]);
  *                           speed only, never results
  *   IVF_OPT_ASSIGN_SLICE    > 0: rows per assignment slice, below the
  *                           default 2^28 (each slice is screened with its own
- *                           worklists); speed only, never results */
+ *                           worklists); speed only, never results
+ *   IVF_OPT_S1_ID_ORDER     1 = the single-plane screen visits centroids in id
+ *                           order (default 0: in ascending distance to the
+ *                           mean of the centroids, a stable counting sort per
+ *                           call, so that rows meet good centroids early and
+ *                           the scan inserts fewer scores); speed only, never
+ *                           results */
 typedef enum {
     IVF_OPT_FORCE_FALLBACK = 0,
     IVF_OPT_SAMPLE_RANK = 1,
@@ -263,7 +269,8 @@ typedef enum {
     IVF_OPT_I8_TWO_PLANE_ONLY = 6,
     IVF_OPT_FORCE_RESCREEN = 7,
     IVF_OPT_RESCREEN_CAP = 8,
-    IVF_OPT_ASSIGN_SLICE = 9
+    IVF_OPT_ASSIGN_SLICE = 9,
+    IVF_OPT_S1_ID_ORDER = 10
 } ivf_option;
 ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
 

@@ -31,6 +31,7 @@ from ._binding import (  # noqa: F401
     IVF_OPT_I8_TWO_PLANE_ONLY,
     IVF_OPT_PROFILE,
     IVF_OPT_RESCREEN_CAP,
+    IVF_OPT_S1_ID_ORDER,
     IVF_OPT_SAMPLE_RANK,
     IVF_OPT_SCREEN_WAVES,
     IVF_U8,

@@ -18,7 +18,7 @@ IVF_F32, IVF_U8 = 0, 1
 IVF_OP_ROUTE, IVF_OP_KMEANS_STEP, IVF_OP_ASSIGN_BUILD, IVF_OP_BUILD_LISTS, IVF_OP_PQ_TRAIN_STEP, IVF_OP_ADC_SCAN = range(6)
 (IVF_OPT_FORCE_FALLBACK, IVF_OPT_SAMPLE_RANK, IVF_OPT_PROFILE, IVF_OPT_BUILD_BLOCKS, IVF_OPT_SCREEN_WAVES,
  IVF_OPT_FP32_SCREEN, IVF_OPT_I8_TWO_PLANE_ONLY, IVF_OPT_FORCE_RESCREEN, IVF_OPT_RESCREEN_CAP,
- IVF_OPT_ASSIGN_SLICE) = range(10)
+ IVF_OPT_ASSIGN_SLICE, IVF_OPT_S1_ID_ORDER) = range(11)
 
 STATUS_NAMES = {0: "IVF_OK", 1: "IVF_EINVAL", 2: "IVF_EUNSUPPORTED", 3: "IVF_ENOMEM", 4: "IVF_EDEVICE"}
 

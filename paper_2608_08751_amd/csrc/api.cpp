@@ -32,6 +32,7 @@ struct ivf_ctx {
     int screen_waves = 8;
     int fp32_screen = 0;  // 1: uint8 rows also take the fp32 MFMA screen
     int two_plane_only = 0;  // 1: no single-plane int8 pre-screen
+    int s1_id_order = 0;     // 1: the single plane visits centroids in id order
     int force_rescreen = 0;  // 1: the single-plane screen lists every row
     int64_t rescreen_cap = 0;  // > 0: smaller capacity of that list (tests)
     int64_t assign_slice = 0;  // > 0: shorter assignment slices (tests)
@@ -276,6 +277,16 @@ struct AssignLayout {
     // single plane (padded dimension <= 128) and the rows it leaves
     int8_t *qc1;
     int32_t *negb1;
+    // its visiting order: keys, column sums and mean, counting-sort scratch,
+    // bucket counts and offsets, order (plane row -> id) and positions
+    int32_t *okeys;
+    double *opart;
+    float *omean;
+    void *oradix;
+    int64_t *ocounts;
+    int64_t *ooffsets;
+    uint32_t *ord1;
+    int32_t *pos1;
     int32_t *list;
     int64_t list_cap;
     int32_t *wl;
@@ -335,6 +346,14 @@ AssignLayout layout_assign(void *base, int64_t N, int64_t C, int qdp, bool need_
         if (qdp <= 128) {
             l.qc1 = c.take<int8_t>((size_t)quantized_pad1(C) * qdp);
             l.negb1 = c.take<int32_t>(quantized_pad1(C));
+            l.okeys = c.take<int32_t>(C);
+            l.opart = c.take<double>((size_t)order1_parts(C) * qdp);
+            l.omean = c.take<float>(qdp);
+            l.oradix = c.take<unsigned char>(radix_scratch_bytes(plan_radix(C, kOrder1Keys, num_cus)));
+            l.ocounts = c.take<int64_t>(kOrder1Keys);
+            l.ooffsets = c.take<int64_t>(kOrder1Keys + 1);
+            l.ord1 = c.take<uint32_t>(C);
+            l.pos1 = c.take<int32_t>(C);
             l.list_cap = rescreen_cap(std::min(N, kAssignSlice));
             l.list = c.take<int32_t>(l.list_cap);
         }
@@ -469,11 +488,29 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     uint32_t *q_bad1 = l.sc.mc2_bits + 3;
     uint32_t *e_bits = l.sc.mc2_bits + 4;
     uint32_t *list_cnt = l.sc.mc2_bits + 5;
+    const uint32_t *ord1 = nullptr;
+    const int32_t *pos1 = nullptr;
     if (int8) {
         // int8 MFMA screens; the fp32 kernel runs only if some centroid does not quantise
         TIMED("quantize", launch_quantize_centroids(cent, C, D, DP, l.qc, l.negb, q_bad, s));
-        if (single)
-            TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, s));
+        if (single) {
+            const bool ordered = !ctx->s1_id_order;
+            if (ordered) {
+                // the plane's visiting order: a stable counting sort of the
+                // centroids by their distance bucket
+                TIMED("order1_keys", launch_order1_keys(cent, C, D, l.opart, l.omean, l.okeys, s));
+                const RadixPlan rp = plan_radix(C, kOrder1Keys, ctx->num_cus);
+                const RadixScratch rs = carve_radix(rp, l.oradix);
+                TIMED("order1_level0", launch_radix_level0(rp, l.okeys, rs, s));
+                TIMED("order1_counts", launch_radix_level1_counts(rp, rs, l.ocounts, s));
+                TIMED("order1_offsets", launch_offsets(l.ocounts, kOrder1Keys, l.ooffsets, s));
+                TIMED("order1_scatter", launch_radix_level1_scatter(rp, rs, l.ooffsets, l.ord1, s));
+            }
+            TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, s,
+                                                          ordered ? l.ord1 : nullptr, ordered ? l.pos1 : nullptr));
+            ord1 = ordered ? l.ord1 : nullptr;
+            pos1 = ordered ? l.pos1 : nullptr;
+        }
     }
     for (int64_t r0 = 0; r0 < N; r0 += slice) {
         const int64_t n = std::min(slice, N - r0);
@@ -531,6 +568,8 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
                 // a forced fallback passes every row on to the two planes, which send it on
                 q.force_rescreen = ctx->force_rescreen || ctx->force_fallback;
                 q.hint = hint ? hint + r0 : nullptr;
+                q.ord1 = ord1;
+                q.pos1 = pos1;
                 TIMED("screen_top1_i8s", launch_screen_i8_single(DP, q, ctx->num_cus, s));
             }
             TIMED("screen_top1_i8", launch_screen_i8(DP, q, ctx->num_cus, s));
@@ -685,6 +724,7 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value)
         if (value < 0) return fail(ctx, IVF_EINVAL, "rescreen capacity must be >= 0");
         ctx->rescreen_cap = value;
         return IVF_OK;
+    case IVF_OPT_S1_ID_ORDER: ctx->s1_id_order = value ? 1 : 0; return IVF_OK;
     case IVF_OPT_ASSIGN_SLICE:
         if (value < 0) return fail(ctx, IVF_EINVAL, "assignment slice must be >= 0");
         ctx->assign_slice = value;

@@ -100,6 +100,10 @@ struct ScreenI8Args {
     // single plane: a label per row from an earlier step, or null; the row's
     // keep threshold starts from that centroid's score (speed only)
     const int32_t *hint;
+    // single plane in visiting order (null: id order): plane row p holds
+    // centroid ord1[p], and centroid c sits at plane row pos1[c]
+    const uint32_t *ord1;
+    const int32_t *pos1;
 };
 int64_t quantized_pad(int64_t C);
 // the single plane (qc1, negb1) is padded to whole staged chunks of 256
@@ -112,8 +116,19 @@ hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStrea
 // Single-plane int8 screen (DP <= 128): plane rint(c - 128) [quantized_pad1(C)][DP],
 // biases, *q_bad1 when some centroid does not fit, *e_bits = the largest
 // coordinate residual as float bits (both zeroed by the caller).
+// ord (null: id order) puts centroid ord[p] at plane row p and records
+// pos[ord[p]] = p.
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
-                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s);
+                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s,
+                                      const uint32_t *ord = nullptr, int32_t *pos = nullptr);
+// Visiting order of the single plane: keys[c] = a 15-bit bucket of
+// ||c - mean||^2 (mean over the centroids; the float's exponent and top 7
+// mantissa bits, so buckets are 0.8 % wide at any scale). part holds
+// order1_parts(C) x D doubles, mean D floats.
+constexpr int kOrder1Keys = 32768;
+int64_t order1_parts(int64_t C);
+hipError_t launch_order1_keys(const float *cent, int64_t C, int D, double *part, float *mean, int32_t *keys,
+                              hipStream_t s);
 hipError_t launch_screen_i8_single(int DP, const ScreenI8Args &a, int num_cus, hipStream_t s);
 
 // ---- norms, selection, fallbacks (select.hip) -----------------------------

@@ -47,6 +47,7 @@ typedef int i32x16 __attribute__((ext_vector_type(16)));
 constexpr int kQChunk = kQuantChunk;  // centroids per staged chunk (sub-chunk of the single plane)
 constexpr int kS1Sub = 4;            // 64-centroid sub-chunks per staged chunk of the single plane
 constexpr int kS1Chunk = kS1Sub * kQChunk;
+constexpr int kOrder1PartRows = 32;  // centroids per column-sum block of the visiting order
 constexpr int kNoScore = INT32_MIN;  // score of a padded centroid (below any real score)
 constexpr int kNoBias = -(1 << 23);  // H accumulator start of a padded centroid: s = kNoScore
 
@@ -1046,19 +1047,23 @@ constexpr int kNoBias1 = -(1 << 26);  // bias of a padded centroid: below every 
 __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict__ cent, int64_t C, int D, int DP,
                                                         int64_t Cpad, int8_t *__restrict__ q1,
                                                         int32_t *__restrict__ negb1, uint32_t *__restrict__ q_bad1,
-                                                        uint32_t *__restrict__ e_bits)
+                                                        uint32_t *__restrict__ e_bits, const uint32_t *__restrict__ ord,
+                                                        int32_t *__restrict__ pos)
 {
     const int lane = threadIdx.x & 63;
     const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
     for (int64_t j = w0; j < Cpad; j += nw) {
+        // plane row j holds centroid c (rows past C are padding)
+        const int64_t c = ord && j < C ? (int64_t)ord[j] : j;
+        if (pos && j < C && lane == 0) pos[c] = (int32_t)j;
         double n2 = 0.0, e = 0.0;
         bool bad = false;
         int8_t *q = q1 + j * DP;
         for (int d = lane; d < DP; d += 64) {
             int hb = 0;
             if (j < C && d < D) {
-                const double cp = (double)cent[j * D + d] - 128.0;
+                const double cp = (double)cent[c * D + d] - 128.0;
                 const double p = rint(cp);
                 if (!(p >= -128.0 && p <= 127.0)) {  // also true for NaN
                     bad = true;
@@ -1082,6 +1087,74 @@ __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict_
             // skips the atomic once a larger residual is recorded
             const uint32_t eb = __float_as_uint(__double2float_ru(e));
             if (j < C && e > 0.0 && eb > __atomic_load_n(e_bits, __ATOMIC_RELAXED)) atomicMax(e_bits, eb);
+        }
+    }
+}
+
+// ------------------------------------------------------------ visiting order
+// The single plane's scan inserts a score only when it comes near the row's
+// best so far, so the cost of insertions follows how often that best rises.
+// Centroids near the middle of the data score well for most rows; visiting
+// them first raises every row's best early. The order is a heuristic (any
+// order gives the same certified results): ascending ||c - mean||^2 with the
+// mean taken over the centroids, in 15-bit buckets of the float's bits,
+// stable by id within a bucket (a counting sort, the list build's kernels).
+
+// Column sums of rows [b * R, (b + 1) * R): one thread per dimension, fp64,
+// a fixed order (the result is the same on every run).
+__global__ __launch_bounds__(128) void order1_part_kernel(const float *__restrict__ cent, int64_t C, int D,
+                                                          double *__restrict__ part)
+{
+    const int d = threadIdx.x;
+    if (d >= D) return;
+    const int64_t c0 = (int64_t)blockIdx.x * kOrder1PartRows;
+    const int64_t c1 = c0 + kOrder1PartRows < C ? c0 + kOrder1PartRows : C;
+    double sum = 0.0;
+#pragma unroll 8
+    for (int64_t c = c0; c < c1; ++c) sum += (double)cent[c * D + d];
+    part[(int64_t)blockIdx.x * D + d] = sum;
+}
+
+// One block per dimension: strided partial sums, then a tree in LDS (a fixed
+// order).
+__global__ __launch_bounds__(256) void order1_mean_kernel(const double *__restrict__ part, int64_t parts, int64_t C,
+                                                          int D, float *__restrict__ mean)
+{
+    __shared__ double red[256];
+    const int d = blockIdx.x;
+    const int t = threadIdx.x;
+    double sum = 0.0;
+#pragma unroll 4
+    for (int64_t b = t; b < parts; b += 256) sum += part[b * D + d];
+    red[t] = sum;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) red[t] += red[t + w];
+        __syncthreads();
+    }
+    if (t == 0) mean[d] = (float)(red[0] / (double)C);
+}
+
+// One wave per centroid: key = the top 15 bits of fl32(||c - mean||^2)
+// (non-negative floats order like their bit patterns; NaN takes the last
+// bucket).
+__global__ __launch_bounds__(256) void order1_keys_kernel(const float *__restrict__ cent, int64_t C, int D,
+                                                          const float *__restrict__ mean, int32_t *__restrict__ keys)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t c = w0; c < C; c += nw) {
+        float s2 = 0.0f;
+        for (int d = lane; d < D; d += 64) {
+            const float t = cent[c * D + d] - mean[d];
+            s2 += t * t;
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) s2 += __shfl_xor(s2, o);
+        if (lane == 0) {
+            const uint32_t b = __float_as_uint(s2) >> 16;
+            keys[c] = (int32_t)(b < (uint32_t)kOrder1Keys ? b : (uint32_t)kOrder1Keys - 1u);
         }
     }
 }
@@ -1197,8 +1270,11 @@ __device__ __forceinline__ void s1_block(Frags1<DP> &f, const i32x4 (&x)[RB][DP 
 
 // Merges the two half-lanes of a row and certifies with the window T:
 // settled rows get their label (two-way near-ties decided in fp64), the
-// others are listed for the two-plane screen. A centroid id is used only
-// when it names a real centroid.
+// others are listed for the two-plane screen. The scan's ids are plane rows;
+// one is used only when it names a real centroid, through the visiting
+// order. Equal scores may rank in plane-row order, which never decides a
+// label: a gap above T excludes ties, and the fp64 decision breaks them by
+// centroid id.
 __device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bool rvalid, int h, const Top3i &st)
 {
     Top3i o;
@@ -1215,13 +1291,15 @@ __device__ __forceinline__ void s1_finish(const ScreenI8Args &a, int64_t row, bo
         const bool ok1 = m.i1 >= 0 && m.i1 < a.ncent;
         const bool ok2 = m.i2 >= 0 && m.i2 < a.ncent;
         if (!a.force_rescreen && ok1) {
+            const int c1 = a.ord1 ? (int)a.ord1[m.i1] : m.i1;
             if ((int64_t)m.k1 - (int64_t)m.k2 > T) {
-                label = m.i1;
+                label = c1;
             } else if ((int64_t)m.k1 - (int64_t)m.k3 > T && ok2) {
+                const int c2 = a.ord1 ? (int)a.ord1[m.i2] : m.i2;
                 const uint8_t *x = a.rows + row * (int64_t)a.D;
-                const double d1 = exact_dist(x, a.cent + (int64_t)m.i1 * a.D, a.D);
-                const double d2 = exact_dist(x, a.cent + (int64_t)m.i2 * a.D, a.D);
-                label = dist_lt(d2, m.i2, d1, m.i1) ? m.i2 : m.i1;
+                const double d1 = exact_dist(x, a.cent + (int64_t)c1 * a.D, a.D);
+                const double d2 = exact_dist(x, a.cent + (int64_t)c2 * a.D, a.D);
+                label = dist_lt(d2, c2, d1, c1) ? c2 : c1;
                 refined = true;
             }
         }
@@ -1303,8 +1381,10 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
             const int hl = row < a.nrows ? a.hint[row] : -1;
             const bool ok = hl >= 0 && hl < a.ncent;
             int dot = 0;
+            int hp = 0;  // the hinted centroid's plane row
             if (ok) {
-                const int8_t *qr = a.qc1 + (int64_t)hl * DP + 16 * h;
+                hp = a.pos1 ? a.pos1[hl] : hl;
+                const int8_t *qr = a.qc1 + (int64_t)hp * DP + 16 * h;
 #pragma unroll
                 for (int k = 0; k < DP / 32; ++k) {
                     const i32x4 v = *reinterpret_cast<const i32x4 *>(qr + 32 * k);
@@ -1314,7 +1394,7 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
             }
             dot += __shfl_xor(dot, 32);
             if (ok) {
-                st[rb].ks = dot + a.negb1[hl];
+                st[rb].ks = dot + a.negb1[hp];
                 st[rb].t3 = st[rb].ks - st[rb].twoR - 1;
             }
         }
@@ -1424,12 +1504,28 @@ hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP
 }
 
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
-                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s)
+                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s, const uint32_t *ord,
+                                      int32_t *pos)
 {
     const int64_t cpad = quantized_pad1(C);
     const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
     hipLaunchKernelGGL(quantize1_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, q1, negb1,
-                       q_bad1, e_bits);
+                       q_bad1, e_bits, ord, pos);
+    return hipGetLastError();
+}
+
+int64_t order1_parts(int64_t C) { return (C + kOrder1PartRows - 1) / kOrder1PartRows; }
+
+hipError_t launch_order1_keys(const float *cent, int64_t C, int D, double *part, float *mean, int32_t *keys,
+                              hipStream_t s)
+{
+    if (C <= 0) return hipSuccess;
+    if (D > 128) return hipErrorInvalidValue;  // the single plane's dimensions
+    const int64_t parts = order1_parts(C);
+    hipLaunchKernelGGL(order1_part_kernel, dim3((unsigned)parts), dim3(128), 0, s, cent, C, D, part);
+    hipLaunchKernelGGL(order1_mean_kernel, dim3((unsigned)D), dim3(256), 0, s, part, parts, C, D, mean);
+    const int64_t blocks = std::min<int64_t>((C + 3) / 4, 65536);
+    hipLaunchKernelGGL(order1_keys_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, mean, keys);
     return hipGetLastError();
 }
 

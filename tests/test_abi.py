@@ -165,6 +165,8 @@ def test_row_counts_above_int32(vctx):
     assert lib.ivf_set_option(h, B.IVF_OPT_ASSIGN_SLICE, 1000) == B.IVF_OK
     assert lib.ivf_set_option(h, B.IVF_OPT_ASSIGN_SLICE, -1) == B.IVF_EINVAL
     assert lib.ivf_set_option(h, B.IVF_OPT_ASSIGN_SLICE, 0) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_S1_ID_ORDER, 1) == B.IVF_OK
+    assert lib.ivf_set_option(h, B.IVF_OPT_S1_ID_ORDER, 0) == B.IVF_OK
 
 
 def test_route_noalloc_validation(vctx):

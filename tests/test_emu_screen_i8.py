@@ -74,7 +74,7 @@ def emu_bin(tmp_path_factory):
 
 
 def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen=0, rescreen_cap=0,
-        run_fallback=0, wl_cap=0, hints=None):
+        run_fallback=0, wl_cap=0, hints=None, order=None):
     N, D = x.shape
     src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
     with open(src, "wb") as f:
@@ -86,6 +86,14 @@ def run(exe, tmp_path, x, c, num_cus=3, force_fallback=0, mode=0, force_rescreen
         hp = tmp_path / "hints.bin"
         np.ascontiguousarray(hints, np.int32).tofile(hp)
         extra = [str(hp)]
+    if order is not None:
+        extra = extra or ["-"]
+        if isinstance(order, str):
+            extra.append(order)
+        else:
+            op = tmp_path / "order.bin"
+            np.ascontiguousarray(order, np.uint32).tofile(op)
+            extra.append(str(op))
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
     r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(force_fallback), str(mode),
                         str(force_rescreen), str(rescreen_cap), str(run_fallback), str(wl_cap)] + extra,
@@ -255,3 +263,37 @@ def test_emulated_single_plane_with_hints(emu_bin, tmp_path, oracle_mod):
         check(oracle_mod, lab, wl, st, x, c)
         assert np.array_equal(lab, lab0) and np.array_equal(np.sort(wl), np.sort(wl0))
         assert run.listed == listed0 and int(st[1]) == int(st0[1])
+
+
+@pytest.mark.parametrize("case", ["mixture", "ties"])
+def test_emulated_single_plane_visiting_order(emu_bin, tmp_path, oracle_mod, case):
+    """The single plane in another visiting order (plane row p holds centroid
+    ord[p]): a random permutation and the library's own order (its keys
+    kernel, then a stable sort by key) settle the same rows with the same
+    labels, hand on the same rows and count the same refinements as id order,
+    also with hint labels, which then go through the positions. Pairs and
+    crowds of equal and nearly equal centroids put equal scores in different
+    plane-row order."""
+    if case == "mixture":
+        x, c = rows_and_centroids(900, 530, 64, seed=21)
+    else:
+        rng = np.random.default_rng(22)
+        D = 64
+        pa = rng.integers(20, 236, size=(15, D)).astype(np.float32)
+        cr = rng.integers(20, 236, size=(15, D)).astype(np.float32)
+        c = np.vstack([pa, pa + 1e-3, cr, cr.copy(), cr + 1e-3, cr - 1.0 / 512, cr + 0.5,
+                       rng.uniform(0, 255, size=(200, D))]).astype(np.float32)
+        x = np.vstack([np.rint(pa), np.rint(pa + 0.25), np.rint(cr), rng.integers(0, 256, size=(300, D))])
+        x = np.clip(x, 0, 255).astype(np.uint8)
+    C = c.shape[0]
+    lab0, wl0, st0, _ = run(emu_bin, tmp_path, x, c, mode=1)
+    listed0 = run.listed
+    check(oracle_mod, lab0, wl0, st0, x, c)
+    rng = np.random.default_rng(23)
+    olab = oracle_mod.assign(x, c).astype(np.int32)
+    for order in (rng.permutation(C).astype(np.uint32), "auto"):
+        for hints in (None, olab):
+            lab, wl, st, _ = run(emu_bin, tmp_path, x, c, mode=1, order=order, hints=hints)
+            check(oracle_mod, lab, wl, st, x, c)
+            assert np.array_equal(lab, lab0) and np.array_equal(np.sort(wl), np.sort(wl0))
+            assert run.listed == listed0 and int(st[1]) == int(st0[1]) and int(st[6]) == int(st0[6])

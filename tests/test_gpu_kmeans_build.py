@@ -198,3 +198,42 @@ def test_kmeans_label_hints_change_nothing(ivf_ctx, oracle_mod, N, C, D):
         out = [t.cpu().numpy() for t in out]
         assert (out[0] == ref[0]).all() and (out[1] == ref[1]).all() and (out[2] == ref[2]).all()
         assert out[3][0] == ref[3][0]
+
+
+@pytest.mark.parametrize("N,C,D", [(30000, 700, 128), (12000, 2600, 64)])
+def test_single_plane_visiting_order_changes_nothing(ivf_ctx, oracle_mod, N, C, D):
+    """The single plane's visiting order (ascending distance to the centroid
+    mean, the default) against id order: the same labels, centroids, counts,
+    objective and statistics on a k-means step from mean centroids (with and
+    without hint labels) and on an assign-build, and the oracle's labels."""
+    import torch
+
+    import paper_2608_08751_amd as ivf
+
+    means = synth.uniform_means(max(C // 2, 1), D, seed=N)
+    x, _ = synth.mixture_rows_u8(means, 0, N, seed=N)
+    c0 = x[synth.kmeans_init(N, C, seed=1)].astype(np.float32)
+    xd = to_dev(x)
+    lab0, c1, _, _ = ivf.ivf_kmeans_step(ivf_ctx, xd, to_dev(c0), seed=0, it=0)
+    outs = {}
+    for id_order in (1, 0):
+        ivf_ctx.set_option(ivf.IVF_OPT_S1_ID_ORDER, id_order)
+        try:
+            k = ivf.ivf_kmeans_step(ivf_ctx, xd, c1, seed=0, it=1)
+            torch.cuda.synchronize()
+            st = ivf_ctx.last_stats()
+            kh = ivf.ivf_kmeans_step(ivf_ctx, xd, c1, seed=0, it=1, hint_labels=lab0)
+            a = ivf.ivf_assign_build(ivf_ctx, xd, c1)
+            torch.cuda.synchronize()
+            # the objective is element 0 of its buffer
+            outs[id_order] = ([t.cpu().numpy() for t in k[:3]] + [k[3][:1].cpu().numpy()], st,
+                              [t.cpu().numpy() for t in kh[:3]] + [kh[3][:1].cpu().numpy()],
+                              [t.cpu().numpy() for t in a])
+        finally:
+            ivf_ctx.set_option(ivf.IVF_OPT_S1_ID_ORDER, 0)
+    (k1, s1, h1, a1), (k0, s0, h0, a0) = outs[1], outs[0]
+    olab = oracle_mod.assign(x, c1.cpu().numpy())
+    assert (k0[0] == olab).all() and (a0[0] == olab).all()
+    for u, v in ((k0, k1), (h0, h1), (h0, k1), (a0, a1)):
+        assert all((p == q).all() for p, q in zip(u, v))
+    assert s0 == s1 and s0["rescreen"] > 0 and s0["refine2"] > 0

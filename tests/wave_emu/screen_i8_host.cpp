@@ -7,13 +7,18 @@
 // settles the rows the screens hand on. Writes the labels, the worklist and
 // the statistics for the test to check against the oracle.
 //   usage: screen_i8_host in.bin out.bin num_cus force_fallback
-//                         [mode force_rescreen rescreen_cap run_fallback wl_cap hints.bin]
-//   hints.bin (optional): int32 hint labels [N] for the single plane
+//                         [mode force_rescreen rescreen_cap run_fallback wl_cap hints.bin order]
+//   hints.bin (optional, "-" for none): int32 hint labels [N] for the single plane
+//   order (optional): the single plane's visiting order, either a file of
+//        uint32 [C] (plane row -> centroid id) or "auto": the library's keys
+//        kernel, then a stable sort by key on the host (the counting sort
+//        the library runs with the list build's kernels)
 //   in:  int64 N, C, D; uint8 rows [N][D]; float centroids [C][D]
 //   out: int32 labels [N]; uint32 worklist count; int32 worklist [count];
 //        uint64 stats [8]; uint32 quantisation flag; uint32 single-plane
 //        quantisation flag; uint32 rescreen list count
 #include "hip/hip_runtime.h"
+#include <vector>
 namespace emu {
 thread_local dim3 tid, bid;
 dim3 bdim, gdim;
@@ -90,7 +95,35 @@ int main(int argc, char **argv)
     a.force_fallback = atoi(argv[4]);
     a.ncent = C;
     if (single) {
-        launch_quantize_centroids1(cent, C, D, DP, qc1, negb1, q_bad1, e_bits, nullptr);
+        uint32_t *ord = nullptr;
+        int32_t *pos = nullptr;
+        if (argc > 11) {
+            ord = alloc<uint32_t>(C, 0);
+            pos = alloc<int32_t>(C, 0xff);
+            if (strcmp(argv[11], "auto") == 0) {
+                int32_t *keys = alloc<int32_t>(C, 0xff);
+                double *part = alloc<double>(order1_parts(C) * D, 0);
+                float *mean = alloc<float>(D, 0);
+                if (launch_order1_keys(cent, C, D, part, mean, keys, nullptr) != hipSuccess) return 3;
+                std::vector<uint32_t> o(C);
+                for (int64_t c = 0; c < C; ++c) {
+                    if (keys[c] < 0 || keys[c] >= kOrder1Keys) return 4;
+                    o[c] = (uint32_t)c;
+                }
+                std::stable_sort(o.begin(), o.end(), [&](uint32_t u, uint32_t v) { return keys[u] < keys[v]; });
+                memcpy(ord, o.data(), 4 * C);
+                free(keys);
+                free(part);
+                free(mean);
+            } else {
+                FILE *of = fopen(argv[11], "rb");
+                if (!of || fread(ord, 4, C, of) != (size_t)C) return 2;
+                fclose(of);
+            }
+        }
+        launch_quantize_centroids1(cent, C, D, DP, qc1, negb1, q_bad1, e_bits, nullptr, ord, pos);
+        a.ord1 = ord;
+        a.pos1 = pos;
         a.qc1 = qc1;
         a.negb1 = negb1;
         a.e_bits = e_bits;
@@ -102,7 +135,7 @@ int main(int argc, char **argv)
         // as the library: a forced fallback passes every row on to the two planes
         a.force_rescreen = (argc > 6 ? atoi(argv[6]) : 0) || a.force_fallback;
         int32_t *hint = nullptr;
-        if (argc > 10) {
+        if (argc > 10 && strcmp(argv[10], "-") != 0) {
             hint = alloc<int32_t>(N, 0);
             FILE *hf = fopen(argv[10], "rb");
             if (!hf || fread(hint, 4, N, hf) != (size_t)N) return 2;
