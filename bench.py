@@ -380,6 +380,7 @@ def main():
         timeline = ctx.kernel_times()
         ctx.set_option(ivf.IVF_OPT_PROFILE, 0)
         ms_per_step = 1e3 * t_total / args.steps
+        stats = ctx.last_stats()  # of the last timed step
 
         agg = {}
         for name, ms in timeline:
