@@ -184,7 +184,8 @@ int pow2_ceil(int64_t v)
 
 struct RoutePlan {
     int64_t QB;   // queries per internal batch
-    int64_t Cs;   // threshold sample size (centroids [0, Cs)), 0 = none
+    int64_t Cs;   // threshold sample size, 0 = none
+    int64_t Ss;   // the sample: chunks j * Ss of kChunk centroids, j < Cs / kChunk
     int L;        // candidate capacity per query
     int rank_j;
     int qdp;      // padded dimension of the int8 route planes; 0 = fp32 kernels only
@@ -197,6 +198,7 @@ RoutePlan plan_route(int64_t Q, int64_t C, int k, int rank_override, int D)
     p.qdp = quant_dim(D);
     if (C <= 2048) {
         p.Cs = 0;
+        p.Ss = 1;
         p.L = pow2_ceil(std::max<int64_t>(C, k));
         p.rank_j = 0;
         return p;
@@ -213,6 +215,9 @@ RoutePlan plan_route(int64_t Q, int64_t C, int k, int rank_override, int D)
     Cs = std::min<int64_t>(Cs, 65536);
     Cs = std::max<int64_t>(Cs, kChunk);
     p.Cs = Cs;
+    // spread over the table (a table sorted by position or by list would
+    // bias a contiguous sample); Cs <= C / 2 gives a stride of at least 2
+    p.Ss = (C / kChunk) / (Cs / kChunk);
     p.rank_j = (int)std::min<int64_t>(r, Cs / 16);
     const double expected = (double)p.rank_j * (double)C / (double)Cs;
     if (rank_override > 0) p.rank_j = (int)std::min<int64_t>(rank_override, Cs / 16);
@@ -905,13 +910,15 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         if (i8) TIMED("route_i8_bound", launch_route_i8_bound(qrows, nb, D, q_bad, i8_off, l.qbound, s));
         if (p.Cs > 0) {
             a.c_begin = 0;
-            a.c_end = p.Cs;
+            a.c_end = C;
             a.nchunks = p.Cs / kChunk;
+            a.cstride = p.Ss;
             a.keys = l.keys;
             if (i8) {
                 ra.c_begin = 0;
                 ra.c_end = p.Cs;
                 ra.nchunks = p.Cs / kQuantChunk;
+                ra.cstride = p.Ss;
                 ra.keys = l.keys;
                 TIMED("route_i8_keys", launch_route_i8(kRouteKeys, p.qdp, ra, ctx->num_cus, s));
             }
@@ -926,6 +933,7 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         r.k = nprobe;
         r.L = p.L;
         r.Cs = p.Cs;
+        r.sstride = p.Ss;
         r.rank_j = p.rank_j;
         r.keys = l.keys;
         r.tau = l.tau;
@@ -944,9 +952,13 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         r.qbound = l.qbound;
         TIMED("route_threshold", launch_route_threshold(r, s));
         if (p.Cs < C) {
-            a.c_begin = p.Cs;
+            // every chunk the sample left
+            a.c_begin = 0;
             a.c_end = C;
-            a.nchunks = (C - p.Cs + kChunk - 1) / kChunk;
+            a.nchunks = (C + kChunk - 1) / kChunk - p.Cs / kChunk;
+            a.cstride = 1;
+            a.skip_n = p.Cs / kChunk;
+            a.skip_s = p.Ss;
             a.keys = nullptr;
             a.tau = l.tau;
             a.cand_cnt = l.cand_cnt;
@@ -957,6 +969,7 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
                 ra.c_begin = 0;
                 ra.c_end = C;
                 ra.nchunks = (C + kQuantChunk - 1) / kQuantChunk;
+                ra.cstride = 1;
                 ra.keys = nullptr;
                 ra.tau = l.tau;
                 ra.cand_cnt = l.cand_cnt;

@@ -37,9 +37,15 @@ struct ScreenArgs {
     const float *cnorm;     // [C] fl32(||c||^2)
     int64_t c_begin;        // first centroid of the range (multiple of kChunk)
     int64_t c_end;          // one past the last centroid of the range
-    int64_t nchunks;        // ceil((c_end - c_begin) / kChunk)
+    int64_t nchunks;        // chunks of kChunk centroids the kernel visits
+    // chunk k of the visit is physical chunk (c_begin / kChunk) + k, except:
+    // keys mode with cstride > 1: chunk k * cstride (a spread sample); filter
+    // mode with skip_n > 0: the k-th chunk that is not one of the skip_n
+    // sampled chunks j * skip_s
+    int64_t cstride;
+    int64_t skip_n, skip_s;
     // keys mode
-    float *keys;            // [nrows, c_end - c_begin]
+    float *keys;            // [nrows, nchunks * kChunk]
     // filter mode
     const float *tau;       // [nrows]
     uint32_t *cand_cnt;     // [nrows]
@@ -145,7 +151,8 @@ struct RouteArgs {
     int D;
     int k;
     int L;
-    int64_t Cs;             // centroids in the threshold sample [0, Cs)
+    int64_t Cs;             // centroids in the threshold sample
+    int64_t sstride;        // the sample is the chunks j * sstride of kChunk centroids (0: 1)
     int rank_j;
     const float *keys;      // [nq, Cs]
     float *tau;             // [nq]
@@ -184,6 +191,7 @@ struct RouteI8Args {
     int64_t cpad;
     int64_t c_begin, c_end; // centroid range; chunks of 64 from c_begin
     int64_t nchunks;
+    int64_t cstride;        // keys mode: chunk k of the range is physical chunk k * cstride (0: 1)
     const uint32_t *off;
     float *keys;            // keys mode: group minima [nq, (c_end - c_begin) / 16] (c_begin, c_end multiples of 16)
     const float *tau;       // filter mode: [nq], lists [nq, L]

@@ -580,6 +580,50 @@ __device__ __forceinline__ void filter_drain(const f32x16 &p0, const f32x16 &p1,
     }
 }
 
+// First centroid of visited chunk k (the maps of ScreenArgs).
+__device__ __forceinline__ int64_t keys_chunk_base(const ScreenArgs &a, int64_t k)
+{
+    return a.c_begin + k * (a.cstride > 1 ? a.cstride : 1) * kChunk;
+}
+
+// The filter's chunks in visiting order: every chunk but the sampled ones
+// j * skip_s (j < skip_n). One division to start, then steps; chunk indices
+// fit int32 (centroid ids do).
+struct ChunkWalk {
+    int phys;    // physical chunk of the current visit
+    int next_s;  // next sampled chunk after it (INT_MAX: none)
+    int left_s;  // sampled chunks from next_s on
+    int stride;
+
+    // every member assigned once, without early returns (the compiler keeps
+    // the walk in registers)
+    __device__ __forceinline__ void init(const ScreenArgs &a, int64_t k64)
+    {
+        const int k = (int)k64;
+        const int ns = (int)a.skip_n;
+        const bool on = ns > 0;
+        const int st = on ? (int)a.skip_s : 2;
+        const int run = st - 1;  // unsampled chunks after each sampled one
+        const int p = !on ? k : k < ns * run ? (k / run) * st + 1 + k % run : k + ns;
+        const int j = p / st + 1;  // the first sampled chunk after p (p is not sampled)
+        const int left = on ? ns - j : 0;
+        phys = p;
+        left_s = left;
+        next_s = left > 0 ? j * st : INT_MAX;
+        stride = st;
+    }
+
+    __device__ __forceinline__ void next()
+    {
+        ++phys;
+        if (phys == next_s) {
+            ++phys;  // skip_s >= 2: the chunk after a sampled one is not sampled
+            --left_s;
+            next_s = left_s > 0 ? next_s + stride : INT_MAX;
+        }
+    }
+};
+
 // Filter over the chunks [ch_lo, ch_hi) of one tile: chunk j's MFMAs carry
 // chunk j-1's epilogue; the last chunk's accumulators are drained after.
 template <int DP, int W>
@@ -615,28 +659,41 @@ __device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t
     const float *Nb = lds_n + 4 * h;
     // centroid ids fit int32; the id of register r of block rb of a chunk at
     // cbase is cbase + 4h + rb*32 + 8*(r/4) + r%4
-    const int idh = (int)a.c_begin + 4 * h;
     const int nch = (int)(ch_hi - ch_lo);
+    // first centroids of the last three fetched chunks: visits k - 1, k, k + 1
+    // once chunk k + 1 is fetched
+    ChunkWalk cw;
+    cw.init(a, ch_lo);
+    const int cb = (int)a.c_begin;
+    int b_prev2 = 0, b_prev1 = 0, b_cur = cb + cw.phys * kChunk;
+    auto advance = [&]() __attribute__((always_inline)) {
+        cw.next();
+        b_prev2 = b_prev1;
+        b_prev1 = b_cur;
+        b_cur = cb + cw.phys * kChunk;
+    };
+    auto idp_of = [&](int base) { return base + 4 * h; };
 
     Stager<DP, NT> cr;
     cr.init(a.D);
-    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
+    cr.fetch(a.cent, a.cnorm, b_cur, a.c_end, a.D);
     cr.template store<true>(lds_c, lds_n);
     __syncthreads();
 
     Top3 unused{};
     f32x16 x0, x1, y0, y1;
-    cr.fetch(a.cent, a.cnorm, a.c_begin + (ch_lo + 1) * kChunk, a.c_end, a.D);
+    advance();
+    cr.fetch(a.cent, a.cnorm, b_cur, a.c_end, a.D);
     mfma_chunk<DP, false>(Ab, Nb, b, x0, x1, x0, x1, 0, unused);
     cr.template store<true>(lds_c + CS, lds_n + kChunk);
     __syncthreads();
 
     // chunk j (relative to ch_lo) sits in buffer j & 1
-    auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) {
-        cr.fetch(a.cent, a.cnorm, a.c_begin + (ch_lo + j + 1) * kChunk, a.c_end, a.D);
+    auto step = [&](int j, f32x16 &c0, f32x16 &c1, const f32x16 &p0, const f32x16 &p1) __attribute__((always_inline)) {
+        advance();  // b_cur: visit j + 1, b_prev2: visit j - 1
+        cr.fetch(a.cent, a.cnorm, b_cur, a.c_end, a.D);
         const int bj = j & 1;
-        filter_chunk<DP, W>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1,
-                            idh + (int)(ch_lo + j - 1) * kChunk, fs);
+        filter_chunk<DP, W>(Ab + bj * CS, Nb + bj * kChunk, b, c0, c1, p0, p1, idp_of(b_prev2), fs);
         cr.template store<true>(lds_c + (bj ^ 1) * CS, lds_n + (bj ^ 1) * kChunk);
         __syncthreads();
     };
@@ -647,9 +704,9 @@ __device__ __forceinline__ void screen_filter_range(const ScreenArgs &a, int64_t
     }
     if (j < nch) {
         step(j, y0, y1, x0, x1);
-        filter_drain(y0, y1, idh + (int)(ch_lo + j) * kChunk, fs);
+        filter_drain(y0, y1, idp_of(b_prev1), fs);  // visit j
     } else {
-        filter_drain(x0, x1, idh + (int)(ch_lo + j - 1) * kChunk, fs);
+        filter_drain(x0, x1, idp_of(b_prev1), fs);  // visit j - 1
     }
     filter_flush(fs);
 }
@@ -678,7 +735,7 @@ __device__ void screen_keys_range(const ScreenArgs &a, int64_t tile, int64_t ch_
 
     Stager<DP, NT> cr;
     cr.init(a.D);
-    cr.fetch(a.cent, a.cnorm, a.c_begin + ch_lo * kChunk, a.c_end, a.D);
+    cr.fetch(a.cent, a.cnorm, keys_chunk_base(a, ch_lo), a.c_end, a.D);
     cr.template store<true>(lds_c, lds_n);
     __syncthreads();
 
@@ -686,16 +743,15 @@ __device__ void screen_keys_range(const ScreenArgs &a, int64_t tile, int64_t ch_
     const float *Nb = lds_n + 4 * h;
     for (int64_t ch = ch_lo; ch < ch_hi; ++ch) {
         const int buf = (int)((ch - ch_lo) & 1);
-        const int64_t cbase = a.c_begin + ch * kChunk;
-        cr.fetch(a.cent, a.cnorm, cbase + kChunk, a.c_end, a.D);  // unconditional; see screen_top1
+        cr.fetch(a.cent, a.cnorm, keys_chunk_base(a, ch + 1), a.c_end, a.D);  // unconditional; see screen_top1
 
         f32x16 acc0, acc1;
         mfma_chunk<DP, false>(Ab + buf * CS, Nb + buf * kChunk, b, acc0, acc1, acc0, acc1, 0, unused);
 
         // register r of block rb holds centroid rb*32 + 8*(r/4) + 4*h + r%4
         if (rvalid) {
-            const int64_t ld = a.c_end - a.c_begin;  // a multiple of kChunk
-            float *out = a.keys + row * ld + (cbase - a.c_begin) + 4 * h;
+            const int64_t ld = a.nchunks * kChunk;  // keys in visiting order
+            float *out = a.keys + row * ld + ch * kChunk + 4 * h;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 *reinterpret_cast<float4 *>(out + 8 * g) =

@@ -897,20 +897,25 @@ __device__ void route_i8_range(const RouteI8Args &a, int64_t tile, int64_t ch_lo
 
     const char *A0 = lds + jl * St::kPitch + 16 * h;
     const char *B0 = lds + St::kBias + 16 * h;
-    const int64_t cb0 = a.c_begin + ch_lo * kQChunk;  // first centroid of the range's chunk 0
+    // ids count chunks in visiting order (the keys' slots); chunk jj of the
+    // range is read from physical chunk (ch_lo + jj) * cstride (keys of a
+    // spread sample; 1 otherwise)
+    const int64_t cb0 = a.c_begin + ch_lo * kQChunk;
     const int idh = (int)cb0 + 4 * h;
     const int nch = (int)(ch_hi - ch_lo);
+    const int64_t cst = a.cstride > 1 ? a.cstride : 1;
+    auto pbase = [&](int64_t jj) { return a.c_begin + (ch_lo + jj) * cst * kQChunk; };
     auto abuf = [&](int jj) { return A0 + (jj & 1) * CS; };
     auto bbuf = [&](int jj) { return reinterpret_cast<const int *>(B0 + (jj & 1) * CS); };
 
     St q;
     q.init();
-    q.fetch(a.qc, a.negb, cb0, a.cpad, lds);
+    q.fetch(a.qc, a.negb, pbase(0), a.cpad, lds);
     __syncthreads();
-    q.fetch(a.qc, a.negb, cb0 + kQChunk, a.cpad, lds + CS);
+    q.fetch(a.qc, a.negb, pbase(1), a.cpad, lds + CS);
     auto stage = [&](int jj) {
         __syncthreads();
-        q.fetch(a.qc, a.negb, cb0 + (int64_t)(jj + 1) * kQChunk, a.cpad, lds + ((jj + 1) & 1) * CS);
+        q.fetch(a.qc, a.negb, pbase(jj + 1), a.cpad, lds + ((jj + 1) & 1) * CS);
     };
 
     // T1 starts as a tile of lowest scores: the first epilogue keeps nothing

@@ -187,8 +187,8 @@ __device__ uint32_t block_select(const uint32_t (&v)[V], int nv, int k, uint32_t
     return prefix;
 }
 
-// Routing threshold from the sample keys [0, Cs) of one query: the keys are cut
-// into groups of 16 consecutive centroids, tau = the rank_j-th smallest group
+// Routing threshold from the Cs sample keys of one query: the keys are cut
+// into groups of 16 consecutive sample centroids, tau = the rank_j-th smallest group
 // minimum (so about rank_j sample keys lie at or below tau), and every sample
 // key <= tau is emitted as a candidate. With Cs == 0, tau = +inf.
 constexpr int kMaxGroups = 4096;
@@ -196,6 +196,14 @@ constexpr int kGroupsPerThread = kMaxGroups / 256;
 
 // true when the int8 route kernels produce this call's keys (group minima)
 __device__ __forceinline__ bool int8_keys(const RouteArgs &a) { return a.i8_off && *a.i8_off == 0u; }
+
+// Centroid id of sample key s: the sample is the chunks j * sstride of kChunk
+// centroids, its keys in that order.
+__device__ __forceinline__ uint32_t sample_id(const RouteArgs &a, int64_t s)
+{
+    const int64_t st = a.sstride > 1 ? a.sstride : 1;
+    return (uint32_t)((s / kChunk) * st * kChunk + s % kChunk);
+}
 
 __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
 {
@@ -242,7 +250,7 @@ __global__ __launch_bounds__(256) void route_threshold_kernel(RouteArgs a)
             if (kk[e] <= th) {
                 const uint32_t slot = atomicAdd(&s_cnt, 1u);
                 if (slot < (uint32_t)a.L)
-                    a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[e]), (uint32_t)(4 * i + e));
+                    a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[e]), sample_id(a, 4 * i + e));
             }
         }
     }
@@ -301,7 +309,7 @@ __global__ __launch_bounds__(256) void route_threshold_reg_kernel(RouteArgs a)
                 if (g < G && kk[c] <= th) {
                     const uint32_t slot = atomicAdd(&s_cnt, 1u);
                     if (slot < (uint32_t)a.L)
-                        a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[c]), (uint32_t)(16 * g + 4 * i + c));
+                        a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[c]), sample_id(a, 16 * g + 4 * i + c));
                 }
             }
         }

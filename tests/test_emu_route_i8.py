@@ -39,7 +39,7 @@ def emu_route(tmp_path_factory):
     return exe
 
 
-def run(exe, tmp_path, q, c, Cs, L, tau, num_cus=2):
+def run(exe, tmp_path, q, c, Cs, L, tau, num_cus=2, stride=1):
     Q, D = q.shape
     C = c.shape[0]
     src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
@@ -49,8 +49,8 @@ def run(exe, tmp_path, q, c, Cs, L, tau, num_cus=2):
         np.ascontiguousarray(c, np.float32).tofile(f)
         np.ascontiguousarray(tau, np.float32).tofile(f)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1")
-    r = subprocess.run([exe, str(src), str(dst), str(num_cus)], capture_output=True, text=True, timeout=900,
-                       env=env)
+    r = subprocess.run([exe, str(src), str(dst), str(num_cus), str(stride)], capture_output=True, text=True,
+                       timeout=900, env=env)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-6000:]
     raw = np.fromfile(dst, np.uint8)
     o = 0
@@ -104,19 +104,24 @@ def taus(s, rng):
     return t
 
 
-@pytest.mark.parametrize("Q,C,D,Cs,cus", [(40, 300, 36, 128, 2), (70, 200, 128, 64, 3), (33, 130, 256, 64, 2),
-                                          (20, 193, 96, 128, 4)])
-def test_emulated_route_keys_and_filter(emu_route, tmp_path, Q, C, D, Cs, cus):
+@pytest.mark.parametrize("Q,C,D,Cs,cus,stride", [(40, 300, 36, 128, 2, 2), (70, 200, 128, 64, 3, 3),
+                                                 (33, 130, 256, 64, 2, 1), (20, 193, 96, 128, 4, 1)])
+def test_emulated_route_keys_and_filter(emu_route, tmp_path, Q, C, D, Cs, cus, stride):
+    """Keys of the threshold sample (contiguous, or the 64-centroid chunks
+    j * stride spread over the table) and the candidate filter over every
+    centroid."""
     q, c = case(Q, C, D, seed=Q + C + D)
     s = exact_scores(q, c)
     rng = np.random.default_rng(D)
     tau = taus(s, rng)
     L = C + 8
-    off, q_bad, qbound, keys, cnt, cand = run(emu_route, tmp_path, q, c, Cs, L, tau, num_cus=cus)
+    off, q_bad, qbound, keys, cnt, cand = run(emu_route, tmp_path, q, c, Cs, L, tau, num_cus=cus, stride=stride)
     assert off == 0 and q_bad == 0
     l1 = np.abs(q.astype(np.int64) - 128).sum(axis=1)
     assert np.array_equal(qbound, (0.5 * (390 + l1)).astype(np.float32))
-    gmin = f32key(s[:, :Cs].reshape(Q, Cs // 16, 16).max(axis=2))
+    sample = np.concatenate([np.arange(64 * j * stride, 64 * j * stride + 64) for j in range(Cs // 64)])
+    assert sample[-1] < C
+    gmin = f32key(s[:, sample].reshape(Q, Cs // 16, 16).max(axis=2))
     assert np.array_equal(keys.view(np.uint32), gmin.view(np.uint32))
     k = f32key(s)
     for i in range(Q):

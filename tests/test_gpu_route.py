@@ -227,3 +227,24 @@ def test_route_int8_forced_fallback_and_extreme_ranks(ivf_ctx, oracle_mod):
             assert stats["screen_i8"] == 1
         finally:
             ivf_ctx.set_option(opt, 0)
+
+
+@pytest.mark.parametrize("kind", ["uint8", "normalised"])
+def test_route_sorted_table_keeps_threshold(ivf_ctx, oracle_mod, kind):
+    """A centroid table in spatial order (sorted by norm, or along the axis
+    of largest spread), as a table ordered by list or position would be: the
+    threshold sample is spread over the table, so the threshold is not
+    biased: no query overflows its candidate list or falls back, and ids and
+    distances equal the oracle's."""
+    if kind == "uint8":
+        d = synth.uniform_mixture_route(16384, 400, 128, seed=5, plants=0)
+        c, k = d["centroids"], 64
+        order = np.argsort((c.astype(np.float64) ** 2).sum(axis=1), kind="stable")
+    else:
+        d = synth.normalised_route(32768, 300, 96, seed=5, plants=0)
+        c, k = d["centroids"], 128
+        order = np.argsort(c[:, int(np.argmax(c.var(axis=0)))], kind="stable")
+    c = np.ascontiguousarray(c[order])
+    stats = assert_route_equal(ivf_ctx, oracle_mod, d["queries"], c, k)
+    assert stats["fallback"] == 0 and stats["overflow"] == 0
+    assert stats["sample"] > 0

@@ -4,7 +4,9 @@
 // minima, the candidate filter against given thresholds), with every array in
 // an allocation of its own, and writes what they produced for the test to
 // check against exact integer arithmetic.
-//   usage: route_i8_host in.bin out.bin num_cus
+//   usage: route_i8_host in.bin out.bin num_cus [stride]
+//   stride (optional, default 1): the sample is the 64-centroid chunks
+//        j * stride, j < Cs / 64 (the library spreads it over the table)
 //   in:  int64 Q, C, D, Cs, L; float queries [Q][D]; float centroids [C][D];
 //        float tau [Q]
 //   out: uint32 off flag; uint32 quantisation flag; float qbound [Q];
@@ -77,8 +79,10 @@ int main(int argc, char **argv)
         a.c_begin = 0;
         a.c_end = Cs;
         a.nchunks = Cs / kQuantChunk;
+        a.cstride = argc > 4 ? atoll(argv[4]) : 1;
         a.keys = keys;
         launch_route_i8(kRouteKeys, DP, a, num_cus, nullptr);
+        a.cstride = 1;
     }
     a.c_begin = 0;
     a.c_end = C;
