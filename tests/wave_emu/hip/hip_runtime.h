@@ -331,13 +331,31 @@ inline uint32_t atomicMax(uint32_t *p, uint32_t v)
 }
 
 namespace emu {
-// runs every block of the grid, one after another, with one host thread per lane
+// runs every block of the grid, one after another, with one host thread per
+// lane; the lane threads are created once per launch and run every block
+// (between blocks they wait at a launch barrier while the next block's LDS,
+// barriers and state are set up afresh)
 template <typename K, typename... A>
 void launch(K kernel, dim3 grid, dim3 block, size_t shared_bytes, A... args)
 {
     gdim = grid;
     bdim = block;
     const int nt = block.x;
+    std::barrier<> start(nt + 1), done(nt + 1);
+    bool quit = false;
+    unsigned cur = 0;
+    std::vector<std::thread> th;
+    for (int t = 0; t < nt; ++t)
+        th.emplace_back([&, t]() {
+            tid = dim3(t);
+            for (;;) {
+                start.arrive_and_wait();
+                if (quit) return;
+                bid = dim3(cur);
+                kernel(args...);
+                done.arrive_and_wait();
+            }
+        });
     for (unsigned b = 0; b < grid.x; ++b) {
         // a fresh allocation per block, filled with a pattern, so that reads
         // of LDS the block did not write are seen and overruns are reported
@@ -352,16 +370,14 @@ void launch(K kernel, dim3 grid, dim3 block, size_t shared_bytes, A... args)
             B.waves[w].bar = wb.back();
         }
         blk = &B;
-        std::vector<std::thread> th;
-        for (int t = 0; t < nt; ++t)
-            th.emplace_back([=]() {
-                tid = dim3(t);
-                bid = dim3(b);
-                kernel(args...);
-            });
-        for (auto &t : th) t.join();
+        cur = b;
+        start.arrive_and_wait();  // the block runs
+        done.arrive_and_wait();   // every lane has finished it
         for (auto *p : wb) delete p;
     }
+    quit = true;
+    start.arrive_and_wait();
+    for (auto &t : th) t.join();
 }
 }  // namespace emu
 #define hipLaunchKernelGGL(k, g, b, sh, s, ...) emu::launch(k, g, b, (size_t)(sh), __VA_ARGS__)
