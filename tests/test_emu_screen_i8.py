@@ -247,9 +247,9 @@ def test_emulated_pipeline_with_fallback(emu_bin, tmp_path, oracle_mod, mode, fo
 
 def test_emulated_single_plane_with_hints(emu_bin, tmp_path, oracle_mod):
     """Hinted labels (speed only) start each row's keep threshold from the
-    hinted centroid's score: a mix of exact labels and garbage (out of range,
-    negative, random) gives the same settled labels, worklist and rescreen
-    list as no hints."""
+    hinted centroid's score: the exact labels, garbage (out of range,
+    negative, random) and a mix give the same settled labels, worklist and
+    rescreen list as no hints."""
     x, c = rows_and_centroids(500, 140, 128, seed=12)
     lab0, wl0, st0, _ = run(emu_bin, tmp_path, x, c, mode=1)
     listed0 = run.listed
@@ -258,8 +258,7 @@ def test_emulated_single_plane_with_hints(emu_bin, tmp_path, oracle_mod):
     rng = np.random.default_rng(13)
     garbage = rng.integers(-5, 200, size=500).astype(np.int32)
     garbage[:10] = np.iinfo(np.int32).min
-    # exact hints for half of the rows, garbage (out of range, negative, random) for the rest
-    for hints in (np.where(rng.random(500) < 0.5, olab, garbage).astype(np.int32),):
+    for hints in (olab, garbage, np.where(rng.random(500) < 0.5, olab, garbage).astype(np.int32)):
         lab, wl, st, _ = run(emu_bin, tmp_path, x, c, mode=1, hints=hints)
         check(oracle_mod, lab, wl, st, x, c)
         assert np.array_equal(lab, lab0) and np.array_equal(np.sort(wl), np.sort(wl0))
@@ -293,9 +292,7 @@ def test_emulated_single_plane_visiting_order(emu_bin, tmp_path, oracle_mod, cas
     rng = np.random.default_rng(23)
     perm = rng.permutation(C).astype(np.uint32)
     olab = oracle_mod.assign(x, c).astype(np.int32)
-    # the library's keys once (their kernels are the same for any rows)
-    cases = ((perm, olab),) if case == "mixture" else (("auto", None),)
-    for order, hints in cases:
+    for order, hints in ((perm, None), (perm, olab), ("auto", None)):
         lab, wl, st, _ = run(emu_bin, tmp_path, x, c, mode=1, order=order, hints=hints)
         check(oracle_mod, lab, wl, st, x, c)
         assert np.array_equal(lab, lab0) and np.array_equal(np.sort(wl), np.sort(wl0))
