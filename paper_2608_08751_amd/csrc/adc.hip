@@ -219,12 +219,12 @@ __global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
     const float *__restrict__ Q, int D, const float *__restrict__ cent, int P, const uint32_t *__restrict__ perm,
     const uint8_t *__restrict__ codes, int M, const float *__restrict__ codebooks, int k,
     const int32_t *__restrict__ gcnt, const int32_t *__restrict__ dl, const longlong2 *__restrict__ dpos,
-    uint64_t *__restrict__ handoff)
+    uint64_t *__restrict__ handoff, int32_t *__restrict__ hcnt)
 {
-    extern __shared__ float dyn[];  // r [D] then LUT [M][256]
+    extern __shared__ double dyn[];  // r [D] (fp64) then LUT [M][256] (fp32)
     __shared__ PoolLds pool;
-    float *r = dyn;
-    float *lut = dyn + D;
+    double *r = dyn;
+    float *lut = reinterpret_cast<float *>(dyn + D);
     const int t = threadIdx.x;
     const int64_t b = blockIdx.x / (2 * P);
     const int j = (int)(blockIdx.x - b * 2 * P);
@@ -233,18 +233,36 @@ __global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
     const int32_t l = dl[slot];
     const longlong2 range = dpos[slot];
     const int dsub = D / M;
-    for (int d = t; d < D; d += kAdcThreads) r[d] = Q[b * D + d] - cent[(int64_t)l * D + d];
+    // the residual in fp32 (as defined), held in fp64 for the table's sums
+    for (int d = t; d < D; d += kAdcThreads) r[d] = (double)(Q[b * D + d] - cent[(int64_t)l * D + d]);
     if (t == 0) pool.n = 0;
     __syncthreads();
-    for (int e = t; e < M * kPqK; e += kAdcThreads) {
-        const float *wr = codebooks + (int64_t)e * dsub;
-        const float *rm = r + (e >> 8) * dsub;
-        double acc = 0.0;
-        for (int d = 0; d < dsub; ++d) {
-            const double v = (double)rm[d] - (double)wr[d];
-            acc = fma(v, v, acc);
+    if (dsub == 8) {
+        // the common 8-dimension subspace: two 16-byte codebook loads per entry
+        for (int e = t; e < M * kPqK; e += kAdcThreads) {
+            const float4 *wr = reinterpret_cast<const float4 *>(codebooks + (int64_t)e * 8);
+            const float4 w0 = wr[0], w1 = wr[1];
+            const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            const double *rm = r + (e >> 8) * 8;
+            double acc = 0.0;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) {
+                const double v = rm[d] - (double)w[d];
+                acc = fma(v, v, acc);
+            }
+            lut[e] = (float)acc;
         }
-        lut[e] = (float)acc;
+    } else {
+        for (int e = t; e < M * kPqK; e += kAdcThreads) {
+            const float *wr = codebooks + (int64_t)e * dsub;
+            const double *rm = r + (e >> 8) * dsub;
+            double acc = 0.0;
+            for (int d = 0; d < dsub; ++d) {
+                const double v = rm[d] - (double)wr[d];
+                acc = fma(v, v, acc);
+            }
+            lut[e] = (float)acc;
+        }
     }
     __syncthreads();
     for (int64_t c0 = range.x; c0 < range.y; c0 += kAdcChunk) {
@@ -272,32 +290,38 @@ __global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
         __syncthreads();
         if ((int)pool.n > k) pool_trim(pool, k);
     }
+    // the group's keys (at most k) and their count
     uint64_t *out = handoff + slot * k;
     const int n = (int)pool.n;
-    for (int i = t; i < k; i += kAdcThreads) out[i] = i < n ? pool.key[i] : kNoKey;
+    for (int i = t; i < n; i += kAdcThreads) out[i] = pool.key[i];
+    if (t == 0) hcnt[slot] = n;
 }
 
 __global__ __launch_bounds__(kAdcThreads) void adc_merge_kernel(const uint64_t *__restrict__ handoff,
-                                                               int P, int k, const int32_t *__restrict__ gcnt,
+                                                               const int32_t *__restrict__ hcnt, int P, int k,
+                                                               const int32_t *__restrict__ gcnt,
                                                                uint32_t *__restrict__ ids, float *__restrict__ dist)
 {
     __shared__ PoolLds pool;
     const int t = threadIdx.x;
     const int64_t b = blockIdx.x;
     const uint64_t *in = handoff + b * 2 * (int64_t)P * k;
-    const int64_t total = (int64_t)gcnt[b] * k;  // the query's groups
+    const int32_t *hc = hcnt + b * 2 * (int64_t)P;
+    const int G = gcnt[b];  // the query's groups
     if (t == 0) pool.n = 0;
     __syncthreads();
-    for (int64_t c0 = 0; c0 < total; c0 += kAdcChunk) {
-        const int len = (int)min((int64_t)kAdcChunk, total - c0);
-        // append the chunk's real keys (missing entries are skipped)
-        for (int i = t; i < len; i += kAdcThreads) {
-            const uint64_t v = in[c0 + i];
-            if (v != kNoKey) pool.key[atomicAdd(&pool.n, 1u)] = v;
-        }
+    // append the groups' keys (n <= k each) while they fit the pool; trim it
+    // to the k smallest only when the next group would not fit
+    for (int g = 0; g < G; ++g) {
+        const int n = hc[g];
+        if ((int)pool.n + n > kAdcPool) pool_trim(pool, k);  // then pool.n = k, and k + n <= kAdcPool
+        const int base = (int)pool.n;
+        for (int i = t; i < n; i += kAdcThreads) pool.key[base + i] = in[(int64_t)g * k + i];
         __syncthreads();
-        if ((int)pool.n > k) pool_trim(pool, k);
+        if (t == 0) pool.n = (uint32_t)(base + n);
+        __syncthreads();
     }
+    if ((int)pool.n > k) pool_trim(pool, k);
     // bitonic sort of the pool (at most k <= kAdcMaxK keys) ascending
     const int n = (int)pool.n;
     int np = 1;
@@ -340,12 +364,12 @@ hipError_t launch_adc_scan(const float *Q, int64_t B, int D, const float *cent, 
                        w.gcnt, w.dl, w.dpos);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t lds = (size_t)(D + M * kPqK) * sizeof(float);
+    const size_t lds = (size_t)D * sizeof(double) + (size_t)M * kPqK * sizeof(float);
     hipLaunchKernelGGL(adc_group_kernel, dim3((unsigned)(B * 2 * P)), dim3(kAdcThreads), lds, s, Q, D, cent, P,
-                       perm, codes, M, codebooks, k, w.gcnt, w.dl, w.dpos, w.handoff);
+                       perm, codes, M, codebooks, k, w.gcnt, w.dl, w.dpos, w.handoff, w.hcnt);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(adc_merge_kernel, dim3((unsigned)B), dim3(kAdcThreads), 0, s, w.handoff, P, k, w.gcnt,
-                       ids, dist);
+    hipLaunchKernelGGL(adc_merge_kernel, dim3((unsigned)B), dim3(kAdcThreads), 0, s, w.handoff, w.hcnt, P, k,
+                       w.gcnt, ids, dist);
     return hipGetLastError();
 }
 

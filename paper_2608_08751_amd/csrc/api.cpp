@@ -123,6 +123,7 @@ size_t layout_adc(void *base, int64_t B, int64_t P, int64_t k, AdcScratch *w)
     Carver c(base);
     AdcScratch s;
     s.handoff = c.take<uint64_t>((size_t)B * 2 * P * k);
+    s.hcnt = c.take<int32_t>((size_t)B * 2 * P);
     s.dl = c.take<int32_t>((size_t)B * 2 * P);
     s.dpos = c.take<longlong2>((size_t)B * 2 * P);
     s.gcnt = c.take<int32_t>((size_t)B);

@@ -312,6 +312,7 @@ constexpr int kMaxAdcProbes = 4096;
 // k keys and a descriptor (list id, code range), and each query's group count.
 struct AdcScratch {
     uint64_t *handoff;  // [B * 2P * k]
+    int32_t *hcnt;      // [B * 2P] keys the group handed over (<= k)
     int32_t *dl;        // [B * 2P] list of the group
     longlong2 *dpos;    // [B * 2P] first and end code position of the group
     int32_t *gcnt;      // [B] groups of the query
