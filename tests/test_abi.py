@@ -312,8 +312,9 @@ def test_adc_scan_validation(vctx, lib):
                                         a.get("N", 100000), codes, a.get("M", 16), cb, a.get("k", 512),
                                         a.get("ids", ids), a.get("dist", dist))
     need = lib.ivf_workspace_bytes(B.IVF_OP_ADC_SCAN, 100, 64, 128, 512)
-    # handoff keys (at most 2 * 64 groups of 512 per query) plus the group descriptors
-    assert 100 * 128 * 512 * 8 < need <= 100 * 128 * (512 * 8 + 20) + 100 * 4 + 5 * 256
+    # handoff keys (at most 2 * 64 groups of 512 per query) plus the group
+    # descriptors and handoff counts
+    assert 100 * 128 * 512 * 8 < need <= 100 * 128 * (512 * 8 + 24) + 100 * 4 + 6 * 256
     assert lib.ivf_workspace_bytes(B.IVF_OP_ADC_SCAN, 100, 64, 128, 2000) == 0
     assert call() == B.IVF_ENOMEM
     assert lib.ivf_set_workspace(h, P(20 * GB), need) == B.IVF_OK
