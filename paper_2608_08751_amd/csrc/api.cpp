@@ -135,8 +135,9 @@ size_t layout_adc(void *base, int64_t B, int64_t P, int64_t k, AdcScratch *w)
 // [1] worklist counter, [2] nonzero when some centroid does not quantise for
 // the int8 screen, [3] the same for its single plane, [4] the single plane's
 // largest coordinate residual (float bits), [5] counter of the rows the
-// single plane leaves to the two planes, then (from word 16) kNumStats
-// uint64 counters.
+// single plane leaves to the two planes, [6] the int8 routing gate, [7] the
+// single plane's largest residual norm (float bits), then (from word 16)
+// kNumStats uint64 counters.
 struct Scalars {
     uint32_t *mc2_bits;
     uint32_t *wl_cnt;
@@ -494,6 +495,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
     uint32_t *q_bad1 = l.sc.mc2_bits + 3;
     uint32_t *e_bits = l.sc.mc2_bits + 4;
     uint32_t *list_cnt = l.sc.mc2_bits + 5;
+    uint32_t *r2_bits = l.sc.mc2_bits + 7;
     const uint32_t *ord1 = nullptr;
     const int32_t *pos1 = nullptr;
     if (int8) {
@@ -512,8 +514,8 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
                 TIMED("order1_offsets", launch_offsets(l.ocounts, kOrder1Keys, l.ooffsets, s));
                 TIMED("order1_scatter", launch_radix_level1_scatter(rp, rs, l.ooffsets, l.ord1, s));
             }
-            TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, s,
-                                                          ordered ? l.ord1 : nullptr, ordered ? l.pos1 : nullptr));
+            TIMED("quantize1", launch_quantize_centroids1(cent, C, D, DP, l.qc1, l.negb1, q_bad1, e_bits, r2_bits,
+                                                          s, ordered ? l.ord1 : nullptr, ordered ? l.pos1 : nullptr));
             ord1 = ordered ? l.ord1 : nullptr;
             pos1 = ordered ? l.pos1 : nullptr;
         }
@@ -567,6 +569,7 @@ ivf_status enqueue_assign(ivf_ctx *ctx, const void *rows, int rowtype, int64_t N
                 q.qc1 = l.qc1;
                 q.negb1 = l.negb1;
                 q.e_bits = e_bits;
+                q.r2_bits = r2_bits;
                 q.q_bad1 = q_bad1;
                 q.list = l.list;
                 q.list_cnt = list_cnt;

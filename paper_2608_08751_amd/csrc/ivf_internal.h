@@ -101,6 +101,7 @@ struct ScreenI8Args {
     const int8_t *qc1;
     const int32_t *negb1;
     const uint32_t *e_bits;
+    const uint32_t *r2_bits;  // the largest residual norm ||c' - H1||_2 (float bits; null: E only)
     int64_t ncent;
     int force_rescreen;
     // single plane: a label per row from an earlier step, or null; the row's
@@ -125,7 +126,7 @@ hipError_t launch_screen_i8(int DP, const ScreenI8Args &a, int num_cus, hipStrea
 // ord (null: id order) puts centroid ord[p] at plane row p and records
 // pos[ord[p]] = p.
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
-                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s,
+                                      uint32_t *q_bad1, uint32_t *e_bits, uint32_t *r2_bits, hipStream_t s,
                                       const uint32_t *ord = nullptr, int32_t *pos = nullptr);
 // Visiting order of the single plane: keys[c] = a 15-bit bucket of
 // ||c - mean||^2 (mean over the centroids; the float's exponent and top 7

@@ -1052,8 +1052,8 @@ constexpr int kNoBias1 = -(1 << 26);  // bias of a padded centroid: below every 
 __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict__ cent, int64_t C, int D, int DP,
                                                         int64_t Cpad, int8_t *__restrict__ q1,
                                                         int32_t *__restrict__ negb1, uint32_t *__restrict__ q_bad1,
-                                                        uint32_t *__restrict__ e_bits, const uint32_t *__restrict__ ord,
-                                                        int32_t *__restrict__ pos)
+                                                        uint32_t *__restrict__ e_bits, uint32_t *__restrict__ r2_bits,
+                                                        const uint32_t *__restrict__ ord, int32_t *__restrict__ pos)
 {
     const int lane = threadIdx.x & 63;
     const int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -1062,7 +1062,7 @@ __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict_
         // plane row j holds centroid c (rows past C are padding)
         const int64_t c = ord && j < C ? (int64_t)ord[j] : j;
         if (pos && j < C && lane == 0) pos[c] = (int32_t)j;
-        double n2 = 0.0, e = 0.0;
+        double n2 = 0.0, e = 0.0, q2 = 0.0;
         bool bad = false;
         int8_t *q = q1 + j * DP;
         for (int d = lane; d < DP; d += 64) {
@@ -1075,6 +1075,7 @@ __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict_
                 } else {
                     hb = (int)p;
                     e = fmax(e, fabs(cp - p));
+                    q2 = fma(cp - p, cp - p, q2);  // cp - p is exact
                     n2 = fma(cp, cp, n2);
                 }
             }
@@ -1083,6 +1084,7 @@ __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict_
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
             n2 += __shfl_xor(n2, o);
+            q2 += __shfl_xor(q2, o);
             e = fmax(e, __shfl_xor(e, o));
         }
         if (__any(bad) && lane == 0) *q_bad1 = 1u;
@@ -1092,6 +1094,11 @@ __global__ __launch_bounds__(256) void quantize1_kernel(const float *__restrict_
             // skips the atomic once a larger residual is recorded
             const uint32_t eb = __float_as_uint(__double2float_ru(e));
             if (j < C && e > 0.0 && eb > __atomic_load_n(e_bits, __ATOMIC_RELAXED)) atomicMax(e_bits, eb);
+            // the residual vector's norm, rounded up (2^-40 covers the
+            // rounding of the sum of squares and of the square root)
+            const uint32_t rb = __float_as_uint(__double2float_ru(sqrt(q2) * (1.0 + 0x1p-40)));
+            if (r2_bits && j < C && q2 > 0.0 && rb > __atomic_load_n(r2_bits, __ATOMIC_RELAXED))
+                atomicMax(r2_bits, rb);
         }
     }
 }
@@ -1364,13 +1371,23 @@ __device__ void screen1_tile(const ScreenI8Args &a, int64_t tile, char *__restri
     uint32_t l1[RB];
     load_rows<DP, RB>(a.rows, row0, a.nrows, a.D, wave, jl, h, xf, l1);
 
-    // T = ceil(2 E ||x'||_1 + 1) + 1 >= 2W (E rounded up; one unit of margin)
+    // T = ceil(2 min(E ||x'||_1, R2 ||x'||_2) + 1) + 1 >= 2W (E and R2
+    // rounded up; one unit of margin): |x'.(c' - H1)| is at most both
+    // E ||x'||_1 and, by Cauchy-Schwarz, ||x'||_2 ||c' - H1||_2 <= ||x'||_2 R2
     const double E = (double)__uint_as_float(*a.e_bits);
+    const double R2 = a.r2_bits ? (double)__uint_as_float(*a.r2_bits) : __builtin_huge_val();
     Top3i st[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         l1[rb] += __shfl_xor(l1[rb], 32);
-        const int T = (int)ceil(2.0 * E * (double)l1[rb]) + 2;
+        int q2 = 0;  // ||x'||_2^2 (exact; the lane's half of the dimensions, then both)
+#pragma unroll
+        for (int k = 0; k < DP / 32; ++k)
+#pragma unroll
+            for (int w = 0; w < 4; ++w) q2 = __builtin_amdgcn_sdot4(xf[rb][k][w], xf[rb][k][w], q2, false);
+        q2 += __shfl_xor(q2, 32);
+        const double wb = fmin(E * (double)l1[rb], sqrt((double)q2) * R2);
+        const int T = (int)ceil(2.0 * wb) + 2;
         st[rb] = Top3i{kNoScore, kNoScore, kNoScore, -1, -1, kNoScore, T, kNoScore};
     }
     // A hinted label (an earlier step's) starts the keep threshold from that
@@ -1509,13 +1526,13 @@ hipError_t launch_quantize_centroids(const float *cent, int64_t C, int D, int DP
 }
 
 hipError_t launch_quantize_centroids1(const float *cent, int64_t C, int D, int DP, int8_t *q1, int32_t *negb1,
-                                      uint32_t *q_bad1, uint32_t *e_bits, hipStream_t s, const uint32_t *ord,
-                                      int32_t *pos)
+                                      uint32_t *q_bad1, uint32_t *e_bits, uint32_t *r2_bits, hipStream_t s,
+                                      const uint32_t *ord, int32_t *pos)
 {
     const int64_t cpad = quantized_pad1(C);
     const int64_t blocks = std::min<int64_t>((cpad + 3) / 4, 65536);
     hipLaunchKernelGGL(quantize1_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cent, C, D, DP, cpad, q1, negb1,
-                       q_bad1, e_bits, ord, pos);
+                       q_bad1, e_bits, r2_bits, ord, pos);
     return hipGetLastError();
 }
 

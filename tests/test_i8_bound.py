@@ -7,9 +7,10 @@ c' = c - 128), and the prefilter inequality s <= 256 h + 128 ||x'||_1 with
 h = x'.H - Bh. Distances are evaluated exactly with rational arithmetic on a
 subset. The single-plane screen's arithmetic: one int8 plane H1 = rint(c'),
 the score s1 = x'.H1 - b1 with b1 = rint(||c'||^2 / 2), and the bound
-|g - s1| <= E ||x'||_1 + 1/2 with g = x'.c' - ||c'||^2 / 2 = -k / 2 and E the
-largest coordinate residual |c' - H1|, on which its window
-T = ceil(2 E ||x'||_1) + 2 rests."""
+|g - s1| <= min(E ||x'||_1, R2 ||x'||_2) + 1/2 with g = x'.c' - ||c'||^2 / 2
+= -k / 2, E the largest coordinate residual |c' - H1| and R2 the largest
+residual norm ||c' - H1||_2 (Cauchy-Schwarz), on which its window
+T = ceil(2 min(E ||x'||_1, R2 ||x'||_2)) + 2 rests."""
 from fractions import Fraction
 
 import numpy as np
@@ -149,20 +150,29 @@ def test_int32_headroom_at_the_largest_dimension():
 
 # ---------------------------------------------------------------- single plane
 
+def _f32_up(v):
+    f = np.float32(v)
+    return float(np.nextafter(f, np.float32(np.inf))) if float(f) < v else float(f)
+
+
 def quantise1(c):
-    """One int8 plane, its biases and E rounded up to fp32 (as the kernel)."""
+    """One int8 plane, its biases, E and R2 rounded up to fp32 (as the
+    kernel: R2 from the fp64 sum of squared residuals, its square root
+    times 1 + 2^-40)."""
     cp = c.astype(np.float64) - 128.0
     H1 = np.rint(cp)
     assert np.all((H1 >= -128) & (H1 <= 127))
     b1 = np.rint(0.5 * np.sum(cp * cp, axis=1)).astype(np.int64)
     e = float(np.max(np.abs(cp - H1))) if c.size else 0.0
-    E = float(np.nextafter(np.float32(e), np.float32(1))) if np.float32(e) < e else float(np.float32(e))
-    return H1.astype(np.int64), b1, E
+    r = float(np.max(np.sqrt(np.sum((cp - H1) ** 2, axis=1)))) if c.size else 0.0
+    return H1.astype(np.int64), b1, _f32_up(e), _f32_up(r * (1.0 + 2.0 ** -40))
 
 
-def window(x, E):
-    l1 = np.abs(x.astype(np.int64) - 128).sum(axis=1)
-    return np.ceil(2.0 * E * l1).astype(np.int64) + 2
+def window(x, E, R2):
+    xp = x.astype(np.int64) - 128
+    l1 = np.abs(xp).sum(axis=1)
+    l2 = np.sqrt((xp * xp).sum(axis=1).astype(np.float64))
+    return np.ceil(2.0 * np.minimum(E * l1, l2 * R2)).astype(np.int64) + 2
 
 
 def test_single_plane_range_and_integer_centroids():
@@ -170,17 +180,18 @@ def test_single_plane_range_and_integer_centroids():
     E = 0; 255.5 rounds (half to even) to 128 and does not fit."""
     rng = np.random.default_rng(5)
     c = rng.uniform(-0.49, 255.49, size=(300, 40)).astype(np.float32)
-    H1, _, E = quantise1(c)
-    assert H1.min() >= -128 and H1.max() <= 127 and 0.0 < E <= 0.5
+    H1, _, E, R2 = quantise1(c)
+    assert H1.min() >= -128 and H1.max() <= 127 and 0.0 < E <= 0.5 and 0.0 < R2 <= 0.5 * 40 ** 0.5 + 1e-6
     ci = rng.integers(0, 256, size=(50, 40)).astype(np.float32)
-    assert quantise1(ci)[2] == 0.0
+    assert quantise1(ci)[2:] == (0.0, 0.0)
     assert np.rint(np.float64(np.float32(255.5)) - 128.0) == 128.0
 
 
 def test_single_plane_error_within_bound_exact_arithmetic():
-    """|g - s1| <= E ||x'||_1 + 1/2 in exact rational arithmetic, including
-    centroids on and next to the half-unit rounding boundaries, and the
-    kernel's window T exceeds twice that error."""
+    """|g - s1| <= min(E ||x'||_1, R2 ||x'||_2) + 1/2 in exact rational
+    arithmetic (the second bound compared squared), including centroids on
+    and next to the half-unit rounding boundaries; R2 bounds every residual
+    norm; the kernel's window T exceeds twice the error."""
     rng = np.random.default_rng(6)
     D, C = 16, 40
     c = rng.uniform(0.0, 255.4, size=(C, D)).astype(np.float32)
@@ -192,20 +203,25 @@ def test_single_plane_error_within_bound_exact_arithmetic():
     x = rng.integers(0, 256, size=(30, D))
     x[0] = 0
     x[1] = 255
-    H1, b1, E = quantise1(c)
+    H1, b1, E, R2 = quantise1(c)
     s1 = (x - 128) @ H1.T - b1[None, :]
-    T = window(x, E)
+    T = window(x, E, R2)
     cf = [[Fraction(float(v)) - 128 for v in row] for row in c]
+    for j in range(C):  # R2 bounds each residual norm
+        assert sum((cf[j][d] - int(H1[j, d])) ** 2 for d in range(D)) <= Fraction(R2) ** 2
     worst = Fraction(0)
     for i in range(x.shape[0]):
         xp = [int(v) - 128 for v in x[i]]
-        W = Fraction(E) * sum(abs(v) for v in xp) + Fraction(1, 2)
+        W1 = Fraction(E) * sum(abs(v) for v in xp)
+        n2 = sum(v * v for v in xp)
         for j in range(C):
             g = sum(a * b for a, b in zip(xp, cf[j])) - sum(v * v for v in cf[j]) / 2
-            e = g - int(s1[i, j])
-            assert abs(e) <= W, (i, j, float(e), float(W))
-            assert 2 * abs(e) < int(T[i])
-            worst = max(worst, abs(e) / W)
+            e = abs(g - int(s1[i, j]))
+            assert e <= W1 + Fraction(1, 2), (i, j, float(e), float(W1))
+            if e > Fraction(1, 2):
+                assert (e - Fraction(1, 2)) ** 2 <= n2 * Fraction(R2) ** 2, (i, j, float(e))
+            assert 2 * e < int(T[i])
+            worst = max(worst, e / (W1 + Fraction(1, 2)))
     assert worst > Fraction(1, 20)
 
 
@@ -225,9 +241,12 @@ def test_single_plane_certificate_never_excludes_the_nearest():
             c = np.rint(c).astype(np.float32)
         base = np.rint(c[rng.integers(0, C, N)])
         x = np.clip(base + rng.integers(-20, 21, size=(N, D)), 0, 255).astype(np.int64)
-        H1, b1, E = quantise1(c)
+        H1, b1, E, R2 = quantise1(c)
         s1 = (x - 128) @ H1.T - b1[None, :]
-        T = window(x, E)
+        T = window(x, E, R2)
+        if not integer:  # the norm bound is the tighter one for mean-like centroids
+            l1 = np.abs(x - 128).sum(axis=1)
+            assert np.mean(T) < 0.85 * np.mean(np.ceil(2.0 * E * l1) + 2)
         d = ((x[:, None, :].astype(np.float64) - c[None, :, :].astype(np.float64)) ** 2).sum(axis=2)
         nearest = np.argmin(d, axis=1)
         order = np.argsort(-s1, axis=1, kind="stable")
@@ -249,7 +268,7 @@ def test_single_plane_int32_headroom():
     bias -2^26 stays below every real score) and well inside int32."""
     D = 128
     c = np.stack([np.zeros(D), np.full(D, 255.4)]).astype(np.float32)
-    H1, b1, _ = quantise1(c)
+    H1, b1, _, _ = quantise1(c)
     for xv in (0, 255):
         x = np.full((1, D), xv, np.int64)
         s1 = (x - 128) @ H1.T - b1[None, :]

@@ -74,6 +74,7 @@ int main(int argc, char **argv)
     int32_t *list = single ? alloc<int32_t>(list_cap, 0) : nullptr;
     uint32_t *q_bad1 = alloc<uint32_t>(1, 0);
     uint32_t *e_bits = alloc<uint32_t>(1, 0);
+    uint32_t *r2_bits = alloc<uint32_t>(1, 0);
     uint32_t *list_cnt = alloc<uint32_t>(1, 0);
 
     launch_quantize_centroids(cent, C, D, DP, qc, negb, q_bad, nullptr);
@@ -121,12 +122,13 @@ int main(int argc, char **argv)
                 fclose(of);
             }
         }
-        launch_quantize_centroids1(cent, C, D, DP, qc1, negb1, q_bad1, e_bits, nullptr, ord, pos);
+        launch_quantize_centroids1(cent, C, D, DP, qc1, negb1, q_bad1, e_bits, r2_bits, nullptr, ord, pos);
         a.ord1 = ord;
         a.pos1 = pos;
         a.qc1 = qc1;
         a.negb1 = negb1;
         a.e_bits = e_bits;
+        a.r2_bits = r2_bits;
         a.q_bad1 = q_bad1;
         a.list = list;
         a.list_cnt = list_cnt;
