@@ -237,6 +237,7 @@ struct RouteLayout {
     uint32_t *cand_cnt;
     uint2 *cand;
     float *keys;
+    float *kmin;
     int32_t *wl;
     // int8 route planes (plan.qdp > 0): two planes [quantized_pad(C)][2 qdp],
     // biases, per-query bounds
@@ -257,6 +258,7 @@ RouteLayout layout_route(void *base, const RoutePlan &p, int64_t C)
     l.cand_cnt = c.take<uint32_t>(p.QB);
     l.cand = c.take<uint2>((size_t)p.QB * p.L);
     l.keys = c.take<float>((size_t)p.QB * p.Cs);
+    l.kmin = c.take<float>((size_t)p.QB * (p.Cs / 16));
     l.wl = c.take<int32_t>(p.QB);
     l.qc = nullptr;
     l.negb = nullptr;
@@ -918,6 +920,7 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
             a.nchunks = p.Cs / kChunk;
             a.cstride = p.Ss;
             a.keys = l.keys;
+            a.kmin = l.kmin;
             if (i8) {
                 ra.c_begin = 0;
                 ra.c_end = p.Cs;
@@ -940,6 +943,7 @@ ivf_status enqueue_route(ivf_ctx *ctx, const float *queries, int64_t Q, const fl
         r.sstride = p.Ss;
         r.rank_j = p.rank_j;
         r.keys = l.keys;
+        r.kmin = l.kmin;
         r.tau = l.tau;
         r.cand_cnt = l.cand_cnt;
         r.cand = l.cand;

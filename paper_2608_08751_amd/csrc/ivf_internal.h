@@ -46,6 +46,7 @@ struct ScreenArgs {
     int64_t skip_n, skip_s;
     // keys mode
     float *keys;            // [nrows, nchunks * kChunk]
+    float *kmin;            // [nrows, nchunks * kChunk / 16]: the minimum of every 16 keys
     // filter mode
     const float *tau;       // [nrows]
     uint32_t *cand_cnt;     // [nrows]
@@ -156,6 +157,7 @@ struct RouteArgs {
     int64_t sstride;        // the sample is the chunks j * sstride of kChunk centroids (0: 1)
     int rank_j;
     const float *keys;      // [nq, Cs]
+    const float *kmin;      // [nq, Cs / 16] the minimum of every 16 sample keys (fp32 keys)
     float *tau;             // [nq]
     uint32_t *cand_cnt;     // [nq]
     uint2 *cand;            // [nq, L]

@@ -748,9 +748,25 @@ __device__ void screen_keys_range(const ScreenArgs &a, int64_t tile, int64_t ch_
         f32x16 acc0, acc1;
         mfma_chunk<DP, false>(Ab + buf * CS, Nb + buf * kChunk, b, acc0, acc1, acc0, acc1, 0, unused);
 
+        // the minimum key of each 16 consecutive sample positions: group m
+        // of the chunk is registers 8(m%2) .. 8(m%2)+7 of block m/2 in both
+        // half-lanes, and min(-2v) = -2 max(v) exactly
+        float gm[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const f32x16 &p = m < 2 ? acc0 : acc1;
+            const int r0 = 8 * (m & 1);
+            float v = fmaxf(fmaxf(fmaxf(p[r0], p[r0 + 1]), fmaxf(p[r0 + 2], p[r0 + 3])),
+                            fmaxf(fmaxf(p[r0 + 4], p[r0 + 5]), fmaxf(p[r0 + 6], p[r0 + 7])));
+            v = fmaxf(v, __shfl_xor(v, 32));
+            gm[m] = -2.0f * v;
+        }
         // register r of block rb holds centroid rb*32 + 8*(r/4) + 4*h + r%4
         if (rvalid) {
             const int64_t ld = a.nchunks * kChunk;  // keys in visiting order
+            if (h == 0 && a.kmin)
+                *reinterpret_cast<float4 *>(a.kmin + row * (ld / 16) + ch * (kChunk / 16)) =
+                    make_float4(gm[0], gm[1], gm[2], gm[3]);
             float *out = a.keys + row * ld + ch * kChunk + 4 * h;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {

@@ -321,6 +321,60 @@ __global__ __launch_bounds__(256) void route_threshold_reg_kernel(RouteArgs a)
     }
 }
 
+// The threshold from the group minima the fp32 keys pass wrote: tau = the
+// rank_j-th smallest minimum, then only the groups whose minimum is <= tau
+// (about rank_j of them) are read for their keys <= tau, which become
+// candidates (a group whose minimum exceeds tau holds none).
+__global__ __launch_bounds__(256) void route_threshold_gmin_kernel(RouteArgs a)
+{
+    if (int8_keys(a)) return;
+    const int64_t q = blockIdx.x;
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t sh[2];
+    __shared__ uint32_t s_cnt;
+    const int G = (int)(a.Cs / 16);
+    const float *gmin = a.kmin + q * G;
+    uint32_t v[kGroupsPerThread];
+    int nv = 0;
+#pragma unroll
+    for (int e = 0; e < kGroupsPerThread; ++e) {
+        const int g = threadIdx.x + 256 * e;
+        v[e] = 0xFFFFFFFFu;
+        if (g < G) {
+            v[e] = f2o(gmin[g]);
+            nv = e + 1;
+        }
+    }
+    if (threadIdx.x == 0) s_cnt = 0;
+    const uint32_t tho = block_select(v, nv, min(a.rank_j, G), hist, sh);
+    const float th = o2f(tho);
+    const float4 *k4 = reinterpret_cast<const float4 *>(a.keys + q * a.Cs);
+#pragma unroll
+    for (int e = 0; e < kGroupsPerThread; ++e) {
+        const int g = threadIdx.x + 256 * e;
+        if (g < G && v[e] <= tho) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 w = k4[4 * (int64_t)g + i];
+                const float kk[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (kk[c] <= th) {
+                        const uint32_t slot = atomicAdd(&s_cnt, 1u);
+                        if (slot < (uint32_t)a.L)
+                            a.cand[q * a.L + slot] = make_uint2(__float_as_uint(kk[c]), sample_id(a, 16 * g + 4 * i + c));
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a.tau[q] = th;
+        a.cand_cnt[q] = s_cnt;
+    }
+}
+
 // The threshold when the int8 route kernels ran: the keys buffer holds the
 // sample's group minima [nq, Cs / 16] directly, tau = the rank_j-th smallest,
 // and the sample's centroids are left to the filter, which then covers every
@@ -539,7 +593,9 @@ hipError_t launch_route_threshold(const RouteArgs &a, hipStream_t s)
 {
     const int64_t G = a.Cs / 16;
     if (a.i8_off && a.Cs > 0) hipLaunchKernelGGL(route_threshold_min_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
-    if (a.Cs > 0 && G <= 256)
+    if (a.Cs > 0 && a.kmin && G <= kMaxGroups)
+        hipLaunchKernelGGL(route_threshold_gmin_kernel, dim3((unsigned)a.nq), dim3(256), 0, s, a);
+    else if (a.Cs > 0 && G <= 256)
         hipLaunchKernelGGL(route_threshold_reg_kernel<1>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
     else if (a.Cs > 0 && G <= 512)
         hipLaunchKernelGGL(route_threshold_reg_kernel<2>, dim3((unsigned)a.nq), dim3(256), 0, s, a);
