@@ -1039,9 +1039,11 @@ hipError_t launch_route_i8_mode(int DP, const RouteI8Args &a, int num_cus, hipSt
 // integer
 //     s1(c) = x'.H1 - b1,
 // which differs from g(c) = x'.c' - ||c'||^2 / 2 = -k(c) / 2 by at most
-//     W = E ||x'||_1 + 1/2,   E = max_{c,d} |c'_d - H1_d|
-// (E = 0 for integer-valued centroids, such as rows sampled as the k-means
-// initialisation). With T >= 2W: if the best score beats the second by more
+//     W = min(E ||x'||_1, R2 ||x'||_2) + 1/2,
+//     E = max_{c,d} |c'_d - H1_d|,   R2 = max_c ||c' - H1||_2
+// (Cauchy-Schwarz for the second; E = R2 = 0 for integer-valued centroids,
+// such as rows sampled as the k-means initialisation). With T >= 2W: if the
+// best score beats the second by more
 // than T, its centroid is the unique nearest; if it beats the third by more
 // than T, the nearest is one of the two best and an exact fp64 evaluation
 // decides; otherwise the row is listed for the two-plane screen, whose bound
