@@ -115,11 +115,17 @@ __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
 // before the current choice. Ids outside [0, C) are skipped; a row without a
 // valid member gets -1 and an infinite distance.
 //
-// One wave per row: the row goes to the wave's LDS slot as fp32 (exact for
-// uint8), lane l evaluates members l, l + 64, ... and, on a hop, neighbour l,
-// each with the exact sequential fp64 chain (ds_read_b128 of the row is a
-// broadcast), and a butterfly takes the wave's (distance, id) minimum.
+// Eight rows per wave, eight lanes per row: each row goes to its LDS slot as
+// fp32 (exact for uint8), lane s of the row evaluates members s, s + 8, ...
+// and, on a hop, neighbours s, s + 8, ..., each with the exact sequential
+// fp64 chain (the row's ds_read_b128 is a broadcast within its eight lanes;
+// the slots are padded apart by four banks), and a butterfly over the eight
+// lanes takes the row's (distance, id) minimum. Every lane is busy in both
+// phases (one row per wave left 49 of 128 member lanes and 56 of 64 walk
+// lanes idle); the rows of a wave walk until none of them moves.
 constexpr int kAcWaves = 4;
+constexpr int kAcRows = 8;                      // rows per wave
+constexpr int kAcPitch = kCellsMaxDim + 4;      // floats per row slot
 
 __device__ __forceinline__ double dist_lds(const float *__restrict__ xs, const float *__restrict__ c, int D)
 {
@@ -149,9 +155,10 @@ __device__ __forceinline__ double dist_lds(const float *__restrict__ xs, const f
     return acc;
 }
 
-__device__ __forceinline__ void wave_min(double &d, int &id)
+// (distance, id) minimum over the eight lanes of a row
+__device__ __forceinline__ void row_min(double &d, int &id)
 {
-    for (int off = 32; off > 0; off >>= 1) {
+    for (int off = 4; off > 0; off >>= 1) {
         const double od = __shfl_xor(d, off);
         const int oid = __shfl_xor(id, off);
         if (dist_lt(od, oid, d, id)) {
@@ -168,32 +175,37 @@ __global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
     const uint32_t *__restrict__ members, int64_t M, const int32_t *__restrict__ graph, int S, int hops,
     const uint32_t *__restrict__ order, int32_t *__restrict__ labels, float *__restrict__ dist)
 {
-    __shared__ __attribute__((aligned(16))) float xs_all[kAcWaves][kCellsMaxDim];
+    __shared__ __attribute__((aligned(16))) float xs_all[kAcWaves][kAcRows][kAcPitch];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    float *xs = xs_all[wave];
+    const int slot = lane >> 3;  // the row of this lane within the wave
+    const int sub = lane & 7;    // its lane within the row
+    float *xs = xs_all[wave][slot];
     // a contiguous range of processing positions per workgroup: with rows in
     // cell order, consecutive rows of a workgroup read the same members
-    const int64_t per = ((N + gridDim.x - 1) / gridDim.x + kAcWaves - 1) / kAcWaves * kAcWaves;
+    constexpr int kPer = kAcWaves * kAcRows;
+    const int64_t per = ((N + gridDim.x - 1) / gridDim.x + kPer - 1) / kPer * kPer;
     const int64_t p0 = (int64_t)blockIdx.x * per, p1 = min(N, p0 + per);
-    for (int64_t p = p0 + wave; p < p1; p += kAcWaves) {
-        const int64_t i = order ? (int64_t)order[p] : p;
-        if (i >= N) continue;  // not a row
-        // the row into this wave's slot; the wave's own LDS operations run in
+    for (int64_t pb = p0 + wave * kAcRows; pb < p1; pb += kPer) {
+        const int64_t p = pb + slot;
+        const int64_t i = p < p1 ? (order ? (int64_t)order[p] : p) : N;
+        const bool live = i < N;  // order entries >= N are not rows
+        // the rows into their slots; the wave's own LDS operations run in
         // order, the fence keeps the compiler from moving reads above writes
         __builtin_amdgcn_wave_barrier();
-        for (int d = lane; d < D; d += 64) xs[d] = (float)X[i * D + d];
+        if (live)
+            for (int d = sub; d < D; d += kAcRows) xs[d] = (float)X[i * D + d];
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         __builtin_amdgcn_wave_barrier();
 
         double bd = __builtin_huge_val();
         int bi = INT_MAX;  // loses every comparison against a real candidate
-        const int32_t g = cell[i];
+        const int32_t g = live ? cell[i] : -1;
         if (g >= 0 && g < G) {
             int64_t m0 = offsets[g], m1 = offsets[g + 1];
             m0 = min(max(m0, (int64_t)0), M);
             m1 = min(max(m1, m0), M);
-            for (int64_t e = m0 + lane; e < m1; e += 64) {
+            for (int64_t e = m0 + sub; e < m1; e += kAcRows) {
                 const uint32_t j = members[e];
                 if ((int64_t)j < C) {
                     const double d = dist_lds(xs, cent + (int64_t)j * D, D);
@@ -204,23 +216,34 @@ __global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
                 }
             }
         }
-        wave_min(bd, bi);
-        for (int h = 0; bi != INT_MAX && graph && h < hops; ++h) {
+        row_min(bd, bi);
+        // greedy walk; a row that did not move stays where it is (its
+        // neighbours, and so its decision, do not change)
+        bool moving = bi != INT_MAX && graph != nullptr;
+        for (int h = 0; h < hops && __any(moving); ++h) {
             double nd = __builtin_huge_val();
             int ni = INT_MAX;
-            if (lane < S) {
-                const int32_t j = graph[(int64_t)bi * S + lane];
-                if (j >= 0 && j < C) {
-                    nd = dist_lds(xs, cent + (int64_t)j * D, D);
-                    ni = j;
+            if (moving) {
+                for (int n = sub; n < S; n += kAcRows) {
+                    const int32_t j = graph[(int64_t)bi * S + n];
+                    if (j >= 0 && j < C) {
+                        const double d = dist_lds(xs, cent + (int64_t)j * D, D);
+                        if (dist_lt(d, j, nd, ni)) {
+                            nd = d;
+                            ni = j;
+                        }
+                    }
                 }
             }
-            wave_min(nd, ni);
-            if (ni == INT_MAX || !dist_lt(nd, ni, bd, bi)) break;
-            bd = nd;
-            bi = ni;
+            row_min(nd, ni);
+            const bool better = moving && ni != INT_MAX && dist_lt(nd, ni, bd, bi);
+            if (better) {
+                bd = nd;
+                bi = ni;
+            }
+            moving = better;
         }
-        if (lane == 0) {
+        if (live && sub == 0) {
             const bool none = bi == INT_MAX;
             labels[i] = none ? -1 : bi;
             if (dist) dist[i] = none ? __builtin_huge_valf() : (float)bd;
@@ -258,7 +281,7 @@ hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const f
                                int32_t *labels, float *dist, int num_cus, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
-    const int64_t blocks = (N + kAcWaves - 1) / kAcWaves;
+    const int64_t blocks = (N + kAcWaves * kAcRows - 1) / (kAcWaves * kAcRows);
     const unsigned grid = (unsigned)std::min<int64_t>(blocks, (int64_t)num_cus * 32);
     if (rowtype == kRowU8)
         hipLaunchKernelGGL(assign_cells_kernel<uint8_t>, dim3(grid), dim3(kAcWaves * 64), 0, s,
