@@ -115,38 +115,49 @@ __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
 // before the current choice. Ids outside [0, C) are skipped; a row without a
 // valid member gets -1 and an infinite distance.
 //
-// Eight rows per wave, eight lanes per row: each row goes to its LDS slot as
-// fp32 (exact for uint8), lane s of the row evaluates members s, s + 8, ...
-// and, on a hop, neighbours s, s + 8, ..., each with the exact sequential
-// fp64 chain (the row's ds_read_b128 is a broadcast within its eight lanes;
-// the slots are padded apart by four banks), and a butterfly over the eight
-// lanes takes the row's (distance, id) minimum. Every lane is busy in both
-// phases (one row per wave left 49 of 128 member lanes and 56 of 64 walk
-// lanes idle); the rows of a wave walk until none of them moves.
-constexpr int kAcWaves = 4;
-constexpr int kAcRows = 8;                      // rows per wave
-constexpr int kAcPitch = kCellsMaxDim + 4;      // floats per row slot
+// A wave holds a tile of eight rows, each in its LDS slot as fp64 (exact for
+// uint8 and fp32 rows, so the chain needs no conversion of the row). When
+// every live row of the tile lies in the same cell (nearly always when the
+// rows come in cell order), the 64 lanes share the cell's members: lane l
+// takes members l, l + 64, ... and runs the exact sequential fp64 chain of
+// each against all eight rows at once, so one load of a centroid element
+// serves eight distances (the rows' LDS reads are broadcasts). A reduce-
+// scatter over the lanes then leaves each group of eight lanes (lanes 8r ..
+// 8r + 7) with row r's partial minima. Otherwise each row's eight lanes go
+// over the row's own members s, s + 8, .... Either way a butterfly inside the
+// group gives the row's (distance, id) minimum, and on a hop lane s of the
+// group evaluates neighbours s, s + 8, ...; the rows of a wave walk until
+// none of them moves. The slots are D + 2 doubles apart (four banks), so
+// the eight groups' reads of the walk do not collide.
+constexpr int kAcRows = 8;  // rows per wave
 
-__device__ __forceinline__ double dist_lds(const float *__restrict__ xs, const float *__restrict__ c, int D)
+__host__ __device__ constexpr int ac_pitch(int D) { return D + 2; }
+
+// waves per workgroup: four, or fewer where the slots would exceed 64 KiB
+int ac_waves(int D)
+{
+    const int w = 65536 / (kAcRows * ac_pitch(D) * (int)sizeof(double));
+    return w < 1 ? 1 : (w > 4 ? 4 : w);
+}
+
+__device__ __forceinline__ double dist_lds(const double *__restrict__ xs, const float *__restrict__ c, int D)
 {
     double acc = 0.0;
     for (int k0 = 0; k0 < D; k0 += 32) {
-        float4 xv[8], cv[8];
+        float4 cv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (k0 + 4 * q < D) cv[q] = *reinterpret_cast<const float4 *>(c + k0 + 4 * q);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             if (k0 + 4 * q < D) {
-                xv[q] = *reinterpret_cast<const float4 *>(xs + k0 + 4 * q);
-                cv[q] = *reinterpret_cast<const float4 *>(c + k0 + 4 * q);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            if (k0 + 4 * q < D) {
-                const float xa[4] = {xv[q].x, xv[q].y, xv[q].z, xv[q].w};
+                const double2 xa = *reinterpret_cast<const double2 *>(xs + k0 + 4 * q);
+                const double2 xb = *reinterpret_cast<const double2 *>(xs + k0 + 4 * q + 2);
+                const double xv[4] = {xa.x, xa.y, xb.x, xb.y};
                 const float ca[4] = {cv[q].x, cv[q].y, cv[q].z, cv[q].w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const double t = (double)xa[e] - (double)ca[e];
+                    const double t = xv[e] - (double)ca[e];
                     acc = fma(t, t, acc);
                 }
             }
@@ -155,65 +166,160 @@ __device__ __forceinline__ double dist_lds(const float *__restrict__ xs, const f
     return acc;
 }
 
+// The exact distances of centroid c to the eight rows of a tile (slots
+// `pitch` doubles apart), each its own sequential chain in dim order.
+__device__ __forceinline__ void dist_tile(const double *__restrict__ tile, int pitch, const float *__restrict__ c,
+                                          int D, double (&acc)[kAcRows])
+{
+#pragma unroll
+    for (int r = 0; r < kAcRows; ++r) acc[r] = 0.0;
+    for (int k0 = 0; k0 < D; k0 += 16) {
+        float4 cv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (k0 + 4 * q < D) cv[q] = *reinterpret_cast<const float4 *>(c + k0 + 4 * q);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (k0 + 4 * q < D) {
+                const double cd[4] = {(double)cv[q].x, (double)cv[q].y, (double)cv[q].z, (double)cv[q].w};
+#pragma unroll
+                for (int r = 0; r < kAcRows; ++r) {
+                    const double *xs = tile + r * pitch + k0 + 4 * q;
+                    const double2 xa = *reinterpret_cast<const double2 *>(xs);
+                    const double2 xb = *reinterpret_cast<const double2 *>(xs + 2);
+                    const double xv[4] = {xa.x, xa.y, xb.x, xb.y};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double t = xv[e] - cd[e];
+                        acc[r] = fma(t, t, acc[r]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void take_min(double &d, int &id, double od, int oid)
+{
+    if (dist_lt(od, oid, d, id)) {
+        d = od;
+        id = oid;
+    }
+}
+
+// Reduce-scatter of the eight rows' (distance, id) minima over the lane bits
+// 5, 4, 3: lane l keeps row (l >> 3), minimised over the lanes l ^ 8k.
+__device__ __forceinline__ void tile_scatter_min(const double (&bd)[kAcRows], const int (&bi)[kAcRows], int lane,
+                                                 double &d, int &id)
+{
+    const bool h5 = lane & 32, h4 = lane & 16, h3 = lane & 8;
+    double d4[4];
+    int i4[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {  // rows 4 * bit5 + k stay
+        const double sd = h5 ? bd[k] : bd[k + 4];
+        const int si = h5 ? bi[k] : bi[k + 4];
+        d4[k] = h5 ? bd[k + 4] : bd[k];
+        i4[k] = h5 ? bi[k + 4] : bi[k];
+        take_min(d4[k], i4[k], __shfl_xor(sd, 32), __shfl_xor(si, 32));
+    }
+    double d2[2];
+    int i2[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {  // of those, 2 * bit4 + k stay
+        const double sd = h4 ? d4[k] : d4[k + 2];
+        const int si = h4 ? i4[k] : i4[k + 2];
+        d2[k] = h4 ? d4[k + 2] : d4[k];
+        i2[k] = h4 ? i4[k + 2] : i4[k];
+        take_min(d2[k], i2[k], __shfl_xor(sd, 16), __shfl_xor(si, 16));
+    }
+    const double sd = h3 ? d2[0] : d2[1];
+    const int si = h3 ? i2[0] : i2[1];
+    d = h3 ? d2[1] : d2[0];
+    id = h3 ? i2[1] : i2[0];
+    take_min(d, id, __shfl_xor(sd, 8), __shfl_xor(si, 8));
+}
+
 // (distance, id) minimum over the eight lanes of a row
 __device__ __forceinline__ void row_min(double &d, int &id)
 {
     for (int off = 4; off > 0; off >>= 1) {
         const double od = __shfl_xor(d, off);
         const int oid = __shfl_xor(id, off);
-        if (dist_lt(od, oid, d, id)) {
-            d = od;
-            id = oid;
-        }
+        take_min(d, id, od, oid);
     }
 }
 
 template <typename XT>
-__global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
+__global__ __launch_bounds__(256) void assign_cells_kernel(
     const XT *__restrict__ X, int64_t N, const float *__restrict__ cent, int64_t C, int D,
     const int32_t *__restrict__ cell, int64_t G, const int64_t *__restrict__ offsets,
     const uint32_t *__restrict__ members, int64_t M, const int32_t *__restrict__ graph, int S, int hops,
     const uint32_t *__restrict__ order, int32_t *__restrict__ labels, float *__restrict__ dist)
 {
-    __shared__ __attribute__((aligned(16))) float xs_all[kAcWaves][kAcRows][kAcPitch];
+    extern __shared__ __attribute__((aligned(16))) unsigned char ac_lds[];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int slot = lane >> 3;  // the row of this lane within the wave
+    const int slot = lane >> 3;  // the row of this lane within the tile
     const int sub = lane & 7;    // its lane within the row
-    float *xs = xs_all[wave][slot];
+    const int pitch = ac_pitch(D);
+    double *tile = reinterpret_cast<double *>(ac_lds) + (size_t)wave * kAcRows * pitch;
+    double *xs = tile + slot * pitch;
     // a contiguous range of processing positions per workgroup: with rows in
     // cell order, consecutive rows of a workgroup read the same members
-    constexpr int kPer = kAcWaves * kAcRows;
-    const int64_t per = ((N + gridDim.x - 1) / gridDim.x + kPer - 1) / kPer * kPer;
+    const int per_tile = (int)(blockDim.x >> 6) * kAcRows;
+    const int64_t per = ((N + gridDim.x - 1) / gridDim.x + per_tile - 1) / per_tile * per_tile;
     const int64_t p0 = (int64_t)blockIdx.x * per, p1 = min(N, p0 + per);
-    for (int64_t pb = p0 + wave * kAcRows; pb < p1; pb += kPer) {
+    for (int64_t pb = p0 + wave * kAcRows; pb < p1; pb += per_tile) {
         const int64_t p = pb + slot;
         const int64_t i = p < p1 ? (order ? (int64_t)order[p] : p) : N;
         const bool live = i < N;  // order entries >= N are not rows
-        // the rows into their slots; the wave's own LDS operations run in
-        // order, the fence keeps the compiler from moving reads above writes
+        // the rows into their slots (a dead slot holds zeros); the wave's own
+        // LDS operations run in order, the fence keeps the compiler from
+        // moving reads above writes
         __builtin_amdgcn_wave_barrier();
-        if (live)
-            for (int d = sub; d < D; d += kAcRows) xs[d] = (float)X[i * D + d];
+        for (int d = sub; d < D; d += kAcRows) xs[d] = live ? (double)X[i * D + d] : 0.0;
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         __builtin_amdgcn_wave_barrier();
 
         double bd = __builtin_huge_val();
         int bi = INT_MAX;  // loses every comparison against a real candidate
         const int32_t g = live ? cell[i] : -1;
-        if (g >= 0 && g < G) {
+        const uint64_t lm = __ballot(live);
+        const int32_t g0 = __shfl(g, lm ? __ffsll((unsigned long long)lm) - 1 : 0);
+        const bool shared = lm != 0 && g0 >= 0 && g0 < G && !__any(live && g != g0);
+        if (shared) {
+            int64_t m0 = offsets[g0], m1 = offsets[g0 + 1];
+            m0 = min(max(m0, (int64_t)0), M);
+            m1 = min(max(m1, m0), M);
+            double td[kAcRows];
+            int ti[kAcRows];
+#pragma unroll
+            for (int r = 0; r < kAcRows; ++r) {
+                td[r] = __builtin_huge_val();
+                ti[r] = INT_MAX;
+            }
+            for (int64_t e = m0 + lane; e < m1; e += 64) {
+                const uint32_t j = members[e];
+                if ((int64_t)j < C) {
+                    double acc[kAcRows];
+                    dist_tile(tile, pitch, cent + (int64_t)j * D, D, acc);
+#pragma unroll
+                    for (int r = 0; r < kAcRows; ++r) take_min(td[r], ti[r], acc[r], (int)j);
+                }
+            }
+            tile_scatter_min(td, ti, lane, bd, bi);
+            if (!live) {  // a dead slot's row is not one
+                bd = __builtin_huge_val();
+                bi = INT_MAX;
+            }
+        } else if (g >= 0 && g < G) {
             int64_t m0 = offsets[g], m1 = offsets[g + 1];
             m0 = min(max(m0, (int64_t)0), M);
             m1 = min(max(m1, m0), M);
             for (int64_t e = m0 + sub; e < m1; e += kAcRows) {
                 const uint32_t j = members[e];
-                if ((int64_t)j < C) {
-                    const double d = dist_lds(xs, cent + (int64_t)j * D, D);
-                    if (dist_lt(d, (int)j, bd, bi)) {
-                        bd = d;
-                        bi = (int)j;
-                    }
-                }
+                if ((int64_t)j < C) take_min(bd, bi, dist_lds(xs, cent + (int64_t)j * D, D), (int)j);
             }
         }
         row_min(bd, bi);
@@ -226,13 +332,7 @@ __global__ __launch_bounds__(kAcWaves * 64) void assign_cells_kernel(
             if (moving) {
                 for (int n = sub; n < S; n += kAcRows) {
                     const int32_t j = graph[(int64_t)bi * S + n];
-                    if (j >= 0 && j < C) {
-                        const double d = dist_lds(xs, cent + (int64_t)j * D, D);
-                        if (dist_lt(d, j, nd, ni)) {
-                            nd = d;
-                            ni = j;
-                        }
-                    }
+                    if (j >= 0 && j < C) take_min(nd, ni, dist_lds(xs, cent + (int64_t)j * D, D), j);
                 }
             }
             row_min(nd, ni);
@@ -281,14 +381,17 @@ hipError_t launch_assign_cells(const void *rows, int rowtype, int64_t N, const f
                                int32_t *labels, float *dist, int num_cus, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
-    const int64_t blocks = (N + kAcWaves * kAcRows - 1) / (kAcWaves * kAcRows);
+    if (D < 4 || D > kCellsMaxDim || D % 4) return hipErrorInvalidValue;
+    const int waves = ac_waves(D);
+    const size_t lds = (size_t)waves * kAcRows * ac_pitch(D) * sizeof(double);
+    const int64_t blocks = (N + waves * kAcRows - 1) / (waves * kAcRows);
     const unsigned grid = (unsigned)std::min<int64_t>(blocks, (int64_t)num_cus * 32);
     if (rowtype == kRowU8)
-        hipLaunchKernelGGL(assign_cells_kernel<uint8_t>, dim3(grid), dim3(kAcWaves * 64), 0, s,
+        hipLaunchKernelGGL(assign_cells_kernel<uint8_t>, dim3(grid), dim3(waves * 64), lds, s,
                            (const uint8_t *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
                            order, labels, dist);
     else
-        hipLaunchKernelGGL(assign_cells_kernel<float>, dim3(grid), dim3(kAcWaves * 64), 0, s,
+        hipLaunchKernelGGL(assign_cells_kernel<float>, dim3(grid), dim3(waves * 64), lds, s,
                            (const float *)rows, N, cent, C, D, cell, G, offsets, members, M, graph, S, hops,
                            order, labels, dist);
     return hipGetLastError();

@@ -1,5 +1,6 @@
 // Host emulation of the HIP device environment used by the int8 screening
-// kernels (test infrastructure only; the library never runs on the host).
+// kernels and the cell assignment kernel (test infrastructure only; the
+// library never runs on the host).
 // One host thread per lane; wave-collective operations (__shfl_xor, __any,
 // readfirstlane, the int8 MFMA) exchange values through a per-wave barrier,
 // __syncthreads is a per-block barrier, and blocks of a grid run one after
@@ -40,6 +41,9 @@ inline uint2 make_uint2(unsigned x, unsigned y) { return uint2{x, y}; }
 inline float4 make_float4(float x, float y, float z, float w) { return float4{x, y, z, w}; }
 struct longlong2 {
     long long x, y;
+};
+struct double2 {
+    double x, y;
 };
 typedef int hipError_t;
 typedef void *hipStream_t;
@@ -295,6 +299,10 @@ inline int __builtin_amdgcn_readfirstlane(int v)
 }
 
 inline void __builtin_amdgcn_sched_barrier(int) {}
+// the wave's lanes meet (every lane of the wave must come)
+inline void __builtin_amdgcn_wave_barrier() { emu::wave().bar->arrive_and_wait(); }
+// a compiler fence; the host's barriers already order the lanes' accesses
+inline void __builtin_amdgcn_fence(int, const char *) {}
 
 inline uint32_t __float_as_uint(float f)
 {
