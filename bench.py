@@ -710,9 +710,9 @@ def bench_assign_cells(ctx, N=10_000_000, G=1024, S=8, hops=8):
     (three Lloyd steps over the centroid table), the cells of the centroids
     and of the rows against it (ivf_assign_build), the 8-nearest-centroid
     graph, then the nearest member of each row's cell and up to 8 greedy
-    graph moves, rows taken in cell order. Median of 3 calls of each timed
-    part; agreement with, and time against, the exact assignment of the same
-    rows."""
+    graph moves, rows taken in cell order (and the nearest member alone,
+    first_choice_ms). Median of 3 calls of each timed part; agreement
+    with, and time against, the exact assignment of the same rows."""
     import torch
 
     import synth
@@ -743,13 +743,15 @@ def bench_assign_cells(ctx, N=10_000_000, G=1024, S=8, hops=8):
     torch.cuda.synchronize()
     t = _timed(ctx, fn)
     agree = float((lab == exact).float().mean())
-    ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, None, 0, order=by_cell, out_labels=lab,
-                         out_dist=dist)
+    fn0 = lambda: ivf.ivf_assign_cells(ctx, x, cent, cell, c_off, c_mem, None, 0, order=by_cell, out_labels=lab,
+                                       out_dist=dist)
+    t0 = _timed(ctx, fn0)
     agree0 = float((lab == exact).float().mean())
     members_per_row = float(c_cnt[cell.long()].double().mean())
     per_row = t + t_cell
     out = {"rows": N, "centroids": C, "cells": G, "degree": S, "hops": hops, "coarse_train_ms": t_coarse,
            "members_ms": t_members, "graph_ms": t_graph, "row_cells_ms": t_cell, "assign_ms": t,
+           "first_choice_ms": t0,
            "members_per_cell_max": int(c_cnt.max()), "members_per_row_mean": members_per_row,
            "rows_per_s": N / (per_row * 1e-3), "agreement_with_exact": agree,
            "agreement_first_choice_only": agree0, "exact_assignment_ms": t_full,
