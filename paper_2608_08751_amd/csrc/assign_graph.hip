@@ -121,7 +121,9 @@ __global__ __launch_bounds__(kAgThreads) void assign_graph_kernel(
 // rows come in cell order), the 64 lanes share the cell's members: lane l
 // takes members l, l + 64, ... and runs the exact sequential fp64 chain of
 // each against all eight rows at once, so one load of a centroid element
-// serves eight distances (the rows' LDS reads are broadcasts). A reduce-
+// serves eight distances (the rows' LDS reads are broadcasts); a last pass
+// of at most 32 members gives each half of the wave four of the rows, so it
+// issues half the instructions of a full pass. A reduce-
 // scatter over the lanes then leaves each group of eight lanes (lanes 8r ..
 // 8r + 7) with row r's partial minima. Otherwise each row's eight lanes go
 // over the row's own members s, s + 8, .... Either way a butterfly inside the
@@ -166,13 +168,14 @@ __device__ __forceinline__ double dist_lds(const double *__restrict__ xs, const 
     return acc;
 }
 
-// The exact distances of centroid c to the eight rows of a tile (slots
-// `pitch` doubles apart), each its own sequential chain in dim order.
-__device__ __forceinline__ void dist_tile(const double *__restrict__ tile, int pitch, const float *__restrict__ c,
-                                          int D, double (&acc)[kAcRows])
+// The exact distances of centroid c to the NR rows of a tile from `rows` on
+// (slots `pitch` doubles apart), each its own sequential chain in dim order.
+template <int NR>
+__device__ __forceinline__ void dist_tile(const double *__restrict__ rows, int pitch, const float *__restrict__ c,
+                                          int D, double (&acc)[NR])
 {
 #pragma unroll
-    for (int r = 0; r < kAcRows; ++r) acc[r] = 0.0;
+    for (int r = 0; r < NR; ++r) acc[r] = 0.0;
     for (int k0 = 0; k0 < D; k0 += 16) {
         float4 cv[4];
 #pragma unroll
@@ -183,8 +186,8 @@ __device__ __forceinline__ void dist_tile(const double *__restrict__ tile, int p
             if (k0 + 4 * q < D) {
                 const double cd[4] = {(double)cv[q].x, (double)cv[q].y, (double)cv[q].z, (double)cv[q].w};
 #pragma unroll
-                for (int r = 0; r < kAcRows; ++r) {
-                    const double *xs = tile + r * pitch + k0 + 4 * q;
+                for (int r = 0; r < NR; ++r) {
+                    const double *xs = rows + r * pitch + k0 + 4 * q;
                     const double2 xa = *reinterpret_cast<const double2 *>(xs);
                     const double2 xb = *reinterpret_cast<const double2 *>(xs + 2);
                     const double xv[4] = {xa.x, xa.y, xb.x, xb.y};
@@ -299,13 +302,33 @@ __global__ __launch_bounds__(256) void assign_cells_kernel(
                 td[r] = __builtin_huge_val();
                 ti[r] = INT_MAX;
             }
-            for (int64_t e = m0 + lane; e < m1; e += 64) {
-                const uint32_t j = members[e];
-                if ((int64_t)j < C) {
-                    double acc[kAcRows];
-                    dist_tile(tile, pitch, cent + (int64_t)j * D, D, acc);
+            for (int64_t eb = m0; eb < m1; eb += 64) {
+                if (m1 - eb > 32) {
+                    const int64_t e = eb + lane;
+                    const uint32_t j = e < m1 ? members[e] : UINT32_MAX;
+                    if ((int64_t)j < C) {
+                        double acc[kAcRows];
+                        dist_tile<kAcRows>(tile, pitch, cent + (int64_t)j * D, D, acc);
 #pragma unroll
-                    for (int r = 0; r < kAcRows; ++r) take_min(td[r], ti[r], acc[r], (int)j);
+                        for (int r = 0; r < kAcRows; ++r) take_min(td[r], ti[r], acc[r], (int)j);
+                    }
+                } else {
+                    // a last pass of at most 32 members: half h of the wave
+                    // takes rows 4h .. 4h + 3, each lane half the chains
+                    const bool h = lane & 32;
+                    const int64_t e = eb + (lane & 31);
+                    const uint32_t j = e < m1 ? members[e] : UINT32_MAX;
+                    if ((int64_t)j < C) {
+                        double acc[4];
+                        dist_tile<4>(tile + (h ? 4 * pitch : 0), pitch, cent + (int64_t)j * D, D, acc);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            if (h)
+                                take_min(td[4 + r], ti[4 + r], acc[r], (int)j);
+                            else
+                                take_min(td[r], ti[r], acc[r], (int)j);
+                        }
+                    }
                 }
             }
             tile_scatter_min(td, ti, lane, bd, bi);
