@@ -611,6 +611,7 @@ def bench_pq(ctx, res, M=16, train_rows=1 << 20):
     flops = 3.0 * 256 * D * N
     tf = flops / (t_enc * 1e-3) / 1e12
     return ({"rows": N, "dim": D, "subspaces": M, "train_rows": train_rows, "train_step_ms": t_train,
+             "train_members_per_codeword_max": int(cnt.max()),
              "encode_ms": t_enc, "encode_rows_per_s": N / (t_enc * 1e-3), "encode_fp64_tflops": tf,
              "encode_fp64_frac": tf / PEAK_FP64_VECTOR_TFLOPS}, codes, cb)
 

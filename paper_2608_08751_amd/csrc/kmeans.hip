@@ -37,13 +37,13 @@ template <typename T> struct SumType;
 template <> struct SumType<uint8_t> { typedef unsigned long long type; };
 template <> struct SumType<float> { typedef double type; };
 
-constexpr int kMaxDimsPerLane = 4;  // D <= 256
 
 // Group g = blockIdx.y is an independent problem (a subspace of product
 // quantisation): its rows start g * gs.x elements further, its centroids
 // g * C * D floats, its counts, offsets and permutation g * C, g * (C + 1)
 // and g * N entries further, and its reseed uses seed + g.
-template <typename XT>
+// K dims per lane (D <= 64 K), 32 / K member rows in flight.
+template <typename XT, int K>
 __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, int64_t N, int D,
                                                      int64_t ld,
                                                      const float *__restrict__ cin, int64_t C,
@@ -71,10 +71,10 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
     }
     const int64_t n = counts[j];
     const int64_t o = offsets[j];
-    S sum[kMaxDimsPerLane];
-    double cj[kMaxDimsPerLane];
+    S sum[K];
+    double cj[K];
 #pragma unroll
-    for (int k = 0; k < kMaxDimsPerLane; ++k) {
+    for (int k = 0; k < K; ++k) {
         sum[k] = 0;
         const int d = lane + 64 * k;
         cj[k] = d < D ? (double)cin[j * D + d] : 0.0;
@@ -84,23 +84,24 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
         const int64_t cnt = min((int64_t)64, n - t0);
         const uint32_t myidx = lane < cnt ? perm[o + t0 + lane] : 0u;
         int u = 0;
-        // eight member rows in flight, then their values added in row order
-        for (; u + 8 <= cnt; u += 8) {
-            XT v[8][kMaxDimsPerLane];
+        // B member rows in flight, then their values added in row order
+        constexpr int B = 32 / K;
+        for (; u + B <= cnt; u += B) {
+            XT v[B][K];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < B; ++q) {
                 const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, u + q);
                 const XT *x = X + i * ld;
 #pragma unroll
-                for (int k = 0; k < kMaxDimsPerLane; ++k) {
+                for (int k = 0; k < K; ++k) {
                     const int d = lane + 64 * k;
                     v[q][k] = d < D ? x[d] : (XT)0;
                 }
             }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < B; ++q) {
 #pragma unroll
-                for (int k = 0; k < kMaxDimsPerLane; ++k) {
+                for (int k = 0; k < K; ++k) {
                     const int d = lane + 64 * k;
                     if (d < D) {
                         sum[k] += (S)v[q][k];
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
             const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, u);
             const XT *x = X + i * ld;
 #pragma unroll
-            for (int k = 0; k < kMaxDimsPerLane; ++k) {
+            for (int k = 0; k < K; ++k) {
                 const int d = lane + 64 * k;
                 if (d < D) {
                     const XT v = x[d];
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
     int64_t r = -1;
     if (n == 0) r = reseed_row(seed, iter, j, N);
 #pragma unroll
-    for (int k = 0; k < kMaxDimsPerLane; ++k) {
+    for (int k = 0; k < K; ++k) {
         const int d = lane + 64 * k;
         if (d < D) {
             float v;
@@ -138,6 +139,88 @@ __global__ __launch_bounds__(256) void update_kernel(const XT *__restrict__ X, i
                 v = (float)X[r * ld + d];
             cout[j * D + d] = v;
         }
+    }
+    for (int off = 32; off > 0; off >>= 1) jp += __shfl_xor(jp, off);
+    if (lane == 0) jpart[j] = jp;
+}
+
+// D = DS dividing 64 (1 ... 32): every lane loads. Lane (q, d) = (lane / DS,
+// lane % DS) reads dim d of member b * (64 / DS) + q of each chunk of 64
+// members into register b, P chunks in flight (64 P member rows per round
+// trip, against 32 / K above); the sums then take the members in list order,
+// each value fetched from its lane by a shuffle, so every sum and the
+// objective are those of update_kernel bit for bit (lanes q > 0 run copies
+// of the chains and drop them).
+template <typename XT, int DS>
+__global__ __launch_bounds__(256) void update_small_kernel(const XT *__restrict__ X, int64_t N, int D, int64_t ld,
+                                                           const float *__restrict__ cin, int64_t C,
+                                                           const int64_t *__restrict__ counts,
+                                                           const int64_t *__restrict__ offsets,
+                                                           const uint32_t *__restrict__ perm, uint64_t seed,
+                                                           int32_t iter, float *__restrict__ cout,
+                                                           double *__restrict__ jpart, int64_t x_group)
+{
+    typedef typename SumType<XT>::type S;
+    constexpr int R = 64 / DS;                       // members per wave load
+    constexpr int P = DS <= 8 ? 4 : DS == 16 ? 2 : 1;  // chunks in flight
+    const int lane = threadIdx.x & 63;
+    const int q = lane / DS, d = lane % DS;
+    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (j >= C) return;
+    {
+        const int64_t g = blockIdx.y;
+        X += g * x_group;
+        cin += g * C * D;
+        cout += g * C * D;
+        counts += g * C;
+        offsets += g * (C + 1);
+        perm += g * N;
+        jpart += g * C;
+        seed += (uint64_t)g;
+    }
+    const int64_t n = counts[j];
+    const int64_t o = offsets[j];
+    S sum = 0;
+    const double cj = (double)cin[j * D + d];
+    double jp = 0.0;
+    for (int64_t t0 = 0; t0 < n; t0 += 64 * P) {
+        XT v[P][DS];
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int64_t c0 = t0 + 64 * p;
+            const int64_t cnt = n - c0;  // members left from this chunk on (may be <= 0)
+            const uint32_t myidx = lane < cnt ? perm[o + c0 + lane] : 0u;
+#pragma unroll
+            for (int b = 0; b < DS; ++b) {
+                const int mm = b * R + q;
+                const int64_t i = (int64_t)(uint32_t)__shfl((int)myidx, mm);
+                v[p][b] = mm < cnt ? X[i * ld + d] : (XT)0;
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int64_t cnt = n - (t0 + 64 * p);
+#pragma unroll
+            for (int m = 0; m < 64; ++m) {
+                // member m of the chunk: register m / R of lane (m % R) * DS + d
+                const XT w = __shfl(v[p][m / R], (m % R) * DS + d);
+                if (m < cnt) {
+                    sum += (S)w;
+                    const double t = (double)w - cj;
+                    jp = fma(t, t, jp);
+                }
+            }
+        }
+    }
+    if (q == 0) {
+        float r;
+        if (n > 0)
+            r = (float)((double)sum / (double)n);
+        else
+            r = (float)X[reseed_row(seed, iter, j, N) * ld + d];
+        cout[j * D + d] = r;
+    } else {
+        jp = 0.0;
     }
     for (int off = 32; off > 0; off >>= 1) jp += __shfl_xor(jp, off);
     if (lane == 0) jpart[j] = jp;
@@ -265,12 +348,55 @@ hipError_t launch_kmeans_update(const void *rows, int rowtype, int64_t N, int D,
                  : U == 8 ? update_u8v_kernel<8> : update_u8v_kernel<16>;
         hipLaunchKernelGGL(k, grid, dim3(256), 0, s, (const uint8_t *)rows, N, D, ld, cent_in, C, counts, offsets,
                            perm, seed, iter, cent_out, jpart, x_group);
-    } else if (rowtype == kRowU8)
-        hipLaunchKernelGGL(update_kernel<uint8_t>, grid, dim3(256), 0, s, (const uint8_t *)rows, N, D,
-                           ld, cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group);
-    else
-        hipLaunchKernelGGL(update_kernel<float>, grid, dim3(256), 0, s, (const float *)rows, N, D, ld,
-                           cent_in, C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group);
+    } else {
+        // dims per lane: 1, 2 or 4 (D <= 64, 128, 256), member rows in flight 32, 16, 8
+        const int K = D <= 64 ? 1 : D <= 128 ? 2 : 4;
+        const bool small = D == 1 || D == 2 || D == 4 || D == 8 || D == 16 || D == 32;
+#define IVF_UPDATE_SMALL(XT, DS_)                                                                              \
+    hipLaunchKernelGGL((update_small_kernel<XT, DS_>), grid, dim3(256), 0, s, (const XT *)rows, N, D, ld, cent_in, \
+                       C, counts, offsets, perm, seed, iter, cent_out, jpart, x_group)
+#define IVF_UPDATE_SMALL_ALL(XT)         \
+    do {                                 \
+        if (D == 1)                      \
+            IVF_UPDATE_SMALL(XT, 1);     \
+        else if (D == 2)                 \
+            IVF_UPDATE_SMALL(XT, 2);     \
+        else if (D == 4)                 \
+            IVF_UPDATE_SMALL(XT, 4);     \
+        else if (D == 8)                 \
+            IVF_UPDATE_SMALL(XT, 8);     \
+        else if (D == 16)                \
+            IVF_UPDATE_SMALL(XT, 16);    \
+        else                             \
+            IVF_UPDATE_SMALL(XT, 32);    \
+    } while (0)
+#define IVF_UPDATE_LAUNCH(XT, K_)                                                                              \
+    hipLaunchKernelGGL((update_kernel<XT, K_>), grid, dim3(256), 0, s, (const XT *)rows, N, D, ld, cent_in, C, \
+                       counts, offsets, perm, seed, iter, cent_out, jpart, x_group)
+        if (small) {
+            if (rowtype == kRowU8)
+                IVF_UPDATE_SMALL_ALL(uint8_t);
+            else
+                IVF_UPDATE_SMALL_ALL(float);
+        } else if (rowtype == kRowU8) {
+            if (K == 1)
+                IVF_UPDATE_LAUNCH(uint8_t, 1);
+            else if (K == 2)
+                IVF_UPDATE_LAUNCH(uint8_t, 2);
+            else
+                IVF_UPDATE_LAUNCH(uint8_t, 4);
+        } else {
+            if (K == 1)
+                IVF_UPDATE_LAUNCH(float, 1);
+            else if (K == 2)
+                IVF_UPDATE_LAUNCH(float, 2);
+            else
+                IVF_UPDATE_LAUNCH(float, 4);
+        }
+#undef IVF_UPDATE_LAUNCH
+#undef IVF_UPDATE_SMALL_ALL
+#undef IVF_UPDATE_SMALL
+    }
     if (objective)
         hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)groups), dim3(1024), 0, s, jpart, C, objective);
     return hipGetLastError();
