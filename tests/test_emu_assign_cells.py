@@ -1,6 +1,6 @@
-"""The cell-and-walk assignment kernel (assign_graph.hip) built for the host
-against the wave64 emulation (tests/wave_emu) and run under
-AddressSanitizer: labels equal to the oracle's and distances equal to its
+"""The cell-and-walk assignment kernel and the candidate-restricted kernels
+(assign_graph.hip) built for the host against the wave64 emulation
+(tests/wave_emu) and run under AddressSanitizer: labels equal to the oracle's and distances equal to its
 fp64 distance rounded to fp32, on tiles whose rows share one cell (the
 shared-member path, rows in cell order) and tiles that mix cells (random
 order), with dead slots, invalid cells and members, empty cells, cells of
@@ -133,3 +133,35 @@ def test_emulated_assign_cells_large_cells(emu_cells, tmp_path, oracle_mod):
     cell = np.repeat(np.arange(3), 32).astype(np.int32)
     graph = rng.integers(0, C, (C, 6)).astype(np.int32)
     check(emu_cells, tmp_path, oracle_mod, x, c, cell, offsets, members, graph, 3, None, 1)
+
+
+def run_graph(exe, tmp_path, x, c, graph, prev, order=None):
+    """ivf_assign_graph's kernels on the emulation (a header with G = 0)."""
+    return run(exe, tmp_path, x, c, prev, np.zeros(1, np.int64), np.zeros(0, np.uint32), graph, 0, order)
+
+
+@pytest.mark.parametrize("N,C,D,S,labels_used,dt", [
+    (300, 40, 128, 8, 10, "u8"), (200, 30, 36, 12, 4, "f32"), (130, 50, 8, 3, 50, "u8"), (150, 20, 16, 17, 3, "f32"),
+])
+def test_emulated_assign_graph(emu_cells, tmp_path, oracle_mod, N, C, D, S, labels_used, dt):
+    """Rows grouped by previous label (labels covering whole waves: the
+    shared-candidate passes), random order (the one-lane-per-row rows), row
+    order; invalid previous labels and graph ids; S = 17 takes the lane-group
+    kernel."""
+    rng = np.random.default_rng(N + S)
+    if dt == "u8":
+        x = rng.integers(0, 256, (N, D)).astype(np.uint8)
+        c = rng.uniform(0, 255, (C, D)).astype(np.float32)
+    else:
+        x = rng.standard_normal((N, D)).astype(np.float32)
+        c = rng.standard_normal((C, D)).astype(np.float32)
+    graph = rng.integers(-2, C + 2, (C, S)).astype(np.int32)
+    prev = rng.integers(0, labels_used, N).astype(np.int32)
+    prev[rng.choice(N, 5, replace=False)] = rng.choice([-3, -1, C, C + 7], 5)
+    olab, od = oracle_mod.assign_graph(x, c, graph, prev, return_dist=True)
+    by_prev = np.argsort(prev, kind="stable")
+    for order in (by_prev, rng.permutation(N), None):
+        lab, dist = run_graph(emu_cells, tmp_path, x, c, graph, prev, order)
+        assert (lab == olab).all()
+        assert (dist == od.astype(np.float32)).all()
+    assert (olab == -1).any()

@@ -1,11 +1,15 @@
 // Runs the cell-and-walk assignment kernel of assign_graph.hip on the host
-// emulation, with every array in an allocation of its own, and writes the
-// labels and distances for the test to check against the oracle.
+// emulation (or, with a graph-only header, the candidate-restricted kernel),
+// with every array in an allocation of its own, and writes the labels and
+// distances for the test to check against the oracle.
 //   usage: assign_cells_host in.bin out.bin num_cus
 //   in:  int64 N, C, D, G, M, S, hops, rowtype (0 uint8, 1 fp32), has_graph,
 //        has_order; rows [N][D] (uint8 or fp32); float centroids [C][D];
 //        int32 cell [N]; int64 offsets [G + 1]; uint32 members [M];
-//        int32 graph [C][S] if has_graph; uint32 order [N] if has_order
+//        int32 graph [C][S] if has_graph; uint32 order [N] if has_order.
+//        G = 0 selects ivf_assign_graph's kernels instead: the cell array
+//        holds the previous labels (offsets then holds one unused entry,
+//        members none)
 //   out: int32 labels [N]; float dist [N] (entries no processing position
 //        names keep the fill 0x7F7F7F7F)
 #include "hip/hip_runtime.h"
@@ -59,7 +63,11 @@ int main(int argc, char **argv)
     fclose(f);
     int32_t *labels = alloc<int32_t>(N, 0x7f);
     float *dist = alloc<float>(N, 0x7f);
-    if (launch_assign_cells(x, rowtype == 0 ? kRowU8 : kRowF32, N, cent, C, D, cell, G, offsets, members, M, graph,
+    if (G == 0) {
+        if (!graph || launch_assign_graph(x, rowtype == 0 ? kRowU8 : kRowF32, N, cent, C, D, graph, S, cell, order,
+                                          labels, dist, nullptr) != hipSuccess)
+            return 3;
+    } else if (launch_assign_cells(x, rowtype == 0 ? kRowU8 : kRowF32, N, cent, C, D, cell, G, offsets, members, M, graph,
                             graph ? S : 0, hops, order, labels, dist, atoi(argv[3]), nullptr) != hipSuccess)
         return 3;
     FILE *o = fopen(argv[2], "wb");
