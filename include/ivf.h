@@ -291,7 +291,8 @@ ivf_status ivf_set_option(ivf_ctx *ctx, int option, int64_t value);
  *   order      [N] uint32 processing order, or NULL (row order): results do
  *              not depend on it, speed does (rows with the same previous
  *              label next to each other share their candidates' loads; the
- *              previous step's list permutation is that order). Entries >= N
+ *              previous step's list permutation is that order; an order
+ *              that does not group them is slower than NULL). Entries >= N
  *              are skipped; a row that order does not list is left untouched.
  *   out_dist   [N] fp32 squared distance (fp64 rounded), may be NULL
  * No workspace. Errors: IVF_EINVAL, IVF_EUNSUPPORTED (D, N), IVF_EDEVICE. */

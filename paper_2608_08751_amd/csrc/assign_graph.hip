@@ -8,11 +8,14 @@
 // this library (t = (double)x_d - (double)c_d; s = fma(t, t, s), d
 // ascending).
 //
-// A row owns a group of SP = next power of two >= S lanes of one wave; lane s
-// of the group evaluates candidate s with one sequential fma chain over the
-// dims (float4 loads of the centroid row; the lanes of a group read the same
-// row addresses, which the memory system merges), and a shuffle butterfly
-// inside the group takes the (distance, id) minimum.
+// Without a processing order (or for S > 16) a row owns a group of SP = next
+// power of two >= S lanes of one wave; lane s of the group evaluates
+// candidate s with one sequential fma chain over the dims (float4 loads of
+// the centroid row; the lanes of a group read the same row addresses, which
+// the memory system merges), and a shuffle butterfly inside the group takes
+// the (distance, id) minimum. With an order that groups rows by previous
+// label, one row per lane and the label's candidates shared by the wave
+// (assign_graph_tile_kernel below).
 #include "ivf_internal.h"
 #include "exact.h"
 
