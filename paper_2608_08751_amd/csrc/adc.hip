@@ -59,6 +59,7 @@ __device__ __forceinline__ float o2f(uint32_t u)
 
 struct PoolLds {
     uint64_t key[kAdcPool];
+    uint64_t thr;  // the k-th smallest key at the last trim (keys >= thr cannot enter)
     uint32_t hist[256];
     uint32_t sel_digit, sel_below;
     uint32_t n;  // keys in the pool
@@ -121,7 +122,10 @@ __device__ void pool_trim(PoolLds &P, int k)
         const int i = t + e * kAdcThreads;
         mine[e] = i < n ? P.key[i] : kNoKey;
     }
-    if (t == 0) P.n = 0;
+    if (t == 0) {
+        P.n = 0;
+        P.thr = prefix;
+    }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < kAdcKeysPerThread; ++e)
@@ -235,7 +239,10 @@ __global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
     const int dsub = D / M;
     // the residual in fp32 (as defined), held in fp64 for the table's sums
     for (int d = t; d < D; d += kAdcThreads) r[d] = (double)(Q[b * D + d] - cent[(int64_t)l * D + d]);
-    if (t == 0) pool.n = 0;
+    if (t == 0) {
+        pool.n = 0;
+        pool.thr = kNoKey;
+    }
     __syncthreads();
     if (dsub == 8) {
         // the common 8-dimension subspace: two 16-byte codebook loads per entry
@@ -265,31 +272,47 @@ __global__ __launch_bounds__(kAdcThreads) void adc_group_kernel(
         }
     }
     __syncthreads();
+    // Keys are unique (distance bits, then the row id), so once a trim has
+    // left the k smallest, a key at or above the k-th of them cannot enter:
+    // only smaller keys are appended (a wave reserves its slots with one LDS
+    // atomic), and the pool is trimmed when the next chunk might not fit.
+    const int lane = t & 63;
     for (int64_t c0 = range.x; c0 < range.y; c0 += kAdcChunk) {
         const int len = (int)min((int64_t)kAdcChunk, range.y - c0);
-        const int base = (int)pool.n;
-        for (int i = t; i < len; i += kAdcThreads) {
-            const int64_t pos = c0 + i;
-            const uint8_t *a = codes + pos * M;
-            float acc = 0.0f;
-            if ((M & 3) == 0) {
-                for (int m = 0; m < M; m += 4) {
-                    const uint32_t w = *reinterpret_cast<const uint32_t *>(a + m);
-                    acc = acc + lut[(m + 0) * kPqK + (w & 0xFFu)];
-                    acc = acc + lut[(m + 1) * kPqK + ((w >> 8) & 0xFFu)];
-                    acc = acc + lut[(m + 2) * kPqK + ((w >> 16) & 0xFFu)];
-                    acc = acc + lut[(m + 3) * kPqK + (w >> 24)];
+        const uint64_t thr = pool.thr;
+        for (int i0 = 0; i0 < len; i0 += kAdcThreads) {
+            const int i = i0 + t;
+            uint64_t key = kNoKey;
+            if (i < len) {
+                const int64_t pos = c0 + i;
+                const uint8_t *a = codes + pos * M;
+                float acc = 0.0f;
+                if ((M & 3) == 0) {
+                    for (int m = 0; m < M; m += 4) {
+                        const uint32_t w = *reinterpret_cast<const uint32_t *>(a + m);
+                        acc = acc + lut[(m + 0) * kPqK + (w & 0xFFu)];
+                        acc = acc + lut[(m + 1) * kPqK + ((w >> 8) & 0xFFu)];
+                        acc = acc + lut[(m + 2) * kPqK + ((w >> 16) & 0xFFu)];
+                        acc = acc + lut[(m + 3) * kPqK + (w >> 24)];
+                    }
+                } else {
+                    for (int m = 0; m < M; ++m) acc = acc + lut[m * kPqK + a[m]];
                 }
-            } else {
-                for (int m = 0; m < M; ++m) acc = acc + lut[m * kPqK + a[m]];
+                key = ((uint64_t)f2o(acc) << 32) | perm[pos];
             }
-            pool.key[base + i] = ((uint64_t)f2o(acc) << 32) | perm[pos];
+            const bool keep = i < len && key < thr;
+            const uint64_t want = __ballot(keep);
+            if (want != 0) {
+                uint32_t wbase = 0;
+                if (lane == 0) wbase = atomicAdd(&pool.n, (uint32_t)__popcll(want));
+                wbase = __shfl(wbase, 0);
+                if (keep) pool.key[wbase + __popcll(want & ((1ull << lane) - 1))] = key;
+            }
         }
         __syncthreads();
-        if (t == 0) pool.n = (uint32_t)(base + len);
-        __syncthreads();
-        if ((int)pool.n > k) pool_trim(pool, k);
+        if ((int)pool.n > kAdcPool - kAdcChunk) pool_trim(pool, k);
     }
+    if ((int)pool.n > k) pool_trim(pool, k);
     // the group's keys (at most k) and their count
     uint64_t *out = handoff + slot * k;
     const int n = (int)pool.n;
